@@ -1,0 +1,165 @@
+/*
+ * qdelta.h -- C ABI of libqdelta.so: the Q-Delta layer on AMD Instinct MI355X
+ * (gfx950), as hand-written HIP kernels.
+ *
+ * The operation (Sec. 3.3, Eq. (qdelta_decay), with the mixed input of
+ * Eq. (qdelta_gated_form)).  For every sequence n and head h independently,
+ * with a state S in R^{Dv x Dk} (row = value component):
+ *
+ *     x_t = k_t + lam_t q_t
+ *     S_t = alpha_t S_{t-1} (I - beta_t x_t k_t^T) + beta_t v_t k_t^T
+ *     o_t = S_t q_t                           (read-out from the updated state)
+ *
+ * The chunk entry points evaluate this with the chunkwise-parallel form of
+ * Sec. 3.3 ("Chunkwise parallel form"; App. D.1 WY representation, App. D.2 UT
+ * transform): chunks of `chunk` consecutive tokens, a UT-transform triangular
+ * solve inside each chunk, and a sequential fp32 scan of the state across
+ * chunks.  The result equals the recurrence up to floating-point rounding.
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ *  - All tensor pointers are DEVICE pointers owned by the caller.  Inputs are
+ *    never written.  Every output is fully overwritten (never accumulated).
+ *  - Tensors are dense, row-major, contiguous, 16-byte aligned.
+ *  - Activations q, k, v, o (and dO, dq, dk, dv) use `dtype`: QDELTA_BF16 or
+ *    QDELTA_F32.  Gates, states and gate gradients are always float32.
+ *  - Decay is passed as log(alpha) (float32, <= 0 expected); log_alpha == NULL
+ *    means alpha == 1 everywhere.  Gate values are not clamped.
+ *  - Calls are asynchronous on `stream` (0 = the null stream): no host
+ *    synchronisation and no device allocation.  Scratch memory is a caller
+ *    workspace of at least the size reported by qdelta_chunk_workspace_bytes.
+ *  - Validation of every host-visible argument happens before the first
+ *    launch; on any error nothing is launched and nothing is written.
+ *  - There is no global mutable state; calls on different streams may
+ *    overlap provided their workspaces and outputs do not.
+ *  - Supported: Dk in {64, 128}; Dv in {64, 128, 256}; chunk == 64; T >= 0 need
+ *    not be a multiple of chunk.  QDELTA_F32 additionally requires Dk == 64.
+ *    Anything else returns QDELTA_EUNSUPPORTED.
+ *
+ * Sequence layouts
+ * ----------------
+ *  dense   q,k [B,T,H,Dk]  v,o [B,T,H,Dv]  gates [B,T,H]  states [B,H,Dv,Dk]
+ *  varlen  the same with B == 1 and T = total tokens, split into N sequences by
+ *          cu_seqlens (device int32[N+1], cu[0] = 0, non-decreasing,
+ *          cu[N] = T); states are [N,H,Dv,Dk].  Chunks restart at every
+ *          sequence start, so results do not depend on how sequences are packed.
+ *          A malformed cu_seqlens cannot be checked without a host copy: the
+ *          kernels then skip the offending sequences (their outputs are left
+ *          unspecified) but never access memory out of bounds.
+ *
+ * Saved per-chunk entry states (written by the forward, read by the backward)
+ * ---------------------------------------------------------------------------
+ *  float32 [n_slots, H, Dv, Dk], n_slots from qdelta_saved_state_slots.  Chunk c
+ *  (0-based) of sequence n occupies slot  n*ceil(T/chunk) + c  (dense) or
+ *  floor(cu[n]/chunk) + n + c  (varlen); slots no chunk maps to are untouched.
+ *  Each slot holds the state S that the chunk starts from.
+ */
+#ifndef QDELTA_H
+#define QDELTA_H
+
+#include <stddef.h>
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  QDELTA_OK = 0,
+  QDELTA_EINVAL = 1,        /* NULL where a pointer is required, negative or inconsistent size, misalignment */
+  QDELTA_EUNSUPPORTED = 2,  /* valid but not implemented: head dims, chunk, dtype combination */
+  QDELTA_ENOWORKSPACE = 3,  /* workspace smaller than qdelta_chunk_workspace_bytes() */
+  QDELTA_EHIP = 4           /* a kernel launch reported an error */
+} qdelta_status;
+
+typedef enum { QDELTA_F32 = 0, QDELTA_BF16 = 1 } qdelta_dtype;
+
+/* Static text for a status code (never NULL). */
+const char* qdelta_status_string(int status);
+
+/* Library version as MAJOR*10000 + MINOR*100 + PATCH. */
+int qdelta_version(void);
+
+/* Number of saved-state slots (first dimension of saved_states).
+ * n_seqs == 0: dense batch of B sequences of T tokens -> B*ceil(T/chunk).
+ * n_seqs  > 0: varlen batch of T total tokens in n_seqs sequences ->
+ *              floor(T/chunk) + n_seqs (an upper bound that needs no host copy
+ *              of cu_seqlens).  Returns 0 for invalid sizes. */
+size_t qdelta_saved_state_slots(int32_t B, int32_t T, int32_t chunk, int32_t n_seqs);
+
+/* Workspace bytes needed by qdelta_chunk_fwd[_varlen] (is_bwd == 0) or
+ * qdelta_chunk_bwd[_varlen] (is_bwd != 0) for these sizes (same meaning of
+ * n_seqs as above).  Returns 0 for unsupported or invalid sizes. */
+size_t qdelta_chunk_workspace_bytes(int32_t B, int32_t T, int32_t H, int32_t Dk, int32_t Dv,
+                                    int32_t chunk, int32_t dtype, int32_t n_seqs, int32_t is_bwd);
+
+/* Chunkwise forward (Sec. 3.3 chunkwise form; App. D).
+ *   q, k [B,T,H,Dk], v [B,T,H,Dv]           activations (dtype)
+ *   beta, lam [B,T,H]                        write strength and query-feedback gate (fp32)
+ *   log_alpha [B,T,H] or NULL                log of the forget gate (fp32)
+ *   initial_state [B,H,Dv,Dk] or NULL        entry state (NULL = zero)
+ *   o [B,T,H,Dv]                             output o_t = S_t q_t (dtype)
+ *   final_state [B,H,Dv,Dk] or NULL          state after the last token
+ *   saved_states or NULL                     per-chunk entry states for the backward
+ *   ws, ws_bytes                             device workspace */
+int qdelta_chunk_fwd(int32_t B, int32_t T, int32_t H, int32_t Dk, int32_t Dv, int32_t chunk,
+                     int32_t dtype, const void* q, const void* k, const void* v,
+                     const float* beta, const float* lam, const float* log_alpha,
+                     const float* initial_state, void* o, float* final_state,
+                     float* saved_states, void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* Varlen forward: as qdelta_chunk_fwd with B == 1, T total tokens, N sequences
+ * delimited by the device array cu_seqlens[N+1]; states are [N,H,Dv,Dk]. */
+int qdelta_chunk_fwd_varlen(int32_t T, int32_t N, const int32_t* cu_seqlens, int32_t H,
+                            int32_t Dk, int32_t Dv, int32_t chunk, int32_t dtype,
+                            const void* q, const void* k, const void* v, const float* beta,
+                            const float* lam, const float* log_alpha,
+                            const float* initial_state, void* o, float* final_state,
+                            float* saved_states, void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* Chunkwise backward: exact gradients (up to rounding) of
+ *     L = <d_o, o> + <d_final_state, final_state>
+ * with respect to q, k, v, beta, lam, log_alpha and initial_state.  The paper
+ * states no backward pass; this is the derivative of the forward above.
+ *   saved_states    from qdelta_chunk_fwd on the same inputs, or NULL to
+ *                   recompute the state scan inside this call
+ *   d_o [B,T,H,Dv]  (dtype);  d_final_state [B,H,Dv,Dk] or NULL (= zero)
+ *   dq, dk [B,T,H,Dk], dv [B,T,H,Dv] (dtype); dbeta, dlam [B,T,H] (fp32)
+ *   dlog_alpha [B,T,H] fp32: required iff log_alpha != NULL, else must be NULL
+ *   d_initial_state [B,H,Dv,Dk] or NULL */
+int qdelta_chunk_bwd(int32_t B, int32_t T, int32_t H, int32_t Dk, int32_t Dv, int32_t chunk,
+                     int32_t dtype, const void* q, const void* k, const void* v,
+                     const float* beta, const float* lam, const float* log_alpha,
+                     const float* initial_state, const float* saved_states, const void* d_o,
+                     const float* d_final_state, void* dq, void* dk, void* dv, float* dbeta,
+                     float* dlam, float* dlog_alpha, float* d_initial_state, void* ws,
+                     size_t ws_bytes, hipStream_t stream);
+
+/* Varlen backward: as qdelta_chunk_bwd with the varlen layout. */
+int qdelta_chunk_bwd_varlen(int32_t T, int32_t N, const int32_t* cu_seqlens, int32_t H,
+                            int32_t Dk, int32_t Dv, int32_t chunk, int32_t dtype,
+                            const void* q, const void* k, const void* v, const float* beta,
+                            const float* lam, const float* log_alpha,
+                            const float* initial_state, const float* saved_states,
+                            const void* d_o, const float* d_final_state, void* dq, void* dk,
+                            void* dv, float* dbeta, float* dlam, float* dlog_alpha,
+                            float* d_initial_state, void* ws, size_t ws_bytes,
+                            hipStream_t stream);
+
+/* One token of the recurrence for N sequences (decode), Sec. 3.3
+ * Eq. (qdelta_decay) applied once:
+ *   q, k [N,H,Dk], v [N,H,Dv] (dtype); beta, lam, log_alpha [N,H] (fp32,
+ *   log_alpha may be NULL);  state [N,H,Dv,Dk] fp32, updated in place;
+ *   o [N,H,Dv] (dtype) = updated state times q.
+ * Supported: Dk in {64, 128}, Dv a positive multiple of 8 up to 256, any dtype. */
+int qdelta_recurrent_step(int32_t N, int32_t H, int32_t Dk, int32_t Dv, int32_t dtype,
+                          const void* q, const void* k, const void* v, const float* beta,
+                          const float* lam, const float* log_alpha, float* state, void* o,
+                          hipStream_t stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* QDELTA_H */

@@ -1,0 +1,302 @@
+// C ABI of libqdelta.so (declared in include/qdelta.h): argument validation,
+// workspace carving and kernel launches on the caller's stream.  No host
+// synchronisation and no device allocation happen here.
+#include <stddef.h>
+#include <stdint.h>
+
+#include "qd_launch.h"
+#include "qdelta.h"
+
+namespace {
+
+using qd::C;
+
+constexpr int kVersion = 10000;  // 1.0.0
+
+struct Layout {
+  size_t wb = 0, wU = 0, wW = 0, wP = 0, wT = 0;
+  size_t dSo = 0, dD = 0, dW = 0, dq = 0, dk = 0, dP = 0, dT = 0, db = 0, states = 0;
+  size_t total = 0;
+};
+
+Layout make_layout(size_t units, int Dk, int Dv, int esz, bool bwd) {
+  Layout L;
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    const size_t at = off;
+    off += (bytes + 255) & ~size_t(255);
+    return at;
+  };
+  L.wb = take(units * C * 4);
+  L.wU = take(units * C * Dv * esz);
+  L.wW = take(units * C * Dk * esz);
+  L.wP = take(units * C * C * esz);
+  if (bwd) {
+    L.wT = take(units * 2 * C * C * esz);
+    L.dSo = take(units * (size_t)Dv * Dk * 4);
+    L.dD = take(units * C * Dv * 4);
+    L.dW = take(units * C * Dk * 4);
+    L.dq = take(units * C * Dk * 4);
+    L.dk = take(units * C * Dk * 4);
+    L.dP = take(units * C * C * 4);
+    L.dT = take(units * C * C * 4);
+    L.db = take(units * C * 4);
+    L.states = take(units * (size_t)Dv * Dk * 4);
+  }
+  L.total = off;
+  return L;
+}
+
+bool aligned(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+bool ok_ptr(const void* p) { return p != nullptr && aligned(p); }
+bool ok_opt(const void* p) { return p == nullptr || aligned(p); }
+
+int check_dims(int64_t tokens, int32_t H, int32_t Dk, int32_t Dv, int32_t chunk, int32_t dtype) {
+  if (tokens < 0 || H <= 0 || chunk <= 0 || Dk <= 0 || Dv <= 0) return QDELTA_EINVAL;
+  if (dtype != QDELTA_F32 && dtype != QDELTA_BF16) return QDELTA_EINVAL;
+  if (chunk != C) return QDELTA_EUNSUPPORTED;
+  if (Dk != 64 && Dk != 128) return QDELTA_EUNSUPPORTED;
+  if (Dv != 64 && Dv != 128 && Dv != 256) return QDELTA_EUNSUPPORTED;
+  if (dtype == QDELTA_F32 && Dk != 64) return QDELTA_EUNSUPPORTED;
+  // element offsets of the largest tensors stay below 2^31 tokens * heads
+  if (tokens * (int64_t)H >= (int64_t(1) << 31)) return QDELTA_EUNSUPPORTED;
+  return QDELTA_OK;
+}
+
+size_t slots_for(int32_t B, int32_t T, int32_t n_seqs) {
+  if (n_seqs > 0) return (size_t)(T / C) + (size_t)n_seqs;
+  return (size_t)B * (size_t)((T + C - 1) / C);
+}
+
+struct Sizes {
+  int32_t T;        // dense: per-sequence tokens; varlen: total tokens
+  int32_t N;        // sequences
+  const int32_t* cu;
+  size_t slots;
+  int64_t tokens;   // total tokens
+};
+
+int make_sizes(bool varlen, int32_t B, int32_t T, int32_t N, const int32_t* cu, Sizes& s) {
+  if (T < 0) return QDELTA_EINVAL;
+  if (varlen) {
+    if (N < 0 || cu == nullptr) return QDELTA_EINVAL;
+    s.T = T;
+    s.N = N;
+    s.cu = cu;
+    s.slots = slots_for(1, T, N > 0 ? N : 0);
+    if (N == 0) s.slots = 0;
+    s.tokens = T;
+  } else {
+    if (B < 0) return QDELTA_EINVAL;
+    s.T = T;
+    s.N = B;
+    s.cu = nullptr;
+    s.slots = slots_for(B, T, 0);
+    s.tokens = (int64_t)B * T;
+  }
+  return QDELTA_OK;
+}
+
+int fwd_impl(bool varlen, int32_t B, int32_t T, int32_t N, const int32_t* cu, int32_t H,
+             int32_t Dk, int32_t Dv, int32_t chunk, int32_t dtype, const void* q, const void* k,
+             const void* v, const float* beta, const float* lam, const float* log_alpha,
+             const float* initial_state, void* o, float* final_state, float* saved_states,
+             void* ws, size_t ws_bytes, hipStream_t stream) {
+  Sizes s;
+  int rc = make_sizes(varlen, B, T, N, cu, s);
+  if (rc) return rc;
+  rc = check_dims(s.tokens, H, Dk, Dv, chunk, dtype);
+  if (rc) return rc;
+  const bool has_tokens = s.tokens > 0;
+  if (has_tokens && !(ok_ptr(q) && ok_ptr(k) && ok_ptr(v) && ok_ptr(beta) && ok_ptr(lam) && ok_ptr(o)))
+    return QDELTA_EINVAL;
+  if (!ok_opt(log_alpha) || !ok_opt(initial_state) || !ok_opt(final_state) || !ok_opt(saved_states))
+    return QDELTA_EINVAL;
+  const int esz = dtype == QDELTA_BF16 ? 2 : 4;
+  const Layout L = make_layout(s.slots * (size_t)H, Dk, Dv, esz, false);
+  if (L.total > 0 && (ws == nullptr || !aligned(ws))) return QDELTA_EINVAL;
+  if (ws_bytes < L.total) return QDELTA_ENOWORKSPACE;
+  if (s.N == 0) return QDELTA_OK;
+
+  char* w = static_cast<char*>(ws);
+  qd::Params p{};
+  p.T = s.T;
+  p.N = s.N;
+  p.H = H;
+  p.NT = varlen ? 0 : (s.T + C - 1) / C;
+  p.n_slots = (int)s.slots;
+  p.cu = s.cu;
+  p.q = q; p.k = k; p.v = v;
+  p.beta = beta; p.lam = lam; p.la = log_alpha; p.S0 = initial_state;
+  p.o = has_tokens ? o : nullptr;
+  p.Sfin = final_state;
+  p.saved = saved_states;
+  p.wb = reinterpret_cast<float*>(w + L.wb);
+  p.wU = w + L.wU;
+  p.wW = w + L.wW;
+  p.wP = w + L.wP;
+  hipError_t e = qd::launch_fwd(p, dtype, Dk, Dv, 0, 1, stream);
+  return e == hipSuccess ? QDELTA_OK : QDELTA_EHIP;
+}
+
+int bwd_impl(bool varlen, int32_t B, int32_t T, int32_t N, const int32_t* cu, int32_t H,
+             int32_t Dk, int32_t Dv, int32_t chunk, int32_t dtype, const void* q, const void* k,
+             const void* v, const float* beta, const float* lam, const float* log_alpha,
+             const float* initial_state, const float* saved_states, const void* d_o,
+             const float* d_final_state, void* dq, void* dk, void* dv, float* dbeta, float* dlam,
+             float* dlog_alpha, float* d_initial_state, void* ws, size_t ws_bytes,
+             hipStream_t stream) {
+  Sizes s;
+  int rc = make_sizes(varlen, B, T, N, cu, s);
+  if (rc) return rc;
+  rc = check_dims(s.tokens, H, Dk, Dv, chunk, dtype);
+  if (rc) return rc;
+  const bool has_tokens = s.tokens > 0;
+  if (has_tokens &&
+      !(ok_ptr(q) && ok_ptr(k) && ok_ptr(v) && ok_ptr(beta) && ok_ptr(lam) && ok_ptr(d_o) &&
+        ok_ptr(dq) && ok_ptr(dk) && ok_ptr(dv) && ok_ptr(dbeta) && ok_ptr(dlam)))
+    return QDELTA_EINVAL;
+  if ((log_alpha == nullptr) != (dlog_alpha == nullptr) && has_tokens) return QDELTA_EINVAL;
+  if (!ok_opt(log_alpha) || !ok_opt(dlog_alpha) || !ok_opt(initial_state) ||
+      !ok_opt(saved_states) || !ok_opt(d_final_state) || !ok_opt(d_initial_state))
+    return QDELTA_EINVAL;
+  const int esz = dtype == QDELTA_BF16 ? 2 : 4;
+  const Layout L = make_layout(s.slots * (size_t)H, Dk, Dv, esz, true);
+  if (L.total > 0 && (ws == nullptr || !aligned(ws))) return QDELTA_EINVAL;
+  if (ws_bytes < L.total) return QDELTA_ENOWORKSPACE;
+  if (s.N == 0) return QDELTA_OK;
+
+  char* w = static_cast<char*>(ws);
+  qd::Params p{};
+  p.T = s.T;
+  p.N = s.N;
+  p.H = H;
+  p.NT = varlen ? 0 : (s.T + C - 1) / C;
+  p.n_slots = (int)s.slots;
+  p.cu = s.cu;
+  p.q = q; p.k = k; p.v = v;
+  p.beta = beta; p.lam = lam; p.la = log_alpha; p.S0 = initial_state;
+  p.wb = reinterpret_cast<float*>(w + L.wb);
+  p.wU = w + L.wU;
+  p.wW = w + L.wW;
+  p.wP = w + L.wP;
+  p.wT = w + L.wT;
+  p.dO = d_o;
+  p.dSfin = d_final_state;
+  p.dq = dq; p.dk = dk; p.dv = dv;
+  p.dbeta = dbeta; p.dlam = dlam; p.dla = dlog_alpha; p.dS0 = d_initial_state;
+  p.w_dSo = reinterpret_cast<float*>(w + L.dSo);
+  p.w_dD = reinterpret_cast<float*>(w + L.dD);
+  p.w_dW = reinterpret_cast<float*>(w + L.dW);
+  p.w_dq = reinterpret_cast<float*>(w + L.dq);
+  p.w_dk = reinterpret_cast<float*>(w + L.dk);
+  p.w_dP = reinterpret_cast<float*>(w + L.dP);
+  p.w_dT = reinterpret_cast<float*>(w + L.dT);
+  p.w_db = reinterpret_cast<float*>(w + L.db);
+  hipError_t e;
+  if (saved_states) {
+    p.saved = const_cast<float*>(saved_states);
+    e = qd::launch_fwd(p, dtype, Dk, Dv, 1, 0, stream);
+  } else {
+    // recompute the per-chunk entry states (no outputs) into the workspace
+    p.saved = reinterpret_cast<float*>(w + L.states);
+    e = qd::launch_fwd(p, dtype, Dk, Dv, 1, 1, stream);
+  }
+  if (e != hipSuccess) return QDELTA_EHIP;
+  e = qd::launch_bwd(p, dtype, Dk, Dv, stream);
+  return e == hipSuccess ? QDELTA_OK : QDELTA_EHIP;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* qdelta_status_string(int status) {
+  switch (status) {
+    case QDELTA_OK: return "ok";
+    case QDELTA_EINVAL: return "invalid argument (null or misaligned pointer, bad size)";
+    case QDELTA_EUNSUPPORTED: return "unsupported configuration (head dims, chunk or dtype)";
+    case QDELTA_ENOWORKSPACE: return "workspace too small";
+    case QDELTA_EHIP: return "HIP launch error";
+    default: return "unknown status";
+  }
+}
+
+int qdelta_version(void) { return kVersion; }
+
+size_t qdelta_saved_state_slots(int32_t B, int32_t T, int32_t chunk, int32_t n_seqs) {
+  if (B < 0 || T < 0 || n_seqs < 0 || chunk != C) return 0;
+  return slots_for(B, T, n_seqs);
+}
+
+size_t qdelta_chunk_workspace_bytes(int32_t B, int32_t T, int32_t H, int32_t Dk, int32_t Dv,
+                                    int32_t chunk, int32_t dtype, int32_t n_seqs, int32_t is_bwd) {
+  if (B < 0 || T < 0 || n_seqs < 0) return 0;
+  const int64_t tokens = n_seqs > 0 ? (int64_t)T : (int64_t)B * T;
+  if (check_dims(tokens, H, Dk, Dv, chunk, dtype) != QDELTA_OK) return 0;
+  const size_t slots = slots_for(B, T, n_seqs);
+  return make_layout(slots * (size_t)H, Dk, Dv, dtype == QDELTA_BF16 ? 2 : 4, is_bwd != 0).total;
+}
+
+int qdelta_chunk_fwd(int32_t B, int32_t T, int32_t H, int32_t Dk, int32_t Dv, int32_t chunk,
+                     int32_t dtype, const void* q, const void* k, const void* v,
+                     const float* beta, const float* lam, const float* log_alpha,
+                     const float* initial_state, void* o, float* final_state,
+                     float* saved_states, void* ws, size_t ws_bytes, hipStream_t stream) {
+  return fwd_impl(false, B, T, B, nullptr, H, Dk, Dv, chunk, dtype, q, k, v, beta, lam,
+                  log_alpha, initial_state, o, final_state, saved_states, ws, ws_bytes, stream);
+}
+
+int qdelta_chunk_fwd_varlen(int32_t T, int32_t N, const int32_t* cu_seqlens, int32_t H,
+                            int32_t Dk, int32_t Dv, int32_t chunk, int32_t dtype,
+                            const void* q, const void* k, const void* v, const float* beta,
+                            const float* lam, const float* log_alpha,
+                            const float* initial_state, void* o, float* final_state,
+                            float* saved_states, void* ws, size_t ws_bytes, hipStream_t stream) {
+  return fwd_impl(true, 1, T, N, cu_seqlens, H, Dk, Dv, chunk, dtype, q, k, v, beta, lam,
+                  log_alpha, initial_state, o, final_state, saved_states, ws, ws_bytes, stream);
+}
+
+int qdelta_chunk_bwd(int32_t B, int32_t T, int32_t H, int32_t Dk, int32_t Dv, int32_t chunk,
+                     int32_t dtype, const void* q, const void* k, const void* v,
+                     const float* beta, const float* lam, const float* log_alpha,
+                     const float* initial_state, const float* saved_states, const void* d_o,
+                     const float* d_final_state, void* dq, void* dk, void* dv, float* dbeta,
+                     float* dlam, float* dlog_alpha, float* d_initial_state, void* ws,
+                     size_t ws_bytes, hipStream_t stream) {
+  return bwd_impl(false, B, T, B, nullptr, H, Dk, Dv, chunk, dtype, q, k, v, beta, lam,
+                  log_alpha, initial_state, saved_states, d_o, d_final_state, dq, dk, dv, dbeta,
+                  dlam, dlog_alpha, d_initial_state, ws, ws_bytes, stream);
+}
+
+int qdelta_chunk_bwd_varlen(int32_t T, int32_t N, const int32_t* cu_seqlens, int32_t H,
+                            int32_t Dk, int32_t Dv, int32_t chunk, int32_t dtype,
+                            const void* q, const void* k, const void* v, const float* beta,
+                            const float* lam, const float* log_alpha,
+                            const float* initial_state, const float* saved_states,
+                            const void* d_o, const float* d_final_state, void* dq, void* dk,
+                            void* dv, float* dbeta, float* dlam, float* dlog_alpha,
+                            float* d_initial_state, void* ws, size_t ws_bytes,
+                            hipStream_t stream) {
+  return bwd_impl(true, 1, T, N, cu_seqlens, H, Dk, Dv, chunk, dtype, q, k, v, beta, lam,
+                  log_alpha, initial_state, saved_states, d_o, d_final_state, dq, dk, dv, dbeta,
+                  dlam, dlog_alpha, d_initial_state, ws, ws_bytes, stream);
+}
+
+int qdelta_recurrent_step(int32_t N, int32_t H, int32_t Dk, int32_t Dv, int32_t dtype,
+                          const void* q, const void* k, const void* v, const float* beta,
+                          const float* lam, const float* log_alpha, float* state, void* o,
+                          hipStream_t stream) {
+  if (N < 0 || H <= 0) return QDELTA_EINVAL;
+  if (dtype != QDELTA_F32 && dtype != QDELTA_BF16) return QDELTA_EINVAL;
+  if ((Dk != 64 && Dk != 128) || Dv <= 0 || Dv > 256 || (Dv % 8) != 0) return QDELTA_EUNSUPPORTED;
+  if ((int64_t)N * H * 32 >= (int64_t(1) << 31)) return QDELTA_EUNSUPPORTED;
+  if (N == 0) return QDELTA_OK;
+  if (!(ok_ptr(q) && ok_ptr(k) && ok_ptr(v) && ok_ptr(beta) && ok_ptr(lam) && ok_ptr(state) &&
+        ok_ptr(o) && ok_opt(log_alpha)))
+    return QDELTA_EINVAL;
+  hipError_t e = qd::launch_step(N, H, Dk, Dv, dtype, q, k, v, beta, lam, log_alpha, state, o, stream);
+  return e == hipSuccess ? QDELTA_OK : QDELTA_EHIP;
+}
+
+}  // extern "C"

@@ -1,0 +1,244 @@
+"""Python binding of libqdelta.so (ctypes).  Argument marshalling only.
+
+PyTorch supplies device memory and the current HIP stream; every step of the
+Q-Delta computation runs in the library's HIP kernels.  There is no fallback:
+if ``libqdelta.so`` is missing or fails to load, every entry point raises.
+
+Functions mirror the C ABI in ``include/qdelta.h``:
+
+chunk_fwd(q, k, v, beta, lam, log_alpha=None, initial_state=None, cu_seqlens=None,
+          output_final_state=True, save_states=False) -> (o, final_state, saved_states)
+chunk_bwd(q, k, v, beta, lam, log_alpha, initial_state, saved_states, d_o,
+          d_final_state=None, cu_seqlens=None) -> dict of gradients
+recurrent_step(q, k, v, beta, lam, log_alpha, state) -> o        (state updated in place)
+"""
+import ctypes
+import os
+
+import torch
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libqdelta.so")
+CHUNK = 64
+
+QDELTA_OK, QDELTA_EINVAL, QDELTA_EUNSUPPORTED, QDELTA_ENOWORKSPACE, QDELTA_EHIP = range(5)
+QDELTA_F32, QDELTA_BF16 = 0, 1
+
+EXPORTS = (
+    "qdelta_status_string", "qdelta_version", "qdelta_saved_state_slots",
+    "qdelta_chunk_workspace_bytes", "qdelta_chunk_fwd", "qdelta_chunk_fwd_varlen",
+    "qdelta_chunk_bwd", "qdelta_chunk_bwd_varlen", "qdelta_recurrent_step",
+)
+
+_lib = None
+
+
+class QDeltaError(RuntimeError):
+    def __init__(self, fn, status):
+        self.status = status
+        msg = lib().qdelta_status_string(status).decode() if _lib is not None else str(status)
+        super().__init__(f"{fn} failed with status {status}: {msg}")
+
+
+def lib():
+    """Load libqdelta.so (raises if it is not built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is not built; run paper_2606_08804_amd/build.py")
+        L = ctypes.CDLL(LIB_PATH)
+        i32, sz, P = ctypes.c_int32, ctypes.c_size_t, ctypes.c_void_p
+        L.qdelta_status_string.argtypes = [ctypes.c_int]
+        L.qdelta_status_string.restype = ctypes.c_char_p
+        L.qdelta_version.argtypes = []
+        L.qdelta_version.restype = ctypes.c_int
+        L.qdelta_saved_state_slots.argtypes = [i32, i32, i32, i32]
+        L.qdelta_saved_state_slots.restype = sz
+        L.qdelta_chunk_workspace_bytes.argtypes = [i32] * 9
+        L.qdelta_chunk_workspace_bytes.restype = sz
+        L.qdelta_chunk_fwd.argtypes = [i32] * 7 + [P] * 10 + [P, sz, P]
+        L.qdelta_chunk_fwd.restype = ctypes.c_int
+        L.qdelta_chunk_fwd_varlen.argtypes = [i32, i32, P] + [i32] * 5 + [P] * 10 + [P, sz, P]
+        L.qdelta_chunk_fwd_varlen.restype = ctypes.c_int
+        L.qdelta_chunk_bwd.argtypes = [i32] * 7 + [P] * 17 + [P, sz, P]
+        L.qdelta_chunk_bwd.restype = ctypes.c_int
+        L.qdelta_chunk_bwd_varlen.argtypes = [i32, i32, P] + [i32] * 5 + [P] * 17 + [P, sz, P]
+        L.qdelta_chunk_bwd_varlen.restype = ctypes.c_int
+        L.qdelta_recurrent_step.argtypes = [i32] * 5 + [P] * 8 + [P]
+        L.qdelta_recurrent_step.restype = ctypes.c_int
+        _lib = L
+    return _lib
+
+
+def _dt(t):
+    if t.dtype == torch.bfloat16:
+        return QDELTA_BF16
+    if t.dtype == torch.float32:
+        return QDELTA_F32
+    raise TypeError(f"unsupported activation dtype {t.dtype}")
+
+
+def _p(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream():
+    return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+
+
+def _need(t, name, dtype=None, shape=None):
+    if t is None:
+        raise ValueError(f"{name} is required")
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a device tensor")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if dtype is not None and t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
+    if shape is not None and tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} has shape {tuple(t.shape)}, expected {tuple(shape)}")
+    return t
+
+
+def _opt(t, name, dtype=None, shape=None):
+    return None if t is None else _need(t, name, dtype, shape)
+
+
+def _check(fn, status):
+    if status != QDELTA_OK:
+        raise QDeltaError(fn, status)
+
+
+def _dims(q, v, cu_seqlens):
+    if cu_seqlens is None:
+        B, T, H, Dk = q.shape
+        N = B
+    else:
+        if q.dim() == 4:
+            if q.shape[0] != 1:
+                raise ValueError("a packed batch has leading dimension 1")
+            _, T, H, Dk = q.shape
+        else:
+            T, H, Dk = q.shape
+        B = 1
+        N = cu_seqlens.numel() - 1
+    return B, T, H, Dk, v.shape[-1], N
+
+
+def saved_state_slots(B, T, n_seqs=0):
+    return int(lib().qdelta_saved_state_slots(B, T, CHUNK, n_seqs))
+
+
+def workspace_bytes(B, T, H, Dk, Dv, dtype, n_seqs=0, is_bwd=False):
+    return int(lib().qdelta_chunk_workspace_bytes(B, T, H, Dk, Dv, CHUNK, dtype, n_seqs, int(is_bwd)))
+
+
+def _workspace(nbytes, device, workspace):
+    if nbytes == 0:
+        return None
+    if workspace is not None:
+        if workspace.numel() * workspace.element_size() < nbytes:
+            raise ValueError("workspace too small")
+        return workspace
+    return torch.empty(nbytes, dtype=torch.uint8, device=device)
+
+
+def chunk_fwd(q, k, v, beta, lam, log_alpha=None, initial_state=None, cu_seqlens=None,
+              output_final_state=True, save_states=False, workspace=None):
+    """Chunkwise Q-Delta forward.  Returns (o, final_state or None, saved_states or None)."""
+    L = lib()
+    dt = _dt(q)
+    B, T, H, Dk, Dv, N = _dims(q, v, cu_seqlens)
+    act = q.shape[:-1]
+    _need(q, "q", q.dtype)
+    _need(k, "k", q.dtype, q.shape)
+    _need(v, "v", q.dtype, tuple(act) + (Dv,))
+    _need(beta, "beta", torch.float32, act)
+    _need(lam, "lam", torch.float32, act)
+    _opt(log_alpha, "log_alpha", torch.float32, act)
+    _opt(initial_state, "initial_state", torch.float32, (N, H, Dv, Dk))
+    if cu_seqlens is not None:
+        _need(cu_seqlens, "cu_seqlens", torch.int32)
+    dev = q.device
+    o = torch.empty(tuple(act) + (Dv,), dtype=q.dtype, device=dev)
+    Sf = torch.empty((N, H, Dv, Dk), dtype=torch.float32, device=dev) if output_final_state else None
+    n_seqs = N if cu_seqlens is not None else 0
+    saved = None
+    if save_states:
+        saved = torch.empty((saved_state_slots(B, T, n_seqs), H, Dv, Dk), dtype=torch.float32, device=dev)
+    nbytes = workspace_bytes(B, T, H, Dk, Dv, dt, n_seqs, False)
+    ws = _workspace(nbytes, dev, workspace)
+    common = (H, Dk, Dv, CHUNK, dt, _p(q), _p(k), _p(v), _p(beta), _p(lam), _p(log_alpha),
+              _p(initial_state), _p(o), _p(Sf), _p(saved), _p(ws), nbytes, _stream())
+    if cu_seqlens is None:
+        _check("qdelta_chunk_fwd", L.qdelta_chunk_fwd(B, T, *common))
+    else:
+        _check("qdelta_chunk_fwd_varlen", L.qdelta_chunk_fwd_varlen(T, N, _p(cu_seqlens), *common))
+    return o, Sf, saved
+
+
+def chunk_bwd(q, k, v, beta, lam, log_alpha, initial_state, saved_states, d_o,
+              d_final_state=None, cu_seqlens=None, need_d_initial_state=True, workspace=None):
+    """Chunkwise Q-Delta backward.  Returns a dict: dq, dk, dv, dbeta, dlam,
+    dlog_alpha (None without decay), d_initial_state (None if not requested)."""
+    L = lib()
+    dt = _dt(q)
+    B, T, H, Dk, Dv, N = _dims(q, v, cu_seqlens)
+    act = q.shape[:-1]
+    _need(q, "q", q.dtype)
+    _need(k, "k", q.dtype, q.shape)
+    _need(v, "v", q.dtype, tuple(act) + (Dv,))
+    _need(beta, "beta", torch.float32, act)
+    _need(lam, "lam", torch.float32, act)
+    _opt(log_alpha, "log_alpha", torch.float32, act)
+    _opt(initial_state, "initial_state", torch.float32, (N, H, Dv, Dk))
+    _opt(saved_states, "saved_states", torch.float32)
+    _need(d_o, "d_o", q.dtype, tuple(act) + (Dv,))
+    _opt(d_final_state, "d_final_state", torch.float32, (N, H, Dv, Dk))
+    if cu_seqlens is not None:
+        _need(cu_seqlens, "cu_seqlens", torch.int32)
+    n_seqs = N if cu_seqlens is not None else 0
+    if saved_states is not None:
+        exp = (saved_state_slots(B, T, n_seqs), H, Dv, Dk)
+        if tuple(saved_states.shape) != exp:
+            raise ValueError(f"saved_states has shape {tuple(saved_states.shape)}, expected {exp}")
+    dev = q.device
+    dq = torch.empty_like(q)
+    dk = torch.empty_like(k)
+    dv = torch.empty_like(v)
+    dbeta = torch.empty_like(beta)
+    dlam = torch.empty_like(lam)
+    dla = torch.empty_like(log_alpha) if log_alpha is not None else None
+    dS0 = torch.empty((N, H, Dv, Dk), dtype=torch.float32, device=dev) if need_d_initial_state else None
+    nbytes = workspace_bytes(B, T, H, Dk, Dv, dt, n_seqs, True)
+    ws = _workspace(nbytes, dev, workspace)
+    common = (H, Dk, Dv, CHUNK, dt, _p(q), _p(k), _p(v), _p(beta), _p(lam), _p(log_alpha),
+              _p(initial_state), _p(saved_states), _p(d_o), _p(d_final_state), _p(dq), _p(dk),
+              _p(dv), _p(dbeta), _p(dlam), _p(dla), _p(dS0), _p(ws), nbytes, _stream())
+    if cu_seqlens is None:
+        _check("qdelta_chunk_bwd", L.qdelta_chunk_bwd(B, T, *common))
+    else:
+        _check("qdelta_chunk_bwd_varlen", L.qdelta_chunk_bwd_varlen(T, N, _p(cu_seqlens), *common))
+    return dict(dq=dq, dk=dk, dv=dv, dbeta=dbeta, dlam=dlam, dlog_alpha=dla, d_initial_state=dS0)
+
+
+def recurrent_step(q, k, v, beta, lam, log_alpha, state, out=None):
+    """One token for N sequences: q,k [N,H,Dk], v [N,H,Dv], gates [N,H],
+    state [N,H,Dv,Dk] fp32 (updated in place).  Returns o [N,H,Dv]."""
+    L = lib()
+    dt = _dt(q)
+    N, H, Dk = q.shape
+    Dv = v.shape[-1]
+    _need(q, "q", q.dtype)
+    _need(k, "k", q.dtype, q.shape)
+    _need(v, "v", q.dtype, (N, H, Dv))
+    _need(beta, "beta", torch.float32, (N, H))
+    _need(lam, "lam", torch.float32, (N, H))
+    _opt(log_alpha, "log_alpha", torch.float32, (N, H))
+    _need(state, "state", torch.float32, (N, H, Dv, Dk))
+    o = out if out is not None else torch.empty((N, H, Dv), dtype=q.dtype, device=q.device)
+    _need(o, "out", q.dtype, (N, H, Dv))
+    _check("qdelta_recurrent_step",
+           L.qdelta_recurrent_step(N, H, Dk, Dv, dt, _p(q), _p(k), _p(v), _p(beta), _p(lam),
+                                   _p(log_alpha), _p(state), _p(o), _stream()))
+    return o

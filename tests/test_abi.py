@@ -1,0 +1,128 @@
+"""C ABI checks that need no GPU: the library loads, exports every symbol the
+header declares, sizes its workspace, and rejects bad arguments before any
+launch (fake, never dereferenced, aligned pointers are used)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2606_08804_amd import qdelta
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "qdelta.h")
+
+
+def header_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(qdelta_[a-z_]+)\s*\(", text)))
+
+
+def test_library_exports_every_declared_symbol():
+    L = qdelta.lib()
+    names = header_functions()
+    assert len(names) == 9
+    for n in names:
+        assert hasattr(L, n), n
+    assert sorted(names) == sorted(qdelta.EXPORTS)
+
+
+def test_status_strings_and_version():
+    L = qdelta.lib()
+    for s in range(5):
+        assert L.qdelta_status_string(s)
+    assert L.qdelta_status_string(99) == b"unknown status"
+    assert L.qdelta_version() >= 10000
+
+
+def test_saved_state_slots():
+    assert qdelta.saved_state_slots(4, 4096) == 4 * 64
+    assert qdelta.saved_state_slots(2, 65) == 4
+    assert qdelta.saved_state_slots(1, 0) == 0
+    assert qdelta.saved_state_slots(1, 32768, 20) == 512 + 20
+    assert qdelta.lib().qdelta_saved_state_slots(1, 64, 32, 0) == 0   # chunk 32 unsupported
+
+
+def test_workspace_sizes_monotone_and_zero_for_unsupported():
+    ws = qdelta.workspace_bytes
+    a = ws(4, 4096, 16, 128, 128, 1)
+    b = ws(4, 4096, 16, 128, 128, 1, is_bwd=True)
+    assert 0 < a < b
+    assert ws(4, 8192, 16, 128, 128, 1) > a
+    assert ws(4, 4096, 32, 128, 128, 1) > a
+    assert ws(4, 4096, 16, 128, 256, 1) > a
+    assert ws(4, 4096, 16, 96, 128, 1) == 0      # Dk 96 unsupported
+    assert ws(4, 4096, 16, 128, 128, 0) == 0     # fp32 needs Dk 64
+    assert ws(1, 100, 2, 64, 64, 0) > 0
+    assert ws(-1, 100, 2, 64, 64, 0) == 0
+
+
+FAKE = 1 << 20          # aligned, never dereferenced: every call below fails validation
+
+
+def _fwd(B=1, T=64, H=1, Dk=64, Dv=64, chunk=64, dtype=1, ptrs=None, ws=FAKE, ws_bytes=1 << 40):
+    p = dict(q=FAKE, k=FAKE, v=FAKE, beta=FAKE, lam=FAKE, la=None, s0=None, o=FAKE, sf=None, sv=None)
+    if ptrs:
+        p.update(ptrs)
+    return qdelta.lib().qdelta_chunk_fwd(B, T, H, Dk, Dv, chunk, dtype, p["q"], p["k"], p["v"],
+                                         p["beta"], p["lam"], p["la"], p["s0"], p["o"], p["sf"],
+                                         p["sv"], ws, ws_bytes, None)
+
+
+def test_fwd_rejects_bad_arguments_before_launch():
+    E = qdelta
+    assert _fwd(Dk=96) == E.QDELTA_EUNSUPPORTED
+    assert _fwd(Dv=32) == E.QDELTA_EUNSUPPORTED
+    assert _fwd(chunk=32) == E.QDELTA_EUNSUPPORTED
+    assert _fwd(dtype=0, Dk=128) == E.QDELTA_EUNSUPPORTED
+    assert _fwd(dtype=7) == E.QDELTA_EINVAL
+    assert _fwd(H=0) == E.QDELTA_EINVAL
+    assert _fwd(T=-1) == E.QDELTA_EINVAL
+    assert _fwd(ptrs=dict(q=None)) == E.QDELTA_EINVAL
+    assert _fwd(ptrs=dict(v=FAKE + 4)) == E.QDELTA_EINVAL          # misaligned
+    assert _fwd(ptrs=dict(sf=FAKE + 8)) == E.QDELTA_EINVAL
+    assert _fwd(ws_bytes=16) == E.QDELTA_ENOWORKSPACE
+    assert _fwd(ws=None) == E.QDELTA_EINVAL
+    # nothing to do: zero sequences
+    assert _fwd(B=0, ws=None, ws_bytes=0) == E.QDELTA_OK
+
+
+def test_bwd_and_varlen_reject_bad_arguments():
+    L = qdelta.lib()
+    E = qdelta
+    f = FAKE
+    # log_alpha given but dlog_alpha missing
+    rc = L.qdelta_chunk_bwd(1, 64, 1, 64, 64, 64, 1, f, f, f, f, f, f, None, None, f, None, f, f, f, f,
+                            f, None, None, f, 1 << 40, None)
+    assert rc == E.QDELTA_EINVAL
+    # too small workspace
+    rc = L.qdelta_chunk_bwd(1, 64, 1, 64, 64, 64, 1, f, f, f, f, f, None, None, None, f, None, f, f, f, f,
+                            f, None, None, f, 1024, None)
+    assert rc == E.QDELTA_ENOWORKSPACE
+    # varlen needs cu_seqlens
+    rc = L.qdelta_chunk_fwd_varlen(64, 1, None, 1, 64, 64, 64, 1, f, f, f, f, f, None, None, f, None,
+                                   None, f, 1 << 40, None)
+    assert rc == E.QDELTA_EINVAL
+    rc = L.qdelta_chunk_bwd_varlen(64, -1, f, 1, 64, 64, 64, 1, f, f, f, f, f, None, None, None, f, None,
+                                   f, f, f, f, f, None, None, f, 1 << 40, None)
+    assert rc == E.QDELTA_EINVAL
+
+
+def test_recurrent_step_rejects_bad_arguments():
+    L = qdelta.lib()
+    E = qdelta
+    f = FAKE
+    assert L.qdelta_recurrent_step(1, 1, 96, 64, 1, f, f, f, f, f, None, f, f, None) == E.QDELTA_EUNSUPPORTED
+    assert L.qdelta_recurrent_step(1, 1, 64, 12, 1, f, f, f, f, f, None, f, f, None) == E.QDELTA_EUNSUPPORTED
+    assert L.qdelta_recurrent_step(1, 1, 64, 64, 1, f, f, f, f, f, None, f + 4, f, None) == E.QDELTA_EINVAL
+    assert L.qdelta_recurrent_step(1, 0, 64, 64, 1, f, f, f, f, f, None, f, f, None) == E.QDELTA_EINVAL
+    assert L.qdelta_recurrent_step(0, 1, 64, 64, 1, None, None, None, None, None, None, None, None,
+                                   None) == E.QDELTA_OK
+
+
+def test_binding_validates_before_calling_library():
+    import torch
+    q = torch.zeros(1, 64, 1, 64)
+    with pytest.raises(ValueError):
+        qdelta.chunk_fwd(q, q, q, torch.zeros(1, 64, 1), torch.zeros(1, 64, 1))   # CPU tensors
