@@ -30,8 +30,9 @@
  *    workspace of at least the size reported by qdelta_chunk_workspace_bytes.
  *  - Validation of every host-visible argument happens before the first
  *    launch; on any error nothing is launched and nothing is written.
- *  - There is no global mutable state; calls on different streams may
- *    overlap provided their workspaces and outputs do not.
+ *  - Apart from the opt-in measurement facility at the end of this file, there
+ *    is no global mutable state; calls on different streams may overlap
+ *    provided their workspaces and outputs do not.
  *  - Supported: Dk in {64, 128}; Dv in {64, 128, 256}; chunk == 64; T >= 0 need
  *    not be a multiple of chunk.  QDELTA_F32 additionally requires Dk == 64.
  *    Anything else returns QDELTA_EUNSUPPORTED.
@@ -157,6 +158,21 @@ int qdelta_recurrent_step(int32_t N, int32_t H, int32_t Dk, int32_t Dv, int32_t 
                           const void* q, const void* k, const void* v, const float* beta,
                           const float* lam, const float* log_alpha, float* state, void* o,
                           hipStream_t stream);
+
+/* Measurement facility (benchmarks and profiling only; not thread-safe).
+ * qdelta_profile_begin() starts recording a pair of HIP events around every
+ * kernel launch of the library, on the launch stream, tagged by stage:
+ *   0 chunk preparation (forward)       1 forward state scan + chunk output
+ *   2 chunk preparation (backward)      3 backward state scan
+ *   4 intra-chunk backward, Dv products 5 intra-chunk backward, UT solve and Dk products
+ *   6 recurrent step
+ * qdelta_profile_end() waits for the recorded events, writes the summed kernel
+ * time (milliseconds) and the number of launches of each stage into the
+ * caller's arrays of QDELTA_N_STAGES entries (either may be NULL) and stops
+ * recording.  Returns QDELTA_EHIP if an event call failed. */
+#define QDELTA_N_STAGES 7
+int qdelta_profile_begin(void);
+int qdelta_profile_end(float* ms, int32_t* launches);
 
 #ifdef __cplusplus
 }

@@ -4,6 +4,8 @@
 #include <stddef.h>
 #include <stdint.h>
 
+#include <vector>
+
 #include "qd_launch.h"
 #include "qdelta.h"
 
@@ -207,9 +209,69 @@ int bwd_impl(bool varlen, int32_t B, int32_t T, int32_t N, const int32_t* cu, in
   return e == hipSuccess ? QDELTA_OK : QDELTA_EHIP;
 }
 
+// Measurement facility state (process-wide; benchmarks only).
+struct Prof {
+  bool on = false;
+  bool failed = false;
+  std::vector<hipEvent_t> start[qd::ST_COUNT], stop[qd::ST_COUNT];
+  int used[qd::ST_COUNT] = {};
+};
+Prof g_prof;
+
 }  // namespace
 
+void qd::prof_mark(int stage, int after, hipStream_t st) {
+  Prof& P = g_prof;
+  if (!P.on || stage < 0 || stage >= ST_COUNT) return;
+  const int i = P.used[stage];
+  if (!after) {
+    if (i == (int)P.start[stage].size()) {
+      hipEvent_t a = nullptr, b = nullptr;
+      if (hipEventCreate(&a) != hipSuccess || hipEventCreate(&b) != hipSuccess) {
+        P.failed = true;
+        return;
+      }
+      P.start[stage].push_back(a);
+      P.stop[stage].push_back(b);
+    }
+    if (hipEventRecord(P.start[stage][i], st) != hipSuccess) P.failed = true;
+  } else {
+    if (i >= (int)P.stop[stage].size()) return;
+    if (hipEventRecord(P.stop[stage][i], st) != hipSuccess) P.failed = true;
+    P.used[stage] = i + 1;
+  }
+}
+
 extern "C" {
+
+int qdelta_profile_begin(void) {
+  g_prof.on = true;
+  g_prof.failed = false;
+  for (int s = 0; s < qd::ST_COUNT; ++s) g_prof.used[s] = 0;
+  return QDELTA_OK;
+}
+
+int qdelta_profile_end(float* ms, int32_t* launches) {
+  Prof& P = g_prof;
+  bool failed = P.failed;
+  for (int s = 0; s < qd::ST_COUNT; ++s) {
+    float tot = 0.f;
+    for (int i = 0; i < P.used[s]; ++i) {
+      float t = 0.f;
+      if (hipEventSynchronize(P.stop[s][i]) != hipSuccess ||
+          hipEventElapsedTime(&t, P.start[s][i], P.stop[s][i]) != hipSuccess) {
+        failed = true;
+        continue;
+      }
+      tot += t;
+    }
+    if (ms) ms[s] = tot;
+    if (launches) launches[s] = P.used[s];
+    P.used[s] = 0;
+  }
+  P.on = false;
+  return failed ? QDELTA_EHIP : QDELTA_OK;
+}
 
 const char* qdelta_status_string(int status) {
   switch (status) {

@@ -605,11 +605,19 @@ static hipError_t launch_bwd_t(const Params& p, hipStream_t st) {
   constexpr int KH = 32;
   const int units = p.N * p.H;
   const int nb = ((units + 7) / 8) * 8 * (DV / BV);
-  if (nb > 0) hipLaunchKernelGGL((k_scan_bwd<E, DK, DV, BV>), dim3(nb), dim3(NTHREADS), 0, st, p);
+  if (nb > 0) {
+    prof_mark(ST_SCAN_BWD, 0, st);
+    hipLaunchKernelGGL((k_scan_bwd<E, DK, DV, BV>), dim3(nb), dim3(NTHREADS), 0, st, p);
+    prof_mark(ST_SCAN_BWD, 1, st);
+  }
   if (p.n_slots > 0) {
     dim3 gp(p.n_slots, p.H);
+    prof_mark(ST_INTRA_A, 0, st);
     hipLaunchKernelGGL((k_intra_a<E, DK, DV, BV>), gp, dim3(NTHREADS), 0, st, p);
+    prof_mark(ST_INTRA_A, 1, st);
+    prof_mark(ST_INTRA_B, 0, st);
     hipLaunchKernelGGL((k_intra_b<E, DK, KH>), gp, dim3(NTHREADS), 0, st, p);
+    prof_mark(ST_INTRA_B, 1, st);
   }
   return hipGetLastError();
 }

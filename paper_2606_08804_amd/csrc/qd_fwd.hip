@@ -257,15 +257,22 @@ static hipError_t launch_fwd_t(const Params& p, int bwd_prep, int with_scan, hip
   constexpr int BV = 32;
   if (p.n_slots > 0) {
     dim3 gp(p.n_slots, p.H);
+    const int stage = bwd_prep ? ST_PREP_BWD : ST_PREP_FWD;
+    prof_mark(stage, 0, st);
     if (bwd_prep)
       hipLaunchKernelGGL((k_prep<E, DK, DV, true>), gp, dim3(NTHREADS), 0, st, p);
     else
       hipLaunchKernelGGL((k_prep<E, DK, DV, false>), gp, dim3(NTHREADS), 0, st, p);
+    prof_mark(stage, 1, st);
   }
   if (with_scan) {
     const int units = p.N * p.H;
     const int nb = ((units + 7) / 8) * 8 * (DV / BV);
-    if (nb > 0) hipLaunchKernelGGL((k_scan_fwd<E, DK, DV, BV>), dim3(nb), dim3(NTHREADS), 0, st, p);
+    if (nb > 0) {
+      prof_mark(ST_SCAN_FWD, 0, st);
+      hipLaunchKernelGGL((k_scan_fwd<E, DK, DV, BV>), dim3(nb), dim3(NTHREADS), 0, st, p);
+      prof_mark(ST_SCAN_FWD, 1, st);
+    }
   }
   return hipGetLastError();
 }

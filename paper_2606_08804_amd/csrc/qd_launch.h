@@ -7,6 +7,21 @@
 
 namespace qd {
 
+enum Stage {
+  ST_PREP_FWD = 0,
+  ST_SCAN_FWD = 1,
+  ST_PREP_BWD = 2,
+  ST_SCAN_BWD = 3,
+  ST_INTRA_A = 4,
+  ST_INTRA_B = 5,
+  ST_STEP = 6,
+  ST_COUNT = 7
+};
+
+// Records a HIP event on `st` before (after == 0) or after (after == 1) a
+// kernel launch of `stage` while the measurement facility is active.
+void prof_mark(int stage, int after, hipStream_t st);
+
 // Chunk preparation (UT solve, WY factors) over all slots, then, if
 // with_scan, the sequential forward state scan (+ chunk outputs when p.o is
 // set).  bwd_prep also stores T and P^T for the backward kernels.

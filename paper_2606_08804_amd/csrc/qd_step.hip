@@ -70,11 +70,13 @@ hipError_t launch_step(int N, int H, int Dk, int Dv, int dtype, const void* q, c
 #define QD_STEP(ET, DKV)                                                                        \
   hipLaunchKernelGGL((k_step<ET, DKV>), grid, dim3(NTHREADS), 0, st, Dv, nrb, (const ET*)q,     \
                      (const ET*)k, (const ET*)v, beta, lam, la, state, (ET*)o)
+  if (!((dtype == 1 || dtype == 0) && (Dk == 128 || Dk == 64))) return hipErrorInvalidValue;
+  prof_mark(ST_STEP, 0, st);
   if (dtype == 1 && Dk == 128) QD_STEP(__bf16, 128);
   else if (dtype == 1 && Dk == 64) QD_STEP(__bf16, 64);
   else if (dtype == 0 && Dk == 128) QD_STEP(float, 128);
-  else if (dtype == 0 && Dk == 64) QD_STEP(float, 64);
-  else return hipErrorInvalidValue;
+  else QD_STEP(float, 64);
+  prof_mark(ST_STEP, 1, st);
 #undef QD_STEP
   return hipGetLastError();
 }

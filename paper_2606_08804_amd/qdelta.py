@@ -28,7 +28,10 @@ EXPORTS = (
     "qdelta_status_string", "qdelta_version", "qdelta_saved_state_slots",
     "qdelta_chunk_workspace_bytes", "qdelta_chunk_fwd", "qdelta_chunk_fwd_varlen",
     "qdelta_chunk_bwd", "qdelta_chunk_bwd_varlen", "qdelta_recurrent_step",
+    "qdelta_profile_begin", "qdelta_profile_end",
 )
+
+STAGES = ("prep_fwd", "scan_fwd", "prep_bwd", "scan_bwd", "intra_a", "intra_b", "step")
 
 _lib = None
 
@@ -66,6 +69,10 @@ def lib():
         L.qdelta_chunk_bwd_varlen.restype = ctypes.c_int
         L.qdelta_recurrent_step.argtypes = [i32] * 5 + [P] * 8 + [P]
         L.qdelta_recurrent_step.restype = ctypes.c_int
+        L.qdelta_profile_begin.argtypes = []
+        L.qdelta_profile_begin.restype = ctypes.c_int
+        L.qdelta_profile_end.argtypes = [P, P]
+        L.qdelta_profile_end.restype = ctypes.c_int
         _lib = L
     return _lib
 
@@ -242,3 +249,17 @@ def recurrent_step(q, k, v, beta, lam, log_alpha, state, out=None):
            L.qdelta_recurrent_step(N, H, Dk, Dv, dt, _p(q), _p(k), _p(v), _p(beta), _p(lam),
                                    _p(log_alpha), _p(state), _p(o), _stream()))
     return o
+
+
+def profile_begin():
+    """Start timing every library kernel launch with HIP events (per stage)."""
+    _check("qdelta_profile_begin", lib().qdelta_profile_begin())
+
+
+def profile_end():
+    """Stop timing; returns {stage: (total_ms, launches)}."""
+    n = len(STAGES)
+    ms = (ctypes.c_float * n)()
+    cnt = (ctypes.c_int32 * n)()
+    _check("qdelta_profile_end", lib().qdelta_profile_end(ms, cnt))
+    return {name: (float(ms[i]), int(cnt[i])) for i, name in enumerate(STAGES)}

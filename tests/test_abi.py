@@ -22,7 +22,7 @@ def header_functions():
 def test_library_exports_every_declared_symbol():
     L = qdelta.lib()
     names = header_functions()
-    assert len(names) == 9
+    assert len(names) == 11
     for n in names:
         assert hasattr(L, n), n
     assert sorted(names) == sorted(qdelta.EXPORTS)
