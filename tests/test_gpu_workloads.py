@@ -1,0 +1,86 @@
+"""GPU parity at the full workload sizes, in the launch configuration the
+benchmark times.  Where the full fp64 oracle would be slow, the GPU runs the
+whole workload and the oracle checks a sample of heads (every head is an
+independent computation, so a sampled head is compared over all its tokens)."""
+import numpy as np
+import pytest
+import torch
+
+from paper_2606_08804_amd import qdelta, synth
+from tests.gpu_helpers import (TOL, bwd_errors, f64, fwd_errors, gpu_bwd, gpu_fwd, normwise,
+                               oracle_fwd, select_heads)
+
+pytestmark = pytest.mark.gpu
+
+
+def _sel_out(x, heads, packed=False):
+    return x[:, :, heads] if not packed else x[:, :, heads]
+
+
+@pytest.mark.parametrize("gate", ["G1", "G2"])
+def test_forward_bf16_layer_full(gate):
+    d = synth.make_workload(2, gate)
+    o, Sf, _ = gpu_fwd(d)
+    e = fwd_errors(d, o, Sf)
+    assert all(v <= TOL["bf16"] for v in e.values()), e
+
+
+@pytest.mark.parametrize("gate", ["G1", "G2"])
+def test_training_step_full(gate):
+    d = synth.make_workload(3, gate)
+    o, Sf, saved = gpu_fwd(d, save_states=True)
+    e = fwd_errors(d, o, Sf)
+    assert all(v <= TOL["bf16"] for v in e.values()), e
+    g = gpu_bwd(d, saved)
+    e = bwd_errors(d, g)
+    assert all(v <= TOL["bf16"] for v in e.values()), e
+
+
+def test_long_context_forward_sampled_heads():
+    d = synth.make_workload(4, "G1")
+    o, Sf, _ = gpu_fwd(d)
+    heads = [0, 7, 15]
+    ds = select_heads(d, heads)
+    o_ref, S_ref = oracle_fwd(ds)
+    assert normwise(f64(o[:, :, heads].cpu()), o_ref) <= TOL["bf16"]
+    assert normwise(f64(Sf[:, heads].cpu()), S_ref) <= TOL["bf16"]
+
+
+def test_decode_full_sampled_units():
+    N, H, D, steps = 64, 16, 128, 1024
+    d = synth.make_decode(N, H, D, steps)
+    S = d["initial_state"].cuda()
+    q, k, v = d["q"].cuda(), d["k"].cuda(), d["v"].cuda()
+    beta, lam, la = d["beta"].cuda(), d["lam"].cuda(), d["log_alpha"].cuda()
+    outs = torch.empty((steps, N, H, D), dtype=torch.bfloat16, device="cuda")
+    for s in range(steps):
+        qdelta.recurrent_step(q[s], k[s], v[s], beta[s], lam[s], la[s], S, out=outs[s])
+    torch.cuda.synchronize()
+    seqs = [0, 31, 63]
+    heads = [0, 9]
+    ref_in = {}
+    for key in ("q", "k", "v", "beta", "lam", "log_alpha"):
+        x = d[key][:, seqs][:, :, heads]
+        ref_in[key] = x.transpose(0, 1).contiguous()
+    ref_in.update(initial_state=d["initial_state"][seqs][:, heads].contiguous(), cu_seqlens=None)
+    o_ref, S_ref = oracle_fwd(ref_in)
+    o_got = f64(outs[:, seqs][:, :, heads].transpose(0, 1).cpu())
+    assert normwise(o_got, o_ref) <= TOL["bf16"]
+    assert normwise(f64(S[seqs][:, heads].cpu()), S_ref) <= TOL["bf16"]
+
+
+def test_varlen_full_sampled_heads():
+    d = synth.make_workload(5, "G2")
+    assert d["cu_seqlens"][-1].item() == 32768
+    o, Sf, saved = gpu_fwd(d, save_states=True)
+    g = gpu_bwd(d, saved)
+    heads = [0, 13, 31]
+    ds = select_heads(d, heads)
+    ref_o, ref_S = oracle_fwd(ds)
+    assert normwise(f64(o[0][:, heads].cpu()), ref_o) <= TOL["bf16"]
+    assert normwise(f64(Sf[:, heads].cpu()), ref_S) <= TOL["bf16"]
+    gs = {key: (None if val is None else
+                (val[:, heads].contiguous() if key == "d_initial_state" else val[:, :, heads].contiguous()))
+          for key, val in g.items()}
+    e = bwd_errors(ds, gs)
+    assert all(v <= TOL["bf16"] for v in e.values()), e
