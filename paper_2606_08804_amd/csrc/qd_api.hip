@@ -16,7 +16,7 @@ using qd::C;
 constexpr int kVersion = 10000;  // 1.0.0
 
 struct Layout {
-  size_t wb = 0, wU = 0, wW = 0, wP = 0, wT = 0;
+  size_t wb = 0, wU = 0, wW = 0, wP = 0, wKt = 0, wT = 0, wWt = 0, wQgt = 0, wdOt = 0;
   size_t dSo = 0, dD = 0, dW = 0, dq = 0, dk = 0, dP = 0, dT = 0, db = 0, states = 0;
   size_t total = 0;
 };
@@ -33,8 +33,12 @@ Layout make_layout(size_t units, int Dk, int Dv, int esz, bool bwd) {
   L.wU = take(units * C * Dv * esz);
   L.wW = take(units * C * Dk * esz);
   L.wP = take(units * C * C * esz);
+  L.wKt = take(units * C * Dk * esz);
   if (bwd) {
     L.wT = take(units * 2 * C * C * esz);
+    L.wWt = take(units * C * Dk * esz);
+    L.wQgt = take(units * C * Dk * esz);
+    L.wdOt = take(units * C * Dv * esz);
     L.dSo = take(units * (size_t)Dv * Dk * 4);
     L.dD = take(units * C * Dv * 4);
     L.dW = take(units * C * Dk * 4);
@@ -137,6 +141,7 @@ int fwd_impl(bool varlen, int32_t B, int32_t T, int32_t N, const int32_t* cu, in
   p.wU = w + L.wU;
   p.wW = w + L.wW;
   p.wP = w + L.wP;
+  p.wKt = w + L.wKt;
   hipError_t e = qd::launch_fwd(p, dtype, Dk, Dv, 0, 1, stream);
   return e == hipSuccess ? QDELTA_OK : QDELTA_EHIP;
 }
@@ -182,9 +187,13 @@ int bwd_impl(bool varlen, int32_t B, int32_t T, int32_t N, const int32_t* cu, in
   p.wU = w + L.wU;
   p.wW = w + L.wW;
   p.wP = w + L.wP;
+  p.wKt = w + L.wKt;
   p.wT = w + L.wT;
+  p.wWt = w + L.wWt;
+  p.wQgt = w + L.wQgt;
+  p.wdOt = w + L.wdOt;
   p.dO = d_o;
-  p.dSfin = d_final_state;
+  p.dSfin = d_final_state;   // dO is read by the backward-mode preparation as well
   p.dq = dq; p.dk = dk; p.dv = dv;
   p.dbeta = dbeta; p.dlam = dlam; p.dla = dlog_alpha; p.dS0 = d_initial_state;
   p.w_dSo = reinterpret_cast<float*>(w + L.dSo);

@@ -36,22 +36,35 @@ template <typename E, int DK, int BV>
 struct ScanBwdSmem {
   static constexpr int P = Pad<E>::v;
   float b[C];
-  E PT[C][C + P];     // P^T [r][i]
-  E dOt[BV][C + P];   // dO tile, transposed [v][r]
-  E Kb[C][DK + P];    // Kbar [r][k]
-  E Qt[DK][C + P];    // (diag(g) Q)^T [k][r]
-  E Wt[DK][C + P];    // -W^T [k][r]
   E dS[BV][DK + P];   // dS' tile [v][k]
-  E dDt[BV][C + P];   // dD tile, transposed [v][r]
+  E dDn[BV][C + P];   // -dD tile, transposed [v][r]
 };
 
+// Operands of one chunk for one wave of the backward scan, prefetched from
+// global memory straight into MFMA fragments.
+template <typename E, int DK, int KPW, int NB>
+struct ScanBwdPre {
+  AFrag<E, C> PT;          // rows 16w.. of P^T
+  AFrag<E, DK> K;          // rows 16w.. of K
+  AFrag<E, C> Qg[KPW];     // rows of (diag(g) Q)^T for this wave's key blocks
+  AFrag<E, C> Wt[KPW];     // rows of W^T for this wave's key blocks
+  AFrag<E, C> dO[NB];      // B fragments of dO^T for the tile's value blocks
+  float b;
+};
+
+// One workgroup per (sequence, head, Dv tile of BV = 32); reverse pass over
+// the chunks with the next (earlier) chunk's operands prefetched.
 template <typename E, int DK, int DV, int BV>
 __global__ __launch_bounds__(NTHREADS) void k_scan_bwd(Params p) {
   constexpr int P = Pad<E>::v;
   constexpr int LK = DK + P, LC = C + P;
   constexpr int NVT = DV / BV;
-  constexpr int SPW = (DK / 16) * (BV / 16) / NWAVES;
-  constexpr int DPW = (C / 16) * (BV / 16) / NWAVES;
+  constexpr int NB = BV / 16;
+  constexpr int KS = Mma<E>::KS;
+  constexpr int KPW = DK / 16 / NWAVES;
+  static_assert(KPW >= 1 && KPW * 16 * NWAVES == DK, "key blocks per wave");
+  typedef typename Quad<E>::raw QR;
+  typedef typename Mma<E>::frag FR;
   __shared__ ScanBwdSmem<E, DK, BV> sm;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   int unit, vt;
@@ -59,97 +72,101 @@ __global__ __launch_bounds__(NTHREADS) void k_scan_bwd(Params p) {
   const int H = p.H, n = unit / H, h = unit % H, v0 = vt * BV;
   int s, e;
   if (!seq_range(p, n, s, e)) return;
-  const int nch = (e - s + C - 1) / C;
   const int base = slot_base(p, n, s);
+  const int nch = max(0, min((e - s + C - 1) / C, p.n_slots - base));
 
-  f4 acc[SPW];
+  f4 acc[KPW][NB];
 #pragma unroll
-  for (int i = 0; i < SPW; ++i) {
-    const int t = w * SPW + i, kt = t / (BV / 16), nt = t % (BV / 16);
-    if (p.dSfin)
-      acc[i] = *(const f4*)(p.dSfin + ((size_t)unit * DV + v0 + nt * 16 + fcol(lane)) * DK + kt * 16 +
-                            frow(lane, 0));
-    else
-      acc[i] = zero4();
-  }
-  const E* qb = (const E*)p.q;
+  for (int i = 0; i < KPW; ++i)
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) {
+      const int kt = KPW * w + i;
+      acc[i][nb] = p.dSfin ? *(const f4*)(p.dSfin + ((size_t)unit * DV + v0 + nb * 16 + fcol(lane)) * DK +
+                                          kt * 16 + frow(lane, 0))
+                           : zero4();
+    }
   const E* kb = (const E*)p.k;
-  const E* dob = (const E*)p.dO;
-  for (int c = nch - 1; c >= 0; --c) {
-    const int slot = base + c;
-    if (slot >= p.n_slots) continue;
+  ScanBwdPre<E, DK, KPW, NB> pre;
+  auto prefetch = [&](int c) {
     const int t0 = s + c * C, len = min(C, e - t0);
-    const size_t gi = (size_t)slot * H + h;
-    __syncthreads();
-    if (tid < C) sm.b[tid] = p.wb[gi * C + tid];
-    load_rows<E, C>(&sm.PT[0][0], LC, (const E*)p.wT + gi * 2 * C * C + C * C, C, C, tid);
-    load_rows_t<E, BV>(&sm.dOt[0][0], LC, dob + ((size_t)t0 * H + h) * DV + v0, (size_t)H * DV, len, tid, One());
+    const size_t gi = (size_t)(base + c) * H + h;
+    pre.b = tid < C ? p.wb[gi * C + tid] : 0.f;
+    pre.PT.load((const E*)p.wT + gi * 2 * C * C + C * C + (size_t)(16 * w) * C, C, 16, lane);
+    pre.K.load(kb + ((size_t)(t0 + 16 * w) * H + h) * DK, (size_t)H * DK, len - 16 * w, lane);
 #pragma unroll
-    for (int i = 0; i < SPW; ++i) {
-      const int t = w * SPW + i, kt = t / (BV / 16), nt = t % (BV / 16);
-#pragma unroll
-      for (int j = 0; j < 4; ++j) sm.dS[nt * 16 + fcol(lane)][kt * 16 + frow(lane, j)] = fromf<E>(acc[i][j]);
-      *(f4*)(p.w_dSo + (gi * DV + v0 + nt * 16 + fcol(lane)) * DK + kt * 16 + frow(lane, 0)) = acc[i];
+    for (int i = 0; i < KPW; ++i) {
+      const size_t row = (size_t)16 * (KPW * w + i) * C;
+      pre.Qg[i].load((const E*)p.wQgt + gi * DK * C + row, C, 16, lane);
+      pre.Wt[i].load((const E*)p.wWt + gi * DK * C + row, C, 16, lane);
     }
-    __syncthreads();
-    const float bl = sm.b[C - 1];
-    // Kbar rows (row-major) and (g Q)^T, -W^T (transposed)
-    {
-      const E* ks = kb + ((size_t)t0 * H + h) * DK;
-      constexpr int VEC = 16 / sizeof(E), PR = DK / VEC;
-      for (int idx = tid; idx < C * PR; idx += NTHREADS) {
-        const int r = idx / PR, cc = (idx % PR) * VEC;
-        E vals[VEC];
-        if (r < len) {
-          uint4 raw = *(const uint4*)(ks + (size_t)r * H * DK + cc);
-          const E* pv = (const E*)&raw;
-          const float sc = __expf(bl - sm.b[r]);
 #pragma unroll
-          for (int j = 0; j < VEC; ++j) vals[j] = fromf<E>(tof(pv[j]) * sc);
-        } else {
+    for (int nb = 0; nb < NB; ++nb)
+      pre.dO[nb].load((const E*)p.wdOt + gi * DV * C + (size_t)(v0 + 16 * nb) * C, C, 16, lane);
+  };
+  if (nch > 0) prefetch(nch - 1);
+
+  for (int c = nch - 1; c >= 0; --c) {
+    const size_t gi = (size_t)(base + c) * H + h;
+    const ScanBwdPre<E, DK, KPW, NB> cur = pre;
+    block_sync_lds();
+    if (tid < C) sm.b[tid] = cur.b;
 #pragma unroll
-          for (int j = 0; j < VEC; ++j) vals[j] = fromf<E>(0.f);
-        }
+    for (int i = 0; i < KPW; ++i)
 #pragma unroll
-        for (int j = 0; j < VEC; ++j) sm.Kb[r][cc + j] = vals[j];
+      for (int nb = 0; nb < NB; ++nb) {
+        const int kt = KPW * w + i;
+        *(QR*)&sm.dS[nb * 16 + fcol(lane)][kt * 16 + frow(lane, 0)] = Quad<E>::pack(acc[i][nb]);
+        *(f4*)(p.w_dSo + (gi * DV + v0 + nb * 16 + fcol(lane)) * DK + kt * 16 + frow(lane, 0)) = acc[i][nb];
       }
-    }
-    load_rows_t<E, DK>(&sm.Qt[0][0], LC, qb + ((size_t)t0 * H + h) * DK, (size_t)H * DK, len, tid,
-                       [&](int r) { return __expf(sm.b[r]); });
-    load_rows_t<E, DK>(&sm.Wt[0][0], LC, (const E*)p.wW + gi * C * DK, DK, C, tid,
-                       [](int) { return -1.f; });
-    __syncthreads();
-    // dD = P^T dO + Kbar dS'^T
+    block_sync_lds();
+    if (c > 0) prefetch(c - 1);
+    const float bl = sm.b[C - 1];
+    // dD = P^T dO + diag(g_C/g) K dS'^T   (rows 16w..)
 #pragma unroll
-    for (int i = 0; i < DPW; ++i) {
-      const int t = w * DPW + i, mt = t / (BV / 16), nt = t % (BV / 16);
-      f4 d = mma_k<E, C>(kmaj(&sm.PT[0][0], LC), kmaj(&sm.dOt[0][0], LC), mt * 16, nt * 16, zero4(), lane);
-      d = mma_k<E, DK>(kmaj(&sm.Kb[0][0], LK), kmaj(&sm.dS[0][0], LK), mt * 16, nt * 16, d, lane);
+    for (int nb = 0; nb < NB; ++nb) {
+      f4 d1 = zero4(), d2 = zero4();
+#pragma unroll
+      for (int ks = 0; ks < C / KS; ++ks) d1 = Mma<E>::mma(cur.PT.f[ks], cur.dO[nb].f[ks], d1);
+#pragma unroll
+      for (int ks = 0; ks < DK / KS; ++ks)
+        d2 = Mma<E>::mma(cur.K.f[ks], Frag<E>::load(kmaj(&sm.dS[0][0], LK), nb * 16, ks * KS, lane), d2);
+      f4 dn;
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
-        const int r = mt * 16 + frow(lane, j), vv = nt * 16 + fcol(lane);
-        p.w_dD[(gi * C + r) * DV + v0 + vv] = d[j];
-        sm.dDt[vv][r] = fromf<E>(d[j]);
+        const int r = 16 * w + frow(lane, j);
+        const float d = d1[j] + __expf(bl - sm.b[r]) * d2[j];
+        dn[j] = -d;
+        p.w_dD[(gi * C + r) * DV + v0 + nb * 16 + fcol(lane)] = d;
       }
+      *(QR*)&sm.dDn[nb * 16 + fcol(lane)][16 * w + frow(lane, 0)] = Quad<E>::pack(dn);
     }
-    __syncthreads();
+    block_sync_lds();
     // dS_entry^T = g_C dS'^T + (g Q)^T dO - W^T dD
     const float gC = __expf(bl);
 #pragma unroll
-    for (int i = 0; i < SPW; ++i) {
-      const int t = w * SPW + i, kt = t / (BV / 16), nt = t % (BV / 16);
-      f4 a = gC * acc[i];
-      a = mma_k<E, C>(kmaj(&sm.Qt[0][0], LC), kmaj(&sm.dOt[0][0], LC), kt * 16, nt * 16, a, lane);
-      a = mma_k<E, C>(kmaj(&sm.Wt[0][0], LC), kmaj(&sm.dDt[0][0], LC), kt * 16, nt * 16, a, lane);
-      acc[i] = a;
+    for (int nb = 0; nb < NB; ++nb) {
+#pragma unroll
+      for (int i = 0; i < KPW; ++i) acc[i][nb] = gC * acc[i][nb];
+#pragma unroll
+      for (int ks = 0; ks < C / KS; ++ks) {
+        const FR bd = Frag<E>::load(kmaj(&sm.dDn[0][0], LC), nb * 16, ks * KS, lane);
+#pragma unroll
+        for (int i = 0; i < KPW; ++i) {
+          acc[i][nb] = Mma<E>::mma(cur.Qg[i].f[ks], cur.dO[nb].f[ks], acc[i][nb]);
+          acc[i][nb] = Mma<E>::mma(cur.Wt[i].f[ks], bd, acc[i][nb]);
+        }
+      }
     }
   }
   if (p.dS0) {
 #pragma unroll
-    for (int i = 0; i < SPW; ++i) {
-      const int t = w * SPW + i, kt = t / (BV / 16), nt = t % (BV / 16);
-      *(f4*)(p.dS0 + ((size_t)unit * DV + v0 + nt * 16 + fcol(lane)) * DK + kt * 16 + frow(lane, 0)) = acc[i];
-    }
+    for (int i = 0; i < KPW; ++i)
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb) {
+        const int kt = KPW * w + i;
+        *(f4*)(p.dS0 + ((size_t)unit * DV + v0 + nb * 16 + fcol(lane)) * DK + kt * 16 + frow(lane, 0)) =
+            acc[i][nb];
+      }
   }
 }
 
@@ -363,7 +380,7 @@ struct IntraBSmem {
 template <typename E, int DK, int KH>
 __global__ __launch_bounds__(NTHREADS) void k_intra_b(Params p) {
   constexpr int P = Pad<E>::v;
-  constexpr int LH = KH + P, LC = C + P, LF = C + 4, LX = KH + 4;
+  constexpr int LH = KH + P, LC = C + P, LF = C + 4;
   constexpr int HT = (C / 16) * (KH / 16);   // C x KH tiles
   __shared__ IntraBSmem<E, KH> sm;
   const int g = blockIdx.x, h = blockIdx.y, tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
@@ -442,12 +459,17 @@ __global__ __launch_bounds__(NTHREADS) void k_intra_b(Params p) {
   }
   __syncthreads();
   unit_lower_inverse(&sm.u.c.A[0][0], LF, &sm.u.c.M[0][0], LF, sm.u.c.tmp, tid);
+  // Four lanes share one row (or column) of the C x C element-wise passes:
+  // lane quad q4 = tid >> 2 owns row/column q4, segment (tid & 3) * 16 .. +16.
+  const int q4 = tid >> 2, seg = (tid & 3) * 16;
   // dbeta (T = Minv diag(beta)): column sums of dT * Minv;  T into LDS
-  if (tid < C) {
-    const int i = tid;
-    float s = 0.f;
-    for (int r = 0; r < C; ++r) s += sm.u.c.dT[r][i] * sm.u.c.M[r][i];
-    sm.dbeta[i] = s;
+  {
+    float s4 = 0.f;
+#pragma unroll 4
+    for (int r = seg; r < seg + 16; ++r) s4 += sm.u.c.dT[r][q4] * sm.u.c.M[r][q4];
+    s4 += __shfl_xor(s4, 1, 64);
+    s4 += __shfl_xor(s4, 2, 64);
+    if ((tid & 3) == 0) sm.dbeta[q4] = s4;
   }
   for (int idx = tid; idx < C * C; idx += NTHREADS) {
     const int r = idx / C, i = idx % C;
@@ -481,44 +503,61 @@ __global__ __launch_bounds__(NTHREADS) void k_intra_b(Params p) {
     }
   }
   __syncthreads();
-  // element-wise: dbeta row part, dG, dQK, and the decay terms of db
-  float* dbg = p.w_db + gi * C;
-  if (tid < C) {
-    const int r = tid;
+  // dP (from intra A) into the dead Y buffer, coalesced
+  for (int idx = tid; idx < C * C / 4; idx += NTHREADS) {
+    const int r = idx / (C / 4), c = (idx % (C / 4)) * 4;
+    *(f4*)&sm.u.c.Y[r][c] = *(const f4*)(dPg + r * C + c);
+  }
+  __syncthreads();
+  // element-wise, by rows: dbeta row part, dG, dQK, and the row sums of
+  // dGam * Gam (decay gradient), with dGam = dA beta G + dP QK on r >= i
+  const float* dbg = p.w_db + gi * C;
+  {
+    const int r = q4;
     const float br = sm.b[r], betar = sm.beta[r];
     float dbr = 0.f, er = 0.f;
-    for (int i = 0; i < C; ++i) {
+#pragma unroll 4
+    for (int i = seg; i < seg + 16; ++i) {
+      float dg = 0.f, dqk = 0.f;
       if (i <= r) {
         const float gam = __expf(br - sm.b[i]);
         const float dA = sm.u.c.A[r][i];
         const float Gv = sm.u.c.G[r][i];
-        const float dP = dPg[r * C + i];
+        const float dP = sm.u.c.Y[r][i];
         dbr += dA * gam * Gv;
-        sm.dG[r][i] = fromf<E>(dA * betar * gam);
-        sm.dQK[r][i] = fromf<E>(dP * gam);
-        const float dgam = dA * betar * Gv + dP * sm.u.c.QK[r][i];
-        er += dgam * gam;
-      } else {
-        sm.dG[r][i] = fromf<E>(0.f);
-        sm.dQK[r][i] = fromf<E>(0.f);
+        dg = dA * betar * gam;
+        dqk = dP * gam;
+        er += (dA * betar * Gv + dP * sm.u.c.QK[r][i]) * gam;
       }
+      sm.dG[r][i] = fromf<E>(dg);
+      sm.dQK[r][i] = fromf<E>(dqk);
     }
-    sm.db[r] = dbg[r] + er;
-    sm.dbeta[r] += dbr;
-  } else if (tid < 2 * C) {
-    // column sums wait for the row pass (below)
+    dbr += __shfl_xor(dbr, 1, 64);
+    dbr += __shfl_xor(dbr, 2, 64);
+    er += __shfl_xor(er, 1, 64);
+    er += __shfl_xor(er, 2, 64);
+    __syncthreads();   // dbeta column part written above (other lanes) is complete
+    if ((tid & 3) == 0) {
+      sm.dbeta[r] += dbr;
+      sm.db[r] = dbg[r] + er;
+    }
   }
   __syncthreads();
-  if (tid < C) {
-    const int i = tid;
+  // element-wise, by columns: subtract the column sums of dGam * Gam
+  {
+    const int i = q4;
     const float bi = sm.b[i];
     float ec = 0.f;
-    for (int r = i; r < C; ++r) {
-      const float gam = __expf(sm.b[r] - bi);
-      const float dgam = sm.u.c.A[r][i] * sm.beta[r] * sm.u.c.G[r][i] + dPg[r * C + i] * sm.u.c.QK[r][i];
-      ec += dgam * gam;
+#pragma unroll 4
+    for (int r = seg; r < seg + 16; ++r) {
+      if (r >= i) {
+        const float gam = __expf(sm.b[r] - bi);
+        ec += (sm.u.c.A[r][i] * sm.beta[r] * sm.u.c.G[r][i] + sm.u.c.Y[r][i] * sm.u.c.QK[r][i]) * gam;
+      }
     }
-    sm.db[i] -= ec;
+    ec += __shfl_xor(ec, 1, 64);
+    ec += __shfl_xor(ec, 2, 64);
+    if ((tid & 3) == 0) sm.db[i] -= ec;
   }
   __syncthreads();
 
@@ -540,11 +579,14 @@ __global__ __launch_bounds__(NTHREADS) void k_intra_b(Params p) {
       for (int j = 0; j < 4; ++j) sm.u.h.dX[m0 + frow(lane, j)][n0 + fcol(lane)] = d[j];
     }
     __syncthreads();
-    if (tid < C) {
-      const int r = tid;
-      float s = 0.f;
-      for (int c = 0; c < KH; ++c) s += tof(sm.u.h.X[r][c]) * sm.u.h.dX[r][c];
-      sm.db[r] += sm.g[r] * s;
+    {
+      const int r = q4, c0 = (tid & 3) * (KH / 4);
+      float s4 = 0.f;
+#pragma unroll
+      for (int c = c0; c < c0 + KH / 4; ++c) s4 += tof(sm.u.h.X[r][c]) * sm.u.h.dX[r][c];
+      s4 += __shfl_xor(s4, 1, 64);
+      s4 += __shfl_xor(s4, 2, 64);
+      if ((tid & 3) == 0) sm.db[r] += sm.g[r] * s4;
     }
     __syncthreads();
     // dX = g dgX + dG K
@@ -558,11 +600,14 @@ __global__ __launch_bounds__(NTHREADS) void k_intra_b(Params p) {
       }
     }
     __syncthreads();
-    if (tid < C) {
-      const int r = tid;
-      float s = 0.f;
-      for (int c = 0; c < KH; ++c) s += tof(sm.u.h.Q[r][c]) * sm.u.h.dX[r][c];
-      sm.dlam[r] += s;
+    {
+      const int r = q4, c0 = (tid & 3) * (KH / 4);
+      float s4 = 0.f;
+#pragma unroll
+      for (int c = c0; c < c0 + KH / 4; ++c) s4 += tof(sm.u.h.Q[r][c]) * sm.u.h.dX[r][c];
+      s4 += __shfl_xor(s4, 1, 64);
+      s4 += __shfl_xor(s4, 2, 64);
+      if ((tid & 3) == 0) sm.dlam[r] += s4;
     }
     // dQ = dq_part + dQK K + lambda dX ;  dK = dk_part + dQK^T Q + dG^T X + dX
     for (int t = w; t < HT; t += NWAVES) {
@@ -602,12 +647,13 @@ __global__ __launch_bounds__(NTHREADS) void k_intra_b(Params p) {
 template <typename E, int DK, int DV>
 static hipError_t launch_bwd_t(const Params& p, hipStream_t st) {
   constexpr int BV = 32;
+  constexpr int SBV = 32;   // value columns per backward-scan workgroup
   constexpr int KH = 32;
   const int units = p.N * p.H;
-  const int nb = ((units + 7) / 8) * 8 * (DV / BV);
+  const int nb = ((units + 7) / 8) * 8 * (DV / SBV);
   if (nb > 0) {
     prof_mark(ST_SCAN_BWD, 0, st);
-    hipLaunchKernelGGL((k_scan_bwd<E, DK, DV, BV>), dim3(nb), dim3(NTHREADS), 0, st, p);
+    hipLaunchKernelGGL((k_scan_bwd<E, DK, DV, SBV>), dim3(nb), dim3(NTHREADS), 0, st, p);
     prof_mark(ST_SCAN_BWD, 1, st);
   }
   if (p.n_slots > 0) {

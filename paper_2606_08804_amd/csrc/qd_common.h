@@ -162,6 +162,89 @@ __device__ inline void load_rows_t(E* dst, int ld, const E* src, size_t gs, int 
 
 struct One { __device__ float operator()(int) const { return 1.f; } };
 
+// Register staging of an R x COLS tile (row stride `rs` elements in global,
+// rows >= valid read as zero) for software prefetch: load() issues the global
+// reads, store() writes the tile to LDS with 16-byte stores.
+template <typename E, int R, int COLS>
+struct TileRegs {
+  static constexpr int VEC = 16 / sizeof(E);
+  static constexpr int PR = COLS / VEC;
+  static constexpr int TOTAL = R * PR;
+  static constexpr int N = (TOTAL + NTHREADS - 1) / NTHREADS;
+  static_assert(TOTAL % NTHREADS == 0 || TOTAL < NTHREADS, "tile must split evenly over the workgroup");
+  uint4 v[N];
+  __device__ static inline bool owns(int i, int tid) { return TOTAL >= NTHREADS || tid + i * NTHREADS < TOTAL; }
+  __device__ inline void load(const E* src, size_t rs, int valid, int tid) {
+#pragma unroll
+    for (int i = 0; i < N; ++i) {
+      const int idx = tid + i * NTHREADS, r = idx / PR, c = (idx % PR) * VEC;
+      v[i] = (owns(i, tid) && r < valid) ? *(const uint4*)(src + (size_t)r * rs + c) : make_uint4(0, 0, 0, 0);
+    }
+  }
+  __device__ inline void store(E* dst, int ld, int tid) const {
+#pragma unroll
+    for (int i = 0; i < N; ++i) {
+      const int idx = tid + i * NTHREADS, r = idx / PR, c = (idx % PR) * VEC;
+      if (owns(i, tid)) *(uint4*)(dst + (size_t)r * ld + c) = v[i];
+    }
+  }
+};
+
+template <typename F> __device__ inline F zero_frag();
+template <> __device__ inline bf8 zero_frag<bf8>() { return __builtin_bit_cast(bf8, make_uint4(0, 0, 0, 0)); }
+template <> __device__ inline float zero_frag<float>() { return 0.f; }
+
+// MFMA A-operand fragments of one 16-row block, loaded straight from global
+// memory into registers (row-major source, k contiguous, row stride `ld`).
+// Rows at or beyond `valid` (relative to the block's first row) read as zero.
+template <typename E, int K>
+struct AFrag {
+  typedef typename Mma<E>::frag frag;
+  static constexpr int NK = K / Mma<E>::KS;
+  frag f[NK];
+  __device__ inline void load(const E* row0, size_t ld, int valid, int lane) {
+    const int r = lane & 15;
+    const E* src = row0 + (size_t)r * ld + (lane >> 4) * Mma<E>::KPL;
+#pragma unroll
+    for (int ks = 0; ks < NK; ++ks)
+      f[ks] = r < valid ? *(const frag*)(src + ks * Mma<E>::KS) : zero_frag<frag>();
+  }
+};
+
+// Workgroup barrier that orders LDS traffic only: outstanding global loads
+// (software prefetch) stay in flight across it.
+__device__ inline void block_sync_lds() {
+  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
+
+// Four consecutive activation-dtype values of one lane's C fragment.
+template <typename E> struct Quad;
+template <> struct Quad<__bf16> {
+  typedef uint2 raw;
+  __device__ static inline float get(raw r, int j) {
+    const __bf16* e = (const __bf16*)&r;
+    return (float)e[j];
+  }
+  __device__ static inline raw pack(f4 x) {
+    raw r;
+    __bf16* e = (__bf16*)&r;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) e[j] = (__bf16)x[j];
+    return r;
+  }
+};
+template <> struct Quad<float> {
+  typedef uint4 raw;
+  __device__ static inline float get(raw r, int j) { return ((const float*)&r)[j]; }
+  __device__ static inline raw pack(f4 x) {
+    raw r;
+    float* e = (float*)&r;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) e[j] = x[j];
+    return r;
+  }
+};
+
 // ----------------------------------------------------------------- parameters
 struct Params {
   // sizes
@@ -187,8 +270,12 @@ struct Params {
   float* wb;             // [slot][H][C] chunk-local prefix sums of log alpha
   void* wU;              // [slot][H] C x Dv, C-fragment tiled
   void* wW;              // [slot][H][C][Dk]
-  void* wP;              // [slot][H][C][C]  (forward: P; backward: P^T)
-  void* wT;              // [slot][H][C][C]  T (backward only)
+  void* wP;              // [slot][H][C][C]   P = Gam * M * Q K^T
+  void* wKt;             // [slot][H][Dk][C]  K^T
+  void* wT;              // [slot][H][2][C][C] T and P^T (backward only)
+  void* wWt;             // [slot][H][Dk][C]  W^T (backward only)
+  void* wQgt;            // [slot][H][Dk][C]  (diag(g) Q)^T (backward only)
+  void* wdOt;            // [slot][H][Dv][C]  dO^T (backward only)
   // backward
   const void* dO;
   const float* dSfin;

@@ -34,6 +34,7 @@ struct PrepSmem {
       E X[C][DK + P];
     } a;
     E Vt[DV][C + P];
+    E dO[C][DV + P];
   } u;
   E GXt[DK][C + P];
   float A[C][C + 4];
@@ -42,7 +43,24 @@ struct PrepSmem {
   E Tm[C][C + P];
 };
 
-// BWD: additionally write P^T and T for the backward kernels.
+// dst[c*C + r] = scale(r) * src[r*ld + c] for a C x D LDS tile, written to
+// global memory with 16-byte stores (one store covers 16/sizeof(E) rows).
+template <typename E, int D, typename Scale>
+__device__ inline void store_transposed(E* dst, const E* src, int ld, int tid, Scale scale) {
+  constexpr int VEC = 16 / sizeof(E);
+  constexpr int G = C / VEC;
+  for (int idx = tid; idx < D * G; idx += NTHREADS) {
+    const int c = idx / G, r0 = (idx % G) * VEC;
+    uint4 raw;
+    E* e = (E*)&raw;
+#pragma unroll
+    for (int j = 0; j < VEC; ++j) e[j] = fromf<E>(tof(src[(size_t)(r0 + j) * ld + c]) * scale(r0 + j));
+    *(uint4*)(dst + (size_t)c * C + r0) = raw;
+  }
+}
+
+// Forward mode writes b, U, W, P and K^T.  Backward mode (BWD) writes b, U,
+// W and K^T plus T, P^T, W^T and (diag(g) Q)^T for the backward kernels.
 template <typename E, int DK, int DV, bool BWD>
 __global__ __launch_bounds__(NTHREADS) void k_prep(Params p) {
   constexpr int P = Pad<E>::v;
@@ -71,6 +89,11 @@ __global__ __launch_bounds__(NTHREADS) void k_prep(Params p) {
   load_rows<E, DK>(&sm.u.a.Q[0][0], LK, qg, (size_t)H * DK, len, tid);
   __syncthreads();
 
+  // transposed copies for the scans: K^T, and (diag(g) Q)^T for the backward
+  store_transposed<E, DK>((E*)p.wKt + gi * DK * C, &sm.u.a.K[0][0], LK, tid, One());
+  if (BWD)
+    store_transposed<E, DK>((E*)p.wQgt + gi * DK * C, &sm.u.a.Q[0][0], LK, tid,
+                            [&](int r) { return __expf(sm.b[r]); });
   // mixed inputs X = K + lambda Q and the transposed decayed copy (g X)^T
   for (int idx = tid; idx < C * DK; idx += NTHREADS) {
     const int r = idx % C, c = idx / C;
@@ -81,21 +104,23 @@ __global__ __launch_bounds__(NTHREADS) void k_prep(Params p) {
   __syncthreads();
 
   // Gram products X K^T and Q K^T; A (fp32, LDS) and P (workspace)
-  E* wP = (E*)p.wP + gi * C * C;
-  E* wPT = BWD ? (E*)p.wT + gi * 2 * C * C + C * C : nullptr;
+  E* wP = BWD ? (E*)p.wT + gi * 2 * C * C + C * C : (E*)p.wP + gi * C * C;
   for (int t = w; t < 16; t += NWAVES) {
     const int m0 = (t >> 2) * 16, n0 = (t & 3) * 16;
     const f4 gx = mma_k<E, DK>(kmaj(&sm.u.a.X[0][0], LK), kmaj(&sm.u.a.K[0][0], LK), m0, n0, zero4(), lane);
     const f4 qk = mma_k<E, DK>(kmaj(&sm.u.a.Q[0][0], LK), kmaj(&sm.u.a.K[0][0], LK), m0, n0, zero4(), lane);
+    f4 pv;
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const int r = m0 + frow(lane, j), i = n0 + fcol(lane);
       const float gam = (r >= i) ? __expf(sm.b[r] - sm.b[i]) : 0.f;
       sm.A[r][i] = (r > i) ? sm.beta[r] * gam * gx[j] : 0.f;
-      const E pv = fromf<E>(gam * qk[j]);
-      wP[r * C + i] = pv;
-      if (BWD) wPT[i * C + r] = pv;
+      pv[j] = gam * qk[j];
+      if (!BWD) wP[r * C + i] = fromf<E>(pv[j]);
     }
+    // backward: P^T, four consecutive entries of one row of P^T per lane
+    if (BWD)
+      *(typename Quad<E>::raw*)(wP + (n0 + fcol(lane)) * C + m0 + frow(lane, 0)) = Quad<E>::pack(pv);
   }
   __syncthreads();
 
@@ -108,7 +133,7 @@ __global__ __launch_bounds__(NTHREADS) void k_prep(Params p) {
     sm.Tm[r][i] = tv;
     if (BWD) wT[idx] = tv;
   }
-  // V^T (K, Q, X are dead: all Gram reads finished before the solve's barriers)
+  // V^T (K, Q, X are dead: all reads of them finished before the solve's barriers)
   load_rows_t<E, DV>(&sm.u.Vt[0][0], LC, vg, (size_t)H * DV, len, tid, One());
   __syncthreads();
 
@@ -117,17 +142,25 @@ __global__ __launch_bounds__(NTHREADS) void k_prep(Params p) {
   for (int t = w; t < (C / 16) * (DV / 16); t += NWAVES) {
     const int m0 = (t / (DV / 16)) * 16, n0 = (t % (DV / 16)) * 16;
     const f4 u = mma_k<E, C>(kmaj(&sm.Tm[0][0], LC), kmaj(&sm.u.Vt[0][0], LC), m0, n0, zero4(), lane);
-    E* dst = wU + ((size_t)t * 64 + lane) * 4;
-#pragma unroll
-    for (int j = 0; j < 4; ++j) dst[j] = fromf<E>(u[j]);
+    *(typename Quad<E>::raw*)(wU + ((size_t)t * 64 + lane) * 4) = Quad<E>::pack(u);
   }
-  // W = T diag(g) X, row-major C x DK
+  // W = T diag(g) X, row-major C x DK (and W^T in backward mode)
   E* wW = (E*)p.wW + gi * C * DK;
+  E* wWt = BWD ? (E*)p.wWt + gi * DK * C : nullptr;
   for (int t = w; t < (C / 16) * (DK / 16); t += NWAVES) {
     const int m0 = (t / (DK / 16)) * 16, n0 = (t % (DK / 16)) * 16;
     const f4 wv = mma_k<E, C>(kmaj(&sm.Tm[0][0], LC), kmaj(&sm.GXt[0][0], LC), m0, n0, zero4(), lane);
 #pragma unroll
     for (int j = 0; j < 4; ++j) wW[(m0 + frow(lane, j)) * DK + n0 + fcol(lane)] = fromf<E>(wv[j]);
+    if (BWD)
+      *(typename Quad<E>::raw*)(wWt + (size_t)(n0 + fcol(lane)) * C + m0 + frow(lane, 0)) = Quad<E>::pack(wv);
+  }
+  if (BWD) {
+    // dO^T for the backward scan's fragment loads
+    __syncthreads();
+    load_rows<E, DV>(&sm.u.dO[0][0], DV + P, (const E*)p.dO + ((size_t)t0 * H + h) * DV, (size_t)H * DV, len, tid);
+    __syncthreads();
+    store_transposed<E, DV>((E*)p.wdOt + gi * DV * C, &sm.u.dO[0][0], DV + P, tid, One());
   }
 }
 
@@ -135,25 +168,40 @@ template <typename E, int DK, int BV>
 struct ScanFwdSmem {
   static constexpr int P = Pad<E>::v;
   float b[C];
-  E W[C][DK + P];
-  E Q[C][DK + P];
-  E Kt[DK][C + P];
-  E Pm[C][C + P];
-  E S[BV][DK + P];
-  E Dt[BV][C + P];
+  E S[BV][DK + P];    // state tile (MFMA operand copy)
+  E Dt[BV][C + P];    // D^T
+  E Dkt[BV][C + P];   // (diag(g_C / g) D)^T
+  E O[C][BV + P];     // output tile staging
 };
 
-// One workgroup per (sequence, head, Dv tile of BV columns).  The state tile
-// S^T (Dk x BV) lives in fp32 MFMA accumulators across the whole sequence.
-// When p.o is null only the states are produced (saved / final).
+// Operands of one chunk for one wave of the forward scan, prefetched from
+// global memory straight into MFMA fragments (no LDS staging).
+template <typename E, int DK, int DPW>
+struct ScanFwdPre {
+  AFrag<E, DK> W, Q;      // rows 16w.. of W and Q
+  AFrag<E, C> P;          // rows 16w.. of P
+  AFrag<E, C> Kt[2];      // rows 16(2w+i).. of K^T
+  typename Quad<E>::raw U[DPW];
+  float b;
+};
+
+// One workgroup per (sequence, head, Dv tile of BV = 32 value rows); wave w
+// owns rows 16w.. of the chunk's D and O tiles and key rows 32w.. of the
+// state tile.  The state tile S^T (Dk x BV) lives in fp32 MFMA accumulators
+// across the whole sequence.  The next chunk's operands are prefetched into
+// registers while the current chunk is computed.  When p.o is null only the
+// states are produced.
 template <typename E, int DK, int DV, int BV>
 __global__ __launch_bounds__(NTHREADS) void k_scan_fwd(Params p) {
   constexpr int P = Pad<E>::v;
   constexpr int LK = DK + P, LC = C + P;
   constexpr int NVT = DV / BV;
-  constexpr int SPW = (DK / 16) * (BV / 16) / NWAVES;   // state tiles per wave
-  constexpr int DPW = (C / 16) * (BV / 16) / NWAVES;    // D / O tiles per wave
-  static_assert(SPW >= 1 && DPW >= 1, "tile split");
+  constexpr int NB = BV / 16;                 // 16-column blocks per tile
+  constexpr int KS = Mma<E>::KS;
+  static_assert(DK / 16 == 2 * NWAVES || DK / 16 == NWAVES, "key blocks per wave");
+  constexpr int KPW = DK / 16 / NWAVES;       // key row blocks of S^T per wave (1 or 2)
+  typedef typename Quad<E>::raw QR;
+  typedef typename Mma<E>::frag FR;
   __shared__ ScanFwdSmem<E, DK, BV> sm;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   int unit, vt;
@@ -161,100 +209,140 @@ __global__ __launch_bounds__(NTHREADS) void k_scan_fwd(Params p) {
   const int H = p.H, n = unit / H, h = unit % H, v0 = vt * BV;
   int s, e;
   if (!seq_range(p, n, s, e)) return;
-  const int nch = (e - s + C - 1) / C;
   const int base = slot_base(p, n, s);
+  const int nch = max(0, min((e - s + C - 1) / C, p.n_slots - base));
+  const bool with_o = p.o != nullptr;
 
-  f4 acc[SPW];
+  // state: acc[i][nb] = S^T rows 16*(KPW*w+i).., columns 16*nb.. of this tile
+  f4 acc[KPW][NB];
 #pragma unroll
-  for (int i = 0; i < SPW; ++i) {
-    const int t = w * SPW + i, kt = t / (BV / 16), nt = t % (BV / 16);
-    if (p.S0) {
-      const float* src = p.S0 + ((size_t)unit * DV + v0 + nt * 16 + fcol(lane)) * DK + kt * 16 + frow(lane, 0);
-      acc[i] = *(const f4*)src;
-    } else {
-      acc[i] = zero4();
+  for (int i = 0; i < KPW; ++i)
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) {
+      const int kt = KPW * w + i;
+      acc[i][nb] = p.S0 ? *(const f4*)(p.S0 + ((size_t)unit * DV + v0 + nb * 16 + fcol(lane)) * DK + kt * 16 +
+                                       frow(lane, 0))
+                        : zero4();
     }
-  }
 
   const E* qbase = (const E*)p.q;
-  const E* kbase = (const E*)p.k;
-  for (int c = 0; c < nch; ++c) {
-    const int slot = base + c;
-    if (slot >= p.n_slots) break;
+  ScanFwdPre<E, DK, NB> pre;
+  auto prefetch = [&](int c) {
     const int t0 = s + c * C, len = min(C, e - t0);
-    const size_t gi = (size_t)slot * H + h;
-    __syncthreads();
-    if (tid < C) sm.b[tid] = p.wb[gi * C + tid];
-    load_rows<E, DK>(&sm.W[0][0], LK, (const E*)p.wW + gi * C * DK, DK, C, tid);
-    if (p.o) {
-      load_rows<E, DK>(&sm.Q[0][0], LK, qbase + ((size_t)t0 * H + h) * DK, (size_t)H * DK, len, tid);
-      load_rows<E, C>(&sm.Pm[0][0], LC, (const E*)p.wP + gi * C * C, C, C, tid);
+    const size_t gi = (size_t)(base + c) * H + h;
+    pre.b = tid < C ? p.wb[gi * C + tid] : 0.f;
+    pre.W.load((const E*)p.wW + gi * C * DK + (size_t)(16 * w) * DK, DK, 16, lane);
+#pragma unroll
+    for (int i = 0; i < KPW; ++i)
+      pre.Kt[i].load((const E*)p.wKt + gi * DK * C + (size_t)(16 * (KPW * w + i)) * C, C, 16, lane);
+    if (with_o) {
+      pre.Q.load(qbase + ((size_t)(t0 + 16 * w) * H + h) * DK, (size_t)H * DK, len - 16 * w, lane);
+      pre.P.load((const E*)p.wP + gi * C * C + (size_t)(16 * w) * C, C, 16, lane);
     }
 #pragma unroll
-    for (int i = 0; i < SPW; ++i) {
-      const int t = w * SPW + i, kt = t / (BV / 16), nt = t % (BV / 16);
+    for (int nb = 0; nb < NB; ++nb)
+      pre.U[nb] = *(const QR*)((const E*)p.wU + gi * C * DV +
+                               ((size_t)(w * (DV / 16) + vt * NB + nb) * 64 + lane) * 4);
+  };
+  if (nch > 0) prefetch(0);
+
+  for (int c = 0; c < nch; ++c) {
+    const int t0 = s + c * C, len = min(C, e - t0);
+    const size_t gi = (size_t)(base + c) * H + h;
+    const ScanFwdPre<E, DK, NB> cur = pre;
+    block_sync_lds();                      // previous chunk's LDS reads are done
+    if (tid < C) sm.b[tid] = cur.b;
 #pragma unroll
-      for (int j = 0; j < 4; ++j) sm.S[nt * 16 + fcol(lane)][kt * 16 + frow(lane, j)] = fromf<E>(acc[i][j]);
-      if (p.saved)
-        *(f4*)(p.saved + (gi * DV + v0 + nt * 16 + fcol(lane)) * DK + kt * 16 + frow(lane, 0)) = acc[i];
-    }
-    __syncthreads();
+    for (int i = 0; i < KPW; ++i)
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb) {
+        const int kt = KPW * w + i;
+        *(QR*)&sm.S[nb * 16 + fcol(lane)][kt * 16 + frow(lane, 0)] = Quad<E>::pack(acc[i][nb]);
+        if (p.saved)
+          *(f4*)(p.saved + (gi * DV + v0 + nb * 16 + fcol(lane)) * DK + kt * 16 + frow(lane, 0)) = acc[i][nb];
+      }
+    block_sync_lds();
+    if (c + 1 < nch) prefetch(c + 1);
     const float bl = sm.b[C - 1];
-    load_rows_t<E, DK>(&sm.Kt[0][0], LC, kbase + ((size_t)t0 * H + h) * DK, (size_t)H * DK, len, tid,
-                       [&](int r) { return __expf(bl - sm.b[r]); });
-    // D = U - W S^T
-    f4 dfr[DPW];
+    // S fragments (B operand, shared by D and O)
+    FR sf[NB][DK / KS];
 #pragma unroll
-    for (int i = 0; i < DPW; ++i) {
-      const int t = w * DPW + i, mt = t / (BV / 16), nt = t % (BV / 16);
-      const E* us = (const E*)p.wU + gi * C * DV +
-                    ((size_t)(mt * (DV / 16) + vt * (BV / 16) + nt) * 64 + lane) * 4;
-      f4 d = mma_k<E, DK>(kmaj(&sm.W[0][0], LK), kmaj(&sm.S[0][0], LK), mt * 16, nt * 16, zero4(), lane);
+    for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+      for (int ks = 0; ks < DK / KS; ++ks)
+        sf[nb][ks] = Frag<E>::load(kmaj(&sm.S[0][0], LK), nb * 16, ks * KS, lane);
+    // D = U - W S^T (rows 16w..), to LDS as D^T and (diag(g_C/g) D)^T
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) {
+      f4 d = zero4();
+#pragma unroll
+      for (int ks = 0; ks < DK / KS; ++ks) d = Mma<E>::mma(cur.W.f[ks], sf[nb][ks], d);
+      f4 dk;
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
-        d[j] = tof(us[j]) - d[j];
-        sm.Dt[nt * 16 + fcol(lane)][mt * 16 + frow(lane, j)] = fromf<E>(d[j]);
+        d[j] = Quad<E>::get(cur.U[nb], j) - d[j];
+        dk[j] = __expf(bl - sm.b[16 * w + frow(lane, j)]) * d[j];
       }
-      dfr[i] = d;
+      *(QR*)&sm.Dt[nb * 16 + fcol(lane)][16 * w + frow(lane, 0)] = Quad<E>::pack(d);
+      *(QR*)&sm.Dkt[nb * 16 + fcol(lane)][16 * w + frow(lane, 0)] = Quad<E>::pack(dk);
     }
-    __syncthreads();
-    if (p.o) {
-      E* obase = (E*)p.o;
+    block_sync_lds();
+    if (with_o) {
+      // O = diag(g) Q S^T + P D   (rows 16w..)
 #pragma unroll
-      for (int i = 0; i < DPW; ++i) {
-        const int t = w * DPW + i, mt = t / (BV / 16), nt = t % (BV / 16);
-        const f4 o1 = mma_k<E, DK>(kmaj(&sm.Q[0][0], LK), kmaj(&sm.S[0][0], LK), mt * 16, nt * 16, zero4(), lane);
-        const f4 o2 = mma_k<E, C>(kmaj(&sm.Pm[0][0], LC), kmaj(&sm.Dt[0][0], LC), mt * 16, nt * 16, zero4(), lane);
+      for (int nb = 0; nb < NB; ++nb) {
+        f4 o1 = zero4(), o2 = zero4();
+#pragma unroll
+        for (int ks = 0; ks < DK / KS; ++ks) o1 = Mma<E>::mma(cur.Q.f[ks], sf[nb][ks], o1);
+#pragma unroll
+        for (int ks = 0; ks < C / KS; ++ks)
+          o2 = Mma<E>::mma(cur.P.f[ks], Frag<E>::load(kmaj(&sm.Dt[0][0], LC), nb * 16, ks * KS, lane), o2);
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
-          const int r = mt * 16 + frow(lane, j);
-          if (r < len)
-            obase[((size_t)(t0 + r) * H + h) * DV + v0 + nt * 16 + fcol(lane)] =
-                fromf<E>(__expf(sm.b[r]) * o1[j] + o2[j]);
+          const int r = 16 * w + frow(lane, j);
+          sm.O[r][nb * 16 + fcol(lane)] = fromf<E>(__expf(sm.b[r]) * o1[j] + o2[j]);
         }
       }
     }
-    (void)dfr;
+    // S^T <- g_C S^T + K^T diag(g_C/g) D
     const float gC = __expf(bl);
 #pragma unroll
-    for (int i = 0; i < SPW; ++i) {
-      const int t = w * SPW + i, kt = t / (BV / 16), nt = t % (BV / 16);
-      acc[i] = mma_k<E, C>(kmaj(&sm.Kt[0][0], LC), kmaj(&sm.Dt[0][0], LC), kt * 16, nt * 16, gC * acc[i], lane);
+    for (int nb = 0; nb < NB; ++nb) {
+#pragma unroll
+      for (int i = 0; i < KPW; ++i) acc[i][nb] = gC * acc[i][nb];
+#pragma unroll
+      for (int ks = 0; ks < C / KS; ++ks) {
+        const FR bf = Frag<E>::load(kmaj(&sm.Dkt[0][0], LC), nb * 16, ks * KS, lane);
+#pragma unroll
+        for (int i = 0; i < KPW; ++i) acc[i][nb] = Mma<E>::mma(cur.Kt[i].f[ks], bf, acc[i][nb]);
+      }
+    }
+    if (with_o) {
+      block_sync_lds();
+      constexpr int VEC = 16 / sizeof(E), PR = BV / VEC;
+      E* obase = (E*)p.o + ((size_t)t0 * H + h) * DV + v0;
+      for (int idx = tid; idx < C * PR; idx += NTHREADS) {
+        const int r = idx / PR, cc = (idx % PR) * VEC;
+        if (r < len) *(uint4*)(obase + (size_t)r * H * DV + cc) = *(const uint4*)&sm.O[r][cc];
+      }
     }
   }
   if (p.Sfin) {
 #pragma unroll
-    for (int i = 0; i < SPW; ++i) {
-      const int t = w * SPW + i, kt = t / (BV / 16), nt = t % (BV / 16);
-      *(f4*)(p.Sfin + ((size_t)unit * DV + v0 + nt * 16 + fcol(lane)) * DK + kt * 16 + frow(lane, 0)) = acc[i];
-    }
+    for (int i = 0; i < KPW; ++i)
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb) {
+        const int kt = KPW * w + i;
+        *(f4*)(p.Sfin + ((size_t)unit * DV + v0 + nb * 16 + fcol(lane)) * DK + kt * 16 + frow(lane, 0)) =
+            acc[i][nb];
+      }
   }
 }
 
 // ------------------------------------------------------------------ launchers
 template <typename E, int DK, int DV>
 static hipError_t launch_fwd_t(const Params& p, int bwd_prep, int with_scan, hipStream_t st) {
-  constexpr int BV = 32;
+  constexpr int BV = 32;   // value columns per forward-scan workgroup
   if (p.n_slots > 0) {
     dim3 gp(p.n_slots, p.H);
     const int stage = bwd_prep ? ST_PREP_BWD : ST_PREP_FWD;
