@@ -54,20 +54,16 @@ def stage_bytes_per_unit(stage, Dk, Dv, e):
     gates = C * 4
     state = Dv * Dk * 4
     cc_e = C * C * e
-    cc_f = C * C * 4
-    if stage == "prep_fwd":
-        return 2 * act_qk + act_v + 3 * gates + gates + act_v + act_qk + cc_e
-    if stage == "prep_bwd":
-        return 2 * act_qk + act_v + 3 * gates + gates + act_v + act_qk + 3 * cc_e
-    if stage == "scan_fwd":
-        return gates + act_qk + 2 * act_qk + cc_e + act_v + act_v + state
-    if stage == "scan_bwd":
-        return gates + cc_e + act_v + 2 * act_qk + act_qk + state + C * Dv * 4
-    if stage == "intra_a":
-        return (gates + act_qk + cc_e + 2 * act_qk + 2 * state + 2 * act_v + C * Dv * 4 + act_v
-                + act_v + 3 * C * Dk * 4 + 2 * cc_f + gates)
-    if stage == "intra_b":
-        return 3 * gates + 2 * act_qk + 3 * C * Dk * 4 + 2 * cc_f + gates + 2 * act_qk + 3 * gates
+    if stage == "prep_fwd":      # q,k,v, 3 gates -> b, U, W, P, K^T
+        return 2 * act_qk + act_v + 3 * gates + gates + act_v + 2 * act_qk + cc_e
+    if stage == "prep_bwd":      # q,k,v,dO, 3 gates -> b, U, W, K^T, T^T, P^T, W^T, (gQ)^T, dO^T
+        return 2 * act_qk + 2 * act_v + 3 * gates + gates + act_v + 4 * act_qk + 2 * cc_e + act_v
+    if stage == "scan_fwd":      # b, W, K^T, q, P, U -> o, state, D
+        return gates + 3 * act_qk + cc_e + act_v + act_v + state + act_v
+    if stage == "scan_bwd":      # b, P^T, T^T, k, (gQ)^T, W^T, dO^T -> dS', dD, dv
+        return gates + 2 * cc_e + 3 * act_qk + act_v + state + act_v + act_v
+    if stage == "intra":         # b, beta, lam, S, dS', D, dD, dO, v, q, k -> dq, dk, dbeta, dlam, dlog_alpha
+        return 3 * gates + 2 * state + 4 * act_v + 2 * act_qk + 2 * act_qk + 3 * gates
     raise KeyError(stage)
 
 

@@ -48,12 +48,17 @@
  *          kernels then skip the offending sequences (their outputs are left
  *          unspecified) but never access memory out of bounds.
  *
- * Saved per-chunk entry states (written by the forward, read by the backward)
- * ---------------------------------------------------------------------------
- *  float32 [n_slots, H, Dv, Dk], n_slots from qdelta_saved_state_slots.  Chunk c
- *  (0-based) of sequence n occupies slot  n*ceil(T/chunk) + c  (dense) or
- *  floor(cu[n]/chunk) + n + c  (varlen); slots no chunk maps to are untouched.
- *  Each slot holds the state S that the chunk starts from.
+ * Saved context (written by the forward, read by the backward)
+ * --------------------------------------------------------------
+ *  A caller-owned device buffer of qdelta_saved_bytes() bytes (16-byte
+ *  aligned) with two regions, each indexed by unit u = slot * H + h:
+ *    states  float32 [n_slots*H, Dk, Dv] at byte 0: the transposed entry state
+ *            S^T of the chunk (element (k, v) = S[v][k]);
+ *    D       dtype [n_slots*H, C, Dv] after the states: the chunk's
+ *            "new values" D = U - W S^T, rows >= the chunk's length zero.
+ *  n_slots from qdelta_saved_state_slots.  Chunk c (0-based) of sequence n
+ *  occupies slot  n*ceil(T/chunk) + c  (dense) or  floor(cu[n]/chunk) + n + c
+ *  (varlen); slots no chunk maps to are untouched.
  */
 #ifndef QDELTA_H
 #define QDELTA_H
@@ -82,12 +87,16 @@ const char* qdelta_status_string(int status);
 /* Library version as MAJOR*10000 + MINOR*100 + PATCH. */
 int qdelta_version(void);
 
-/* Number of saved-state slots (first dimension of saved_states).
+/* Number of saved-context slots (chunks, counting the varlen holes).
  * n_seqs == 0: dense batch of B sequences of T tokens -> B*ceil(T/chunk).
  * n_seqs  > 0: varlen batch of T total tokens in n_seqs sequences ->
  *              floor(T/chunk) + n_seqs (an upper bound that needs no host copy
  *              of cu_seqlens).  Returns 0 for invalid sizes. */
 size_t qdelta_saved_state_slots(int32_t B, int32_t T, int32_t chunk, int32_t n_seqs);
+
+/* Bytes of the saved context for these sizes (0 for unsupported sizes). */
+size_t qdelta_saved_bytes(int32_t B, int32_t T, int32_t H, int32_t Dk, int32_t Dv, int32_t chunk,
+                          int32_t dtype, int32_t n_seqs);
 
 /* Workspace bytes needed by qdelta_chunk_fwd[_varlen] (is_bwd == 0) or
  * qdelta_chunk_bwd[_varlen] (is_bwd != 0) for these sizes (same meaning of
@@ -102,13 +111,13 @@ size_t qdelta_chunk_workspace_bytes(int32_t B, int32_t T, int32_t H, int32_t Dk,
  *   initial_state [B,H,Dv,Dk] or NULL        entry state (NULL = zero)
  *   o [B,T,H,Dv]                             output o_t = S_t q_t (dtype)
  *   final_state [B,H,Dv,Dk] or NULL          state after the last token
- *   saved_states or NULL                     per-chunk entry states for the backward
+ *   saved or NULL                            saved context for the backward (see above)
  *   ws, ws_bytes                             device workspace */
 int qdelta_chunk_fwd(int32_t B, int32_t T, int32_t H, int32_t Dk, int32_t Dv, int32_t chunk,
                      int32_t dtype, const void* q, const void* k, const void* v,
                      const float* beta, const float* lam, const float* log_alpha,
                      const float* initial_state, void* o, float* final_state,
-                     float* saved_states, void* ws, size_t ws_bytes, hipStream_t stream);
+                     void* saved, void* ws, size_t ws_bytes, hipStream_t stream);
 
 /* Varlen forward: as qdelta_chunk_fwd with B == 1, T total tokens, N sequences
  * delimited by the device array cu_seqlens[N+1]; states are [N,H,Dv,Dk]. */
@@ -117,14 +126,14 @@ int qdelta_chunk_fwd_varlen(int32_t T, int32_t N, const int32_t* cu_seqlens, int
                             const void* q, const void* k, const void* v, const float* beta,
                             const float* lam, const float* log_alpha,
                             const float* initial_state, void* o, float* final_state,
-                            float* saved_states, void* ws, size_t ws_bytes, hipStream_t stream);
+                            void* saved, void* ws, size_t ws_bytes, hipStream_t stream);
 
 /* Chunkwise backward: exact gradients (up to rounding) of
  *     L = <d_o, o> + <d_final_state, final_state>
  * with respect to q, k, v, beta, lam, log_alpha and initial_state.  The paper
  * states no backward pass; this is the derivative of the forward above.
- *   saved_states    from qdelta_chunk_fwd on the same inputs, or NULL to
- *                   recompute the state scan inside this call
+ *   saved           the saved context from qdelta_chunk_fwd on the same inputs,
+ *                   or NULL to recompute the state scan inside this call
  *   d_o [B,T,H,Dv]  (dtype);  d_final_state [B,H,Dv,Dk] or NULL (= zero)
  *   dq, dk [B,T,H,Dk], dv [B,T,H,Dv] (dtype); dbeta, dlam [B,T,H] (fp32)
  *   dlog_alpha [B,T,H] fp32: required iff log_alpha != NULL, else must be NULL
@@ -132,7 +141,7 @@ int qdelta_chunk_fwd_varlen(int32_t T, int32_t N, const int32_t* cu_seqlens, int
 int qdelta_chunk_bwd(int32_t B, int32_t T, int32_t H, int32_t Dk, int32_t Dv, int32_t chunk,
                      int32_t dtype, const void* q, const void* k, const void* v,
                      const float* beta, const float* lam, const float* log_alpha,
-                     const float* initial_state, const float* saved_states, const void* d_o,
+                     const float* initial_state, const void* saved, const void* d_o,
                      const float* d_final_state, void* dq, void* dk, void* dv, float* dbeta,
                      float* dlam, float* dlog_alpha, float* d_initial_state, void* ws,
                      size_t ws_bytes, hipStream_t stream);
@@ -142,7 +151,7 @@ int qdelta_chunk_bwd_varlen(int32_t T, int32_t N, const int32_t* cu_seqlens, int
                             int32_t Dk, int32_t Dv, int32_t chunk, int32_t dtype,
                             const void* q, const void* k, const void* v, const float* beta,
                             const float* lam, const float* log_alpha,
-                            const float* initial_state, const float* saved_states,
+                            const float* initial_state, const void* saved,
                             const void* d_o, const float* d_final_state, void* dq, void* dk,
                             void* dv, float* dbeta, float* dlam, float* dlog_alpha,
                             float* d_initial_state, void* ws, size_t ws_bytes,
@@ -163,14 +172,13 @@ int qdelta_recurrent_step(int32_t N, int32_t H, int32_t Dk, int32_t Dv, int32_t 
  * qdelta_profile_begin() starts recording a pair of HIP events around every
  * kernel launch of the library, on the launch stream, tagged by stage:
  *   0 chunk preparation (forward)       1 forward state scan + chunk output
- *   2 chunk preparation (backward)      3 backward state scan
- *   4 intra-chunk backward, Dv products 5 intra-chunk backward, UT solve and Dk products
- *   6 recurrent step
+ *   2 chunk preparation (backward)      3 backward state scan (+ dv)
+ *   4 intra-chunk backward              5 recurrent step
  * qdelta_profile_end() waits for the recorded events, writes the summed kernel
  * time (milliseconds) and the number of launches of each stage into the
  * caller's arrays of QDELTA_N_STAGES entries (either may be NULL) and stops
  * recording.  Returns QDELTA_EHIP if an event call failed. */
-#define QDELTA_N_STAGES 7
+#define QDELTA_N_STAGES 6
 int qdelta_profile_begin(void);
 int qdelta_profile_end(float* ms, int32_t* launches);
 

@@ -17,9 +17,15 @@ constexpr int kVersion = 10000;  // 1.0.0
 
 struct Layout {
   size_t wb = 0, wU = 0, wW = 0, wP = 0, wKt = 0, wT = 0, wWt = 0, wQgt = 0, wdOt = 0;
-  size_t dSo = 0, dD = 0, dW = 0, dq = 0, dk = 0, dP = 0, dT = 0, db = 0, states = 0;
+  size_t dSo = 0, dDb = 0, states = 0;
   size_t total = 0;
 };
+
+// Saved context: fp32 S^T per unit, then D per unit in the activation dtype.
+size_t saved_states_bytes(size_t units, int Dk, int Dv) { return units * (size_t)Dk * Dv * 4; }
+size_t saved_total_bytes(size_t units, int Dk, int Dv, int esz) {
+  return saved_states_bytes(units, Dk, Dv) + units * (size_t)C * Dv * esz;
+}
 
 Layout make_layout(size_t units, int Dk, int Dv, int esz, bool bwd) {
   Layout L;
@@ -40,14 +46,8 @@ Layout make_layout(size_t units, int Dk, int Dv, int esz, bool bwd) {
     L.wQgt = take(units * C * Dk * esz);
     L.wdOt = take(units * C * Dv * esz);
     L.dSo = take(units * (size_t)Dv * Dk * 4);
-    L.dD = take(units * C * Dv * 4);
-    L.dW = take(units * C * Dk * 4);
-    L.dq = take(units * C * Dk * 4);
-    L.dk = take(units * C * Dk * 4);
-    L.dP = take(units * C * C * 4);
-    L.dT = take(units * C * C * 4);
-    L.db = take(units * C * 4);
-    L.states = take(units * (size_t)Dv * Dk * 4);
+    L.dDb = take(units * C * Dv * esz);
+    L.states = take(saved_total_bytes(units, Dk, Dv, esz));
   }
   L.total = off;
   return L;
@@ -106,7 +106,7 @@ int make_sizes(bool varlen, int32_t B, int32_t T, int32_t N, const int32_t* cu, 
 int fwd_impl(bool varlen, int32_t B, int32_t T, int32_t N, const int32_t* cu, int32_t H,
              int32_t Dk, int32_t Dv, int32_t chunk, int32_t dtype, const void* q, const void* k,
              const void* v, const float* beta, const float* lam, const float* log_alpha,
-             const float* initial_state, void* o, float* final_state, float* saved_states,
+             const float* initial_state, void* o, float* final_state, void* saved,
              void* ws, size_t ws_bytes, hipStream_t stream) {
   Sizes s;
   int rc = make_sizes(varlen, B, T, N, cu, s);
@@ -116,7 +116,7 @@ int fwd_impl(bool varlen, int32_t B, int32_t T, int32_t N, const int32_t* cu, in
   const bool has_tokens = s.tokens > 0;
   if (has_tokens && !(ok_ptr(q) && ok_ptr(k) && ok_ptr(v) && ok_ptr(beta) && ok_ptr(lam) && ok_ptr(o)))
     return QDELTA_EINVAL;
-  if (!ok_opt(log_alpha) || !ok_opt(initial_state) || !ok_opt(final_state) || !ok_opt(saved_states))
+  if (!ok_opt(log_alpha) || !ok_opt(initial_state) || !ok_opt(final_state) || !ok_opt(saved))
     return QDELTA_EINVAL;
   const int esz = dtype == QDELTA_BF16 ? 2 : 4;
   const Layout L = make_layout(s.slots * (size_t)H, Dk, Dv, esz, false);
@@ -136,7 +136,10 @@ int fwd_impl(bool varlen, int32_t B, int32_t T, int32_t N, const int32_t* cu, in
   p.beta = beta; p.lam = lam; p.la = log_alpha; p.S0 = initial_state;
   p.o = has_tokens ? o : nullptr;
   p.Sfin = final_state;
-  p.saved = saved_states;
+  if (saved) {
+    p.saved = static_cast<float*>(saved);
+    p.savedD = static_cast<char*>(saved) + saved_states_bytes(s.slots * (size_t)H, Dk, Dv);
+  }
   p.wb = reinterpret_cast<float*>(w + L.wb);
   p.wU = w + L.wU;
   p.wW = w + L.wW;
@@ -149,7 +152,7 @@ int fwd_impl(bool varlen, int32_t B, int32_t T, int32_t N, const int32_t* cu, in
 int bwd_impl(bool varlen, int32_t B, int32_t T, int32_t N, const int32_t* cu, int32_t H,
              int32_t Dk, int32_t Dv, int32_t chunk, int32_t dtype, const void* q, const void* k,
              const void* v, const float* beta, const float* lam, const float* log_alpha,
-             const float* initial_state, const float* saved_states, const void* d_o,
+             const float* initial_state, const void* saved, const void* d_o,
              const float* d_final_state, void* dq, void* dk, void* dv, float* dbeta, float* dlam,
              float* dlog_alpha, float* d_initial_state, void* ws, size_t ws_bytes,
              hipStream_t stream) {
@@ -165,7 +168,7 @@ int bwd_impl(bool varlen, int32_t B, int32_t T, int32_t N, const int32_t* cu, in
     return QDELTA_EINVAL;
   if ((log_alpha == nullptr) != (dlog_alpha == nullptr) && has_tokens) return QDELTA_EINVAL;
   if (!ok_opt(log_alpha) || !ok_opt(dlog_alpha) || !ok_opt(initial_state) ||
-      !ok_opt(saved_states) || !ok_opt(d_final_state) || !ok_opt(d_initial_state))
+      !ok_opt(saved) || !ok_opt(d_final_state) || !ok_opt(d_initial_state))
     return QDELTA_EINVAL;
   const int esz = dtype == QDELTA_BF16 ? 2 : 4;
   const Layout L = make_layout(s.slots * (size_t)H, Dk, Dv, esz, true);
@@ -197,20 +200,17 @@ int bwd_impl(bool varlen, int32_t B, int32_t T, int32_t N, const int32_t* cu, in
   p.dq = dq; p.dk = dk; p.dv = dv;
   p.dbeta = dbeta; p.dlam = dlam; p.dla = dlog_alpha; p.dS0 = d_initial_state;
   p.w_dSo = reinterpret_cast<float*>(w + L.dSo);
-  p.w_dD = reinterpret_cast<float*>(w + L.dD);
-  p.w_dW = reinterpret_cast<float*>(w + L.dW);
-  p.w_dq = reinterpret_cast<float*>(w + L.dq);
-  p.w_dk = reinterpret_cast<float*>(w + L.dk);
-  p.w_dP = reinterpret_cast<float*>(w + L.dP);
-  p.w_dT = reinterpret_cast<float*>(w + L.dT);
-  p.w_db = reinterpret_cast<float*>(w + L.db);
+  p.w_dDb = w + L.dDb;
+  const size_t units = s.slots * (size_t)H;
   hipError_t e;
-  if (saved_states) {
-    p.saved = const_cast<float*>(saved_states);
+  if (saved) {
+    p.saved = const_cast<float*>(static_cast<const float*>(saved));
+    p.savedD = const_cast<char*>(static_cast<const char*>(saved)) + saved_states_bytes(units, Dk, Dv);
     e = qd::launch_fwd(p, dtype, Dk, Dv, 1, 0, stream);
   } else {
-    // recompute the per-chunk entry states (no outputs) into the workspace
+    // recompute the saved context (no outputs) into the workspace
     p.saved = reinterpret_cast<float*>(w + L.states);
+    p.savedD = w + L.states + saved_states_bytes(units, Dk, Dv);
     e = qd::launch_fwd(p, dtype, Dk, Dv, 1, 1, stream);
   }
   if (e != hipSuccess) return QDELTA_EHIP;
@@ -228,6 +228,18 @@ struct Prof {
 Prof g_prof;
 
 }  // namespace
+
+int qd::device_cu_count() {
+  static int cached[64] = {0};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+  if (cached[dev] == 0) {
+    int n = 0;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) n = 256;
+    cached[dev] = n;
+  }
+  return cached[dev];
+}
 
 void qd::prof_mark(int stage, int after, hipStream_t st) {
   Prof& P = g_prof;
@@ -300,6 +312,14 @@ size_t qdelta_saved_state_slots(int32_t B, int32_t T, int32_t chunk, int32_t n_s
   return slots_for(B, T, n_seqs);
 }
 
+size_t qdelta_saved_bytes(int32_t B, int32_t T, int32_t H, int32_t Dk, int32_t Dv, int32_t chunk,
+                          int32_t dtype, int32_t n_seqs) {
+  if (B < 0 || T < 0 || n_seqs < 0) return 0;
+  const int64_t tokens = n_seqs > 0 ? (int64_t)T : (int64_t)B * T;
+  if (check_dims(tokens, H, Dk, Dv, chunk, dtype) != QDELTA_OK) return 0;
+  return saved_total_bytes(slots_for(B, T, n_seqs) * (size_t)H, Dk, Dv, dtype == QDELTA_BF16 ? 2 : 4);
+}
+
 size_t qdelta_chunk_workspace_bytes(int32_t B, int32_t T, int32_t H, int32_t Dk, int32_t Dv,
                                     int32_t chunk, int32_t dtype, int32_t n_seqs, int32_t is_bwd) {
   if (B < 0 || T < 0 || n_seqs < 0) return 0;
@@ -313,9 +333,9 @@ int qdelta_chunk_fwd(int32_t B, int32_t T, int32_t H, int32_t Dk, int32_t Dv, in
                      int32_t dtype, const void* q, const void* k, const void* v,
                      const float* beta, const float* lam, const float* log_alpha,
                      const float* initial_state, void* o, float* final_state,
-                     float* saved_states, void* ws, size_t ws_bytes, hipStream_t stream) {
+                     void* saved, void* ws, size_t ws_bytes, hipStream_t stream) {
   return fwd_impl(false, B, T, B, nullptr, H, Dk, Dv, chunk, dtype, q, k, v, beta, lam,
-                  log_alpha, initial_state, o, final_state, saved_states, ws, ws_bytes, stream);
+                  log_alpha, initial_state, o, final_state, saved, ws, ws_bytes, stream);
 }
 
 int qdelta_chunk_fwd_varlen(int32_t T, int32_t N, const int32_t* cu_seqlens, int32_t H,
@@ -323,20 +343,20 @@ int qdelta_chunk_fwd_varlen(int32_t T, int32_t N, const int32_t* cu_seqlens, int
                             const void* q, const void* k, const void* v, const float* beta,
                             const float* lam, const float* log_alpha,
                             const float* initial_state, void* o, float* final_state,
-                            float* saved_states, void* ws, size_t ws_bytes, hipStream_t stream) {
+                            void* saved, void* ws, size_t ws_bytes, hipStream_t stream) {
   return fwd_impl(true, 1, T, N, cu_seqlens, H, Dk, Dv, chunk, dtype, q, k, v, beta, lam,
-                  log_alpha, initial_state, o, final_state, saved_states, ws, ws_bytes, stream);
+                  log_alpha, initial_state, o, final_state, saved, ws, ws_bytes, stream);
 }
 
 int qdelta_chunk_bwd(int32_t B, int32_t T, int32_t H, int32_t Dk, int32_t Dv, int32_t chunk,
                      int32_t dtype, const void* q, const void* k, const void* v,
                      const float* beta, const float* lam, const float* log_alpha,
-                     const float* initial_state, const float* saved_states, const void* d_o,
+                     const float* initial_state, const void* saved, const void* d_o,
                      const float* d_final_state, void* dq, void* dk, void* dv, float* dbeta,
                      float* dlam, float* dlog_alpha, float* d_initial_state, void* ws,
                      size_t ws_bytes, hipStream_t stream) {
   return bwd_impl(false, B, T, B, nullptr, H, Dk, Dv, chunk, dtype, q, k, v, beta, lam,
-                  log_alpha, initial_state, saved_states, d_o, d_final_state, dq, dk, dv, dbeta,
+                  log_alpha, initial_state, saved, d_o, d_final_state, dq, dk, dv, dbeta,
                   dlam, dlog_alpha, d_initial_state, ws, ws_bytes, stream);
 }
 
@@ -344,13 +364,13 @@ int qdelta_chunk_bwd_varlen(int32_t T, int32_t N, const int32_t* cu_seqlens, int
                             int32_t Dk, int32_t Dv, int32_t chunk, int32_t dtype,
                             const void* q, const void* k, const void* v, const float* beta,
                             const float* lam, const float* log_alpha,
-                            const float* initial_state, const float* saved_states,
+                            const float* initial_state, const void* saved,
                             const void* d_o, const float* d_final_state, void* dq, void* dk,
                             void* dv, float* dbeta, float* dlam, float* dlog_alpha,
                             float* d_initial_state, void* ws, size_t ws_bytes,
                             hipStream_t stream) {
   return bwd_impl(true, 1, T, N, cu_seqlens, H, Dk, Dv, chunk, dtype, q, k, v, beta, lam,
-                  log_alpha, initial_state, saved_states, d_o, d_final_state, dq, dk, dv, dbeta,
+                  log_alpha, initial_state, saved, d_o, d_final_state, dq, dk, dv, dbeta,
                   dlam, dlog_alpha, d_initial_state, ws, ws_bytes, stream);
 }
 

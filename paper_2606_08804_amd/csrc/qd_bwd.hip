@@ -20,12 +20,11 @@
 //     dlog alpha = reverse chunk-local cumulative sum of db, where db collects
 //     every term through g, Gam, Kbar and g_C.
 //
-// k_scan_bwd : one workgroup per (sequence, head, Dv tile); dS^T tile in fp32
-//              accumulators; writes dD and dS' per chunk.
-// k_intra_a  : per (chunk, head); the products that contract over Dv
-//              (dO S, D dS', dD S, dO D^T, dD V^T) and dV.
-// k_intra_b  : per (chunk, head); UT-solve backward and the remaining
-//              products over Dk, in halves of KH columns; final gradients.
+// k_scan_bwd  : one workgroup per (sequence, head, Dv tile); dS^T tile in fp32
+//               accumulators; per chunk writes dD and dS' and produces dV = T^T dD.
+// k_bwd_intra : per (chunk, head); the products that contract over Dv
+//               (dO S, D dS', dD S, dO D^T, dD V^T), then the UT-solve backward
+//               and the products over Dk; final dq, dk, dbeta, dlambda, dlog alpha.
 #include "qd_common.h"
 #include "qd_launch.h"
 
@@ -38,6 +37,8 @@ struct ScanBwdSmem {
   float b[C];
   E dS[BV][DK + P];   // dS' tile [v][k]
   E dDn[BV][C + P];   // -dD tile, transposed [v][r]
+  E dDr[C][BV + P];   // dD tile staging [r][v]
+  E dV[C][BV + P];    // dV tile staging [i][v]
 };
 
 // Operands of one chunk for one wave of the backward scan, prefetched from
@@ -45,6 +46,7 @@ struct ScanBwdSmem {
 template <typename E, int DK, int KPW, int NB>
 struct ScanBwdPre {
   AFrag<E, C> PT;          // rows 16w.. of P^T
+  AFrag<E, C> TT;          // rows 16w.. of T^T
   AFrag<E, DK> K;          // rows 16w.. of K
   AFrag<E, C> Qg[KPW];     // rows of (diag(g) Q)^T for this wave's key blocks
   AFrag<E, C> Wt[KPW];     // rows of W^T for this wave's key blocks
@@ -92,6 +94,7 @@ __global__ __launch_bounds__(NTHREADS) void k_scan_bwd(Params p) {
     const size_t gi = (size_t)(base + c) * H + h;
     pre.b = tid < C ? p.wb[gi * C + tid] : 0.f;
     pre.PT.load((const E*)p.wT + gi * 2 * C * C + C * C + (size_t)(16 * w) * C, C, 16, lane);
+    pre.TT.load((const E*)p.wT + gi * 2 * C * C + (size_t)(16 * w) * C, C, 16, lane);
     pre.K.load(kb + ((size_t)(t0 + 16 * w) * H + h) * DK, (size_t)H * DK, len - 16 * w, lane);
 #pragma unroll
     for (int i = 0; i < KPW; ++i) {
@@ -107,6 +110,7 @@ __global__ __launch_bounds__(NTHREADS) void k_scan_bwd(Params p) {
 
   for (int c = nch - 1; c >= 0; --c) {
     const size_t gi = (size_t)(base + c) * H + h;
+    const int t0 = s + c * C, len = min(C, e - t0);
     const ScanBwdPre<E, DK, KPW, NB> cur = pre;
     block_sync_lds();
     if (tid < C) sm.b[tid] = cur.b;
@@ -116,7 +120,9 @@ __global__ __launch_bounds__(NTHREADS) void k_scan_bwd(Params p) {
       for (int nb = 0; nb < NB; ++nb) {
         const int kt = KPW * w + i;
         *(QR*)&sm.dS[nb * 16 + fcol(lane)][kt * 16 + frow(lane, 0)] = Quad<E>::pack(acc[i][nb]);
-        *(f4*)(p.w_dSo + (gi * DV + v0 + nb * 16 + fcol(lane)) * DK + kt * 16 + frow(lane, 0)) = acc[i][nb];
+        float* dst = p.w_dSo + (gi * DK + kt * 16 + frow(lane, 0)) * DV + v0 + nb * 16 + fcol(lane);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) dst[(size_t)j * DV] = acc[i][nb][j];
       }
     block_sync_lds();
     if (c > 0) prefetch(c - 1);
@@ -136,11 +142,21 @@ __global__ __launch_bounds__(NTHREADS) void k_scan_bwd(Params p) {
         const int r = 16 * w + frow(lane, j);
         const float d = d1[j] + __expf(bl - sm.b[r]) * d2[j];
         dn[j] = -d;
-        p.w_dD[(gi * C + r) * DV + v0 + nb * 16 + fcol(lane)] = d;
+        sm.dDr[r][nb * 16 + fcol(lane)] = fromf<E>(d);
       }
       *(QR*)&sm.dDn[nb * 16 + fcol(lane)][16 * w + frow(lane, 0)] = Quad<E>::pack(dn);
     }
     block_sync_lds();
+    // dV = T^T dD  (rows 16w..), staged for coalesced stores
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) {
+      f4 dv = zero4();
+#pragma unroll
+      for (int ks = 0; ks < C / KS; ++ks)
+        dv = Mma<E>::mma(cur.TT.f[ks], Frag<E>::load(kmaj(&sm.dDn[0][0], LC), nb * 16, ks * KS, lane), dv);
+#pragma unroll
+      for (int j = 0; j < 4; ++j) sm.dV[16 * w + frow(lane, j)][nb * 16 + fcol(lane)] = fromf<E>(-dv[j]);
+    }
     // dS_entry^T = g_C dS'^T + (g Q)^T dO - W^T dD
     const float gC = __expf(bl);
 #pragma unroll
@@ -157,6 +173,17 @@ __global__ __launch_bounds__(NTHREADS) void k_scan_bwd(Params p) {
         }
       }
     }
+    block_sync_lds();
+    {
+      constexpr int VEC = 16 / sizeof(E), PR = BV / VEC;
+      E* ddst = (E*)p.w_dDb + gi * C * DV + v0;
+      E* vdst = (E*)p.dv + ((size_t)t0 * H + h) * DV + v0;
+      for (int idx = tid; idx < C * PR; idx += NTHREADS) {
+        const int r = idx / PR, cc = (idx % PR) * VEC;
+        *(uint4*)(ddst + (size_t)r * DV + cc) = *(const uint4*)&sm.dDr[r][cc];
+        if (r < len) *(uint4*)(vdst + (size_t)r * H * DV + cc) = *(const uint4*)&sm.dV[r][cc];
+      }
+    }
   }
   if (p.dS0) {
 #pragma unroll
@@ -170,190 +197,30 @@ __global__ __launch_bounds__(NTHREADS) void k_scan_bwd(Params p) {
   }
 }
 
-// ------------------------------------------------------------------ intra A
-template <typename E, int DK, int BV>
-struct IntraASmem {
+// ------------------------------------------------------------------ intra
+// Fused intra-chunk backward, one workgroup per (chunk, head) unit.
+//
+// Phase A walks the value dimension in tiles of 32 columns (next tile
+// prefetched into registers) and accumulates, for rows 16w.. of wave w,
+//   aQ = dO S,  aK = D dS',  aW = dD S   (C x Dk)   and   aP = dO D^T, aT = dD V^T (C x C)
+// with dO, D, dD fragments loaded straight from global memory and the S^T,
+// dS'^T, D and V tiles shared through LDS.  Phase B recomputes the Gram
+// products and the UT solve, back-propagates through it, and produces dq, dk,
+// dbeta, dlambda and the decay gradient; the Dk direction is processed in
+// quarters of KH columns with the next quarter's q and k prefetched.
+template <typename E, int DK>
+struct BwdSmem {
   static constexpr int P = Pad<E>::v;
-  float b[C], g[C], kb[C], rq[C], rk[C];
+  static constexpr int BV = 32, KH = 32;
+  float b[C], g[C], kb[C], beta[C], lam[C], db[C], dbeta[C], dlam[C], tk[C];
   float sdot[NWAVES];
-  E W[C][DK + P];
-  E Tm[C][C + P];
-  E Q[C][DK + P];
-  E K[C][DK + P];
-  E S[BV][DK + P];
-  E dS[BV][DK + P];
-  E dO[C][BV + P];
-  E dD[C][BV + P];
-  E V[C][BV + P];
-  E D[C][BV + P];
-};
-
-template <typename E, int DK, int DV, int BV>
-__global__ __launch_bounds__(NTHREADS) void k_intra_a(Params p) {
-  constexpr int P = Pad<E>::v;
-  constexpr int LK = DK + P, LC = C + P, LB = BV + P;
-  constexpr int QT = (C / 16) * (DK / 16) / NWAVES;   // C x DK tiles per wave (one row block)
-  constexpr int PT = 16 / NWAVES;                      // C x C tiles per wave
-  constexpr int DT = (C / 16) * (BV / 16) / NWAVES;    // C x BV tiles per wave
-  static_assert(QT == DK / 16, "each wave owns one 16-row block of the C x Dk accumulators");
-  __shared__ IntraASmem<E, DK, BV> sm;
-  const int g = blockIdx.x, h = blockIdx.y, tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-  int n, t0, len;
-  if (!locate(p, g, n, t0, len)) return;
-  const int H = p.H;
-  const size_t gi = (size_t)g * H + h;
-
-  if (tid < C) {
-    const float b = p.wb[gi * C + tid];
-    sm.b[tid] = b;
-    sm.g[tid] = __expf(b);
-  }
-  load_rows<E, DK>(&sm.W[0][0], LK, (const E*)p.wW + gi * C * DK, DK, C, tid);
-  load_rows<E, C>(&sm.Tm[0][0], LC, (const E*)p.wT + gi * 2 * C * C, C, C, tid);
-  load_rows<E, DK>(&sm.Q[0][0], LK, (const E*)p.q + ((size_t)t0 * H + h) * DK, (size_t)H * DK, len, tid);
-  load_rows<E, DK>(&sm.K[0][0], LK, (const E*)p.k + ((size_t)t0 * H + h) * DK, (size_t)H * DK, len, tid);
-
-  f4 aQ[QT], aK[QT], aW[QT], aP[PT], aT[PT];
-#pragma unroll
-  for (int i = 0; i < QT; ++i) aQ[i] = aK[i] = aW[i] = zero4();
-#pragma unroll
-  for (int i = 0; i < PT; ++i) aP[i] = aT[i] = zero4();
-  float sdot = 0.f;
-
-  const float* Sg = p.saved + gi * DV * DK;
-  const float* dSg = p.w_dSo + gi * DV * DK;
-  const E* dOg = (const E*)p.dO + ((size_t)t0 * H + h) * DV;
-  const E* Vg = (const E*)p.v + ((size_t)t0 * H + h) * DV;
-  const float* dDg = p.w_dD + gi * C * DV;
-  E* dvout = (E*)p.dv;
-
-  for (int vt = 0; vt < DV / BV; ++vt) {
-    const int v0 = vt * BV;
-    __syncthreads();
-    for (int idx = tid; idx < BV * DK / 4; idx += NTHREADS) {
-      const int vv = idx / (DK / 4), kk = (idx % (DK / 4)) * 4;
-      const f4 sv = *(const f4*)(Sg + (size_t)(v0 + vv) * DK + kk);
-      const f4 dv = *(const f4*)(dSg + (size_t)(v0 + vv) * DK + kk);
-      sdot += sv[0] * dv[0] + sv[1] * dv[1] + sv[2] * dv[2] + sv[3] * dv[3];
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        sm.S[vv][kk + j] = fromf<E>(sv[j]);
-        sm.dS[vv][kk + j] = fromf<E>(dv[j]);
-      }
-    }
-    load_rows<E, BV>(&sm.dO[0][0], LB, dOg + v0, (size_t)H * DV, len, tid);
-    load_rows<E, BV>(&sm.V[0][0], LB, Vg + v0, (size_t)H * DV, len, tid);
-    for (int idx = tid; idx < C * BV / 4; idx += NTHREADS) {
-      const int r = idx / (BV / 4), vv = (idx % (BV / 4)) * 4;
-      const f4 d = *(const f4*)(dDg + (size_t)r * DV + v0 + vv);
-#pragma unroll
-      for (int j = 0; j < 4; ++j) sm.dD[r][vv + j] = fromf<E>(d[j]);
-    }
-    __syncthreads();
-    // D = U - W S^T (tile) and dV = T^T dD (tile)
-#pragma unroll
-    for (int i = 0; i < DT; ++i) {
-      const int t = w * DT + i, mt = t / (BV / 16), nt = t % (BV / 16);
-      const E* us = (const E*)p.wU + gi * C * DV +
-                    ((size_t)(mt * (DV / 16) + vt * (BV / 16) + nt) * 64 + lane) * 4;
-      f4 d = mma_k<E, DK>(kmaj(&sm.W[0][0], LK), kmaj(&sm.S[0][0], LK), mt * 16, nt * 16, zero4(), lane);
-#pragma unroll
-      for (int j = 0; j < 4; ++j)
-        sm.D[mt * 16 + frow(lane, j)][nt * 16 + fcol(lane)] = fromf<E>(tof(us[j]) - d[j]);
-      const f4 dv = mma_k<E, C>(imaj(&sm.Tm[0][0], LC), imaj(&sm.dD[0][0], LB), mt * 16, nt * 16, zero4(), lane);
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const int r = mt * 16 + frow(lane, j);
-        if (r < len) dvout[((size_t)(t0 + r) * H + h) * DV + v0 + nt * 16 + fcol(lane)] = fromf<E>(dv[j]);
-      }
-    }
-    __syncthreads();
-#pragma unroll
-    for (int i = 0; i < QT; ++i) {
-      const int t = w * QT + i, mt = t / (DK / 16), nt = t % (DK / 16);
-      aQ[i] = mma_k<E, BV>(kmaj(&sm.dO[0][0], LB), imaj(&sm.S[0][0], LK), mt * 16, nt * 16, aQ[i], lane);
-      aK[i] = mma_k<E, BV>(kmaj(&sm.D[0][0], LB), imaj(&sm.dS[0][0], LK), mt * 16, nt * 16, aK[i], lane);
-      aW[i] = mma_k<E, BV>(kmaj(&sm.dD[0][0], LB), imaj(&sm.S[0][0], LK), mt * 16, nt * 16, aW[i], lane);
-    }
-#pragma unroll
-    for (int i = 0; i < PT; ++i) {
-      const int t = w * PT + i, mt = t / 4, nt = t % 4;
-      aP[i] = mma_k<E, BV>(kmaj(&sm.dO[0][0], LB), kmaj(&sm.D[0][0], LB), mt * 16, nt * 16, aP[i], lane);
-      aT[i] = mma_k<E, BV>(kmaj(&sm.dD[0][0], LB), kmaj(&sm.V[0][0], LB), mt * 16, nt * 16, aT[i], lane);
-    }
-  }
-
-  // <dS', S> over the whole state
-  sdot = wave_sum(sdot);
-  if (lane == 0) sm.sdot[w] = sdot;
-
-  // epilogue: dq part, dk part, dW, dP, dT_part and the db terms
-  float* wq = p.w_dq + gi * C * DK;
-  float* wk = p.w_dk + gi * C * DK;
-  float* ww = p.w_dW + gi * C * DK;
-  float rq[4] = {0.f, 0.f, 0.f, 0.f}, rk[4] = {0.f, 0.f, 0.f, 0.f};
-  const int mt = w;   // this wave's row block
-#pragma unroll
-  for (int i = 0; i < QT; ++i) {
-    const int nt = (w * QT + i) % (DK / 16);
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int r = mt * 16 + frow(lane, j), kk = nt * 16 + fcol(lane);
-      rq[j] += tof(sm.Q[r][kk]) * aQ[i][j];
-      rk[j] += tof(sm.K[r][kk]) * aK[i][j];
-      wq[r * DK + kk] = sm.g[r] * aQ[i][j];
-      wk[r * DK + kk] = __expf(sm.b[C - 1] - sm.b[r]) * aK[i][j];
-      ww[r * DK + kk] = -aW[i][j];
-    }
-  }
-#pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    rq[j] = sum16(rq[j]);
-    rk[j] = sum16(rk[j]);
-  }
-  if (fcol(lane) == 0) {
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int r = mt * 16 + frow(lane, j);
-      sm.rq[r] = rq[j];
-      sm.rk[r] = rk[j];
-    }
-  }
-  float* wPd = p.w_dP + gi * C * C;
-  float* wTd = p.w_dT + gi * C * C;
-#pragma unroll
-  for (int i = 0; i < PT; ++i) {
-    const int t = w * PT + i, m0 = (t / 4) * 16, n0 = (t % 4) * 16;
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int r = m0 + frow(lane, j), c = n0 + fcol(lane);
-      wPd[r * C + c] = aP[i][j];
-      wTd[r * C + c] = aT[i][j];
-    }
-  }
-  __syncthreads();
-  if (tid < C) {
-    const int r = tid;
-    const float bl = sm.b[C - 1];
-    const float tr = __expf(bl - sm.b[r]) * sm.rk[r];   // Kbar row term
-    float db = sm.g[r] * sm.rq[r] - tr;
-    float tot = tr;
-#pragma unroll
-    for (int off = 32; off >= 1; off >>= 1) tot += __shfl_xor(tot, off, 64);
-    if (r == C - 1) {
-      const float sd = sm.sdot[0] + sm.sdot[1] + sm.sdot[2] + sm.sdot[3];
-      db += tot + __expf(bl) * sd;
-    }
-    p.w_db[gi * C + r] = db;
-  }
-}
-
-// ------------------------------------------------------------------ intra B
-template <typename E, int KH>
-struct IntraBSmem {
-  static constexpr int P = Pad<E>::v;
-  float b[C], g[C], beta[C], lam[C], db[C], dbeta[C], dlam[C];
   union {
+    struct {
+      E St[DK][BV + P];     // S^T tile (k, v)
+      E dSt[DK][BV + P];    // dS'^T tile (k, v)
+      E D[C][BV + P];       // D tile (r, v)
+      E V[C][BV + P];       // V tile (r, v)
+    } a;
     struct {
       E Q[C][KH + P];
       E K[C][KH + P];
@@ -377,41 +244,123 @@ struct IntraBSmem {
   E dQK[C][C + P];
 };
 
-template <typename E, int DK, int KH>
-__global__ __launch_bounds__(NTHREADS) void k_intra_b(Params p) {
+template <typename E, int DK>
+struct BwdPreA {
+  TileRegsF<E, DK, 32> S, dS;   // S^T, dS'^T tiles (fp32 in memory)
+  TileRegs<E, C, 32> D, V;
+  AFrag<E, 32> dO, Df, dD;      // rows 16w.. of dO, D, dD over the tile's columns
+};
+
+template <typename E, int DK, int DV>
+__global__ __launch_bounds__(NTHREADS) void k_bwd_intra(Params p) {
   constexpr int P = Pad<E>::v;
-  constexpr int LH = KH + P, LC = C + P, LF = C + 4;
-  constexpr int HT = (C / 16) * (KH / 16);   // C x KH tiles
-  __shared__ IntraBSmem<E, KH> sm;
+  constexpr int BV = 32, KH = 32;
+  constexpr int LC = C + P, LB = BV + P, LH = KH + P, LF = C + 4;
+  constexpr int KS = Mma<E>::KS;
+  constexpr int NKB = DK / 16;        // 16-column blocks of Dk
+  constexpr int NQ = DK / KH;         // Dk quarters in phase B
+  constexpr int NVT = DV / BV;
+  typedef typename Mma<E>::frag FR;
+  __shared__ BwdSmem<E, DK> sm;
   const int g = blockIdx.x, h = blockIdx.y, tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   int n, t0, len;
   if (!locate(p, g, n, t0, len)) return;
   const int H = p.H;
   const size_t gi = (size_t)g * H + h;
+  const size_t arow = (size_t)t0 * H + h;   // first activation row of the chunk
 
   if (tid < C) {
     const bool ok = tid < len;
-    const size_t gt = (size_t)(t0 + tid) * H + h;
+    const size_t gt = arow + (size_t)tid * H;
     const float b = p.wb[gi * C + tid];
     sm.b[tid] = b;
     sm.g[tid] = __expf(b);
     sm.beta[tid] = ok ? p.beta[gt] : 0.f;
     sm.lam[tid] = ok ? p.lam[gt] : 0.f;
     sm.dlam[tid] = 0.f;
+    sm.tk[tid] = 0.f;
   }
-  const E* qg = (const E*)p.q + ((size_t)t0 * H + h) * DK;
-  const E* kg = (const E*)p.k + ((size_t)t0 * H + h) * DK;
-  const float* dWg = p.w_dW + gi * C * DK;
 
-  auto load_half = [&](int k0) {
-    load_rows<E, KH>(&sm.u.h.Q[0][0], LH, qg + k0, (size_t)H * DK, len, tid);
-    load_rows<E, KH>(&sm.u.h.K[0][0], LH, kg + k0, (size_t)H * DK, len, tid);
-    for (int idx = tid; idx < C * KH / 4; idx += NTHREADS) {
-      const int r = idx / (KH / 4), kk = (idx % (KH / 4)) * 4;
-      const f4 d = *(const f4*)(dWg + (size_t)r * DK + k0 + kk);
+  // ---------------- phase A: contractions over the value dimension
+  f4 aQ[NKB], aK[NKB], aW[NKB], aP[4], aT[4];
 #pragma unroll
-      for (int j = 0; j < 4; ++j) sm.u.h.dW[r][kk + j] = fromf<E>(d[j]);
+  for (int i = 0; i < NKB; ++i) aQ[i] = aK[i] = aW[i] = zero4();
+#pragma unroll
+  for (int i = 0; i < 4; ++i) aP[i] = aT[i] = zero4();
+  float sdot = 0.f;
+  const float* Sg = p.saved + gi * DK * DV;
+  const float* dSg = p.w_dSo + gi * DK * DV;
+  const E* Dg = (const E*)p.savedD + gi * C * DV;
+  const E* dDg = (const E*)p.w_dDb + gi * C * DV;
+  const E* dOg = (const E*)p.dO + arow * DV;
+  const E* Vg = (const E*)p.v + arow * DV;
+  BwdPreA<E, DK> pa;
+  auto fetchA = [&](int vt) {
+    const int v0 = vt * BV;
+    pa.S.load(Sg + v0, DV, tid);
+    pa.dS.load(dSg + v0, DV, tid);
+    pa.D.load(Dg + v0, DV, C, tid);
+    pa.V.load(Vg + v0, (size_t)H * DV, len, tid);
+    pa.dO.load(dOg + (size_t)(16 * w) * H * DV + v0, (size_t)H * DV, len - 16 * w, lane);
+    pa.Df.load(Dg + (size_t)(16 * w) * DV + v0, DV, 16, lane);
+    pa.dD.load(dDg + (size_t)(16 * w) * DV + v0, DV, 16, lane);
+  };
+  fetchA(0);
+  for (int vt = 0; vt < NVT; ++vt) {
+    const BwdPreA<E, DK> cur = pa;
+    if (vt + 1 < NVT) fetchA(vt + 1);
+    block_sync_lds();
+    cur.S.store(&sm.u.a.St[0][0], LB, tid);
+    cur.dS.store(&sm.u.a.dSt[0][0], LB, tid);
+    cur.D.store(&sm.u.a.D[0][0], LB, tid);
+    cur.V.store(&sm.u.a.V[0][0], LB, tid);
+#pragma unroll
+    for (int i = 0; i < cur.S.N; ++i)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) sdot += cur.S.v[i][j] * cur.dS.v[i][j];
+    block_sync_lds();
+#pragma unroll
+    for (int kb = 0; kb < NKB; ++kb) {
+#pragma unroll
+      for (int ks = 0; ks < BV / KS; ++ks) {
+        const FR bS = Frag<E>::load(kmaj(&sm.u.a.St[0][0], LB), kb * 16, ks * KS, lane);
+        const FR bdS = Frag<E>::load(kmaj(&sm.u.a.dSt[0][0], LB), kb * 16, ks * KS, lane);
+        aQ[kb] = Mma<E>::mma(cur.dO.f[ks], bS, aQ[kb]);
+        aW[kb] = Mma<E>::mma(cur.dD.f[ks], bS, aW[kb]);
+        aK[kb] = Mma<E>::mma(cur.Df.f[ks], bdS, aK[kb]);
+      }
     }
+#pragma unroll
+    for (int ib = 0; ib < 4; ++ib) {
+#pragma unroll
+      for (int ks = 0; ks < BV / KS; ++ks) {
+        const FR bD = Frag<E>::load(kmaj(&sm.u.a.D[0][0], LB), ib * 16, ks * KS, lane);
+        const FR bV = Frag<E>::load(kmaj(&sm.u.a.V[0][0], LB), ib * 16, ks * KS, lane);
+        aP[ib] = Mma<E>::mma(cur.dO.f[ks], bD, aP[ib]);
+        aT[ib] = Mma<E>::mma(cur.dD.f[ks], bV, aT[ib]);
+      }
+    }
+  }
+  sdot = wave_sum(sdot);
+  if (lane == 0) sm.sdot[w] = sdot;
+
+  // ---------------- phase B
+  const E* qg = (const E*)p.q + arow * DK;
+  const E* kg = (const E*)p.k + arow * DK;
+  TileRegs<E, C, KH> rQ, rK;
+  auto fetchQ = [&](int k0) {
+    rQ.load(qg + k0, (size_t)H * DK, len, tid);
+    rK.load(kg + k0, (size_t)H * DK, len, tid);
+  };
+  // stage quarter kq of Q, K (from registers), dW = -aW (rows 16w..) and X, g X
+  auto stage_quarter = [&](int kq) {
+    rQ.store(&sm.u.h.Q[0][0], LH, tid);
+    rK.store(&sm.u.h.K[0][0], LH, tid);
+#pragma unroll
+    for (int nb = 0; nb < KH / 16; ++nb)
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        sm.u.h.dW[16 * w + frow(lane, j)][nb * 16 + fcol(lane)] = fromf<E>(-aW[kq * (KH / 16) + nb][j]);
   };
   auto make_x = [&]() {
     for (int idx = tid; idx < C * KH; idx += NTHREADS) {
@@ -422,47 +371,44 @@ __global__ __launch_bounds__(NTHREADS) void k_intra_b(Params p) {
     }
   };
 
-  // ---- phase 1: G = X K^T, QK = Q K^T, dT2 = dW (g X)^T over Dk halves
+  // phase B1: G = X K^T, QK = Q K^T, dT2 = dW (g X)^T, over the Dk quarters
   f4 aG[4], aQK[4], adT[4];
 #pragma unroll
   for (int i = 0; i < 4; ++i) aG[i] = aQK[i] = adT[i] = zero4();
-  for (int k0 = 0; k0 < DK; k0 += KH) {
-    __syncthreads();
-    load_half(k0);
-    __syncthreads();
-    make_x();
-    __syncthreads();
+  fetchQ(0);
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int t = w * 4 + i, m0 = (t / 4) * 16, n0 = (t % 4) * 16;
-      aG[i] = mma_k<E, KH>(kmaj(&sm.u.h.X[0][0], LH), kmaj(&sm.u.h.K[0][0], LH), m0, n0, aG[i], lane);
-      aQK[i] = mma_k<E, KH>(kmaj(&sm.u.h.Q[0][0], LH), kmaj(&sm.u.h.K[0][0], LH), m0, n0, aQK[i], lane);
-      adT[i] = mma_k<E, KH>(kmaj(&sm.u.h.dW[0][0], LH), kmaj(&sm.u.h.GX[0][0], LH), m0, n0, adT[i], lane);
+  for (int kq = 0; kq < NQ; ++kq) {
+    block_sync_lds();
+    stage_quarter(kq);
+    fetchQ(kq + 1 < NQ ? (kq + 1) * KH : 0);
+    block_sync_lds();
+    make_x();
+    block_sync_lds();
+#pragma unroll
+    for (int ib = 0; ib < 4; ++ib) {
+      aG[ib] = mma_k<E, KH>(kmaj(&sm.u.h.X[0][0], LH), kmaj(&sm.u.h.K[0][0], LH), 16 * w, ib * 16, aG[ib], lane);
+      aQK[ib] = mma_k<E, KH>(kmaj(&sm.u.h.Q[0][0], LH), kmaj(&sm.u.h.K[0][0], LH), 16 * w, ib * 16, aQK[ib], lane);
+      adT[ib] = mma_k<E, KH>(kmaj(&sm.u.h.dW[0][0], LH), kmaj(&sm.u.h.GX[0][0], LH), 16 * w, ib * 16, adT[ib], lane);
     }
   }
-  __syncthreads();
+  block_sync_lds();
 
-  // ---- phase 2: UT-solve backward and the C x C gradient terms
-  const float* dTg = p.w_dT + gi * C * C;
-  const float* dPg = p.w_dP + gi * C * C;
+  // phase B2: UT-solve backward and the C x C gradient terms
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int t = w * 4 + i, m0 = (t / 4) * 16, n0 = (t % 4) * 16;
+  for (int ib = 0; ib < 4; ++ib) {
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
-      const int r = m0 + frow(lane, j), c = n0 + fcol(lane);
-      sm.u.c.G[r][c] = aG[i][j];
-      sm.u.c.QK[r][c] = aQK[i][j];
-      sm.u.c.dT[r][c] = dTg[r * C + c] + adT[i][j];
-      sm.u.c.A[r][c] = (r > c) ? sm.beta[r] * __expf(sm.b[r] - sm.b[c]) * aG[i][j] : 0.f;
+      const int r = 16 * w + frow(lane, j), c = ib * 16 + fcol(lane);
+      sm.u.c.G[r][c] = aG[ib][j];
+      sm.u.c.QK[r][c] = aQK[ib][j];
+      sm.u.c.dT[r][c] = aT[ib][j] + adT[ib][j];
+      sm.u.c.A[r][c] = (r > c) ? sm.beta[r] * __expf(sm.b[r] - sm.b[c]) * aG[ib][j] : 0.f;
     }
   }
-  __syncthreads();
+  if (tid < C) sm.kb[tid] = __expf(sm.b[C - 1] - sm.b[tid]);
+  block_sync_lds();
   unit_lower_inverse(&sm.u.c.A[0][0], LF, &sm.u.c.M[0][0], LF, sm.u.c.tmp, tid);
-  // Four lanes share one row (or column) of the C x C element-wise passes:
-  // lane quad q4 = tid >> 2 owns row/column q4, segment (tid & 3) * 16 .. +16.
   const int q4 = tid >> 2, seg = (tid & 3) * 16;
-  // dbeta (T = Minv diag(beta)): column sums of dT * Minv;  T into LDS
   {
     float s4 = 0.f;
 #pragma unroll 4
@@ -475,43 +421,34 @@ __global__ __launch_bounds__(NTHREADS) void k_intra_b(Params p) {
     const int r = idx / C, i = idx % C;
     sm.Tm[r][i] = fromf<E>(sm.u.c.M[r][i] * sm.beta[i]);
   }
-  __syncthreads();
-  // dMinv = dT diag(beta), in place
+  block_sync_lds();
   for (int idx = tid; idx < C * C; idx += NTHREADS) {
     const int r = idx / C, i = idx % C;
-    sm.u.c.dT[r][i] *= sm.beta[i];
+    sm.u.c.dT[r][i] *= sm.beta[i];          // dMinv = dT diag(beta)
   }
-  __syncthreads();
-  // Y = Minv^T dMinv
+  block_sync_lds();
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int t = w * 4 + i, m0 = (t / 4) * 16, n0 = (t % 4) * 16;
-    const f4 y = mma_k<E, C>(imaj(&sm.u.c.M[0][0], LF), imaj(&sm.u.c.dT[0][0], LF), m0, n0, zero4(), lane);
+  for (int ib = 0; ib < 4; ++ib) {            // Y = Minv^T dMinv
+    const f4 y = mma_k<E, C>(imaj(&sm.u.c.M[0][0], LF), imaj(&sm.u.c.dT[0][0], LF), 16 * w, ib * 16, zero4(), lane);
 #pragma unroll
-    for (int j = 0; j < 4; ++j) sm.u.c.Y[m0 + frow(lane, j)][n0 + fcol(lane)] = y[j];
+    for (int j = 0; j < 4; ++j) sm.u.c.Y[16 * w + frow(lane, j)][ib * 16 + fcol(lane)] = y[j];
   }
-  __syncthreads();
-  // dA = strictLower(-Y Minv^T)   (A is dead after the solve: reuse its storage)
+  block_sync_lds();
+  // dP = dO D^T from phase A (rows 16w..) into the dead dMinv buffer
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int t = w * 4 + i, m0 = (t / 4) * 16, n0 = (t % 4) * 16;
-    const f4 y = mma_k<E, C>(kmaj(&sm.u.c.Y[0][0], LF), kmaj(&sm.u.c.M[0][0], LF), m0, n0, zero4(), lane);
+  for (int ib = 0; ib < 4; ++ib)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) sm.u.c.dT[16 * w + frow(lane, j)][ib * 16 + fcol(lane)] = aP[ib][j];
+#pragma unroll
+  for (int ib = 0; ib < 4; ++ib) {            // dA = strictLower(-Y Minv^T)
+    const f4 y = mma_k<E, C>(kmaj(&sm.u.c.Y[0][0], LF), kmaj(&sm.u.c.M[0][0], LF), 16 * w, ib * 16, zero4(), lane);
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
-      const int r = m0 + frow(lane, j), c = n0 + fcol(lane);
+      const int r = 16 * w + frow(lane, j), c = ib * 16 + fcol(lane);
       sm.u.c.A[r][c] = (r > c) ? -y[j] : 0.f;
     }
   }
-  __syncthreads();
-  // dP (from intra A) into the dead Y buffer, coalesced
-  for (int idx = tid; idx < C * C / 4; idx += NTHREADS) {
-    const int r = idx / (C / 4), c = (idx % (C / 4)) * 4;
-    *(f4*)&sm.u.c.Y[r][c] = *(const f4*)(dPg + r * C + c);
-  }
-  __syncthreads();
-  // element-wise, by rows: dbeta row part, dG, dQK, and the row sums of
-  // dGam * Gam (decay gradient), with dGam = dA beta G + dP QK on r >= i
-  const float* dbg = p.w_db + gi * C;
+  block_sync_lds();
   {
     const int r = q4;
     const float br = sm.b[r], betar = sm.beta[r];
@@ -523,7 +460,7 @@ __global__ __launch_bounds__(NTHREADS) void k_intra_b(Params p) {
         const float gam = __expf(br - sm.b[i]);
         const float dA = sm.u.c.A[r][i];
         const float Gv = sm.u.c.G[r][i];
-        const float dP = sm.u.c.Y[r][i];
+        const float dP = sm.u.c.dT[r][i];
         dbr += dA * gam * Gv;
         dg = dA * betar * gam;
         dqk = dP * gam;
@@ -536,14 +473,13 @@ __global__ __launch_bounds__(NTHREADS) void k_intra_b(Params p) {
     dbr += __shfl_xor(dbr, 2, 64);
     er += __shfl_xor(er, 1, 64);
     er += __shfl_xor(er, 2, 64);
-    __syncthreads();   // dbeta column part written above (other lanes) is complete
+    block_sync_lds();
     if ((tid & 3) == 0) {
       sm.dbeta[r] += dbr;
-      sm.db[r] = dbg[r] + er;
+      sm.db[r] = er;
     }
   }
-  __syncthreads();
-  // element-wise, by columns: subtract the column sums of dGam * Gam
+  block_sync_lds();
   {
     const int i = q4;
     const float bi = sm.b[i];
@@ -552,54 +488,78 @@ __global__ __launch_bounds__(NTHREADS) void k_intra_b(Params p) {
     for (int r = seg; r < seg + 16; ++r) {
       if (r >= i) {
         const float gam = __expf(sm.b[r] - bi);
-        ec += (sm.u.c.A[r][i] * sm.beta[r] * sm.u.c.G[r][i] + sm.u.c.Y[r][i] * sm.u.c.QK[r][i]) * gam;
+        ec += (sm.u.c.A[r][i] * sm.beta[r] * sm.u.c.G[r][i] + sm.u.c.dT[r][i] * sm.u.c.QK[r][i]) * gam;
       }
     }
     ec += __shfl_xor(ec, 1, 64);
     ec += __shfl_xor(ec, 2, 64);
     if ((tid & 3) == 0) sm.db[i] -= ec;
   }
-  __syncthreads();
 
-  // ---- phase 3: dX, dQ, dK over Dk halves
+  // phase B3: dX, dq, dk over the Dk quarters (wave w owns rows 16w..)
   E* dqo = (E*)p.dq;
   E* dko = (E*)p.dk;
-  const float* wq = p.w_dq + gi * C * DK;
-  const float* wk = p.w_dk + gi * C * DK;
-  for (int k0 = 0; k0 < DK; k0 += KH) {
-    __syncthreads();
-    load_half(k0);
-    __syncthreads();
-    make_x();
-    // dgX = T^T dW
-    for (int t = w; t < HT; t += NWAVES) {
-      const int m0 = (t / (KH / 16)) * 16, n0 = (t % (KH / 16)) * 16;
-      const f4 d = mma_k<E, C>(imaj(&sm.Tm[0][0], LC), imaj(&sm.u.h.dW[0][0], LH), m0, n0, zero4(), lane);
 #pragma unroll
-      for (int j = 0; j < 4; ++j) sm.u.h.dX[m0 + frow(lane, j)][n0 + fcol(lane)] = d[j];
+  for (int kq = 0; kq < NQ; ++kq) {
+    const int k0 = kq * KH;
+    block_sync_lds();
+    stage_quarter(kq);
+    if (kq + 1 < NQ) fetchQ((kq + 1) * KH);
+    block_sync_lds();
+    make_x();
+    // dgX = T^T dW (rows 16w..)
+#pragma unroll
+    for (int nb = 0; nb < KH / 16; ++nb) {
+      const f4 d = mma_k<E, C>(imaj(&sm.Tm[0][0], LC), imaj(&sm.u.h.dW[0][0], LH), 16 * w, nb * 16, zero4(), lane);
+#pragma unroll
+      for (int j = 0; j < 4; ++j) sm.u.h.dX[16 * w + frow(lane, j)][nb * 16 + fcol(lane)] = d[j];
     }
-    __syncthreads();
+    block_sync_lds();
     {
+      // db_r += g_r X_r . dgX_r + g_r Q_r . aQ_r ;  tk_r += kb_r K_r . aK_r   (this quarter)
       const int r = q4, c0 = (tid & 3) * (KH / 4);
       float s4 = 0.f;
 #pragma unroll
       for (int c = c0; c < c0 + KH / 4; ++c) s4 += tof(sm.u.h.X[r][c]) * sm.u.h.dX[r][c];
       s4 += __shfl_xor(s4, 1, 64);
       s4 += __shfl_xor(s4, 2, 64);
-      if ((tid & 3) == 0) sm.db[r] += sm.g[r] * s4;
-    }
-    __syncthreads();
-    // dX = g dgX + dG K
-    for (int t = w; t < HT; t += NWAVES) {
-      const int m0 = (t / (KH / 16)) * 16, n0 = (t % (KH / 16)) * 16;
-      const f4 d = mma_k<E, C>(kmaj(&sm.dG[0][0], LC), imaj(&sm.u.h.K[0][0], LH), m0, n0, zero4(), lane);
+      float rq[4] = {0.f, 0.f, 0.f, 0.f}, rk[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int nb = 0; nb < KH / 16; ++nb)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const int rr = 16 * w + frow(lane, j), cc = nb * 16 + fcol(lane);
+          rq[j] += tof(sm.u.h.Q[rr][cc]) * aQ[kq * (KH / 16) + nb][j];
+          rk[j] += tof(sm.u.h.K[rr][cc]) * aK[kq * (KH / 16) + nb][j];
+        }
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
-        const int r = m0 + frow(lane, j), c = n0 + fcol(lane);
+        rq[j] = sum16(rq[j]);
+        rk[j] = sum16(rk[j]);
+      }
+      block_sync_lds();
+      if ((tid & 3) == 0) sm.db[r] += sm.g[r] * s4;
+      block_sync_lds();
+      if (fcol(lane) == 0) {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const int rr = 16 * w + frow(lane, j);
+          sm.db[rr] += sm.g[rr] * rq[j];
+          sm.tk[rr] += sm.kb[rr] * rk[j];
+        }
+      }
+    }
+    // dX = g dgX + dG K
+#pragma unroll
+    for (int nb = 0; nb < KH / 16; ++nb) {
+      const f4 d = mma_k<E, C>(kmaj(&sm.dG[0][0], LC), imaj(&sm.u.h.K[0][0], LH), 16 * w, nb * 16, zero4(), lane);
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int r = 16 * w + frow(lane, j), c = nb * 16 + fcol(lane);
         sm.u.h.dX[r][c] = sm.g[r] * sm.u.h.dX[r][c] + d[j];
       }
     }
-    __syncthreads();
+    block_sync_lds();
     {
       const int r = q4, c0 = (tid & 3) * (KH / 4);
       float s4 = 0.f;
@@ -609,33 +569,40 @@ __global__ __launch_bounds__(NTHREADS) void k_intra_b(Params p) {
       s4 += __shfl_xor(s4, 2, 64);
       if ((tid & 3) == 0) sm.dlam[r] += s4;
     }
-    // dQ = dq_part + dQK K + lambda dX ;  dK = dk_part + dQK^T Q + dG^T X + dX
-    for (int t = w; t < HT; t += NWAVES) {
-      const int m0 = (t / (KH / 16)) * 16, n0 = (t % (KH / 16)) * 16;
-      const f4 a = mma_k<E, C>(kmaj(&sm.dQK[0][0], LC), imaj(&sm.u.h.K[0][0], LH), m0, n0, zero4(), lane);
-      f4 bk = mma_k<E, C>(imaj(&sm.dQK[0][0], LC), imaj(&sm.u.h.Q[0][0], LH), m0, n0, zero4(), lane);
-      bk = mma_k<E, C>(imaj(&sm.dG[0][0], LC), imaj(&sm.u.h.X[0][0], LH), m0, n0, bk, lane);
+    // dq = g aQ + dQK K + lambda dX ;  dk = kb aK + dQK^T Q + dG^T X + dX
+#pragma unroll
+    for (int nb = 0; nb < KH / 16; ++nb) {
+      const f4 a = mma_k<E, C>(kmaj(&sm.dQK[0][0], LC), imaj(&sm.u.h.K[0][0], LH), 16 * w, nb * 16, zero4(), lane);
+      f4 bk = mma_k<E, C>(imaj(&sm.dQK[0][0], LC), imaj(&sm.u.h.Q[0][0], LH), 16 * w, nb * 16, zero4(), lane);
+      bk = mma_k<E, C>(imaj(&sm.dG[0][0], LC), imaj(&sm.u.h.X[0][0], LH), 16 * w, nb * 16, bk, lane);
+      const int kbk = kq * (KH / 16) + nb;
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
-        const int r = m0 + frow(lane, j), c = n0 + fcol(lane);
+        const int r = 16 * w + frow(lane, j), c = nb * 16 + fcol(lane);
         if (r < len) {
           const float dx = sm.u.h.dX[r][c];
-          const size_t o = ((size_t)(t0 + r) * H + h) * DK + k0 + c;
-          dqo[o] = fromf<E>(wq[r * DK + k0 + c] + a[j] + sm.lam[r] * dx);
-          dko[o] = fromf<E>(wk[r * DK + k0 + c] + bk[j] + dx);
+          const size_t o = (arow + (size_t)r * H) * DK + k0 + c;
+          dqo[o] = fromf<E>(sm.g[r] * aQ[kbk][j] + a[j] + sm.lam[r] * dx);
+          dko[o] = fromf<E>(sm.kb[r] * aK[kbk][j] + bk[j] + dx);
         }
       }
     }
   }
-  __syncthreads();
+  block_sync_lds();
   if (tid < C) {
-    // dlog alpha_j = sum_{r >= j} db_r  (chunk-local reverse cumulative sum)
+    // Kbar terms: db_r -= t_r, db_{C-1} += sum_r t_r + g_C <dS', S>;
+    // then dlog alpha_j = sum_{r >= j} db_r (chunk-local reverse cumulative sum)
     const int j = tid;
-    float x = sm.db[C - 1 - j];
-    x = wave_incl_scan(x, lane);     // lane j holds sum_{r >= C-1-j} db_r
+    float tot = sm.tk[j];
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) tot += __shfl_xor(tot, off, 64);
+    float dbj = sm.db[j] - sm.tk[j];
+    if (j == C - 1) dbj += tot + sm.g[C - 1] * (sm.sdot[0] + sm.sdot[1] + sm.sdot[2] + sm.sdot[3]);
+    float x = __shfl(dbj, C - 1 - j, 64);
+    x = wave_incl_scan(x, lane);
     const float suffix = __shfl(x, C - 1 - j, 64);
     if (j < len) {
-      const size_t gt = (size_t)(t0 + j) * H + h;
+      const size_t gt = arow + (size_t)j * H;
       p.dbeta[gt] = sm.dbeta[j];
       p.dlam[gt] = sm.dlam[j];
       if (p.dla) p.dla[gt] = suffix;
@@ -646,9 +613,7 @@ __global__ __launch_bounds__(NTHREADS) void k_intra_b(Params p) {
 // ------------------------------------------------------------------ launchers
 template <typename E, int DK, int DV>
 static hipError_t launch_bwd_t(const Params& p, hipStream_t st) {
-  constexpr int BV = 32;
   constexpr int SBV = 32;   // value columns per backward-scan workgroup
-  constexpr int KH = 32;
   const int units = p.N * p.H;
   const int nb = ((units + 7) / 8) * 8 * (DV / SBV);
   if (nb > 0) {
@@ -658,12 +623,9 @@ static hipError_t launch_bwd_t(const Params& p, hipStream_t st) {
   }
   if (p.n_slots > 0) {
     dim3 gp(p.n_slots, p.H);
-    prof_mark(ST_INTRA_A, 0, st);
-    hipLaunchKernelGGL((k_intra_a<E, DK, DV, BV>), gp, dim3(NTHREADS), 0, st, p);
-    prof_mark(ST_INTRA_A, 1, st);
-    prof_mark(ST_INTRA_B, 0, st);
-    hipLaunchKernelGGL((k_intra_b<E, DK, KH>), gp, dim3(NTHREADS), 0, st, p);
-    prof_mark(ST_INTRA_B, 1, st);
+    prof_mark(ST_INTRA, 0, st);
+    hipLaunchKernelGGL((k_bwd_intra<E, DK, DV>), gp, dim3(NTHREADS), 0, st, p);
+    prof_mark(ST_INTRA, 1, st);
   }
   return hipGetLastError();
 }

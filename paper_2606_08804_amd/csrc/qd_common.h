@@ -162,61 +162,6 @@ __device__ inline void load_rows_t(E* dst, int ld, const E* src, size_t gs, int 
 
 struct One { __device__ float operator()(int) const { return 1.f; } };
 
-// Register staging of an R x COLS tile (row stride `rs` elements in global,
-// rows >= valid read as zero) for software prefetch: load() issues the global
-// reads, store() writes the tile to LDS with 16-byte stores.
-template <typename E, int R, int COLS>
-struct TileRegs {
-  static constexpr int VEC = 16 / sizeof(E);
-  static constexpr int PR = COLS / VEC;
-  static constexpr int TOTAL = R * PR;
-  static constexpr int N = (TOTAL + NTHREADS - 1) / NTHREADS;
-  static_assert(TOTAL % NTHREADS == 0 || TOTAL < NTHREADS, "tile must split evenly over the workgroup");
-  uint4 v[N];
-  __device__ static inline bool owns(int i, int tid) { return TOTAL >= NTHREADS || tid + i * NTHREADS < TOTAL; }
-  __device__ inline void load(const E* src, size_t rs, int valid, int tid) {
-#pragma unroll
-    for (int i = 0; i < N; ++i) {
-      const int idx = tid + i * NTHREADS, r = idx / PR, c = (idx % PR) * VEC;
-      v[i] = (owns(i, tid) && r < valid) ? *(const uint4*)(src + (size_t)r * rs + c) : make_uint4(0, 0, 0, 0);
-    }
-  }
-  __device__ inline void store(E* dst, int ld, int tid) const {
-#pragma unroll
-    for (int i = 0; i < N; ++i) {
-      const int idx = tid + i * NTHREADS, r = idx / PR, c = (idx % PR) * VEC;
-      if (owns(i, tid)) *(uint4*)(dst + (size_t)r * ld + c) = v[i];
-    }
-  }
-};
-
-template <typename F> __device__ inline F zero_frag();
-template <> __device__ inline bf8 zero_frag<bf8>() { return __builtin_bit_cast(bf8, make_uint4(0, 0, 0, 0)); }
-template <> __device__ inline float zero_frag<float>() { return 0.f; }
-
-// MFMA A-operand fragments of one 16-row block, loaded straight from global
-// memory into registers (row-major source, k contiguous, row stride `ld`).
-// Rows at or beyond `valid` (relative to the block's first row) read as zero.
-template <typename E, int K>
-struct AFrag {
-  typedef typename Mma<E>::frag frag;
-  static constexpr int NK = K / Mma<E>::KS;
-  frag f[NK];
-  __device__ inline void load(const E* row0, size_t ld, int valid, int lane) {
-    const int r = lane & 15;
-    const E* src = row0 + (size_t)r * ld + (lane >> 4) * Mma<E>::KPL;
-#pragma unroll
-    for (int ks = 0; ks < NK; ++ks)
-      f[ks] = r < valid ? *(const frag*)(src + ks * Mma<E>::KS) : zero_frag<frag>();
-  }
-};
-
-// Workgroup barrier that orders LDS traffic only: outstanding global loads
-// (software prefetch) stay in flight across it.
-__device__ inline void block_sync_lds() {
-  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
-}
-
 // Four consecutive activation-dtype values of one lane's C fragment.
 template <typename E> struct Quad;
 template <> struct Quad<__bf16> {
@@ -245,6 +190,119 @@ template <> struct Quad<float> {
   }
 };
 
+// Register staging of an R x COLS tile (row stride `rs` elements in global,
+// rows >= valid read as zero) for software prefetch: load() issues the global
+// reads, store() writes the tile to LDS with 16-byte stores.
+template <typename E, int R, int COLS>
+struct TileRegs {
+  static constexpr int VEC = 16 / sizeof(E);
+  static constexpr int PR = COLS / VEC;
+  static constexpr int TOTAL = R * PR;
+  static constexpr int N = (TOTAL + NTHREADS - 1) / NTHREADS;
+  static_assert(TOTAL % NTHREADS == 0 || TOTAL < NTHREADS, "tile must split evenly over the workgroup");
+  uint4 v[N];
+  __device__ static inline bool owns(int i, int tid) { return TOTAL >= NTHREADS || tid + i * NTHREADS < TOTAL; }
+  __device__ inline void load(const E* src, size_t rs, int valid, int tid) {
+#pragma unroll
+    for (int i = 0; i < N; ++i) {
+      const int idx = tid + i * NTHREADS, r = idx / PR, c = (idx % PR) * VEC;
+      v[i] = (owns(i, tid) && r < valid) ? *(const uint4*)(src + (size_t)r * rs + c) : make_uint4(0, 0, 0, 0);
+    }
+  }
+  __device__ inline void store(E* dst, int ld, int tid) const {
+#pragma unroll
+    for (int i = 0; i < N; ++i) {
+      const int idx = tid + i * NTHREADS, r = idx / PR, c = (idx % PR) * VEC;
+      if (owns(i, tid)) *(uint4*)(dst + (size_t)r * ld + c) = v[i];
+    }
+  }
+};
+
+// As TileRegs, but consecutive threads take consecutive rows, so that the
+// transposed LDS store storeT() (dst[c*ld + r]) is free of bank conflicts.
+template <typename E, int R, int COLS>
+struct TileRegsT {
+  static constexpr int VEC = 16 / sizeof(E);
+  static constexpr int PR = COLS / VEC;
+  static constexpr int N = R * PR / NTHREADS;
+  static_assert(N >= 1 && N * NTHREADS == R * PR && NTHREADS % R == 0, "tile split");
+  uint4 v[N];
+  __device__ inline void load(const E* src, size_t rs, int valid, int tid) {
+#pragma unroll
+    for (int i = 0; i < N; ++i) {
+      const int idx = tid + i * NTHREADS, r = idx % R, c = (idx / R) * VEC;
+      v[i] = r < valid ? *(const uint4*)(src + (size_t)r * rs + c) : make_uint4(0, 0, 0, 0);
+    }
+  }
+  __device__ inline void storeT(E* dst, int ld, int tid) const {
+#pragma unroll
+    for (int i = 0; i < N; ++i) {
+      const int idx = tid + i * NTHREADS, r = idx % R, c = (idx / R) * VEC;
+      const E* e = (const E*)&v[i];
+#pragma unroll
+      for (int j = 0; j < VEC; ++j) dst[(size_t)(c + j) * ld + r] = e[j];
+    }
+  }
+};
+
+// fp32 tile staged in registers and written to LDS converted to E.
+template <typename E, int R, int COLS>
+struct TileRegsF {
+  static constexpr int PR = COLS / 4;
+  static constexpr int TOTAL = R * PR;
+  static constexpr int N = TOTAL / NTHREADS;
+  static_assert(N >= 1 && N * NTHREADS == TOTAL, "tile split");
+  f4 v[N];
+  __device__ inline void load(const float* src, size_t rs, int tid) {
+#pragma unroll
+    for (int i = 0; i < N; ++i) {
+      const int idx = tid + i * NTHREADS, r = idx / PR, c = (idx % PR) * 4;
+      v[i] = *(const f4*)(src + (size_t)r * rs + c);
+    }
+  }
+  __device__ inline void store(E* dst, int ld, int tid) const {
+#pragma unroll
+    for (int i = 0; i < N; ++i) {
+      const int idx = tid + i * NTHREADS, r = idx / PR, c = (idx % PR) * 4;
+      *(typename Quad<E>::raw*)(dst + (size_t)r * ld + c) = Quad<E>::pack(v[i]);
+    }
+  }
+};
+
+struct NoRegs {};
+
+// Number of compute units of the current device (host side, cached).
+int device_cu_count();
+
+template <typename F> __device__ inline F zero_frag();
+template <> __device__ inline bf8 zero_frag<bf8>() { return __builtin_bit_cast(bf8, make_uint4(0, 0, 0, 0)); }
+template <> __device__ inline float zero_frag<float>() { return 0.f; }
+
+// MFMA A-operand fragments of one 16-row block, loaded straight from global
+// memory into registers (row-major source, k contiguous, row stride `ld`).
+// Rows at or beyond `valid` (relative to the block's first row) read as zero.
+template <typename E, int K>
+struct AFrag {
+  typedef typename Mma<E>::frag frag;
+  static constexpr int NK = K / Mma<E>::KS;
+  frag f[NK];
+  __device__ inline void load(const E* row0, size_t ld, int valid, int lane) {
+    const int r = lane & 15;
+    const E* src = row0 + (size_t)r * ld + (lane >> 4) * Mma<E>::KPL;
+#pragma unroll
+    for (int ks = 0; ks < NK; ++ks)
+      f[ks] = r < valid ? *(const frag*)(src + ks * Mma<E>::KS) : zero_frag<frag>();
+  }
+};
+
+// Workgroup barrier that orders LDS traffic only: outstanding global loads
+// (software prefetch) stay in flight across it.
+__device__ inline void block_sync_lds() {
+  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
+
+
+
 // ----------------------------------------------------------------- parameters
 struct Params {
   // sizes
@@ -265,14 +323,15 @@ struct Params {
   // forward outputs
   void* o;
   float* Sfin;
-  float* saved;          // per-slot entry states [slot][H][Dv][Dk]
+  float* saved;          // saved context: entry states S^T [slot][H][Dk][Dv] (fp32)
+  void* savedD;          // saved context: D [slot][H][C][Dv] (dtype)
   // workspace (per slot and head)
   float* wb;             // [slot][H][C] chunk-local prefix sums of log alpha
   void* wU;              // [slot][H] C x Dv, C-fragment tiled
   void* wW;              // [slot][H][C][Dk]
   void* wP;              // [slot][H][C][C]   P = Gam * M * Q K^T
   void* wKt;             // [slot][H][Dk][C]  K^T
-  void* wT;              // [slot][H][2][C][C] T and P^T (backward only)
+  void* wT;              // [slot][H][2][C][C] T^T and P^T (backward only)
   void* wWt;             // [slot][H][Dk][C]  W^T (backward only)
   void* wQgt;            // [slot][H][Dk][C]  (diag(g) Q)^T (backward only)
   void* wdOt;            // [slot][H][Dv][C]  dO^T (backward only)
@@ -286,14 +345,8 @@ struct Params {
   float* dlam;
   float* dla;
   float* dS0;
-  float* w_dSo;          // [slot][H][Dv][Dk] gradient w.r.t. each chunk's exit state
-  float* w_dD;           // [slot][H][C][Dv]
-  float* w_dW;           // [slot][H][C][Dk]
-  float* w_dq;           // [slot][H][C][Dk]
-  float* w_dk;           // [slot][H][C][Dk]
-  float* w_dP;           // [slot][H][C][C]
-  float* w_dT;           // [slot][H][C][C]
-  float* w_db;           // [slot][H][C]
+  float* w_dSo;          // [slot][H][Dk][Dv] gradient w.r.t. each chunk's exit state, transposed
+  void* w_dDb;           // [slot][H][C][Dv] dD (dtype)
 };
 
 // Token range of sequence n; false when cu_seqlens is malformed for n.

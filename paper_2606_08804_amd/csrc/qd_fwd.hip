@@ -21,6 +21,8 @@
 #include "qd_common.h"
 #include "qd_launch.h"
 
+#include <type_traits>
+
 namespace qd {
 
 template <typename E, int DK, int DV>
@@ -59,108 +61,146 @@ __device__ inline void store_transposed(E* dst, const E* src, int ld, int tid, S
   }
 }
 
+// Raw inputs of one (chunk, head) unit, staged in registers one unit ahead.
+template <typename E, int DK, int DV, bool BWD>
+struct PrepPre {
+  TileRegs<E, C, DK> K, Q;
+  TileRegsT<E, C, DV> V;
+  typename std::conditional<BWD, TileRegs<E, C, DV>, NoRegs>::type dO;
+  float la, beta, lam;
+  int t0, len, g, h;
+  bool valid;
+};
+
 // Forward mode writes b, U, W, P and K^T.  Backward mode (BWD) writes b, U,
-// W and K^T plus T, P^T, W^T and (diag(g) Q)^T for the backward kernels.
+// W and K^T plus T, P^T, W^T, (diag(g) Q)^T and dO^T for the backward kernels.
+// Persistent: each workgroup walks units blockIdx.x, +gridDim.x, ... and
+// prefetches the next unit's inputs into registers while computing the
+// current one.
 template <typename E, int DK, int DV, bool BWD>
 __global__ __launch_bounds__(NTHREADS) void k_prep(Params p) {
   constexpr int P = Pad<E>::v;
   constexpr int LK = DK + P, LC = C + P;
+  typedef PrepPre<E, DK, DV, BWD> Pre;
   __shared__ PrepSmem<E, DK, DV> sm;
-  const int g = blockIdx.x, h = blockIdx.y, tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-  int n, t0, len;
-  if (!locate(p, g, n, t0, len)) return;
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int H = p.H;
-  const size_t gi = (size_t)g * H + h;
+  const int total = p.n_slots * H;
 
-  if (tid < C) {
-    const bool ok = tid < len;
-    const size_t gt = (size_t)(t0 + tid) * H + h;
-    const float la = (ok && p.la) ? p.la[gt] : 0.f;
-    const float b = wave_incl_scan(la, lane);
-    sm.b[tid] = b;
-    sm.beta[tid] = ok ? p.beta[gt] : 0.f;
-    sm.lam[tid] = ok ? p.lam[gt] : 0.f;
-    p.wb[gi * C + tid] = b;
-  }
-  const E* qg = (const E*)p.q + ((size_t)t0 * H + h) * DK;
-  const E* kg = (const E*)p.k + ((size_t)t0 * H + h) * DK;
-  const E* vg = (const E*)p.v + ((size_t)t0 * H + h) * DV;
-  load_rows<E, DK>(&sm.u.a.K[0][0], LK, kg, (size_t)H * DK, len, tid);
-  load_rows<E, DK>(&sm.u.a.Q[0][0], LK, qg, (size_t)H * DK, len, tid);
-  __syncthreads();
-
-  // transposed copies for the scans: K^T, and (diag(g) Q)^T for the backward
-  store_transposed<E, DK>((E*)p.wKt + gi * DK * C, &sm.u.a.K[0][0], LK, tid, One());
-  if (BWD)
-    store_transposed<E, DK>((E*)p.wQgt + gi * DK * C, &sm.u.a.Q[0][0], LK, tid,
-                            [&](int r) { return __expf(sm.b[r]); });
-  // mixed inputs X = K + lambda Q and the transposed decayed copy (g X)^T
-  for (int idx = tid; idx < C * DK; idx += NTHREADS) {
-    const int r = idx % C, c = idx / C;
-    const float x = tof(sm.u.a.K[r][c]) + sm.lam[r] * tof(sm.u.a.Q[r][c]);
-    sm.u.a.X[r][c] = fromf<E>(x);
-    sm.GXt[c][r] = fromf<E>(__expf(sm.b[r]) * x);
-  }
-  __syncthreads();
-
-  // Gram products X K^T and Q K^T; A (fp32, LDS) and P (workspace)
-  E* wP = BWD ? (E*)p.wT + gi * 2 * C * C + C * C : (E*)p.wP + gi * C * C;
-  for (int t = w; t < 16; t += NWAVES) {
-    const int m0 = (t >> 2) * 16, n0 = (t & 3) * 16;
-    const f4 gx = mma_k<E, DK>(kmaj(&sm.u.a.X[0][0], LK), kmaj(&sm.u.a.K[0][0], LK), m0, n0, zero4(), lane);
-    const f4 qk = mma_k<E, DK>(kmaj(&sm.u.a.Q[0][0], LK), kmaj(&sm.u.a.K[0][0], LK), m0, n0, zero4(), lane);
-    f4 pv;
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int r = m0 + frow(lane, j), i = n0 + fcol(lane);
-      const float gam = (r >= i) ? __expf(sm.b[r] - sm.b[i]) : 0.f;
-      sm.A[r][i] = (r > i) ? sm.beta[r] * gam * gx[j] : 0.f;
-      pv[j] = gam * qk[j];
-      if (!BWD) wP[r * C + i] = fromf<E>(pv[j]);
+  auto fetch = [&](int u, Pre& x) {
+    x.valid = false;
+    if (u >= total) return;
+    x.g = u / H;
+    x.h = u % H;
+    int n;
+    if (!locate(p, x.g, n, x.t0, x.len)) return;
+    x.valid = true;
+    const size_t row = (size_t)x.t0 * H + x.h;
+    x.K.load((const E*)p.k + row * DK, (size_t)H * DK, x.len, tid);
+    x.Q.load((const E*)p.q + row * DK, (size_t)H * DK, x.len, tid);
+    x.V.load((const E*)p.v + row * DV, (size_t)H * DV, x.len, tid);
+    if constexpr (BWD) x.dO.load((const E*)p.dO + row * DV, (size_t)H * DV, x.len, tid);
+    if (tid < C) {
+      const bool ok = tid < x.len;
+      const size_t gt = row + (size_t)tid * H;
+      x.la = (ok && p.la) ? p.la[gt] : 0.f;
+      x.beta = ok ? p.beta[gt] : 0.f;
+      x.lam = ok ? p.lam[gt] : 0.f;
     }
-    // backward: P^T, four consecutive entries of one row of P^T per lane
+  };
+
+  Pre pre;
+  fetch(blockIdx.x, pre);
+  for (int u = blockIdx.x; u < total; u += gridDim.x) {
+    const Pre x = pre;
+    fetch(u + gridDim.x, pre);
+    if (!x.valid) continue;                 // uniform across the workgroup
+    const int h = x.h;
+    const size_t gi = (size_t)x.g * H + h;
+    __syncthreads();                        // previous unit's LDS use is over
+    x.K.store(&sm.u.a.K[0][0], LK, tid);
+    x.Q.store(&sm.u.a.Q[0][0], LK, tid);
+    if (tid < C) {
+      const float b = wave_incl_scan(x.la, lane);
+      sm.b[tid] = b;
+      sm.beta[tid] = x.beta;
+      sm.lam[tid] = x.lam;
+      p.wb[gi * C + tid] = b;
+    }
+    __syncthreads();
+
+    // transposed copies for the scans: K^T, and (diag(g) Q)^T for the backward
+    store_transposed<E, DK>((E*)p.wKt + gi * DK * C, &sm.u.a.K[0][0], LK, tid, One());
     if (BWD)
-      *(typename Quad<E>::raw*)(wP + (n0 + fcol(lane)) * C + m0 + frow(lane, 0)) = Quad<E>::pack(pv);
-  }
-  __syncthreads();
+      store_transposed<E, DK>((E*)p.wQgt + gi * DK * C, &sm.u.a.Q[0][0], LK, tid,
+                              [&](int r) { return __expf(sm.b[r]); });
+    // mixed inputs X = K + lambda Q and the transposed decayed copy (g X)^T
+    for (int idx = tid; idx < C * DK; idx += NTHREADS) {
+      const int r = idx % C, c = idx / C;
+      const float xv = tof(sm.u.a.K[r][c]) + sm.lam[r] * tof(sm.u.a.Q[r][c]);
+      sm.u.a.X[r][c] = fromf<E>(xv);
+      sm.GXt[c][r] = fromf<E>(__expf(sm.b[r]) * xv);
+    }
+    __syncthreads();
 
-  // UT solve: M = (I + A)^{-1}, T = M diag(beta)
-  unit_lower_inverse(&sm.A[0][0], C + 4, &sm.M[0][0], C + 4, sm.tmp, tid);
-  E* wT = BWD ? (E*)p.wT + gi * 2 * C * C : nullptr;
-  for (int idx = tid; idx < C * C; idx += NTHREADS) {
-    const int r = idx / C, i = idx % C;
-    const E tv = fromf<E>(sm.M[r][i] * sm.beta[i]);
-    sm.Tm[r][i] = tv;
-    if (BWD) wT[idx] = tv;
-  }
-  // V^T (K, Q, X are dead: all reads of them finished before the solve's barriers)
-  load_rows_t<E, DV>(&sm.u.Vt[0][0], LC, vg, (size_t)H * DV, len, tid, One());
-  __syncthreads();
-
-  // U = T V, stored C-fragment tiled: tile (mt, nt) at ((mt*(DV/16)+nt)*64 + lane)*4
-  E* wU = (E*)p.wU + gi * C * DV;
-  for (int t = w; t < (C / 16) * (DV / 16); t += NWAVES) {
-    const int m0 = (t / (DV / 16)) * 16, n0 = (t % (DV / 16)) * 16;
-    const f4 u = mma_k<E, C>(kmaj(&sm.Tm[0][0], LC), kmaj(&sm.u.Vt[0][0], LC), m0, n0, zero4(), lane);
-    *(typename Quad<E>::raw*)(wU + ((size_t)t * 64 + lane) * 4) = Quad<E>::pack(u);
-  }
-  // W = T diag(g) X, row-major C x DK (and W^T in backward mode)
-  E* wW = (E*)p.wW + gi * C * DK;
-  E* wWt = BWD ? (E*)p.wWt + gi * DK * C : nullptr;
-  for (int t = w; t < (C / 16) * (DK / 16); t += NWAVES) {
-    const int m0 = (t / (DK / 16)) * 16, n0 = (t % (DK / 16)) * 16;
-    const f4 wv = mma_k<E, C>(kmaj(&sm.Tm[0][0], LC), kmaj(&sm.GXt[0][0], LC), m0, n0, zero4(), lane);
+    // Gram products X K^T and Q K^T; A (fp32, LDS) and P or P^T (workspace)
+    E* wP = BWD ? (E*)p.wT + gi * 2 * C * C + C * C : (E*)p.wP + gi * C * C;
+    for (int t = w; t < 16; t += NWAVES) {
+      const int m0 = (t >> 2) * 16, n0 = (t & 3) * 16;
+      const f4 gx = mma_k<E, DK>(kmaj(&sm.u.a.X[0][0], LK), kmaj(&sm.u.a.K[0][0], LK), m0, n0, zero4(), lane);
+      const f4 qk = mma_k<E, DK>(kmaj(&sm.u.a.Q[0][0], LK), kmaj(&sm.u.a.K[0][0], LK), m0, n0, zero4(), lane);
+      f4 pv;
 #pragma unroll
-    for (int j = 0; j < 4; ++j) wW[(m0 + frow(lane, j)) * DK + n0 + fcol(lane)] = fromf<E>(wv[j]);
-    if (BWD)
-      *(typename Quad<E>::raw*)(wWt + (size_t)(n0 + fcol(lane)) * C + m0 + frow(lane, 0)) = Quad<E>::pack(wv);
-  }
-  if (BWD) {
-    // dO^T for the backward scan's fragment loads
+      for (int j = 0; j < 4; ++j) {
+        const int r = m0 + frow(lane, j), i = n0 + fcol(lane);
+        const float gam = (r >= i) ? __expf(sm.b[r] - sm.b[i]) : 0.f;
+        sm.A[r][i] = (r > i) ? sm.beta[r] * gam * gx[j] : 0.f;
+        pv[j] = gam * qk[j];
+        if (!BWD) wP[r * C + i] = fromf<E>(pv[j]);
+      }
+      if (BWD)
+        *(typename Quad<E>::raw*)(wP + (n0 + fcol(lane)) * C + m0 + frow(lane, 0)) = Quad<E>::pack(pv);
+    }
     __syncthreads();
-    load_rows<E, DV>(&sm.u.dO[0][0], DV + P, (const E*)p.dO + ((size_t)t0 * H + h) * DV, (size_t)H * DV, len, tid);
+
+    // UT solve: M = (I + A)^{-1}, T = M diag(beta)
+    unit_lower_inverse(&sm.A[0][0], C + 4, &sm.M[0][0], C + 4, sm.tmp, tid);
+    E* wTt = BWD ? (E*)p.wT + gi * 2 * C * C : nullptr;
+    for (int idx = tid; idx < C * C; idx += NTHREADS) {
+      const int r = idx / C, i = idx % C;
+      const E tv = fromf<E>(sm.M[r][i] * sm.beta[i]);
+      sm.Tm[r][i] = tv;
+      if (BWD) wTt[i * C + r] = tv;     // T^T for the backward scan's dV = T^T dD
+    }
+    // V^T (K, Q, X are dead: all reads of them finished before the solve's barriers)
+    x.V.storeT(&sm.u.Vt[0][0], LC, tid);
     __syncthreads();
-    store_transposed<E, DV>((E*)p.wdOt + gi * DV * C, &sm.u.dO[0][0], DV + P, tid, One());
+
+    // U = T V, stored C-fragment tiled: tile (mt, nt) at ((mt*(DV/16)+nt)*64 + lane)*4
+    E* wU = (E*)p.wU + gi * C * DV;
+    for (int t = w; t < (C / 16) * (DV / 16); t += NWAVES) {
+      const int m0 = (t / (DV / 16)) * 16, n0 = (t % (DV / 16)) * 16;
+      const f4 uu = mma_k<E, C>(kmaj(&sm.Tm[0][0], LC), kmaj(&sm.u.Vt[0][0], LC), m0, n0, zero4(), lane);
+      *(typename Quad<E>::raw*)(wU + ((size_t)t * 64 + lane) * 4) = Quad<E>::pack(uu);
+    }
+    // W = T diag(g) X, row-major C x DK (and W^T in backward mode)
+    E* wW = (E*)p.wW + gi * C * DK;
+    E* wWt = BWD ? (E*)p.wWt + gi * DK * C : nullptr;
+    for (int t = w; t < (C / 16) * (DK / 16); t += NWAVES) {
+      const int m0 = (t / (DK / 16)) * 16, n0 = (t % (DK / 16)) * 16;
+      const f4 wv = mma_k<E, C>(kmaj(&sm.Tm[0][0], LC), kmaj(&sm.GXt[0][0], LC), m0, n0, zero4(), lane);
+#pragma unroll
+      for (int j = 0; j < 4; ++j) wW[(m0 + frow(lane, j)) * DK + n0 + fcol(lane)] = fromf<E>(wv[j]);
+      if (BWD)
+        *(typename Quad<E>::raw*)(wWt + (size_t)(n0 + fcol(lane)) * C + m0 + frow(lane, 0)) = Quad<E>::pack(wv);
+    }
+    if constexpr (BWD) {
+      // dO^T for the backward scan's fragment loads
+      __syncthreads();
+      x.dO.store(&sm.u.dO[0][0], DV + P, tid);
+      __syncthreads();
+      store_transposed<E, DV>((E*)p.wdOt + gi * DV * C, &sm.u.dO[0][0], DV + P, tid, One());
+    }
   }
 }
 
@@ -172,6 +212,7 @@ struct ScanFwdSmem {
   E Dt[BV][C + P];    // D^T
   E Dkt[BV][C + P];   // (diag(g_C / g) D)^T
   E O[C][BV + P];     // output tile staging
+  E Dr[C][BV + P];    // D tile staging for the saved context
 };
 
 // Operands of one chunk for one wave of the forward scan, prefetched from
@@ -258,8 +299,12 @@ __global__ __launch_bounds__(NTHREADS) void k_scan_fwd(Params p) {
       for (int nb = 0; nb < NB; ++nb) {
         const int kt = KPW * w + i;
         *(QR*)&sm.S[nb * 16 + fcol(lane)][kt * 16 + frow(lane, 0)] = Quad<E>::pack(acc[i][nb]);
-        if (p.saved)
-          *(f4*)(p.saved + (gi * DV + v0 + nb * 16 + fcol(lane)) * DK + kt * 16 + frow(lane, 0)) = acc[i][nb];
+        if (p.saved) {
+          // saved entry state, transposed: element (k, v) at [k][v]
+          float* dst = p.saved + (gi * DK + kt * 16 + frow(lane, 0)) * DV + v0 + nb * 16 + fcol(lane);
+#pragma unroll
+          for (int j = 0; j < 4; ++j) dst[(size_t)j * DV] = acc[i][nb][j];
+        }
       }
     block_sync_lds();
     if (c + 1 < nch) prefetch(c + 1);
@@ -285,8 +330,21 @@ __global__ __launch_bounds__(NTHREADS) void k_scan_fwd(Params p) {
       }
       *(QR*)&sm.Dt[nb * 16 + fcol(lane)][16 * w + frow(lane, 0)] = Quad<E>::pack(d);
       *(QR*)&sm.Dkt[nb * 16 + fcol(lane)][16 * w + frow(lane, 0)] = Quad<E>::pack(dk);
+      if (p.saved) {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) sm.Dr[16 * w + frow(lane, j)][nb * 16 + fcol(lane)] = fromf<E>(d[j]);
+      }
     }
     block_sync_lds();
+    if (p.saved) {
+      // D rows of this tile into the saved context (rows past the chunk are zero)
+      constexpr int VEC = 16 / sizeof(E), PR = BV / VEC;
+      E* dbase = (E*)p.savedD + gi * C * DV + v0;
+      for (int idx = tid; idx < C * PR; idx += NTHREADS) {
+        const int r = idx / PR, cc = (idx % PR) * VEC;
+        *(uint4*)(dbase + (size_t)r * DV + cc) = *(const uint4*)&sm.Dr[r][cc];
+      }
+    }
     if (with_o) {
       // O = diag(g) Q S^T + P D   (rows 16w..)
 #pragma unroll
@@ -344,7 +402,8 @@ template <typename E, int DK, int DV>
 static hipError_t launch_fwd_t(const Params& p, int bwd_prep, int with_scan, hipStream_t st) {
   constexpr int BV = 32;   // value columns per forward-scan workgroup
   if (p.n_slots > 0) {
-    dim3 gp(p.n_slots, p.H);
+    const int units = p.n_slots * p.H;
+    dim3 gp(min(units, device_cu_count()));
     const int stage = bwd_prep ? ST_PREP_BWD : ST_PREP_FWD;
     prof_mark(stage, 0, st);
     if (bwd_prep)

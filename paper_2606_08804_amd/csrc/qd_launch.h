@@ -12,10 +12,9 @@ enum Stage {
   ST_SCAN_FWD = 1,
   ST_PREP_BWD = 2,
   ST_SCAN_BWD = 3,
-  ST_INTRA_A = 4,
-  ST_INTRA_B = 5,
-  ST_STEP = 6,
-  ST_COUNT = 7
+  ST_INTRA = 4,
+  ST_STEP = 5,
+  ST_COUNT = 6
 };
 
 // Records a HIP event on `st` before (after == 0) or after (after == 1) a

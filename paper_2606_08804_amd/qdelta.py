@@ -7,7 +7,8 @@ if ``libqdelta.so`` is missing or fails to load, every entry point raises.
 Functions mirror the C ABI in ``include/qdelta.h``:
 
 chunk_fwd(q, k, v, beta, lam, log_alpha=None, initial_state=None, cu_seqlens=None,
-          output_final_state=True, save_states=False) -> (o, final_state, saved_states)
+          output_final_state=True, save_states=False) -> (o, final_state, saved)
+          (saved: uint8 device buffer holding the saved context for the backward)
 chunk_bwd(q, k, v, beta, lam, log_alpha, initial_state, saved_states, d_o,
           d_final_state=None, cu_seqlens=None) -> dict of gradients
 recurrent_step(q, k, v, beta, lam, log_alpha, state) -> o        (state updated in place)
@@ -25,13 +26,13 @@ QDELTA_OK, QDELTA_EINVAL, QDELTA_EUNSUPPORTED, QDELTA_ENOWORKSPACE, QDELTA_EHIP 
 QDELTA_F32, QDELTA_BF16 = 0, 1
 
 EXPORTS = (
-    "qdelta_status_string", "qdelta_version", "qdelta_saved_state_slots",
+    "qdelta_status_string", "qdelta_version", "qdelta_saved_state_slots", "qdelta_saved_bytes",
     "qdelta_chunk_workspace_bytes", "qdelta_chunk_fwd", "qdelta_chunk_fwd_varlen",
     "qdelta_chunk_bwd", "qdelta_chunk_bwd_varlen", "qdelta_recurrent_step",
     "qdelta_profile_begin", "qdelta_profile_end",
 )
 
-STAGES = ("prep_fwd", "scan_fwd", "prep_bwd", "scan_bwd", "intra_a", "intra_b", "step")
+STAGES = ("prep_fwd", "scan_fwd", "prep_bwd", "scan_bwd", "intra", "step")
 
 _lib = None
 
@@ -57,6 +58,8 @@ def lib():
         L.qdelta_version.restype = ctypes.c_int
         L.qdelta_saved_state_slots.argtypes = [i32, i32, i32, i32]
         L.qdelta_saved_state_slots.restype = sz
+        L.qdelta_saved_bytes.argtypes = [i32] * 8
+        L.qdelta_saved_bytes.restype = sz
         L.qdelta_chunk_workspace_bytes.argtypes = [i32] * 9
         L.qdelta_chunk_workspace_bytes.restype = sz
         L.qdelta_chunk_fwd.argtypes = [i32] * 7 + [P] * 10 + [P, sz, P]
@@ -136,6 +139,11 @@ def saved_state_slots(B, T, n_seqs=0):
     return int(lib().qdelta_saved_state_slots(B, T, CHUNK, n_seqs))
 
 
+def saved_bytes(B, T, H, Dk, Dv, dtype, n_seqs=0):
+    """Bytes of the saved context (per-chunk states and new values) for the backward."""
+    return int(lib().qdelta_saved_bytes(B, T, H, Dk, Dv, CHUNK, dtype, n_seqs))
+
+
 def workspace_bytes(B, T, H, Dk, Dv, dtype, n_seqs=0, is_bwd=False):
     return int(lib().qdelta_chunk_workspace_bytes(B, T, H, Dk, Dv, CHUNK, dtype, n_seqs, int(is_bwd)))
 
@@ -172,7 +180,7 @@ def chunk_fwd(q, k, v, beta, lam, log_alpha=None, initial_state=None, cu_seqlens
     n_seqs = N if cu_seqlens is not None else 0
     saved = None
     if save_states:
-        saved = torch.empty((saved_state_slots(B, T, n_seqs), H, Dv, Dk), dtype=torch.float32, device=dev)
+        saved = torch.empty(saved_bytes(B, T, H, Dk, Dv, dt, n_seqs), dtype=torch.uint8, device=dev)
     nbytes = workspace_bytes(B, T, H, Dk, Dv, dt, n_seqs, False)
     ws = _workspace(nbytes, dev, workspace)
     common = (H, Dk, Dv, CHUNK, dt, _p(q), _p(k), _p(v), _p(beta), _p(lam), _p(log_alpha),
@@ -199,16 +207,16 @@ def chunk_bwd(q, k, v, beta, lam, log_alpha, initial_state, saved_states, d_o,
     _need(lam, "lam", torch.float32, act)
     _opt(log_alpha, "log_alpha", torch.float32, act)
     _opt(initial_state, "initial_state", torch.float32, (N, H, Dv, Dk))
-    _opt(saved_states, "saved_states", torch.float32)
+    _opt(saved_states, "saved_states")
     _need(d_o, "d_o", q.dtype, tuple(act) + (Dv,))
     _opt(d_final_state, "d_final_state", torch.float32, (N, H, Dv, Dk))
     if cu_seqlens is not None:
         _need(cu_seqlens, "cu_seqlens", torch.int32)
     n_seqs = N if cu_seqlens is not None else 0
     if saved_states is not None:
-        exp = (saved_state_slots(B, T, n_seqs), H, Dv, Dk)
-        if tuple(saved_states.shape) != exp:
-            raise ValueError(f"saved_states has shape {tuple(saved_states.shape)}, expected {exp}")
+        nb = saved_bytes(B, T, H, Dk, Dv, dt, n_seqs)
+        if saved_states.dtype != torch.uint8 or saved_states.numel() < nb:
+            raise ValueError(f"saved_states must be a uint8 buffer of at least {nb} bytes")
     dev = q.device
     dq = torch.empty_like(q)
     dk = torch.empty_like(k)

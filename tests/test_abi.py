@@ -22,7 +22,7 @@ def header_functions():
 def test_library_exports_every_declared_symbol():
     L = qdelta.lib()
     names = header_functions()
-    assert len(names) == 11
+    assert len(names) == 12
     for n in names:
         assert hasattr(L, n), n
     assert sorted(names) == sorted(qdelta.EXPORTS)
@@ -42,6 +42,13 @@ def test_saved_state_slots():
     assert qdelta.saved_state_slots(1, 0) == 0
     assert qdelta.saved_state_slots(1, 32768, 20) == 512 + 20
     assert qdelta.lib().qdelta_saved_state_slots(1, 64, 32, 0) == 0   # chunk 32 unsupported
+
+
+def test_saved_context_bytes():
+    # per (slot, head): fp32 Dk x Dv state + C x Dv new values in the activation dtype
+    assert qdelta.saved_bytes(4, 4096, 16, 128, 128, 1) == 256 * 16 * (128 * 128 * 4 + 64 * 128 * 2)
+    assert qdelta.saved_bytes(1, 100, 2, 64, 64, 0) == 2 * 2 * (64 * 64 * 4 + 64 * 64 * 4)
+    assert qdelta.saved_bytes(4, 4096, 16, 96, 128, 1) == 0
 
 
 def test_workspace_sizes_monotone_and_zero_for_unsupported():
