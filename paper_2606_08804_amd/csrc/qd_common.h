@@ -124,11 +124,11 @@ __device__ inline int fcol(int lane) { return lane & 15; }
 // ----------------------------------------------------------------- tile loads
 // Load rows [0, C) of a [*, ld_g] global matrix block (row stride `gs`
 // elements, D columns) into LDS dst[r*ld + c], zero-filling rows >= len.
-template <typename E, int D>
+template <typename E, int D, int NT = NTHREADS>
 __device__ inline void load_rows(E* dst, int ld, const E* src, size_t gs, int len, int tid) {
   constexpr int VEC = 16 / sizeof(E);
   constexpr int PR = D / VEC;
-  for (int idx = tid; idx < C * PR; idx += NTHREADS) {
+  for (int idx = tid; idx < C * PR; idx += NT) {
     const int r = idx / PR, c = (idx % PR) * VEC;
     uint4 val = make_uint4(0, 0, 0, 0);
     if (r < len) val = *(const uint4*)(src + (size_t)r * gs + c);
@@ -137,12 +137,12 @@ __device__ inline void load_rows(E* dst, int ld, const E* src, size_t gs, int le
 }
 
 // Same, storing the transpose: dst[c*ld + r] = scale(r) * src[r][c].
-template <typename E, int D, typename Scale>
+template <typename E, int D, typename Scale, int NT = NTHREADS>
 __device__ inline void load_rows_t(E* dst, int ld, const E* src, size_t gs, int len, int tid,
                                    Scale scale) {
   constexpr int VEC = 16 / sizeof(E);
   constexpr int PR = D / VEC;
-  for (int idx = tid; idx < C * PR; idx += NTHREADS) {
+  for (int idx = tid; idx < C * PR; idx += NT) {
     const int r = idx % C, c = (idx / C) * VEC;   // consecutive threads -> consecutive rows
     E vals[VEC];
     if (r < len) {
@@ -193,26 +193,26 @@ template <> struct Quad<float> {
 // Register staging of an R x COLS tile (row stride `rs` elements in global,
 // rows >= valid read as zero) for software prefetch: load() issues the global
 // reads, store() writes the tile to LDS with 16-byte stores.
-template <typename E, int R, int COLS>
+template <typename E, int R, int COLS, int NT = NTHREADS>
 struct TileRegs {
   static constexpr int VEC = 16 / sizeof(E);
   static constexpr int PR = COLS / VEC;
   static constexpr int TOTAL = R * PR;
-  static constexpr int N = (TOTAL + NTHREADS - 1) / NTHREADS;
-  static_assert(TOTAL % NTHREADS == 0 || TOTAL < NTHREADS, "tile must split evenly over the workgroup");
+  static constexpr int N = (TOTAL + NT - 1) / NT;
+  static_assert(TOTAL % NT == 0 || TOTAL < NT, "tile must split evenly over the workgroup");
   uint4 v[N];
-  __device__ static inline bool owns(int i, int tid) { return TOTAL >= NTHREADS || tid + i * NTHREADS < TOTAL; }
+  __device__ static inline bool owns(int i, int tid) { return TOTAL >= NT || tid + i * NT < TOTAL; }
   __device__ inline void load(const E* src, size_t rs, int valid, int tid) {
 #pragma unroll
     for (int i = 0; i < N; ++i) {
-      const int idx = tid + i * NTHREADS, r = idx / PR, c = (idx % PR) * VEC;
+      const int idx = tid + i * NT, r = idx / PR, c = (idx % PR) * VEC;
       v[i] = (owns(i, tid) && r < valid) ? *(const uint4*)(src + (size_t)r * rs + c) : make_uint4(0, 0, 0, 0);
     }
   }
   __device__ inline void store(E* dst, int ld, int tid) const {
 #pragma unroll
     for (int i = 0; i < N; ++i) {
-      const int idx = tid + i * NTHREADS, r = idx / PR, c = (idx % PR) * VEC;
+      const int idx = tid + i * NT, r = idx / PR, c = (idx % PR) * VEC;
       if (owns(i, tid)) *(uint4*)(dst + (size_t)r * ld + c) = v[i];
     }
   }
@@ -220,24 +220,24 @@ struct TileRegs {
 
 // As TileRegs, but consecutive threads take consecutive rows, so that the
 // transposed LDS store storeT() (dst[c*ld + r]) is free of bank conflicts.
-template <typename E, int R, int COLS>
+template <typename E, int R, int COLS, int NT = NTHREADS>
 struct TileRegsT {
   static constexpr int VEC = 16 / sizeof(E);
   static constexpr int PR = COLS / VEC;
-  static constexpr int N = R * PR / NTHREADS;
-  static_assert(N >= 1 && N * NTHREADS == R * PR && NTHREADS % R == 0, "tile split");
+  static constexpr int N = R * PR / NT;
+  static_assert(N >= 1 && N * NT == R * PR && NT % R == 0, "tile split");
   uint4 v[N];
   __device__ inline void load(const E* src, size_t rs, int valid, int tid) {
 #pragma unroll
     for (int i = 0; i < N; ++i) {
-      const int idx = tid + i * NTHREADS, r = idx % R, c = (idx / R) * VEC;
+      const int idx = tid + i * NT, r = idx % R, c = (idx / R) * VEC;
       v[i] = r < valid ? *(const uint4*)(src + (size_t)r * rs + c) : make_uint4(0, 0, 0, 0);
     }
   }
   __device__ inline void storeT(E* dst, int ld, int tid) const {
 #pragma unroll
     for (int i = 0; i < N; ++i) {
-      const int idx = tid + i * NTHREADS, r = idx % R, c = (idx / R) * VEC;
+      const int idx = tid + i * NT, r = idx % R, c = (idx / R) * VEC;
       const E* e = (const E*)&v[i];
 #pragma unroll
       for (int j = 0; j < VEC; ++j) dst[(size_t)(c + j) * ld + r] = e[j];
@@ -246,24 +246,24 @@ struct TileRegsT {
 };
 
 // fp32 tile staged in registers and written to LDS converted to E.
-template <typename E, int R, int COLS>
+template <typename E, int R, int COLS, int NT = NTHREADS>
 struct TileRegsF {
   static constexpr int PR = COLS / 4;
   static constexpr int TOTAL = R * PR;
-  static constexpr int N = TOTAL / NTHREADS;
-  static_assert(N >= 1 && N * NTHREADS == TOTAL, "tile split");
+  static constexpr int N = TOTAL / NT;
+  static_assert(N >= 1 && N * NT == TOTAL, "tile split");
   f4 v[N];
   __device__ inline void load(const float* src, size_t rs, int tid) {
 #pragma unroll
     for (int i = 0; i < N; ++i) {
-      const int idx = tid + i * NTHREADS, r = idx / PR, c = (idx % PR) * 4;
+      const int idx = tid + i * NT, r = idx / PR, c = (idx % PR) * 4;
       v[i] = *(const f4*)(src + (size_t)r * rs + c);
     }
   }
   __device__ inline void store(E* dst, int ld, int tid) const {
 #pragma unroll
     for (int i = 0; i < N; ++i) {
-      const int idx = tid + i * NTHREADS, r = idx / PR, c = (idx % PR) * 4;
+      const int idx = tid + i * NT, r = idx / PR, c = (idx % PR) * 4;
       *(typename Quad<E>::raw*)(dst + (size_t)r * ld + c) = Quad<E>::pack(v[i]);
     }
   }
@@ -416,23 +416,39 @@ __device__ inline float sum16(float x) {
 // the off-diagonal blocks by increasing block distance,
 //   Minv_ij = - Minv_ii * sum_{m=j}^{i-1} A_im Minv_mj,
 // with fp32 MFMA products.  Must be called by all threads of the block.
+template <int NT = NTHREADS>
 __device__ inline void unit_lower_inverse(const float* sA, int lda, float* sM, int ldm,
                                           float* tmp, int tid) {
+  static_assert(NT >= 256, "needs at least four waves");
   const int lane = tid & 63, w = tid >> 6;
   // zero the strictly-upper blocks
-  for (int idx = tid; idx < C * C; idx += NTHREADS) {
+  for (int idx = tid; idx < C * C; idx += NT) {
     const int r = idx / C, i = idx % C;
     if ((i >> 4) > (r >> 4)) sM[r * ldm + i] = 0.f;
   }
-  if (lane < 16) {
+  if (lane < 16 && w < 4) {
+    // forward substitution for column j of the inverse of diagonal block w;
+    // row r of the block is read as four broadcast 16-byte loads, one row
+    // ahead of its use, so the dependent FMA chain runs from registers
     const int base = w * 16, j = lane;
+    const float* blk = sA + (size_t)base * lda + base;
     float m[16];
+    f4 cur[4], nxt[4];
 #pragma unroll
-    for (int r = 0; r < 16; ++r) {
+    for (int q = 0; q < 4; ++q) cur[q] = *(const f4*)(blk + (size_t)1 * lda + 4 * q);
+    m[0] = (j == 0) ? 1.f : 0.f;
+#pragma unroll
+    for (int r = 1; r < 16; ++r) {
+      if (r + 1 < 16) {
+#pragma unroll
+        for (int q = 0; q < 4; ++q) nxt[q] = *(const f4*)(blk + (size_t)(r + 1) * lda + 4 * q);
+      }
       float s = (r == j) ? 1.f : 0.f;
 #pragma unroll
-      for (int i = 0; i < r; ++i) s -= sA[(base + r) * lda + base + i] * m[i];
+      for (int i = 0; i < r; ++i) s -= cur[i >> 2][i & 3] * m[i];
       m[r] = s;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) cur[q] = nxt[q];
     }
 #pragma unroll
     for (int r = 0; r < 16; ++r) sM[(base + r) * ldm + base + j] = m[r];

@@ -41,18 +41,20 @@ struct PrepSmem {
   E GXt[DK][C + P];
   float A[C][C + 4];
   float M[C][C + 4];
-  float tmp[NWAVES * 16 * 17];
+  float tmp[4 * 16 * 17];
   E Tm[C][C + P];
 };
 
 // dst[c*C + r] = scale(r) * src[r*ld + c] for a C x D LDS tile, written to
 // global memory with 16-byte stores (one store covers 16/sizeof(E) rows).
-template <typename E, int D, typename Scale>
+template <typename E, int D, int NT, typename Scale>
 __device__ inline void store_transposed(E* dst, const E* src, int ld, int tid, Scale scale) {
   constexpr int VEC = 16 / sizeof(E);
   constexpr int G = C / VEC;
-  for (int idx = tid; idx < D * G; idx += NTHREADS) {
-    const int c = idx / G, r0 = (idx % G) * VEC;
+  // consecutive threads take consecutive columns c: the column reads of the
+  // LDS tile hit consecutive addresses (no bank conflicts)
+  for (int idx = tid; idx < D * G; idx += NT) {
+    const int c = idx % D, r0 = (idx / D) * VEC;
     uint4 raw;
     E* e = (E*)&raw;
 #pragma unroll
@@ -62,11 +64,13 @@ __device__ inline void store_transposed(E* dst, const E* src, int ld, int tid, S
 }
 
 // Raw inputs of one (chunk, head) unit, staged in registers one unit ahead.
+constexpr int PREP_THREADS = 512;   // 8 waves: two per SIMD hide each other's latency
+
 template <typename E, int DK, int DV, bool BWD>
 struct PrepPre {
-  TileRegs<E, C, DK> K, Q;
-  TileRegsT<E, C, DV> V;
-  typename std::conditional<BWD, TileRegs<E, C, DV>, NoRegs>::type dO;
+  TileRegs<E, C, DK, PREP_THREADS> K, Q;
+  TileRegsT<E, C, DV, PREP_THREADS> V;
+  typename std::conditional<BWD, TileRegs<E, C, DV, PREP_THREADS>, NoRegs>::type dO;
   float la, beta, lam;
   int t0, len, g, h;
   bool valid;
@@ -78,7 +82,8 @@ struct PrepPre {
 // prefetches the next unit's inputs into registers while computing the
 // current one.
 template <typename E, int DK, int DV, bool BWD>
-__global__ __launch_bounds__(NTHREADS) void k_prep(Params p) {
+__global__ __launch_bounds__(PREP_THREADS) void k_prep(Params p) {
+  constexpr int NT = PREP_THREADS, NW = NT / 64;
   constexpr int P = Pad<E>::v;
   constexpr int LK = DK + P, LC = C + P;
   typedef PrepPre<E, DK, DV, BWD> Pre;
@@ -130,22 +135,37 @@ __global__ __launch_bounds__(NTHREADS) void k_prep(Params p) {
     __syncthreads();
 
     // transposed copies for the scans: K^T, and (diag(g) Q)^T for the backward
-    store_transposed<E, DK>((E*)p.wKt + gi * DK * C, &sm.u.a.K[0][0], LK, tid, One());
+    store_transposed<E, DK, NT>((E*)p.wKt + gi * DK * C, &sm.u.a.K[0][0], LK, tid, One());
     if (BWD)
-      store_transposed<E, DK>((E*)p.wQgt + gi * DK * C, &sm.u.a.Q[0][0], LK, tid,
+      store_transposed<E, DK, NT>((E*)p.wQgt + gi * DK * C, &sm.u.a.Q[0][0], LK, tid,
                               [&](int r) { return __expf(sm.b[r]); });
-    // mixed inputs X = K + lambda Q and the transposed decayed copy (g X)^T
-    for (int idx = tid; idx < C * DK; idx += NTHREADS) {
-      const int r = idx % C, c = idx / C;
-      const float xv = tof(sm.u.a.K[r][c]) + sm.lam[r] * tof(sm.u.a.Q[r][c]);
-      sm.u.a.X[r][c] = fromf<E>(xv);
-      sm.GXt[c][r] = fromf<E>(__expf(sm.b[r]) * xv);
+    // mixed inputs X = K + lambda Q and the transposed decayed copy (g X)^T;
+    // a thread takes 16 bytes of one row, consecutive threads consecutive rows
+    {
+      constexpr int VEC = 16 / sizeof(E);
+      for (int idx = tid; idx < C * DK / VEC; idx += NT) {
+        const int r = idx % C, c0 = (idx / C) * VEC;
+        const uint4 kr = *(const uint4*)&sm.u.a.K[r][c0];
+        const uint4 qr = *(const uint4*)&sm.u.a.Q[r][c0];
+        const E* ke = (const E*)&kr;
+        const E* qe = (const E*)&qr;
+        const float lr = sm.lam[r], gr = __expf(sm.b[r]);
+        uint4 xr;
+        E* xe = (E*)&xr;
+#pragma unroll
+        for (int j = 0; j < VEC; ++j) {
+          const float xv = tof(ke[j]) + lr * tof(qe[j]);
+          xe[j] = fromf<E>(xv);
+          sm.GXt[c0 + j][r] = fromf<E>(gr * xv);
+        }
+        *(uint4*)&sm.u.a.X[r][c0] = xr;
+      }
     }
     __syncthreads();
 
     // Gram products X K^T and Q K^T; A (fp32, LDS) and P or P^T (workspace)
     E* wP = BWD ? (E*)p.wT + gi * 2 * C * C + C * C : (E*)p.wP + gi * C * C;
-    for (int t = w; t < 16; t += NWAVES) {
+    for (int t = w; t < 16; t += NW) {
       const int m0 = (t >> 2) * 16, n0 = (t & 3) * 16;
       const f4 gx = mma_k<E, DK>(kmaj(&sm.u.a.X[0][0], LK), kmaj(&sm.u.a.K[0][0], LK), m0, n0, zero4(), lane);
       const f4 qk = mma_k<E, DK>(kmaj(&sm.u.a.Q[0][0], LK), kmaj(&sm.u.a.K[0][0], LK), m0, n0, zero4(), lane);
@@ -164,9 +184,9 @@ __global__ __launch_bounds__(NTHREADS) void k_prep(Params p) {
     __syncthreads();
 
     // UT solve: M = (I + A)^{-1}, T = M diag(beta)
-    unit_lower_inverse(&sm.A[0][0], C + 4, &sm.M[0][0], C + 4, sm.tmp, tid);
+    unit_lower_inverse<NT>(&sm.A[0][0], C + 4, &sm.M[0][0], C + 4, sm.tmp, tid);
     E* wTt = BWD ? (E*)p.wT + gi * 2 * C * C : nullptr;
-    for (int idx = tid; idx < C * C; idx += NTHREADS) {
+    for (int idx = tid; idx < C * C; idx += NT) {
       const int r = idx / C, i = idx % C;
       const E tv = fromf<E>(sm.M[r][i] * sm.beta[i]);
       sm.Tm[r][i] = tv;
@@ -178,7 +198,7 @@ __global__ __launch_bounds__(NTHREADS) void k_prep(Params p) {
 
     // U = T V, stored C-fragment tiled: tile (mt, nt) at ((mt*(DV/16)+nt)*64 + lane)*4
     E* wU = (E*)p.wU + gi * C * DV;
-    for (int t = w; t < (C / 16) * (DV / 16); t += NWAVES) {
+    for (int t = w; t < (C / 16) * (DV / 16); t += NW) {
       const int m0 = (t / (DV / 16)) * 16, n0 = (t % (DV / 16)) * 16;
       const f4 uu = mma_k<E, C>(kmaj(&sm.Tm[0][0], LC), kmaj(&sm.u.Vt[0][0], LC), m0, n0, zero4(), lane);
       *(typename Quad<E>::raw*)(wU + ((size_t)t * 64 + lane) * 4) = Quad<E>::pack(uu);
@@ -186,7 +206,7 @@ __global__ __launch_bounds__(NTHREADS) void k_prep(Params p) {
     // W = T diag(g) X, row-major C x DK (and W^T in backward mode)
     E* wW = (E*)p.wW + gi * C * DK;
     E* wWt = BWD ? (E*)p.wWt + gi * DK * C : nullptr;
-    for (int t = w; t < (C / 16) * (DK / 16); t += NWAVES) {
+    for (int t = w; t < (C / 16) * (DK / 16); t += NW) {
       const int m0 = (t / (DK / 16)) * 16, n0 = (t % (DK / 16)) * 16;
       const f4 wv = mma_k<E, C>(kmaj(&sm.Tm[0][0], LC), kmaj(&sm.GXt[0][0], LC), m0, n0, zero4(), lane);
 #pragma unroll
@@ -199,7 +219,7 @@ __global__ __launch_bounds__(NTHREADS) void k_prep(Params p) {
       __syncthreads();
       x.dO.store(&sm.u.dO[0][0], DV + P, tid);
       __syncthreads();
-      store_transposed<E, DV>((E*)p.wdOt + gi * DV * C, &sm.u.dO[0][0], DV + P, tid, One());
+      store_transposed<E, DV, NT>((E*)p.wdOt + gi * DV * C, &sm.u.dO[0][0], DV + P, tid, One());
     }
   }
 }
@@ -407,9 +427,9 @@ static hipError_t launch_fwd_t(const Params& p, int bwd_prep, int with_scan, hip
     const int stage = bwd_prep ? ST_PREP_BWD : ST_PREP_FWD;
     prof_mark(stage, 0, st);
     if (bwd_prep)
-      hipLaunchKernelGGL((k_prep<E, DK, DV, true>), gp, dim3(NTHREADS), 0, st, p);
+      hipLaunchKernelGGL((k_prep<E, DK, DV, true>), gp, dim3(PREP_THREADS), 0, st, p);
     else
-      hipLaunchKernelGGL((k_prep<E, DK, DV, false>), gp, dim3(NTHREADS), 0, st, p);
+      hipLaunchKernelGGL((k_prep<E, DK, DV, false>), gp, dim3(PREP_THREADS), 0, st, p);
     prof_mark(stage, 1, st);
   }
   if (with_scan) {
