@@ -16,7 +16,7 @@ using qd::C;
 constexpr int kVersion = 10000;  // 1.0.0
 
 struct Layout {
-  size_t wb = 0, wU = 0, wW = 0, wP = 0, wKt = 0, wT = 0, wWt = 0, wQgt = 0, wdOt = 0;
+  size_t wb = 0, wU = 0, wW = 0, wP = 0, wKt = 0, wT = 0, wWt = 0, wQgt = 0, wQt = 0, wdOt = 0;
   size_t dSo = 0, dDb = 0, states = 0;
   size_t total = 0;
 };
@@ -44,6 +44,7 @@ Layout make_layout(size_t units, int Dk, int Dv, int esz, bool bwd) {
     L.wT = take(units * 2 * C * C * esz);
     L.wWt = take(units * C * Dk * esz);
     L.wQgt = take(units * C * Dk * esz);
+    L.wQt = take(units * C * Dk * esz);
     L.wdOt = take(units * C * Dv * esz);
     L.dSo = take(units * (size_t)Dv * Dk * 4);
     L.dDb = take(units * C * Dv * esz);
@@ -194,6 +195,7 @@ int bwd_impl(bool varlen, int32_t B, int32_t T, int32_t N, const int32_t* cu, in
   p.wT = w + L.wT;
   p.wWt = w + L.wWt;
   p.wQgt = w + L.wQgt;
+  p.wQt = w + L.wQt;
   p.wdOt = w + L.wdOt;
   p.dO = d_o;
   p.dSfin = d_final_state;   // dO is read by the backward-mode preparation as well

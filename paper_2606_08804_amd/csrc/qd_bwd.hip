@@ -28,6 +28,8 @@
 #include "qd_common.h"
 #include "qd_launch.h"
 
+#include <type_traits>
+
 namespace qd {
 
 // ------------------------------------------------------------------ scan
@@ -211,7 +213,10 @@ __global__ __launch_bounds__(NTHREADS) void k_scan_bwd(Params p) {
 template <typename E, int DK>
 struct BwdSmem {
   static constexpr int P = Pad<E>::v;
-  static constexpr int BV = 32, KH = 32;
+  static constexpr int BV = 32;
+  // bf16 operands need explicit transposed copies of dG and dQK for
+  // contiguous fragment loads; fp32 fragments are single scalars either way
+  static constexpr bool TCOPY = sizeof(E) == 2;
   float b[C], g[C], kb[C], beta[C], lam[C], db[C], dbeta[C], dlam[C], tk[C];
   float sdot[NWAVES];
   union {
@@ -222,13 +227,10 @@ struct BwdSmem {
       E V[C][BV + P];       // V tile (r, v)
     } a;
     struct {
-      E Q[C][KH + P];
-      E K[C][KH + P];
-      E X[C][KH + P];
-      E GX[C][KH + P];
-      E dW[C][KH + P];
-      float dX[C][KH + 4];
-    } h;
+      E K[C][DK + P];       // chunk keys (r, k)
+      E Q[C][DK + P];       // chunk queries (r, k)
+      E dW[C][DK + P];      // dW = -dD S (r, k)
+    } b1;
     struct {
       float G[C][C + 4];
       float QK[C][C + 4];
@@ -236,13 +238,51 @@ struct BwdSmem {
       float A[C][C + 4];
       float M[C][C + 4];
       float Y[C][C + 4];
-      float tmp[NWAVES * 16 * 17];
+      float tmp[4 * 16 * 17];
     } c;
+    struct {
+      E dWt[DK][C + P];     // dW^T (k, r)
+      E Kt[DK][C + P];      // K^T (k, r)
+      E Qt[DK][C + P];      // Q^T (k, r)
+      E oq[C][DK + P];      // dq staging
+      E ok[C][DK + P];      // dk staging
+    } b3;
   } u;
-  E Tm[C][C + P];
-  E dG[C][C + P];
-  E dQK[C][C + P];
+  E TmT[C][C + P];          // T^T (i, r)
+  E dG[C][C + P];           // dG (r, i)
+  E dQK[C][C + P];          // dQK (r, i)
+  typename std::conditional<TCOPY, E[C][C + P], char[16]>::type dGt;    // dG^T (i, r)
+  typename std::conditional<TCOPY, E[C][C + P], char[16]>::type dQKt;   // dQK^T (i, r)
 };
+
+// s * (k + l * q) element-wise on one fragment, rounded to the operand type
+template <typename FR>
+__device__ inline FR mix_frag(FR kf, FR qf, float l, float sc);
+template <>
+__device__ inline bf8 mix_frag<bf8>(bf8 kf, bf8 qf, float l, float sc) {
+  bf8 r;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) r[e] = (__bf16)(sc * ((float)kf[e] + l * (float)qf[e]));
+  return r;
+}
+template <>
+__device__ inline float mix_frag<float>(float kf, float qf, float l, float sc) {
+  return sc * (kf + l * qf);
+}
+// k + l_e q per element e of a fragment whose elements run over tokens
+template <typename FR>
+__device__ inline FR mix_tokens(FR kf, FR qf, const float* lam);
+template <>
+__device__ inline bf8 mix_tokens<bf8>(bf8 kf, bf8 qf, const float* lam) {
+  bf8 r;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) r[e] = (__bf16)((float)kf[e] + lam[e] * (float)qf[e]);
+  return r;
+}
+template <>
+__device__ inline float mix_tokens<float>(float kf, float qf, const float* lam) {
+  return kf + lam[0] * qf;
+}
 
 template <typename E, int DK>
 struct BwdPreA {
@@ -254,11 +294,10 @@ struct BwdPreA {
 template <typename E, int DK, int DV>
 __global__ __launch_bounds__(NTHREADS) void k_bwd_intra(Params p) {
   constexpr int P = Pad<E>::v;
-  constexpr int BV = 32, KH = 32;
-  constexpr int LC = C + P, LB = BV + P, LH = KH + P, LF = C + 4;
+  constexpr int BV = 32;
+  constexpr int LC = C + P, LB = BV + P, LF = C + 4;
   constexpr int KS = Mma<E>::KS;
   constexpr int NKB = DK / 16;        // 16-column blocks of Dk
-  constexpr int NQ = DK / KH;         // Dk quarters in phase B
   constexpr int NVT = DV / BV;
   typedef typename Mma<E>::frag FR;
   __shared__ BwdSmem<E, DK> sm;
@@ -305,10 +344,16 @@ __global__ __launch_bounds__(NTHREADS) void k_bwd_intra(Params p) {
     pa.Df.load(Dg + (size_t)(16 * w) * DV + v0, DV, 16, lane);
     pa.dD.load(dDg + (size_t)(16 * w) * DV + v0, DV, 16, lane);
   };
+  TileRegs<E, C, DK> rKf, rQf;    // chunk K, Q rows for phase B1
   fetchA(0);
   for (int vt = 0; vt < NVT; ++vt) {
     const BwdPreA<E, DK> cur = pa;
-    if (vt + 1 < NVT) fetchA(vt + 1);
+    if (vt + 1 < NVT) {
+      fetchA(vt + 1);
+    } else {
+      rKf.load((const E*)p.k + arow * DK, (size_t)H * DK, len, tid);
+      rQf.load((const E*)p.q + arow * DK, (size_t)H * DK, len, tid);
+    }
     block_sync_lds();
     cur.S.store(&sm.u.a.St[0][0], LB, tid);
     cur.dS.store(&sm.u.a.dSt[0][0], LB, tid);
@@ -344,56 +389,51 @@ __global__ __launch_bounds__(NTHREADS) void k_bwd_intra(Params p) {
   sdot = wave_sum(sdot);
   if (lane == 0) sm.sdot[w] = sdot;
 
-  // ---------------- phase B
-  const E* qg = (const E*)p.q + arow * DK;
-  const E* kg = (const E*)p.k + arow * DK;
-  TileRegs<E, C, KH> rQ, rK;
-  auto fetchQ = [&](int k0) {
-    rQ.load(qg + k0, (size_t)H * DK, len, tid);
-    rK.load(kg + k0, (size_t)H * DK, len, tid);
-  };
-  // stage quarter kq of Q, K (from registers), dW = -aW (rows 16w..) and X, g X
-  auto stage_quarter = [&](int kq) {
-    rQ.store(&sm.u.h.Q[0][0], LH, tid);
-    rK.store(&sm.u.h.K[0][0], LH, tid);
+  // ---------------- phase B1: G = X K^T, QK = Q K^T, dT2 = dW (g X)^T
+  constexpr int LKD = DK + P;
+  block_sync_lds();
+  rKf.store(&sm.u.b1.K[0][0], LKD, tid);
+  rQf.store(&sm.u.b1.Q[0][0], LKD, tid);
 #pragma unroll
-    for (int nb = 0; nb < KH / 16; ++nb)
+  for (int kb = 0; kb < NKB; ++kb)
 #pragma unroll
-      for (int j = 0; j < 4; ++j)
-        sm.u.h.dW[16 * w + frow(lane, j)][nb * 16 + fcol(lane)] = fromf<E>(-aW[kq * (KH / 16) + nb][j]);
-  };
-  auto make_x = [&]() {
-    for (int idx = tid; idx < C * KH; idx += NTHREADS) {
-      const int r = idx / KH, c = idx % KH;
-      const float x = tof(sm.u.h.K[r][c]) + sm.lam[r] * tof(sm.u.h.Q[r][c]);
-      sm.u.h.X[r][c] = fromf<E>(x);
-      sm.u.h.GX[r][c] = fromf<E>(sm.g[r] * x);
-    }
-  };
-
-  // phase B1: G = X K^T, QK = Q K^T, dT2 = dW (g X)^T, over the Dk quarters
+    for (int j = 0; j < 4; ++j) sm.u.b1.dW[16 * w + frow(lane, j)][kb * 16 + fcol(lane)] = fromf<E>(-aW[kb][j]);
+  block_sync_lds();
   f4 aG[4], aQK[4], adT[4];
 #pragma unroll
   for (int i = 0; i < 4; ++i) aG[i] = aQK[i] = adT[i] = zero4();
-  fetchQ(0);
-#pragma unroll
-  for (int kq = 0; kq < NQ; ++kq) {
-    block_sync_lds();
-    stage_quarter(kq);
-    fetchQ(kq + 1 < NQ ? (kq + 1) * KH : 0);
-    block_sync_lds();
-    make_x();
-    block_sync_lds();
+  {
+    const float lam_a = sm.lam[16 * w + (lane & 15)];
+    float lam_b[4], g_b[4];
 #pragma unroll
     for (int ib = 0; ib < 4; ++ib) {
-      aG[ib] = mma_k<E, KH>(kmaj(&sm.u.h.X[0][0], LH), kmaj(&sm.u.h.K[0][0], LH), 16 * w, ib * 16, aG[ib], lane);
-      aQK[ib] = mma_k<E, KH>(kmaj(&sm.u.h.Q[0][0], LH), kmaj(&sm.u.h.K[0][0], LH), 16 * w, ib * 16, aQK[ib], lane);
-      adT[ib] = mma_k<E, KH>(kmaj(&sm.u.h.dW[0][0], LH), kmaj(&sm.u.h.GX[0][0], LH), 16 * w, ib * 16, adT[ib], lane);
+      lam_b[ib] = sm.lam[ib * 16 + (lane & 15)];
+      g_b[ib] = sm.g[ib * 16 + (lane & 15)];
+    }
+#pragma unroll
+    for (int ks = 0; ks < DK / KS; ++ks) {
+      const FR kA = Frag<E>::load(kmaj(&sm.u.b1.K[0][0], LKD), 16 * w, ks * KS, lane);
+      const FR qA = Frag<E>::load(kmaj(&sm.u.b1.Q[0][0], LKD), 16 * w, ks * KS, lane);
+      const FR xA = mix_frag<FR>(kA, qA, lam_a, 1.f);
+      const FR dwA = Frag<E>::load(kmaj(&sm.u.b1.dW[0][0], LKD), 16 * w, ks * KS, lane);
+#pragma unroll
+      for (int ib = 0; ib < 4; ++ib) {
+        const FR kB = Frag<E>::load(kmaj(&sm.u.b1.K[0][0], LKD), ib * 16, ks * KS, lane);
+        const FR qB = Frag<E>::load(kmaj(&sm.u.b1.Q[0][0], LKD), ib * 16, ks * KS, lane);
+        const FR gxB = mix_frag<FR>(kB, qB, lam_b[ib], g_b[ib]);
+        aG[ib] = Mma<E>::mma(xA, kB, aG[ib]);
+        aQK[ib] = Mma<E>::mma(qA, kB, aQK[ib]);
+        adT[ib] = Mma<E>::mma(dwA, gxB, adT[ib]);
+      }
     }
   }
+  // K^T and Q^T for phase B3, in flight during phase B2
+  TileRegs<E, DK, C> rKt, rQt;
+  rKt.load((const E*)p.wKt + gi * DK * C, C, DK, tid);
+  rQt.load((const E*)p.wQt + gi * DK * C, C, DK, tid);
   block_sync_lds();
 
-  // phase B2: UT-solve backward and the C x C gradient terms
+  // ---------------- phase B2: UT-solve backward and the C x C gradient terms
 #pragma unroll
   for (int ib = 0; ib < 4; ++ib) {
 #pragma unroll
@@ -418,8 +458,8 @@ __global__ __launch_bounds__(NTHREADS) void k_bwd_intra(Params p) {
     if ((tid & 3) == 0) sm.dbeta[q4] = s4;
   }
   for (int idx = tid; idx < C * C; idx += NTHREADS) {
-    const int r = idx / C, i = idx % C;
-    sm.Tm[r][i] = fromf<E>(sm.u.c.M[r][i] * sm.beta[i]);
+    const int r = idx % C, i = idx / C;
+    sm.TmT[i][r] = fromf<E>(sm.u.c.M[r][i] * sm.beta[i]);
   }
   block_sync_lds();
   for (int idx = tid; idx < C * C; idx += NTHREADS) {
@@ -468,6 +508,10 @@ __global__ __launch_bounds__(NTHREADS) void k_bwd_intra(Params p) {
       }
       sm.dG[r][i] = fromf<E>(dg);
       sm.dQK[r][i] = fromf<E>(dqk);
+      if constexpr (BwdSmem<E, DK>::TCOPY) {
+        sm.dGt[i][r] = fromf<E>(dg);
+        sm.dQKt[i][r] = fromf<E>(dqk);
+      }
     }
     dbr += __shfl_xor(dbr, 1, 64);
     dbr += __shfl_xor(dbr, 2, 64);
@@ -495,96 +539,97 @@ __global__ __launch_bounds__(NTHREADS) void k_bwd_intra(Params p) {
     ec += __shfl_xor(ec, 2, 64);
     if ((tid & 3) == 0) sm.db[i] -= ec;
   }
+  block_sync_lds();
 
-  // phase B3: dX, dq, dk over the Dk quarters (wave w owns rows 16w..)
-  E* dqo = (E*)p.dq;
-  E* dko = (E*)p.dk;
+  // ---------------- phase B3: dX, dq, dk (wave w owns rows 16w..)
+  rKt.store(&sm.u.b3.Kt[0][0], LC, tid);
+  rQt.store(&sm.u.b3.Qt[0][0], LC, tid);
 #pragma unroll
-  for (int kq = 0; kq < NQ; ++kq) {
-    const int k0 = kq * KH;
-    block_sync_lds();
-    stage_quarter(kq);
-    if (kq + 1 < NQ) fetchQ((kq + 1) * KH);
-    block_sync_lds();
-    make_x();
-    // dgX = T^T dW (rows 16w..)
+  for (int kb = 0; kb < NKB; ++kb) {
+    f4 nw;
 #pragma unroll
-    for (int nb = 0; nb < KH / 16; ++nb) {
-      const f4 d = mma_k<E, C>(imaj(&sm.Tm[0][0], LC), imaj(&sm.u.h.dW[0][0], LH), 16 * w, nb * 16, zero4(), lane);
+    for (int j = 0; j < 4; ++j) nw[j] = -aW[kb][j];
+    *(typename Quad<E>::raw*)&sm.u.b3.dWt[kb * 16 + fcol(lane)][16 * w + frow(lane, 0)] = Quad<E>::pack(nw);
+  }
+  block_sync_lds();
+  {
+    constexpr int NTK = C / KS;
+    FR tA[NTK], gA[NTK], qkA[NTK], qktA[NTK], gtA[NTK];
+    float lamk[NTK][Mma<E>::KPL];
 #pragma unroll
-      for (int j = 0; j < 4; ++j) sm.u.h.dX[16 * w + frow(lane, j)][nb * 16 + fcol(lane)] = d[j];
+    for (int ks = 0; ks < NTK; ++ks) {
+      tA[ks] = Frag<E>::load(kmaj(&sm.TmT[0][0], LC), 16 * w, ks * KS, lane);
+      gA[ks] = Frag<E>::load(kmaj(&sm.dG[0][0], LC), 16 * w, ks * KS, lane);
+      qkA[ks] = Frag<E>::load(kmaj(&sm.dQK[0][0], LC), 16 * w, ks * KS, lane);
+      if constexpr (BwdSmem<E, DK>::TCOPY) {
+        qktA[ks] = Frag<E>::load(kmaj(&sm.dQKt[0][0], LC), 16 * w, ks * KS, lane);
+        gtA[ks] = Frag<E>::load(kmaj(&sm.dGt[0][0], LC), 16 * w, ks * KS, lane);
+      } else {
+        qktA[ks] = Frag<E>::load(imaj(&sm.dQK[0][0], LC), 16 * w, ks * KS, lane);
+        gtA[ks] = Frag<E>::load(imaj(&sm.dG[0][0], LC), 16 * w, ks * KS, lane);
+      }
+#pragma unroll
+      for (int e = 0; e < Mma<E>::KPL; ++e) lamk[ks][e] = sm.lam[ks * KS + (lane >> 4) * Mma<E>::KPL + e];
     }
-    block_sync_lds();
-    {
-      // db_r += g_r X_r . dgX_r + g_r Q_r . aQ_r ;  tk_r += kb_r K_r . aK_r   (this quarter)
-      const int r = q4, c0 = (tid & 3) * (KH / 4);
-      float s4 = 0.f;
+    const int r0 = 16 * w + frow(lane, 0);
+    float rdb[4] = {0.f, 0.f, 0.f, 0.f}, rtk[4] = {0.f, 0.f, 0.f, 0.f}, rdl[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-      for (int c = c0; c < c0 + KH / 4; ++c) s4 += tof(sm.u.h.X[r][c]) * sm.u.h.dX[r][c];
-      s4 += __shfl_xor(s4, 1, 64);
-      s4 += __shfl_xor(s4, 2, 64);
-      float rq[4] = {0.f, 0.f, 0.f, 0.f}, rk[4] = {0.f, 0.f, 0.f, 0.f};
+    for (int kb = 0; kb < NKB; ++kb) {
+      f4 dgx = zero4(), dxp = zero4(), dqp = zero4(), dkp = zero4();
 #pragma unroll
-      for (int nb = 0; nb < KH / 16; ++nb)
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          const int rr = 16 * w + frow(lane, j), cc = nb * 16 + fcol(lane);
-          rq[j] += tof(sm.u.h.Q[rr][cc]) * aQ[kq * (KH / 16) + nb][j];
-          rk[j] += tof(sm.u.h.K[rr][cc]) * aK[kq * (KH / 16) + nb][j];
-        }
+      for (int ks = 0; ks < NTK; ++ks) {
+        const FR ktB = Frag<E>::load(kmaj(&sm.u.b3.Kt[0][0], LC), kb * 16, ks * KS, lane);
+        const FR qtB = Frag<E>::load(kmaj(&sm.u.b3.Qt[0][0], LC), kb * 16, ks * KS, lane);
+        const FR dwB = Frag<E>::load(kmaj(&sm.u.b3.dWt[0][0], LC), kb * 16, ks * KS, lane);
+        const FR xtB = mix_tokens<FR>(ktB, qtB, lamk[ks]);
+        dgx = Mma<E>::mma(tA[ks], dwB, dgx);      // T^T dW
+        dxp = Mma<E>::mma(gA[ks], ktB, dxp);      // dG K
+        dqp = Mma<E>::mma(qkA[ks], ktB, dqp);     // dQK K
+        dkp = Mma<E>::mma(qktA[ks], qtB, dkp);    // dQK^T Q
+        dkp = Mma<E>::mma(gtA[ks], xtB, dkp);     // dG^T X
+      }
+      const int kc = kb * 16 + fcol(lane);
+      const typename Quad<E>::raw kv = *(const typename Quad<E>::raw*)&sm.u.b3.Kt[kc][r0];
+      const typename Quad<E>::raw qv = *(const typename Quad<E>::raw*)&sm.u.b3.Qt[kc][r0];
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
-        rq[j] = sum16(rq[j]);
-        rk[j] = sum16(rk[j]);
-      }
-      block_sync_lds();
-      if ((tid & 3) == 0) sm.db[r] += sm.g[r] * s4;
-      block_sync_lds();
-      if (fcol(lane) == 0) {
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          const int rr = 16 * w + frow(lane, j);
-          sm.db[rr] += sm.g[rr] * rq[j];
-          sm.tk[rr] += sm.kb[rr] * rk[j];
-        }
+        const int r = r0 + j;
+        const float Kv = Quad<E>::get(kv, j), Qv = Quad<E>::get(qv, j);
+        const float gr = sm.g[r], lr = sm.lam[r], kbr = sm.kb[r];
+        const float X = Kv + lr * Qv;
+        rdb[j] += gr * (X * dgx[j] + Qv * aQ[kb][j]);
+        rtk[j] += kbr * Kv * aK[kb][j];
+        const float dX = gr * dgx[j] + dxp[j];
+        rdl[j] += Qv * dX;
+        sm.u.b3.oq[r][kc] = fromf<E>(gr * aQ[kb][j] + dqp[j] + lr * dX);
+        sm.u.b3.ok[r][kc] = fromf<E>(kbr * aK[kb][j] + dkp[j] + dX);
       }
     }
-    // dX = g dgX + dG K
 #pragma unroll
-    for (int nb = 0; nb < KH / 16; ++nb) {
-      const f4 d = mma_k<E, C>(kmaj(&sm.dG[0][0], LC), imaj(&sm.u.h.K[0][0], LH), 16 * w, nb * 16, zero4(), lane);
+    for (int j = 0; j < 4; ++j) {
+      rdb[j] = sum16(rdb[j]);
+      rtk[j] = sum16(rtk[j]);
+      rdl[j] = sum16(rdl[j]);
+    }
+    if (fcol(lane) == 0) {
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
-        const int r = 16 * w + frow(lane, j), c = nb * 16 + fcol(lane);
-        sm.u.h.dX[r][c] = sm.g[r] * sm.u.h.dX[r][c] + d[j];
+        sm.db[r0 + j] += rdb[j];
+        sm.tk[r0 + j] += rtk[j];
+        sm.dlam[r0 + j] += rdl[j];
       }
     }
-    block_sync_lds();
-    {
-      const int r = q4, c0 = (tid & 3) * (KH / 4);
-      float s4 = 0.f;
-#pragma unroll
-      for (int c = c0; c < c0 + KH / 4; ++c) s4 += tof(sm.u.h.Q[r][c]) * sm.u.h.dX[r][c];
-      s4 += __shfl_xor(s4, 1, 64);
-      s4 += __shfl_xor(s4, 2, 64);
-      if ((tid & 3) == 0) sm.dlam[r] += s4;
-    }
-    // dq = g aQ + dQK K + lambda dX ;  dk = kb aK + dQK^T Q + dG^T X + dX
-#pragma unroll
-    for (int nb = 0; nb < KH / 16; ++nb) {
-      const f4 a = mma_k<E, C>(kmaj(&sm.dQK[0][0], LC), imaj(&sm.u.h.K[0][0], LH), 16 * w, nb * 16, zero4(), lane);
-      f4 bk = mma_k<E, C>(imaj(&sm.dQK[0][0], LC), imaj(&sm.u.h.Q[0][0], LH), 16 * w, nb * 16, zero4(), lane);
-      bk = mma_k<E, C>(imaj(&sm.dG[0][0], LC), imaj(&sm.u.h.X[0][0], LH), 16 * w, nb * 16, bk, lane);
-      const int kbk = kq * (KH / 16) + nb;
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const int r = 16 * w + frow(lane, j), c = nb * 16 + fcol(lane);
-        if (r < len) {
-          const float dx = sm.u.h.dX[r][c];
-          const size_t o = (arow + (size_t)r * H) * DK + k0 + c;
-          dqo[o] = fromf<E>(sm.g[r] * aQ[kbk][j] + a[j] + sm.lam[r] * dx);
-          dko[o] = fromf<E>(sm.kb[r] * aK[kbk][j] + bk[j] + dx);
-        }
+  }
+  block_sync_lds();
+  {
+    constexpr int VEC = 16 / sizeof(E), PR = DK / VEC;
+    E* dqo = (E*)p.dq + arow * DK;
+    E* dko = (E*)p.dk + arow * DK;
+    for (int idx = tid; idx < C * PR; idx += NTHREADS) {
+      const int r = idx / PR, cc = (idx % PR) * VEC;
+      if (r < len) {
+        *(uint4*)(dqo + (size_t)r * H * DK + cc) = *(const uint4*)&sm.u.b3.oq[r][cc];
+        *(uint4*)(dko + (size_t)r * H * DK + cc) = *(const uint4*)&sm.u.b3.ok[r][cc];
       }
     }
   }

@@ -334,6 +334,7 @@ struct Params {
   void* wT;              // [slot][H][2][C][C] T^T and P^T (backward only)
   void* wWt;             // [slot][H][Dk][C]  W^T (backward only)
   void* wQgt;            // [slot][H][Dk][C]  (diag(g) Q)^T (backward only)
+  void* wQt;             // [slot][H][Dk][C]  Q^T (backward only)
   void* wdOt;            // [slot][H][Dv][C]  dO^T (backward only)
   // backward
   const void* dO;

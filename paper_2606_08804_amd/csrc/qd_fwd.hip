@@ -136,9 +136,11 @@ __global__ __launch_bounds__(PREP_THREADS) void k_prep(Params p) {
 
     // transposed copies for the scans: K^T, and (diag(g) Q)^T for the backward
     store_transposed<E, DK, NT>((E*)p.wKt + gi * DK * C, &sm.u.a.K[0][0], LK, tid, One());
-    if (BWD)
+    if (BWD) {
       store_transposed<E, DK, NT>((E*)p.wQgt + gi * DK * C, &sm.u.a.Q[0][0], LK, tid,
-                              [&](int r) { return __expf(sm.b[r]); });
+                                  [&](int r) { return __expf(sm.b[r]); });
+      store_transposed<E, DK, NT>((E*)p.wQt + gi * DK * C, &sm.u.a.Q[0][0], LK, tid, One());
+    }
     // mixed inputs X = K + lambda Q and the transposed decayed copy (g X)^T;
     // a thread takes 16 bytes of one row, consecutive threads consecutive rows
     {
