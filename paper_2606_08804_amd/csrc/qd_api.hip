@@ -16,7 +16,7 @@ using qd::C;
 constexpr int kVersion = 10000;  // 1.0.0
 
 struct Layout {
-  size_t wb = 0, wU = 0, wW = 0, wP = 0, wKt = 0, wT = 0, wWt = 0, wQgt = 0, wQt = 0, wdOt = 0;
+  size_t wb = 0, wU = 0, wW = 0, wP = 0, wKt = 0, wT = 0, wWt = 0, wQgt = 0, wQt = 0, wM = 0, wdOt = 0;
   size_t dSo = 0, dDb = 0, states = 0;
   size_t total = 0;
 };
@@ -45,6 +45,7 @@ Layout make_layout(size_t units, int Dk, int Dv, int esz, bool bwd) {
     L.wWt = take(units * C * Dk * esz);
     L.wQgt = take(units * C * Dk * esz);
     L.wQt = take(units * C * Dk * esz);
+    L.wM = take(units * C * C * esz);
     L.wdOt = take(units * C * Dv * esz);
     L.dSo = take(units * (size_t)Dv * Dk * 4);
     L.dDb = take(units * C * Dv * esz);
@@ -196,6 +197,7 @@ int bwd_impl(bool varlen, int32_t B, int32_t T, int32_t N, const int32_t* cu, in
   p.wWt = w + L.wWt;
   p.wQgt = w + L.wQgt;
   p.wQt = w + L.wQt;
+  p.wM = w + L.wM;
   p.wdOt = w + L.wdOt;
   p.dO = d_o;
   p.dSfin = d_final_state;   // dO is read by the backward-mode preparation as well

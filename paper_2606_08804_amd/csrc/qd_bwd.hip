@@ -211,7 +211,7 @@ __global__ __launch_bounds__(NTHREADS) void k_scan_bwd(Params p) {
 // dbeta, dlambda and the decay gradient; the Dk direction is processed in
 // quarters of KH columns with the next quarter's q and k prefetched.
 template <typename E, int DK>
-struct BwdSmem {
+struct alignas(16) BwdSmem {
   static constexpr int P = Pad<E>::v;
   static constexpr int BV = 32;
   // bf16 operands need explicit transposed copies of dG and dQK for
@@ -219,6 +219,8 @@ struct BwdSmem {
   static constexpr bool TCOPY = sizeof(E) == 2;
   float b[C], g[C], kb[C], beta[C], lam[C], db[C], dbeta[C], dlam[C], tk[C];
   float sdot[NWAVES];
+  float dbc[NWAVES][C];     // per-wave column sums of dT (.) M
+  float ecc[NWAVES][C];     // per-wave column sums of the decay-gradient terms
   union {
     struct {
       E St[DK][BV + P];     // S^T tile (k, v)
@@ -232,14 +234,10 @@ struct BwdSmem {
       E dW[C][DK + P];      // dW = -dD S (r, k)
     } b1;
     struct {
-      float G[C][C + 4];
-      float QK[C][C + 4];
-      float dT[C][C + 4];
-      float A[C][C + 4];
-      float M[C][C + 4];
-      float Y[C][C + 4];
-      float tmp[4 * 16 * 17];
-    } c;
+      E MT[C][C + P];       // M^T (i, r)
+      E dMt[C][C + P];      // (dT diag(beta))^T (i, r)
+      E Y[C][C + P];        // M^T dT diag(beta) (r, i), rows private to their wave
+    } b2;
     struct {
       E dWt[DK][C + P];     // dW^T (k, r)
       E Kt[DK][C + P];      // K^T (k, r)
@@ -248,6 +246,7 @@ struct BwdSmem {
       E ok[C][DK + P];      // dk staging
     } b3;
   } u;
+  E Mm[C][C + P];           // M = (I + A)^{-1} (r, i)
   E TmT[C][C + P];          // T^T (i, r)
   E dG[C][C + P];           // dG (r, i)
   E dQK[C][C + P];          // dQK (r, i)
@@ -295,7 +294,7 @@ template <typename E, int DK, int DV>
 __global__ __launch_bounds__(NTHREADS) void k_bwd_intra(Params p) {
   constexpr int P = Pad<E>::v;
   constexpr int BV = 32;
-  constexpr int LC = C + P, LB = BV + P, LF = C + 4;
+  constexpr int LC = C + P, LB = BV + P;
   constexpr int KS = Mma<E>::KS;
   constexpr int NKB = DK / 16;        // 16-column blocks of Dk
   constexpr int NVT = DV / BV;
@@ -345,6 +344,7 @@ __global__ __launch_bounds__(NTHREADS) void k_bwd_intra(Params p) {
     pa.dD.load(dDg + (size_t)(16 * w) * DV + v0, DV, 16, lane);
   };
   TileRegs<E, C, DK> rKf, rQf;    // chunk K, Q rows for phase B1
+  TileRegs<E, C, C> rM, rT;       // M = (I + A)^{-1} and T^T from the preparation
   fetchA(0);
   for (int vt = 0; vt < NVT; ++vt) {
     const BwdPreA<E, DK> cur = pa;
@@ -353,6 +353,8 @@ __global__ __launch_bounds__(NTHREADS) void k_bwd_intra(Params p) {
     } else {
       rKf.load((const E*)p.k + arow * DK, (size_t)H * DK, len, tid);
       rQf.load((const E*)p.q + arow * DK, (size_t)H * DK, len, tid);
+      rM.load((const E*)p.wM + gi * C * C, C, C, tid);
+      rT.load((const E*)p.wT + gi * 2 * C * C, C, C, tid);
     }
     block_sync_lds();
     cur.S.store(&sm.u.a.St[0][0], LB, tid);
@@ -394,10 +396,13 @@ __global__ __launch_bounds__(NTHREADS) void k_bwd_intra(Params p) {
   block_sync_lds();
   rKf.store(&sm.u.b1.K[0][0], LKD, tid);
   rQf.store(&sm.u.b1.Q[0][0], LKD, tid);
+  rM.store(&sm.Mm[0][0], LC, tid);
+  rT.store(&sm.TmT[0][0], LC, tid);
 #pragma unroll
   for (int kb = 0; kb < NKB; ++kb)
 #pragma unroll
     for (int j = 0; j < 4; ++j) sm.u.b1.dW[16 * w + frow(lane, j)][kb * 16 + fcol(lane)] = fromf<E>(-aW[kb][j]);
+  if (tid < C) sm.kb[tid] = __expf(sm.b[C - 1] - sm.b[tid]);
   block_sync_lds();
   f4 aG[4], aQK[4], adT[4];
 #pragma unroll
@@ -431,113 +436,104 @@ __global__ __launch_bounds__(NTHREADS) void k_bwd_intra(Params p) {
   TileRegs<E, DK, C> rKt, rQt;
   rKt.load((const E*)p.wKt + gi * DK * C, C, DK, tid);
   rQt.load((const E*)p.wQt + gi * DK * C, C, DK, tid);
-  block_sync_lds();
 
-  // ---------------- phase B2: UT-solve backward and the C x C gradient terms
-#pragma unroll
-  for (int ib = 0; ib < 4; ++ib) {
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int r = 16 * w + frow(lane, j), c = ib * 16 + fcol(lane);
-      sm.u.c.G[r][c] = aG[ib][j];
-      sm.u.c.QK[r][c] = aQK[ib][j];
-      sm.u.c.dT[r][c] = aT[ib][j] + adT[ib][j];
-      sm.u.c.A[r][c] = (r > c) ? sm.beta[r] * __expf(sm.b[r] - sm.b[c]) * aG[ib][j] : 0.f;
-    }
-  }
-  if (tid < C) sm.kb[tid] = __expf(sm.b[C - 1] - sm.b[tid]);
-  block_sync_lds();
-  unit_lower_inverse(&sm.u.c.A[0][0], LF, &sm.u.c.M[0][0], LF, sm.u.c.tmp, tid);
-  const int q4 = tid >> 2, seg = (tid & 3) * 16;
+  // ---------------- phase B2: UT-solve backward and the C x C gradient terms.
+  // Lane (w, lane) holds element (r, c) = (16w + frow(lane, j), 16ib + fcol(lane))
+  // of every C x C accumulator.
+  const int rw = 16 * w + frow(lane, 0), cl = fcol(lane);
+  block_sync_lds();                    // K, Q, dW dead: the b2 buffers may be written
   {
-    float s4 = 0.f;
-#pragma unroll 4
-    for (int r = seg; r < seg + 16; ++r) s4 += sm.u.c.dT[r][q4] * sm.u.c.M[r][q4];
-    s4 += __shfl_xor(s4, 1, 64);
-    s4 += __shfl_xor(s4, 2, 64);
-    if ((tid & 3) == 0) sm.dbeta[q4] = s4;
-  }
-  for (int idx = tid; idx < C * C; idx += NTHREADS) {
-    const int r = idx % C, i = idx / C;
-    sm.TmT[i][r] = fromf<E>(sm.u.c.M[r][i] * sm.beta[i]);
-  }
-  block_sync_lds();
-  for (int idx = tid; idx < C * C; idx += NTHREADS) {
-    const int r = idx / C, i = idx % C;
-    sm.u.c.dT[r][i] *= sm.beta[i];          // dMinv = dT diag(beta)
-  }
-  block_sync_lds();
+    // dT = dD V^T + dW (g X)^T: column sums of dT (.) M feed dbeta; M^T and
+    // (dT diag(beta))^T become the operands of Y = M^T dT diag(beta)
 #pragma unroll
-  for (int ib = 0; ib < 4; ++ib) {            // Y = Minv^T dMinv
-    const f4 y = mma_k<E, C>(imaj(&sm.u.c.M[0][0], LF), imaj(&sm.u.c.dT[0][0], LF), 16 * w, ib * 16, zero4(), lane);
+    for (int ib = 0; ib < 4; ++ib) {
+      const int c = ib * 16 + cl;
+      const float bc = sm.beta[c];
+      f4 mv, dm;
+      float cs = 0.f;
 #pragma unroll
-    for (int j = 0; j < 4; ++j) sm.u.c.Y[16 * w + frow(lane, j)][ib * 16 + fcol(lane)] = y[j];
-  }
-  block_sync_lds();
-  // dP = dO D^T from phase A (rows 16w..) into the dead dMinv buffer
-#pragma unroll
-  for (int ib = 0; ib < 4; ++ib)
-#pragma unroll
-    for (int j = 0; j < 4; ++j) sm.u.c.dT[16 * w + frow(lane, j)][ib * 16 + fcol(lane)] = aP[ib][j];
-#pragma unroll
-  for (int ib = 0; ib < 4; ++ib) {            // dA = strictLower(-Y Minv^T)
-    const f4 y = mma_k<E, C>(kmaj(&sm.u.c.Y[0][0], LF), kmaj(&sm.u.c.M[0][0], LF), 16 * w, ib * 16, zero4(), lane);
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int r = 16 * w + frow(lane, j), c = ib * 16 + fcol(lane);
-      sm.u.c.A[r][c] = (r > c) ? -y[j] : 0.f;
-    }
-  }
-  block_sync_lds();
-  {
-    const int r = q4;
-    const float br = sm.b[r], betar = sm.beta[r];
-    float dbr = 0.f, er = 0.f;
-#pragma unroll 4
-    for (int i = seg; i < seg + 16; ++i) {
-      float dg = 0.f, dqk = 0.f;
-      if (i <= r) {
-        const float gam = __expf(br - sm.b[i]);
-        const float dA = sm.u.c.A[r][i];
-        const float Gv = sm.u.c.G[r][i];
-        const float dP = sm.u.c.dT[r][i];
-        dbr += dA * gam * Gv;
-        dg = dA * betar * gam;
-        dqk = dP * gam;
-        er += (dA * betar * Gv + dP * sm.u.c.QK[r][i]) * gam;
+      for (int j = 0; j < 4; ++j) {
+        const float m = tof(sm.Mm[rw + j][c]);
+        const float dt = aT[ib][j] + adT[ib][j];
+        cs += dt * m;
+        mv[j] = m;
+        dm[j] = dt * bc;
       }
-      sm.dG[r][i] = fromf<E>(dg);
-      sm.dQK[r][i] = fromf<E>(dqk);
+      *(typename Quad<E>::raw*)&sm.u.b2.MT[c][rw] = Quad<E>::pack(mv);
+      *(typename Quad<E>::raw*)&sm.u.b2.dMt[c][rw] = Quad<E>::pack(dm);
+      cs += __shfl_xor(cs, 16, 64);
+      cs += __shfl_xor(cs, 32, 64);
+      if (lane < 16) sm.dbc[w][c] = cs;
+    }
+  }
+  block_sync_lds();
+  f4 adA[4];
+  {
+#pragma unroll
+    for (int ib = 0; ib < 4; ++ib) {        // Y = M^T dMinv, rows 16w..
+      const f4 y = mma_k<E, C>(kmaj(&sm.u.b2.MT[0][0], LC), kmaj(&sm.u.b2.dMt[0][0], LC), 16 * w, ib * 16, zero4(), lane);
+#pragma unroll
+      for (int j = 0; j < 4; ++j) sm.u.b2.Y[rw + j][ib * 16 + cl] = fromf<E>(y[j]);
+    }
+    // Y rows 16w.. are read back by this wave only
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+#pragma unroll
+    for (int ib = 0; ib < 4; ++ib)          // dA = strictLower(-Y M^T)
+      adA[ib] = mma_k<E, C>(kmaj(&sm.u.b2.Y[0][0], LC), kmaj(&sm.Mm[0][0], LC), 16 * w, ib * 16, zero4(), lane);
+  }
+  {
+    // dG = diag(beta) dA (.) Gamma, dQK = dP (.) Gamma (causal, inclusive),
+    // the decay-gradient terms t = (dG (.) G + dQK (.) QK) and the rows of
+    // dbeta from A = strictLower(diag(beta) Gamma (.) G)
+    float br[4], betar[4], dbr[4] = {0.f, 0.f, 0.f, 0.f}, er[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      br[j] = sm.b[rw + j];
+      betar[j] = sm.beta[rw + j];
+    }
+#pragma unroll
+    for (int ib = 0; ib < 4; ++ib) {
+      const int c = ib * 16 + cl;
+      const float bc = sm.b[c];
+      f4 vg, vq;
+      float ec = 0.f;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int r = rw + j;
+        const float gam = (r >= c) ? __expf(br[j] - bc) : 0.f;
+        const float dA = (r > c) ? -adA[ib][j] : 0.f;
+        const float dAg = dA * gam;
+        const float dg = dAg * betar[j];
+        const float dqk = aP[ib][j] * gam;
+        const float t = dg * aG[ib][j] + dqk * aQK[ib][j];
+        dbr[j] += dAg * aG[ib][j];
+        er[j] += t;
+        ec += t;
+        vg[j] = dg;
+        vq[j] = dqk;
+        sm.dG[r][c] = fromf<E>(dg);
+        sm.dQK[r][c] = fromf<E>(dqk);
+      }
       if constexpr (BwdSmem<E, DK>::TCOPY) {
-        sm.dGt[i][r] = fromf<E>(dg);
-        sm.dQKt[i][r] = fromf<E>(dqk);
+        *(typename Quad<E>::raw*)&sm.dGt[c][rw] = Quad<E>::pack(vg);
+        *(typename Quad<E>::raw*)&sm.dQKt[c][rw] = Quad<E>::pack(vq);
+      }
+      ec += __shfl_xor(ec, 16, 64);
+      ec += __shfl_xor(ec, 32, 64);
+      if (lane < 16) sm.ecc[w][c] = ec;
+    }
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      dbr[j] = sum16(dbr[j]);
+      er[j] = sum16(er[j]);
+    }
+    if (cl == 0) {
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        sm.dbeta[rw + j] = dbr[j];
+        sm.db[rw + j] = er[j];
       }
     }
-    dbr += __shfl_xor(dbr, 1, 64);
-    dbr += __shfl_xor(dbr, 2, 64);
-    er += __shfl_xor(er, 1, 64);
-    er += __shfl_xor(er, 2, 64);
-    block_sync_lds();
-    if ((tid & 3) == 0) {
-      sm.dbeta[r] += dbr;
-      sm.db[r] = er;
-    }
-  }
-  block_sync_lds();
-  {
-    const int i = q4;
-    const float bi = sm.b[i];
-    float ec = 0.f;
-#pragma unroll 4
-    for (int r = seg; r < seg + 16; ++r) {
-      if (r >= i) {
-        const float gam = __expf(sm.b[r] - bi);
-        ec += (sm.u.c.A[r][i] * sm.beta[r] * sm.u.c.G[r][i] + sm.u.c.dT[r][i] * sm.u.c.QK[r][i]) * gam;
-      }
-    }
-    ec += __shfl_xor(ec, 1, 64);
-    ec += __shfl_xor(ec, 2, 64);
-    if ((tid & 3) == 0) sm.db[i] -= ec;
   }
   block_sync_lds();
 
@@ -642,13 +638,19 @@ __global__ __launch_bounds__(NTHREADS) void k_bwd_intra(Params p) {
 #pragma unroll
     for (int off = 32; off >= 1; off >>= 1) tot += __shfl_xor(tot, off, 64);
     float dbj = sm.db[j] - sm.tk[j];
+    float dbeta = sm.dbeta[j];
+#pragma unroll
+    for (int v = 0; v < NWAVES; ++v) {
+      dbj -= sm.ecc[v][j];
+      dbeta += sm.dbc[v][j];
+    }
     if (j == C - 1) dbj += tot + sm.g[C - 1] * (sm.sdot[0] + sm.sdot[1] + sm.sdot[2] + sm.sdot[3]);
     float x = __shfl(dbj, C - 1 - j, 64);
     x = wave_incl_scan(x, lane);
     const float suffix = __shfl(x, C - 1 - j, 64);
     if (j < len) {
       const size_t gt = arow + (size_t)j * H;
-      p.dbeta[gt] = sm.dbeta[j];
+      p.dbeta[gt] = dbeta;
       p.dlam[gt] = sm.dlam[j];
       if (p.dla) p.dla[gt] = suffix;
     }

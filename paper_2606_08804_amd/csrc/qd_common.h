@@ -335,6 +335,7 @@ struct Params {
   void* wWt;             // [slot][H][Dk][C]  W^T (backward only)
   void* wQgt;            // [slot][H][Dk][C]  (diag(g) Q)^T (backward only)
   void* wQt;             // [slot][H][Dk][C]  Q^T (backward only)
+  void* wM;              // [slot][H][C][C]   (I + A)^{-1} (backward only)
   void* wdOt;            // [slot][H][Dv][C]  dO^T (backward only)
   // backward
   const void* dO;

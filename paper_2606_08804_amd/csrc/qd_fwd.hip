@@ -187,12 +187,38 @@ __global__ __launch_bounds__(PREP_THREADS) void k_prep(Params p) {
 
     // UT solve: M = (I + A)^{-1}, T = M diag(beta)
     unit_lower_inverse<NT>(&sm.A[0][0], C + 4, &sm.M[0][0], C + 4, sm.tmp, tid);
-    E* wTt = BWD ? (E*)p.wT + gi * 2 * C * C : nullptr;
-    for (int idx = tid; idx < C * C; idx += NT) {
-      const int r = idx / C, i = idx % C;
-      const E tv = fromf<E>(sm.M[r][i] * sm.beta[i]);
-      sm.Tm[r][i] = tv;
-      if (BWD) wTt[i * C + r] = tv;     // T^T for the backward scan's dV = T^T dD
+    {
+      // T row-major into LDS (and M into the workspace in backward mode);
+      // a thread takes VEC consecutive columns of one row
+      constexpr int VEC = 16 / sizeof(E);
+      E* wM = BWD ? (E*)p.wM + gi * C * C : nullptr;
+      for (int idx = tid; idx < C * C / VEC; idx += NT) {
+        const int r = idx / (C / VEC), i0 = (idx % (C / VEC)) * VEC;
+        uint4 tr, mr;
+        E* te = (E*)&tr;
+        E* me = (E*)&mr;
+#pragma unroll
+        for (int j = 0; j < VEC; ++j) {
+          const float m = sm.M[r][i0 + j];
+          te[j] = fromf<E>(m * sm.beta[i0 + j]);
+          me[j] = fromf<E>(m);
+        }
+        *(uint4*)&sm.Tm[r][i0] = tr;
+        if (BWD) *(uint4*)(wM + r * C + i0) = mr;
+      }
+      if (BWD) {
+        // T^T for the backward kernels: VEC consecutive rows of one column
+        E* wTt = (E*)p.wT + gi * 2 * C * C;
+        for (int idx = tid; idx < C * C / VEC; idx += NT) {
+          const int i = idx % C, r0 = (idx / C) * VEC;
+          const float bi = sm.beta[i];
+          uint4 tr;
+          E* te = (E*)&tr;
+#pragma unroll
+          for (int j = 0; j < VEC; ++j) te[j] = fromf<E>(sm.M[r0 + j][i] * bi);
+          *(uint4*)(wTt + i * C + r0) = tr;
+        }
+      }
     }
     // V^T (K, Q, X are dead: all reads of them finished before the solve's barriers)
     x.V.storeT(&sm.u.Vt[0][0], LC, tid);
