@@ -411,29 +411,33 @@ __device__ inline float sum16(float x) {
 }
 
 // ----------------------------------------------------------------- UT solve
-// In-place-free inverse of the unit lower-triangular C x C matrix I + A,
-// A strictly lower, fp32, A at sA[r*lda + i].  Writes Minv = (I + A)^{-1} to
-// sM[r*ldm + i] (upper part zero).  `tmp` is scratch of >= 4*16*17 floats.
-// Diagonal 16x16 blocks by forward substitution (one lane per column), then
-// the off-diagonal blocks by increasing block distance,
-//   Minv_ij = - Minv_ii * sum_{m=j}^{i-1} A_im Minv_mj,
-// with fp32 MFMA products.  Must be called by all threads of the block.
-template <int NT = NTHREADS>
-__device__ inline void unit_lower_inverse(const float* sA, int lda, float* sM, int ldm,
-                                          float* tmp, int tid) {
-  static_assert(NT >= 256, "needs at least four waves");
+// Inverse of the unit lower-triangular C x C matrix I + A (the UT transform
+// of the delta-rule chunk form), A strictly lower, fp32, at sA[r*lda + i].
+// Writes M = (I + A)^{-1} to sM[r*ldm + i] for the 16 x 16 blocks on and
+// below the diagonal; the strictly-upper blocks of sM are left untouched and
+// callers treat them as zero.  sA is overwritten.  Called by all threads of
+// an eight-wave workgroup.
+//  1. diagonal blocks M_jj = (I + A_jj)^{-1} by forward substitution (one
+//     lane per column, row sums split four ways to shorten the FMA chain);
+//  2. A~_mj = A_mj M_jj for the six blocks below the diagonal, in place;
+//  3. from M L = I: M_ij = -sum_{m=j+1..i} M_im A~_mj, by block distance
+//     i - j, one fp32 MFMA product per wave and level (products that need
+//     only the diagonal blocks start at the first level).
+template <int NT>
+__device__ inline void unit_lower_inverse(float* sA, int lda, float* sM, int ldm, int tid) {
+  static_assert(NT == 512, "eight waves");
   const int lane = tid & 63, w = tid >> 6;
-  // zero the strictly-upper blocks
-  for (int idx = tid; idx < C * C; idx += NT) {
-    const int r = idx / C, i = idx % C;
-    if ((i >> 4) > (r >> 4)) sM[r * ldm + i] = 0.f;
-  }
-  if (lane < 16 && w < 4) {
-    // forward substitution for column j of the inverse of diagonal block w;
-    // row r of the block is read as four broadcast 16-byte loads, one row
-    // ahead of its use, so the dependent FMA chain runs from registers
-    const int base = w * 16, j = lane;
-    const float* blk = sA + (size_t)base * lda + base;
+  auto blkA = [&](int i, int j) { return sA + (size_t)(16 * i) * lda + 16 * j; };
+  auto blkM = [&](int i, int j) { return sM + (size_t)(16 * i) * ldm + 16 * j; };
+  auto put = [&](float* dst, int ld, f4 v, float sc) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) dst[frow(lane, j) * ld + fcol(lane)] = sc * v[j];
+  };
+  if (w < 4 && lane < 16) {
+    // column j of (I + A_ww)^{-1}; row r of the block is read as four
+    // broadcast 16-byte loads one row ahead of its use
+    const int j = lane;
+    const float* blk = blkA(w, w);
     float m[16];
     f4 cur[4], nxt[4];
 #pragma unroll
@@ -445,40 +449,49 @@ __device__ inline void unit_lower_inverse(const float* sA, int lda, float* sM, i
 #pragma unroll
         for (int q = 0; q < 4; ++q) nxt[q] = *(const f4*)(blk + (size_t)(r + 1) * lda + 4 * q);
       }
-      float s = (r == j) ? 1.f : 0.f;
+      float s4[4] = {(r == j) ? 1.f : 0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-      for (int i = 0; i < r; ++i) s -= cur[i >> 2][i & 3] * m[i];
-      m[r] = s;
+      for (int i = 0; i < r; ++i) s4[i & 3] -= cur[i >> 2][i & 3] * m[i];
+      m[r] = (s4[0] + s4[1]) + (s4[2] + s4[3]);
 #pragma unroll
       for (int q = 0; q < 4; ++q) cur[q] = nxt[q];
     }
+    float* out = blkM(w, w);
 #pragma unroll
-    for (int r = 0; r < 16; ++r) sM[(base + r) * ldm + base + j] = m[r];
+    for (int r = 0; r < 16; ++r) out[r * ldm + j] = m[r];
   }
-  __syncthreads();
-  float* X = tmp + w * (16 * 17);
-  for (int d = 1; d < 4; ++d) {
-    const int nb = 4 - d;            // blocks at this distance
-    if (w < nb) {
-      const int bj = w, bi = w + d;
-      f4 acc = zero4();
-      for (int m = bj; m < bi; ++m)
-        acc = mma_k<float, 16>(kmaj(sA + bi * 16 * lda + m * 16, lda),
-                               imaj(sM + m * 16 * ldm + bj * 16, ldm), 0, 0, acc, lane);
-#pragma unroll
-      for (int j = 0; j < 4; ++j) X[frow(lane, j) * 17 + fcol(lane)] = acc[j];
-      // same wave wrote X; wave-level barrier is enough but keep block-uniform flow
-    }
-    __syncthreads();
-    if (w < nb) {
-      const int bj = w, bi = w + d;
-      f4 acc = zero4();
-      acc = mma_k<float, 16>(kmaj(sM + bi * 16 * ldm + bi * 16, ldm), imaj(X, 17), 0, 0, acc, lane);
-#pragma unroll
-      for (int j = 0; j < 4; ++j) sM[(bi * 16 + frow(lane, j)) * ldm + bj * 16 + fcol(lane)] = -acc[j];
-    }
-    __syncthreads();
+  block_sync_lds();
+  // wave -> (m, j) of A~_mj: (1,0) (2,1) (3,2) (2,0) (3,1) (3,0)
+  const int bm = (w < 3) ? w + 1 : (w == 3 ? 2 : 3);
+  const int bj = (w < 3) ? w : (w == 4 ? 1 : 0);
+  if (w < 6) {
+    const f4 t = mma_k<float, 16>(kmaj(blkA(bm, bj), lda), imaj(blkM(bj, bj), ldm), 0, 0, zero4(), lane);
+    put(blkA(bm, bj), lda, t, 1.f);
   }
+  block_sync_lds();
+  // level 1: M_10, M_21, M_32 (waves 0-2) and the partial sums of M_20, M_31,
+  // M_30 that use diagonal blocks only (waves 3-5)
+  f4 part = zero4();
+  if (w < 6) {
+    const int bi = (w < 3) ? w + 1 : (w == 3 ? 2 : 3);   // M_{bi,bi} A~_{bm,bj}
+    part = mma_k<float, 16>(kmaj(blkM(bi, bi), ldm), imaj(blkA(bm, bj), lda), 0, 0, part, lane);
+    if (w < 3) put(blkM(bm, bj), ldm, part, -1.f);
+  }
+  block_sync_lds();
+  // level 2: M_20 += M_21 A~_10, M_31 += M_32 A~_21, and M_30 += M_32 A~_20
+  if (w >= 3 && w < 6) {
+    const int li = (w == 3) ? 2 : 3, lm = (w == 3) ? 1 : 2;     // M_{li,lm}
+    const int ai = (w == 3) ? 1 : 2, aj = (w == 5) ? 0 : ai - 1; // A~_{lm,aj}
+    part = mma_k<float, 16>(kmaj(blkM(li, lm), ldm), imaj(blkA(ai, aj), lda), 0, 0, part, lane);
+    if (w < 5) put(blkM(li, aj), ldm, part, -1.f);
+  }
+  block_sync_lds();
+  // level 3: M_30 += M_31 A~_10
+  if (w == 5) {
+    part = mma_k<float, 16>(kmaj(blkM(3, 1), ldm), imaj(blkA(1, 0), lda), 0, 0, part, lane);
+    put(blkM(3, 0), ldm, part, -1.f);
+  }
+  block_sync_lds();
 }
 
 // Inclusive prefix sum of 64 values held one per lane of wave 0 (lane < 64).

@@ -41,7 +41,6 @@ struct PrepSmem {
   E GXt[DK][C + P];
   float A[C][C + 4];
   float M[C][C + 4];
-  float tmp[4 * 16 * 17];
   E Tm[C][C + P];
 };
 
@@ -122,7 +121,7 @@ __global__ __launch_bounds__(PREP_THREADS) void k_prep(Params p) {
     if (!x.valid) continue;                 // uniform across the workgroup
     const int h = x.h;
     const size_t gi = (size_t)x.g * H + h;
-    __syncthreads();                        // previous unit's LDS use is over
+    block_sync_lds();                        // previous unit's LDS use is over
     x.K.store(&sm.u.a.K[0][0], LK, tid);
     x.Q.store(&sm.u.a.Q[0][0], LK, tid);
     if (tid < C) {
@@ -132,7 +131,7 @@ __global__ __launch_bounds__(PREP_THREADS) void k_prep(Params p) {
       sm.lam[tid] = x.lam;
       p.wb[gi * C + tid] = b;
     }
-    __syncthreads();
+    block_sync_lds();
 
     // transposed copies for the scans: K^T, and (diag(g) Q)^T for the backward
     store_transposed<E, DK, NT>((E*)p.wKt + gi * DK * C, &sm.u.a.K[0][0], LK, tid, One());
@@ -163,7 +162,7 @@ __global__ __launch_bounds__(PREP_THREADS) void k_prep(Params p) {
         *(uint4*)&sm.u.a.X[r][c0] = xr;
       }
     }
-    __syncthreads();
+    block_sync_lds();
 
     // Gram products X K^T and Q K^T; A (fp32, LDS) and P or P^T (workspace)
     E* wP = BWD ? (E*)p.wT + gi * 2 * C * C + C * C : (E*)p.wP + gi * C * C;
@@ -183,10 +182,10 @@ __global__ __launch_bounds__(PREP_THREADS) void k_prep(Params p) {
       if (BWD)
         *(typename Quad<E>::raw*)(wP + (n0 + fcol(lane)) * C + m0 + frow(lane, 0)) = Quad<E>::pack(pv);
     }
-    __syncthreads();
+    block_sync_lds();
 
     // UT solve: M = (I + A)^{-1}, T = M diag(beta)
-    unit_lower_inverse<NT>(&sm.A[0][0], C + 4, &sm.M[0][0], C + 4, sm.tmp, tid);
+    unit_lower_inverse<NT>(&sm.A[0][0], C + 4, &sm.M[0][0], C + 4, tid);
     {
       // T row-major into LDS (and M into the workspace in backward mode);
       // a thread takes VEC consecutive columns of one row
@@ -194,12 +193,13 @@ __global__ __launch_bounds__(PREP_THREADS) void k_prep(Params p) {
       E* wM = BWD ? (E*)p.wM + gi * C * C : nullptr;
       for (int idx = tid; idx < C * C / VEC; idx += NT) {
         const int r = idx / (C / VEC), i0 = (idx % (C / VEC)) * VEC;
+        const bool upper = (i0 >> 4) > (r >> 4);   // strictly-upper block: zero
         uint4 tr, mr;
         E* te = (E*)&tr;
         E* me = (E*)&mr;
 #pragma unroll
         for (int j = 0; j < VEC; ++j) {
-          const float m = sm.M[r][i0 + j];
+          const float m = upper ? 0.f : sm.M[r][i0 + j];
           te[j] = fromf<E>(m * sm.beta[i0 + j]);
           me[j] = fromf<E>(m);
         }
@@ -215,14 +215,14 @@ __global__ __launch_bounds__(PREP_THREADS) void k_prep(Params p) {
           uint4 tr;
           E* te = (E*)&tr;
 #pragma unroll
-          for (int j = 0; j < VEC; ++j) te[j] = fromf<E>(sm.M[r0 + j][i] * bi);
+          for (int j = 0; j < VEC; ++j) te[j] = fromf<E>(((i >> 4) > ((r0 + j) >> 4)) ? 0.f : sm.M[r0 + j][i] * bi);
           *(uint4*)(wTt + i * C + r0) = tr;
         }
       }
     }
     // V^T (K, Q, X are dead: all reads of them finished before the solve's barriers)
     x.V.storeT(&sm.u.Vt[0][0], LC, tid);
-    __syncthreads();
+    block_sync_lds();
 
     // U = T V, stored C-fragment tiled: tile (mt, nt) at ((mt*(DV/16)+nt)*64 + lane)*4
     E* wU = (E*)p.wU + gi * C * DV;
@@ -244,9 +244,9 @@ __global__ __launch_bounds__(PREP_THREADS) void k_prep(Params p) {
     }
     if constexpr (BWD) {
       // dO^T for the backward scan's fragment loads
-      __syncthreads();
+      block_sync_lds();
       x.dO.store(&sm.u.dO[0][0], DV + P, tid);
-      __syncthreads();
+      block_sync_lds();
       store_transposed<E, DV, NT>((E*)p.wdOt + gi * DV * C, &sm.u.dO[0][0], DV + P, tid, One());
     }
   }
