@@ -47,7 +47,7 @@ Layout make_layout(size_t units, int Dk, int Dv, int esz, bool bwd) {
     L.wQt = take(units * C * Dk * esz);
     L.wM = take(units * C * C * esz);
     L.wdOt = take(units * C * Dv * esz);
-    L.dSo = take(units * (size_t)Dv * Dk * 4);
+    L.dSo = take(units * (size_t)Dv * Dk * esz);
     L.dDb = take(units * C * Dv * esz);
     L.states = take(saved_total_bytes(units, Dk, Dv, esz));
   }
@@ -203,7 +203,7 @@ int bwd_impl(bool varlen, int32_t B, int32_t T, int32_t N, const int32_t* cu, in
   p.dSfin = d_final_state;   // dO is read by the backward-mode preparation as well
   p.dq = dq; p.dk = dk; p.dv = dv;
   p.dbeta = dbeta; p.dlam = dlam; p.dla = dlog_alpha; p.dS0 = d_initial_state;
-  p.w_dSo = reinterpret_cast<float*>(w + L.dSo);
+  p.w_dSo = w + L.dSo;
   p.w_dDb = w + L.dDb;
   const size_t units = s.slots * (size_t)H;
   hipError_t e;

@@ -41,6 +41,7 @@ struct ScanBwdSmem {
   E dDn[BV][C + P];   // -dD tile, transposed [v][r]
   E dDr[C][BV + P];   // dD tile staging [r][v]
   E dV[C][BV + P];    // dV tile staging [i][v]
+  float Sf[DK][BV + 4];  // fp32 dS' tile staging [k][v]
 };
 
 // Operands of one chunk for one wave of the backward scan, prefetched from
@@ -122,11 +123,24 @@ __global__ __launch_bounds__(NTHREADS) void k_scan_bwd(Params p) {
       for (int nb = 0; nb < NB; ++nb) {
         const int kt = KPW * w + i;
         *(QR*)&sm.dS[nb * 16 + fcol(lane)][kt * 16 + frow(lane, 0)] = Quad<E>::pack(acc[i][nb]);
-        float* dst = p.w_dSo + (gi * DK + kt * 16 + frow(lane, 0)) * DV + v0 + nb * 16 + fcol(lane);
 #pragma unroll
-        for (int j = 0; j < 4; ++j) dst[(size_t)j * DV] = acc[i][nb][j];
+        for (int j = 0; j < 4; ++j) sm.Sf[kt * 16 + frow(lane, j)][nb * 16 + fcol(lane)] = acc[i][nb][j];
       }
     block_sync_lds();
+    {
+      // dS' of this chunk for the intra-chunk kernel, transposed ([k][v]) in
+      // the activation dtype (its consumer is an MFMA operand), 16-byte stores
+      constexpr int VEC = 16 / sizeof(E);
+      E* dst = (E*)p.w_dSo + gi * DK * DV + v0;
+      for (int idx = tid; idx < DK * (BV / VEC); idx += NTHREADS) {
+        const int r = idx / (BV / VEC), c0 = (idx % (BV / VEC)) * VEC;
+        uint4 o;
+        E* oe = (E*)&o;
+#pragma unroll
+        for (int j = 0; j < VEC; ++j) oe[j] = fromf<E>(sm.Sf[r][c0 + j]);
+        *(uint4*)(dst + (size_t)r * DV + c0) = o;
+      }
+    }
     if (c > 0) prefetch(c - 1);
     const float bl = sm.b[C - 1];
     // dD = P^T dO + diag(g_C/g) K dS'^T   (rows 16w..)
@@ -202,18 +216,31 @@ __global__ __launch_bounds__(NTHREADS) void k_scan_bwd(Params p) {
 // ------------------------------------------------------------------ intra
 // Fused intra-chunk backward, one workgroup per (chunk, head) unit.
 //
-// Phase A walks the value dimension in tiles of 32 columns (next tile
-// prefetched into registers) and accumulates, for rows 16w.. of wave w,
-//   aQ = dO S,  aK = D dS',  aW = dD S   (C x Dk)   and   aP = dO D^T, aT = dD V^T (C x C)
-// with dO, D, dD fragments loaded straight from global memory and the S^T,
-// dS'^T, D and V tiles shared through LDS.  Phase B recomputes the Gram
-// products and the UT solve, back-propagates through it, and produces dq, dk,
-// dbeta, dlambda and the decay gradient; the Dk direction is processed in
-// quarters of KH columns with the next quarter's q and k prefetched.
+// Phase A walks the value dimension in tiles of 32 columns, streamed into LDS
+// by direct global->LDS loads through a ring of three tiles (two in flight
+// while one is consumed), and accumulates, for rows 16w.. of wave w,
+//   aQ = dO S,  aK = D dS',  aW = dD S   (C x Dk)   and   aP = dO D^T, aT = dD V^T (C x C).
+// Phase B1 forms the Gram products G = X K^T, Q K^T and the second part of
+// dT; B2 back-propagates through the UT solve with the saved (I + A)^{-1} and
+// forms dG, dQK and the beta and decay terms in MFMA-layout registers; B3
+// produces dX, dq and dk.  The tail turns the decay terms into d log alpha.
+
+// Phase-A tile of 32 value columns: S^T (fp32), dS'^T, D, V, dO, dD, each in
+// the swizzled direct-load layout; a ring of NBUF tiles keeps two in flight.
+template <typename E, int DK>
+struct TileA {
+  static constexpr int BV = 32;
+  static constexpr int RS = BV * 4;                 // S^T row bytes
+  static constexpr int RE = BV * (int)sizeof(E);    // row bytes of the dtype tiles
+  static constexpr int S = 0, DS = S + DK * RS, D = DS + DK * RE, V = D + C * RE, DO = V + C * RE,
+                       DD = DO + C * RE, BYTES = DD + C * RE;
+  static constexpr int NBUF = sizeof(E) == 2 ? 3 : 2;   // fp32 tiles are twice as large
+  static constexpr int LOADS = BYTES / 1024 / NWAVES;   // direct loads per wave and tile
+};
+
 template <typename E, int DK>
 struct alignas(16) BwdSmem {
   static constexpr int P = Pad<E>::v;
-  static constexpr int BV = 32;
   // bf16 operands need explicit transposed copies of dG and dQK for
   // contiguous fragment loads; fp32 fragments are single scalars either way
   static constexpr bool TCOPY = sizeof(E) == 2;
@@ -222,36 +249,37 @@ struct alignas(16) BwdSmem {
   float dbc[NWAVES][C];     // per-wave column sums of dT (.) M
   float ecc[NWAVES][C];     // per-wave column sums of the decay-gradient terms
   union {
+    alignas(16) char tiles[TileA<E, DK>::NBUF][TileA<E, DK>::BYTES];   // phase A
     struct {
-      E St[DK][BV + P];     // S^T tile (k, v)
-      E dSt[DK][BV + P];    // dS'^T tile (k, v)
-      E D[C][BV + P];       // D tile (r, v)
-      E V[C][BV + P];       // V tile (r, v)
-    } a;
-    struct {
-      E K[C][DK + P];       // chunk keys (r, k)
-      E Q[C][DK + P];       // chunk queries (r, k)
-      E dW[C][DK + P];      // dW = -dD S (r, k)
-    } b1;
-    struct {
-      E MT[C][C + P];       // M^T (i, r)
-      E dMt[C][C + P];      // (dT diag(beta))^T (i, r)
-      E Y[C][C + P];        // M^T dT diag(beta) (r, i), rows private to their wave
-    } b2;
-    struct {
-      E dWt[DK][C + P];     // dW^T (k, r)
-      E Kt[DK][C + P];      // K^T (k, r)
-      E Qt[DK][C + P];      // Q^T (k, r)
-      E oq[C][DK + P];      // dq staging
-      E ok[C][DK + P];      // dk staging
-    } b3;
-  } u;
-  E Mm[C][C + P];           // M = (I + A)^{-1} (r, i)
-  E TmT[C][C + P];          // T^T (i, r)
-  E dG[C][C + P];           // dG (r, i)
-  E dQK[C][C + P];          // dQK (r, i)
-  typename std::conditional<TCOPY, E[C][C + P], char[16]>::type dGt;    // dG^T (i, r)
-  typename std::conditional<TCOPY, E[C][C + P], char[16]>::type dQKt;   // dQK^T (i, r)
+      union {
+        struct {
+          E K[C][DK + P];       // chunk keys (r, k)
+          E Q[C][DK + P];       // chunk queries (r, k)
+          E dW[C][DK + P];      // dW = -dD S (r, k)
+        } b1;
+        struct {
+          E MT[C][C + P];       // M^T (i, r)
+          E dMt[C][C + P];      // (dT diag(beta))^T (i, r)
+          E Y[C][C + P];        // M^T dT diag(beta) (r, i), rows private to their wave
+        } b2;
+        struct {
+          E dWt[DK][C + P];     // dW^T (k, r)
+          E Kt[DK][C + P];      // K^T (k, r)
+          E Qt[DK][C + P];      // Q^T (k, r)
+          E oq[C][DK + P];      // dq staging
+          E ok[C][DK + P];      // dk staging
+        } b3;
+      } u;
+      E dG[C][C + P];           // dG (r, i)
+      E dQK[C][C + P];          // dQK (r, i)
+      typename std::conditional<TCOPY, E[C][C + P], char[16]>::type dGt;    // dG^T (i, r)
+      typename std::conditional<TCOPY, E[C][C + P], char[16]>::type dQKt;   // dQK^T (i, r)
+    } s;
+  } x;
+  // M = (I + A)^{-1} (r, i) and T^T (i, r), direct-loaded at the start (swizzled
+  // rows of C elements, outside the phase-A ring)
+  alignas(16) char Mm[C * C * sizeof(E)];
+  alignas(16) char TmT[C * C * sizeof(E)];
 };
 
 // s * (k + l * q) element-wise on one fragment, rounded to the operand type
@@ -283,18 +311,11 @@ __device__ inline float mix_tokens<float>(float kf, float qf, const float* lam) 
   return kf + lam[0] * qf;
 }
 
-template <typename E, int DK>
-struct BwdPreA {
-  TileRegsF<E, DK, 32> S, dS;   // S^T, dS'^T tiles (fp32 in memory)
-  TileRegs<E, C, 32> D, V;
-  AFrag<E, 32> dO, Df, dD;      // rows 16w.. of dO, D, dD over the tile's columns
-};
-
 template <typename E, int DK, int DV>
 __global__ __launch_bounds__(NTHREADS) void k_bwd_intra(Params p) {
   constexpr int P = Pad<E>::v;
   constexpr int BV = 32;
-  constexpr int LC = C + P, LB = BV + P;
+  constexpr int LC = C + P;
   constexpr int KS = Mma<E>::KS;
   constexpr int NKB = DK / 16;        // 16-column blocks of Dk
   constexpr int NVT = DV / BV;
@@ -307,101 +328,111 @@ __global__ __launch_bounds__(NTHREADS) void k_bwd_intra(Params p) {
   const size_t gi = (size_t)g * H + h;
   const size_t arow = (size_t)t0 * H + h;   // first activation row of the chunk
 
-  if (tid < C) {
-    const bool ok = tid < len;
-    const size_t gt = arow + (size_t)tid * H;
-    const float b = p.wb[gi * C + tid];
-    sm.b[tid] = b;
-    sm.g[tid] = __expf(b);
-    sm.beta[tid] = ok ? p.beta[gt] : 0.f;
-    sm.lam[tid] = ok ? p.lam[gt] : 0.f;
-    sm.dlam[tid] = 0.f;
-    sm.tk[tid] = 0.f;
-  }
+  // gate loads first (branch-free: rows past the chunk re-read its last row)
+  const int ti = tid & (C - 1);
+  const size_t gtc = arow + (size_t)min(ti, len - 1) * H;
+  const float gb = p.wb[gi * C + ti], gbeta = p.beta[gtc], glam = p.lam[gtc];
 
   // ---------------- phase A: contractions over the value dimension
+  typedef TileA<E, DK> TA;
   f4 aQ[NKB], aK[NKB], aW[NKB], aP[4], aT[4];
 #pragma unroll
   for (int i = 0; i < NKB; ++i) aQ[i] = aK[i] = aW[i] = zero4();
 #pragma unroll
   for (int i = 0; i < 4; ++i) aP[i] = aT[i] = zero4();
   float sdot = 0.f;
-  const float* Sg = p.saved + gi * DK * DV;
-  const float* dSg = p.w_dSo + gi * DK * DV;
-  const E* Dg = (const E*)p.savedD + gi * C * DV;
-  const E* dDg = (const E*)p.w_dDb + gi * C * DV;
-  const E* dOg = (const E*)p.dO + arow * DV;
-  const E* Vg = (const E*)p.v + arow * DV;
-  BwdPreA<E, DK> pa;
-  auto fetchA = [&](int vt) {
-    const int v0 = vt * BV;
-    pa.S.load(Sg + v0, DV, tid);
-    pa.dS.load(dSg + v0, DV, tid);
-    pa.D.load(Dg + v0, DV, C, tid);
-    pa.V.load(Vg + v0, (size_t)H * DV, len, tid);
-    pa.dO.load(dOg + (size_t)(16 * w) * H * DV + v0, (size_t)H * DV, len - 16 * w, lane);
-    pa.Df.load(Dg + (size_t)(16 * w) * DV + v0, DV, 16, lane);
-    pa.dD.load(dDg + (size_t)(16 * w) * DV + v0, DV, 16, lane);
-  };
+  constexpr size_t ES = sizeof(E);
+  const char* Sg = (const char*)(p.saved + gi * DK * DV);
+  const char* dSg = (const char*)((const E*)p.w_dSo + gi * DK * DV);
+  const char* Dg = (const char*)((const E*)p.savedD + gi * C * DV);
+  const char* dDg = (const char*)((const E*)p.w_dDb + gi * C * DV);
+  const char* dOg = (const char*)((const E*)p.dO + arow * DV);
+  const char* Vg = (const char*)((const E*)p.v + arow * DV);
+  // phase-B operands first, so that they are older than every tile load
   TileRegs<E, C, DK> rKf, rQf;    // chunk K, Q rows for phase B1
-  TileRegs<E, C, C> rM, rT;       // M = (I + A)^{-1} and T^T from the preparation
-  fetchA(0);
+  rKf.load_clamped((const E*)p.k + arow * DK, (size_t)H * DK, len, tid);
+  rQf.load_clamped((const E*)p.q + arow * DK, (size_t)H * DK, len, tid);
+  asm volatile("" ::: "memory");
+  // M = (I + A)^{-1} and T^T from the preparation
+  constexpr int RBC = C * (int)sizeof(E);
+  {
+    const char* Mg = (const char*)((const E*)p.wM + gi * C * C);
+    const char* Tg = (const char*)((const E*)p.wT + gi * 2 * C * C);
+    dma_rows<RBC, C>(sm.Mm, Mg, RBC, C, Mg, 0, w, lane);
+    dma_rows<RBC, C>(sm.TmT, Tg, RBC, C, Tg, 0, w, lane);
+  }
+  // rows of V and dO past the chunk come from D, whose rows there are zero
+  auto issue = [&](int vt) {
+    char* t = &sm.x.tiles[vt % TA::NBUF][0];
+    const size_t vb = (size_t)vt * BV;
+    dma_rows<TA::RS, DK>(t + TA::S, Sg + vb * 4, DV * 4, DK, Sg, 0, w, lane);
+    dma_rows<TA::RE, DK>(t + TA::DS, dSg + vb * ES, DV * ES, DK, dSg, 0, w, lane);
+    dma_rows<TA::RE, C>(t + TA::D, Dg + vb * ES, DV * ES, C, Dg, 0, w, lane);
+    dma_rows<TA::RE, C>(t + TA::DD, dDg + vb * ES, DV * ES, C, dDg, 0, w, lane);
+    dma_rows<TA::RE, C>(t + TA::V, Vg + vb * ES, (size_t)H * DV * ES, len, Dg + vb * ES, DV * ES, w, lane);
+    dma_rows<TA::RE, C>(t + TA::DO, dOg + vb * ES, (size_t)H * DV * ES, len, Dg + vb * ES, DV * ES, w, lane);
+  };
+  constexpr int NB0 = NVT < TA::NBUF ? NVT : TA::NBUF;
+#pragma unroll
+  for (int vt = 0; vt < NB0; ++vt) issue(vt);
+#pragma unroll
   for (int vt = 0; vt < NVT; ++vt) {
-    const BwdPreA<E, DK> cur = pa;
-    if (vt + 1 < NVT) {
-      fetchA(vt + 1);
-    } else {
-      rKf.load((const E*)p.k + arow * DK, (size_t)H * DK, len, tid);
-      rQf.load((const E*)p.q + arow * DK, (size_t)H * DK, len, tid);
-      rM.load((const E*)p.wM + gi * C * C, C, C, tid);
-      rT.load((const E*)p.wT + gi * 2 * C * C, C, C, tid);
-    }
-    block_sync_lds();
-    cur.S.store(&sm.u.a.St[0][0], LB, tid);
-    cur.dS.store(&sm.u.a.dSt[0][0], LB, tid);
-    cur.D.store(&sm.u.a.D[0][0], LB, tid);
-    cur.V.store(&sm.u.a.V[0][0], LB, tid);
+    // tile vt is complete once at most `after` tiles' loads are outstanding
+    const int after = (vt == 0 ? NB0 : min(NVT, vt + TA::NBUF - 1)) - 1 - vt;
+    if (after >= 2) wait_vm<2 * TA::LOADS>();
+    else if (after == 1) wait_vm<TA::LOADS>();
+    else wait_vm<0>();
+    block_sync_lds();                 // tile vt visible; tile vt-1's buffer is free
+    if (vt >= 1 && vt + TA::NBUF - 1 < NVT) issue(vt + TA::NBUF - 1);
+    const char* t = &sm.x.tiles[vt % TA::NBUF][0];
 #pragma unroll
-    for (int i = 0; i < cur.S.N; ++i)
+    for (int ks = 0; ks < BV / KS; ++ks) {
+      const FR aO = tile_frag<E, TA::RE>(t + TA::DO, 16 * w, ks * KS, lane);
+      const FR adD = tile_frag<E, TA::RE>(t + TA::DD, 16 * w, ks * KS, lane);
+      const FR aD = tile_frag<E, TA::RE>(t + TA::D, 16 * w, ks * KS, lane);
 #pragma unroll
-      for (int j = 0; j < 4; ++j) sdot += cur.S.v[i][j] * cur.dS.v[i][j];
-    block_sync_lds();
+      for (int kb = 0; kb < NKB; ++kb) {
+        float sv[Mma<E>::KPL];
+        const FR bS = tile_frag_f32<E>(t + TA::S, kb * 16, ks * KS, lane, sv);
+        const FR bdS = tile_frag<E, TA::RE>(t + TA::DS, kb * 16, ks * KS, lane);
+        aQ[kb] = Mma<E>::mma(aO, bS, aQ[kb]);
+        aW[kb] = Mma<E>::mma(adD, bS, aW[kb]);
+        aK[kb] = Mma<E>::mma(aD, bdS, aK[kb]);
+        const E* de = (const E*)&bdS;
 #pragma unroll
-    for (int kb = 0; kb < NKB; ++kb) {
-#pragma unroll
-      for (int ks = 0; ks < BV / KS; ++ks) {
-        const FR bS = Frag<E>::load(kmaj(&sm.u.a.St[0][0], LB), kb * 16, ks * KS, lane);
-        const FR bdS = Frag<E>::load(kmaj(&sm.u.a.dSt[0][0], LB), kb * 16, ks * KS, lane);
-        aQ[kb] = Mma<E>::mma(cur.dO.f[ks], bS, aQ[kb]);
-        aW[kb] = Mma<E>::mma(cur.dD.f[ks], bS, aW[kb]);
-        aK[kb] = Mma<E>::mma(cur.Df.f[ks], bdS, aK[kb]);
+        for (int e = 0; e < Mma<E>::KPL; ++e) sdot += sv[e] * tof(de[e]);
       }
-    }
 #pragma unroll
-    for (int ib = 0; ib < 4; ++ib) {
-#pragma unroll
-      for (int ks = 0; ks < BV / KS; ++ks) {
-        const FR bD = Frag<E>::load(kmaj(&sm.u.a.D[0][0], LB), ib * 16, ks * KS, lane);
-        const FR bV = Frag<E>::load(kmaj(&sm.u.a.V[0][0], LB), ib * 16, ks * KS, lane);
-        aP[ib] = Mma<E>::mma(cur.dO.f[ks], bD, aP[ib]);
-        aT[ib] = Mma<E>::mma(cur.dD.f[ks], bV, aT[ib]);
+      for (int ib = 0; ib < 4; ++ib) {
+        const FR bD = tile_frag<E, TA::RE>(t + TA::D, ib * 16, ks * KS, lane);
+        const FR bV = tile_frag<E, TA::RE>(t + TA::V, ib * 16, ks * KS, lane);
+        aP[ib] = Mma<E>::mma(aO, bD, aP[ib]);
+        aT[ib] = Mma<E>::mma(adD, bV, aT[ib]);
       }
     }
   }
+  // every wave read the whole of S^T and dS'^T: one copy of <S, dS'> suffices
   sdot = wave_sum(sdot);
-  if (lane == 0) sm.sdot[w] = sdot;
+  if (tid == 0) sm.sdot[0] = sdot;
+  if (tid < C) {
+    const bool ok = tid < len;
+    sm.b[tid] = gb;
+    sm.g[tid] = __expf(gb);
+    sm.beta[tid] = ok ? gbeta : 0.f;
+    sm.lam[tid] = ok ? glam : 0.f;
+    sm.dlam[tid] = 0.f;
+    sm.tk[tid] = 0.f;
+  }
 
   // ---------------- phase B1: G = X K^T, QK = Q K^T, dT2 = dW (g X)^T
   constexpr int LKD = DK + P;
   block_sync_lds();
-  rKf.store(&sm.u.b1.K[0][0], LKD, tid);
-  rQf.store(&sm.u.b1.Q[0][0], LKD, tid);
-  rM.store(&sm.Mm[0][0], LC, tid);
-  rT.store(&sm.TmT[0][0], LC, tid);
+  rKf.store_rows(&sm.x.s.u.b1.K[0][0], LKD, len, tid);
+  rQf.store_rows(&sm.x.s.u.b1.Q[0][0], LKD, len, tid);
 #pragma unroll
   for (int kb = 0; kb < NKB; ++kb)
 #pragma unroll
-    for (int j = 0; j < 4; ++j) sm.u.b1.dW[16 * w + frow(lane, j)][kb * 16 + fcol(lane)] = fromf<E>(-aW[kb][j]);
+    for (int j = 0; j < 4; ++j) sm.x.s.u.b1.dW[16 * w + frow(lane, j)][kb * 16 + fcol(lane)] = fromf<E>(-aW[kb][j]);
   if (tid < C) sm.kb[tid] = __expf(sm.b[C - 1] - sm.b[tid]);
   block_sync_lds();
   f4 aG[4], aQK[4], adT[4];
@@ -417,14 +448,14 @@ __global__ __launch_bounds__(NTHREADS) void k_bwd_intra(Params p) {
     }
 #pragma unroll
     for (int ks = 0; ks < DK / KS; ++ks) {
-      const FR kA = Frag<E>::load(kmaj(&sm.u.b1.K[0][0], LKD), 16 * w, ks * KS, lane);
-      const FR qA = Frag<E>::load(kmaj(&sm.u.b1.Q[0][0], LKD), 16 * w, ks * KS, lane);
+      const FR kA = Frag<E>::load(kmaj(&sm.x.s.u.b1.K[0][0], LKD), 16 * w, ks * KS, lane);
+      const FR qA = Frag<E>::load(kmaj(&sm.x.s.u.b1.Q[0][0], LKD), 16 * w, ks * KS, lane);
       const FR xA = mix_frag<FR>(kA, qA, lam_a, 1.f);
-      const FR dwA = Frag<E>::load(kmaj(&sm.u.b1.dW[0][0], LKD), 16 * w, ks * KS, lane);
+      const FR dwA = Frag<E>::load(kmaj(&sm.x.s.u.b1.dW[0][0], LKD), 16 * w, ks * KS, lane);
 #pragma unroll
       for (int ib = 0; ib < 4; ++ib) {
-        const FR kB = Frag<E>::load(kmaj(&sm.u.b1.K[0][0], LKD), ib * 16, ks * KS, lane);
-        const FR qB = Frag<E>::load(kmaj(&sm.u.b1.Q[0][0], LKD), ib * 16, ks * KS, lane);
+        const FR kB = Frag<E>::load(kmaj(&sm.x.s.u.b1.K[0][0], LKD), ib * 16, ks * KS, lane);
+        const FR qB = Frag<E>::load(kmaj(&sm.x.s.u.b1.Q[0][0], LKD), ib * 16, ks * KS, lane);
         const FR gxB = mix_frag<FR>(kB, qB, lam_b[ib], g_b[ib]);
         aG[ib] = Mma<E>::mma(xA, kB, aG[ib]);
         aQK[ib] = Mma<E>::mma(qA, kB, aQK[ib]);
@@ -453,14 +484,14 @@ __global__ __launch_bounds__(NTHREADS) void k_bwd_intra(Params p) {
       float cs = 0.f;
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
-        const float m = tof(sm.Mm[rw + j][c]);
+        const float m = tof(*(const E*)(sm.Mm + tile_off<RBC>(rw + j, c * (int)sizeof(E))));
         const float dt = aT[ib][j] + adT[ib][j];
         cs += dt * m;
         mv[j] = m;
         dm[j] = dt * bc;
       }
-      *(typename Quad<E>::raw*)&sm.u.b2.MT[c][rw] = Quad<E>::pack(mv);
-      *(typename Quad<E>::raw*)&sm.u.b2.dMt[c][rw] = Quad<E>::pack(dm);
+      *(typename Quad<E>::raw*)&sm.x.s.u.b2.MT[c][rw] = Quad<E>::pack(mv);
+      *(typename Quad<E>::raw*)&sm.x.s.u.b2.dMt[c][rw] = Quad<E>::pack(dm);
       cs += __shfl_xor(cs, 16, 64);
       cs += __shfl_xor(cs, 32, 64);
       if (lane < 16) sm.dbc[w][c] = cs;
@@ -471,15 +502,20 @@ __global__ __launch_bounds__(NTHREADS) void k_bwd_intra(Params p) {
   {
 #pragma unroll
     for (int ib = 0; ib < 4; ++ib) {        // Y = M^T dMinv, rows 16w..
-      const f4 y = mma_k<E, C>(kmaj(&sm.u.b2.MT[0][0], LC), kmaj(&sm.u.b2.dMt[0][0], LC), 16 * w, ib * 16, zero4(), lane);
+      const f4 y = mma_k<E, C>(kmaj(&sm.x.s.u.b2.MT[0][0], LC), kmaj(&sm.x.s.u.b2.dMt[0][0], LC), 16 * w, ib * 16, zero4(), lane);
 #pragma unroll
-      for (int j = 0; j < 4; ++j) sm.u.b2.Y[rw + j][ib * 16 + cl] = fromf<E>(y[j]);
+      for (int j = 0; j < 4; ++j) sm.x.s.u.b2.Y[rw + j][ib * 16 + cl] = fromf<E>(y[j]);
     }
     // Y rows 16w.. are read back by this wave only
     asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
 #pragma unroll
-    for (int ib = 0; ib < 4; ++ib)          // dA = strictLower(-Y M^T)
-      adA[ib] = mma_k<E, C>(kmaj(&sm.u.b2.Y[0][0], LC), kmaj(&sm.Mm[0][0], LC), 16 * w, ib * 16, zero4(), lane);
+    for (int ib = 0; ib < 4; ++ib) {        // dA = strictLower(-Y M^T)
+      adA[ib] = zero4();
+#pragma unroll
+      for (int ks = 0; ks < C / KS; ++ks)
+        adA[ib] = Mma<E>::mma(Frag<E>::load(kmaj(&sm.x.s.u.b2.Y[0][0], LC), 16 * w, ks * KS, lane),
+                              tile_frag<E, RBC>(sm.Mm, ib * 16, ks * KS, lane), adA[ib]);
+    }
   }
   {
     // dG = diag(beta) dA (.) Gamma, dQK = dP (.) Gamma (causal, inclusive),
@@ -511,12 +547,12 @@ __global__ __launch_bounds__(NTHREADS) void k_bwd_intra(Params p) {
         ec += t;
         vg[j] = dg;
         vq[j] = dqk;
-        sm.dG[r][c] = fromf<E>(dg);
-        sm.dQK[r][c] = fromf<E>(dqk);
+        sm.x.s.dG[r][c] = fromf<E>(dg);
+        sm.x.s.dQK[r][c] = fromf<E>(dqk);
       }
       if constexpr (BwdSmem<E, DK>::TCOPY) {
-        *(typename Quad<E>::raw*)&sm.dGt[c][rw] = Quad<E>::pack(vg);
-        *(typename Quad<E>::raw*)&sm.dQKt[c][rw] = Quad<E>::pack(vq);
+        *(typename Quad<E>::raw*)&sm.x.s.dGt[c][rw] = Quad<E>::pack(vg);
+        *(typename Quad<E>::raw*)&sm.x.s.dQKt[c][rw] = Quad<E>::pack(vq);
       }
       ec += __shfl_xor(ec, 16, 64);
       ec += __shfl_xor(ec, 32, 64);
@@ -538,14 +574,14 @@ __global__ __launch_bounds__(NTHREADS) void k_bwd_intra(Params p) {
   block_sync_lds();
 
   // ---------------- phase B3: dX, dq, dk (wave w owns rows 16w..)
-  rKt.store(&sm.u.b3.Kt[0][0], LC, tid);
-  rQt.store(&sm.u.b3.Qt[0][0], LC, tid);
+  rKt.store(&sm.x.s.u.b3.Kt[0][0], LC, tid);
+  rQt.store(&sm.x.s.u.b3.Qt[0][0], LC, tid);
 #pragma unroll
   for (int kb = 0; kb < NKB; ++kb) {
     f4 nw;
 #pragma unroll
     for (int j = 0; j < 4; ++j) nw[j] = -aW[kb][j];
-    *(typename Quad<E>::raw*)&sm.u.b3.dWt[kb * 16 + fcol(lane)][16 * w + frow(lane, 0)] = Quad<E>::pack(nw);
+    *(typename Quad<E>::raw*)&sm.x.s.u.b3.dWt[kb * 16 + fcol(lane)][16 * w + frow(lane, 0)] = Quad<E>::pack(nw);
   }
   block_sync_lds();
   {
@@ -554,15 +590,15 @@ __global__ __launch_bounds__(NTHREADS) void k_bwd_intra(Params p) {
     float lamk[NTK][Mma<E>::KPL];
 #pragma unroll
     for (int ks = 0; ks < NTK; ++ks) {
-      tA[ks] = Frag<E>::load(kmaj(&sm.TmT[0][0], LC), 16 * w, ks * KS, lane);
-      gA[ks] = Frag<E>::load(kmaj(&sm.dG[0][0], LC), 16 * w, ks * KS, lane);
-      qkA[ks] = Frag<E>::load(kmaj(&sm.dQK[0][0], LC), 16 * w, ks * KS, lane);
+      tA[ks] = tile_frag<E, RBC>(sm.TmT, 16 * w, ks * KS, lane);
+      gA[ks] = Frag<E>::load(kmaj(&sm.x.s.dG[0][0], LC), 16 * w, ks * KS, lane);
+      qkA[ks] = Frag<E>::load(kmaj(&sm.x.s.dQK[0][0], LC), 16 * w, ks * KS, lane);
       if constexpr (BwdSmem<E, DK>::TCOPY) {
-        qktA[ks] = Frag<E>::load(kmaj(&sm.dQKt[0][0], LC), 16 * w, ks * KS, lane);
-        gtA[ks] = Frag<E>::load(kmaj(&sm.dGt[0][0], LC), 16 * w, ks * KS, lane);
+        qktA[ks] = Frag<E>::load(kmaj(&sm.x.s.dQKt[0][0], LC), 16 * w, ks * KS, lane);
+        gtA[ks] = Frag<E>::load(kmaj(&sm.x.s.dGt[0][0], LC), 16 * w, ks * KS, lane);
       } else {
-        qktA[ks] = Frag<E>::load(imaj(&sm.dQK[0][0], LC), 16 * w, ks * KS, lane);
-        gtA[ks] = Frag<E>::load(imaj(&sm.dG[0][0], LC), 16 * w, ks * KS, lane);
+        qktA[ks] = Frag<E>::load(imaj(&sm.x.s.dQK[0][0], LC), 16 * w, ks * KS, lane);
+        gtA[ks] = Frag<E>::load(imaj(&sm.x.s.dG[0][0], LC), 16 * w, ks * KS, lane);
       }
 #pragma unroll
       for (int e = 0; e < Mma<E>::KPL; ++e) lamk[ks][e] = sm.lam[ks * KS + (lane >> 4) * Mma<E>::KPL + e];
@@ -574,9 +610,9 @@ __global__ __launch_bounds__(NTHREADS) void k_bwd_intra(Params p) {
       f4 dgx = zero4(), dxp = zero4(), dqp = zero4(), dkp = zero4();
 #pragma unroll
       for (int ks = 0; ks < NTK; ++ks) {
-        const FR ktB = Frag<E>::load(kmaj(&sm.u.b3.Kt[0][0], LC), kb * 16, ks * KS, lane);
-        const FR qtB = Frag<E>::load(kmaj(&sm.u.b3.Qt[0][0], LC), kb * 16, ks * KS, lane);
-        const FR dwB = Frag<E>::load(kmaj(&sm.u.b3.dWt[0][0], LC), kb * 16, ks * KS, lane);
+        const FR ktB = Frag<E>::load(kmaj(&sm.x.s.u.b3.Kt[0][0], LC), kb * 16, ks * KS, lane);
+        const FR qtB = Frag<E>::load(kmaj(&sm.x.s.u.b3.Qt[0][0], LC), kb * 16, ks * KS, lane);
+        const FR dwB = Frag<E>::load(kmaj(&sm.x.s.u.b3.dWt[0][0], LC), kb * 16, ks * KS, lane);
         const FR xtB = mix_tokens<FR>(ktB, qtB, lamk[ks]);
         dgx = Mma<E>::mma(tA[ks], dwB, dgx);      // T^T dW
         dxp = Mma<E>::mma(gA[ks], ktB, dxp);      // dG K
@@ -585,8 +621,8 @@ __global__ __launch_bounds__(NTHREADS) void k_bwd_intra(Params p) {
         dkp = Mma<E>::mma(gtA[ks], xtB, dkp);     // dG^T X
       }
       const int kc = kb * 16 + fcol(lane);
-      const typename Quad<E>::raw kv = *(const typename Quad<E>::raw*)&sm.u.b3.Kt[kc][r0];
-      const typename Quad<E>::raw qv = *(const typename Quad<E>::raw*)&sm.u.b3.Qt[kc][r0];
+      const typename Quad<E>::raw kv = *(const typename Quad<E>::raw*)&sm.x.s.u.b3.Kt[kc][r0];
+      const typename Quad<E>::raw qv = *(const typename Quad<E>::raw*)&sm.x.s.u.b3.Qt[kc][r0];
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
         const int r = r0 + j;
@@ -597,8 +633,8 @@ __global__ __launch_bounds__(NTHREADS) void k_bwd_intra(Params p) {
         rtk[j] += kbr * Kv * aK[kb][j];
         const float dX = gr * dgx[j] + dxp[j];
         rdl[j] += Qv * dX;
-        sm.u.b3.oq[r][kc] = fromf<E>(gr * aQ[kb][j] + dqp[j] + lr * dX);
-        sm.u.b3.ok[r][kc] = fromf<E>(kbr * aK[kb][j] + dkp[j] + dX);
+        sm.x.s.u.b3.oq[r][kc] = fromf<E>(gr * aQ[kb][j] + dqp[j] + lr * dX);
+        sm.x.s.u.b3.ok[r][kc] = fromf<E>(kbr * aK[kb][j] + dkp[j] + dX);
       }
     }
 #pragma unroll
@@ -624,8 +660,8 @@ __global__ __launch_bounds__(NTHREADS) void k_bwd_intra(Params p) {
     for (int idx = tid; idx < C * PR; idx += NTHREADS) {
       const int r = idx / PR, cc = (idx % PR) * VEC;
       if (r < len) {
-        *(uint4*)(dqo + (size_t)r * H * DK + cc) = *(const uint4*)&sm.u.b3.oq[r][cc];
-        *(uint4*)(dko + (size_t)r * H * DK + cc) = *(const uint4*)&sm.u.b3.ok[r][cc];
+        *(uint4*)(dqo + (size_t)r * H * DK + cc) = *(const uint4*)&sm.x.s.u.b3.oq[r][cc];
+        *(uint4*)(dko + (size_t)r * H * DK + cc) = *(const uint4*)&sm.x.s.u.b3.ok[r][cc];
       }
     }
   }
@@ -644,7 +680,7 @@ __global__ __launch_bounds__(NTHREADS) void k_bwd_intra(Params p) {
       dbj -= sm.ecc[v][j];
       dbeta += sm.dbc[v][j];
     }
-    if (j == C - 1) dbj += tot + sm.g[C - 1] * (sm.sdot[0] + sm.sdot[1] + sm.sdot[2] + sm.sdot[3]);
+    if (j == C - 1) dbj += tot + sm.g[C - 1] * sm.sdot[0];
     float x = __shfl(dbj, C - 1 - j, 64);
     x = wave_incl_scan(x, lane);
     const float suffix = __shfl(x, C - 1 - j, 64);

@@ -216,6 +216,23 @@ struct TileRegs {
       if (owns(i, tid)) *(uint4*)(dst + (size_t)r * ld + c) = v[i];
     }
   }
+  // Branch-free variant for loads that must not wait on each other: rows at
+  // or past `valid` (>= 1) re-read row valid - 1, and store_rows() writes
+  // them as zero.
+  __device__ inline void load_clamped(const E* src, size_t rs, int valid, int tid) {
+#pragma unroll
+    for (int i = 0; i < N; ++i) {
+      const int idx = tid + i * NT, r = min(idx / PR, valid - 1), c = (idx % PR) * VEC;
+      if (owns(i, tid)) v[i] = *(const uint4*)(src + (size_t)r * rs + c);
+    }
+  }
+  __device__ inline void store_rows(E* dst, int ld, int valid, int tid) const {
+#pragma unroll
+    for (int i = 0; i < N; ++i) {
+      const int idx = tid + i * NT, r = idx / PR, c = (idx % PR) * VEC;
+      if (owns(i, tid)) *(uint4*)(dst + (size_t)r * ld + c) = r < valid ? v[i] : make_uint4(0, 0, 0, 0);
+    }
+  }
 };
 
 // As TileRegs, but consecutive threads take consecutive rows, so that the
@@ -301,6 +318,80 @@ __device__ inline void block_sync_lds() {
   asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
 }
 
+// Wait until at most N vector-memory operations of this wave are outstanding
+// (they complete in issue order).  Needed for direct global->LDS loads, whose
+// LDS writes the compiler does not track.
+template <int N>
+__device__ inline void wait_vm() {
+  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
+
+// LDS tiles written by direct loads are rows of RB bytes (64, 128 or 256) made of
+// 16-byte chunks; chunk c of row r sits at slot c ^ swz(r), so that sixteen
+// consecutive rows read at the same chunk hit distinct banks.
+template <int RB>
+__device__ inline int tile_swz(int row) {
+  static_assert(RB == 64 || RB == 128 || RB == 256, "row size");
+  return RB == 64 ? ((row >> 2) & 3) : RB == 128 ? ((row >> 1) & 7) : (row & 15);
+}
+template <int RB>
+__device__ inline int tile_off(int row, int byte) {
+  return row * RB + (((byte >> 4) ^ tile_swz<RB>(row)) << 4) + (byte & 15);
+}
+
+// Direct global->LDS copy of a ROWS x RB-byte block (row stride `stride`
+// bytes) into the swizzled layout at `dst`.  Each instruction moves 1 KB
+// (lane i writes LDS bytes 16i..16i+15 of it); wave w issues instructions
+// w, w + NWAVES, ...  Rows at or past `valid` are read from `zsrc` (stride
+// `zstride`) instead, which the caller points at rows known to be zero.
+template <int RB, int ROWS>
+__device__ inline void dma_rows(char* dst, const char* src, size_t stride, int valid, const char* zsrc,
+                                size_t zstride, int w, int lane) {
+  constexpr int NCH = RB / 16, RPI = 1024 / RB, NI = ROWS / RPI;
+  static_assert(NI % NWAVES == 0, "instructions split evenly over the waves");
+#pragma unroll
+  for (int j = 0; j < NI / NWAVES; ++j) {
+    const int i = j * NWAVES + w;
+    const int row = i * RPI + lane / NCH;
+    const int c = (lane % NCH) ^ tile_swz<RB>(row);
+    const char* g = row < valid ? src + (size_t)row * stride + c * 16 : zsrc + (size_t)row * zstride + c * 16;
+    __builtin_amdgcn_global_load_lds((const void*)g, (__attribute__((address_space(3))) void*)(dst + i * 1024), 16,
+                                     0, 0);
+  }
+}
+
+// MFMA fragment (A or B operand; both map lane l to row l & 15 and to the
+// KPL consecutive k from (l >> 4) * KPL) read from a swizzled LDS tile of
+// element type E.
+template <typename E, int RB>
+__device__ inline typename Mma<E>::frag tile_frag(const char* t, int row0, int k0, int lane) {
+  const int row = row0 + (lane & 15), k = k0 + (lane >> 4) * Mma<E>::KPL;
+  return *(const typename Mma<E>::frag*)(t + tile_off<RB>(row, k * (int)sizeof(E)));
+}
+// Same from an fp32 tile, converted to E; the fp32 values are returned in v.
+template <typename E>
+__device__ inline typename Mma<E>::frag tile_frag_f32(const char* t, int row0, int k0, int lane,
+                                                      float (&v)[Mma<E>::KPL]) {
+  constexpr int RB = 128;
+  const int row = row0 + (lane & 15), k = k0 + (lane >> 4) * Mma<E>::KPL;
+  if constexpr (Mma<E>::KPL == 8) {
+    const f4 a = *(const f4*)(t + tile_off<RB>(row, k * 4));
+    const f4 b = *(const f4*)(t + tile_off<RB>(row, k * 4 + 16));
+    typename Mma<E>::frag f;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      v[e] = a[e];
+      v[4 + e] = b[e];
+      f[e] = (E)a[e];
+      f[4 + e] = (E)b[e];
+    }
+    return f;
+  } else {
+    v[0] = *(const float*)(t + tile_off<RB>(row, k * 4));
+    return v[0];
+  }
+}
+
 
 
 // ----------------------------------------------------------------- parameters
@@ -347,7 +438,7 @@ struct Params {
   float* dlam;
   float* dla;
   float* dS0;
-  float* w_dSo;          // [slot][H][Dk][Dv] gradient w.r.t. each chunk's exit state, transposed
+  void* w_dSo;           // [slot][H][Dk][Dv] gradient w.r.t. each chunk's exit state, transposed (dtype)
   void* w_dDb;           // [slot][H][C][Dv] dD (dtype)
 };
 

@@ -261,6 +261,7 @@ struct ScanFwdSmem {
   E Dkt[BV][C + P];   // (diag(g_C / g) D)^T
   E O[C][BV + P];     // output tile staging
   E Dr[C][BV + P];    // D tile staging for the saved context
+  float Sf[DK][BV + 4];  // fp32 entry-state tile staging for the saved context
 };
 
 // Operands of one chunk for one wave of the forward scan, prefetched from
@@ -348,13 +349,19 @@ __global__ __launch_bounds__(NTHREADS) void k_scan_fwd(Params p) {
         const int kt = KPW * w + i;
         *(QR*)&sm.S[nb * 16 + fcol(lane)][kt * 16 + frow(lane, 0)] = Quad<E>::pack(acc[i][nb]);
         if (p.saved) {
-          // saved entry state, transposed: element (k, v) at [k][v]
-          float* dst = p.saved + (gi * DK + kt * 16 + frow(lane, 0)) * DV + v0 + nb * 16 + fcol(lane);
 #pragma unroll
-          for (int j = 0; j < 4; ++j) dst[(size_t)j * DV] = acc[i][nb][j];
+          for (int j = 0; j < 4; ++j) sm.Sf[kt * 16 + frow(lane, j)][nb * 16 + fcol(lane)] = acc[i][nb][j];
         }
       }
     block_sync_lds();
+    if (p.saved) {
+      // saved entry state, transposed (element (k, v) at [k][v]), 16-byte stores
+      float* dst = p.saved + gi * DK * DV + v0;
+      for (int idx = tid; idx < DK * (BV / 4); idx += NTHREADS) {
+        const int r = idx / (BV / 4), c4 = (idx % (BV / 4)) * 4;
+        *(f4*)(dst + (size_t)r * DV + c4) = *(const f4*)&sm.Sf[r][c4];
+      }
+    }
     if (c + 1 < nch) prefetch(c + 1);
     const float bl = sm.b[C - 1];
     // S fragments (B operand, shared by D and O)
