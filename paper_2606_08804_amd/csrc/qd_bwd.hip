@@ -246,8 +246,6 @@ struct alignas(16) BwdSmem {
   static constexpr bool TCOPY = sizeof(E) == 2;
   float b[C], g[C], kb[C], beta[C], lam[C], db[C], dbeta[C], dlam[C], tk[C];
   float sdot[NWAVES];
-  float dbc[NWAVES][C];     // per-wave column sums of dT (.) M
-  float ecc[NWAVES][C];     // per-wave column sums of the decay-gradient terms
   union {
     alignas(16) char tiles[TileA<E, DK>::NBUF][TileA<E, DK>::BYTES];   // phase A
     struct {
@@ -261,6 +259,8 @@ struct alignas(16) BwdSmem {
           E MT[C][C + P];       // M^T (i, r)
           E dMt[C][C + P];      // (dT diag(beta))^T (i, r)
           E Y[C][C + P];        // M^T dT diag(beta) (r, i), rows private to their wave
+          float dbc[4 * NWAVES][C];   // column partial sums of dT (.) M, per wave and lane group
+          float ecc[4 * NWAVES][C];   // column partial sums of the decay-gradient terms
         } b2;
         struct {
           E dWt[DK][C + P];     // dW^T (k, r)
@@ -492,9 +492,7 @@ __global__ __launch_bounds__(NTHREADS) void k_bwd_intra(Params p) {
       }
       *(typename Quad<E>::raw*)&sm.x.s.u.b2.MT[c][rw] = Quad<E>::pack(mv);
       *(typename Quad<E>::raw*)&sm.x.s.u.b2.dMt[c][rw] = Quad<E>::pack(dm);
-      cs += __shfl_xor(cs, 16, 64);
-      cs += __shfl_xor(cs, 32, 64);
-      if (lane < 16) sm.dbc[w][c] = cs;
+      sm.x.s.u.b2.dbc[4 * w + (lane >> 4)][c] = cs;
     }
   }
   block_sync_lds();
@@ -554,9 +552,7 @@ __global__ __launch_bounds__(NTHREADS) void k_bwd_intra(Params p) {
         *(typename Quad<E>::raw*)&sm.x.s.dGt[c][rw] = Quad<E>::pack(vg);
         *(typename Quad<E>::raw*)&sm.x.s.dQKt[c][rw] = Quad<E>::pack(vq);
       }
-      ec += __shfl_xor(ec, 16, 64);
-      ec += __shfl_xor(ec, 32, 64);
-      if (lane < 16) sm.ecc[w][c] = ec;
+      sm.x.s.u.b2.ecc[4 * w + (lane >> 4)][c] = ec;
     }
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
@@ -572,6 +568,18 @@ __global__ __launch_bounds__(NTHREADS) void k_bwd_intra(Params p) {
     }
   }
   block_sync_lds();
+  if (tid < C) {
+    // column parts: dbeta += colsum(dT (.) M), db -= colsum of the decay terms
+    float cb = 0.f, ce = 0.f;
+#pragma unroll
+    for (int v = 0; v < 4 * NWAVES; ++v) {
+      cb += sm.x.s.u.b2.dbc[v][tid];
+      ce += sm.x.s.u.b2.ecc[v][tid];
+    }
+    sm.dbeta[tid] += cb;
+    sm.db[tid] -= ce;
+  }
+  block_sync_lds();                    // the b2 buffers are dead past here
 
   // ---------------- phase B3: dX, dq, dk (wave w owns rows 16w..)
   rKt.store(&sm.x.s.u.b3.Kt[0][0], LC, tid);
@@ -605,6 +613,13 @@ __global__ __launch_bounds__(NTHREADS) void k_bwd_intra(Params p) {
     }
     const int r0 = 16 * w + frow(lane, 0);
     float rdb[4] = {0.f, 0.f, 0.f, 0.f}, rtk[4] = {0.f, 0.f, 0.f, 0.f}, rdl[4] = {0.f, 0.f, 0.f, 0.f};
+    float gr4[4], lr4[4], kbr4[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      gr4[j] = sm.g[r0 + j];
+      lr4[j] = sm.lam[r0 + j];
+      kbr4[j] = sm.kb[r0 + j];
+    }
 #pragma unroll
     for (int kb = 0; kb < NKB; ++kb) {
       f4 dgx = zero4(), dxp = zero4(), dqp = zero4(), dkp = zero4();
@@ -627,7 +642,7 @@ __global__ __launch_bounds__(NTHREADS) void k_bwd_intra(Params p) {
       for (int j = 0; j < 4; ++j) {
         const int r = r0 + j;
         const float Kv = Quad<E>::get(kv, j), Qv = Quad<E>::get(qv, j);
-        const float gr = sm.g[r], lr = sm.lam[r], kbr = sm.kb[r];
+        const float gr = gr4[j], lr = lr4[j], kbr = kbr4[j];
         const float X = Kv + lr * Qv;
         rdb[j] += gr * (X * dgx[j] + Qv * aQ[kb][j]);
         rtk[j] += kbr * Kv * aK[kb][j];
@@ -674,12 +689,7 @@ __global__ __launch_bounds__(NTHREADS) void k_bwd_intra(Params p) {
 #pragma unroll
     for (int off = 32; off >= 1; off >>= 1) tot += __shfl_xor(tot, off, 64);
     float dbj = sm.db[j] - sm.tk[j];
-    float dbeta = sm.dbeta[j];
-#pragma unroll
-    for (int v = 0; v < NWAVES; ++v) {
-      dbj -= sm.ecc[v][j];
-      dbeta += sm.dbc[v][j];
-    }
+    const float dbeta = sm.dbeta[j];
     if (j == C - 1) dbj += tot + sm.g[C - 1] * sm.sdot[0];
     float x = __shfl(dbj, C - 1 - j, 64);
     x = wave_incl_scan(x, lane);

@@ -495,9 +495,17 @@ __device__ inline float wave_sum(float x) {
 }
 
 // Sum over the 16 lanes that share (lane >> 4).
+// Sum over each row of 16 lanes with DPP lane moves (no LDS crossbar):
+// swaps within pairs and quads, then rotations by 4 and 8 within the row.
+template <int CTRL>
+__device__ inline float dpp_mov(float x) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, x), CTRL, 0xF, 0xF, false));
+}
 __device__ inline float sum16(float x) {
-#pragma unroll
-  for (int off = 8; off >= 1; off >>= 1) x += __shfl_xor(x, off, 64);
+  x += dpp_mov<0xB1>(x);    // quad_perm [1,0,3,2]
+  x += dpp_mov<0x4E>(x);    // quad_perm [2,3,0,1]
+  x += dpp_mov<0x124>(x);   // row_ror:4
+  x += dpp_mov<0x128>(x);   // row_ror:8
   return x;
 }
 
