@@ -128,6 +128,9 @@ def main():
     ap.add_argument("--gate", default="G2", choices=["G1", "G2", "G3"])
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--cpu-units", type=int, default=32)
+    ap.add_argument("--calib-copy", type=int, default=0, metavar="MIB",
+                    help="after the run, copy a MIB-MiB device buffer three times (outside the timed "
+                         "region) so that a counter profile holds a plain copy of known size")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported "
@@ -191,6 +194,13 @@ def main():
         "kernel_avg_us": breakdown,
         "roofline": roof,
     }
+    if args.calib_copy > 0:
+        src = torch.ones(args.calib_copy << 20, dtype=torch.uint8, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        out["calib_copy_bytes"] = args.calib_copy << 20
     if not args.no_cpu:
         out["cpu_baseline"] = cpu_baseline(d, args.cpu_units)
     print(json.dumps(out), flush=True)
