@@ -10,6 +10,7 @@
 #pragma once
 
 #include <hip/hip_runtime.h>
+#include <cstdint>
 #include <stdint.h>
 
 namespace qd {
@@ -339,25 +340,57 @@ __device__ inline int tile_off(int row, int byte) {
   return row * RB + (((byte >> 4) ^ tile_swz<RB>(row)) << 4) + (byte & 15);
 }
 
+// One 16-byte (or 4-byte) direct global->LDS load per lane through inline
+// assembly: lane i's bytes land at LDS byte `lds` + 16i (4i).  The compiler
+// does not see these as LDS writes, so it adds no waits of its own for them
+// (it would otherwise wait on every wave's stores before LDS accesses that it
+// cannot prove disjoint); every consumer must be ordered by an explicit
+// vmcnt wait in the issuing wave plus a barrier.  m0 holds the LDS base;
+// kernels using this form issue no compiler-generated direct loads, the only
+// other user of m0 here.
+#pragma clang diagnostic push
+#pragma clang diagnostic ignored "-Winline-asm"
+__device__ inline void dma16_asm(const void* g, char* lds) {
+  const uint32_t base = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) char*)lds;
+  asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, off" ::"s"(base), "v"(g) : "memory", "m0");
+}
+__device__ inline void dma4_asm(const void* g, char* lds) {
+  const uint32_t base = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) char*)lds;
+  asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dword %1, off" ::"s"(base), "v"(g) : "memory", "m0");
+}
+#pragma clang diagnostic pop
+
 // Direct global->LDS copy of a ROWS x RB-byte block (row stride `stride`
 // bytes) into the swizzled layout at `dst`.  Each instruction moves 1 KB
-// (lane i writes LDS bytes 16i..16i+15 of it); wave w issues instructions
-// w, w + NWAVES, ...  Rows at or past `valid` are read from `zsrc` (stride
+// (lane i writes LDS bytes 16i..16i+15 of it); wave w of NW issues
+// instructions w, w + NW, ...  Rows at or past `valid` are read from `zsrc` (stride
 // `zstride`) instead, which the caller points at rows known to be zero.
-template <int RB, int ROWS>
+template <int RB, int ROWS, int NW = NWAVES, bool ASM = false>
 __device__ inline void dma_rows(char* dst, const char* src, size_t stride, int valid, const char* zsrc,
                                 size_t zstride, int w, int lane) {
   constexpr int NCH = RB / 16, RPI = 1024 / RB, NI = ROWS / RPI;
-  static_assert(NI % NWAVES == 0, "instructions split evenly over the waves");
+  static_assert(NI % NW == 0, "instructions split evenly over the waves");
 #pragma unroll
-  for (int j = 0; j < NI / NWAVES; ++j) {
-    const int i = j * NWAVES + w;
+  for (int j = 0; j < NI / NW; ++j) {
+    const int i = j * NW + w;
     const int row = i * RPI + lane / NCH;
     const int c = (lane % NCH) ^ tile_swz<RB>(row);
     const char* g = row < valid ? src + (size_t)row * stride + c * 16 : zsrc + (size_t)row * zstride + c * 16;
-    __builtin_amdgcn_global_load_lds((const void*)g, (__attribute__((address_space(3))) void*)(dst + i * 1024), 16,
-                                     0, 0);
+    if constexpr (ASM)
+      dma16_asm(g, dst + i * 1024);
+    else
+      __builtin_amdgcn_global_load_lds((const void*)g, (__attribute__((address_space(3))) void*)(dst + i * 1024),
+                                       16, 0, 0);
   }
+}
+
+// Direct global->LDS copy (assembly form) of NBYTES contiguous bytes, a
+// multiple of 1 KB, by one wave, byte for byte.
+template <int NBYTES>
+__device__ inline void dma_block_asm(char* dst, const char* src, int lane) {
+  static_assert(NBYTES % 1024 == 0, "whole instructions");
+#pragma unroll
+  for (int i = 0; i < NBYTES / 1024; ++i) dma16_asm(src + i * 1024 + lane * 16, dst + i * 1024);
 }
 
 // MFMA fragment (A or B operand; both map lane l to row l & 15 and to the

@@ -252,37 +252,48 @@ __global__ __launch_bounds__(PREP_THREADS) void k_prep(Params p) {
   }
 }
 
+// Forward-scan operands of one chunk, filled by direct global->LDS loads:
+// W (C x Dk), K^T (Dk x C), Q (C x Dk), P (C x C) as swizzled tiles, then
+// this workgroup's U fragments (byte copy of the C-fragment-ordered layout)
+// and b (C fp32).
 template <typename E, int DK, int BV>
-struct ScanFwdSmem {
+struct ScanFwdRing {
+  static constexpr int RK = DK * (int)sizeof(E), RC = C * (int)sizeof(E);   // row bytes
+  static constexpr int NB = BV / 16;
+  static constexpr int UM = NB * 64 * 4 * (int)sizeof(E);   // U bytes per 16-row block
+  static constexpr int W = 0, KT = W + C * RK, Q = KT + DK * RC, PP = Q + C * RK, U = PP + C * RC,
+                       B = U + 4 * UM, BYTES = B + C * 4;
+  static constexpr int NBUF = sizeof(E) == 2 ? 2 : 1;      // fp32 tiles are twice as large
+  static constexpr int LOADS = (B - W) / 1024 + 1;           // direct loads per chunk
+  static_assert(NBUF == 1 || LOADS <= 63, "outstanding-load counter range");
+};
+
+template <typename E, int DK, int BV>
+struct alignas(16) ScanFwdSmem {
   static constexpr int P = Pad<E>::v;
-  float b[C];
-  E S[BV][DK + P];    // state tile (MFMA operand copy)
+  typedef ScanFwdRing<E, DK, BV> R;
+  alignas(16) char ring[R::NBUF][R::BYTES];
   E Dt[BV][C + P];    // D^T
   E Dkt[BV][C + P];   // (diag(g_C / g) D)^T
-  E O[C][BV + P];     // output tile staging
-  E Dr[C][BV + P];    // D tile staging for the saved context
-  float Sf[DK][BV + 4];  // fp32 entry-state tile staging for the saved context
+  union {
+    struct {
+      E S[BV][DK + P];        // state tile (MFMA operand copy)
+      float Sf[DK][BV + 4];   // fp32 entry-state tile staging for the saved context
+    } s;
+    E O[C][BV + P];           // output tile staging (after the state copies are dead)
+  } u;
 };
 
-// Operands of one chunk for one wave of the forward scan, prefetched from
-// global memory straight into MFMA fragments (no LDS staging).
-template <typename E, int DK, int DPW>
-struct ScanFwdPre {
-  AFrag<E, DK> W, Q;      // rows 16w.. of W and Q
-  AFrag<E, C> P;          // rows 16w.. of P
-  AFrag<E, C> Kt[2];      // rows 16(2w+i).. of K^T
-  typename Quad<E>::raw U[DPW];
-  float b;
-};
-
-// One workgroup per (sequence, head, Dv tile of BV = 32 value rows); wave w
-// owns rows 16w.. of the chunk's D and O tiles and key rows 32w.. of the
-// state tile.  The state tile S^T (Dk x BV) lives in fp32 MFMA accumulators
-// across the whole sequence.  The next chunk's operands are prefetched into
-// registers while the current chunk is computed.  When p.o is null only the
-// states are produced.
+// One workgroup per (sequence, head, Dv tile of BV = 32 value rows): four
+// compute waves and one producer wave.  Compute wave w owns rows 16w.. of the
+// chunk's D and O tiles and key rows 16 KPW w.. of the state tile S^T
+// (Dk x BV), which lives in fp32 MFMA accumulators across the whole sequence.
+// The producer wave streams each chunk's operands into a two-chunk LDS ring
+// with direct loads, one chunk ahead; it issues no other memory operations,
+// so its outstanding-load count is exact.  When p.o is null only the states
+// are produced.
 template <typename E, int DK, int DV, int BV>
-__global__ __launch_bounds__(NTHREADS) void k_scan_fwd(Params p) {
+__global__ __launch_bounds__(NTHREADS + 64) void k_scan_fwd(Params p) {
   constexpr int P = Pad<E>::v;
   constexpr int LK = DK + P, LC = C + P;
   constexpr int NVT = DV / BV;
@@ -292,8 +303,10 @@ __global__ __launch_bounds__(NTHREADS) void k_scan_fwd(Params p) {
   constexpr int KPW = DK / 16 / NWAVES;       // key row blocks of S^T per wave (1 or 2)
   typedef typename Quad<E>::raw QR;
   typedef typename Mma<E>::frag FR;
+  typedef ScanFwdRing<E, DK, BV> R;
   __shared__ ScanFwdSmem<E, DK, BV> sm;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const bool producer = w == NWAVES;
   int unit, vt;
   if (!xcd_unit_tile(blockIdx.x, p.N * p.H, NVT, unit, vt)) return;
   const int H = p.H, n = unit / H, h = unit % H, v0 = vt * BV;
@@ -303,6 +316,28 @@ __global__ __launch_bounds__(NTHREADS) void k_scan_fwd(Params p) {
   const int nch = max(0, min((e - s + C - 1) / C, p.n_slots - base));
   const bool with_o = p.o != nullptr;
 
+  // producer: all operands of chunk c into ring buffer `buf`
+  auto issue = [&](int c, int buf) {
+    char* r = sm.ring[buf];
+    const int t0 = s + c * C, len = min(C, e - t0);
+    const size_t gi = (size_t)(base + c) * H + h;
+    const char* Wg = (const char*)((const E*)p.wW + gi * C * DK);
+    const char* Kg = (const char*)((const E*)p.wKt + gi * DK * C);
+    const char* Qg = (const char*)((const E*)p.q + ((size_t)t0 * H + h) * DK);
+    const char* Pg = (const char*)((const E*)p.wP + gi * C * C);
+    dma_rows<R::RK, C, 1, true>(r + R::W, Wg, R::RK, C, Wg, 0, 0, lane);
+    dma_rows<R::RC, DK, 1, true>(r + R::KT, Kg, R::RC, DK, Kg, 0, 0, lane);
+    // rows of Q past the chunk come from W, whose rows there are zero
+    dma_rows<R::RK, C, 1, true>(r + R::Q, Qg, (size_t)H * R::RK, len, Wg, R::RK, 0, lane);
+    dma_rows<R::RC, C, 1, true>(r + R::PP, Pg, R::RC, C, Pg, 0, 0, lane);
+#pragma unroll
+    for (int mt = 0; mt < 4; ++mt)
+      dma_block_asm<R::UM>(r + R::U + mt * R::UM,
+                           (const char*)((const E*)p.wU + gi * C * DV + (size_t)(mt * (DV / 16) + vt * NB) * 256),
+                           lane);
+    dma4_asm(p.wb + gi * C + lane, r + R::B);
+  };
+
   // state: acc[i][nb] = S^T rows 16*(KPW*w+i).., columns 16*nb.. of this tile
   f4 acc[KPW][NB];
 #pragma unroll
@@ -310,137 +345,159 @@ __global__ __launch_bounds__(NTHREADS) void k_scan_fwd(Params p) {
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb) {
       const int kt = KPW * w + i;
-      acc[i][nb] = p.S0 ? *(const f4*)(p.S0 + ((size_t)unit * DV + v0 + nb * 16 + fcol(lane)) * DK + kt * 16 +
-                                       frow(lane, 0))
-                        : zero4();
+      acc[i][nb] = (p.S0 && !producer)
+                       ? *(const f4*)(p.S0 + ((size_t)unit * DV + v0 + nb * 16 + fcol(lane)) * DK + kt * 16 +
+                                      frow(lane, 0))
+                       : zero4();
     }
 
-  const E* qbase = (const E*)p.q;
-  ScanFwdPre<E, DK, NB> pre;
-  auto prefetch = [&](int c) {
-    const int t0 = s + c * C, len = min(C, e - t0);
-    const size_t gi = (size_t)(base + c) * H + h;
-    pre.b = tid < C ? p.wb[gi * C + tid] : 0.f;
-    pre.W.load((const E*)p.wW + gi * C * DK + (size_t)(16 * w) * DK, DK, 16, lane);
-#pragma unroll
-    for (int i = 0; i < KPW; ++i)
-      pre.Kt[i].load((const E*)p.wKt + gi * DK * C + (size_t)(16 * (KPW * w + i)) * C, C, 16, lane);
-    if (with_o) {
-      pre.Q.load(qbase + ((size_t)(t0 + 16 * w) * H + h) * DK, (size_t)H * DK, len - 16 * w, lane);
-      pre.P.load((const E*)p.wP + gi * C * C + (size_t)(16 * w) * C, C, 16, lane);
-    }
-#pragma unroll
-    for (int nb = 0; nb < NB; ++nb)
-      pre.U[nb] = *(const QR*)((const E*)p.wU + gi * C * DV +
-                               ((size_t)(w * (DV / 16) + vt * NB + nb) * 64 + lane) * 4);
-  };
-  if (nch > 0) prefetch(0);
-
+  if (producer && nch > 0) {
+    issue(0, 0);
+    if (R::NBUF == 2 && nch > 1) issue(1, 1);
+  }
   for (int c = 0; c < nch; ++c) {
     const int t0 = s + c * C, len = min(C, e - t0);
     const size_t gi = (size_t)(base + c) * H + h;
-    const ScanFwdPre<E, DK, NB> cur = pre;
-    block_sync_lds();                      // previous chunk's LDS reads are done
-    if (tid < C) sm.b[tid] = cur.b;
+    const char* rc = sm.ring[R::NBUF == 2 ? (c & 1) : 0];
+    FR sf[NB][DK / KS];                    // S fragments (B operand of D and O)
+    const float* bch = (const float*)(rc + R::B);
+    if (producer) {
+      if (R::NBUF == 2 && c + 1 < nch) wait_vm<R::NBUF == 2 ? R::LOADS : 0>();
+      else wait_vm<0>();
+    }
+    block_sync_lds();                      // chunk c's operands visible; chunk c-1 done
+    if (!producer) {
 #pragma unroll
-    for (int i = 0; i < KPW; ++i)
+      for (int i = 0; i < KPW; ++i)
 #pragma unroll
-      for (int nb = 0; nb < NB; ++nb) {
-        const int kt = KPW * w + i;
-        *(QR*)&sm.S[nb * 16 + fcol(lane)][kt * 16 + frow(lane, 0)] = Quad<E>::pack(acc[i][nb]);
-        if (p.saved) {
+        for (int nb = 0; nb < NB; ++nb) {
+          const int kt = KPW * w + i;
+          *(QR*)&sm.u.s.S[nb * 16 + fcol(lane)][kt * 16 + frow(lane, 0)] = Quad<E>::pack(acc[i][nb]);
+          if (p.saved) {
 #pragma unroll
-          for (int j = 0; j < 4; ++j) sm.Sf[kt * 16 + frow(lane, j)][nb * 16 + fcol(lane)] = acc[i][nb][j];
+            for (int j = 0; j < 4; ++j) sm.u.s.Sf[kt * 16 + frow(lane, j)][nb * 16 + fcol(lane)] = acc[i][nb][j];
+          }
+        }
+    }
+    block_sync_lds();
+    if (!producer) {
+      if (p.saved) {
+        // saved entry state, transposed (element (k, v) at [k][v]), 16-byte stores
+        float* dst = p.saved + gi * DK * DV + v0;
+        for (int idx = tid; idx < DK * (BV / 4); idx += NTHREADS) {
+          const int r = idx / (BV / 4), c4 = (idx % (BV / 4)) * 4;
+          *(f4*)(dst + (size_t)r * DV + c4) = *(const f4*)&sm.u.s.Sf[r][c4];
         }
       }
-    block_sync_lds();
-    if (p.saved) {
-      // saved entry state, transposed (element (k, v) at [k][v]), 16-byte stores
-      float* dst = p.saved + gi * DK * DV + v0;
-      for (int idx = tid; idx < DK * (BV / 4); idx += NTHREADS) {
-        const int r = idx / (BV / 4), c4 = (idx % (BV / 4)) * 4;
-        *(f4*)(dst + (size_t)r * DV + c4) = *(const f4*)&sm.Sf[r][c4];
-      }
-    }
-    if (c + 1 < nch) prefetch(c + 1);
-    const float bl = sm.b[C - 1];
-    // S fragments (B operand, shared by D and O)
-    FR sf[NB][DK / KS];
+      const float bl = bch[C - 1];
+      // S fragments (B operand, shared by D and O)
 #pragma unroll
-    for (int nb = 0; nb < NB; ++nb)
+      for (int nb = 0; nb < NB; ++nb)
 #pragma unroll
-      for (int ks = 0; ks < DK / KS; ++ks)
-        sf[nb][ks] = Frag<E>::load(kmaj(&sm.S[0][0], LK), nb * 16, ks * KS, lane);
-    // D = U - W S^T (rows 16w..), to LDS as D^T and (diag(g_C/g) D)^T
-#pragma unroll
-    for (int nb = 0; nb < NB; ++nb) {
-      f4 d = zero4();
-#pragma unroll
-      for (int ks = 0; ks < DK / KS; ++ks) d = Mma<E>::mma(cur.W.f[ks], sf[nb][ks], d);
-      f4 dk;
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        d[j] = Quad<E>::get(cur.U[nb], j) - d[j];
-        dk[j] = __expf(bl - sm.b[16 * w + frow(lane, j)]) * d[j];
-      }
-      *(QR*)&sm.Dt[nb * 16 + fcol(lane)][16 * w + frow(lane, 0)] = Quad<E>::pack(d);
-      *(QR*)&sm.Dkt[nb * 16 + fcol(lane)][16 * w + frow(lane, 0)] = Quad<E>::pack(dk);
-      if (p.saved) {
-#pragma unroll
-        for (int j = 0; j < 4; ++j) sm.Dr[16 * w + frow(lane, j)][nb * 16 + fcol(lane)] = fromf<E>(d[j]);
-      }
-    }
-    block_sync_lds();
-    if (p.saved) {
-      // D rows of this tile into the saved context (rows past the chunk are zero)
-      constexpr int VEC = 16 / sizeof(E), PR = BV / VEC;
-      E* dbase = (E*)p.savedD + gi * C * DV + v0;
-      for (int idx = tid; idx < C * PR; idx += NTHREADS) {
-        const int r = idx / PR, cc = (idx % PR) * VEC;
-        *(uint4*)(dbase + (size_t)r * DV + cc) = *(const uint4*)&sm.Dr[r][cc];
-      }
-    }
-    if (with_o) {
-      // O = diag(g) Q S^T + P D   (rows 16w..)
+        for (int ks = 0; ks < DK / KS; ++ks)
+          sf[nb][ks] = Frag<E>::load(kmaj(&sm.u.s.S[0][0], LK), nb * 16, ks * KS, lane);
+      // D = U - W S^T (rows 16w..), to LDS as D^T and (diag(g_C/g) D)^T
 #pragma unroll
       for (int nb = 0; nb < NB; ++nb) {
-        f4 o1 = zero4(), o2 = zero4();
+        f4 d = zero4();
 #pragma unroll
-        for (int ks = 0; ks < DK / KS; ++ks) o1 = Mma<E>::mma(cur.Q.f[ks], sf[nb][ks], o1);
-#pragma unroll
-        for (int ks = 0; ks < C / KS; ++ks)
-          o2 = Mma<E>::mma(cur.P.f[ks], Frag<E>::load(kmaj(&sm.Dt[0][0], LC), nb * 16, ks * KS, lane), o2);
+        for (int ks = 0; ks < DK / KS; ++ks)
+          d = Mma<E>::mma(tile_frag<E, R::RK>(rc + R::W, 16 * w, ks * KS, lane), sf[nb][ks], d);
+        const QR uq = *(const QR*)(rc + R::U + ((w * NB + nb) * 64 + lane) * 4 * sizeof(E));
+        f4 dk;
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
-          const int r = 16 * w + frow(lane, j);
-          sm.O[r][nb * 16 + fcol(lane)] = fromf<E>(__expf(sm.b[r]) * o1[j] + o2[j]);
+          d[j] = Quad<E>::get(uq, j) - d[j];
+          dk[j] = __expf(bl - bch[16 * w + frow(lane, j)]) * d[j];
+        }
+        *(QR*)&sm.Dt[nb * 16 + fcol(lane)][16 * w + frow(lane, 0)] = Quad<E>::pack(d);
+        *(QR*)&sm.Dkt[nb * 16 + fcol(lane)][16 * w + frow(lane, 0)] = Quad<E>::pack(dk);
+      }
+    }
+    block_sync_lds();
+    if (!producer) {
+      if (p.saved) {
+        // D rows of this tile into the saved context (rows past the chunk are zero),
+        // read back from D^T; one thread per (row, 8-column group)
+        constexpr int VEC = 16 / sizeof(E), PR = BV / VEC;
+        E* dbase = (E*)p.savedD + gi * C * DV + v0;
+        for (int idx = tid; idx < C * PR; idx += NTHREADS) {
+          const int r = idx % C, cc = (idx / C) * VEC;
+          uint4 o;
+          E* oe = (E*)&o;
+#pragma unroll
+          for (int j = 0; j < VEC; ++j) oe[j] = sm.Dt[cc + j][r];
+          *(uint4*)(dbase + (size_t)r * DV + cc) = o;
+        }
+      }
+      const float bl = bch[C - 1];
+      if (with_o) {
+        // O = diag(g) Q S^T + P D   (rows 16w..)
+        f4 oo[NB];
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb) {
+          f4 o1 = zero4(), o2 = zero4();
+#pragma unroll
+          for (int ks = 0; ks < DK / KS; ++ks)
+            o1 = Mma<E>::mma(tile_frag<E, R::RK>(rc + R::Q, 16 * w, ks * KS, lane), sf[nb][ks], o1);
+#pragma unroll
+          for (int ks = 0; ks < C / KS; ++ks)
+            o2 = Mma<E>::mma(tile_frag<E, R::RC>(rc + R::PP, 16 * w, ks * KS, lane),
+                             Frag<E>::load(kmaj(&sm.Dt[0][0], LC), nb * 16, ks * KS, lane), o2);
+#pragma unroll
+          for (int j = 0; j < 4; ++j) oo[nb][j] = __expf(bch[16 * w + frow(lane, j)]) * o1[j] + o2[j];
+        }
+        // S^T <- g_C S^T + K^T diag(g_C/g) D
+        const float gC = __expf(bl);
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb) {
+#pragma unroll
+          for (int i = 0; i < KPW; ++i) acc[i][nb] = gC * acc[i][nb];
+#pragma unroll
+          for (int ks = 0; ks < C / KS; ++ks) {
+            const FR bf = Frag<E>::load(kmaj(&sm.Dkt[0][0], LC), nb * 16, ks * KS, lane);
+#pragma unroll
+            for (int i = 0; i < KPW; ++i)
+              acc[i][nb] = Mma<E>::mma(tile_frag<E, R::RC>(rc + R::KT, 16 * (KPW * w + i), ks * KS, lane), bf,
+                                       acc[i][nb]);
+          }
+        }
+        // the state copies aliased by O were last read before the previous barrier
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+          for (int j = 0; j < 4; ++j) sm.u.O[16 * w + frow(lane, j)][nb * 16 + fcol(lane)] = fromf<E>(oo[nb][j]);
+      } else {
+        const float gC = __expf(bl);
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb) {
+#pragma unroll
+          for (int i = 0; i < KPW; ++i) acc[i][nb] = gC * acc[i][nb];
+#pragma unroll
+          for (int ks = 0; ks < C / KS; ++ks) {
+            const FR bf = Frag<E>::load(kmaj(&sm.Dkt[0][0], LC), nb * 16, ks * KS, lane);
+#pragma unroll
+            for (int i = 0; i < KPW; ++i)
+              acc[i][nb] = Mma<E>::mma(tile_frag<E, R::RC>(rc + R::KT, 16 * (KPW * w + i), ks * KS, lane), bf,
+                                       acc[i][nb]);
+          }
         }
       }
     }
-    // S^T <- g_C S^T + K^T diag(g_C/g) D
-    const float gC = __expf(bl);
-#pragma unroll
-    for (int nb = 0; nb < NB; ++nb) {
-#pragma unroll
-      for (int i = 0; i < KPW; ++i) acc[i][nb] = gC * acc[i][nb];
-#pragma unroll
-      for (int ks = 0; ks < C / KS; ++ks) {
-        const FR bf = Frag<E>::load(kmaj(&sm.Dkt[0][0], LC), nb * 16, ks * KS, lane);
-#pragma unroll
-        for (int i = 0; i < KPW; ++i) acc[i][nb] = Mma<E>::mma(cur.Kt[i].f[ks], bf, acc[i][nb]);
-      }
-    }
-    if (with_o) {
-      block_sync_lds();
+    block_sync_lds();                      // chunk c's ring buffer and O tile complete
+    if (producer) {
+      if (R::NBUF == 2 && c + 2 < nch) issue(c + 2, c & 1);
+      if (R::NBUF == 1 && c + 1 < nch) issue(c + 1, 0);
+    } else if (with_o) {
       constexpr int VEC = 16 / sizeof(E), PR = BV / VEC;
       E* obase = (E*)p.o + ((size_t)t0 * H + h) * DV + v0;
       for (int idx = tid; idx < C * PR; idx += NTHREADS) {
         const int r = idx / PR, cc = (idx % PR) * VEC;
-        if (r < len) *(uint4*)(obase + (size_t)r * H * DV + cc) = *(const uint4*)&sm.O[r][cc];
+        if (r < len) *(uint4*)(obase + (size_t)r * H * DV + cc) = *(const uint4*)&sm.u.O[r][cc];
       }
     }
   }
-  if (p.Sfin) {
+  if (p.Sfin && !producer) {
 #pragma unroll
     for (int i = 0; i < KPW; ++i)
 #pragma unroll
@@ -472,7 +529,7 @@ static hipError_t launch_fwd_t(const Params& p, int bwd_prep, int with_scan, hip
     const int nb = ((units + 7) / 8) * 8 * (DV / BV);
     if (nb > 0) {
       prof_mark(ST_SCAN_FWD, 0, st);
-      hipLaunchKernelGGL((k_scan_fwd<E, DK, DV, BV>), dim3(nb), dim3(NTHREADS), 0, st, p);
+      hipLaunchKernelGGL((k_scan_fwd<E, DK, DV, BV>), dim3(nb), dim3(NTHREADS + 64), 0, st, p);
       prof_mark(ST_SCAN_FWD, 1, st);
     }
   }
