@@ -244,8 +244,10 @@ struct alignas(16) BwdSmem {
   // bf16 operands need explicit transposed copies of dG and dQK for
   // contiguous fragment loads; fp32 fragments are single scalars either way
   static constexpr bool TCOPY = sizeof(E) == 2;
-  float b[C], g[C], kb[C], beta[C], lam[C], db[C], dbeta[C], dlam[C], tk[C];
-  float sdot[NWAVES];
+  float b[C], g[C], kb[C], beta[C], lam[C], db[C], dbeta[C];
+  float rsum[5][2][C];      // per-row partial sums of the two column halves:
+                            // dbeta rows, decay rows (B2); decay, Kbar, dlambda rows (B3)
+  float sdot[2];
   union {
     alignas(16) char tiles[TileA<E, DK>::NBUF][TileA<E, DK>::BYTES];   // phase A
     struct {
@@ -258,9 +260,9 @@ struct alignas(16) BwdSmem {
         struct {
           E MT[C][C + P];       // M^T (i, r)
           E dMt[C][C + P];      // (dT diag(beta))^T (i, r)
-          E Y[C][C + P];        // M^T dT diag(beta) (r, i), rows private to their wave
-          float dbc[4 * NWAVES][C];   // column partial sums of dT (.) M, per wave and lane group
-          float ecc[4 * NWAVES][C];   // column partial sums of the decay-gradient terms
+          E Y[2][C][C + P];     // M^T dT diag(beta) (r, i), one copy per column half
+          float dbc[16][C];     // column partial sums of dT (.) M, per row block and lane group
+          float ecc[16][C];     // column partial sums of the decay-gradient terms
         } b2;
         struct {
           E dWt[DK][C + P];     // dW^T (k, r)
@@ -311,17 +313,36 @@ __device__ inline float mix_tokens<float>(float kf, float qf, const float* lam) 
   return kf + lam[0] * qf;
 }
 
+// Eight waves: wave w takes rows 16 rb.. (rb = w & 3) of every C-row operand
+// and one half (ch = w >> 2) of the Dk column blocks and of the C x C column
+// blocks; two waves share each SIMD and hide each other's latency.
+constexpr int INTRA_THREADS = 2 * NTHREADS;
+
 template <typename E, int DK, int DV>
-__global__ __launch_bounds__(NTHREADS) void k_bwd_intra(Params p) {
+__global__ __launch_bounds__(INTRA_THREADS) void k_bwd_intra(Params p) {
   constexpr int P = Pad<E>::v;
   constexpr int BV = 32;
   constexpr int LC = C + P;
   constexpr int KS = Mma<E>::KS;
   constexpr int NKB = DK / 16;        // 16-column blocks of Dk
+  constexpr int HK = NKB / 2;         // Dk blocks per column half
   constexpr int NVT = DV / BV;
+  constexpr int IT = INTRA_THREADS;
   typedef typename Mma<E>::frag FR;
+  typedef typename Quad<E>::raw QR;
   __shared__ BwdSmem<E, DK> sm;
-  const int g = blockIdx.x, h = blockIdx.y, tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  if ((int)blockIdx.x < p.lead) {
+    // a leading workgroup holds its CU for about half a unit, so that half of
+    // the CUs run phase-shifted and their value-dimension loads overlap the
+    // other half's compute phases
+    const long long t0c = clock64();
+    while (clock64() - t0c < p.lead_cycles) __builtin_amdgcn_s_sleep(32);
+    return;
+  }
+  const int bid = (int)blockIdx.x - p.lead;
+  const int g = bid % p.n_slots, h = bid / p.n_slots, tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int rb = w & 3, ch = w >> 2;
+  const int kb0 = ch * HK, ib0 = 2 * ch;
   int n, t0, len;
   if (!locate(p, g, n, t0, len)) return;
   const int H = p.H;
@@ -335,11 +356,11 @@ __global__ __launch_bounds__(NTHREADS) void k_bwd_intra(Params p) {
 
   // ---------------- phase A: contractions over the value dimension
   typedef TileA<E, DK> TA;
-  f4 aQ[NKB], aK[NKB], aW[NKB], aP[4], aT[4];
+  f4 aQ[HK], aK[HK], aW[HK], aP[2], aT[2];
 #pragma unroll
-  for (int i = 0; i < NKB; ++i) aQ[i] = aK[i] = aW[i] = zero4();
+  for (int i = 0; i < HK; ++i) aQ[i] = aK[i] = aW[i] = zero4();
 #pragma unroll
-  for (int i = 0; i < 4; ++i) aP[i] = aT[i] = zero4();
+  for (int i = 0; i < 2; ++i) aP[i] = aT[i] = zero4();
   float sdot = 0.f;
   constexpr size_t ES = sizeof(E);
   const char* Sg = (const char*)(p.saved + gi * DK * DV);
@@ -349,13 +370,15 @@ __global__ __launch_bounds__(NTHREADS) void k_bwd_intra(Params p) {
   const char* dOg = (const char*)((const E*)p.dO + arow * DV);
   const char* Vg = (const char*)((const E*)p.v + arow * DV);
   // phase-B operands first, so that they are older than every tile load
-  TileRegs<E, C, DK> rKf, rQf;    // chunk K, Q rows for phase B1
+  TileRegs<E, C, DK, IT> rKf, rQf;    // chunk K, Q rows for phase B1
   rKf.load_clamped((const E*)p.k + arow * DK, (size_t)H * DK, len, tid);
   rQf.load_clamped((const E*)p.q + arow * DK, (size_t)H * DK, len, tid);
   asm volatile("" ::: "memory");
+  // direct loads are issued by waves 0-3 only; the others' waits are no-ops
+  const bool loader = w < NWAVES;
   // M = (I + A)^{-1} and T^T from the preparation
   constexpr int RBC = C * (int)sizeof(E);
-  {
+  if (loader) {
     const char* Mg = (const char*)((const E*)p.wM + gi * C * C);
     const char* Tg = (const char*)((const E*)p.wT + gi * 2 * C * C);
     dma_rows<RBC, C>(sm.Mm, Mg, RBC, C, Mg, 0, w, lane);
@@ -373,9 +396,12 @@ __global__ __launch_bounds__(NTHREADS) void k_bwd_intra(Params p) {
     dma_rows<TA::RE, C>(t + TA::DO, dOg + vb * ES, (size_t)H * DV * ES, len, Dg + vb * ES, DV * ES, w, lane);
   };
   constexpr int NB0 = NVT < TA::NBUF ? NVT : TA::NBUF;
+  if (loader) {
 #pragma unroll
-  for (int vt = 0; vt < NB0; ++vt) issue(vt);
-#pragma unroll
+    for (int vt = 0; vt < NB0; ++vt) issue(vt);
+  }
+  constexpr int UVT = NVT > 4 ? 1 : NVT;   // full unroll only for short tile loops
+#pragma unroll UVT
   for (int vt = 0; vt < NVT; ++vt) {
     // tile vt is complete once at most `after` tiles' loads are outstanding
     const int after = (vt == 0 ? NB0 : min(NVT, vt + TA::NBUF - 1)) - 1 - vt;
@@ -383,45 +409,45 @@ __global__ __launch_bounds__(NTHREADS) void k_bwd_intra(Params p) {
     else if (after == 1) wait_vm<TA::LOADS>();
     else wait_vm<0>();
     block_sync_lds();                 // tile vt visible; tile vt-1's buffer is free
-    if (vt >= 1 && vt + TA::NBUF - 1 < NVT) issue(vt + TA::NBUF - 1);
+    if (loader && vt >= 1 && vt + TA::NBUF - 1 < NVT) issue(vt + TA::NBUF - 1);
     const char* t = &sm.x.tiles[vt % TA::NBUF][0];
 #pragma unroll
     for (int ks = 0; ks < BV / KS; ++ks) {
-      const FR aO = tile_frag<E, TA::RE>(t + TA::DO, 16 * w, ks * KS, lane);
-      const FR adD = tile_frag<E, TA::RE>(t + TA::DD, 16 * w, ks * KS, lane);
-      const FR aD = tile_frag<E, TA::RE>(t + TA::D, 16 * w, ks * KS, lane);
+      const FR aO = tile_frag<E, TA::RE>(t + TA::DO, 16 * rb, ks * KS, lane);
+      const FR adD = tile_frag<E, TA::RE>(t + TA::DD, 16 * rb, ks * KS, lane);
+      const FR aD = tile_frag<E, TA::RE>(t + TA::D, 16 * rb, ks * KS, lane);
 #pragma unroll
-      for (int kb = 0; kb < NKB; ++kb) {
+      for (int i = 0; i < HK; ++i) {
+        const int kb = kb0 + i;
         float sv[Mma<E>::KPL];
         const FR bS = tile_frag_f32<E>(t + TA::S, kb * 16, ks * KS, lane, sv);
         const FR bdS = tile_frag<E, TA::RE>(t + TA::DS, kb * 16, ks * KS, lane);
-        aQ[kb] = Mma<E>::mma(aO, bS, aQ[kb]);
-        aW[kb] = Mma<E>::mma(adD, bS, aW[kb]);
-        aK[kb] = Mma<E>::mma(aD, bdS, aK[kb]);
+        aQ[i] = Mma<E>::mma(aO, bS, aQ[i]);
+        aW[i] = Mma<E>::mma(adD, bS, aW[i]);
+        aK[i] = Mma<E>::mma(aD, bdS, aK[i]);
         const E* de = (const E*)&bdS;
 #pragma unroll
         for (int e = 0; e < Mma<E>::KPL; ++e) sdot += sv[e] * tof(de[e]);
       }
 #pragma unroll
-      for (int ib = 0; ib < 4; ++ib) {
+      for (int i = 0; i < 2; ++i) {
+        const int ib = ib0 + i;
         const FR bD = tile_frag<E, TA::RE>(t + TA::D, ib * 16, ks * KS, lane);
         const FR bV = tile_frag<E, TA::RE>(t + TA::V, ib * 16, ks * KS, lane);
-        aP[ib] = Mma<E>::mma(aO, bD, aP[ib]);
-        aT[ib] = Mma<E>::mma(adD, bV, aT[ib]);
+        aP[i] = Mma<E>::mma(aO, bD, aP[i]);
+        aT[i] = Mma<E>::mma(adD, bV, aT[i]);
       }
     }
   }
-  // every wave read the whole of S^T and dS'^T: one copy of <S, dS'> suffices
+  // the two row-block-0 waves together read all of S^T and dS'^T once
   sdot = wave_sum(sdot);
-  if (tid == 0) sm.sdot[0] = sdot;
+  if (rb == 0 && lane == 0) sm.sdot[ch] = sdot;
   if (tid < C) {
     const bool ok = tid < len;
     sm.b[tid] = gb;
     sm.g[tid] = __expf(gb);
     sm.beta[tid] = ok ? gbeta : 0.f;
     sm.lam[tid] = ok ? glam : 0.f;
-    sm.dlam[tid] = 0.f;
-    sm.tk[tid] = 0.f;
   }
 
   // ---------------- phase B1: G = X K^T, QK = Q K^T, dT2 = dW (g X)^T
@@ -430,89 +456,93 @@ __global__ __launch_bounds__(NTHREADS) void k_bwd_intra(Params p) {
   rKf.store_rows(&sm.x.s.u.b1.K[0][0], LKD, len, tid);
   rQf.store_rows(&sm.x.s.u.b1.Q[0][0], LKD, len, tid);
 #pragma unroll
-  for (int kb = 0; kb < NKB; ++kb)
+  for (int i = 0; i < HK; ++i)
 #pragma unroll
-    for (int j = 0; j < 4; ++j) sm.x.s.u.b1.dW[16 * w + frow(lane, j)][kb * 16 + fcol(lane)] = fromf<E>(-aW[kb][j]);
+    for (int j = 0; j < 4; ++j)
+      sm.x.s.u.b1.dW[16 * rb + frow(lane, j)][(kb0 + i) * 16 + fcol(lane)] = fromf<E>(-aW[i][j]);
   if (tid < C) sm.kb[tid] = __expf(sm.b[C - 1] - sm.b[tid]);
   block_sync_lds();
-  f4 aG[4], aQK[4], adT[4];
+  f4 aG[2], aQK[2], adT[2];
 #pragma unroll
-  for (int i = 0; i < 4; ++i) aG[i] = aQK[i] = adT[i] = zero4();
+  for (int i = 0; i < 2; ++i) aG[i] = aQK[i] = adT[i] = zero4();
   {
-    const float lam_a = sm.lam[16 * w + (lane & 15)];
-    float lam_b[4], g_b[4];
+    const float lam_a = sm.lam[16 * rb + (lane & 15)];
+    float lam_b[2], g_b[2];
 #pragma unroll
-    for (int ib = 0; ib < 4; ++ib) {
-      lam_b[ib] = sm.lam[ib * 16 + (lane & 15)];
-      g_b[ib] = sm.g[ib * 16 + (lane & 15)];
+    for (int i = 0; i < 2; ++i) {
+      lam_b[i] = sm.lam[(ib0 + i) * 16 + (lane & 15)];
+      g_b[i] = sm.g[(ib0 + i) * 16 + (lane & 15)];
     }
 #pragma unroll
     for (int ks = 0; ks < DK / KS; ++ks) {
-      const FR kA = Frag<E>::load(kmaj(&sm.x.s.u.b1.K[0][0], LKD), 16 * w, ks * KS, lane);
-      const FR qA = Frag<E>::load(kmaj(&sm.x.s.u.b1.Q[0][0], LKD), 16 * w, ks * KS, lane);
+      const FR kA = Frag<E>::load(kmaj(&sm.x.s.u.b1.K[0][0], LKD), 16 * rb, ks * KS, lane);
+      const FR qA = Frag<E>::load(kmaj(&sm.x.s.u.b1.Q[0][0], LKD), 16 * rb, ks * KS, lane);
       const FR xA = mix_frag<FR>(kA, qA, lam_a, 1.f);
-      const FR dwA = Frag<E>::load(kmaj(&sm.x.s.u.b1.dW[0][0], LKD), 16 * w, ks * KS, lane);
+      const FR dwA = Frag<E>::load(kmaj(&sm.x.s.u.b1.dW[0][0], LKD), 16 * rb, ks * KS, lane);
 #pragma unroll
-      for (int ib = 0; ib < 4; ++ib) {
+      for (int i = 0; i < 2; ++i) {
+        const int ib = ib0 + i;
         const FR kB = Frag<E>::load(kmaj(&sm.x.s.u.b1.K[0][0], LKD), ib * 16, ks * KS, lane);
         const FR qB = Frag<E>::load(kmaj(&sm.x.s.u.b1.Q[0][0], LKD), ib * 16, ks * KS, lane);
-        const FR gxB = mix_frag<FR>(kB, qB, lam_b[ib], g_b[ib]);
-        aG[ib] = Mma<E>::mma(xA, kB, aG[ib]);
-        aQK[ib] = Mma<E>::mma(qA, kB, aQK[ib]);
-        adT[ib] = Mma<E>::mma(dwA, gxB, adT[ib]);
+        const FR gxB = mix_frag<FR>(kB, qB, lam_b[i], g_b[i]);
+        aG[i] = Mma<E>::mma(xA, kB, aG[i]);
+        aQK[i] = Mma<E>::mma(qA, kB, aQK[i]);
+        adT[i] = Mma<E>::mma(dwA, gxB, adT[i]);
       }
     }
   }
   // K^T and Q^T for phase B3, in flight during phase B2
-  TileRegs<E, DK, C> rKt, rQt;
+  TileRegs<E, DK, C, IT> rKt, rQt;
   rKt.load((const E*)p.wKt + gi * DK * C, C, DK, tid);
   rQt.load((const E*)p.wQt + gi * DK * C, C, DK, tid);
 
   // ---------------- phase B2: UT-solve backward and the C x C gradient terms.
-  // Lane (w, lane) holds element (r, c) = (16w + frow(lane, j), 16ib + fcol(lane))
-  // of every C x C accumulator.
-  const int rw = 16 * w + frow(lane, 0), cl = fcol(lane);
+  // Lane (w, lane) holds element (r, c) = (16 rb + frow(lane, j), 16 ib + fcol(lane))
+  // of every C x C accumulator, for the two column blocks ib of its half.
+  const int rw = 16 * rb + frow(lane, 0), cl = fcol(lane);
   block_sync_lds();                    // K, Q, dW dead: the b2 buffers may be written
   {
     // dT = dD V^T + dW (g X)^T: column sums of dT (.) M feed dbeta; M^T and
     // (dT diag(beta))^T become the operands of Y = M^T dT diag(beta)
 #pragma unroll
-    for (int ib = 0; ib < 4; ++ib) {
-      const int c = ib * 16 + cl;
+    for (int i = 0; i < 2; ++i) {
+      const int c = (ib0 + i) * 16 + cl;
       const float bc = sm.beta[c];
       f4 mv, dm;
       float cs = 0.f;
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
         const float m = tof(*(const E*)(sm.Mm + tile_off<RBC>(rw + j, c * (int)sizeof(E))));
-        const float dt = aT[ib][j] + adT[ib][j];
+        const float dt = aT[i][j] + adT[i][j];
         cs += dt * m;
         mv[j] = m;
         dm[j] = dt * bc;
       }
-      *(typename Quad<E>::raw*)&sm.x.s.u.b2.MT[c][rw] = Quad<E>::pack(mv);
-      *(typename Quad<E>::raw*)&sm.x.s.u.b2.dMt[c][rw] = Quad<E>::pack(dm);
-      sm.x.s.u.b2.dbc[4 * w + (lane >> 4)][c] = cs;
+      *(QR*)&sm.x.s.u.b2.MT[c][rw] = Quad<E>::pack(mv);
+      *(QR*)&sm.x.s.u.b2.dMt[c][rw] = Quad<E>::pack(dm);
+      sm.x.s.u.b2.dbc[4 * rb + (lane >> 4)][c] = cs;
     }
   }
   block_sync_lds();
-  f4 adA[4];
+  f4 adA[2];
   {
+    // Y = M^T dMinv, rows 16 rb.. over all columns (each half keeps a copy)
 #pragma unroll
-    for (int ib = 0; ib < 4; ++ib) {        // Y = M^T dMinv, rows 16w..
-      const f4 y = mma_k<E, C>(kmaj(&sm.x.s.u.b2.MT[0][0], LC), kmaj(&sm.x.s.u.b2.dMt[0][0], LC), 16 * w, ib * 16, zero4(), lane);
+    for (int ib = 0; ib < 4; ++ib) {
+      const f4 y = mma_k<E, C>(kmaj(&sm.x.s.u.b2.MT[0][0], LC), kmaj(&sm.x.s.u.b2.dMt[0][0], LC), 16 * rb, ib * 16,
+                               zero4(), lane);
 #pragma unroll
-      for (int j = 0; j < 4; ++j) sm.x.s.u.b2.Y[rw + j][ib * 16 + cl] = fromf<E>(y[j]);
+      for (int j = 0; j < 4; ++j) sm.x.s.u.b2.Y[ch][rw + j][ib * 16 + cl] = fromf<E>(y[j]);
     }
-    // Y rows 16w.. are read back by this wave only
+    // this copy of Y rows 16 rb.. is read back by this wave only
     asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
 #pragma unroll
-    for (int ib = 0; ib < 4; ++ib) {        // dA = strictLower(-Y M^T)
-      adA[ib] = zero4();
+    for (int i = 0; i < 2; ++i) {           // dA = strictLower(-Y M^T)
+      adA[i] = zero4();
 #pragma unroll
       for (int ks = 0; ks < C / KS; ++ks)
-        adA[ib] = Mma<E>::mma(Frag<E>::load(kmaj(&sm.x.s.u.b2.Y[0][0], LC), 16 * w, ks * KS, lane),
-                              tile_frag<E, RBC>(sm.Mm, ib * 16, ks * KS, lane), adA[ib]);
+        adA[i] = Mma<E>::mma(Frag<E>::load(kmaj(&sm.x.s.u.b2.Y[ch][0][0], LC), 16 * rb, ks * KS, lane),
+                             tile_frag<E, RBC>(sm.Mm, (ib0 + i) * 16, ks * KS, lane), adA[i]);
     }
   }
   {
@@ -526,8 +556,8 @@ __global__ __launch_bounds__(NTHREADS) void k_bwd_intra(Params p) {
       betar[j] = sm.beta[rw + j];
     }
 #pragma unroll
-    for (int ib = 0; ib < 4; ++ib) {
-      const int c = ib * 16 + cl;
+    for (int i = 0; i < 2; ++i) {
+      const int c = (ib0 + i) * 16 + cl;
       const float bc = sm.b[c];
       f4 vg, vq;
       float ec = 0.f;
@@ -535,12 +565,12 @@ __global__ __launch_bounds__(NTHREADS) void k_bwd_intra(Params p) {
       for (int j = 0; j < 4; ++j) {
         const int r = rw + j;
         const float gam = (r >= c) ? __expf(br[j] - bc) : 0.f;
-        const float dA = (r > c) ? -adA[ib][j] : 0.f;
+        const float dA = (r > c) ? -adA[i][j] : 0.f;
         const float dAg = dA * gam;
         const float dg = dAg * betar[j];
-        const float dqk = aP[ib][j] * gam;
-        const float t = dg * aG[ib][j] + dqk * aQK[ib][j];
-        dbr[j] += dAg * aG[ib][j];
+        const float dqk = aP[i][j] * gam;
+        const float t = dg * aG[i][j] + dqk * aQK[i][j];
+        dbr[j] += dAg * aG[i][j];
         er[j] += t;
         ec += t;
         vg[j] = dg;
@@ -549,10 +579,10 @@ __global__ __launch_bounds__(NTHREADS) void k_bwd_intra(Params p) {
         sm.x.s.dQK[r][c] = fromf<E>(dqk);
       }
       if constexpr (BwdSmem<E, DK>::TCOPY) {
-        *(typename Quad<E>::raw*)&sm.x.s.dGt[c][rw] = Quad<E>::pack(vg);
-        *(typename Quad<E>::raw*)&sm.x.s.dQKt[c][rw] = Quad<E>::pack(vq);
+        *(QR*)&sm.x.s.dGt[c][rw] = Quad<E>::pack(vg);
+        *(QR*)&sm.x.s.dQKt[c][rw] = Quad<E>::pack(vq);
       }
-      sm.x.s.u.b2.ecc[4 * w + (lane >> 4)][c] = ec;
+      sm.x.s.u.b2.ecc[4 * rb + (lane >> 4)][c] = ec;
     }
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
@@ -562,34 +592,34 @@ __global__ __launch_bounds__(NTHREADS) void k_bwd_intra(Params p) {
     if (cl == 0) {
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
-        sm.dbeta[rw + j] = dbr[j];
-        sm.db[rw + j] = er[j];
+        sm.rsum[0][ch][rw + j] = dbr[j];
+        sm.rsum[1][ch][rw + j] = er[j];
       }
     }
   }
   block_sync_lds();
   if (tid < C) {
-    // column parts: dbeta += colsum(dT (.) M), db -= colsum of the decay terms
+    // dbeta = row parts + colsum(dT (.) M); db = row parts - column parts of the decay terms
     float cb = 0.f, ce = 0.f;
 #pragma unroll
-    for (int v = 0; v < 4 * NWAVES; ++v) {
+    for (int v = 0; v < 16; ++v) {
       cb += sm.x.s.u.b2.dbc[v][tid];
       ce += sm.x.s.u.b2.ecc[v][tid];
     }
-    sm.dbeta[tid] += cb;
-    sm.db[tid] -= ce;
+    sm.dbeta[tid] = sm.rsum[0][0][tid] + sm.rsum[0][1][tid] + cb;
+    sm.db[tid] = sm.rsum[1][0][tid] + sm.rsum[1][1][tid] - ce;
   }
   block_sync_lds();                    // the b2 buffers are dead past here
 
-  // ---------------- phase B3: dX, dq, dk (wave w owns rows 16w..)
+  // ---------------- phase B3: dX, dq, dk (rows 16 rb.., Dk blocks of this half)
   rKt.store(&sm.x.s.u.b3.Kt[0][0], LC, tid);
   rQt.store(&sm.x.s.u.b3.Qt[0][0], LC, tid);
 #pragma unroll
-  for (int kb = 0; kb < NKB; ++kb) {
+  for (int i = 0; i < HK; ++i) {
     f4 nw;
 #pragma unroll
-    for (int j = 0; j < 4; ++j) nw[j] = -aW[kb][j];
-    *(typename Quad<E>::raw*)&sm.x.s.u.b3.dWt[kb * 16 + fcol(lane)][16 * w + frow(lane, 0)] = Quad<E>::pack(nw);
+    for (int j = 0; j < 4; ++j) nw[j] = -aW[i][j];
+    *(QR*)&sm.x.s.u.b3.dWt[(kb0 + i) * 16 + fcol(lane)][16 * rb + frow(lane, 0)] = Quad<E>::pack(nw);
   }
   block_sync_lds();
   {
@@ -598,20 +628,20 @@ __global__ __launch_bounds__(NTHREADS) void k_bwd_intra(Params p) {
     float lamk[NTK][Mma<E>::KPL];
 #pragma unroll
     for (int ks = 0; ks < NTK; ++ks) {
-      tA[ks] = tile_frag<E, RBC>(sm.TmT, 16 * w, ks * KS, lane);
-      gA[ks] = Frag<E>::load(kmaj(&sm.x.s.dG[0][0], LC), 16 * w, ks * KS, lane);
-      qkA[ks] = Frag<E>::load(kmaj(&sm.x.s.dQK[0][0], LC), 16 * w, ks * KS, lane);
+      tA[ks] = tile_frag<E, RBC>(sm.TmT, 16 * rb, ks * KS, lane);
+      gA[ks] = Frag<E>::load(kmaj(&sm.x.s.dG[0][0], LC), 16 * rb, ks * KS, lane);
+      qkA[ks] = Frag<E>::load(kmaj(&sm.x.s.dQK[0][0], LC), 16 * rb, ks * KS, lane);
       if constexpr (BwdSmem<E, DK>::TCOPY) {
-        qktA[ks] = Frag<E>::load(kmaj(&sm.x.s.dQKt[0][0], LC), 16 * w, ks * KS, lane);
-        gtA[ks] = Frag<E>::load(kmaj(&sm.x.s.dGt[0][0], LC), 16 * w, ks * KS, lane);
+        qktA[ks] = Frag<E>::load(kmaj(&sm.x.s.dQKt[0][0], LC), 16 * rb, ks * KS, lane);
+        gtA[ks] = Frag<E>::load(kmaj(&sm.x.s.dGt[0][0], LC), 16 * rb, ks * KS, lane);
       } else {
-        qktA[ks] = Frag<E>::load(imaj(&sm.x.s.dQK[0][0], LC), 16 * w, ks * KS, lane);
-        gtA[ks] = Frag<E>::load(imaj(&sm.x.s.dG[0][0], LC), 16 * w, ks * KS, lane);
+        qktA[ks] = Frag<E>::load(imaj(&sm.x.s.dQK[0][0], LC), 16 * rb, ks * KS, lane);
+        gtA[ks] = Frag<E>::load(imaj(&sm.x.s.dG[0][0], LC), 16 * rb, ks * KS, lane);
       }
 #pragma unroll
       for (int e = 0; e < Mma<E>::KPL; ++e) lamk[ks][e] = sm.lam[ks * KS + (lane >> 4) * Mma<E>::KPL + e];
     }
-    const int r0 = 16 * w + frow(lane, 0);
+    const int r0 = 16 * rb + frow(lane, 0);
     float rdb[4] = {0.f, 0.f, 0.f, 0.f}, rtk[4] = {0.f, 0.f, 0.f, 0.f}, rdl[4] = {0.f, 0.f, 0.f, 0.f};
     float gr4[4], lr4[4], kbr4[4];
 #pragma unroll
@@ -621,7 +651,8 @@ __global__ __launch_bounds__(NTHREADS) void k_bwd_intra(Params p) {
       kbr4[j] = sm.kb[r0 + j];
     }
 #pragma unroll
-    for (int kb = 0; kb < NKB; ++kb) {
+    for (int i = 0; i < HK; ++i) {
+      const int kb = kb0 + i;
       f4 dgx = zero4(), dxp = zero4(), dqp = zero4(), dkp = zero4();
 #pragma unroll
       for (int ks = 0; ks < NTK; ++ks) {
@@ -636,20 +667,20 @@ __global__ __launch_bounds__(NTHREADS) void k_bwd_intra(Params p) {
         dkp = Mma<E>::mma(gtA[ks], xtB, dkp);     // dG^T X
       }
       const int kc = kb * 16 + fcol(lane);
-      const typename Quad<E>::raw kv = *(const typename Quad<E>::raw*)&sm.x.s.u.b3.Kt[kc][r0];
-      const typename Quad<E>::raw qv = *(const typename Quad<E>::raw*)&sm.x.s.u.b3.Qt[kc][r0];
+      const QR kv = *(const QR*)&sm.x.s.u.b3.Kt[kc][r0];
+      const QR qv = *(const QR*)&sm.x.s.u.b3.Qt[kc][r0];
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
         const int r = r0 + j;
         const float Kv = Quad<E>::get(kv, j), Qv = Quad<E>::get(qv, j);
         const float gr = gr4[j], lr = lr4[j], kbr = kbr4[j];
         const float X = Kv + lr * Qv;
-        rdb[j] += gr * (X * dgx[j] + Qv * aQ[kb][j]);
-        rtk[j] += kbr * Kv * aK[kb][j];
+        rdb[j] += gr * (X * dgx[j] + Qv * aQ[i][j]);
+        rtk[j] += kbr * Kv * aK[i][j];
         const float dX = gr * dgx[j] + dxp[j];
         rdl[j] += Qv * dX;
-        sm.x.s.u.b3.oq[r][kc] = fromf<E>(gr * aQ[kb][j] + dqp[j] + lr * dX);
-        sm.x.s.u.b3.ok[r][kc] = fromf<E>(kbr * aK[kb][j] + dkp[j] + dX);
+        sm.x.s.u.b3.oq[r][kc] = fromf<E>(gr * aQ[i][j] + dqp[j] + lr * dX);
+        sm.x.s.u.b3.ok[r][kc] = fromf<E>(kbr * aK[i][j] + dkp[j] + dX);
       }
     }
 #pragma unroll
@@ -661,9 +692,9 @@ __global__ __launch_bounds__(NTHREADS) void k_bwd_intra(Params p) {
     if (fcol(lane) == 0) {
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
-        sm.db[r0 + j] += rdb[j];
-        sm.tk[r0 + j] += rtk[j];
-        sm.dlam[r0 + j] += rdl[j];
+        sm.rsum[2][ch][r0 + j] = rdb[j];
+        sm.rsum[3][ch][r0 + j] = rtk[j];
+        sm.rsum[4][ch][r0 + j] = rdl[j];
       }
     }
   }
@@ -672,7 +703,7 @@ __global__ __launch_bounds__(NTHREADS) void k_bwd_intra(Params p) {
     constexpr int VEC = 16 / sizeof(E), PR = DK / VEC;
     E* dqo = (E*)p.dq + arow * DK;
     E* dko = (E*)p.dk + arow * DK;
-    for (int idx = tid; idx < C * PR; idx += NTHREADS) {
+    for (int idx = tid; idx < C * PR; idx += IT) {
       const int r = idx / PR, cc = (idx % PR) * VEC;
       if (r < len) {
         *(uint4*)(dqo + (size_t)r * H * DK + cc) = *(const uint4*)&sm.x.s.u.b3.oq[r][cc];
@@ -680,24 +711,23 @@ __global__ __launch_bounds__(NTHREADS) void k_bwd_intra(Params p) {
       }
     }
   }
-  block_sync_lds();
   if (tid < C) {
     // Kbar terms: db_r -= t_r, db_{C-1} += sum_r t_r + g_C <dS', S>;
     // then dlog alpha_j = sum_{r >= j} db_r (chunk-local reverse cumulative sum)
     const int j = tid;
-    float tot = sm.tk[j];
+    const float tk = sm.rsum[3][0][j] + sm.rsum[3][1][j];
+    float tot = tk;
 #pragma unroll
     for (int off = 32; off >= 1; off >>= 1) tot += __shfl_xor(tot, off, 64);
-    float dbj = sm.db[j] - sm.tk[j];
-    const float dbeta = sm.dbeta[j];
-    if (j == C - 1) dbj += tot + sm.g[C - 1] * sm.sdot[0];
+    float dbj = sm.db[j] + sm.rsum[2][0][j] + sm.rsum[2][1][j] - tk;
+    if (j == C - 1) dbj += tot + sm.g[C - 1] * (sm.sdot[0] + sm.sdot[1]);
     float x = __shfl(dbj, C - 1 - j, 64);
     x = wave_incl_scan(x, lane);
     const float suffix = __shfl(x, C - 1 - j, 64);
     if (j < len) {
       const size_t gt = arow + (size_t)j * H;
-      p.dbeta[gt] = dbeta;
-      p.dlam[gt] = sm.dlam[j];
+      p.dbeta[gt] = sm.dbeta[j];
+      p.dlam[gt] = sm.rsum[4][0][j] + sm.rsum[4][1][j];
       if (p.dla) p.dla[gt] = suffix;
     }
   }
@@ -715,9 +745,15 @@ static hipError_t launch_bwd_t(const Params& p, hipStream_t st) {
     prof_mark(ST_SCAN_BWD, 1, st);
   }
   if (p.n_slots > 0) {
-    dim3 gp(p.n_slots, p.H);
+    // Every unit costs the same, so without an offset all CUs would load
+    // their value-dimension tiles together and then compute together, leaving
+    // HBM idle half the time.  Half of the CUs start about half a unit later.
+    Params q = p;
+    const int total = p.n_slots * p.H, cus = device_cu_count();
+    q.lead = total >= 4 * cus ? cus / 2 : 0;
+    q.lead_cycles = 15000;
     prof_mark(ST_INTRA, 0, st);
-    hipLaunchKernelGGL((k_bwd_intra<E, DK, DV>), gp, dim3(NTHREADS), 0, st, p);
+    hipLaunchKernelGGL((k_bwd_intra<E, DK, DV>), dim3(total + q.lead), dim3(INTRA_THREADS), 0, st, q);
     prof_mark(ST_INTRA, 1, st);
   }
   return hipGetLastError();

@@ -435,6 +435,8 @@ struct Params {
   int H;
   int NT;         // dense: ceil(T / C)
   int n_slots;    // saved-state / workspace slots
+  int lead;         // intra-chunk backward: leading workgroups that only wait
+  int lead_cycles;  // ... and for how many clock cycles
   const int* cu;  // varlen cu_seqlens (device) or nullptr
   // forward inputs
   const void* q;
