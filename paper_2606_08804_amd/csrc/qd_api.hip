@@ -16,7 +16,7 @@ using qd::C;
 constexpr int kVersion = 10000;  // 1.0.0
 
 struct Layout {
-  size_t wb = 0, wU = 0, wW = 0, wP = 0, wKt = 0, wT = 0, wWt = 0, wQgt = 0, wQt = 0, wM = 0, wdOt = 0;
+  size_t wb = 0, wU = 0, wW = 0, wP = 0, wKt = 0, wT = 0, wWt = 0, wQt = 0, wM = 0, wdOt = 0;
   size_t dSo = 0, dDb = 0, states = 0;
   size_t total = 0;
 };
@@ -43,7 +43,6 @@ Layout make_layout(size_t units, int Dk, int Dv, int esz, bool bwd) {
   if (bwd) {
     L.wT = take(units * 2 * C * C * esz);
     L.wWt = take(units * C * Dk * esz);
-    L.wQgt = take(units * C * Dk * esz);
     L.wQt = take(units * C * Dk * esz);
     L.wM = take(units * C * C * esz);
     L.wdOt = take(units * C * Dv * esz);
@@ -195,7 +194,6 @@ int bwd_impl(bool varlen, int32_t B, int32_t T, int32_t N, const int32_t* cu, in
   p.wKt = w + L.wKt;
   p.wT = w + L.wT;
   p.wWt = w + L.wWt;
-  p.wQgt = w + L.wQgt;
   p.wQt = w + L.wQt;
   p.wM = w + L.wM;
   p.wdOt = w + L.wdOt;
@@ -208,11 +206,13 @@ int bwd_impl(bool varlen, int32_t B, int32_t T, int32_t N, const int32_t* cu, in
   const size_t units = s.slots * (size_t)H;
   hipError_t e;
   if (saved) {
+    p.prep_uw = 0;   // U and W only feed the forward scan, which does not run here
     p.saved = const_cast<float*>(static_cast<const float*>(saved));
     p.savedD = const_cast<char*>(static_cast<const char*>(saved)) + saved_states_bytes(units, Dk, Dv);
     e = qd::launch_fwd(p, dtype, Dk, Dv, 1, 0, stream);
   } else {
     // recompute the saved context (no outputs) into the workspace
+    p.prep_uw = 1;
     p.saved = reinterpret_cast<float*>(w + L.states);
     p.savedD = w + L.states + saved_states_bytes(units, Dk, Dv);
     e = qd::launch_fwd(p, dtype, Dk, Dv, 1, 1, stream);

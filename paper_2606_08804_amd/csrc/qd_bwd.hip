@@ -36,7 +36,7 @@ namespace qd {
 template <typename E, int DK, int BV>
 struct ScanBwdSmem {
   static constexpr int P = Pad<E>::v;
-  float b[C];
+  float b[C], g[C];
   E dS[BV][DK + P];   // dS' tile [v][k]
   E dDn[BV][C + P];   // -dD tile, transposed [v][r]
   E dDr[C][BV + P];   // dD tile staging [r][v]
@@ -51,7 +51,7 @@ struct ScanBwdPre {
   AFrag<E, C> PT;          // rows 16w.. of P^T
   AFrag<E, C> TT;          // rows 16w.. of T^T
   AFrag<E, DK> K;          // rows 16w.. of K
-  AFrag<E, C> Qg[KPW];     // rows of (diag(g) Q)^T for this wave's key blocks
+  AFrag<E, C> Qt[KPW];     // rows of Q^T for this wave's key blocks
   AFrag<E, C> Wt[KPW];     // rows of W^T for this wave's key blocks
   AFrag<E, C> dO[NB];      // B fragments of dO^T for the tile's value blocks
   float b;
@@ -102,7 +102,7 @@ __global__ __launch_bounds__(NTHREADS) void k_scan_bwd(Params p) {
 #pragma unroll
     for (int i = 0; i < KPW; ++i) {
       const size_t row = (size_t)16 * (KPW * w + i) * C;
-      pre.Qg[i].load((const E*)p.wQgt + gi * DK * C + row, C, 16, lane);
+      pre.Qt[i].load((const E*)p.wQt + gi * DK * C + row, C, 16, lane);
       pre.Wt[i].load((const E*)p.wWt + gi * DK * C + row, C, 16, lane);
     }
 #pragma unroll
@@ -116,7 +116,10 @@ __global__ __launch_bounds__(NTHREADS) void k_scan_bwd(Params p) {
     const int t0 = s + c * C, len = min(C, e - t0);
     const ScanBwdPre<E, DK, KPW, NB> cur = pre;
     block_sync_lds();
-    if (tid < C) sm.b[tid] = cur.b;
+    if (tid < C) {
+      sm.b[tid] = cur.b;
+      sm.g[tid] = __expf(cur.b);
+    }
 #pragma unroll
     for (int i = 0; i < KPW; ++i)
 #pragma unroll
@@ -173,8 +176,14 @@ __global__ __launch_bounds__(NTHREADS) void k_scan_bwd(Params p) {
 #pragma unroll
       for (int j = 0; j < 4; ++j) sm.dV[16 * w + frow(lane, j)][nb * 16 + fcol(lane)] = fromf<E>(-dv[j]);
     }
-    // dS_entry^T = g_C dS'^T + (g Q)^T dO - W^T dD
+    // dS_entry^T = g_C dS'^T + Q^T diag(g) dO - W^T dD   (the decay scales the
+    // dO fragment along the contracted token index)
     const float gC = __expf(bl);
+    float gk[C / KS][Mma<E>::KPL];
+#pragma unroll
+    for (int ks = 0; ks < C / KS; ++ks)
+#pragma unroll
+      for (int e = 0; e < Mma<E>::KPL; ++e) gk[ks][e] = sm.g[ks * KS + (lane >> 4) * Mma<E>::KPL + e];
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb) {
 #pragma unroll
@@ -182,9 +191,13 @@ __global__ __launch_bounds__(NTHREADS) void k_scan_bwd(Params p) {
 #pragma unroll
       for (int ks = 0; ks < C / KS; ++ks) {
         const FR bd = Frag<E>::load(kmaj(&sm.dDn[0][0], LC), nb * 16, ks * KS, lane);
+        FR gdo = cur.dO[nb].f[ks];
+        E* ge = (E*)&gdo;
+#pragma unroll
+        for (int e = 0; e < Mma<E>::KPL; ++e) ge[e] = fromf<E>(gk[ks][e] * tof(ge[e]));
 #pragma unroll
         for (int i = 0; i < KPW; ++i) {
-          acc[i][nb] = Mma<E>::mma(cur.Qg[i].f[ks], cur.dO[nb].f[ks], acc[i][nb]);
+          acc[i][nb] = Mma<E>::mma(cur.Qt[i].f[ks], gdo, acc[i][nb]);
           acc[i][nb] = Mma<E>::mma(cur.Wt[i].f[ks], bd, acc[i][nb]);
         }
       }

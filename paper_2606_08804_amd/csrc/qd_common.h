@@ -435,6 +435,7 @@ struct Params {
   int H;
   int NT;         // dense: ceil(T / C)
   int n_slots;    // saved-state / workspace slots
+  int prep_uw;      // backward-mode preparation also writes U and W (for a recompute)
   int lead;         // intra-chunk backward: leading workgroups that only wait
   int lead_cycles;  // ... and for how many clock cycles
   const int* cu;  // varlen cu_seqlens (device) or nullptr
@@ -459,7 +460,6 @@ struct Params {
   void* wKt;             // [slot][H][Dk][C]  K^T
   void* wT;              // [slot][H][2][C][C] T^T and P^T (backward only)
   void* wWt;             // [slot][H][Dk][C]  W^T (backward only)
-  void* wQgt;            // [slot][H][Dk][C]  (diag(g) Q)^T (backward only)
   void* wQt;             // [slot][H][Dk][C]  Q^T (backward only)
   void* wM;              // [slot][H][C][C]   (I + A)^{-1} (backward only)
   void* wdOt;            // [slot][H][Dv][C]  dO^T (backward only)

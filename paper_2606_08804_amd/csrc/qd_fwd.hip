@@ -102,7 +102,7 @@ __global__ __launch_bounds__(PREP_THREADS) void k_prep(Params p) {
     const size_t row = (size_t)x.t0 * H + x.h;
     x.K.load((const E*)p.k + row * DK, (size_t)H * DK, x.len, tid);
     x.Q.load((const E*)p.q + row * DK, (size_t)H * DK, x.len, tid);
-    x.V.load((const E*)p.v + row * DV, (size_t)H * DV, x.len, tid);
+    if (!BWD || p.prep_uw) x.V.load((const E*)p.v + row * DV, (size_t)H * DV, x.len, tid);
     if constexpr (BWD) x.dO.load((const E*)p.dO + row * DV, (size_t)H * DV, x.len, tid);
     if (tid < C) {
       const bool ok = tid < x.len;
@@ -135,11 +135,7 @@ __global__ __launch_bounds__(PREP_THREADS) void k_prep(Params p) {
 
     // transposed copies for the scans: K^T, and (diag(g) Q)^T for the backward
     store_transposed<E, DK, NT>((E*)p.wKt + gi * DK * C, &sm.u.a.K[0][0], LK, tid, One());
-    if (BWD) {
-      store_transposed<E, DK, NT>((E*)p.wQgt + gi * DK * C, &sm.u.a.Q[0][0], LK, tid,
-                                  [&](int r) { return __expf(sm.b[r]); });
-      store_transposed<E, DK, NT>((E*)p.wQt + gi * DK * C, &sm.u.a.Q[0][0], LK, tid, One());
-    }
+    if (BWD) store_transposed<E, DK, NT>((E*)p.wQt + gi * DK * C, &sm.u.a.Q[0][0], LK, tid, One());
     // mixed inputs X = K + lambda Q and the transposed decayed copy (g X)^T;
     // a thread takes 16 bytes of one row, consecutive threads consecutive rows
     {
@@ -220,13 +216,16 @@ __global__ __launch_bounds__(PREP_THREADS) void k_prep(Params p) {
         }
       }
     }
+    // U and W feed only the forward scan: a backward preparation that has the
+    // forward's saved context skips U and the row-major W
+    const bool uw = !BWD || p.prep_uw;
     // V^T (K, Q, X are dead: all reads of them finished before the solve's barriers)
-    x.V.storeT(&sm.u.Vt[0][0], LC, tid);
+    if (uw) x.V.storeT(&sm.u.Vt[0][0], LC, tid);
     block_sync_lds();
 
     // U = T V, stored C-fragment tiled: tile (mt, nt) at ((mt*(DV/16)+nt)*64 + lane)*4
     E* wU = (E*)p.wU + gi * C * DV;
-    for (int t = w; t < (C / 16) * (DV / 16); t += NW) {
+    for (int t = w; uw && t < (C / 16) * (DV / 16); t += NW) {
       const int m0 = (t / (DV / 16)) * 16, n0 = (t % (DV / 16)) * 16;
       const f4 uu = mma_k<E, C>(kmaj(&sm.Tm[0][0], LC), kmaj(&sm.u.Vt[0][0], LC), m0, n0, zero4(), lane);
       *(typename Quad<E>::raw*)(wU + ((size_t)t * 64 + lane) * 4) = Quad<E>::pack(uu);
@@ -237,8 +236,10 @@ __global__ __launch_bounds__(PREP_THREADS) void k_prep(Params p) {
     for (int t = w; t < (C / 16) * (DK / 16); t += NW) {
       const int m0 = (t / (DK / 16)) * 16, n0 = (t % (DK / 16)) * 16;
       const f4 wv = mma_k<E, C>(kmaj(&sm.Tm[0][0], LC), kmaj(&sm.GXt[0][0], LC), m0, n0, zero4(), lane);
+      if (uw) {
 #pragma unroll
-      for (int j = 0; j < 4; ++j) wW[(m0 + frow(lane, j)) * DK + n0 + fcol(lane)] = fromf<E>(wv[j]);
+        for (int j = 0; j < 4; ++j) wW[(m0 + frow(lane, j)) * DK + n0 + fcol(lane)] = fromf<E>(wv[j]);
+      }
       if (BWD)
         *(typename Quad<E>::raw*)(wWt + (size_t)(n0 + fcol(lane)) * C + m0 + frow(lane, 0)) = Quad<E>::pack(wv);
     }
