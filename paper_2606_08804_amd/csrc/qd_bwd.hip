@@ -33,34 +33,38 @@
 namespace qd {
 
 // ------------------------------------------------------------------ scan
+// Backward-scan operands of one chunk, filled by direct global->LDS loads:
+// P^T, T^T (C x C), K (C x Dk), Q^T, W^T (Dk x C), this tile's rows of dO^T
+// (BV x C) as swizzled tiles, then b (C fp32).  Two producer waves split the
+// loads so that each wave's outstanding count stays within the counter.
 template <typename E, int DK, int BV>
-struct ScanBwdSmem {
+struct ScanBwdRing {
+  static constexpr int RK = DK * (int)sizeof(E), RC = C * (int)sizeof(E);   // row bytes
+  static constexpr int PT = 0, TT = PT + C * RC, K = TT + C * RC, QT = K + C * RK, WT = QT + DK * RC,
+                       DOT = WT + DK * RC, B = DOT + BV * RC, BYTES = B + C * 4;
+  static constexpr int NBUF = sizeof(E) == 2 ? 2 : 1;
+  static constexpr int LOADS0 = (QT - PT) / 1024 + 1;   // producer 0: P^T, T^T, K, b
+  static constexpr int LOADS1 = (B - QT) / 1024;        // producer 1: Q^T, W^T, dO^T
+  static_assert(NBUF == 1 || (LOADS0 <= 63 && LOADS1 <= 63), "outstanding-load counter range");
+};
+
+template <typename E, int DK, int BV>
+struct alignas(16) ScanBwdSmem {
   static constexpr int P = Pad<E>::v;
-  float b[C], g[C];
-  E dS[BV][DK + P];   // dS' tile [v][k]
-  E dDn[BV][C + P];   // -dD tile, transposed [v][r]
-  E dDr[C][BV + P];   // dD tile staging [r][v]
+  typedef ScanBwdRing<E, DK, BV> R;
+  E dS[BV][DK + P];   // dS' tile [v][k] (MFMA operand copy; the dS'^T output is read back from it)
+  E dDn[BV][C + P];   // -dD tile, transposed [v][r] (also the source of the dD output)
   E dV[C][BV + P];    // dV tile staging [i][v]
-  float Sf[DK][BV + 4];  // fp32 dS' tile staging [k][v]
+  alignas(16) char ring[R::NBUF][R::BYTES];
 };
 
-// Operands of one chunk for one wave of the backward scan, prefetched from
-// global memory straight into MFMA fragments.
-template <typename E, int DK, int KPW, int NB>
-struct ScanBwdPre {
-  AFrag<E, C> PT;          // rows 16w.. of P^T
-  AFrag<E, C> TT;          // rows 16w.. of T^T
-  AFrag<E, DK> K;          // rows 16w.. of K
-  AFrag<E, C> Qt[KPW];     // rows of Q^T for this wave's key blocks
-  AFrag<E, C> Wt[KPW];     // rows of W^T for this wave's key blocks
-  AFrag<E, C> dO[NB];      // B fragments of dO^T for the tile's value blocks
-  float b;
-};
-
-// One workgroup per (sequence, head, Dv tile of BV = 32); reverse pass over
-// the chunks with the next (earlier) chunk's operands prefetched.
+// One workgroup per (sequence, head, Dv tile of BV = 32): four compute waves
+// and two producer waves; reverse pass over the chunks.  Compute wave w owns
+// rows 16w.. of dD and dV and key rows 16 KPW w.. of the exit-state gradient
+// tile dS'^T (Dk x BV), held in fp32 MFMA accumulators.  The producers stream
+// each chunk's operands into a two-chunk LDS ring, one chunk ahead.
 template <typename E, int DK, int DV, int BV>
-__global__ __launch_bounds__(NTHREADS) void k_scan_bwd(Params p) {
+__global__ __launch_bounds__(NTHREADS + 128) void k_scan_bwd(Params p) {
   constexpr int P = Pad<E>::v;
   constexpr int LK = DK + P, LC = C + P;
   constexpr int NVT = DV / BV;
@@ -70,8 +74,13 @@ __global__ __launch_bounds__(NTHREADS) void k_scan_bwd(Params p) {
   static_assert(KPW >= 1 && KPW * 16 * NWAVES == DK, "key blocks per wave");
   typedef typename Quad<E>::raw QR;
   typedef typename Mma<E>::frag FR;
+  typedef ScanBwdRing<E, DK, BV> R;
+  // fp32 operands take 4-deep k-steps; their long k loops are only partly unrolled
+  constexpr int UKC = C / KS > 4 ? 4 : C / KS, UKD = DK / KS > 4 ? 4 : DK / KS;
   __shared__ ScanBwdSmem<E, DK, BV> sm;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int prod = w - NWAVES;               // 0 or 1 for the producer waves, negative otherwise
+  const bool producer = prod >= 0;
   int unit, vt;
   if (!xcd_unit_tile(blockIdx.x, p.N * p.H, NVT, unit, vt)) return;
   const int H = p.H, n = unit / H, h = unit % H, v0 = vt * BV;
@@ -80,141 +89,181 @@ __global__ __launch_bounds__(NTHREADS) void k_scan_bwd(Params p) {
   const int base = slot_base(p, n, s);
   const int nch = max(0, min((e - s + C - 1) / C, p.n_slots - base));
 
+  auto issue = [&](int c, int buf) {
+    char* r = sm.ring[buf];
+    const int t0 = s + c * C, len = min(C, e - t0);
+    const size_t gi = (size_t)(base + c) * H + h;
+    if (prod == 0) {
+      const char* Tg = (const char*)((const E*)p.wT + gi * 2 * C * C);
+      const char* Kg = (const char*)((const E*)p.k + ((size_t)t0 * H + h) * DK);
+      dma_rows<R::RC, C, 1, true>(r + R::PT, Tg + C * R::RC, R::RC, C, Tg, 0, 0, lane);
+      dma_rows<R::RC, C, 1, true>(r + R::TT, Tg, R::RC, C, Tg, 0, 0, lane);
+      // rows past the chunk re-read its last row and are zeroed after the wait
+      dma_rows<R::RK, C, 1, true>(r + R::K, Kg, (size_t)H * R::RK, len, Kg + (size_t)(len - 1) * H * R::RK, 0, 0,
+                                  lane);
+      dma4_asm(p.wb + gi * C + lane, r + R::B);
+    } else {
+      const char* Qg = (const char*)((const E*)p.wQt + gi * DK * C);
+      const char* Wg = (const char*)((const E*)p.wWt + gi * DK * C);
+      const char* Og = (const char*)((const E*)p.wdOt + gi * DV * C + (size_t)v0 * C);
+      dma_rows<R::RC, DK, 1, true>(r + R::QT, Qg, R::RC, DK, Qg, 0, 0, lane);
+      dma_rows<R::RC, DK, 1, true>(r + R::WT, Wg, R::RC, DK, Wg, 0, 0, lane);
+      dma_rows<R::RC, BV, 1, true>(r + R::DOT, Og, R::RC, BV, Og, 0, 0, lane);
+    }
+  };
+
   f4 acc[KPW][NB];
 #pragma unroll
   for (int i = 0; i < KPW; ++i)
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb) {
       const int kt = KPW * w + i;
-      acc[i][nb] = p.dSfin ? *(const f4*)(p.dSfin + ((size_t)unit * DV + v0 + nb * 16 + fcol(lane)) * DK +
-                                          kt * 16 + frow(lane, 0))
-                           : zero4();
+      acc[i][nb] = (p.dSfin && !producer)
+                       ? *(const f4*)(p.dSfin + ((size_t)unit * DV + v0 + nb * 16 + fcol(lane)) * DK + kt * 16 +
+                                      frow(lane, 0))
+                       : zero4();
     }
-  const E* kb = (const E*)p.k;
-  ScanBwdPre<E, DK, KPW, NB> pre;
-  auto prefetch = [&](int c) {
-    const int t0 = s + c * C, len = min(C, e - t0);
-    const size_t gi = (size_t)(base + c) * H + h;
-    pre.b = tid < C ? p.wb[gi * C + tid] : 0.f;
-    pre.PT.load((const E*)p.wT + gi * 2 * C * C + C * C + (size_t)(16 * w) * C, C, 16, lane);
-    pre.TT.load((const E*)p.wT + gi * 2 * C * C + (size_t)(16 * w) * C, C, 16, lane);
-    pre.K.load(kb + ((size_t)(t0 + 16 * w) * H + h) * DK, (size_t)H * DK, len - 16 * w, lane);
-#pragma unroll
-    for (int i = 0; i < KPW; ++i) {
-      const size_t row = (size_t)16 * (KPW * w + i) * C;
-      pre.Qt[i].load((const E*)p.wQt + gi * DK * C + row, C, 16, lane);
-      pre.Wt[i].load((const E*)p.wWt + gi * DK * C + row, C, 16, lane);
-    }
-#pragma unroll
-    for (int nb = 0; nb < NB; ++nb)
-      pre.dO[nb].load((const E*)p.wdOt + gi * DV * C + (size_t)(v0 + 16 * nb) * C, C, 16, lane);
-  };
-  if (nch > 0) prefetch(nch - 1);
 
-  for (int c = nch - 1; c >= 0; --c) {
+  if (producer && nch > 0) {
+    issue(nch - 1, 0);
+    if (R::NBUF == 2 && nch > 1) issue(nch - 2, 1);
+  }
+  for (int it = 0; it < nch; ++it) {
+    const int c = nch - 1 - it;
     const size_t gi = (size_t)(base + c) * H + h;
     const int t0 = s + c * C, len = min(C, e - t0);
-    const ScanBwdPre<E, DK, KPW, NB> cur = pre;
-    block_sync_lds();
-    if (tid < C) {
-      sm.b[tid] = cur.b;
-      sm.g[tid] = __expf(cur.b);
+    const int buf = R::NBUF == 2 ? (it & 1) : 0;
+    const char* rc = sm.ring[buf];
+    const float* bch = (const float*)(rc + R::B);
+    if (producer) {
+      const bool ahead = R::NBUF == 2 && it + 1 < nch;
+      if (prod == 0) {
+        if (ahead) wait_vm<R::NBUF == 2 ? R::LOADS0 : 0>();
+        else wait_vm<0>();
+        if (len < C) {
+          // zero the K rows past the chunk (this wave's own loads are complete)
+          char* kz = sm.ring[buf] + R::K;
+          for (int i = len * (R::RK / 16) + lane; i < C * (R::RK / 16); i += 64)
+            *(uint4*)(kz + i * 16) = make_uint4(0, 0, 0, 0);
+        }
+      } else {
+        if (ahead) wait_vm<R::NBUF == 2 ? R::LOADS1 : 0>();
+        else wait_vm<0>();
+      }
     }
+    block_sync_lds();                      // chunk c's operands visible; previous chunk done
+    if (!producer) {
 #pragma unroll
-    for (int i = 0; i < KPW; ++i)
+      for (int i = 0; i < KPW; ++i)
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb) {
+          const int kt = KPW * w + i;
+          *(QR*)&sm.dS[nb * 16 + fcol(lane)][kt * 16 + frow(lane, 0)] = Quad<E>::pack(acc[i][nb]);
+        }
+    }
+    block_sync_lds();
+    if (!producer) {
+      {
+        // dS' of this chunk for the intra-chunk kernel, transposed ([k][v]) in the
+        // activation dtype, read back from the operand copy; 16-byte stores
+        constexpr int VEC = 16 / sizeof(E), PR = BV / VEC;
+        E* dst = (E*)p.w_dSo + gi * DK * DV + v0;
+        for (int idx = tid; idx < DK * PR; idx += NTHREADS) {
+          const int r = idx / PR, c0 = (idx % PR) * VEC;
+          uint4 o;
+          E* oe = (E*)&o;
+#pragma unroll
+          for (int j = 0; j < VEC; ++j) oe[j] = sm.dS[c0 + j][r];
+          *(uint4*)(dst + (size_t)r * DV + c0) = o;
+        }
+      }
+      const float bl = bch[C - 1];
+      // dD = P^T dO + diag(g_C/g) K dS'^T   (rows 16w..)
 #pragma unroll
       for (int nb = 0; nb < NB; ++nb) {
-        const int kt = KPW * w + i;
-        *(QR*)&sm.dS[nb * 16 + fcol(lane)][kt * 16 + frow(lane, 0)] = Quad<E>::pack(acc[i][nb]);
+        f4 d1 = zero4(), d2 = zero4();
+#pragma unroll UKC
+        for (int ks = 0; ks < C / KS; ++ks)
+          d1 = Mma<E>::mma(tile_frag<E, R::RC>(rc + R::PT, 16 * w, ks * KS, lane),
+                           tile_frag<E, R::RC>(rc + R::DOT, nb * 16, ks * KS, lane), d1);
+#pragma unroll UKD
+        for (int ks = 0; ks < DK / KS; ++ks)
+          d2 = Mma<E>::mma(tile_frag<E, R::RK>(rc + R::K, 16 * w, ks * KS, lane),
+                           Frag<E>::load(kmaj(&sm.dS[0][0], LK), nb * 16, ks * KS, lane), d2);
+        f4 dn;
 #pragma unroll
-        for (int j = 0; j < 4; ++j) sm.Sf[kt * 16 + frow(lane, j)][nb * 16 + fcol(lane)] = acc[i][nb][j];
+        for (int j = 0; j < 4; ++j) {
+          const int r = 16 * w + frow(lane, j);
+          dn[j] = -(d1[j] + __expf(bl - bch[r]) * d2[j]);
+        }
+        *(QR*)&sm.dDn[nb * 16 + fcol(lane)][16 * w + frow(lane, 0)] = Quad<E>::pack(dn);
       }
-    block_sync_lds();
-    {
-      // dS' of this chunk for the intra-chunk kernel, transposed ([k][v]) in
-      // the activation dtype (its consumer is an MFMA operand), 16-byte stores
-      constexpr int VEC = 16 / sizeof(E);
-      E* dst = (E*)p.w_dSo + gi * DK * DV + v0;
-      for (int idx = tid; idx < DK * (BV / VEC); idx += NTHREADS) {
-        const int r = idx / (BV / VEC), c0 = (idx % (BV / VEC)) * VEC;
-        uint4 o;
-        E* oe = (E*)&o;
-#pragma unroll
-        for (int j = 0; j < VEC; ++j) oe[j] = fromf<E>(sm.Sf[r][c0 + j]);
-        *(uint4*)(dst + (size_t)r * DV + c0) = o;
-      }
-    }
-    if (c > 0) prefetch(c - 1);
-    const float bl = sm.b[C - 1];
-    // dD = P^T dO + diag(g_C/g) K dS'^T   (rows 16w..)
-#pragma unroll
-    for (int nb = 0; nb < NB; ++nb) {
-      f4 d1 = zero4(), d2 = zero4();
-#pragma unroll
-      for (int ks = 0; ks < C / KS; ++ks) d1 = Mma<E>::mma(cur.PT.f[ks], cur.dO[nb].f[ks], d1);
-#pragma unroll
-      for (int ks = 0; ks < DK / KS; ++ks)
-        d2 = Mma<E>::mma(cur.K.f[ks], Frag<E>::load(kmaj(&sm.dS[0][0], LK), nb * 16, ks * KS, lane), d2);
-      f4 dn;
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const int r = 16 * w + frow(lane, j);
-        const float d = d1[j] + __expf(bl - sm.b[r]) * d2[j];
-        dn[j] = -d;
-        sm.dDr[r][nb * 16 + fcol(lane)] = fromf<E>(d);
-      }
-      *(QR*)&sm.dDn[nb * 16 + fcol(lane)][16 * w + frow(lane, 0)] = Quad<E>::pack(dn);
     }
     block_sync_lds();
-    // dV = T^T dD  (rows 16w..), staged for coalesced stores
+    if (!producer) {
+      {
+        // dD rows for the intra-chunk kernel, read back from -dD^T
+        constexpr int VEC = 16 / sizeof(E), PR = BV / VEC;
+        E* ddst = (E*)p.w_dDb + gi * C * DV + v0;
+        for (int idx = tid; idx < C * PR; idx += NTHREADS) {
+          const int r = idx % C, cc = (idx / C) * VEC;
+          uint4 o;
+          E* oe = (E*)&o;
 #pragma unroll
-    for (int nb = 0; nb < NB; ++nb) {
-      f4 dv = zero4();
+          for (int j = 0; j < VEC; ++j) oe[j] = fromf<E>(-tof(sm.dDn[cc + j][r]));
+          *(uint4*)(ddst + (size_t)r * DV + cc) = o;
+        }
+      }
+      // dV = T^T dD  (rows 16w..), staged for coalesced stores
 #pragma unroll
-      for (int ks = 0; ks < C / KS; ++ks)
-        dv = Mma<E>::mma(cur.TT.f[ks], Frag<E>::load(kmaj(&sm.dDn[0][0], LC), nb * 16, ks * KS, lane), dv);
+      for (int nb = 0; nb < NB; ++nb) {
+        f4 dv = zero4();
+#pragma unroll UKC
+        for (int ks = 0; ks < C / KS; ++ks)
+          dv = Mma<E>::mma(tile_frag<E, R::RC>(rc + R::TT, 16 * w, ks * KS, lane),
+                           Frag<E>::load(kmaj(&sm.dDn[0][0], LC), nb * 16, ks * KS, lane), dv);
 #pragma unroll
-      for (int j = 0; j < 4; ++j) sm.dV[16 * w + frow(lane, j)][nb * 16 + fcol(lane)] = fromf<E>(-dv[j]);
-    }
-    // dS_entry^T = g_C dS'^T + Q^T diag(g) dO - W^T dD   (the decay scales the
-    // dO fragment along the contracted token index)
-    const float gC = __expf(bl);
-    float gk[C / KS][Mma<E>::KPL];
+        for (int j = 0; j < 4; ++j) sm.dV[16 * w + frow(lane, j)][nb * 16 + fcol(lane)] = fromf<E>(-dv[j]);
+      }
+      // dS_entry^T = g_C dS'^T + Q^T diag(g) dO - W^T dD   (the decay scales the
+      // dO fragment along the contracted token index)
+      const float gC = __expf(bch[C - 1]);
 #pragma unroll
-    for (int ks = 0; ks < C / KS; ++ks)
+      for (int nb = 0; nb < NB; ++nb) {
 #pragma unroll
-      for (int e = 0; e < Mma<E>::KPL; ++e) gk[ks][e] = sm.g[ks * KS + (lane >> 4) * Mma<E>::KPL + e];
+        for (int i = 0; i < KPW; ++i) acc[i][nb] = gC * acc[i][nb];
+#pragma unroll UKC
+        for (int ks = 0; ks < C / KS; ++ks) {
+          const FR bd = Frag<E>::load(kmaj(&sm.dDn[0][0], LC), nb * 16, ks * KS, lane);
+          FR gdo = tile_frag<E, R::RC>(rc + R::DOT, nb * 16, ks * KS, lane);
+          E* ge = (E*)&gdo;
 #pragma unroll
-    for (int nb = 0; nb < NB; ++nb) {
+          for (int e2 = 0; e2 < Mma<E>::KPL; ++e2)
+            ge[e2] = fromf<E>(__expf(bch[ks * KS + (lane >> 4) * Mma<E>::KPL + e2]) * tof(ge[e2]));
 #pragma unroll
-      for (int i = 0; i < KPW; ++i) acc[i][nb] = gC * acc[i][nb];
-#pragma unroll
-      for (int ks = 0; ks < C / KS; ++ks) {
-        const FR bd = Frag<E>::load(kmaj(&sm.dDn[0][0], LC), nb * 16, ks * KS, lane);
-        FR gdo = cur.dO[nb].f[ks];
-        E* ge = (E*)&gdo;
-#pragma unroll
-        for (int e = 0; e < Mma<E>::KPL; ++e) ge[e] = fromf<E>(gk[ks][e] * tof(ge[e]));
-#pragma unroll
-        for (int i = 0; i < KPW; ++i) {
-          acc[i][nb] = Mma<E>::mma(cur.Qt[i].f[ks], gdo, acc[i][nb]);
-          acc[i][nb] = Mma<E>::mma(cur.Wt[i].f[ks], bd, acc[i][nb]);
+          for (int i = 0; i < KPW; ++i) {
+            acc[i][nb] = Mma<E>::mma(tile_frag<E, R::RC>(rc + R::QT, 16 * (KPW * w + i), ks * KS, lane), gdo,
+                                     acc[i][nb]);
+            acc[i][nb] = Mma<E>::mma(tile_frag<E, R::RC>(rc + R::WT, 16 * (KPW * w + i), ks * KS, lane), bd,
+                                     acc[i][nb]);
+          }
         }
       }
     }
-    block_sync_lds();
-    {
+    block_sync_lds();                      // chunk c's ring buffer, dDn and dV complete
+    if (producer) {
+      if (R::NBUF == 2 && it + 2 < nch) issue(c - 2, buf);
+      if (R::NBUF == 1 && it + 1 < nch) issue(c - 1, 0);
+    } else {
       constexpr int VEC = 16 / sizeof(E), PR = BV / VEC;
-      E* ddst = (E*)p.w_dDb + gi * C * DV + v0;
       E* vdst = (E*)p.dv + ((size_t)t0 * H + h) * DV + v0;
       for (int idx = tid; idx < C * PR; idx += NTHREADS) {
         const int r = idx / PR, cc = (idx % PR) * VEC;
-        *(uint4*)(ddst + (size_t)r * DV + cc) = *(const uint4*)&sm.dDr[r][cc];
         if (r < len) *(uint4*)(vdst + (size_t)r * H * DV + cc) = *(const uint4*)&sm.dV[r][cc];
       }
     }
   }
-  if (p.dS0) {
+  if (p.dS0 && !producer) {
 #pragma unroll
     for (int i = 0; i < KPW; ++i)
 #pragma unroll
@@ -754,7 +803,7 @@ static hipError_t launch_bwd_t(const Params& p, hipStream_t st) {
   const int nb = ((units + 7) / 8) * 8 * (DV / SBV);
   if (nb > 0) {
     prof_mark(ST_SCAN_BWD, 0, st);
-    hipLaunchKernelGGL((k_scan_bwd<E, DK, DV, SBV>), dim3(nb), dim3(NTHREADS), 0, st, p);
+    hipLaunchKernelGGL((k_scan_bwd<E, DK, DV, SBV>), dim3(nb), dim3(NTHREADS + 128), 0, st, p);
     prof_mark(ST_SCAN_BWD, 1, st);
   }
   if (p.n_slots > 0) {
