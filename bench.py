@@ -62,9 +62,9 @@ def stage_bytes_per_unit(stage, Dk, Dv, e):
         return gates + 3 * act_qk + cc_e + act_v + act_v + state + act_v
     if stage == "scan_bwd":      # b, P^T, T^T, k, Q^T, W^T, dO^T -> dS' (dtype), dD, dv
         return gates + 2 * cc_e + 3 * act_qk + act_v + state * e // 4 + act_v + act_v
-    if stage == "intra":         # b, beta, lam, S (fp32), dS' (dtype), D, dD, dO, v, q, k, K^T, Q^T, M, T^T
+    if stage == "intra":         # b, beta, lam, S (fp32), dS' (dtype), D, dD, dO, v, q, k, M, T^T
         #                          -> dq, dk, dbeta, dlam, dlog_alpha
-        return 3 * gates + state + state * e // 4 + 4 * act_v + 4 * act_qk + 2 * cc_e + 2 * act_qk + 3 * gates
+        return 3 * gates + state + state * e // 4 + 4 * act_v + 2 * act_qk + 2 * cc_e + 2 * act_qk + 3 * gates
     raise KeyError(stage)
 
 

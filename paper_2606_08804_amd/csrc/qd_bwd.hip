@@ -303,9 +303,6 @@ struct TileA {
 template <typename E, int DK>
 struct alignas(16) BwdSmem {
   static constexpr int P = Pad<E>::v;
-  // bf16 operands need explicit transposed copies of dG and dQK for
-  // contiguous fragment loads; fp32 fragments are single scalars either way
-  static constexpr bool TCOPY = sizeof(E) == 2;
   float b[C], g[C], kb[C], beta[C], lam[C], db[C], dbeta[C];
   float rsum[5][2][C];      // per-row partial sums of the two column halves:
                             // dbeta rows, decay rows (B2); decay, Kbar, dlambda rows (B3)
@@ -313,31 +310,33 @@ struct alignas(16) BwdSmem {
   union {
     alignas(16) char tiles[TileA<E, DK>::NBUF][TileA<E, DK>::BYTES];   // phase A
     struct {
+      struct {
+        E K[C][DK + P];       // chunk keys (r, k)
+        E Q[C][DK + P];       // chunk queries (r, k)
+        E dW[C][DK + P];      // dW = -dD S (r, k)
+      } b1;                   // from phase B1 to the end of phase B3
       union {
         struct {
-          E K[C][DK + P];       // chunk keys (r, k)
-          E Q[C][DK + P];       // chunk queries (r, k)
-          E dW[C][DK + P];      // dW = -dD S (r, k)
-        } b1;
-        struct {
-          E MT[C][C + P];       // M^T (i, r)
-          E dMt[C][C + P];      // (dT diag(beta))^T (i, r)
-          E Y[2][C][C + P];     // M^T dT diag(beta) (r, i), one copy per column half
-          float dbc[16][C];     // column partial sums of dT (.) M, per row block and lane group
-          float ecc[16][C];     // column partial sums of the decay-gradient terms
+          union {
+            struct {
+              E MT[C][C + P];     // M^T (i, r)
+              E dMt[C][C + P];    // (dT diag(beta))^T (i, r)
+            } m;
+            struct {
+              E dG[C][C + P];     // dG (r, i), after M^T and dMinv^T are dead
+              E dQK[C][C + P];    // dQK (r, i)
+            } g;
+          } v;
+          E Y[C][C + P];          // M^T dT diag(beta) (r, i)
+          float dbc[16][C];       // column partial sums of dT (.) M, per row block and lane group
+          float ecc[16][C];       // column partial sums of the decay-gradient terms
         } b2;
         struct {
-          E dWt[DK][C + P];     // dW^T (k, r)
-          E Kt[DK][C + P];      // K^T (k, r)
-          E Qt[DK][C + P];      // Q^T (k, r)
-          E oq[C][DK + P];      // dq staging
-          E ok[C][DK + P];      // dk staging
+          E keep[2][C][C + P];    // dG, dQK (read by phase B3 as A operands)
+          E oq[C][DK + P];        // dq staging, over the dead Y and column sums
+          E ok[C][DK + P];        // dk staging
         } b3;
       } u;
-      E dG[C][C + P];           // dG (r, i)
-      E dQK[C][C + P];          // dQK (r, i)
-      typename std::conditional<TCOPY, E[C][C + P], char[16]>::type dGt;    // dG^T (i, r)
-      typename std::conditional<TCOPY, E[C][C + P], char[16]>::type dQKt;   // dQK^T (i, r)
     } s;
   } x;
   // M = (I + A)^{-1} (r, i) and T^T (i, r), direct-loaded at the start (swizzled
@@ -515,13 +514,13 @@ __global__ __launch_bounds__(INTRA_THREADS) void k_bwd_intra(Params p) {
   // ---------------- phase B1: G = X K^T, QK = Q K^T, dT2 = dW (g X)^T
   constexpr int LKD = DK + P;
   block_sync_lds();
-  rKf.store_rows(&sm.x.s.u.b1.K[0][0], LKD, len, tid);
-  rQf.store_rows(&sm.x.s.u.b1.Q[0][0], LKD, len, tid);
+  rKf.store_rows(&sm.x.s.b1.K[0][0], LKD, len, tid);
+  rQf.store_rows(&sm.x.s.b1.Q[0][0], LKD, len, tid);
 #pragma unroll
   for (int i = 0; i < HK; ++i)
 #pragma unroll
     for (int j = 0; j < 4; ++j)
-      sm.x.s.u.b1.dW[16 * rb + frow(lane, j)][(kb0 + i) * 16 + fcol(lane)] = fromf<E>(-aW[i][j]);
+      sm.x.s.b1.dW[16 * rb + frow(lane, j)][(kb0 + i) * 16 + fcol(lane)] = fromf<E>(-aW[i][j]);
   if (tid < C) sm.kb[tid] = __expf(sm.b[C - 1] - sm.b[tid]);
   block_sync_lds();
   f4 aG[2], aQK[2], adT[2];
@@ -537,15 +536,15 @@ __global__ __launch_bounds__(INTRA_THREADS) void k_bwd_intra(Params p) {
     }
 #pragma unroll
     for (int ks = 0; ks < DK / KS; ++ks) {
-      const FR kA = Frag<E>::load(kmaj(&sm.x.s.u.b1.K[0][0], LKD), 16 * rb, ks * KS, lane);
-      const FR qA = Frag<E>::load(kmaj(&sm.x.s.u.b1.Q[0][0], LKD), 16 * rb, ks * KS, lane);
+      const FR kA = Frag<E>::load(kmaj(&sm.x.s.b1.K[0][0], LKD), 16 * rb, ks * KS, lane);
+      const FR qA = Frag<E>::load(kmaj(&sm.x.s.b1.Q[0][0], LKD), 16 * rb, ks * KS, lane);
       const FR xA = mix_frag<FR>(kA, qA, lam_a, 1.f);
-      const FR dwA = Frag<E>::load(kmaj(&sm.x.s.u.b1.dW[0][0], LKD), 16 * rb, ks * KS, lane);
+      const FR dwA = Frag<E>::load(kmaj(&sm.x.s.b1.dW[0][0], LKD), 16 * rb, ks * KS, lane);
 #pragma unroll
       for (int i = 0; i < 2; ++i) {
         const int ib = ib0 + i;
-        const FR kB = Frag<E>::load(kmaj(&sm.x.s.u.b1.K[0][0], LKD), ib * 16, ks * KS, lane);
-        const FR qB = Frag<E>::load(kmaj(&sm.x.s.u.b1.Q[0][0], LKD), ib * 16, ks * KS, lane);
+        const FR kB = Frag<E>::load(kmaj(&sm.x.s.b1.K[0][0], LKD), ib * 16, ks * KS, lane);
+        const FR qB = Frag<E>::load(kmaj(&sm.x.s.b1.Q[0][0], LKD), ib * 16, ks * KS, lane);
         const FR gxB = mix_frag<FR>(kB, qB, lam_b[i], g_b[i]);
         aG[i] = Mma<E>::mma(xA, kB, aG[i]);
         aQK[i] = Mma<E>::mma(qA, kB, aQK[i]);
@@ -553,16 +552,11 @@ __global__ __launch_bounds__(INTRA_THREADS) void k_bwd_intra(Params p) {
       }
     }
   }
-  // K^T and Q^T for phase B3, in flight during phase B2
-  TileRegs<E, DK, C, IT> rKt, rQt;
-  rKt.load((const E*)p.wKt + gi * DK * C, C, DK, tid);
-  rQt.load((const E*)p.wQt + gi * DK * C, C, DK, tid);
 
   // ---------------- phase B2: UT-solve backward and the C x C gradient terms.
   // Lane (w, lane) holds element (r, c) = (16 rb + frow(lane, j), 16 ib + fcol(lane))
   // of every C x C accumulator, for the two column blocks ib of its half.
   const int rw = 16 * rb + frow(lane, 0), cl = fcol(lane);
-  block_sync_lds();                    // K, Q, dW dead: the b2 buffers may be written
   {
     // dT = dD V^T + dW (g X)^T: column sums of dT (.) M feed dbeta; M^T and
     // (dT diag(beta))^T become the operands of Y = M^T dT diag(beta)
@@ -580,30 +574,30 @@ __global__ __launch_bounds__(INTRA_THREADS) void k_bwd_intra(Params p) {
         mv[j] = m;
         dm[j] = dt * bc;
       }
-      *(QR*)&sm.x.s.u.b2.MT[c][rw] = Quad<E>::pack(mv);
-      *(QR*)&sm.x.s.u.b2.dMt[c][rw] = Quad<E>::pack(dm);
+      *(QR*)&sm.x.s.u.b2.v.m.MT[c][rw] = Quad<E>::pack(mv);
+      *(QR*)&sm.x.s.u.b2.v.m.dMt[c][rw] = Quad<E>::pack(dm);
       sm.x.s.u.b2.dbc[4 * rb + (lane >> 4)][c] = cs;
     }
   }
   block_sync_lds();
   f4 adA[2];
   {
-    // Y = M^T dMinv, rows 16 rb.. over all columns (each half keeps a copy)
+    // Y = M^T dMinv: rows 16 rb.., this half's column blocks
 #pragma unroll
-    for (int ib = 0; ib < 4; ++ib) {
-      const f4 y = mma_k<E, C>(kmaj(&sm.x.s.u.b2.MT[0][0], LC), kmaj(&sm.x.s.u.b2.dMt[0][0], LC), 16 * rb, ib * 16,
-                               zero4(), lane);
+    for (int i = 0; i < 2; ++i) {
+      const int ib = ib0 + i;
+      const f4 y = mma_k<E, C>(kmaj(&sm.x.s.u.b2.v.m.MT[0][0], LC), kmaj(&sm.x.s.u.b2.v.m.dMt[0][0], LC), 16 * rb,
+                               ib * 16, zero4(), lane);
 #pragma unroll
-      for (int j = 0; j < 4; ++j) sm.x.s.u.b2.Y[ch][rw + j][ib * 16 + cl] = fromf<E>(y[j]);
+      for (int j = 0; j < 4; ++j) sm.x.s.u.b2.Y[rw + j][ib * 16 + cl] = fromf<E>(y[j]);
     }
-    // this copy of Y rows 16 rb.. is read back by this wave only
-    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+    block_sync_lds();                  // Y complete; M^T and dMinv^T dead after this point
 #pragma unroll
     for (int i = 0; i < 2; ++i) {           // dA = strictLower(-Y M^T)
       adA[i] = zero4();
 #pragma unroll
       for (int ks = 0; ks < C / KS; ++ks)
-        adA[i] = Mma<E>::mma(Frag<E>::load(kmaj(&sm.x.s.u.b2.Y[ch][0][0], LC), 16 * rb, ks * KS, lane),
+        adA[i] = Mma<E>::mma(Frag<E>::load(kmaj(&sm.x.s.u.b2.Y[0][0], LC), 16 * rb, ks * KS, lane),
                              tile_frag<E, RBC>(sm.Mm, (ib0 + i) * 16, ks * KS, lane), adA[i]);
     }
   }
@@ -621,7 +615,6 @@ __global__ __launch_bounds__(INTRA_THREADS) void k_bwd_intra(Params p) {
     for (int i = 0; i < 2; ++i) {
       const int c = (ib0 + i) * 16 + cl;
       const float bc = sm.b[c];
-      f4 vg, vq;
       float ec = 0.f;
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
@@ -635,14 +628,8 @@ __global__ __launch_bounds__(INTRA_THREADS) void k_bwd_intra(Params p) {
         dbr[j] += dAg * aG[i][j];
         er[j] += t;
         ec += t;
-        vg[j] = dg;
-        vq[j] = dqk;
-        sm.x.s.dG[r][c] = fromf<E>(dg);
-        sm.x.s.dQK[r][c] = fromf<E>(dqk);
-      }
-      if constexpr (BwdSmem<E, DK>::TCOPY) {
-        *(QR*)&sm.x.s.dGt[c][rw] = Quad<E>::pack(vg);
-        *(QR*)&sm.x.s.dQKt[c][rw] = Quad<E>::pack(vq);
+        sm.x.s.u.b2.v.g.dG[r][c] = fromf<E>(dg);
+        sm.x.s.u.b2.v.g.dQK[r][c] = fromf<E>(dqk);
       }
       sm.x.s.u.b2.ecc[4 * rb + (lane >> 4)][c] = ec;
     }
@@ -674,32 +661,21 @@ __global__ __launch_bounds__(INTRA_THREADS) void k_bwd_intra(Params p) {
   block_sync_lds();                    // the b2 buffers are dead past here
 
   // ---------------- phase B3: dX, dq, dk (rows 16 rb.., Dk blocks of this half)
-  rKt.store(&sm.x.s.u.b3.Kt[0][0], LC, tid);
-  rQt.store(&sm.x.s.u.b3.Qt[0][0], LC, tid);
-#pragma unroll
-  for (int i = 0; i < HK; ++i) {
-    f4 nw;
-#pragma unroll
-    for (int j = 0; j < 4; ++j) nw[j] = -aW[i][j];
-    *(QR*)&sm.x.s.u.b3.dWt[(kb0 + i) * 16 + fcol(lane)][16 * rb + frow(lane, 0)] = Quad<E>::pack(nw);
-  }
-  block_sync_lds();
+  // K^T, Q^T and dW^T fragments are transpose reads of the row-major K, Q, dW
+  // kept since phase B1; dQK^T and dG^T likewise of dQK and dG
   {
     constexpr int NTK = C / KS;
     FR tA[NTK], gA[NTK], qkA[NTK], qktA[NTK], gtA[NTK];
     float lamk[NTK][Mma<E>::KPL];
+    const E* dGp = &sm.x.s.u.b2.v.g.dG[0][0];
+    const E* dQKp = &sm.x.s.u.b2.v.g.dQK[0][0];
 #pragma unroll
     for (int ks = 0; ks < NTK; ++ks) {
       tA[ks] = tile_frag<E, RBC>(sm.TmT, 16 * rb, ks * KS, lane);
-      gA[ks] = Frag<E>::load(kmaj(&sm.x.s.dG[0][0], LC), 16 * rb, ks * KS, lane);
-      qkA[ks] = Frag<E>::load(kmaj(&sm.x.s.dQK[0][0], LC), 16 * rb, ks * KS, lane);
-      if constexpr (BwdSmem<E, DK>::TCOPY) {
-        qktA[ks] = Frag<E>::load(kmaj(&sm.x.s.dQKt[0][0], LC), 16 * rb, ks * KS, lane);
-        gtA[ks] = Frag<E>::load(kmaj(&sm.x.s.dGt[0][0], LC), 16 * rb, ks * KS, lane);
-      } else {
-        qktA[ks] = Frag<E>::load(imaj(&sm.x.s.dQK[0][0], LC), 16 * rb, ks * KS, lane);
-        gtA[ks] = Frag<E>::load(imaj(&sm.x.s.dG[0][0], LC), 16 * rb, ks * KS, lane);
-      }
+      gA[ks] = Frag<E>::load(kmaj(dGp, LC), 16 * rb, ks * KS, lane);
+      qkA[ks] = Frag<E>::load(kmaj(dQKp, LC), 16 * rb, ks * KS, lane);
+      qktA[ks] = tr_frag<E>(dQKp, LC, ks * KS, 16 * rb, lane);
+      gtA[ks] = tr_frag<E>(dGp, LC, ks * KS, 16 * rb, lane);
 #pragma unroll
       for (int e = 0; e < Mma<E>::KPL; ++e) lamk[ks][e] = sm.lam[ks * KS + (lane >> 4) * Mma<E>::KPL + e];
     }
@@ -712,15 +688,18 @@ __global__ __launch_bounds__(INTRA_THREADS) void k_bwd_intra(Params p) {
       lr4[j] = sm.lam[r0 + j];
       kbr4[j] = sm.kb[r0 + j];
     }
+    const E* Kp = &sm.x.s.b1.K[0][0];
+    const E* Qp = &sm.x.s.b1.Q[0][0];
+    const E* dWp = &sm.x.s.b1.dW[0][0];
 #pragma unroll
     for (int i = 0; i < HK; ++i) {
       const int kb = kb0 + i;
       f4 dgx = zero4(), dxp = zero4(), dqp = zero4(), dkp = zero4();
 #pragma unroll
       for (int ks = 0; ks < NTK; ++ks) {
-        const FR ktB = Frag<E>::load(kmaj(&sm.x.s.u.b3.Kt[0][0], LC), kb * 16, ks * KS, lane);
-        const FR qtB = Frag<E>::load(kmaj(&sm.x.s.u.b3.Qt[0][0], LC), kb * 16, ks * KS, lane);
-        const FR dwB = Frag<E>::load(kmaj(&sm.x.s.u.b3.dWt[0][0], LC), kb * 16, ks * KS, lane);
+        const FR ktB = tr_frag<E>(Kp, LKD, ks * KS, kb * 16, lane);
+        const FR qtB = tr_frag<E>(Qp, LKD, ks * KS, kb * 16, lane);
+        const FR dwB = tr_frag<E>(dWp, LKD, ks * KS, kb * 16, lane);
         const FR xtB = mix_tokens<FR>(ktB, qtB, lamk[ks]);
         dgx = Mma<E>::mma(tA[ks], dwB, dgx);      // T^T dW
         dxp = Mma<E>::mma(gA[ks], ktB, dxp);      // dG K
@@ -729,12 +708,12 @@ __global__ __launch_bounds__(INTRA_THREADS) void k_bwd_intra(Params p) {
         dkp = Mma<E>::mma(gtA[ks], xtB, dkp);     // dG^T X
       }
       const int kc = kb * 16 + fcol(lane);
-      const QR kv = *(const QR*)&sm.x.s.u.b3.Kt[kc][r0];
-      const QR qv = *(const QR*)&sm.x.s.u.b3.Qt[kc][r0];
+      const f4 kv = tr_col4(Kp, LKD, r0, kb * 16, lane);
+      const f4 qv = tr_col4(Qp, LKD, r0, kb * 16, lane);
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
         const int r = r0 + j;
-        const float Kv = Quad<E>::get(kv, j), Qv = Quad<E>::get(qv, j);
+        const float Kv = kv[j], Qv = qv[j];
         const float gr = gr4[j], lr = lr4[j], kbr = kbr4[j];
         const float X = Kv + lr * Qv;
         rdb[j] += gr * (X * dgx[j] + Qv * aQ[i][j]);

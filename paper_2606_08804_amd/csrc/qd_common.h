@@ -402,6 +402,47 @@ __device__ inline typename Mma<E>::frag tile_frag(const char* t, int row0, int k
   const int row = row0 + (lane & 15), k = k0 + (lane >> 4) * Mma<E>::KPL;
   return *(const typename Mma<E>::frag*)(t + tile_off<RB>(row, k * (int)sizeof(E)));
 }
+// MFMA fragment of the TRANSPOSE of a row-major 16-bit LDS matrix: with
+// element (i, j) at base + i * ld + j (ld in elements), returns for lane l the
+// fragment values (i = k0 + (l >> 4) * KPL + e, j = j0 + (l & 15)), e < KPL,
+// i.e. the operand whose "row" index is j and whose k index is i.  Uses the
+// LDS transpose read: in each 16-lane group, lane L names the 8 bytes at row
+// (L >> 2) and columns 4 (L & 3) .. +3 of a 4 x 16 block and receives column
+// L of that block.  The fp32 form is a plain strided read.
+template <typename E>
+__device__ inline typename Mma<E>::frag tr_frag(const E* base, int ld, int k0, int j0, int lane);
+template <>
+__device__ inline bf8 tr_frag<__bf16>(const __bf16* base, int ld, int k0, int j0, int lane) {
+  typedef __bf16 v4b __attribute__((ext_vector_type(4)));
+  typedef __attribute__((address_space(3))) v4b* lp;
+  const int L = lane & 15, i0 = k0 + (lane >> 4) * 8 + (L >> 2), j = j0 + 4 * (L & 3);
+  const __bf16* a = base + (size_t)i0 * ld + j;
+  const v4b lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lp)(uintptr_t)(uint32_t)(uintptr_t)a);
+  const v4b hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lp)(uintptr_t)(uint32_t)(uintptr_t)(a + (size_t)4 * ld));
+  return __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+}
+template <>
+__device__ inline float tr_frag<float>(const float* base, int ld, int k0, int j0, int lane) {
+  return base[(size_t)(k0 + (lane >> 4)) * ld + j0 + (lane & 15)];
+}
+// Four consecutive rows i0 .. i0+3 of column j0 + (l & 15) of a row-major
+// 16-bit LDS matrix for lane l (one transpose read; lanes of a 16-lane group
+// share i0), returned as floats.
+__device__ inline f4 tr_col4(const __bf16* base, int ld, int i0, int j0, int lane) {
+  typedef __bf16 v4b __attribute__((ext_vector_type(4)));
+  typedef __attribute__((address_space(3))) v4b* lp;
+  const int L = lane & 15;
+  const __bf16* a = base + (size_t)(i0 + (L >> 2)) * ld + j0 + 4 * (L & 3);
+  const v4b v = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lp)(uintptr_t)(uint32_t)(uintptr_t)a);
+  return f4{(float)v[0], (float)v[1], (float)v[2], (float)v[3]};
+}
+__device__ inline f4 tr_col4(const float* base, int ld, int i0, int j0, int lane) {
+  f4 r;
+#pragma unroll
+  for (int e = 0; e < 4; ++e) r[e] = base[(size_t)(i0 + e) * ld + j0 + (lane & 15)];
+  return r;
+}
+
 // Same from an fp32 tile, converted to E; the fp32 values are returned in v.
 template <typename E>
 __device__ inline typename Mma<E>::frag tile_frag_f32(const char* t, int row0, int k0, int lane,
