@@ -54,17 +54,15 @@ def stage_bytes_per_unit(stage, Dk, Dv, e):
     gates = C * 4
     state = Dv * Dk * 4
     cc_e = C * C * e
-    if stage == "prep_fwd":      # q,k,v, 3 gates -> b, U, W, P, K^T
-        return 2 * act_qk + act_v + 3 * gates + gates + act_v + 2 * act_qk + cc_e
-    if stage == "prep_bwd":      # q,k,dO, 3 gates -> b, K^T, W^T, Q^T, T^T, P^T, M, dO^T
-        return 2 * act_qk + act_v + 3 * gates + gates + 3 * act_qk + 3 * cc_e + act_v
-    if stage == "scan_fwd":      # b, W, K^T, q, P, U -> o, state, D
+    if stage in ("prep_fwd", "prep_bwd"):   # q,k,v, 3 gates -> b, U, W, P, M
+        return 2 * act_qk + act_v + 3 * gates + gates + act_v + act_qk + 2 * cc_e
+    if stage == "scan_fwd":      # b, W, k, q, P, U -> o, state, D
         return gates + 3 * act_qk + cc_e + act_v + act_v + state + act_v
-    if stage == "scan_bwd":      # b, P^T, T^T, k, Q^T, W^T, dO^T -> dS' (dtype), dD, dv
-        return gates + 2 * cc_e + 3 * act_qk + act_v + state * e // 4 + act_v + act_v
-    if stage == "intra":         # b, beta, lam, S (fp32), dS' (dtype), D, dD, dO, v, q, k, M, T^T
+    if stage == "scan_bwd":      # b, beta, P, M, k, q, W, dO -> dS' (dtype), dD, dv
+        return 2 * gates + 2 * cc_e + 3 * act_qk + act_v + state * e // 4 + act_v + act_v
+    if stage == "intra":         # b, beta, lam, S (fp32), dS' (dtype), D, dD, dO, v, q, k, M
         #                          -> dq, dk, dbeta, dlam, dlog_alpha
-        return 3 * gates + state + state * e // 4 + 4 * act_v + 2 * act_qk + 2 * cc_e + 2 * act_qk + 3 * gates
+        return 3 * gates + state + state * e // 4 + 4 * act_v + 2 * act_qk + cc_e + 2 * act_qk + 3 * gates
     raise KeyError(stage)
 
 

@@ -51,11 +51,20 @@
  * Saved context (written by the forward, read by the backward)
  * --------------------------------------------------------------
  *  A caller-owned device buffer of qdelta_saved_bytes() bytes (16-byte
- *  aligned) with two regions, each indexed by unit u = slot * H + h:
- *    states  float32 [n_slots*H, Dk, Dv] at byte 0: the transposed entry state
- *            S^T of the chunk (element (k, v) = S[v][k]);
- *    D       dtype [n_slots*H, C, Dv] after the states: the chunk's
- *            "new values" D = U - W S^T, rows >= the chunk's length zero.
+ *  aligned) with six regions, one after the other, each indexed by unit
+ *  u = slot * H + h (U = n_slots * H units):
+ *    states  float32 [U, Dk, Dv]: the transposed entry state S^T of the chunk
+ *            (element (k, v) = S[v][k]);
+ *    D       dtype [U, C, Dv]: the chunk's "new values" D = U - W S^T
+ *            (App. D, WY form), rows >= the chunk's length zero;
+ *    b       float32 [U, C]: chunk-local prefix sums of log alpha;
+ *    W       dtype [U, C, Dk]: W = T diag(g) X of the WY form, rows >= the
+ *            chunk's length zero;
+ *    P       dtype [U, C, C]: the intra-chunk output operator
+ *            Gam * M * (Q K^T) (Sec. 3.3 chunkwise form);
+ *    M       dtype [U, C, C]: (I + A)^{-1} of the UT transform (App. D.2),
+ *            row-major, strictly-upper 16 x 16 blocks zero.
+ *  The backward reads all of it and so needs no preparation pass of its own.
  *  n_slots from qdelta_saved_state_slots.  Chunk c (0-based) of sequence n
  *  occupies slot  n*ceil(T/chunk) + c  (dense) or  floor(cu[n]/chunk) + n + c
  *  (varlen); slots no chunk maps to are untouched.

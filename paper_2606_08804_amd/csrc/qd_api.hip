@@ -16,15 +16,27 @@ using qd::C;
 constexpr int kVersion = 10000;  // 1.0.0
 
 struct Layout {
-  size_t wb = 0, wU = 0, wW = 0, wP = 0, wKt = 0, wT = 0, wWt = 0, wQt = 0, wM = 0, wdOt = 0;
-  size_t dSo = 0, dDb = 0, states = 0;
+  size_t wb = 0, wU = 0, wW = 0, wP = 0;   // forward: chunk factors when no saved context is kept
+  size_t dSo = 0, dDb = 0, ctx = 0;        // backward: scan outputs, room to recompute the context
   size_t total = 0;
 };
 
-// Saved context: fp32 S^T per unit, then D per unit in the activation dtype.
-size_t saved_states_bytes(size_t units, int Dk, int Dv) { return units * (size_t)Dk * Dv * 4; }
-size_t saved_total_bytes(size_t units, int Dk, int Dv, int esz) {
-  return saved_states_bytes(units, Dk, Dv) + units * (size_t)C * Dv * esz;
+// Saved context, per unit (slot, head), region after region: S^T fp32
+// [Dk][Dv], D [C][Dv], b fp32 [C], W [C][Dk], P [C][C], M [C][C] (D, W, P
+// and M in the activation dtype).
+struct Ctx {
+  size_t states, D, b, W, P, M, total;
+};
+Ctx ctx_layout(size_t units, int Dk, int Dv, int esz) {
+  Ctx c;
+  c.states = 0;
+  c.D = c.states + units * (size_t)Dk * Dv * 4;
+  c.b = c.D + units * (size_t)C * Dv * esz;
+  c.W = c.b + units * (size_t)C * 4;
+  c.P = c.W + units * (size_t)C * Dk * esz;
+  c.M = c.P + units * (size_t)C * C * esz;
+  c.total = c.M + units * (size_t)C * C * esz;
+  return c;
 }
 
 Layout make_layout(size_t units, int Dk, int Dv, int esz, bool bwd) {
@@ -35,23 +47,29 @@ Layout make_layout(size_t units, int Dk, int Dv, int esz, bool bwd) {
     off += (bytes + 255) & ~size_t(255);
     return at;
   };
-  L.wb = take(units * C * 4);
   L.wU = take(units * C * Dv * esz);
-  L.wW = take(units * C * Dk * esz);
-  L.wP = take(units * C * C * esz);
-  L.wKt = take(units * C * Dk * esz);
   if (bwd) {
-    L.wT = take(units * 2 * C * C * esz);
-    L.wWt = take(units * C * Dk * esz);
-    L.wQt = take(units * C * Dk * esz);
-    L.wM = take(units * C * C * esz);
-    L.wdOt = take(units * C * Dv * esz);
     L.dSo = take(units * (size_t)Dv * Dk * esz);
     L.dDb = take(units * C * Dv * esz);
-    L.states = take(saved_total_bytes(units, Dk, Dv, esz));
+    L.ctx = take(ctx_layout(units, Dk, Dv, esz).total);
+  } else {
+    L.wb = take(units * C * 4);
+    L.wW = take(units * C * Dk * esz);
+    L.wP = take(units * C * C * esz);
   }
   L.total = off;
   return L;
+}
+
+// Points the context fields of p (states, D, b, W, P, M) into a context buffer.
+void bind_ctx(qd::Params& p, char* base, size_t units, int Dk, int Dv, int esz) {
+  const Ctx c = ctx_layout(units, Dk, Dv, esz);
+  p.saved = reinterpret_cast<float*>(base + c.states);
+  p.savedD = base + c.D;
+  p.wb = reinterpret_cast<float*>(base + c.b);
+  p.wW = base + c.W;
+  p.wP = base + c.P;
+  p.wM = base + c.M;
 }
 
 bool aligned(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
@@ -137,15 +155,15 @@ int fwd_impl(bool varlen, int32_t B, int32_t T, int32_t N, const int32_t* cu, in
   p.beta = beta; p.lam = lam; p.la = log_alpha; p.S0 = initial_state;
   p.o = has_tokens ? o : nullptr;
   p.Sfin = final_state;
-  if (saved) {
-    p.saved = static_cast<float*>(saved);
-    p.savedD = static_cast<char*>(saved) + saved_states_bytes(s.slots * (size_t)H, Dk, Dv);
-  }
-  p.wb = reinterpret_cast<float*>(w + L.wb);
+  const size_t units = s.slots * (size_t)H;
   p.wU = w + L.wU;
-  p.wW = w + L.wW;
-  p.wP = w + L.wP;
-  p.wKt = w + L.wKt;
+  if (saved) {
+    bind_ctx(p, static_cast<char*>(saved), units, Dk, Dv, esz);
+  } else {
+    p.wb = reinterpret_cast<float*>(w + L.wb);
+    p.wW = w + L.wW;
+    p.wP = w + L.wP;
+  }
   hipError_t e = qd::launch_fwd(p, dtype, Dk, Dv, 0, 1, stream);
   return e == hipSuccess ? QDELTA_OK : QDELTA_EHIP;
 }
@@ -187,37 +205,23 @@ int bwd_impl(bool varlen, int32_t B, int32_t T, int32_t N, const int32_t* cu, in
   p.cu = s.cu;
   p.q = q; p.k = k; p.v = v;
   p.beta = beta; p.lam = lam; p.la = log_alpha; p.S0 = initial_state;
-  p.wb = reinterpret_cast<float*>(w + L.wb);
-  p.wU = w + L.wU;
-  p.wW = w + L.wW;
-  p.wP = w + L.wP;
-  p.wKt = w + L.wKt;
-  p.wT = w + L.wT;
-  p.wWt = w + L.wWt;
-  p.wQt = w + L.wQt;
-  p.wM = w + L.wM;
-  p.wdOt = w + L.wdOt;
   p.dO = d_o;
-  p.dSfin = d_final_state;   // dO is read by the backward-mode preparation as well
+  p.dSfin = d_final_state;
   p.dq = dq; p.dk = dk; p.dv = dv;
   p.dbeta = dbeta; p.dlam = dlam; p.dla = dlog_alpha; p.dS0 = d_initial_state;
   p.w_dSo = w + L.dSo;
   p.w_dDb = w + L.dDb;
   const size_t units = s.slots * (size_t)H;
-  hipError_t e;
+  hipError_t e = hipSuccess;
   if (saved) {
-    p.prep_uw = 0;   // U and W only feed the forward scan, which does not run here
-    p.saved = const_cast<float*>(static_cast<const float*>(saved));
-    p.savedD = const_cast<char*>(static_cast<const char*>(saved)) + saved_states_bytes(units, Dk, Dv);
-    e = qd::launch_fwd(p, dtype, Dk, Dv, 1, 0, stream);
+    bind_ctx(p, const_cast<char*>(static_cast<const char*>(saved)), units, Dk, Dv, esz);
   } else {
     // recompute the saved context (no outputs) into the workspace
-    p.prep_uw = 1;
-    p.saved = reinterpret_cast<float*>(w + L.states);
-    p.savedD = w + L.states + saved_states_bytes(units, Dk, Dv);
+    bind_ctx(p, w + L.ctx, units, Dk, Dv, esz);
+    p.wU = w + L.wU;
     e = qd::launch_fwd(p, dtype, Dk, Dv, 1, 1, stream);
+    if (e != hipSuccess) return QDELTA_EHIP;
   }
-  if (e != hipSuccess) return QDELTA_EHIP;
   e = qd::launch_bwd(p, dtype, Dk, Dv, stream);
   return e == hipSuccess ? QDELTA_OK : QDELTA_EHIP;
 }
@@ -321,7 +325,7 @@ size_t qdelta_saved_bytes(int32_t B, int32_t T, int32_t H, int32_t Dk, int32_t D
   if (B < 0 || T < 0 || n_seqs < 0) return 0;
   const int64_t tokens = n_seqs > 0 ? (int64_t)T : (int64_t)B * T;
   if (check_dims(tokens, H, Dk, Dv, chunk, dtype) != QDELTA_OK) return 0;
-  return saved_total_bytes(slots_for(B, T, n_seqs) * (size_t)H, Dk, Dv, dtype == QDELTA_BF16 ? 2 : 4);
+  return ctx_layout(slots_for(B, T, n_seqs) * (size_t)H, Dk, Dv, dtype == QDELTA_BF16 ? 2 : 4).total;
 }
 
 size_t qdelta_chunk_workspace_bytes(int32_t B, int32_t T, int32_t H, int32_t Dk, int32_t Dv,

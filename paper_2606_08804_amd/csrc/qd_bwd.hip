@@ -34,17 +34,19 @@ namespace qd {
 
 // ------------------------------------------------------------------ scan
 // Backward-scan operands of one chunk, filled by direct global->LDS loads:
-// P^T, T^T (C x C), K (C x Dk), Q^T, W^T (Dk x C), this tile's rows of dO^T
-// (BV x C) as swizzled tiles, then b (C fp32).  Two producer waves split the
-// loads so that each wave's outstanding count stays within the counter.
+// P, M (C x C), K, Q, W (C x Dk) and this tile's columns of dO (C x BV) as
+// swizzled row-major tiles, then b and beta (C fp32 each).  The transposed
+// operands (P^T, M^T, Q^T, W^T, dO^T) are LDS transpose reads of these tiles.
+// Two producer waves split the loads so that each wave's outstanding count
+// stays within the counter.
 template <typename E, int DK, int BV>
 struct ScanBwdRing {
-  static constexpr int RK = DK * (int)sizeof(E), RC = C * (int)sizeof(E);   // row bytes
-  static constexpr int PT = 0, TT = PT + C * RC, K = TT + C * RC, QT = K + C * RK, WT = QT + DK * RC,
-                       DOT = WT + DK * RC, B = DOT + BV * RC, BYTES = B + C * 4;
+  static constexpr int RK = DK * (int)sizeof(E), RC = C * (int)sizeof(E), RO = BV * (int)sizeof(E);
+  static constexpr int PP = 0, MM = PP + C * RC, K = MM + C * RC, Q = K + C * RK, W = Q + C * RK,
+                       DO = W + C * RK, B = DO + C * RO, BE = B + C * 4, BYTES = BE + C * 4;
   static constexpr int NBUF = sizeof(E) == 2 ? 2 : 1;
-  static constexpr int LOADS0 = (QT - PT) / 1024 + 1;   // producer 0: P^T, T^T, K, b
-  static constexpr int LOADS1 = (B - QT) / 1024;        // producer 1: Q^T, W^T, dO^T
+  static constexpr int LOADS0 = (Q - PP) / 1024 + 2;   // producer 0: P, M, K, b, beta
+  static constexpr int LOADS1 = (B - Q) / 1024;        // producer 1: Q, W, dO
   static_assert(NBUF == 1 || (LOADS0 <= 63 && LOADS1 <= 63), "outstanding-load counter range");
 };
 
@@ -93,22 +95,26 @@ __global__ __launch_bounds__(NTHREADS + 128) void k_scan_bwd(Params p) {
     char* r = sm.ring[buf];
     const int t0 = s + c * C, len = min(C, e - t0);
     const size_t gi = (size_t)(base + c) * H + h;
+    const size_t arow = (size_t)t0 * H + h;
+    // rows of K, Q past the chunk come from W, and rows of dO from D: both
+    // are zero there
+    const char* Wg = (const char*)((const E*)p.wW + gi * C * DK);
     if (prod == 0) {
-      const char* Tg = (const char*)((const E*)p.wT + gi * 2 * C * C);
-      const char* Kg = (const char*)((const E*)p.k + ((size_t)t0 * H + h) * DK);
-      dma_rows<R::RC, C, 1, true>(r + R::PT, Tg + C * R::RC, R::RC, C, Tg, 0, 0, lane);
-      dma_rows<R::RC, C, 1, true>(r + R::TT, Tg, R::RC, C, Tg, 0, 0, lane);
-      // rows past the chunk re-read its last row and are zeroed after the wait
-      dma_rows<R::RK, C, 1, true>(r + R::K, Kg, (size_t)H * R::RK, len, Kg + (size_t)(len - 1) * H * R::RK, 0, 0,
-                                  lane);
+      const char* Pg = (const char*)((const E*)p.wP + gi * C * C);
+      const char* Mg = (const char*)((const E*)p.wM + gi * C * C);
+      const char* Kg = (const char*)((const E*)p.k + arow * DK);
+      dma_rows<R::RC, C, 1, true>(r + R::PP, Pg, R::RC, C, Pg, 0, 0, lane);
+      dma_rows<R::RC, C, 1, true>(r + R::MM, Mg, R::RC, C, Mg, 0, 0, lane);
+      dma_rows<R::RK, C, 1, true>(r + R::K, Kg, (size_t)H * R::RK, len, Wg, R::RK, 0, lane);
       dma4_asm(p.wb + gi * C + lane, r + R::B);
+      dma4_asm(p.beta + arow + (size_t)min(lane, len - 1) * H, r + R::BE);
     } else {
-      const char* Qg = (const char*)((const E*)p.wQt + gi * DK * C);
-      const char* Wg = (const char*)((const E*)p.wWt + gi * DK * C);
-      const char* Og = (const char*)((const E*)p.wdOt + gi * DV * C + (size_t)v0 * C);
-      dma_rows<R::RC, DK, 1, true>(r + R::QT, Qg, R::RC, DK, Qg, 0, 0, lane);
-      dma_rows<R::RC, DK, 1, true>(r + R::WT, Wg, R::RC, DK, Wg, 0, 0, lane);
-      dma_rows<R::RC, BV, 1, true>(r + R::DOT, Og, R::RC, BV, Og, 0, 0, lane);
+      const char* Qg = (const char*)((const E*)p.q + arow * DK);
+      const char* Og = (const char*)((const E*)p.dO + arow * DV + v0);
+      const char* Dg = (const char*)((const E*)p.savedD + gi * C * DV + v0);
+      dma_rows<R::RK, C, 1, true>(r + R::Q, Qg, (size_t)H * R::RK, len, Wg, R::RK, 0, lane);
+      dma_rows<R::RK, C, 1, true>(r + R::W, Wg, R::RK, C, Wg, 0, 0, lane);
+      dma_rows<R::RO, C, 1, true>(r + R::DO, Og, (size_t)H * DV * sizeof(E), len, Dg, DV * sizeof(E), 0, lane);
     }
   };
 
@@ -140,12 +146,6 @@ __global__ __launch_bounds__(NTHREADS + 128) void k_scan_bwd(Params p) {
       if (prod == 0) {
         if (ahead) wait_vm<R::NBUF == 2 ? R::LOADS0 : 0>();
         else wait_vm<0>();
-        if (len < C) {
-          // zero the K rows past the chunk (this wave's own loads are complete)
-          char* kz = sm.ring[buf] + R::K;
-          for (int i = len * (R::RK / 16) + lane; i < C * (R::RK / 16); i += 64)
-            *(uint4*)(kz + i * 16) = make_uint4(0, 0, 0, 0);
-        }
       } else {
         if (ahead) wait_vm<R::NBUF == 2 ? R::LOADS1 : 0>();
         else wait_vm<0>();
@@ -184,8 +184,8 @@ __global__ __launch_bounds__(NTHREADS + 128) void k_scan_bwd(Params p) {
         f4 d1 = zero4(), d2 = zero4();
 #pragma unroll UKC
         for (int ks = 0; ks < C / KS; ++ks)
-          d1 = Mma<E>::mma(tile_frag<E, R::RC>(rc + R::PT, 16 * w, ks * KS, lane),
-                           tile_frag<E, R::RC>(rc + R::DOT, nb * 16, ks * KS, lane), d1);
+          d1 = Mma<E>::mma(tile_tr_frag<E, R::RC>(rc + R::PP, ks * KS, 16 * w, lane),
+                           tile_tr_frag<E, R::RO>(rc + R::DO, ks * KS, nb * 16, lane), d1);
 #pragma unroll UKD
         for (int ks = 0; ks < DK / KS; ++ks)
           d2 = Mma<E>::mma(tile_frag<E, R::RK>(rc + R::K, 16 * w, ks * KS, lane),
@@ -214,16 +214,20 @@ __global__ __launch_bounds__(NTHREADS + 128) void k_scan_bwd(Params p) {
           *(uint4*)(ddst + (size_t)r * DV + cc) = o;
         }
       }
-      // dV = T^T dD  (rows 16w..), staged for coalesced stores
+      // dV = T^T dD = diag(beta) M^T dD  (rows 16w..), staged for coalesced stores
+      const float* bech = (const float*)(rc + R::BE);
+      float nbeta[4];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) nbeta[j] = -bech[16 * w + frow(lane, j)];
 #pragma unroll
       for (int nb = 0; nb < NB; ++nb) {
         f4 dv = zero4();
 #pragma unroll UKC
         for (int ks = 0; ks < C / KS; ++ks)
-          dv = Mma<E>::mma(tile_frag<E, R::RC>(rc + R::TT, 16 * w, ks * KS, lane),
+          dv = Mma<E>::mma(tile_tr_frag<E, R::RC>(rc + R::MM, ks * KS, 16 * w, lane),
                            Frag<E>::load(kmaj(&sm.dDn[0][0], LC), nb * 16, ks * KS, lane), dv);
 #pragma unroll
-        for (int j = 0; j < 4; ++j) sm.dV[16 * w + frow(lane, j)][nb * 16 + fcol(lane)] = fromf<E>(-dv[j]);
+        for (int j = 0; j < 4; ++j) sm.dV[16 * w + frow(lane, j)][nb * 16 + fcol(lane)] = fromf<E>(nbeta[j] * dv[j]);
       }
       // dS_entry^T = g_C dS'^T + Q^T diag(g) dO - W^T dD   (the decay scales the
       // dO fragment along the contracted token index)
@@ -235,16 +239,16 @@ __global__ __launch_bounds__(NTHREADS + 128) void k_scan_bwd(Params p) {
 #pragma unroll UKC
         for (int ks = 0; ks < C / KS; ++ks) {
           const FR bd = Frag<E>::load(kmaj(&sm.dDn[0][0], LC), nb * 16, ks * KS, lane);
-          FR gdo = tile_frag<E, R::RC>(rc + R::DOT, nb * 16, ks * KS, lane);
+          FR gdo = tile_tr_frag<E, R::RO>(rc + R::DO, ks * KS, nb * 16, lane);
           E* ge = (E*)&gdo;
 #pragma unroll
           for (int e2 = 0; e2 < Mma<E>::KPL; ++e2)
             ge[e2] = fromf<E>(__expf(bch[ks * KS + (lane >> 4) * Mma<E>::KPL + e2]) * tof(ge[e2]));
 #pragma unroll
           for (int i = 0; i < KPW; ++i) {
-            acc[i][nb] = Mma<E>::mma(tile_frag<E, R::RC>(rc + R::QT, 16 * (KPW * w + i), ks * KS, lane), gdo,
+            acc[i][nb] = Mma<E>::mma(tile_tr_frag<E, R::RK>(rc + R::Q, ks * KS, 16 * (KPW * w + i), lane), gdo,
                                      acc[i][nb]);
-            acc[i][nb] = Mma<E>::mma(tile_frag<E, R::RC>(rc + R::WT, 16 * (KPW * w + i), ks * KS, lane), bd,
+            acc[i][nb] = Mma<E>::mma(tile_tr_frag<E, R::RK>(rc + R::W, ks * KS, 16 * (KPW * w + i), lane), bd,
                                      acc[i][nb]);
           }
         }
@@ -339,10 +343,9 @@ struct alignas(16) BwdSmem {
       } u;
     } s;
   } x;
-  // M = (I + A)^{-1} (r, i) and T^T (i, r), direct-loaded at the start (swizzled
-  // rows of C elements, outside the phase-A ring)
+  // M = (I + A)^{-1} (r, i), direct-loaded at the start (swizzled rows of C
+  // elements, outside the phase-A ring)
   alignas(16) char Mm[C * C * sizeof(E)];
-  alignas(16) char TmT[C * C * sizeof(E)];
 };
 
 // s * (k + l * q) element-wise on one fragment, rounded to the operand type
@@ -437,13 +440,11 @@ __global__ __launch_bounds__(INTRA_THREADS) void k_bwd_intra(Params p) {
   asm volatile("" ::: "memory");
   // direct loads are issued by waves 0-3 only; the others' waits are no-ops
   const bool loader = w < NWAVES;
-  // M = (I + A)^{-1} and T^T from the preparation
+  // M = (I + A)^{-1} from the preparation
   constexpr int RBC = C * (int)sizeof(E);
   if (loader) {
     const char* Mg = (const char*)((const E*)p.wM + gi * C * C);
-    const char* Tg = (const char*)((const E*)p.wT + gi * 2 * C * C);
     dma_rows<RBC, C>(sm.Mm, Mg, RBC, C, Mg, 0, w, lane);
-    dma_rows<RBC, C>(sm.TmT, Tg, RBC, C, Tg, 0, w, lane);
   }
   // rows of V and dO past the chunk come from D, whose rows there are zero
   auto issue = [&](int vt) {
@@ -662,7 +663,8 @@ __global__ __launch_bounds__(INTRA_THREADS) void k_bwd_intra(Params p) {
 
   // ---------------- phase B3: dX, dq, dk (rows 16 rb.., Dk blocks of this half)
   // K^T, Q^T and dW^T fragments are transpose reads of the row-major K, Q, dW
-  // kept since phase B1; dQK^T and dG^T likewise of dQK and dG
+  // kept since phase B1; dQK^T, dG^T and M^T likewise of dQK, dG and M
+  // (T^T dW = diag(beta) M^T dW)
   {
     constexpr int NTK = C / KS;
     FR tA[NTK], gA[NTK], qkA[NTK], qktA[NTK], gtA[NTK];
@@ -671,7 +673,7 @@ __global__ __launch_bounds__(INTRA_THREADS) void k_bwd_intra(Params p) {
     const E* dQKp = &sm.x.s.u.b2.v.g.dQK[0][0];
 #pragma unroll
     for (int ks = 0; ks < NTK; ++ks) {
-      tA[ks] = tile_frag<E, RBC>(sm.TmT, 16 * rb, ks * KS, lane);
+      tA[ks] = tile_tr_frag<E, RBC>(sm.Mm, ks * KS, 16 * rb, lane);
       gA[ks] = Frag<E>::load(kmaj(dGp, LC), 16 * rb, ks * KS, lane);
       qkA[ks] = Frag<E>::load(kmaj(dQKp, LC), 16 * rb, ks * KS, lane);
       qktA[ks] = tr_frag<E>(dQKp, LC, ks * KS, 16 * rb, lane);
@@ -681,12 +683,13 @@ __global__ __launch_bounds__(INTRA_THREADS) void k_bwd_intra(Params p) {
     }
     const int r0 = 16 * rb + frow(lane, 0);
     float rdb[4] = {0.f, 0.f, 0.f, 0.f}, rtk[4] = {0.f, 0.f, 0.f, 0.f}, rdl[4] = {0.f, 0.f, 0.f, 0.f};
-    float gr4[4], lr4[4], kbr4[4];
+    float gr4[4], lr4[4], kbr4[4], br4[4];
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       gr4[j] = sm.g[r0 + j];
       lr4[j] = sm.lam[r0 + j];
       kbr4[j] = sm.kb[r0 + j];
+      br4[j] = sm.beta[r0 + j];
     }
     const E* Kp = &sm.x.s.b1.K[0][0];
     const E* Qp = &sm.x.s.b1.Q[0][0];
@@ -701,7 +704,7 @@ __global__ __launch_bounds__(INTRA_THREADS) void k_bwd_intra(Params p) {
         const FR qtB = tr_frag<E>(Qp, LKD, ks * KS, kb * 16, lane);
         const FR dwB = tr_frag<E>(dWp, LKD, ks * KS, kb * 16, lane);
         const FR xtB = mix_tokens<FR>(ktB, qtB, lamk[ks]);
-        dgx = Mma<E>::mma(tA[ks], dwB, dgx);      // T^T dW
+        dgx = Mma<E>::mma(tA[ks], dwB, dgx);      // M^T dW
         dxp = Mma<E>::mma(gA[ks], ktB, dxp);      // dG K
         dqp = Mma<E>::mma(qkA[ks], ktB, dqp);     // dQK K
         dkp = Mma<E>::mma(qktA[ks], qtB, dkp);    // dQK^T Q
@@ -715,10 +718,10 @@ __global__ __launch_bounds__(INTRA_THREADS) void k_bwd_intra(Params p) {
         const int r = r0 + j;
         const float Kv = kv[j], Qv = qv[j];
         const float gr = gr4[j], lr = lr4[j], kbr = kbr4[j];
-        const float X = Kv + lr * Qv;
-        rdb[j] += gr * (X * dgx[j] + Qv * aQ[i][j]);
+        const float X = Kv + lr * Qv, tdw = br4[j] * dgx[j];   // (T^T dW)_r
+        rdb[j] += gr * (X * tdw + Qv * aQ[i][j]);
         rtk[j] += kbr * Kv * aK[i][j];
-        const float dX = gr * dgx[j] + dxp[j];
+        const float dX = gr * tdw + dxp[j];
         rdl[j] += Qv * dX;
         sm.x.s.u.b3.oq[r][kc] = fromf<E>(gr * aQ[i][j] + dqp[j] + lr * dX);
         sm.x.s.u.b3.ok[r][kc] = fromf<E>(kbr * aK[i][j] + dkp[j] + dX);

@@ -402,6 +402,26 @@ __device__ inline typename Mma<E>::frag tile_frag(const char* t, int row0, int k
   const int row = row0 + (lane & 15), k = k0 + (lane >> 4) * Mma<E>::KPL;
   return *(const typename Mma<E>::frag*)(t + tile_off<RB>(row, k * (int)sizeof(E)));
 }
+// Fragment of the TRANSPOSE of a swizzled LDS tile (rows of RB bytes): for
+// lane l the values at tile rows k0 + (l >> 4) * KPL + e, e < KPL, and column
+// j0 + (l & 15) (j0 a multiple of 16), i.e. the operand whose "row" index is
+// the tile column.  16-bit tiles use the LDS transpose read (see tr_frag
+// below): each 8-byte piece lies inside one 16-byte chunk, so the swizzle
+// applies per piece.
+template <typename E, int RB>
+__device__ inline typename Mma<E>::frag tile_tr_frag(const char* t, int k0, int j0, int lane) {
+  if constexpr (sizeof(E) == 2) {
+    typedef __bf16 v4b __attribute__((ext_vector_type(4)));
+    typedef __attribute__((address_space(3))) v4b* lp;
+    const int L = lane & 15, i0 = k0 + (lane >> 4) * 8 + (L >> 2), jb = 2 * (j0 + 4 * (L & 3));
+    const v4b lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lp)(uintptr_t)(uint32_t)(uintptr_t)(t + tile_off<RB>(i0, jb)));
+    const v4b hi =
+        __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lp)(uintptr_t)(uint32_t)(uintptr_t)(t + tile_off<RB>(i0 + 4, jb)));
+    return __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+  } else {
+    return *(const float*)(t + tile_off<RB>(k0 + (lane >> 4), 4 * (j0 + (lane & 15))));
+  }
+}
 // MFMA fragment of the TRANSPOSE of a row-major 16-bit LDS matrix: with
 // element (i, j) at base + i * ld + j (ld in elements), returns for lane l the
 // fragment values (i = k0 + (l >> 4) * KPL + e, j = j0 + (l & 15)), e < KPL,
@@ -477,7 +497,6 @@ struct Params {
   int H;
   int NT;         // dense: ceil(T / C)
   int n_slots;    // saved-state / workspace slots
-  int prep_uw;      // backward-mode preparation also writes U and W (for a recompute)
   int lead;         // intra-chunk backward: leading workgroups that only wait
   int lead_cycles;  // ... and for how many clock cycles
   const int* cu;  // varlen cu_seqlens (device) or nullptr
@@ -494,17 +513,13 @@ struct Params {
   float* Sfin;
   float* saved;          // saved context: entry states S^T [slot][H][Dk][Dv] (fp32)
   void* savedD;          // saved context: D [slot][H][C][Dv] (dtype)
-  // workspace (per slot and head)
+  // chunk factors from the preparation, per slot and head (in the saved
+  // context when one is kept, else in the workspace)
   float* wb;             // [slot][H][C] chunk-local prefix sums of log alpha
-  void* wU;              // [slot][H] C x Dv, C-fragment tiled
-  void* wW;              // [slot][H][C][Dk]
+  void* wU;              // [slot][H] C x Dv, C-fragment tiled (workspace only)
+  void* wW;              // [slot][H][C][Dk]  W = T diag(g) X
   void* wP;              // [slot][H][C][C]   P = Gam * M * Q K^T
-  void* wKt;             // [slot][H][Dk][C]  K^T
-  void* wT;              // [slot][H][2][C][C] T^T and P^T (backward only)
-  void* wWt;             // [slot][H][Dk][C]  W^T (backward only)
-  void* wQt;             // [slot][H][Dk][C]  Q^T (backward only)
-  void* wM;              // [slot][H][C][C]   (I + A)^{-1} (backward only)
-  void* wdOt;            // [slot][H][Dv][C]  dO^T (backward only)
+  void* wM;              // [slot][H][C][C]   M = (I + A)^{-1}, or nullptr when not kept
   // backward
   const void* dO;
   const float* dSfin;

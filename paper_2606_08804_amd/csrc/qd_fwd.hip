@@ -13,8 +13,8 @@
 //   O   = diag(g) Q S^T + (Gam * M * Q K^T) D     (M includes the diagonal)
 //   S'  = g_C S + D^T diag(g_C / g) K
 //
-// k_prep   (one workgroup per chunk and head, fully parallel): b, X, the two
-//          Gram products, A, the UT solve, U and W; writes them to workspace.
+// k_prep   (persistent over chunk-head units, fully parallel): b, X, the two
+//          Gram products, A, the UT solve, U and W; writes b, U, W, P and M.
 // k_scan_fwd (one workgroup per sequence, head and Dv tile): the sequential
 //          pass over chunks; the state tile stays in MFMA accumulators in fp32;
 //          D, the chunk output and the state update are computed on chip.
@@ -36,56 +36,50 @@ struct PrepSmem {
       E X[C][DK + P];
     } a;
     E Vt[DV][C + P];
-    E dO[C][DV + P];
   } u;
-  E GXt[DK][C + P];
-  float A[C][C + 4];
+  E GX[C][DK + P];        // diag(g) X (r, k)
+  union {
+    float A[C][C + 4];    // strictly lower A, consumed by the solve
+    E Ws[C][DK + P];      // W staging for 16-byte stores, after the solve
+  } am;
   float M[C][C + 4];
-  E Tm[C][C + P];
+  E Tm[C][C + P];         // P staging during the Gram products, then T
 };
-
-// dst[c*C + r] = scale(r) * src[r*ld + c] for a C x D LDS tile, written to
-// global memory with 16-byte stores (one store covers 16/sizeof(E) rows).
-template <typename E, int D, int NT, typename Scale>
-__device__ inline void store_transposed(E* dst, const E* src, int ld, int tid, Scale scale) {
-  constexpr int VEC = 16 / sizeof(E);
-  constexpr int G = C / VEC;
-  // consecutive threads take consecutive columns c: the column reads of the
-  // LDS tile hit consecutive addresses (no bank conflicts)
-  for (int idx = tid; idx < D * G; idx += NT) {
-    const int c = idx % D, r0 = (idx / D) * VEC;
-    uint4 raw;
-    E* e = (E*)&raw;
-#pragma unroll
-    for (int j = 0; j < VEC; ++j) e[j] = fromf<E>(tof(src[(size_t)(r0 + j) * ld + c]) * scale(r0 + j));
-    *(uint4*)(dst + (size_t)c * C + r0) = raw;
-  }
-}
 
 // Raw inputs of one (chunk, head) unit, staged in registers one unit ahead.
 constexpr int PREP_THREADS = 512;   // 8 waves: two per SIMD hide each other's latency
 
-template <typename E, int DK, int DV, bool BWD>
+template <typename E, int DK, int DV>
 struct PrepPre {
   TileRegs<E, C, DK, PREP_THREADS> K, Q;
   TileRegsT<E, C, DV, PREP_THREADS> V;
-  typename std::conditional<BWD, TileRegs<E, C, DV, PREP_THREADS>, NoRegs>::type dO;
   float la, beta, lam;
   int t0, len, g, h;
   bool valid;
 };
 
-// Forward mode writes b, U, W, P and K^T.  Backward mode (BWD) writes b, U,
-// W and K^T plus T, P^T, W^T, (diag(g) Q)^T and dO^T for the backward kernels.
+// Copies a C x D LDS tile (row stride ld elements) to a dense row-major
+// global block with 16-byte stores.
+template <typename E, int D, int NT>
+__device__ inline void store_tile(E* dst, const E* src, int ld, int tid) {
+  constexpr int VEC = 16 / sizeof(E), PR = D / VEC;
+  for (int idx = tid; idx < C * PR; idx += NT) {
+    const int r = idx / PR, c = (idx % PR) * VEC;
+    *(uint4*)(dst + (size_t)r * D + c) = *(const uint4*)(src + (size_t)r * ld + c);
+  }
+}
+
+// Writes b, U, W, P and, when p.wM is set, M = (I + A)^{-1} for every unit.
 // Persistent: each workgroup walks units blockIdx.x, +gridDim.x, ... and
 // prefetches the next unit's inputs into registers while computing the
 // current one.
-template <typename E, int DK, int DV, bool BWD>
+template <typename E, int DK, int DV>
 __global__ __launch_bounds__(PREP_THREADS) void k_prep(Params p) {
   constexpr int NT = PREP_THREADS, NW = NT / 64;
   constexpr int P = Pad<E>::v;
   constexpr int LK = DK + P, LC = C + P;
-  typedef PrepPre<E, DK, DV, BWD> Pre;
+  constexpr int KS = Mma<E>::KS;
+  typedef PrepPre<E, DK, DV> Pre;
   __shared__ PrepSmem<E, DK, DV> sm;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int H = p.H;
@@ -102,8 +96,7 @@ __global__ __launch_bounds__(PREP_THREADS) void k_prep(Params p) {
     const size_t row = (size_t)x.t0 * H + x.h;
     x.K.load((const E*)p.k + row * DK, (size_t)H * DK, x.len, tid);
     x.Q.load((const E*)p.q + row * DK, (size_t)H * DK, x.len, tid);
-    if (!BWD || p.prep_uw) x.V.load((const E*)p.v + row * DV, (size_t)H * DV, x.len, tid);
-    if constexpr (BWD) x.dO.load((const E*)p.dO + row * DV, (size_t)H * DV, x.len, tid);
+    x.V.load((const E*)p.v + row * DV, (size_t)H * DV, x.len, tid);
     if (tid < C) {
       const bool ok = tid < x.len;
       const size_t gt = row + (size_t)tid * H;
@@ -133,60 +126,56 @@ __global__ __launch_bounds__(PREP_THREADS) void k_prep(Params p) {
     }
     block_sync_lds();
 
-    // transposed copies for the scans: K^T, and (diag(g) Q)^T for the backward
-    store_transposed<E, DK, NT>((E*)p.wKt + gi * DK * C, &sm.u.a.K[0][0], LK, tid, One());
-    if (BWD) store_transposed<E, DK, NT>((E*)p.wQt + gi * DK * C, &sm.u.a.Q[0][0], LK, tid, One());
-    // mixed inputs X = K + lambda Q and the transposed decayed copy (g X)^T;
-    // a thread takes 16 bytes of one row, consecutive threads consecutive rows
+    // mixed inputs X = K + lambda Q and the decayed copy diag(g) X; a thread
+    // takes 16 bytes of one row
     {
       constexpr int VEC = 16 / sizeof(E);
       for (int idx = tid; idx < C * DK / VEC; idx += NT) {
-        const int r = idx % C, c0 = (idx / C) * VEC;
+        const int r = idx / (DK / VEC), c0 = (idx % (DK / VEC)) * VEC;
         const uint4 kr = *(const uint4*)&sm.u.a.K[r][c0];
         const uint4 qr = *(const uint4*)&sm.u.a.Q[r][c0];
         const E* ke = (const E*)&kr;
         const E* qe = (const E*)&qr;
         const float lr = sm.lam[r], gr = __expf(sm.b[r]);
-        uint4 xr;
+        uint4 xr, gxr;
         E* xe = (E*)&xr;
+        E* gxe = (E*)&gxr;
 #pragma unroll
         for (int j = 0; j < VEC; ++j) {
           const float xv = tof(ke[j]) + lr * tof(qe[j]);
           xe[j] = fromf<E>(xv);
-          sm.GXt[c0 + j][r] = fromf<E>(gr * xv);
+          gxe[j] = fromf<E>(gr * xv);
         }
         *(uint4*)&sm.u.a.X[r][c0] = xr;
+        *(uint4*)&sm.GX[r][c0] = gxr;
       }
     }
     block_sync_lds();
 
-    // Gram products X K^T and Q K^T; A (fp32, LDS) and P or P^T (workspace)
-    E* wP = BWD ? (E*)p.wT + gi * 2 * C * C + C * C : (E*)p.wP + gi * C * C;
+    // Gram products X K^T and Q K^T; A (fp32) and P (staged in Tm)
     for (int t = w; t < 16; t += NW) {
       const int m0 = (t >> 2) * 16, n0 = (t & 3) * 16;
       const f4 gx = mma_k<E, DK>(kmaj(&sm.u.a.X[0][0], LK), kmaj(&sm.u.a.K[0][0], LK), m0, n0, zero4(), lane);
       const f4 qk = mma_k<E, DK>(kmaj(&sm.u.a.Q[0][0], LK), kmaj(&sm.u.a.K[0][0], LK), m0, n0, zero4(), lane);
-      f4 pv;
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
         const int r = m0 + frow(lane, j), i = n0 + fcol(lane);
         const float gam = (r >= i) ? __expf(sm.b[r] - sm.b[i]) : 0.f;
-        sm.A[r][i] = (r > i) ? sm.beta[r] * gam * gx[j] : 0.f;
-        pv[j] = gam * qk[j];
-        if (!BWD) wP[r * C + i] = fromf<E>(pv[j]);
+        sm.am.A[r][i] = (r > i) ? sm.beta[r] * gam * gx[j] : 0.f;
+        sm.Tm[r][i] = fromf<E>(gam * qk[j]);
       }
-      if (BWD)
-        *(typename Quad<E>::raw*)(wP + (n0 + fcol(lane)) * C + m0 + frow(lane, 0)) = Quad<E>::pack(pv);
     }
     block_sync_lds();
+    // P out before the solve (whose barriers order the later T writes to Tm)
+    store_tile<E, C, NT>((E*)p.wP + gi * C * C, &sm.Tm[0][0], LC, tid);
 
     // UT solve: M = (I + A)^{-1}, T = M diag(beta)
-    unit_lower_inverse<NT>(&sm.A[0][0], C + 4, &sm.M[0][0], C + 4, tid);
+    unit_lower_inverse<NT>(&sm.am.A[0][0], C + 4, &sm.M[0][0], C + 4, tid);
     {
-      // T row-major into LDS (and M into the workspace in backward mode);
-      // a thread takes VEC consecutive columns of one row
+      // T row-major into LDS and M to global; a thread takes VEC consecutive
+      // columns of one row
       constexpr int VEC = 16 / sizeof(E);
-      E* wM = BWD ? (E*)p.wM + gi * C * C : nullptr;
+      E* wM = (E*)p.wM;
       for (int idx = tid; idx < C * C / VEC; idx += NT) {
         const int r = idx / (C / VEC), i0 = (idx % (C / VEC)) * VEC;
         const bool upper = (i0 >> 4) > (r >> 4);   // strictly-upper block: zero
@@ -200,61 +189,39 @@ __global__ __launch_bounds__(PREP_THREADS) void k_prep(Params p) {
           me[j] = fromf<E>(m);
         }
         *(uint4*)&sm.Tm[r][i0] = tr;
-        if (BWD) *(uint4*)(wM + r * C + i0) = mr;
-      }
-      if (BWD) {
-        // T^T for the backward kernels: VEC consecutive rows of one column
-        E* wTt = (E*)p.wT + gi * 2 * C * C;
-        for (int idx = tid; idx < C * C / VEC; idx += NT) {
-          const int i = idx % C, r0 = (idx / C) * VEC;
-          const float bi = sm.beta[i];
-          uint4 tr;
-          E* te = (E*)&tr;
-#pragma unroll
-          for (int j = 0; j < VEC; ++j) te[j] = fromf<E>(((i >> 4) > ((r0 + j) >> 4)) ? 0.f : sm.M[r0 + j][i] * bi);
-          *(uint4*)(wTt + i * C + r0) = tr;
-        }
+        if (wM) *(uint4*)(wM + gi * C * C + r * C + i0) = mr;
       }
     }
-    // U and W feed only the forward scan: a backward preparation that has the
-    // forward's saved context skips U and the row-major W
-    const bool uw = !BWD || p.prep_uw;
     // V^T (K, Q, X are dead: all reads of them finished before the solve's barriers)
-    if (uw) x.V.storeT(&sm.u.Vt[0][0], LC, tid);
+    x.V.storeT(&sm.u.Vt[0][0], LC, tid);
     block_sync_lds();
 
     // U = T V, stored C-fragment tiled: tile (mt, nt) at ((mt*(DV/16)+nt)*64 + lane)*4
     E* wU = (E*)p.wU + gi * C * DV;
-    for (int t = w; uw && t < (C / 16) * (DV / 16); t += NW) {
+    for (int t = w; t < (C / 16) * (DV / 16); t += NW) {
       const int m0 = (t / (DV / 16)) * 16, n0 = (t % (DV / 16)) * 16;
       const f4 uu = mma_k<E, C>(kmaj(&sm.Tm[0][0], LC), kmaj(&sm.u.Vt[0][0], LC), m0, n0, zero4(), lane);
       *(typename Quad<E>::raw*)(wU + ((size_t)t * 64 + lane) * 4) = Quad<E>::pack(uu);
     }
-    // W = T diag(g) X, row-major C x DK (and W^T in backward mode)
-    E* wW = (E*)p.wW + gi * C * DK;
-    E* wWt = BWD ? (E*)p.wWt + gi * DK * C : nullptr;
+    // W = T diag(g) X (the B operand is a transpose read of diag(g) X), staged
+    // row-major for 16-byte stores
     for (int t = w; t < (C / 16) * (DK / 16); t += NW) {
       const int m0 = (t / (DK / 16)) * 16, n0 = (t % (DK / 16)) * 16;
-      const f4 wv = mma_k<E, C>(kmaj(&sm.Tm[0][0], LC), kmaj(&sm.GXt[0][0], LC), m0, n0, zero4(), lane);
-      if (uw) {
+      f4 wv = zero4();
 #pragma unroll
-        for (int j = 0; j < 4; ++j) wW[(m0 + frow(lane, j)) * DK + n0 + fcol(lane)] = fromf<E>(wv[j]);
-      }
-      if (BWD)
-        *(typename Quad<E>::raw*)(wWt + (size_t)(n0 + fcol(lane)) * C + m0 + frow(lane, 0)) = Quad<E>::pack(wv);
+      for (int ks = 0; ks < C / KS; ++ks)
+        wv = Mma<E>::mma(Frag<E>::load(kmaj(&sm.Tm[0][0], LC), m0, ks * KS, lane),
+                         tr_frag<E>(&sm.GX[0][0], LK, ks * KS, n0, lane), wv);
+#pragma unroll
+      for (int j = 0; j < 4; ++j) sm.am.Ws[m0 + frow(lane, j)][n0 + fcol(lane)] = fromf<E>(wv[j]);
     }
-    if constexpr (BWD) {
-      // dO^T for the backward scan's fragment loads
-      block_sync_lds();
-      x.dO.store(&sm.u.dO[0][0], DV + P, tid);
-      block_sync_lds();
-      store_transposed<E, DV, NT>((E*)p.wdOt + gi * DV * C, &sm.u.dO[0][0], DV + P, tid, One());
-    }
+    block_sync_lds();
+    store_tile<E, DK, NT>((E*)p.wW + gi * C * DK, &sm.am.Ws[0][0], LK, tid);
   }
 }
 
 // Forward-scan operands of one chunk, filled by direct global->LDS loads:
-// W (C x Dk), K^T (Dk x C), Q (C x Dk), P (C x C) as swizzled tiles, then
+// W, K, Q (C x Dk) and P (C x C) as swizzled row-major tiles, then
 // this workgroup's U fragments (byte copy of the C-fragment-ordered layout)
 // and b (C fp32).
 template <typename E, int DK, int BV>
@@ -262,7 +229,7 @@ struct ScanFwdRing {
   static constexpr int RK = DK * (int)sizeof(E), RC = C * (int)sizeof(E);   // row bytes
   static constexpr int NB = BV / 16;
   static constexpr int UM = NB * 64 * 4 * (int)sizeof(E);   // U bytes per 16-row block
-  static constexpr int W = 0, KT = W + C * RK, Q = KT + DK * RC, PP = Q + C * RK, U = PP + C * RC,
+  static constexpr int W = 0, K = W + C * RK, Q = K + C * RK, PP = Q + C * RK, U = PP + C * RC,
                        B = U + 4 * UM, BYTES = B + C * 4;
   static constexpr int NBUF = sizeof(E) == 2 ? 2 : 1;      // fp32 tiles are twice as large
   static constexpr int LOADS = (B - W) / 1024 + 1;           // direct loads per chunk
@@ -323,12 +290,12 @@ __global__ __launch_bounds__(NTHREADS + 64) void k_scan_fwd(Params p) {
     const int t0 = s + c * C, len = min(C, e - t0);
     const size_t gi = (size_t)(base + c) * H + h;
     const char* Wg = (const char*)((const E*)p.wW + gi * C * DK);
-    const char* Kg = (const char*)((const E*)p.wKt + gi * DK * C);
+    const char* Kg = (const char*)((const E*)p.k + ((size_t)t0 * H + h) * DK);
     const char* Qg = (const char*)((const E*)p.q + ((size_t)t0 * H + h) * DK);
     const char* Pg = (const char*)((const E*)p.wP + gi * C * C);
     dma_rows<R::RK, C, 1, true>(r + R::W, Wg, R::RK, C, Wg, 0, 0, lane);
-    dma_rows<R::RC, DK, 1, true>(r + R::KT, Kg, R::RC, DK, Kg, 0, 0, lane);
-    // rows of Q past the chunk come from W, whose rows there are zero
+    // rows of K and Q past the chunk come from W, whose rows there are zero
+    dma_rows<R::RK, C, 1, true>(r + R::K, Kg, (size_t)H * R::RK, len, Wg, R::RK, 0, lane);
     dma_rows<R::RK, C, 1, true>(r + R::Q, Qg, (size_t)H * R::RK, len, Wg, R::RK, 0, lane);
     dma_rows<R::RC, C, 1, true>(r + R::PP, Pg, R::RC, C, Pg, 0, 0, lane);
 #pragma unroll
@@ -448,7 +415,7 @@ __global__ __launch_bounds__(NTHREADS + 64) void k_scan_fwd(Params p) {
 #pragma unroll
           for (int j = 0; j < 4; ++j) oo[nb][j] = __expf(bch[16 * w + frow(lane, j)]) * o1[j] + o2[j];
         }
-        // S^T <- g_C S^T + K^T diag(g_C/g) D
+        // S^T <- g_C S^T + K^T diag(g_C/g) D  (K^T fragments are transpose reads of the K tile)
         const float gC = __expf(bl);
 #pragma unroll
         for (int nb = 0; nb < NB; ++nb) {
@@ -459,7 +426,7 @@ __global__ __launch_bounds__(NTHREADS + 64) void k_scan_fwd(Params p) {
             const FR bf = Frag<E>::load(kmaj(&sm.Dkt[0][0], LC), nb * 16, ks * KS, lane);
 #pragma unroll
             for (int i = 0; i < KPW; ++i)
-              acc[i][nb] = Mma<E>::mma(tile_frag<E, R::RC>(rc + R::KT, 16 * (KPW * w + i), ks * KS, lane), bf,
+              acc[i][nb] = Mma<E>::mma(tile_tr_frag<E, R::RK>(rc + R::K, ks * KS, 16 * (KPW * w + i), lane), bf,
                                        acc[i][nb]);
           }
         }
@@ -479,7 +446,7 @@ __global__ __launch_bounds__(NTHREADS + 64) void k_scan_fwd(Params p) {
             const FR bf = Frag<E>::load(kmaj(&sm.Dkt[0][0], LC), nb * 16, ks * KS, lane);
 #pragma unroll
             for (int i = 0; i < KPW; ++i)
-              acc[i][nb] = Mma<E>::mma(tile_frag<E, R::RC>(rc + R::KT, 16 * (KPW * w + i), ks * KS, lane), bf,
+              acc[i][nb] = Mma<E>::mma(tile_tr_frag<E, R::RK>(rc + R::K, ks * KS, 16 * (KPW * w + i), lane), bf,
                                        acc[i][nb]);
           }
         }
@@ -512,17 +479,14 @@ __global__ __launch_bounds__(NTHREADS + 64) void k_scan_fwd(Params p) {
 
 // ------------------------------------------------------------------ launchers
 template <typename E, int DK, int DV>
-static hipError_t launch_fwd_t(const Params& p, int bwd_prep, int with_scan, hipStream_t st) {
+static hipError_t launch_fwd_t(const Params& p, int in_bwd, int with_scan, hipStream_t st) {
   constexpr int BV = 32;   // value columns per forward-scan workgroup
   if (p.n_slots > 0) {
     const int units = p.n_slots * p.H;
     dim3 gp(min(units, device_cu_count()));
-    const int stage = bwd_prep ? ST_PREP_BWD : ST_PREP_FWD;
+    const int stage = in_bwd ? ST_PREP_BWD : ST_PREP_FWD;
     prof_mark(stage, 0, st);
-    if (bwd_prep)
-      hipLaunchKernelGGL((k_prep<E, DK, DV, true>), gp, dim3(PREP_THREADS), 0, st, p);
-    else
-      hipLaunchKernelGGL((k_prep<E, DK, DV, false>), gp, dim3(PREP_THREADS), 0, st, p);
+    hipLaunchKernelGGL((k_prep<E, DK, DV>), gp, dim3(PREP_THREADS), 0, st, p);
     prof_mark(stage, 1, st);
   }
   if (with_scan) {
@@ -537,10 +501,10 @@ static hipError_t launch_fwd_t(const Params& p, int bwd_prep, int with_scan, hip
   return hipGetLastError();
 }
 
-hipError_t launch_fwd(const Params& p, int dtype, int Dk, int Dv, int bwd_prep, int with_scan,
+hipError_t launch_fwd(const Params& p, int dtype, int Dk, int Dv, int in_bwd, int with_scan,
                       hipStream_t st) {
 #define QD_CASE(ET, DKV, DVV) \
-  if (Dk == DKV && Dv == DVV) return launch_fwd_t<ET, DKV, DVV>(p, bwd_prep, with_scan, st);
+  if (Dk == DKV && Dv == DVV) return launch_fwd_t<ET, DKV, DVV>(p, in_bwd, with_scan, st);
   if (dtype == 1) {
     QD_CASE(__bf16, 64, 64) QD_CASE(__bf16, 64, 128) QD_CASE(__bf16, 64, 256)
     QD_CASE(__bf16, 128, 64) QD_CASE(__bf16, 128, 128) QD_CASE(__bf16, 128, 256)

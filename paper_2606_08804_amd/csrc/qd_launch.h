@@ -23,12 +23,13 @@ void prof_mark(int stage, int after, hipStream_t st);
 
 // Chunk preparation (UT solve, WY factors) over all slots, then, if
 // with_scan, the sequential forward state scan (+ chunk outputs when p.o is
-// set).  bwd_prep also stores T and P^T for the backward kernels.
-hipError_t launch_fwd(const Params& p, int dtype, int Dk, int Dv, int bwd_prep, int with_scan,
+// set).  in_bwd only labels the launches for the measurement facility (a
+// backward that recomputes the saved context).
+hipError_t launch_fwd(const Params& p, int dtype, int Dk, int Dv, int in_bwd, int with_scan,
                       hipStream_t st);
 
-// Backward after the preparation and the saved states are in place: reverse
-// state scan, then the two intra-chunk gradient kernels.
+// Backward once the saved context (states, D, b, W, P, M) is in place:
+// reverse state scan, then the intra-chunk gradient kernel.
 hipError_t launch_bwd(const Params& p, int dtype, int Dk, int Dv, hipStream_t st);
 
 // One token of the recurrence for N sequences.

@@ -45,9 +45,12 @@ def test_saved_state_slots():
 
 
 def test_saved_context_bytes():
-    # per (slot, head): fp32 Dk x Dv state + C x Dv new values in the activation dtype
-    assert qdelta.saved_bytes(4, 4096, 16, 128, 128, 1) == 256 * 16 * (128 * 128 * 4 + 64 * 128 * 2)
-    assert qdelta.saved_bytes(1, 100, 2, 64, 64, 0) == 2 * 2 * (64 * 64 * 4 + 64 * 64 * 4)
+    # per (slot, head): fp32 Dk x Dv state, C x Dv new values D, fp32 b (C), W (C x Dk),
+    # P and M (C x C), all but the state and b in the activation dtype
+    def per_unit(Dk, Dv, e):
+        return Dk * Dv * 4 + 64 * Dv * e + 64 * 4 + 64 * Dk * e + 2 * 64 * 64 * e
+    assert qdelta.saved_bytes(4, 4096, 16, 128, 128, 1) == 256 * 16 * per_unit(128, 128, 2)
+    assert qdelta.saved_bytes(1, 100, 2, 64, 64, 0) == 2 * 2 * per_unit(64, 64, 4)
     assert qdelta.saved_bytes(4, 4096, 16, 96, 128, 1) == 0
 
 
