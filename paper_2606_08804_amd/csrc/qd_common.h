@@ -328,12 +328,20 @@ __device__ inline void wait_vm() {
 }
 
 // LDS tiles written by direct loads are rows of RB bytes (64, 128 or 256) made of
-// 16-byte chunks; chunk c of row r sits at slot c ^ swz(r), so that sixteen
-// consecutive rows read at the same chunk hit distinct banks.
+// 16-byte chunks; chunk c of row r sits at slot c ^ swz(r).  swz is a linear
+// (XOR) map of the low four row bits, chosen by measuring on gfx950 every such
+// map of full rank for three read patterns: MFMA fragments (16 consecutive
+// rows at one chunk per 16 lanes, 16-byte reads), transpose reads (4
+// consecutive rows times two adjacent chunks per 16 lanes, 8-byte reads) and
+// fp32 rows read as bf16 fragments (two adjacent 16-byte chunks per lane).
+// The maps below run all three at the rate of conflict-free contiguous reads.
 template <int RB>
 __device__ inline int tile_swz(int row) {
   static_assert(RB == 64 || RB == 128 || RB == 256, "row size");
-  return RB == 64 ? ((row >> 2) & 3) : RB == 128 ? ((row >> 1) & 7) : (row & 15);
+  const int b0 = row & 1, b1 = (row >> 1) & 1, b2 = (row >> 2) & 1, b3 = (row >> 3) & 1;
+  if constexpr (RB == 64) return b3 | ((b0 ^ b3) << 1);
+  if constexpr (RB == 128) return (b0 ^ b1) | (b1 << 1) | (b3 << 2);
+  return b3 | ((b2 ^ b3) << 1) | (b1 << 2) | (b0 << 3);
 }
 template <int RB>
 __device__ inline int tile_off(int row, int byte) {
