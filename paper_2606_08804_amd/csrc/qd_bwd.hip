@@ -33,40 +33,59 @@
 namespace qd {
 
 // ------------------------------------------------------------------ scan
-// Backward-scan operands of one chunk, filled by direct global->LDS loads:
-// P, M (C x C), K, Q, W (C x Dk) and this tile's columns of dO (C x BV) as
-// swizzled row-major tiles, then b and beta (C fp32 each).  The transposed
-// operands (P^T, M^T, Q^T, W^T, dO^T) are LDS transpose reads of these tiles.
-// Two producer waves split the loads so that each wave's outstanding count
-// stays within the counter.
+// Backward-scan operands of one chunk, filled by direct global->LDS loads as
+// swizzled row-major tiles, in two sets by the phase that reads them:
+//   set A (dD = P^T dO + Kbar dS'^T):           P (C x C), K (C x Dk), this
+//                                              tile's columns of dO (C x BV), b;
+//   set B (dV and the entry-state gradient):   M (C x C), Q, W (C x Dk), dO, b, beta.
+// The transposed operands (P^T, M^T, Q^T, W^T, dO^T) are LDS transpose reads
+// of these tiles.  Each set has its own ring of NBUF chunks and its own
+// producer wave.
 template <typename E, int DK, int BV>
 struct ScanBwdRing {
   static constexpr int RK = DK * (int)sizeof(E), RC = C * (int)sizeof(E), RO = BV * (int)sizeof(E);
-  static constexpr int PP = 0, MM = PP + C * RC, K = MM + C * RC, Q = K + C * RK, W = Q + C * RK,
-                       DO = W + C * RK, B = DO + C * RO, BE = B + C * 4, BYTES = BE + C * 4;
+  static constexpr int AP = 0, AK = AP + C * RC, AO = AK + C * RK, AB = AO + C * RO, ABYTES = AB + C * 4;
+  static constexpr int BM = 0, BQ = BM + C * RC, BW = BQ + C * RK, BO = BW + C * RK, BB = BO + C * RO,
+                       BE = BB + C * 4, BBYTES = BE + C * 4;
   static constexpr int NBUF = sizeof(E) == 2 ? 2 : 1;
-  static constexpr int LOADS0 = (Q - PP) / 1024 + 2;   // producer 0: P, M, K, b, beta
-  static constexpr int LOADS1 = (B - Q) / 1024;        // producer 1: Q, W, dO
-  static_assert(NBUF == 1 || (LOADS0 <= 63 && LOADS1 <= 63), "outstanding-load counter range");
+  // direct loads per chunk of each of the two producers of a set (the 1 KB
+  // instructions of every tile split evenly; in set A producer 1 also loads
+  // b, in set B producer 0 loads beta and producer 1 b)
+  static constexpr int IA = (AB - AP) / 1024, IB = (BB - BM) / 1024;
+  static constexpr int LOADS_A0 = IA / 2, LOADS_A1 = IA / 2 + 1, LOADS_B0 = IB / 2 + 1, LOADS_B1 = IB / 2 + 1;
+  static_assert((C * RK / 1024) % 2 == 0 && (C * RC / 1024) % 2 == 0 && (C * RO / 1024) % 2 == 0, "even split");
+  static_assert(NBUF == 1 || (LOADS_A1 <= 63 && LOADS_B1 <= 63), "outstanding-load counter range");
 };
 
 template <typename E, int DK, int BV>
 struct alignas(16) ScanBwdSmem {
   static constexpr int P = Pad<E>::v;
   typedef ScanBwdRing<E, DK, BV> R;
-  E dS[BV][DK + P];   // dS' tile [v][k] (MFMA operand copy; the dS'^T output is read back from it)
-  E dDn[BV][C + P];   // -dD tile, transposed [v][r] (also the source of the dD output)
-  E dV[C][BV + P];    // dV tile staging [i][v]
-  alignas(16) char ring[R::NBUF][R::BYTES];
+  alignas(16) char ringA[R::NBUF][R::ABYTES];
+  alignas(16) char ringB[R::NBUF][R::BBYTES];
+  union {
+    E dS[BV][DK + P];   // dS' tile [v][k] (MFMA operand copy; the dS'^T output is read back from it)
+    E dV[C][BV + P];    // dV tile staging [i][v], after the dS' copy is dead
+  } u;
+  E dDn[BV][C + P];     // -dD tile, transposed [v][r] (also the source of the dD output)
 };
 
 // One workgroup per (sequence, head, Dv tile of BV = 32): four compute waves
-// and two producer waves; reverse pass over the chunks.  Compute wave w owns
+// and four producer waves (two per operand set; one wave alone issues direct
+// loads at only about 12 bytes per clock); reverse pass over the chunks.  Compute wave w owns
 // rows 16w.. of dD and dV and key rows 16 KPW w.. of the exit-state gradient
-// tile dS'^T (Dk x BV), held in fp32 MFMA accumulators.  The producers stream
-// each chunk's operands into a two-chunk LDS ring, one chunk ahead.
+// tile dS'^T (Dk x BV), held in fp32 MFMA accumulators.
+//
+// Per chunk the compute waves pass four barriers: B1 (start), B2 (dS' staged),
+// B3 (dD staged), B4 (dV staged).  Producers 0-1 stream set A, 2-3 set B,
+// each while the compute waves work on phases that do not read the buffer
+// being refilled (issuing stalls the issuing wave while the memory pipeline
+// is busy, so it must not delay a barrier): set A of the chunk two steps
+// ahead is issued after B3, set B of the next chunk in two parts between B1,
+// B2 and B3; set A is waited for before B2 and set B before B3.  With one
+// buffer per set (fp32) the refills follow the last reader's barrier.
 template <typename E, int DK, int DV, int BV>
-__global__ __launch_bounds__(NTHREADS + 128) void k_scan_bwd(Params p) {
+__global__ __launch_bounds__(NTHREADS + 256) void k_scan_bwd(Params p) {
   constexpr int P = Pad<E>::v;
   constexpr int LK = DK + P, LC = C + P;
   constexpr int NVT = DV / BV;
@@ -77,12 +96,15 @@ __global__ __launch_bounds__(NTHREADS + 128) void k_scan_bwd(Params p) {
   typedef typename Quad<E>::raw QR;
   typedef typename Mma<E>::frag FR;
   typedef ScanBwdRing<E, DK, BV> R;
+  constexpr bool DB = R::NBUF == 2;
   // fp32 operands take 4-deep k-steps; their long k loops are only partly unrolled
   constexpr int UKC = C / KS > 4 ? 4 : C / KS, UKD = DK / KS > 4 ? 4 : DK / KS;
   __shared__ ScanBwdSmem<E, DK, BV> sm;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-  const int prod = w - NWAVES;               // 0 or 1 for the producer waves, negative otherwise
+  const int prod = w - NWAVES;               // 0-3 for the producer waves, negative otherwise
   const bool producer = prod >= 0;
+  const bool prodA = prod == 0 || prod == 1, prodB = prod >= 2;
+  const int wp = prod & 1;                   // producer index within its set
   int unit, vt;
   if (!xcd_unit_tile(blockIdx.x, p.N * p.H, NVT, unit, vt)) return;
   const int H = p.H, n = unit / H, h = unit % H, v0 = vt * BV;
@@ -91,30 +113,51 @@ __global__ __launch_bounds__(NTHREADS + 128) void k_scan_bwd(Params p) {
   const int base = slot_base(p, n, s);
   const int nch = max(0, min((e - s + C - 1) / C, p.n_slots - base));
 
-  auto issue = [&](int c, int buf) {
-    char* r = sm.ring[buf];
-    const int t0 = s + c * C, len = min(C, e - t0);
-    const size_t gi = (size_t)(base + c) * H + h;
-    const size_t arow = (size_t)t0 * H + h;
-    // rows of K, Q past the chunk come from W, and rows of dO from D: both
-    // are zero there
-    const char* Wg = (const char*)((const E*)p.wW + gi * C * DK);
-    if (prod == 0) {
-      const char* Pg = (const char*)((const E*)p.wP + gi * C * C);
+  // rows of K, Q past the chunk come from W, and rows of dO from D: both are
+  // zero there
+  auto chunk_ptrs = [&](int c, size_t& gi, size_t& arow, int& len, const char*& Wg, const char*& Og,
+                        const char*& Dg) {
+    const int t0 = s + c * C;
+    len = min(C, e - t0);
+    gi = (size_t)(base + c) * H + h;
+    arow = (size_t)t0 * H + h;
+    Wg = (const char*)((const E*)p.wW + gi * C * DK);
+    Og = (const char*)((const E*)p.dO + arow * DV + v0);
+    Dg = (const char*)((const E*)p.savedD + gi * C * DV + v0);
+  };
+  // producers 0-1: their share of set A of chunk c into buffer buf
+  auto issueA = [&](int c, int buf) {
+    size_t gi, arow;
+    int len;
+    const char *Wg, *Og, *Dg;
+    chunk_ptrs(c, gi, arow, len, Wg, Og, Dg);
+    char* r = sm.ringA[buf];
+    const char* Pg = (const char*)((const E*)p.wP + gi * C * C);
+    const char* Kg = (const char*)((const E*)p.k + arow * DK);
+    dma_rows<R::RC, C, 2, true>(r + R::AP, Pg, R::RC, C, Pg, 0, wp, lane);
+    dma_rows<R::RK, C, 2, true>(r + R::AK, Kg, (size_t)H * R::RK, len, Wg, R::RK, wp, lane);
+    dma_rows<R::RO, C, 2, true>(r + R::AO, Og, (size_t)H * DV * sizeof(E), len, Dg, DV * sizeof(E), wp, lane);
+    if (wp == 1) dma4_asm(p.wb + gi * C + lane, r + R::AB);
+  };
+  // producers 2-3: their share of part `part` (0: M, dO, b, beta; 1: Q, W;
+  // 2: both) of set B of chunk c into buffer buf
+  auto issueB = [&](int c, int buf, int part) {
+    size_t gi, arow;
+    int len;
+    const char *Wg, *Og, *Dg;
+    chunk_ptrs(c, gi, arow, len, Wg, Og, Dg);
+    char* r = sm.ringB[buf];
+    if (part != 1) {
       const char* Mg = (const char*)((const E*)p.wM + gi * C * C);
-      const char* Kg = (const char*)((const E*)p.k + arow * DK);
-      dma_rows<R::RC, C, 1, true>(r + R::PP, Pg, R::RC, C, Pg, 0, 0, lane);
-      dma_rows<R::RC, C, 1, true>(r + R::MM, Mg, R::RC, C, Mg, 0, 0, lane);
-      dma_rows<R::RK, C, 1, true>(r + R::K, Kg, (size_t)H * R::RK, len, Wg, R::RK, 0, lane);
-      dma4_asm(p.wb + gi * C + lane, r + R::B);
-      dma4_asm(p.beta + arow + (size_t)min(lane, len - 1) * H, r + R::BE);
-    } else {
+      dma_rows<R::RC, C, 2, true>(r + R::BM, Mg, R::RC, C, Mg, 0, wp, lane);
+      dma_rows<R::RO, C, 2, true>(r + R::BO, Og, (size_t)H * DV * sizeof(E), len, Dg, DV * sizeof(E), wp, lane);
+      if (wp == 1) dma4_asm(p.wb + gi * C + lane, r + R::BB);
+      else dma4_asm(p.beta + arow + (size_t)min(lane, len - 1) * H, r + R::BE);
+    }
+    if (part != 0) {
       const char* Qg = (const char*)((const E*)p.q + arow * DK);
-      const char* Og = (const char*)((const E*)p.dO + arow * DV + v0);
-      const char* Dg = (const char*)((const E*)p.savedD + gi * C * DV + v0);
-      dma_rows<R::RK, C, 1, true>(r + R::Q, Qg, (size_t)H * R::RK, len, Wg, R::RK, 0, lane);
-      dma_rows<R::RK, C, 1, true>(r + R::W, Wg, R::RK, C, Wg, 0, 0, lane);
-      dma_rows<R::RO, C, 1, true>(r + R::DO, Og, (size_t)H * DV * sizeof(E), len, Dg, DV * sizeof(E), 0, lane);
+      dma_rows<R::RK, C, 2, true>(r + R::BQ, Qg, (size_t)H * R::RK, len, Wg, R::RK, wp, lane);
+      dma_rows<R::RK, C, 2, true>(r + R::BW, Wg, R::RK, C, Wg, 0, wp, lane);
     }
   };
 
@@ -130,38 +173,44 @@ __global__ __launch_bounds__(NTHREADS + 128) void k_scan_bwd(Params p) {
                        : zero4();
     }
 
-  if (producer && nch > 0) {
-    issue(nch - 1, 0);
-    if (R::NBUF == 2 && nch > 1) issue(nch - 2, 1);
+  if (nch > 0) {
+    if (prodA) {
+      issueA(nch - 1, 0);
+      if (DB && nch > 1) issueA(nch - 2, 1);
+    } else if (prodB) {
+      issueB(nch - 1, 0, 2);
+    }
   }
   for (int it = 0; it < nch; ++it) {
     const int c = nch - 1 - it;
     const size_t gi = (size_t)(base + c) * H + h;
     const int t0 = s + c * C, len = min(C, e - t0);
-    const int buf = R::NBUF == 2 ? (it & 1) : 0;
-    const char* rc = sm.ring[buf];
-    const float* bch = (const float*)(rc + R::B);
-    if (producer) {
-      const bool ahead = R::NBUF == 2 && it + 1 < nch;
-      if (prod == 0) {
-        if (ahead) wait_vm<R::NBUF == 2 ? R::LOADS0 : 0>();
-        else wait_vm<0>();
-      } else {
-        if (ahead) wait_vm<R::NBUF == 2 ? R::LOADS1 : 0>();
-        else wait_vm<0>();
-      }
-    }
-    block_sync_lds();                      // chunk c's operands visible; previous chunk done
+    const int buf = DB ? (it & 1) : 0;
+    const char* ra = sm.ringA[buf];
+    const char* rb = sm.ringB[buf];
+    block_sync_lds();                      // B1: previous chunk done
+    // ---- phase 1: stage dS' (compute); producer 0 waits for set A, producer 1
+    // issues the first part of the next chunk's set B
     if (!producer) {
 #pragma unroll
       for (int i = 0; i < KPW; ++i)
 #pragma unroll
         for (int nb = 0; nb < NB; ++nb) {
           const int kt = KPW * w + i;
-          *(QR*)&sm.dS[nb * 16 + fcol(lane)][kt * 16 + frow(lane, 0)] = Quad<E>::pack(acc[i][nb]);
+          *(QR*)&sm.u.dS[nb * 16 + fcol(lane)][kt * 16 + frow(lane, 0)] = Quad<E>::pack(acc[i][nb]);
         }
+    } else if (prodA) {
+      if (DB && it + 1 < nch) {
+        if (wp == 0) wait_vm<DB ? R::LOADS_A0 : 0>();
+        else wait_vm<DB ? R::LOADS_A1 : 0>();
+      } else {
+        wait_vm<0>();
+      }
+    } else {
+      if (DB && it + 1 < nch) issueB(c - 1, (it + 1) & 1, 0);
     }
-    block_sync_lds();
+    block_sync_lds();                      // B2: dS' staged; set A of this chunk visible
+    // ---- phase 2: dS' output, dD (compute); producer 1 finishes set B
     if (!producer) {
       {
         // dS' of this chunk for the intra-chunk kernel, transposed ([k][v]) in the
@@ -173,10 +222,11 @@ __global__ __launch_bounds__(NTHREADS + 128) void k_scan_bwd(Params p) {
           uint4 o;
           E* oe = (E*)&o;
 #pragma unroll
-          for (int j = 0; j < VEC; ++j) oe[j] = sm.dS[c0 + j][r];
+          for (int j = 0; j < VEC; ++j) oe[j] = sm.u.dS[c0 + j][r];
           *(uint4*)(dst + (size_t)r * DV + c0) = o;
         }
       }
+      const float* bch = (const float*)(ra + R::AB);
       const float bl = bch[C - 1];
       // dD = P^T dO + diag(g_C/g) K dS'^T   (rows 16w..)
 #pragma unroll
@@ -184,12 +234,12 @@ __global__ __launch_bounds__(NTHREADS + 128) void k_scan_bwd(Params p) {
         f4 d1 = zero4(), d2 = zero4();
 #pragma unroll UKC
         for (int ks = 0; ks < C / KS; ++ks)
-          d1 = Mma<E>::mma(tile_tr_frag<E, R::RC>(rc + R::PP, ks * KS, 16 * w, lane),
-                           tile_tr_frag<E, R::RO>(rc + R::DO, ks * KS, nb * 16, lane), d1);
+          d1 = Mma<E>::mma(tile_tr_frag<E, R::RC>(ra + R::AP, ks * KS, 16 * w, lane),
+                           tile_tr_frag<E, R::RO>(ra + R::AO, ks * KS, nb * 16, lane), d1);
 #pragma unroll UKD
         for (int ks = 0; ks < DK / KS; ++ks)
-          d2 = Mma<E>::mma(tile_frag<E, R::RK>(rc + R::K, 16 * w, ks * KS, lane),
-                           Frag<E>::load(kmaj(&sm.dS[0][0], LK), nb * 16, ks * KS, lane), d2);
+          d2 = Mma<E>::mma(tile_frag<E, R::RK>(ra + R::AK, 16 * w, ks * KS, lane),
+                           Frag<E>::load(kmaj(&sm.u.dS[0][0], LK), nb * 16, ks * KS, lane), d2);
         f4 dn;
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
@@ -198,8 +248,18 @@ __global__ __launch_bounds__(NTHREADS + 128) void k_scan_bwd(Params p) {
         }
         *(QR*)&sm.dDn[nb * 16 + fcol(lane)][16 * w + frow(lane, 0)] = Quad<E>::pack(dn);
       }
+    } else if (prodB) {
+      if (DB && it + 1 < nch) {
+        issueB(c - 1, (it + 1) & 1, 1);
+        // set B of this chunk landed; the next one's in flight
+        if (wp == 0) wait_vm<DB ? R::LOADS_B0 : 0>();
+        else wait_vm<DB ? R::LOADS_B1 : 0>();
+      } else {
+        wait_vm<0>();
+      }
     }
-    block_sync_lds();
+    block_sync_lds();                      // B3: dD staged; set B visible; set A of this chunk free
+    // ---- phase 3: dD output, dV, entry-state gradient (compute); producer 0 refills set A
     if (!producer) {
       {
         // dD rows for the intra-chunk kernel, read back from -dD^T
@@ -214,8 +274,10 @@ __global__ __launch_bounds__(NTHREADS + 128) void k_scan_bwd(Params p) {
           *(uint4*)(ddst + (size_t)r * DV + cc) = o;
         }
       }
+      const float* bch = (const float*)(rb + R::BB);
+      const float* bech = (const float*)(rb + R::BE);
       // dV = T^T dD = diag(beta) M^T dD  (rows 16w..), staged for coalesced stores
-      const float* bech = (const float*)(rc + R::BE);
+      // (the dS' copy it overwrites was last read before B3)
       float nbeta[4];
 #pragma unroll
       for (int j = 0; j < 4; ++j) nbeta[j] = -bech[16 * w + frow(lane, j)];
@@ -224,10 +286,10 @@ __global__ __launch_bounds__(NTHREADS + 128) void k_scan_bwd(Params p) {
         f4 dv = zero4();
 #pragma unroll UKC
         for (int ks = 0; ks < C / KS; ++ks)
-          dv = Mma<E>::mma(tile_tr_frag<E, R::RC>(rc + R::MM, ks * KS, 16 * w, lane),
+          dv = Mma<E>::mma(tile_tr_frag<E, R::RC>(rb + R::BM, ks * KS, 16 * w, lane),
                            Frag<E>::load(kmaj(&sm.dDn[0][0], LC), nb * 16, ks * KS, lane), dv);
 #pragma unroll
-        for (int j = 0; j < 4; ++j) sm.dV[16 * w + frow(lane, j)][nb * 16 + fcol(lane)] = fromf<E>(nbeta[j] * dv[j]);
+        for (int j = 0; j < 4; ++j) sm.u.dV[16 * w + frow(lane, j)][nb * 16 + fcol(lane)] = fromf<E>(nbeta[j] * dv[j]);
       }
       // dS_entry^T = g_C dS'^T + Q^T diag(g) dO - W^T dD   (the decay scales the
       // dO fragment along the contracted token index)
@@ -239,31 +301,33 @@ __global__ __launch_bounds__(NTHREADS + 128) void k_scan_bwd(Params p) {
 #pragma unroll UKC
         for (int ks = 0; ks < C / KS; ++ks) {
           const FR bd = Frag<E>::load(kmaj(&sm.dDn[0][0], LC), nb * 16, ks * KS, lane);
-          FR gdo = tile_tr_frag<E, R::RO>(rc + R::DO, ks * KS, nb * 16, lane);
+          FR gdo = tile_tr_frag<E, R::RO>(rb + R::BO, ks * KS, nb * 16, lane);
           E* ge = (E*)&gdo;
 #pragma unroll
           for (int e2 = 0; e2 < Mma<E>::KPL; ++e2)
             ge[e2] = fromf<E>(__expf(bch[ks * KS + (lane >> 4) * Mma<E>::KPL + e2]) * tof(ge[e2]));
 #pragma unroll
           for (int i = 0; i < KPW; ++i) {
-            acc[i][nb] = Mma<E>::mma(tile_tr_frag<E, R::RK>(rc + R::Q, ks * KS, 16 * (KPW * w + i), lane), gdo,
+            acc[i][nb] = Mma<E>::mma(tile_tr_frag<E, R::RK>(rb + R::BQ, ks * KS, 16 * (KPW * w + i), lane), gdo,
                                      acc[i][nb]);
-            acc[i][nb] = Mma<E>::mma(tile_tr_frag<E, R::RK>(rc + R::W, ks * KS, 16 * (KPW * w + i), lane), bd,
+            acc[i][nb] = Mma<E>::mma(tile_tr_frag<E, R::RK>(rb + R::BW, ks * KS, 16 * (KPW * w + i), lane), bd,
                                      acc[i][nb]);
           }
         }
       }
+    } else if (prodA) {
+      if (DB && it + 2 < nch) issueA(c - 2, buf);
+      if (!DB && it + 1 < nch) issueA(c - 1, 0);
     }
-    block_sync_lds();                      // chunk c's ring buffer, dDn and dV complete
-    if (producer) {
-      if (R::NBUF == 2 && it + 2 < nch) issue(c - 2, buf);
-      if (R::NBUF == 1 && it + 1 < nch) issue(c - 1, 0);
-    } else {
+    block_sync_lds();                      // B4: dV staged; set B of this chunk free
+    if (prodB) {
+      if (!DB && it + 1 < nch) issueB(c - 1, 0, 2);
+    } else if (!producer) {
       constexpr int VEC = 16 / sizeof(E), PR = BV / VEC;
       E* vdst = (E*)p.dv + ((size_t)t0 * H + h) * DV + v0;
       for (int idx = tid; idx < C * PR; idx += NTHREADS) {
         const int r = idx / PR, cc = (idx % PR) * VEC;
-        if (r < len) *(uint4*)(vdst + (size_t)r * H * DV + cc) = *(const uint4*)&sm.dV[r][cc];
+        if (r < len) *(uint4*)(vdst + (size_t)r * H * DV + cc) = *(const uint4*)&sm.u.dV[r][cc];
       }
     }
   }
@@ -785,7 +849,7 @@ static hipError_t launch_bwd_t(const Params& p, hipStream_t st) {
   const int nb = ((units + 7) / 8) * 8 * (DV / SBV);
   if (nb > 0) {
     prof_mark(ST_SCAN_BWD, 0, st);
-    hipLaunchKernelGGL((k_scan_bwd<E, DK, DV, SBV>), dim3(nb), dim3(NTHREADS + 128), 0, st, p);
+    hipLaunchKernelGGL((k_scan_bwd<E, DK, DV, SBV>), dim3(nb), dim3(NTHREADS + 256), 0, st, p);
     prof_mark(ST_SCAN_BWD, 1, st);
   }
   if (p.n_slots > 0) {

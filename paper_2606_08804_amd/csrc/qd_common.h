@@ -359,12 +359,13 @@ __device__ inline int tile_off(int row, int byte) {
 #pragma clang diagnostic push
 #pragma clang diagnostic ignored "-Winline-asm"
 __device__ inline void dma16_asm(const void* g, char* lds) {
-  // a generic pointer into LDS holds the LDS byte address in its low 32 bits
-  const uint32_t base = (uint32_t)(uintptr_t)lds;
+  // a generic pointer into LDS holds the LDS byte address in its low 32 bits;
+  // the address is uniform across the wave (callers pass per-wave bases)
+  const uint32_t base = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)lds);
   asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, off" ::"s"(base), "v"(g) : "memory", "m0");
 }
 __device__ inline void dma4_asm(const void* g, char* lds) {
-  const uint32_t base = (uint32_t)(uintptr_t)lds;
+  const uint32_t base = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)lds);
   asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dword %1, off" ::"s"(base), "v"(g) : "memory", "m0");
 }
 #pragma clang diagnostic pop

@@ -220,27 +220,34 @@ __global__ __launch_bounds__(PREP_THREADS) void k_prep(Params p) {
   }
 }
 
-// Forward-scan operands of one chunk, filled by direct global->LDS loads:
-// W, K, Q (C x Dk) and P (C x C) as swizzled row-major tiles, then
-// this workgroup's U fragments (byte copy of the C-fragment-ordered layout)
-// and b (C fp32).
+// Forward-scan operands of one chunk, filled by direct global->LDS loads as
+// swizzled row-major tiles, in two sets by the phase that reads them:
+//   set A (D = U - W S^T):            W (C x Dk), this tile's U fragments (byte
+//                                     copy of the C-fragment-ordered layout), b;
+//   set B (output and state update):  Q, K (C x Dk), P (C x C), b.
+// Each set has its own ring of NBUF chunks and its own producer wave.
 template <typename E, int DK, int BV>
 struct ScanFwdRing {
   static constexpr int RK = DK * (int)sizeof(E), RC = C * (int)sizeof(E);   // row bytes
   static constexpr int NB = BV / 16;
   static constexpr int UM = NB * 64 * 4 * (int)sizeof(E);   // U bytes per 16-row block
-  static constexpr int W = 0, K = W + C * RK, Q = K + C * RK, PP = Q + C * RK, U = PP + C * RC,
-                       B = U + 4 * UM, BYTES = B + C * 4;
+  static constexpr int AW = 0, AU = AW + C * RK, AB = AU + 4 * UM, ABYTES = AB + C * 4;
+  static constexpr int BQ = 0, BK = BQ + C * RK, BP = BK + C * RK, BB = BP + C * RC, BBYTES = BB + C * 4;
   static constexpr int NBUF = sizeof(E) == 2 ? 2 : 1;      // fp32 tiles are twice as large
-  static constexpr int LOADS = (B - W) / 1024 + 1;           // direct loads per chunk
-  static_assert(NBUF == 1 || LOADS <= 63, "outstanding-load counter range");
+  // direct loads per chunk of each of the two producers of a set (the 1 KB
+  // instructions of every tile split evenly; producer 1 also loads b)
+  static constexpr int IA = (AB - AW) / 1024, IB = (BB - BQ) / 1024;
+  static constexpr int LOADS_A0 = IA / 2, LOADS_A1 = IA / 2 + 1, LOADS_B0 = IB / 2, LOADS_B1 = IB / 2 + 1;
+  static_assert((C * RK / 1024) % 2 == 0 && (4 * UM / 1024) % 2 == 0 && (C * RC / 1024) % 2 == 0, "even split");
+  static_assert(NBUF == 1 || (LOADS_A1 <= 63 && LOADS_B1 <= 63), "outstanding-load counter range");
 };
 
 template <typename E, int DK, int BV>
 struct alignas(16) ScanFwdSmem {
   static constexpr int P = Pad<E>::v;
   typedef ScanFwdRing<E, DK, BV> R;
-  alignas(16) char ring[R::NBUF][R::BYTES];
+  alignas(16) char ringA[R::NBUF][R::ABYTES];
+  alignas(16) char ringB[R::NBUF][R::BBYTES];
   E Dt[BV][C + P];    // D^T
   E Dkt[BV][C + P];   // (diag(g_C / g) D)^T
   union {
@@ -253,15 +260,27 @@ struct alignas(16) ScanFwdSmem {
 };
 
 // One workgroup per (sequence, head, Dv tile of BV = 32 value rows): four
-// compute waves and one producer wave.  Compute wave w owns rows 16w.. of the
-// chunk's D and O tiles and key rows 16 KPW w.. of the state tile S^T
+// compute waves and four producer waves (two per operand set; one wave alone
+// issues direct loads at only about 12 bytes per clock).  Compute wave w owns rows 16w.. of
+// the chunk's D and O tiles and key rows 16 KPW w.. of the state tile S^T
 // (Dk x BV), which lives in fp32 MFMA accumulators across the whole sequence.
-// The producer wave streams each chunk's operands into a two-chunk LDS ring
-// with direct loads, one chunk ahead; it issues no other memory operations,
-// so its outstanding-load count is exact.  When p.o is null only the states
-// are produced.
+//
+// Per chunk the compute waves pass four barriers: B1 (start), B2 (S staged),
+// B3 (D staged), B4 (outputs staged).  Producers 0-1 stream set A, 2-3 set
+// B; each issues a chunk's loads while the compute waves work on phases
+// that no longer read the buffer being refilled, so that issuing (which
+// stalls the issuing wave while the memory pipeline is busy) overlaps compute
+// instead of delaying a barrier:
+//   set A of chunk c+2 is issued after B3 of chunk c (its last reader, phase
+//   2, is over) and waited for before B2 of chunk c+2;
+//   set B of chunk c+1 is issued in two parts between B1, B2 and B3 of chunk
+//   c (its buffer was released at B4 of chunk c-1) and waited for before B3
+//   of chunk c+1.
+// The producers issue no other memory operations, so their outstanding-load
+// counts are exact.  With one buffer per set (fp32) the refills follow the
+// last reader's barrier.  When p.o is null only the states are produced.
 template <typename E, int DK, int DV, int BV>
-__global__ __launch_bounds__(NTHREADS + 64) void k_scan_fwd(Params p) {
+__global__ __launch_bounds__(NTHREADS + 256) void k_scan_fwd(Params p) {
   constexpr int P = Pad<E>::v;
   constexpr int LK = DK + P, LC = C + P;
   constexpr int NVT = DV / BV;
@@ -272,9 +291,13 @@ __global__ __launch_bounds__(NTHREADS + 64) void k_scan_fwd(Params p) {
   typedef typename Quad<E>::raw QR;
   typedef typename Mma<E>::frag FR;
   typedef ScanFwdRing<E, DK, BV> R;
+  constexpr bool DB = R::NBUF == 2;
   __shared__ ScanFwdSmem<E, DK, BV> sm;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-  const bool producer = w == NWAVES;
+  const int prod = w - NWAVES;                // 0-3 for the producer waves, negative otherwise
+  const bool producer = prod >= 0;
+  const bool prodA = prod == 0 || prod == 1, prodB = prod >= 2;
+  const int wp = prod & 1;                    // producer index within its set
   int unit, vt;
   if (!xcd_unit_tile(blockIdx.x, p.N * p.H, NVT, unit, vt)) return;
   const int H = p.H, n = unit / H, h = unit % H, v0 = vt * BV;
@@ -284,26 +307,49 @@ __global__ __launch_bounds__(NTHREADS + 64) void k_scan_fwd(Params p) {
   const int nch = max(0, min((e - s + C - 1) / C, p.n_slots - base));
   const bool with_o = p.o != nullptr;
 
-  // producer: all operands of chunk c into ring buffer `buf`
-  auto issue = [&](int c, int buf) {
-    char* r = sm.ring[buf];
-    const int t0 = s + c * C, len = min(C, e - t0);
-    const size_t gi = (size_t)(base + c) * H + h;
-    const char* Wg = (const char*)((const E*)p.wW + gi * C * DK);
-    const char* Kg = (const char*)((const E*)p.k + ((size_t)t0 * H + h) * DK);
-    const char* Qg = (const char*)((const E*)p.q + ((size_t)t0 * H + h) * DK);
-    const char* Pg = (const char*)((const E*)p.wP + gi * C * C);
-    dma_rows<R::RK, C, 1, true>(r + R::W, Wg, R::RK, C, Wg, 0, 0, lane);
-    // rows of K and Q past the chunk come from W, whose rows there are zero
-    dma_rows<R::RK, C, 1, true>(r + R::K, Kg, (size_t)H * R::RK, len, Wg, R::RK, 0, lane);
-    dma_rows<R::RK, C, 1, true>(r + R::Q, Qg, (size_t)H * R::RK, len, Wg, R::RK, 0, lane);
-    dma_rows<R::RC, C, 1, true>(r + R::PP, Pg, R::RC, C, Pg, 0, 0, lane);
+  auto chunk_ptrs = [&](int c, size_t& gi, const char*& Wg, int& len, size_t& arow) {
+    const int t0 = s + c * C;
+    len = min(C, e - t0);
+    gi = (size_t)(base + c) * H + h;
+    arow = (size_t)t0 * H + h;
+    Wg = (const char*)((const E*)p.wW + gi * C * DK);
+  };
+  // producers 0-1: their share of set A of chunk c into buffer buf
+  auto issueA = [&](int c, int buf) {
+    size_t gi, arow;
+    const char* Wg;
+    int len;
+    chunk_ptrs(c, gi, Wg, len, arow);
+    char* r = sm.ringA[buf];
+    dma_rows<R::RK, C, 2, true>(r + R::AW, Wg, R::RK, C, Wg, 0, wp, lane);
 #pragma unroll
     for (int mt = 0; mt < 4; ++mt)
-      dma_block_asm<R::UM>(r + R::U + mt * R::UM,
-                           (const char*)((const E*)p.wU + gi * C * DV + (size_t)(mt * (DV / 16) + vt * NB) * 256),
-                           lane);
-    dma4_asm(p.wb + gi * C + lane, r + R::B);
+      if ((mt & 1) == wp)
+        dma_block_asm<R::UM>(r + R::AU + mt * R::UM,
+                             (const char*)((const E*)p.wU + gi * C * DV + (size_t)(mt * (DV / 16) + vt * NB) * 256),
+                             lane);
+    if (wp == 1) dma4_asm(p.wb + gi * C + lane, r + R::AB);
+  };
+  // producers 2-3: their share of part `part` (0: Q, P; 1: K, b; 2: both)
+  // of set B of chunk c into buffer buf; rows of Q and K past the chunk come
+  // from W, whose rows there are zero
+  auto issueB = [&](int c, int buf, int part) {
+    size_t gi, arow;
+    const char* Wg;
+    int len;
+    chunk_ptrs(c, gi, Wg, len, arow);
+    char* r = sm.ringB[buf];
+    if (part != 1) {
+      const char* Qg = (const char*)((const E*)p.q + arow * DK);
+      const char* Pg = (const char*)((const E*)p.wP + gi * C * C);
+      dma_rows<R::RK, C, 2, true>(r + R::BQ, Qg, (size_t)H * R::RK, len, Wg, R::RK, wp, lane);
+      dma_rows<R::RC, C, 2, true>(r + R::BP, Pg, R::RC, C, Pg, 0, wp, lane);
+    }
+    if (part != 0) {
+      const char* Kg = (const char*)((const E*)p.k + arow * DK);
+      dma_rows<R::RK, C, 2, true>(r + R::BK, Kg, (size_t)H * R::RK, len, Wg, R::RK, wp, lane);
+      if (wp == 1) dma4_asm(p.wb + gi * C + lane, r + R::BB);
+    }
   };
 
   // state: acc[i][nb] = S^T rows 16*(KPW*w+i).., columns 16*nb.. of this tile
@@ -319,21 +365,23 @@ __global__ __launch_bounds__(NTHREADS + 64) void k_scan_fwd(Params p) {
                        : zero4();
     }
 
-  if (producer && nch > 0) {
-    issue(0, 0);
-    if (R::NBUF == 2 && nch > 1) issue(1, 1);
+  if (nch > 0) {
+    if (prodA) {
+      issueA(0, 0);
+      if (DB && nch > 1) issueA(1, 1);
+    } else if (prodB) {
+      issueB(0, 0, 2);
+    }
   }
   for (int c = 0; c < nch; ++c) {
     const int t0 = s + c * C, len = min(C, e - t0);
     const size_t gi = (size_t)(base + c) * H + h;
-    const char* rc = sm.ring[R::NBUF == 2 ? (c & 1) : 0];
+    const int buf = DB ? (c & 1) : 0;
+    const char* ra = sm.ringA[buf];
+    const char* rb = sm.ringB[buf];
     FR sf[NB][DK / KS];                    // S fragments (B operand of D and O)
-    const float* bch = (const float*)(rc + R::B);
-    if (producer) {
-      if (R::NBUF == 2 && c + 1 < nch) wait_vm<R::NBUF == 2 ? R::LOADS : 0>();
-      else wait_vm<0>();
-    }
-    block_sync_lds();                      // chunk c's operands visible; chunk c-1 done
+    block_sync_lds();                      // B1: chunk c-1 done
+    // ---- phase 1: stage S (compute); producer 1 issues the first part of set B of chunk c+1
     if (!producer) {
 #pragma unroll
       for (int i = 0; i < KPW; ++i)
@@ -346,8 +394,19 @@ __global__ __launch_bounds__(NTHREADS + 64) void k_scan_fwd(Params p) {
             for (int j = 0; j < 4; ++j) sm.u.s.Sf[kt * 16 + frow(lane, j)][nb * 16 + fcol(lane)] = acc[i][nb][j];
           }
         }
+    } else if (prodB) {
+      if (DB && c + 1 < nch) issueB(c + 1, (c + 1) & 1, 0);
+    } else {
+      // set A of chunk c must have landed (set A of chunk c+1 may be in flight)
+      if (DB && c + 1 < nch) {
+        if (wp == 0) wait_vm<DB ? R::LOADS_A0 : 0>();
+        else wait_vm<DB ? R::LOADS_A1 : 0>();
+      } else {
+        wait_vm<0>();
+      }
     }
-    block_sync_lds();
+    block_sync_lds();                      // B2: S staged; set A of chunk c visible
+    // ---- phase 2: saved S, D = U - W S^T (compute); producer 1 finishes set B
     if (!producer) {
       if (p.saved) {
         // saved entry state, transposed (element (k, v) at [k][v]), 16-byte stores
@@ -357,8 +416,8 @@ __global__ __launch_bounds__(NTHREADS + 64) void k_scan_fwd(Params p) {
           *(f4*)(dst + (size_t)r * DV + c4) = *(const f4*)&sm.u.s.Sf[r][c4];
         }
       }
+      const float* bch = (const float*)(ra + R::AB);
       const float bl = bch[C - 1];
-      // S fragments (B operand, shared by D and O)
 #pragma unroll
       for (int nb = 0; nb < NB; ++nb)
 #pragma unroll
@@ -370,8 +429,8 @@ __global__ __launch_bounds__(NTHREADS + 64) void k_scan_fwd(Params p) {
         f4 d = zero4();
 #pragma unroll
         for (int ks = 0; ks < DK / KS; ++ks)
-          d = Mma<E>::mma(tile_frag<E, R::RK>(rc + R::W, 16 * w, ks * KS, lane), sf[nb][ks], d);
-        const QR uq = *(const QR*)(rc + R::U + ((w * NB + nb) * 64 + lane) * 4 * sizeof(E));
+          d = Mma<E>::mma(tile_frag<E, R::RK>(ra + R::AW, 16 * w, ks * KS, lane), sf[nb][ks], d);
+        const QR uq = *(const QR*)(ra + R::AU + ((w * NB + nb) * 64 + lane) * 4 * sizeof(E));
         f4 dk;
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
@@ -381,8 +440,18 @@ __global__ __launch_bounds__(NTHREADS + 64) void k_scan_fwd(Params p) {
         *(QR*)&sm.Dt[nb * 16 + fcol(lane)][16 * w + frow(lane, 0)] = Quad<E>::pack(d);
         *(QR*)&sm.Dkt[nb * 16 + fcol(lane)][16 * w + frow(lane, 0)] = Quad<E>::pack(dk);
       }
+    } else if (prodB) {
+      if (DB && c + 1 < nch) {
+        issueB(c + 1, (c + 1) & 1, 1);
+        // set B of chunk c landed; chunk c+1's in flight
+        if (wp == 0) wait_vm<DB ? R::LOADS_B0 : 0>();
+        else wait_vm<DB ? R::LOADS_B1 : 0>();
+      } else {
+        wait_vm<0>();
+      }
     }
-    block_sync_lds();
+    block_sync_lds();                      // B3: D staged; set B of chunk c visible; set A of chunk c free
+    // ---- phase 3: saved D, O, state update (compute); producer 0 refills set A
     if (!producer) {
       if (p.saved) {
         // D rows of this tile into the saved context (rows past the chunk are zero),
@@ -398,7 +467,8 @@ __global__ __launch_bounds__(NTHREADS + 64) void k_scan_fwd(Params p) {
           *(uint4*)(dbase + (size_t)r * DV + cc) = o;
         }
       }
-      const float bl = bch[C - 1];
+      const float* bch = (const float*)(rb + R::BB);
+      const float gC = __expf(bch[C - 1]);
       if (with_o) {
         // O = diag(g) Q S^T + P D   (rows 16w..)
         f4 oo[NB];
@@ -407,56 +477,42 @@ __global__ __launch_bounds__(NTHREADS + 64) void k_scan_fwd(Params p) {
           f4 o1 = zero4(), o2 = zero4();
 #pragma unroll
           for (int ks = 0; ks < DK / KS; ++ks)
-            o1 = Mma<E>::mma(tile_frag<E, R::RK>(rc + R::Q, 16 * w, ks * KS, lane), sf[nb][ks], o1);
+            o1 = Mma<E>::mma(tile_frag<E, R::RK>(rb + R::BQ, 16 * w, ks * KS, lane), sf[nb][ks], o1);
 #pragma unroll
           for (int ks = 0; ks < C / KS; ++ks)
-            o2 = Mma<E>::mma(tile_frag<E, R::RC>(rc + R::PP, 16 * w, ks * KS, lane),
+            o2 = Mma<E>::mma(tile_frag<E, R::RC>(rb + R::BP, 16 * w, ks * KS, lane),
                              Frag<E>::load(kmaj(&sm.Dt[0][0], LC), nb * 16, ks * KS, lane), o2);
 #pragma unroll
           for (int j = 0; j < 4; ++j) oo[nb][j] = __expf(bch[16 * w + frow(lane, j)]) * o1[j] + o2[j];
         }
-        // S^T <- g_C S^T + K^T diag(g_C/g) D  (K^T fragments are transpose reads of the K tile)
-        const float gC = __expf(bl);
-#pragma unroll
-        for (int nb = 0; nb < NB; ++nb) {
-#pragma unroll
-          for (int i = 0; i < KPW; ++i) acc[i][nb] = gC * acc[i][nb];
-#pragma unroll
-          for (int ks = 0; ks < C / KS; ++ks) {
-            const FR bf = Frag<E>::load(kmaj(&sm.Dkt[0][0], LC), nb * 16, ks * KS, lane);
-#pragma unroll
-            for (int i = 0; i < KPW; ++i)
-              acc[i][nb] = Mma<E>::mma(tile_tr_frag<E, R::RK>(rc + R::K, ks * KS, 16 * (KPW * w + i), lane), bf,
-                                       acc[i][nb]);
-          }
-        }
-        // the state copies aliased by O were last read before the previous barrier
+        // the state copies aliased by O were last read before B3
 #pragma unroll
         for (int nb = 0; nb < NB; ++nb)
 #pragma unroll
           for (int j = 0; j < 4; ++j) sm.u.O[16 * w + frow(lane, j)][nb * 16 + fcol(lane)] = fromf<E>(oo[nb][j]);
-      } else {
-        const float gC = __expf(bl);
+      }
+      // S^T <- g_C S^T + K^T diag(g_C/g) D  (K^T fragments are transpose reads of the K tile)
 #pragma unroll
-        for (int nb = 0; nb < NB; ++nb) {
+      for (int nb = 0; nb < NB; ++nb) {
 #pragma unroll
-          for (int i = 0; i < KPW; ++i) acc[i][nb] = gC * acc[i][nb];
+        for (int i = 0; i < KPW; ++i) acc[i][nb] = gC * acc[i][nb];
 #pragma unroll
-          for (int ks = 0; ks < C / KS; ++ks) {
-            const FR bf = Frag<E>::load(kmaj(&sm.Dkt[0][0], LC), nb * 16, ks * KS, lane);
+        for (int ks = 0; ks < C / KS; ++ks) {
+          const FR bf = Frag<E>::load(kmaj(&sm.Dkt[0][0], LC), nb * 16, ks * KS, lane);
 #pragma unroll
-            for (int i = 0; i < KPW; ++i)
-              acc[i][nb] = Mma<E>::mma(tile_tr_frag<E, R::RK>(rc + R::K, ks * KS, 16 * (KPW * w + i), lane), bf,
-                                       acc[i][nb]);
-          }
+          for (int i = 0; i < KPW; ++i)
+            acc[i][nb] = Mma<E>::mma(tile_tr_frag<E, R::RK>(rb + R::BK, ks * KS, 16 * (KPW * w + i), lane), bf,
+                                     acc[i][nb]);
         }
       }
+    } else if (prodA) {
+      if (DB && c + 2 < nch) issueA(c + 2, c & 1);
+      if (!DB && c + 1 < nch) issueA(c + 1, 0);
     }
-    block_sync_lds();                      // chunk c's ring buffer and O tile complete
-    if (producer) {
-      if (R::NBUF == 2 && c + 2 < nch) issue(c + 2, c & 1);
-      if (R::NBUF == 1 && c + 1 < nch) issue(c + 1, 0);
-    } else if (with_o) {
+    block_sync_lds();                      // B4: O staged; set B of chunk c free
+    if (prodB) {
+      if (!DB && c + 1 < nch) issueB(c + 1, 0, 2);
+    } else if (!producer && with_o) {
       constexpr int VEC = 16 / sizeof(E), PR = BV / VEC;
       E* obase = (E*)p.o + ((size_t)t0 * H + h) * DV + v0;
       for (int idx = tid; idx < C * PR; idx += NTHREADS) {
@@ -494,7 +550,7 @@ static hipError_t launch_fwd_t(const Params& p, int in_bwd, int with_scan, hipSt
     const int nb = ((units + 7) / 8) * 8 * (DV / BV);
     if (nb > 0) {
       prof_mark(ST_SCAN_FWD, 0, st);
-      hipLaunchKernelGGL((k_scan_fwd<E, DK, DV, BV>), dim3(nb), dim3(NTHREADS + 64), 0, st, p);
+      hipLaunchKernelGGL((k_scan_fwd<E, DK, DV, BV>), dim3(nb), dim3(NTHREADS + 256), 0, st, p);
       prof_mark(ST_SCAN_FWD, 1, st);
     }
   }
