@@ -53,8 +53,9 @@
  *  A caller-owned device buffer of qdelta_saved_bytes() bytes (16-byte
  *  aligned) with six regions, one after the other, each indexed by unit
  *  u = slot * H + h (U = n_slots * H units):
- *    states  float32 [U, Dk, Dv]: the transposed entry state S^T of the chunk
- *            (element (k, v) = S[v][k]);
+ *    states  dtype [U, Dk, Dv]: the transposed entry state S^T of the chunk
+ *            (element (k, v) = S[v][k]), rounded to the activation dtype (the
+ *            backward's products take it as an MFMA operand of that type);
  *    D       dtype [U, C, Dv]: the chunk's "new values" D = U - W S^T
  *            (App. D, WY form), rows >= the chunk's length zero;
  *    b       float32 [U, C]: chunk-local prefix sums of log alpha;

@@ -21,16 +21,16 @@ struct Layout {
   size_t total = 0;
 };
 
-// Saved context, per unit (slot, head), region after region: S^T fp32
-// [Dk][Dv], D [C][Dv], b fp32 [C], W [C][Dk], P [C][C], M [C][C] (D, W, P
-// and M in the activation dtype).
+// Saved context, per unit (slot, head), region after region: S^T [Dk][Dv],
+// D [C][Dv], b fp32 [C], W [C][Dk], P [C][C], M [C][C] (all but b in the
+// activation dtype).
 struct Ctx {
   size_t states, D, b, W, P, M, total;
 };
 Ctx ctx_layout(size_t units, int Dk, int Dv, int esz) {
   Ctx c;
   c.states = 0;
-  c.D = c.states + units * (size_t)Dk * Dv * 4;
+  c.D = c.states + units * (size_t)Dk * Dv * esz;
   c.b = c.D + units * (size_t)C * Dv * esz;
   c.W = c.b + units * (size_t)C * 4;
   c.P = c.W + units * (size_t)C * Dk * esz;
@@ -64,7 +64,7 @@ Layout make_layout(size_t units, int Dk, int Dv, int esz, bool bwd) {
 // Points the context fields of p (states, D, b, W, P, M) into a context buffer.
 void bind_ctx(qd::Params& p, char* base, size_t units, int Dk, int Dv, int esz) {
   const Ctx c = ctx_layout(units, Dk, Dv, esz);
-  p.saved = reinterpret_cast<float*>(base + c.states);
+  p.saved = base + c.states;
   p.savedD = base + c.D;
   p.wb = reinterpret_cast<float*>(base + c.b);
   p.wW = base + c.W;

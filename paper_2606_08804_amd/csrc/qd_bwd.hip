@@ -355,14 +355,13 @@ __global__ __launch_bounds__(NTHREADS + 256) void k_scan_bwd(Params p) {
 // forms dG, dQK and the beta and decay terms in MFMA-layout registers; B3
 // produces dX, dq and dk.  The tail turns the decay terms into d log alpha.
 
-// Phase-A tile of 32 value columns: S^T (fp32), dS'^T, D, V, dO, dD, each in
-// the swizzled direct-load layout; a ring of NBUF tiles keeps two in flight.
+// Phase-A tile of 32 value columns: S^T, dS'^T, D, V, dO, dD, each in the
+// swizzled direct-load layout; a ring of NBUF tiles keeps two in flight.
 template <typename E, int DK>
 struct TileA {
   static constexpr int BV = 32;
-  static constexpr int RS = BV * 4;                 // S^T row bytes
-  static constexpr int RE = BV * (int)sizeof(E);    // row bytes of the dtype tiles
-  static constexpr int S = 0, DS = S + DK * RS, D = DS + DK * RE, V = D + C * RE, DO = V + C * RE,
+  static constexpr int RE = BV * (int)sizeof(E);    // row bytes
+  static constexpr int S = 0, DS = S + DK * RE, D = DS + DK * RE, V = D + C * RE, DO = V + C * RE,
                        DD = DO + C * RE, BYTES = DD + C * RE;
   static constexpr int NBUF = sizeof(E) == 2 ? 3 : 2;   // fp32 tiles are twice as large
   static constexpr int LOADS = BYTES / 1024 / NWAVES;   // direct loads per wave and tile
@@ -491,7 +490,7 @@ __global__ __launch_bounds__(INTRA_THREADS) void k_bwd_intra(Params p) {
   for (int i = 0; i < 2; ++i) aP[i] = aT[i] = zero4();
   float sdot = 0.f;
   constexpr size_t ES = sizeof(E);
-  const char* Sg = (const char*)(p.saved + gi * DK * DV);
+  const char* Sg = (const char*)((const E*)p.saved + gi * DK * DV);
   const char* dSg = (const char*)((const E*)p.w_dSo + gi * DK * DV);
   const char* Dg = (const char*)((const E*)p.savedD + gi * C * DV);
   const char* dDg = (const char*)((const E*)p.w_dDb + gi * C * DV);
@@ -514,7 +513,7 @@ __global__ __launch_bounds__(INTRA_THREADS) void k_bwd_intra(Params p) {
   auto issue = [&](int vt) {
     char* t = &sm.x.tiles[vt % TA::NBUF][0];
     const size_t vb = (size_t)vt * BV;
-    dma_rows<TA::RS, DK>(t + TA::S, Sg + vb * 4, DV * 4, DK, Sg, 0, w, lane);
+    dma_rows<TA::RE, DK>(t + TA::S, Sg + vb * ES, DV * ES, DK, Sg, 0, w, lane);
     dma_rows<TA::RE, DK>(t + TA::DS, dSg + vb * ES, DV * ES, DK, dSg, 0, w, lane);
     dma_rows<TA::RE, C>(t + TA::D, Dg + vb * ES, DV * ES, C, Dg, 0, w, lane);
     dma_rows<TA::RE, C>(t + TA::DD, dDg + vb * ES, DV * ES, C, dDg, 0, w, lane);
@@ -545,15 +544,15 @@ __global__ __launch_bounds__(INTRA_THREADS) void k_bwd_intra(Params p) {
 #pragma unroll
       for (int i = 0; i < HK; ++i) {
         const int kb = kb0 + i;
-        float sv[Mma<E>::KPL];
-        const FR bS = tile_frag_f32<E>(t + TA::S, kb * 16, ks * KS, lane, sv);
+        const FR bS = tile_frag<E, TA::RE>(t + TA::S, kb * 16, ks * KS, lane);
         const FR bdS = tile_frag<E, TA::RE>(t + TA::DS, kb * 16, ks * KS, lane);
         aQ[i] = Mma<E>::mma(aO, bS, aQ[i]);
         aW[i] = Mma<E>::mma(adD, bS, aW[i]);
         aK[i] = Mma<E>::mma(aD, bdS, aK[i]);
+        const E* se = (const E*)&bS;
         const E* de = (const E*)&bdS;
 #pragma unroll
-        for (int e = 0; e < Mma<E>::KPL; ++e) sdot += sv[e] * tof(de[e]);
+        for (int e = 0; e < Mma<E>::KPL; ++e) sdot += tof(se[e]) * tof(de[e]);
       }
 #pragma unroll
       for (int i = 0; i < 2; ++i) {

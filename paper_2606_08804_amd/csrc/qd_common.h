@@ -520,7 +520,7 @@ struct Params {
   // forward outputs
   void* o;
   float* Sfin;
-  float* saved;          // saved context: entry states S^T [slot][H][Dk][Dv] (fp32)
+  void* saved;           // saved context: entry states S^T [slot][H][Dk][Dv] (dtype)
   void* savedD;          // saved context: D [slot][H][C][Dv] (dtype)
   // chunk factors from the preparation, per slot and head (in the saved
   // context when one is kept, else in the workspace)

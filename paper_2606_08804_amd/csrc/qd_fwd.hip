@@ -253,7 +253,7 @@ struct alignas(16) ScanFwdSmem {
   union {
     struct {
       E S[BV][DK + P];        // state tile (MFMA operand copy)
-      float Sf[DK][BV + 4];   // fp32 entry-state tile staging for the saved context
+      E Sf[DK][BV + P];       // entry-state tile staging for the saved context ([k][v])
     } s;
     E O[C][BV + P];           // output tile staging (after the state copies are dead)
   } u;
@@ -391,7 +391,8 @@ __global__ __launch_bounds__(NTHREADS + 256) void k_scan_fwd(Params p) {
           *(QR*)&sm.u.s.S[nb * 16 + fcol(lane)][kt * 16 + frow(lane, 0)] = Quad<E>::pack(acc[i][nb]);
           if (p.saved) {
 #pragma unroll
-            for (int j = 0; j < 4; ++j) sm.u.s.Sf[kt * 16 + frow(lane, j)][nb * 16 + fcol(lane)] = acc[i][nb][j];
+            for (int j = 0; j < 4; ++j)
+              sm.u.s.Sf[kt * 16 + frow(lane, j)][nb * 16 + fcol(lane)] = fromf<E>(acc[i][nb][j]);
           }
         }
     } else if (prodB) {
@@ -410,10 +411,11 @@ __global__ __launch_bounds__(NTHREADS + 256) void k_scan_fwd(Params p) {
     if (!producer) {
       if (p.saved) {
         // saved entry state, transposed (element (k, v) at [k][v]), 16-byte stores
-        float* dst = p.saved + gi * DK * DV + v0;
-        for (int idx = tid; idx < DK * (BV / 4); idx += NTHREADS) {
-          const int r = idx / (BV / 4), c4 = (idx % (BV / 4)) * 4;
-          *(f4*)(dst + (size_t)r * DV + c4) = *(const f4*)&sm.u.s.Sf[r][c4];
+        constexpr int VEC = 16 / sizeof(E), PR = BV / VEC;
+        E* dst = (E*)p.saved + gi * DK * DV + v0;
+        for (int idx = tid; idx < DK * PR; idx += NTHREADS) {
+          const int r = idx / PR, cc = (idx % PR) * VEC;
+          *(uint4*)(dst + (size_t)r * DV + cc) = *(const uint4*)&sm.u.s.Sf[r][cc];
         }
       }
       const float* bch = (const float*)(ra + R::AB);
