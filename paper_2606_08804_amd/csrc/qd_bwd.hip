@@ -392,6 +392,7 @@ struct alignas(16) BwdSmem {
             struct {
               E dG[C][C + P];     // dG (r, i), after M^T and dMinv^T are dead
               E dQK[C][C + P];    // dQK (r, i)
+              E dGl[C][C + P];    // dQK + diag(lambda) dG (r, i)
             } g;
           } v;
           E Y[C][C + P];          // M^T dT diag(beta) (r, i)
@@ -399,7 +400,7 @@ struct alignas(16) BwdSmem {
           float ecc[16][C];       // column partial sums of the decay-gradient terms
         } b2;
         struct {
-          E keep[2][C][C + P];    // dG, dQK (read by phase B3 as A operands)
+          E keep[3][C][C + P];    // dG, dQK, dQK + diag(lambda) dG (phase-B3 A operands)
           E oq[C][DK + P];        // dq staging, over the dead Y and column sums
           E ok[C][DK + P];        // dk staging
         } b3;
@@ -410,35 +411,6 @@ struct alignas(16) BwdSmem {
   // elements, outside the phase-A ring)
   alignas(16) char Mm[C * C * sizeof(E)];
 };
-
-// s * (k + l * q) element-wise on one fragment, rounded to the operand type
-template <typename FR>
-__device__ inline FR mix_frag(FR kf, FR qf, float l, float sc);
-template <>
-__device__ inline bf8 mix_frag<bf8>(bf8 kf, bf8 qf, float l, float sc) {
-  bf8 r;
-#pragma unroll
-  for (int e = 0; e < 8; ++e) r[e] = (__bf16)(sc * ((float)kf[e] + l * (float)qf[e]));
-  return r;
-}
-template <>
-__device__ inline float mix_frag<float>(float kf, float qf, float l, float sc) {
-  return sc * (kf + l * qf);
-}
-// k + l_e q per element e of a fragment whose elements run over tokens
-template <typename FR>
-__device__ inline FR mix_tokens(FR kf, FR qf, const float* lam);
-template <>
-__device__ inline bf8 mix_tokens<bf8>(bf8 kf, bf8 qf, const float* lam) {
-  bf8 r;
-#pragma unroll
-  for (int e = 0; e < 8; ++e) r[e] = (__bf16)((float)kf[e] + lam[e] * (float)qf[e]);
-  return r;
-}
-template <>
-__device__ inline float mix_tokens<float>(float kf, float qf, const float* lam) {
-  return kf + lam[0] * qf;
-}
 
 // Eight waves: wave w takes rows 16 rb.. (rb = w & 3) of every C-row operand
 // and one half (ch = w >> 2) of the Dk column blocks and of the C x C column
@@ -476,10 +448,6 @@ __global__ __launch_bounds__(INTRA_THREADS) void k_bwd_intra(Params p) {
   const size_t gi = (size_t)g * H + h;
   const size_t arow = (size_t)t0 * H + h;   // first activation row of the chunk
 
-  // gate loads first (branch-free: rows past the chunk re-read its last row)
-  const int ti = tid & (C - 1);
-  const size_t gtc = arow + (size_t)min(ti, len - 1) * H;
-  const float gb = p.wb[gi * C + ti], gbeta = p.beta[gtc], glam = p.lam[gtc];
 
   // ---------------- phase A: contractions over the value dimension
   typedef TileA<E, DK> TA;
@@ -496,19 +464,9 @@ __global__ __launch_bounds__(INTRA_THREADS) void k_bwd_intra(Params p) {
   const char* dDg = (const char*)((const E*)p.w_dDb + gi * C * DV);
   const char* dOg = (const char*)((const E*)p.dO + arow * DV);
   const char* Vg = (const char*)((const E*)p.v + arow * DV);
-  // phase-B operands first, so that they are older than every tile load
-  TileRegs<E, C, DK, IT> rKf, rQf;    // chunk K, Q rows for phase B1
-  rKf.load_clamped((const E*)p.k + arow * DK, (size_t)H * DK, len, tid);
-  rQf.load_clamped((const E*)p.q + arow * DK, (size_t)H * DK, len, tid);
-  asm volatile("" ::: "memory");
   // direct loads are issued by waves 0-3 only; the others' waits are no-ops
   const bool loader = w < NWAVES;
-  // M = (I + A)^{-1} from the preparation
   constexpr int RBC = C * (int)sizeof(E);
-  if (loader) {
-    const char* Mg = (const char*)((const E*)p.wM + gi * C * C);
-    dma_rows<RBC, C>(sm.Mm, Mg, RBC, C, Mg, 0, w, lane);
-  }
   // rows of V and dO past the chunk come from D, whose rows there are zero
   auto issue = [&](int vt) {
     char* t = &sm.x.tiles[vt % TA::NBUF][0];
@@ -520,17 +478,34 @@ __global__ __launch_bounds__(INTRA_THREADS) void k_bwd_intra(Params p) {
     dma_rows<TA::RE, C>(t + TA::V, Vg + vb * ES, (size_t)H * DV * ES, len, Dg + vb * ES, DV * ES, w, lane);
     dma_rows<TA::RE, C>(t + TA::DO, dOg + vb * ES, (size_t)H * DV * ES, len, Dg + vb * ES, DV * ES, w, lane);
   };
+  // the first tile goes out first; then the gates and the chunk's K, Q rows
+  // (registers, for phase B), M = (I + A)^{-1} and the next tiles
   constexpr int NB0 = NVT < TA::NBUF ? NVT : TA::NBUF;
+  if (loader) issue(0);
+  asm volatile("" ::: "memory");
+  const int ti = tid & (C - 1);
+  const size_t gtc = arow + (size_t)min(ti, len - 1) * H;   // rows past the chunk re-read its last row
+  const float gb = p.wb[gi * C + ti], gbeta = p.beta[gtc], glam = p.lam[gtc];
+  TileRegs<E, C, DK, IT> rKf, rQf;
+  rKf.load_clamped((const E*)p.k + arow * DK, (size_t)H * DK, len, tid);
+  rQf.load_clamped((const E*)p.q + arow * DK, (size_t)H * DK, len, tid);
+  asm volatile("" ::: "memory");
   if (loader) {
+    const char* Mg = (const char*)((const E*)p.wM + gi * C * C);
+    dma_rows<RBC, C>(sm.Mm, Mg, RBC, C, Mg, 0, w, lane);
 #pragma unroll
-    for (int vt = 0; vt < NB0; ++vt) issue(vt);
+    for (int vt = 1; vt < NB0; ++vt) issue(vt);
   }
+  // vector-memory operations of each wave issued after the first tile
+  constexpr int AFTER0 = 3 + 2 * TileRegs<E, C, DK, IT>::N + C * RBC / 1024 / NWAVES + (NB0 - 1) * TA::LOADS;
+  static_assert(AFTER0 <= 63, "outstanding-load counter range");
   constexpr int UVT = NVT > 4 ? 1 : NVT;   // full unroll only for short tile loops
 #pragma unroll UVT
   for (int vt = 0; vt < NVT; ++vt) {
     // tile vt is complete once at most `after` tiles' loads are outstanding
     const int after = (vt == 0 ? NB0 : min(NVT, vt + TA::NBUF - 1)) - 1 - vt;
-    if (after >= 2) wait_vm<2 * TA::LOADS>();
+    if (vt == 0) wait_vm<AFTER0>();
+    else if (after >= 2) wait_vm<2 * TA::LOADS>();
     else if (after == 1) wait_vm<TA::LOADS>();
     else wait_vm<0>();
     block_sync_lds();                 // tile vt visible; tile vt-1's buffer is free
@@ -549,10 +524,12 @@ __global__ __launch_bounds__(INTRA_THREADS) void k_bwd_intra(Params p) {
         aQ[i] = Mma<E>::mma(aO, bS, aQ[i]);
         aW[i] = Mma<E>::mma(adD, bS, aW[i]);
         aK[i] = Mma<E>::mma(aD, bdS, aK[i]);
-        const E* se = (const E*)&bS;
-        const E* de = (const E*)&bdS;
+        if (rb == 0) {
+          const E* se = (const E*)&bS;
+          const E* de = (const E*)&bdS;
 #pragma unroll
-        for (int e = 0; e < Mma<E>::KPL; ++e) sdot += tof(se[e]) * tof(de[e]);
+          for (int e = 0; e < Mma<E>::KPL; ++e) sdot += tof(se[e]) * tof(de[e]);
+        }
       }
 #pragma unroll
       for (int i = 0; i < 2; ++i) {
@@ -565,8 +542,10 @@ __global__ __launch_bounds__(INTRA_THREADS) void k_bwd_intra(Params p) {
     }
   }
   // the two row-block-0 waves together read all of S^T and dS'^T once
-  sdot = wave_sum(sdot);
-  if (rb == 0 && lane == 0) sm.sdot[ch] = sdot;
+  if (rb == 0) {
+    sdot = wave_sum(sdot);
+    if (lane == 0) sm.sdot[ch] = sdot;
+  }
   if (tid < C) {
     const bool ok = tid < len;
     sm.b[tid] = gb;
@@ -587,32 +566,39 @@ __global__ __launch_bounds__(INTRA_THREADS) void k_bwd_intra(Params p) {
       sm.x.s.b1.dW[16 * rb + frow(lane, j)][(kb0 + i) * 16 + fcol(lane)] = fromf<E>(-aW[i][j]);
   if (tid < C) sm.kb[tid] = __expf(sm.b[C - 1] - sm.b[tid]);
   block_sync_lds();
+  // G = X K^T = K K^T + diag(lambda) Q K^T and dT2 = dW (diag(g) X)^T =
+  // (dW K^T + dW Q^T diag(lambda)) diag(g): four products of the stored
+  // operands, the gates applied to the fp32 results
   f4 aG[2], aQK[2], adT[2];
-#pragma unroll
-  for (int i = 0; i < 2; ++i) aG[i] = aQK[i] = adT[i] = zero4();
   {
-    const float lam_a = sm.lam[16 * rb + (lane & 15)];
-    float lam_b[2], g_b[2];
+    f4 aKK[2], aDK[2], aDQ[2];
 #pragma unroll
-    for (int i = 0; i < 2; ++i) {
-      lam_b[i] = sm.lam[(ib0 + i) * 16 + (lane & 15)];
-      g_b[i] = sm.g[(ib0 + i) * 16 + (lane & 15)];
-    }
+    for (int i = 0; i < 2; ++i) aKK[i] = aQK[i] = aDK[i] = aDQ[i] = zero4();
 #pragma unroll
     for (int ks = 0; ks < DK / KS; ++ks) {
       const FR kA = Frag<E>::load(kmaj(&sm.x.s.b1.K[0][0], LKD), 16 * rb, ks * KS, lane);
       const FR qA = Frag<E>::load(kmaj(&sm.x.s.b1.Q[0][0], LKD), 16 * rb, ks * KS, lane);
-      const FR xA = mix_frag<FR>(kA, qA, lam_a, 1.f);
       const FR dwA = Frag<E>::load(kmaj(&sm.x.s.b1.dW[0][0], LKD), 16 * rb, ks * KS, lane);
 #pragma unroll
       for (int i = 0; i < 2; ++i) {
         const int ib = ib0 + i;
         const FR kB = Frag<E>::load(kmaj(&sm.x.s.b1.K[0][0], LKD), ib * 16, ks * KS, lane);
         const FR qB = Frag<E>::load(kmaj(&sm.x.s.b1.Q[0][0], LKD), ib * 16, ks * KS, lane);
-        const FR gxB = mix_frag<FR>(kB, qB, lam_b[i], g_b[i]);
-        aG[i] = Mma<E>::mma(xA, kB, aG[i]);
+        aKK[i] = Mma<E>::mma(kA, kB, aKK[i]);
         aQK[i] = Mma<E>::mma(qA, kB, aQK[i]);
-        adT[i] = Mma<E>::mma(dwA, gxB, adT[i]);
+        aDK[i] = Mma<E>::mma(dwA, kB, aDK[i]);
+        aDQ[i] = Mma<E>::mma(dwA, qB, aDQ[i]);
+      }
+    }
+    const int r0 = 16 * rb + frow(lane, 0);
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      const int c = (ib0 + i) * 16 + fcol(lane);
+      const float gc = sm.g[c], lc = sm.lam[c];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        aG[i][j] = aKK[i][j] + sm.lam[r0 + j] * aQK[i][j];
+        adT[i][j] = gc * (aDK[i][j] + lc * aDQ[i][j]);
       }
     }
   }
@@ -669,11 +655,12 @@ __global__ __launch_bounds__(INTRA_THREADS) void k_bwd_intra(Params p) {
     // dG = diag(beta) dA (.) Gamma, dQK = dP (.) Gamma (causal, inclusive),
     // the decay-gradient terms t = (dG (.) G + dQK (.) QK) and the rows of
     // dbeta from A = strictLower(diag(beta) Gamma (.) G)
-    float br[4], betar[4], dbr[4] = {0.f, 0.f, 0.f, 0.f}, er[4] = {0.f, 0.f, 0.f, 0.f};
+    float br[4], betar[4], lamr[4], dbr[4] = {0.f, 0.f, 0.f, 0.f}, er[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       br[j] = sm.b[rw + j];
       betar[j] = sm.beta[rw + j];
+      lamr[j] = sm.lam[rw + j];
     }
 #pragma unroll
     for (int i = 0; i < 2; ++i) {
@@ -694,6 +681,7 @@ __global__ __launch_bounds__(INTRA_THREADS) void k_bwd_intra(Params p) {
         ec += t;
         sm.x.s.u.b2.v.g.dG[r][c] = fromf<E>(dg);
         sm.x.s.u.b2.v.g.dQK[r][c] = fromf<E>(dqk);
+        sm.x.s.u.b2.v.g.dGl[r][c] = fromf<E>(dqk + lamr[j] * dg);
       }
       sm.x.s.u.b2.ecc[4 * rb + (lane >> 4)][c] = ec;
     }
@@ -726,23 +714,21 @@ __global__ __launch_bounds__(INTRA_THREADS) void k_bwd_intra(Params p) {
 
   // ---------------- phase B3: dX, dq, dk (rows 16 rb.., Dk blocks of this half)
   // K^T, Q^T and dW^T fragments are transpose reads of the row-major K, Q, dW
-  // kept since phase B1; dQK^T, dG^T and M^T likewise of dQK, dG and M
-  // (T^T dW = diag(beta) M^T dW)
+  // kept since phase B1; dG^T, (dQK + diag(lambda) dG)^T and M^T likewise
+  // (T^T dW = diag(beta) M^T dW; dQK^T Q + dG^T X = dG^T K + (dQK + diag(lambda) dG)^T Q)
   {
     constexpr int NTK = C / KS;
-    FR tA[NTK], gA[NTK], qkA[NTK], qktA[NTK], gtA[NTK];
-    float lamk[NTK][Mma<E>::KPL];
+    FR tA[NTK], gA[NTK], qkA[NTK], gltA[NTK], gtA[NTK];
     const E* dGp = &sm.x.s.u.b2.v.g.dG[0][0];
     const E* dQKp = &sm.x.s.u.b2.v.g.dQK[0][0];
+    const E* dGlp = &sm.x.s.u.b2.v.g.dGl[0][0];
 #pragma unroll
     for (int ks = 0; ks < NTK; ++ks) {
       tA[ks] = tile_tr_frag<E, RBC>(sm.Mm, ks * KS, 16 * rb, lane);
       gA[ks] = Frag<E>::load(kmaj(dGp, LC), 16 * rb, ks * KS, lane);
       qkA[ks] = Frag<E>::load(kmaj(dQKp, LC), 16 * rb, ks * KS, lane);
-      qktA[ks] = tr_frag<E>(dQKp, LC, ks * KS, 16 * rb, lane);
+      gltA[ks] = tr_frag<E>(dGlp, LC, ks * KS, 16 * rb, lane);
       gtA[ks] = tr_frag<E>(dGp, LC, ks * KS, 16 * rb, lane);
-#pragma unroll
-      for (int e = 0; e < Mma<E>::KPL; ++e) lamk[ks][e] = sm.lam[ks * KS + (lane >> 4) * Mma<E>::KPL + e];
     }
     const int r0 = 16 * rb + frow(lane, 0);
     float rdb[4] = {0.f, 0.f, 0.f, 0.f}, rtk[4] = {0.f, 0.f, 0.f, 0.f}, rdl[4] = {0.f, 0.f, 0.f, 0.f};
@@ -766,12 +752,11 @@ __global__ __launch_bounds__(INTRA_THREADS) void k_bwd_intra(Params p) {
         const FR ktB = tr_frag<E>(Kp, LKD, ks * KS, kb * 16, lane);
         const FR qtB = tr_frag<E>(Qp, LKD, ks * KS, kb * 16, lane);
         const FR dwB = tr_frag<E>(dWp, LKD, ks * KS, kb * 16, lane);
-        const FR xtB = mix_tokens<FR>(ktB, qtB, lamk[ks]);
         dgx = Mma<E>::mma(tA[ks], dwB, dgx);      // M^T dW
         dxp = Mma<E>::mma(gA[ks], ktB, dxp);      // dG K
         dqp = Mma<E>::mma(qkA[ks], ktB, dqp);     // dQK K
-        dkp = Mma<E>::mma(qktA[ks], qtB, dkp);    // dQK^T Q
-        dkp = Mma<E>::mma(gtA[ks], xtB, dkp);     // dG^T X
+        dkp = Mma<E>::mma(gtA[ks], ktB, dkp);     // dG^T K
+        dkp = Mma<E>::mma(gltA[ks], qtB, dkp);    // (dQK + diag(lambda) dG)^T Q
       }
       const int kc = kb * 16 + fcol(lane);
       const f4 kv = tr_col4(Kp, LKD, r0, kb * 16, lane);
