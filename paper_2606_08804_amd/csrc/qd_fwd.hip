@@ -35,7 +35,7 @@ struct PrepSmem {
       E Q[C][DK + P];
       E X[C][DK + P];
     } a;
-    E Vt[DV][C + P];
+    E V[C][DV + P];
   } u;
   E GX[C][DK + P];        // diag(g) X (r, k)
   union {
@@ -52,7 +52,7 @@ constexpr int PREP_THREADS = 512;   // 8 waves: two per SIMD hide each other's l
 template <typename E, int DK, int DV>
 struct PrepPre {
   TileRegs<E, C, DK, PREP_THREADS> K, Q;
-  TileRegsT<E, C, DV, PREP_THREADS> V;
+  TileRegs<E, C, DV, PREP_THREADS> V;
   float la, beta, lam;
   int t0, len, g, h;
   bool valid;
@@ -192,15 +192,20 @@ __global__ __launch_bounds__(PREP_THREADS) void k_prep(Params p) {
         if (wM) *(uint4*)(wM + gi * C * C + r * C + i0) = mr;
       }
     }
-    // V^T (K, Q, X are dead: all reads of them finished before the solve's barriers)
-    x.V.storeT(&sm.u.Vt[0][0], LC, tid);
+    // V (K, Q, X are dead: all reads of them finished before the solve's barriers)
+    x.V.store(&sm.u.V[0][0], DV + P, tid);
     block_sync_lds();
 
-    // U = T V, stored C-fragment tiled: tile (mt, nt) at ((mt*(DV/16)+nt)*64 + lane)*4
+    // U = T V (the B operand is a transpose read of V), stored C-fragment
+    // tiled: tile (mt, nt) at ((mt*(DV/16)+nt)*64 + lane)*4
     E* wU = (E*)p.wU + gi * C * DV;
     for (int t = w; t < (C / 16) * (DV / 16); t += NW) {
       const int m0 = (t / (DV / 16)) * 16, n0 = (t % (DV / 16)) * 16;
-      const f4 uu = mma_k<E, C>(kmaj(&sm.Tm[0][0], LC), kmaj(&sm.u.Vt[0][0], LC), m0, n0, zero4(), lane);
+      f4 uu = zero4();
+#pragma unroll
+      for (int ks = 0; ks < C / KS; ++ks)
+        uu = Mma<E>::mma(Frag<E>::load(kmaj(&sm.Tm[0][0], LC), m0, ks * KS, lane),
+                         tr_frag<E>(&sm.u.V[0][0], DV + P, ks * KS, n0, lane), uu);
       *(typename Quad<E>::raw*)(wU + ((size_t)t * 64 + lane) * 4) = Quad<E>::pack(uu);
     }
     // W = T diag(g) X (the B operand is a transpose read of diag(g) X), staged
