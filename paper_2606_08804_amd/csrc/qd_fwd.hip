@@ -13,8 +13,8 @@
 //   O   = diag(g) Q S^T + (Gam * M * Q K^T) D     (M includes the diagonal)
 //   S'  = g_C S + D^T diag(g_C / g) K
 //
-// k_prep   (persistent over chunk-head units, fully parallel): b, X, the two
-//          Gram products, A, the UT solve, U and W; writes b, U, W, P and M.
+// k_prep   (persistent over chunk-head units, fully parallel): b, the Gram
+//          products, A, the UT solve, U and W; writes b, U, W, P and M.
 // k_scan_fwd (one workgroup per sequence, head and Dv tile): the sequential
 //          pass over chunks; the state tile stays in MFMA accumulators in fp32;
 //          D, the chunk output and the state update are computed on chip.
@@ -26,24 +26,26 @@
 namespace qd {
 
 template <typename E, int DK, int DV>
-struct PrepSmem {
+struct alignas(16) PrepSmem {
   static constexpr int P = Pad<E>::v;
-  float b[C], beta[C], lam[C];
+  alignas(16) float b[C], g[C], gl[C], beta[C], lam[C];   // gl = g lambda
   union {
     struct {
       E K[C][DK + P];
       E Q[C][DK + P];
-      E X[C][DK + P];
     } a;
-    E V[C][DV + P];
+    E V[C][DV + P];           // after W, the last reader of K and Q
   } u;
-  E GX[C][DK + P];        // diag(g) X (r, k)
+  E Ws[C][DK + P];            // W staging for 16-byte stores
   union {
-    float A[C][C + 4];    // strictly lower A, consumed by the solve
-    E Ws[C][DK + P];      // W staging for 16-byte stores, after the solve
+    float A[C][C + 4];        // strictly lower A, consumed by the solve
+    struct {
+      E Tg[C][C + P];         // T diag(g)
+      E Tgl[C][C + P];        // T diag(g lambda)
+    } t;                      // after the solve
   } am;
-  float M[C][C + 4];
-  E Tm[C][C + P];         // P staging during the Gram products, then T
+  alignas(16) float M[C][C + 4];
+  E Tm[C][C + P];             // P staging during the Gram products, then T
 };
 
 // Raw inputs of one (chunk, head) unit, staged in registers one unit ahead.
@@ -118,50 +120,38 @@ __global__ __launch_bounds__(PREP_THREADS) void k_prep(Params p) {
     x.K.store(&sm.u.a.K[0][0], LK, tid);
     x.Q.store(&sm.u.a.Q[0][0], LK, tid);
     if (tid < C) {
-      const float b = wave_incl_scan(x.la, lane);
+      const float b = wave_incl_scan(x.la, lane), g = __expf(b);
       sm.b[tid] = b;
+      sm.g[tid] = g;
+      sm.gl[tid] = g * x.lam;
       sm.beta[tid] = x.beta;
       sm.lam[tid] = x.lam;
       p.wb[gi * C + tid] = b;
     }
     block_sync_lds();
 
-    // mixed inputs X = K + lambda Q and the decayed copy diag(g) X; a thread
-    // takes 16 bytes of one row
-    {
-      constexpr int VEC = 16 / sizeof(E);
-      for (int idx = tid; idx < C * DK / VEC; idx += NT) {
-        const int r = idx / (DK / VEC), c0 = (idx % (DK / VEC)) * VEC;
-        const uint4 kr = *(const uint4*)&sm.u.a.K[r][c0];
-        const uint4 qr = *(const uint4*)&sm.u.a.Q[r][c0];
-        const E* ke = (const E*)&kr;
-        const E* qe = (const E*)&qr;
-        const float lr = sm.lam[r], gr = __expf(sm.b[r]);
-        uint4 xr, gxr;
-        E* xe = (E*)&xr;
-        E* gxe = (E*)&gxr;
+    // Gram products K K^T and Q K^T, with X K^T = K K^T + diag(lambda) Q K^T;
+    // A (fp32) and P (staged in Tm)
 #pragma unroll
-        for (int j = 0; j < VEC; ++j) {
-          const float xv = tof(ke[j]) + lr * tof(qe[j]);
-          xe[j] = fromf<E>(xv);
-          gxe[j] = fromf<E>(gr * xv);
-        }
-        *(uint4*)&sm.u.a.X[r][c0] = xr;
-        *(uint4*)&sm.GX[r][c0] = gxr;
+    for (int tk = 0; tk < 16 / NW; ++tk) {
+      const int t = w + tk * NW;
+      const int m0 = (t >> 2) * 16, n0 = (t & 3) * 16, i = n0 + fcol(lane);
+      const float bi = sm.b[i];
+      float br[4], betr[4], lr[4];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int r = m0 + frow(lane, j);
+        br[j] = sm.b[r];
+        betr[j] = sm.beta[r];
+        lr[j] = sm.lam[r];
       }
-    }
-    block_sync_lds();
-
-    // Gram products X K^T and Q K^T; A (fp32) and P (staged in Tm)
-    for (int t = w; t < 16; t += NW) {
-      const int m0 = (t >> 2) * 16, n0 = (t & 3) * 16;
-      const f4 gx = mma_k<E, DK>(kmaj(&sm.u.a.X[0][0], LK), kmaj(&sm.u.a.K[0][0], LK), m0, n0, zero4(), lane);
+      const f4 kk = mma_k<E, DK>(kmaj(&sm.u.a.K[0][0], LK), kmaj(&sm.u.a.K[0][0], LK), m0, n0, zero4(), lane);
       const f4 qk = mma_k<E, DK>(kmaj(&sm.u.a.Q[0][0], LK), kmaj(&sm.u.a.K[0][0], LK), m0, n0, zero4(), lane);
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
-        const int r = m0 + frow(lane, j), i = n0 + fcol(lane);
-        const float gam = (r >= i) ? __expf(sm.b[r] - sm.b[i]) : 0.f;
-        sm.am.A[r][i] = (r > i) ? sm.beta[r] * gam * gx[j] : 0.f;
+        const int r = m0 + frow(lane, j);
+        const float gam = (r >= i) ? __expf(br[j] - bi) : 0.f;
+        sm.am.A[r][i] = (r > i) ? betr[j] * gam * (kk[j] + lr[j] * qk[j]) : 0.f;
         sm.Tm[r][i] = fromf<E>(gam * qk[j]);
       }
     }
@@ -172,34 +162,73 @@ __global__ __launch_bounds__(PREP_THREADS) void k_prep(Params p) {
     // UT solve: M = (I + A)^{-1}, T = M diag(beta)
     unit_lower_inverse<NT>(&sm.am.A[0][0], C + 4, &sm.M[0][0], C + 4, tid);
     {
-      // T row-major into LDS and M to global; a thread takes VEC consecutive
+      // T, T diag(g) and T diag(g lambda) into LDS (A is dead: the solve ends
+      // with a barrier) and M to global; a thread takes VEC consecutive
       // columns of one row
       constexpr int VEC = 16 / sizeof(E);
       E* wM = (E*)p.wM;
       for (int idx = tid; idx < C * C / VEC; idx += NT) {
         const int r = idx / (C / VEC), i0 = (idx % (C / VEC)) * VEC;
         const bool upper = (i0 >> 4) > (r >> 4);   // strictly-upper block: zero
-        uint4 tr, mr;
+        uint4 tr, tgr, tglr, mr;
         E* te = (E*)&tr;
+        E* tge = (E*)&tgr;
+        E* tgle = (E*)&tglr;
         E* me = (E*)&mr;
+        float mv[VEC], bv[VEC], gv[VEC], glv[VEC];
+#pragma unroll
+        for (int j = 0; j < VEC; j += 4) {
+          *(f4*)&mv[j] = *(const f4*)&sm.M[r][i0 + j];
+          *(f4*)&bv[j] = *(const f4*)&sm.beta[i0 + j];
+          *(f4*)&gv[j] = *(const f4*)&sm.g[i0 + j];
+          *(f4*)&glv[j] = *(const f4*)&sm.gl[i0 + j];
+        }
 #pragma unroll
         for (int j = 0; j < VEC; ++j) {
-          const float m = upper ? 0.f : sm.M[r][i0 + j];
-          te[j] = fromf<E>(m * sm.beta[i0 + j]);
+          const float m = upper ? 0.f : mv[j];
+          const float tv = m * bv[j];
+          te[j] = fromf<E>(tv);
+          tge[j] = fromf<E>(tv * gv[j]);
+          tgle[j] = fromf<E>(tv * glv[j]);
           me[j] = fromf<E>(m);
         }
         *(uint4*)&sm.Tm[r][i0] = tr;
+        *(uint4*)&sm.am.t.Tg[r][i0] = tgr;
+        *(uint4*)&sm.am.t.Tgl[r][i0] = tglr;
         if (wM) *(uint4*)(wM + gi * C * C + r * C + i0) = mr;
       }
     }
-    // V (K, Q, X are dead: all reads of them finished before the solve's barriers)
+    block_sync_lds();
+
+    // W = T diag(g) X = T diag(g) K + T diag(g lambda) Q (B operands: transpose
+    // reads of K and Q), staged row-major for 16-byte stores
+#pragma unroll
+    for (int tk = 0; tk < (C / 16) * (DK / 16) / NW; ++tk) {
+      const int t = w + tk * NW;
+      const int m0 = (t / (DK / 16)) * 16, n0 = (t % (DK / 16)) * 16;
+      f4 wv = zero4();
+#pragma unroll
+      for (int ks = 0; ks < C / KS; ++ks) {
+        wv = Mma<E>::mma(Frag<E>::load(kmaj(&sm.am.t.Tg[0][0], LC), m0, ks * KS, lane),
+                         tr_frag<E>(&sm.u.a.K[0][0], LK, ks * KS, n0, lane), wv);
+        wv = Mma<E>::mma(Frag<E>::load(kmaj(&sm.am.t.Tgl[0][0], LC), m0, ks * KS, lane),
+                         tr_frag<E>(&sm.u.a.Q[0][0], LK, ks * KS, n0, lane), wv);
+      }
+#pragma unroll
+      for (int j = 0; j < 4; ++j) sm.Ws[m0 + frow(lane, j)][n0 + fcol(lane)] = fromf<E>(wv[j]);
+    }
+    block_sync_lds();
+    store_tile<E, DK, NT>((E*)p.wW + gi * C * DK, &sm.Ws[0][0], LK, tid);
+    // V (K and Q are dead: W, their last reader, ended at the barrier above)
     x.V.store(&sm.u.V[0][0], DV + P, tid);
     block_sync_lds();
 
     // U = T V (the B operand is a transpose read of V), stored C-fragment
     // tiled: tile (mt, nt) at ((mt*(DV/16)+nt)*64 + lane)*4
     E* wU = (E*)p.wU + gi * C * DV;
-    for (int t = w; t < (C / 16) * (DV / 16); t += NW) {
+#pragma unroll
+    for (int tk = 0; tk < (C / 16) * (DV / 16) / NW; ++tk) {
+      const int t = w + tk * NW;
       const int m0 = (t / (DV / 16)) * 16, n0 = (t % (DV / 16)) * 16;
       f4 uu = zero4();
 #pragma unroll
@@ -208,20 +237,6 @@ __global__ __launch_bounds__(PREP_THREADS) void k_prep(Params p) {
                          tr_frag<E>(&sm.u.V[0][0], DV + P, ks * KS, n0, lane), uu);
       *(typename Quad<E>::raw*)(wU + ((size_t)t * 64 + lane) * 4) = Quad<E>::pack(uu);
     }
-    // W = T diag(g) X (the B operand is a transpose read of diag(g) X), staged
-    // row-major for 16-byte stores
-    for (int t = w; t < (C / 16) * (DK / 16); t += NW) {
-      const int m0 = (t / (DK / 16)) * 16, n0 = (t % (DK / 16)) * 16;
-      f4 wv = zero4();
-#pragma unroll
-      for (int ks = 0; ks < C / KS; ++ks)
-        wv = Mma<E>::mma(Frag<E>::load(kmaj(&sm.Tm[0][0], LC), m0, ks * KS, lane),
-                         tr_frag<E>(&sm.GX[0][0], LK, ks * KS, n0, lane), wv);
-#pragma unroll
-      for (int j = 0; j < 4; ++j) sm.am.Ws[m0 + frow(lane, j)][n0 + fcol(lane)] = fromf<E>(wv[j]);
-    }
-    block_sync_lds();
-    store_tile<E, DK, NT>((E*)p.wW + gi * C * DK, &sm.am.Ws[0][0], LK, tid);
   }
 }
 
