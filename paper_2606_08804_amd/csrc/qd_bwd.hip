@@ -478,37 +478,49 @@ __global__ __launch_bounds__(INTRA_THREADS) void k_bwd_intra(Params p) {
     dma_rows<TA::RE, C>(t + TA::V, Vg + vb * ES, (size_t)H * DV * ES, len, Dg + vb * ES, DV * ES, w, lane);
     dma_rows<TA::RE, C>(t + TA::DO, dOg + vb * ES, (size_t)H * DV * ES, len, Dg + vb * ES, DV * ES, w, lane);
   };
-  // the first tile goes out first; then the gates and the chunk's K, Q rows
-  // (registers, for phase B), M = (I + A)^{-1} and the next tiles
+  // the first tiles and M = (I + A)^{-1} go out first; the gates and the
+  // chunk's K, Q rows (registers, needed from phase B on) follow once the
+  // first tile has landed, so that they do not compete with it
   constexpr int NB0 = NVT < TA::NBUF ? NVT : TA::NBUF;
-  if (loader) issue(0);
-  asm volatile("" ::: "memory");
-  const int ti = tid & (C - 1);
-  const size_t gtc = arow + (size_t)min(ti, len - 1) * H;   // rows past the chunk re-read its last row
-  const float gb = p.wb[gi * C + ti], gbeta = p.beta[gtc], glam = p.lam[gtc];
-  TileRegs<E, C, DK, IT> rKf, rQf;
-  rKf.load_clamped((const E*)p.k + arow * DK, (size_t)H * DK, len, tid);
-  rQf.load_clamped((const E*)p.q + arow * DK, (size_t)H * DK, len, tid);
-  asm volatile("" ::: "memory");
   if (loader) {
+#pragma unroll
+    for (int vt = 0; vt < NB0; ++vt) issue(vt);
     const char* Mg = (const char*)((const E*)p.wM + gi * C * C);
     dma_rows<RBC, C>(sm.Mm, Mg, RBC, C, Mg, 0, w, lane);
-#pragma unroll
-    for (int vt = 1; vt < NB0; ++vt) issue(vt);
   }
-  // vector-memory operations of each wave issued after the first tile
-  constexpr int AFTER0 = 3 + 2 * TileRegs<E, C, DK, IT>::N + C * RBC / 1024 / NWAVES + (NB0 - 1) * TA::LOADS;
-  static_assert(AFTER0 <= 63, "outstanding-load counter range");
+  const int ti = tid & (C - 1);
+  const size_t gtc = arow + (size_t)min(ti, len - 1) * H;   // rows past the chunk re-read its last row
+  float gb, gbeta, glam;
+  TileRegs<E, C, DK, IT> rKf, rQf;
+  // vector-memory operations a loading wave has issued after tile vt's, at
+  // the wait for tile vt: later tiles, and M and the register loads when
+  // tile vt is one of the first NB0
+  constexpr int ML = C * RBC / 1024 / NWAVES;
+  constexpr int KQN = 3 + 2 * TileRegs<E, C, DK, IT>::N;
+  static_assert((NB0 - 1) * TA::LOADS + ML <= 63 && TA::LOADS + ML + KQN <= 63, "outstanding-load counter range");
   constexpr int UVT = NVT > 4 ? 1 : NVT;   // full unroll only for short tile loops
 #pragma unroll UVT
   for (int vt = 0; vt < NVT; ++vt) {
-    // tile vt is complete once at most `after` tiles' loads are outstanding
+    // tile vt is complete once at most `pending` later operations are outstanding
     const int after = (vt == 0 ? NB0 : min(NVT, vt + TA::NBUF - 1)) - 1 - vt;
-    if (vt == 0) wait_vm<AFTER0>();
-    else if (after >= 2) wait_vm<2 * TA::LOADS>();
-    else if (after == 1) wait_vm<TA::LOADS>();
+    const int extra = vt < NB0 ? ML + (vt >= 1 ? KQN : 0) : 0;
+    const int pending = after * TA::LOADS + extra;
+    if (vt == 0) wait_vm<(NB0 - 1) * TA::LOADS + ML>();
+    else if (pending >= TA::LOADS + ML + KQN) wait_vm<TA::LOADS + ML + KQN>();
+    else if (pending >= ML + KQN) wait_vm<ML + KQN>();
+    else if (pending >= 2 * TA::LOADS) wait_vm<2 * TA::LOADS>();
+    else if (pending >= TA::LOADS) wait_vm<TA::LOADS>();
     else wait_vm<0>();
     block_sync_lds();                 // tile vt visible; tile vt-1's buffer is free
+    if (vt == 0) {
+      asm volatile("" ::: "memory");
+      gb = p.wb[gi * C + ti];
+      gbeta = p.beta[gtc];
+      glam = p.lam[gtc];
+      rKf.load_clamped((const E*)p.k + arow * DK, (size_t)H * DK, len, tid);
+      rQf.load_clamped((const E*)p.q + arow * DK, (size_t)H * DK, len, tid);
+      asm volatile("" ::: "memory");
+    }
     if (loader && vt >= 1 && vt + TA::NBUF - 1 < NVT) issue(vt + TA::NBUF - 1);
     const char* t = &sm.x.tiles[vt % TA::NBUF][0];
 #pragma unroll
