@@ -16,24 +16,23 @@ using qd::C;
 constexpr int kVersion = 10000;  // 1.0.0
 
 struct Layout {
-  size_t wb = 0, wU = 0, wW = 0, wP = 0;   // forward: chunk factors when no saved context is kept
+  size_t wb = 0, wU = 0, wP = 0, wM = 0;   // forward: chunk factors when no saved context is kept
   size_t dSo = 0, dDb = 0, ctx = 0;        // backward: scan outputs, room to recompute the context
   size_t total = 0;
 };
 
-// Saved context, per unit (slot, head), region after region: S^T [Dk][Dv],
-// D [C][Dv], b fp32 [C], W [C][Dk], P [C][C], M [C][C] (all but b in the
-// activation dtype).
+// Saved context, per unit (slot, head), region after region: S [Dv][Dk],
+// D [C][Dv], gate block fp32 [3][C] (b, beta, lambda), P [C][C], M [C][C]
+// (all but the gates in the activation dtype).
 struct Ctx {
-  size_t states, D, b, W, P, M, total;
+  size_t states, D, b, P, M, total;
 };
 Ctx ctx_layout(size_t units, int Dk, int Dv, int esz) {
   Ctx c;
   c.states = 0;
   c.D = c.states + units * (size_t)Dk * Dv * esz;
   c.b = c.D + units * (size_t)C * Dv * esz;
-  c.W = c.b + units * (size_t)C * 4;
-  c.P = c.W + units * (size_t)C * Dk * esz;
+  c.P = c.b + units * (size_t)3 * C * 4;
   c.M = c.P + units * (size_t)C * C * esz;
   c.total = c.M + units * (size_t)C * C * esz;
   return c;
@@ -53,21 +52,20 @@ Layout make_layout(size_t units, int Dk, int Dv, int esz, bool bwd) {
     L.dDb = take(units * C * Dv * esz);
     L.ctx = take(ctx_layout(units, Dk, Dv, esz).total);
   } else {
-    L.wb = take(units * C * 4);
-    L.wW = take(units * C * Dk * esz);
+    L.wb = take(units * 3 * C * 4);
     L.wP = take(units * C * C * esz);
+    L.wM = take(units * C * C * esz);
   }
   L.total = off;
   return L;
 }
 
-// Points the context fields of p (states, D, b, W, P, M) into a context buffer.
+// Points the context fields of p (states, D, gates, P, M) into a context buffer.
 void bind_ctx(qd::Params& p, char* base, size_t units, int Dk, int Dv, int esz) {
   const Ctx c = ctx_layout(units, Dk, Dv, esz);
   p.saved = base + c.states;
   p.savedD = base + c.D;
   p.wb = reinterpret_cast<float*>(base + c.b);
-  p.wW = base + c.W;
   p.wP = base + c.P;
   p.wM = base + c.M;
 }
@@ -161,8 +159,8 @@ int fwd_impl(bool varlen, int32_t B, int32_t T, int32_t N, const int32_t* cu, in
     bind_ctx(p, static_cast<char*>(saved), units, Dk, Dv, esz);
   } else {
     p.wb = reinterpret_cast<float*>(w + L.wb);
-    p.wW = w + L.wW;
     p.wP = w + L.wP;
+    p.wM = w + L.wM;
   }
   hipError_t e = qd::launch_fwd(p, dtype, Dk, Dv, 0, 1, stream);
   return e == hipSuccess ? QDELTA_OK : QDELTA_EHIP;

@@ -6,7 +6,9 @@
 //
 //   inter-chunk (sequential, reverse):
 //     dD   = P^T dO + Kbar dS'^T                  Kbar = diag(g_C / g) K
+//     dV   = T^T dD = diag(beta) M^T dD
 //     dS   = g_C dS' + dO^T diag(g) Q - dD^T W    (gradient w.r.t. the entry state)
+//          = g_C dS' + (dO - diag(lambda) dV)^T diag(g) Q - dV^T diag(g) K
 //   intra-chunk (parallel over chunks):
 //     D    = U - W S^T
 //     dQ   = diag(g) dO S + dQK K + diag(lambda) dX,      dQK = Gam * M * (dO D^T)
@@ -21,7 +23,7 @@
 //     every term through g, Gam, Kbar and g_C.
 //
 // k_scan_bwd  : one workgroup per (sequence, head, Dv tile); dS^T tile in fp32
-//               accumulators; per chunk writes dD and dS' and produces dV = T^T dD.
+//               accumulators; per chunk writes dD and dS' and produces dV.
 // k_bwd_intra : per (chunk, head); the products that contract over Dv
 //               (dO S, D dS', dD S, dO D^T, dD V^T), then the UT-solve backward
 //               and the products over Dk; final dq, dk, dbeta, dlambda, dlog alpha.
@@ -34,77 +36,81 @@ namespace qd {
 
 // ------------------------------------------------------------------ scan
 // Backward-scan operands of one chunk, filled by direct global->LDS loads as
-// swizzled row-major tiles, in two sets by the phase that reads them:
-//   set A (dD = P^T dO + Kbar dS'^T):           P (C x C), K (C x Dk), this
-//                                              tile's columns of dO (C x BV), b;
-//   set B (dV and the entry-state gradient):   M (C x C), Q, W (C x Dk), dO, b, beta.
-// The transposed operands (P^T, M^T, Q^T, W^T, dO^T) are LDS transpose reads
-// of these tiles.  Each set has its own ring of NBUF chunks and its own
-// producer wave.
+// swizzled row-major tiles, in sets by the phases that read them:
+//   set X (phases 2-4): Q, K (C x Dk), this tile's columns of dO (C x BV) and
+//                       the gate block (b, beta, lambda);
+//   P (phase 2):        the output operator Gam * M_causal * Q K^T (C x C);
+//   M (phase 3):        (I + A)^{-1} (C x C).
+// The transposed operands (P, M^T, Q^T, K^T, dO^T) are LDS transpose reads
+// of these tiles.  Set X has a ring of NA chunks, P two buffers and M one.
+// The four producer waves split every tile's 1 KB instructions evenly;
+// producers 0-2 also load one gate vector each.
 template <typename E, int DK, int BV>
 struct ScanBwdRing {
   static constexpr int RK = DK * (int)sizeof(E), RC = C * (int)sizeof(E), RO = BV * (int)sizeof(E);
-  static constexpr int AP = 0, AK = AP + C * RC, AO = AK + C * RK, AB = AO + C * RO, ABYTES = AB + C * 4;
-  static constexpr int BM = 0, BQ = BM + C * RC, BW = BQ + C * RK, BO = BW + C * RK, BB = BO + C * RO,
-                       BE = BB + C * 4, BBYTES = BE + C * 4;
-  static constexpr int NBUF = sizeof(E) == 2 ? 2 : 1;
-  // direct loads per chunk of each of the two producers of a set (the 1 KB
-  // instructions of every tile split evenly; in set A producer 1 also loads
-  // b, in set B producer 0 loads beta and producer 1 b)
-  static constexpr int IA = (AB - AP) / 1024, IB = (BB - BM) / 1024;
-  static constexpr int LOADS_A0 = IA / 2, LOADS_A1 = IA / 2 + 1, LOADS_B0 = IB / 2 + 1, LOADS_B1 = IB / 2 + 1;
-  static_assert((C * RK / 1024) % 2 == 0 && (C * RC / 1024) % 2 == 0 && (C * RO / 1024) % 2 == 0, "even split");
-  static_assert(NBUF == 1 || (LOADS_A1 <= 63 && LOADS_B1 <= 63), "outstanding-load counter range");
+  static constexpr int XQ = 0, XK = XQ + C * RK, XO = XK + C * RK, XG = XO + C * RO, XBYTES = XG + 3 * C * 4;
+  static constexpr int MBYTES = C * RC;
+  static constexpr int NA = sizeof(E) == 2 ? 3 : 2;
+  static constexpr int LQ = C * RK / 1024 / 4;              // loads per producer: Q
+  static constexpr int LK = (C * RK + C * RO) / 1024 / 4;   // K and dO (plus one gate vector for producers 0-2)
+  static constexpr int LM = C * RC / 1024 / 4;              // M, and P
+  static_assert((C * RK / 1024) % 4 == 0 && (C * RC / 1024) % 4 == 0 && (C * RO / 1024) % 4 == 0, "even split");
+  static_assert(2 * LM + LQ + LK + 1 <= 63, "outstanding-load counter range");
 };
 
 template <typename E, int DK, int BV>
 struct alignas(16) ScanBwdSmem {
   static constexpr int P = Pad<E>::v;
   typedef ScanBwdRing<E, DK, BV> R;
-  alignas(16) char ringA[R::NBUF][R::ABYTES];
-  alignas(16) char ringB[R::NBUF][R::BBYTES];
-  union {
-    E dS[BV][DK + P];   // dS' tile [v][k] (MFMA operand copy; the dS'^T output is read back from it)
-    E dV[C][BV + P];    // dV tile staging [i][v], after the dS' copy is dead
-  } u;
-  E dDn[BV][C + P];     // -dD tile, transposed [v][r] (also the source of the dD output)
+  alignas(16) char ringX[R::NA][R::XBYTES];
+  alignas(16) char ringM[R::MBYTES];
+  alignas(16) char ringP[2][R::MBYTES];
+  E dS[BV][DK + P];   // dS' tile (row v, column k): MFMA operand and output source
+  E dD[C][BV + P];    // dD (row i, column v)
+  E dV[C][BV + P];    // dV (row r, column v)
 };
 
 // One workgroup per (sequence, head, Dv tile of BV = 32): four compute waves
-// and four producer waves (two per operand set; one wave alone issues direct
-// loads at only about 12 bytes per clock); reverse pass over the chunks.  Compute wave w owns
-// rows 16w.. of dD and dV and key rows 16 KPW w.. of the exit-state gradient
-// tile dS'^T (Dk x BV), held in fp32 MFMA accumulators.
+// and four producer waves; reverse pass over the chunks.  The exit-state
+// gradient tile dS'^T (Dk x BV) lives in fp32 MFMA accumulators; compute wave
+// w owns its key rows 16 KPW w.. and the chunk rows 16w.. of every C-row
+// operand.
 //
-// Per chunk the compute waves pass four barriers: B1 (start), B2 (dS' staged),
-// B3 (dD staged), B4 (dV staged).  Producers 0-1 stream set A, 2-3 set B,
-// each while the compute waves work on phases that do not read the buffer
-// being refilled (issuing stalls the issuing wave while the memory pipeline
-// is busy, so it must not delay a barrier): set A of the chunk two steps
-// ahead is issued after B3, set B of the next chunk in two parts between B1,
-// B2 and B3; set A is waited for before B2 and set B before B3.  With one
-// buffer per set (fp32) the refills follow the last reader's barrier.
+// W is not read: with W^T = X^T diag(g) diag(beta) M^T the entry-state
+// gradient is
+//   dS = g_C dS' + Q^T diag(g) (dO - diag(lambda) dV) - K^T diag(g) dV,
+// dV = diag(beta) M^T dD being an output anyway.  Per chunk the compute
+// waves pass three barriers:
+//   B_a  dS' staged, set X, P       phase 2: dS' output; dD = P^T dO +
+//        visible                    Kbar dS'^T (as its transpose); dD staged;
+//   B_b  dD staged, set M visible   phase 3: dD output; dV = diag(beta) M^T dD
+//                                   (as its transpose); dV staged;
+//   B_c  dV staged                  phase 4: dV output; entry-state gradient;
+//                                   dS' of the next chunk staged.
+// Producers: Q of the chunk NA-1 steps ahead and P of the next chunk in phase
+// 2, K, dO and gates of the chunk NA-1 steps ahead in phase 3, M of the next
+// chunk in phase 4; they wait for M in phase 2 and for set X and P of the
+// next chunk in phase 4.
 template <typename E, int DK, int DV, int BV>
 __global__ __launch_bounds__(NTHREADS + 256) void k_scan_bwd(Params p) {
   constexpr int P = Pad<E>::v;
-  constexpr int LK = DK + P, LC = C + P;
+  constexpr int LK = DK + P, LV = BV + P;
   constexpr int NVT = DV / BV;
   constexpr int NB = BV / 16;
-  constexpr int KS = Mma<E>::KS;
+  constexpr int KS = Mma<E>::KS, KPL = Mma<E>::KPL;
+  constexpr int NKS = DK / KS;
   constexpr int KPW = DK / 16 / NWAVES;
   static_assert(KPW >= 1 && KPW * 16 * NWAVES == DK, "key blocks per wave");
   typedef typename Quad<E>::raw QR;
   typedef typename Mma<E>::frag FR;
   typedef ScanBwdRing<E, DK, BV> R;
-  constexpr bool DB = R::NBUF == 2;
+  constexpr int NA = R::NA;
   // fp32 operands take 4-deep k-steps; their long k loops are only partly unrolled
-  constexpr int UKC = C / KS > 4 ? 4 : C / KS, UKD = DK / KS > 4 ? 4 : DK / KS;
+  constexpr int UKD = NKS > 4 ? 4 : NKS;
   __shared__ ScanBwdSmem<E, DK, BV> sm;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int prod = w - NWAVES;               // 0-3 for the producer waves, negative otherwise
   const bool producer = prod >= 0;
-  const bool prodA = prod == 0 || prod == 1, prodB = prod >= 2;
-  const int wp = prod & 1;                   // producer index within its set
   int unit, vt;
   if (!xcd_unit_tile(blockIdx.x, p.N * p.H, NVT, unit, vt)) return;
   const int H = p.H, n = unit / H, h = unit % H, v0 = vt * BV;
@@ -113,52 +119,49 @@ __global__ __launch_bounds__(NTHREADS + 256) void k_scan_bwd(Params p) {
   const int base = slot_base(p, n, s);
   const int nch = max(0, min((e - s + C - 1) / C, p.n_slots - base));
 
-  // rows of K, Q past the chunk come from W, and rows of dO from D: both are
-  // zero there
-  auto chunk_ptrs = [&](int c, size_t& gi, size_t& arow, int& len, const char*& Wg, const char*& Og,
-                        const char*& Dg) {
+  auto chunk_at = [&](int c, size_t& gi, size_t& arow, int& len) {
     const int t0 = s + c * C;
     len = min(C, e - t0);
     gi = (size_t)(base + c) * H + h;
     arow = (size_t)t0 * H + h;
-    Wg = (const char*)((const E*)p.wW + gi * C * DK);
-    Og = (const char*)((const E*)p.dO + arow * DV + v0);
-    Dg = (const char*)((const E*)p.savedD + gi * C * DV + v0);
   };
-  // producers 0-1: their share of set A of chunk c into buffer buf
-  auto issueA = [&](int c, int buf) {
+  // producers: Q of the chunk of iteration it (rows past the chunk re-read
+  // its last row: they only meet zero dO rows and zero gates)
+  auto issueQ = [&](int it) {
     size_t gi, arow;
     int len;
-    const char *Wg, *Og, *Dg;
-    chunk_ptrs(c, gi, arow, len, Wg, Og, Dg);
-    char* r = sm.ringA[buf];
-    const char* Pg = (const char*)((const E*)p.wP + gi * C * C);
+    chunk_at(nch - 1 - it, gi, arow, len);
+    const char* Qg = (const char*)((const E*)p.q + arow * DK);
+    dma_rows<R::RK, C, 4, true>(sm.ringX[it % NA] + R::XQ, Qg, (size_t)H * R::RK, len,
+                                Qg + (size_t)(len - 1) * H * R::RK, 0, prod, lane);
+  };
+  // producers: K, dO (rows past the chunk from D, zero there) and the gates
+  auto issueK = [&](int it) {
+    size_t gi, arow;
+    int len;
+    chunk_at(nch - 1 - it, gi, arow, len);
+    char* r = sm.ringX[it % NA];
     const char* Kg = (const char*)((const E*)p.k + arow * DK);
-    dma_rows<R::RC, C, 2, true>(r + R::AP, Pg, R::RC, C, Pg, 0, wp, lane);
-    dma_rows<R::RK, C, 2, true>(r + R::AK, Kg, (size_t)H * R::RK, len, Wg, R::RK, wp, lane);
-    dma_rows<R::RO, C, 2, true>(r + R::AO, Og, (size_t)H * DV * sizeof(E), len, Dg, DV * sizeof(E), wp, lane);
-    if (wp == 1) dma4_asm(p.wb + gi * C + lane, r + R::AB);
+    const char* Og = (const char*)((const E*)p.dO + arow * DV + v0);
+    const char* Dg = (const char*)((const E*)p.savedD + gi * C * DV + v0);
+    dma_rows<R::RK, C, 4, true>(r + R::XK, Kg, (size_t)H * R::RK, len, Kg + (size_t)(len - 1) * H * R::RK, 0,
+                                prod, lane);
+    dma_rows<R::RO, C, 4, true>(r + R::XO, Og, (size_t)H * DV * sizeof(E), len, Dg, DV * sizeof(E), prod, lane);
+    if (prod < 3) dma4_asm(p.wb + gi * 3 * C + prod * C + lane, r + R::XG + prod * C * 4);
   };
-  // producers 2-3: their share of part `part` (0: M, dO, b, beta; 1: Q, W;
-  // 2: both) of set B of chunk c into buffer buf
-  auto issueB = [&](int c, int buf, int part) {
+  auto issueP = [&](int it) {
     size_t gi, arow;
     int len;
-    const char *Wg, *Og, *Dg;
-    chunk_ptrs(c, gi, arow, len, Wg, Og, Dg);
-    char* r = sm.ringB[buf];
-    if (part != 1) {
-      const char* Mg = (const char*)((const E*)p.wM + gi * C * C);
-      dma_rows<R::RC, C, 2, true>(r + R::BM, Mg, R::RC, C, Mg, 0, wp, lane);
-      dma_rows<R::RO, C, 2, true>(r + R::BO, Og, (size_t)H * DV * sizeof(E), len, Dg, DV * sizeof(E), wp, lane);
-      if (wp == 1) dma4_asm(p.wb + gi * C + lane, r + R::BB);
-      else dma4_asm(p.beta + arow + (size_t)min(lane, len - 1) * H, r + R::BE);
-    }
-    if (part != 0) {
-      const char* Qg = (const char*)((const E*)p.q + arow * DK);
-      dma_rows<R::RK, C, 2, true>(r + R::BQ, Qg, (size_t)H * R::RK, len, Wg, R::RK, wp, lane);
-      dma_rows<R::RK, C, 2, true>(r + R::BW, Wg, R::RK, C, Wg, 0, wp, lane);
-    }
+    chunk_at(nch - 1 - it, gi, arow, len);
+    const char* Pg = (const char*)((const E*)p.wP + gi * C * C);
+    dma_rows<R::RC, C, 4, true>(sm.ringP[it & 1], Pg, R::RC, C, Pg, 0, prod, lane);
+  };
+  auto issueM = [&](int it) {
+    size_t gi, arow;
+    int len;
+    chunk_at(nch - 1 - it, gi, arow, len);
+    const char* Mg = (const char*)((const E*)p.wM + gi * C * C);
+    dma_rows<R::RC, C, 4, true>(sm.ringM, Mg, R::RC, C, Mg, 0, prod, lane);
   };
 
   f4 acc[KPW][NB];
@@ -172,166 +175,191 @@ __global__ __launch_bounds__(NTHREADS + 256) void k_scan_bwd(Params p) {
                                       frow(lane, 0))
                        : zero4();
     }
+  auto stage_dS = [&]() {
+#pragma unroll
+    for (int i = 0; i < KPW; ++i)
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb)
+        *(QR*)&sm.dS[nb * 16 + fcol(lane)][(KPW * w + i) * 16 + frow(lane, 0)] = Quad<E>::pack(acc[i][nb]);
+  };
 
   if (nch > 0) {
-    if (prodA) {
-      issueA(nch - 1, 0);
-      if (DB && nch > 1) issueA(nch - 2, 1);
-    } else if (prodB) {
-      issueB(nch - 1, 0, 2);
+    if (producer) {
+      for (int it = 0; it < NA - 1 && it < nch; ++it) {
+        issueQ(it);
+        issueK(it);
+      }
+      issueP(0);
+      issueM(0);
+      wait_vm<0>();
+    } else {
+      stage_dS();
     }
   }
   for (int it = 0; it < nch; ++it) {
     const int c = nch - 1 - it;
     const size_t gi = (size_t)(base + c) * H + h;
     const int t0 = s + c * C, len = min(C, e - t0);
-    const int buf = DB ? (it & 1) : 0;
-    const char* ra = sm.ringA[buf];
-    const char* rb = sm.ringB[buf];
-    block_sync_lds();                      // B1: previous chunk done
-    // ---- phase 1: stage dS' (compute); producer 0 waits for set A, producer 1
-    // issues the first part of the next chunk's set B
-    if (!producer) {
-#pragma unroll
-      for (int i = 0; i < KPW; ++i)
-#pragma unroll
-        for (int nb = 0; nb < NB; ++nb) {
-          const int kt = KPW * w + i;
-          *(QR*)&sm.u.dS[nb * 16 + fcol(lane)][kt * 16 + frow(lane, 0)] = Quad<E>::pack(acc[i][nb]);
-        }
-    } else if (prodA) {
-      if (DB && it + 1 < nch) {
-        if (wp == 0) wait_vm<DB ? R::LOADS_A0 : 0>();
-        else wait_vm<DB ? R::LOADS_A1 : 0>();
-      } else {
-        wait_vm<0>();
-      }
-    } else {
-      if (DB && it + 1 < nch) issueB(c - 1, (it + 1) & 1, 0);
-    }
-    block_sync_lds();                      // B2: dS' staged; set A of this chunk visible
-    // ---- phase 2: dS' output, dD (compute); producer 1 finishes set B
+    const char* rx = sm.ringX[it % NA];
+    const float* gb = (const float*)(rx + R::XG);   // b, then beta, then lambda
+    const int rr = 16 * w + fcol(lane);             // chunk row of this lane's result columns
+    block_sync_lds();                      // B_a: dS' staged; set X of this chunk visible
+    // ---- phase 2
     if (!producer) {
       {
-        // dS' of this chunk for the intra-chunk kernel, transposed ([k][v]) in the
-        // activation dtype, read back from the operand copy; 16-byte stores
-        constexpr int VEC = 16 / sizeof(E), PR = BV / VEC;
-        E* dst = (E*)p.w_dSo + gi * DK * DV + v0;
-        for (int idx = tid; idx < DK * PR; idx += NTHREADS) {
-          const int r = idx / PR, c0 = (idx % PR) * VEC;
-          uint4 o;
-          E* oe = (E*)&o;
-#pragma unroll
-          for (int j = 0; j < VEC; ++j) oe[j] = sm.u.dS[c0 + j][r];
-          *(uint4*)(dst + (size_t)r * DV + c0) = o;
+        // dS' of this chunk for the intra-chunk kernel (row v, column k), 16-byte stores
+        constexpr int VEC = 16 / sizeof(E), PR = DK / VEC;
+        E* dst = (E*)p.w_dSo + gi * DV * DK + (size_t)v0 * DK;
+        for (int idx = tid; idx < BV * PR; idx += NTHREADS) {
+          const int r = idx / PR, cc = (idx % PR) * VEC;
+          *(uint4*)(dst + (size_t)r * DK + cc) = *(const uint4*)&sm.dS[r][cc];
         }
       }
-      const float* bch = (const float*)(ra + R::AB);
-      const float bl = bch[C - 1];
-      // dD = P^T dO + diag(g_C/g) K dS'^T   (rows 16w..)
+      // dD^T (value rows, key columns 16w..) = dS' Kbar^T + dO^T P
+      const float bi = gb[rr], kbi = __expf(gb[C - 1] - bi);
+      f4 dt[NB];
 #pragma unroll
-      for (int nb = 0; nb < NB; ++nb) {
-        f4 d1 = zero4(), d2 = zero4();
-#pragma unroll UKC
-        for (int ks = 0; ks < C / KS; ++ks)
-          d1 = Mma<E>::mma(tile_tr_frag<E, R::RC>(ra + R::AP, ks * KS, 16 * w, lane),
-                           tile_tr_frag<E, R::RO>(ra + R::AO, ks * KS, nb * 16, lane), d1);
+      for (int nb = 0; nb < NB; ++nb) dt[nb] = zero4();
 #pragma unroll UKD
-        for (int ks = 0; ks < DK / KS; ++ks)
-          d2 = Mma<E>::mma(tile_frag<E, R::RK>(ra + R::AK, 16 * w, ks * KS, lane),
-                           Frag<E>::load(kmaj(&sm.u.dS[0][0], LK), nb * 16, ks * KS, lane), d2);
-        f4 dn;
+      for (int ks = 0; ks < NKS; ++ks) {
+        const FR kB = tile_frag<E, R::RK>(rx + R::XK, 16 * w, ks * KS, lane);
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          const int r = 16 * w + frow(lane, j);
-          dn[j] = -(d1[j] + __expf(bl - bch[r]) * d2[j]);
-        }
-        *(QR*)&sm.dDn[nb * 16 + fcol(lane)][16 * w + frow(lane, 0)] = Quad<E>::pack(dn);
+        for (int nb = 0; nb < NB; ++nb)
+          dt[nb] = Mma<E>::mma(Frag<E>::load(kmaj(&sm.dS[0][0], LK), nb * 16, ks * KS, lane), kB, dt[nb]);
       }
-    } else if (prodB) {
-      if (DB && it + 1 < nch) {
-        issueB(c - 1, (it + 1) & 1, 1);
-        // set B of this chunk landed; the next one's in flight
-        if (wp == 0) wait_vm<DB ? R::LOADS_B0 : 0>();
-        else wait_vm<DB ? R::LOADS_B1 : 0>();
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) dt[nb][j] *= kbi;
+      // + dO^T P (P causal: k blocks before this wave's key rows are skipped)
+#pragma unroll
+      for (int ks = 0; ks < C / KS; ++ks)
+        if (ks * KS + KS > 16 * w) {
+          const FR pB = tile_tr_frag<E, R::RC>(sm.ringP[it & 1], ks * KS, 16 * w, lane);
+#pragma unroll
+          for (int nb = 0; nb < NB; ++nb)
+            dt[nb] = Mma<E>::mma(tile_tr_frag<E, R::RO>(rx + R::XO, ks * KS, nb * 16, lane), pB, dt[nb]);
+        }
+      // key rows past the chunk carry no gradient
+      const float keep = rr < len ? 1.f : 0.f;
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb) *(QR*)&sm.dD[rr][nb * 16 + frow(lane, 0)] = Quad<E>::pack(keep * dt[nb]);
+    } else {
+      // Q of the chunk NA-1 steps ahead (its ring slot was freed at B_a) and P
+      // of the next chunk (its buffer was last read in the previous phase 2);
+      // then M of this chunk must have landed
+      if (it + NA - 1 < nch) {
+        issueQ(it + NA - 1);
+        issueP(it + 1);
+        wait_vm<R::LQ + R::LM>();
+      } else if (it + 1 < nch) {
+        issueP(it + 1);
+        wait_vm<R::LM>();
       } else {
         wait_vm<0>();
       }
     }
-    block_sync_lds();                      // B3: dD staged; set B visible; set A of this chunk free
-    // ---- phase 3: dD output, dV, entry-state gradient (compute); producer 0 refills set A
+    block_sync_lds();                      // B_b: dD staged; M of this chunk visible
+    // ---- phase 3
     if (!producer) {
       {
-        // dD rows for the intra-chunk kernel, read back from -dD^T
+        // dD rows for the intra-chunk kernel
         constexpr int VEC = 16 / sizeof(E), PR = BV / VEC;
         E* ddst = (E*)p.w_dDb + gi * C * DV + v0;
         for (int idx = tid; idx < C * PR; idx += NTHREADS) {
-          const int r = idx % C, cc = (idx / C) * VEC;
-          uint4 o;
-          E* oe = (E*)&o;
-#pragma unroll
-          for (int j = 0; j < VEC; ++j) oe[j] = fromf<E>(-tof(sm.dDn[cc + j][r]));
-          *(uint4*)(ddst + (size_t)r * DV + cc) = o;
+          const int r = idx / PR, cc = (idx % PR) * VEC;
+          *(uint4*)(ddst + (size_t)r * DV + cc) = *(const uint4*)&sm.dD[r][cc];
         }
       }
-      const float* bch = (const float*)(rb + R::BB);
-      const float* bech = (const float*)(rb + R::BE);
-      // dV = T^T dD = diag(beta) M^T dD  (rows 16w..), staged for coalesced stores
-      // (the dS' copy it overwrites was last read before B3)
-      float nbeta[4];
-#pragma unroll
-      for (int j = 0; j < 4; ++j) nbeta[j] = -bech[16 * w + frow(lane, j)];
+      // dV^T (value rows, chunk columns 16w..) = beta_r (dD^T M); M is lower
+      // triangular, so k blocks before this wave's rows are skipped
+      const float betar = gb[C + rr];
 #pragma unroll
       for (int nb = 0; nb < NB; ++nb) {
         f4 dv = zero4();
-#pragma unroll UKC
+#pragma unroll
         for (int ks = 0; ks < C / KS; ++ks)
-          dv = Mma<E>::mma(tile_tr_frag<E, R::RC>(rb + R::BM, ks * KS, 16 * w, lane),
-                           Frag<E>::load(kmaj(&sm.dDn[0][0], LC), nb * 16, ks * KS, lane), dv);
+          if (ks * KS + KS > 16 * w)
+            dv = Mma<E>::mma(tr_frag<E>(&sm.dD[0][0], LV, ks * KS, nb * 16, lane),
+                             tile_tr_frag<E, R::RC>(sm.ringM, ks * KS, 16 * w, lane), dv);
 #pragma unroll
-        for (int j = 0; j < 4; ++j) sm.u.dV[16 * w + frow(lane, j)][nb * 16 + fcol(lane)] = fromf<E>(nbeta[j] * dv[j]);
+        for (int j = 0; j < 4; ++j) dv[j] *= betar;
+        *(QR*)&sm.dV[rr][nb * 16 + frow(lane, 0)] = Quad<E>::pack(dv);
       }
-      // dS_entry^T = g_C dS'^T + Q^T diag(g) dO - W^T dD   (the decay scales the
-      // dO fragment along the contracted token index)
-      const float gC = __expf(bch[C - 1]);
+    } else {
+      if (it + NA - 1 < nch) issueK(it + NA - 1);
+    }
+    block_sync_lds();                      // B_c: dV staged; M of this chunk free
+    // ---- phase 4
+    if (!producer) {
+      {
+        constexpr int VEC = 16 / sizeof(E), PR = BV / VEC;
+        E* vdst = (E*)p.dv + ((size_t)t0 * H + h) * DV + v0;
+        for (int idx = tid; idx < C * PR; idx += NTHREADS) {
+          const int r = idx / PR, cc = (idx % PR) * VEC;
+          if (r < len) *(uint4*)(vdst + (size_t)r * H * DV + cc) = *(const uint4*)&sm.dV[r][cc];
+        }
+      }
+      // dS_entry^T = g_C dS'^T + Q^T diag(g) (dO - diag(lambda) dV) - K^T diag(g) dV;
+      // the gates scale the B fragments along the contracted token index
+      const float gC = __expf(gb[C - 1]);
 #pragma unroll
-      for (int nb = 0; nb < NB; ++nb) {
+      for (int i = 0; i < KPW; ++i)
 #pragma unroll
-        for (int i = 0; i < KPW; ++i) acc[i][nb] = gC * acc[i][nb];
-#pragma unroll UKC
-        for (int ks = 0; ks < C / KS; ++ks) {
-          const FR bd = Frag<E>::load(kmaj(&sm.dDn[0][0], LC), nb * 16, ks * KS, lane);
-          FR gdo = tile_tr_frag<E, R::RO>(rb + R::BO, ks * KS, nb * 16, lane);
-          E* ge = (E*)&gdo;
+        for (int nb = 0; nb < NB; ++nb) acc[i][nb] = gC * acc[i][nb];
 #pragma unroll
-          for (int e2 = 0; e2 < Mma<E>::KPL; ++e2)
-            ge[e2] = fromf<E>(__expf(bch[ks * KS + (lane >> 4) * Mma<E>::KPL + e2]) * tof(ge[e2]));
+      for (int ks = 0; ks < C / KS; ++ks) {
+        float gk[KPL], lk[KPL];
+#pragma unroll
+        for (int e2 = 0; e2 < KPL; ++e2) {
+          const int r = ks * KS + (lane >> 4) * KPL + e2;
+          gk[e2] = __expf(gb[r]);
+          lk[e2] = gb[2 * C + r];
+        }
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb) {
+          const FR fo = tile_tr_frag<E, R::RO>(rx + R::XO, ks * KS, nb * 16, lane);
+          const FR fv = tr_frag<E>(&sm.dV[0][0], LV, ks * KS, nb * 16, lane);
+          FR z1, z2;
+          const E* oe = (const E*)&fo;
+          const E* ve = (const E*)&fv;
+          E* z1e = (E*)&z1;
+          E* z2e = (E*)&z2;
+#pragma unroll
+          for (int e2 = 0; e2 < KPL; ++e2) {
+            const float dvv = tof(ve[e2]);
+            z1e[e2] = fromf<E>(gk[e2] * (tof(oe[e2]) - lk[e2] * dvv));
+            z2e[e2] = fromf<E>(-gk[e2] * dvv);
+          }
 #pragma unroll
           for (int i = 0; i < KPW; ++i) {
-            acc[i][nb] = Mma<E>::mma(tile_tr_frag<E, R::RK>(rb + R::BQ, ks * KS, 16 * (KPW * w + i), lane), gdo,
+            acc[i][nb] = Mma<E>::mma(tile_tr_frag<E, R::RK>(rx + R::XQ, ks * KS, 16 * (KPW * w + i), lane), z1,
                                      acc[i][nb]);
-            acc[i][nb] = Mma<E>::mma(tile_tr_frag<E, R::RK>(rb + R::BW, ks * KS, 16 * (KPW * w + i), lane), bd,
+            acc[i][nb] = Mma<E>::mma(tile_tr_frag<E, R::RK>(rx + R::XK, ks * KS, 16 * (KPW * w + i), lane), z2,
                                      acc[i][nb]);
           }
         }
       }
-    } else if (prodA) {
-      if (DB && it + 2 < nch) issueA(c - 2, buf);
-      if (!DB && it + 1 < nch) issueA(c - 1, 0);
-    }
-    block_sync_lds();                      // B4: dV staged; set B of this chunk free
-    if (prodB) {
-      if (!DB && it + 1 < nch) issueB(c - 1, 0, 2);
-    } else if (!producer) {
-      constexpr int VEC = 16 / sizeof(E), PR = BV / VEC;
-      E* vdst = (E*)p.dv + ((size_t)t0 * H + h) * DV + v0;
-      for (int idx = tid; idx < C * PR; idx += NTHREADS) {
-        const int r = idx / PR, cc = (idx % PR) * VEC;
-        if (r < len) *(uint4*)(vdst + (size_t)r * H * DV + cc) = *(const uint4*)&sm.u.dV[r][cc];
+      stage_dS();
+    } else if (it + 1 < nch) {
+      issueM(it + 1);
+      // set X and P of the next chunk complete: what was issued after the
+      // later of their last parts may still be in flight
+      if constexpr (NA == 2) {
+        wait_vm<R::LM>();                  // P, then K: only M follows
+      } else {
+        if (it + 2 < nch) {                // P issued after K of the next chunk: K ahead and M follow
+          if (prod < 3) wait_vm<R::LK + 1 + R::LM>();
+          else wait_vm<R::LK + R::LM>();
+        } else {
+          wait_vm<R::LM>();
+        }
       }
     }
   }
-  if (p.dS0 && !producer) {
+  if (producer) {
+    wait_vm<0>();
+  } else if (p.dS0) {
 #pragma unroll
     for (int i = 0; i < KPW; ++i)
 #pragma unroll
@@ -355,13 +383,15 @@ __global__ __launch_bounds__(NTHREADS + 256) void k_scan_bwd(Params p) {
 // forms dG, dQK and the beta and decay terms in MFMA-layout registers; B3
 // produces dX, dq and dk.  The tail turns the decay terms into d log alpha.
 
-// Phase-A tile of 32 value columns: S^T, dS'^T, D, V, dO, dD, each in the
-// swizzled direct-load layout; a ring of NBUF tiles keeps two in flight.
+// Phase-A tile of 32 value columns: S, dS' (32 value rows of Dk), D, V, dO,
+// dD (C rows of 32), each in the swizzled direct-load layout; a ring of NBUF
+// tiles keeps two in flight.
 template <typename E, int DK>
 struct TileA {
   static constexpr int BV = 32;
-  static constexpr int RE = BV * (int)sizeof(E);    // row bytes
-  static constexpr int S = 0, DS = S + DK * RE, D = DS + DK * RE, V = D + C * RE, DO = V + C * RE,
+  static constexpr int RE = BV * (int)sizeof(E);    // row bytes of the C-row tiles
+  static constexpr int RK = DK * (int)sizeof(E);    // row bytes of the state tiles
+  static constexpr int S = 0, DS = S + BV * RK, D = DS + BV * RK, V = D + C * RE, DO = V + C * RE,
                        DD = DO + C * RE, BYTES = DD + C * RE;
   static constexpr int NBUF = sizeof(E) == 2 ? 3 : 2;   // fp32 tiles are twice as large
   static constexpr int LOADS = BYTES / 1024 / NWAVES;   // direct loads per wave and tile
@@ -471,8 +501,8 @@ __global__ __launch_bounds__(INTRA_THREADS) void k_bwd_intra(Params p) {
   auto issue = [&](int vt) {
     char* t = &sm.x.tiles[vt % TA::NBUF][0];
     const size_t vb = (size_t)vt * BV;
-    dma_rows<TA::RE, DK>(t + TA::S, Sg + vb * ES, DV * ES, DK, Sg, 0, w, lane);
-    dma_rows<TA::RE, DK>(t + TA::DS, dSg + vb * ES, DV * ES, DK, dSg, 0, w, lane);
+    dma_rows<TA::RK, BV>(t + TA::S, Sg + vb * TA::RK, TA::RK, BV, Sg, 0, w, lane);
+    dma_rows<TA::RK, BV>(t + TA::DS, dSg + vb * TA::RK, TA::RK, BV, dSg, 0, w, lane);
     dma_rows<TA::RE, C>(t + TA::D, Dg + vb * ES, DV * ES, C, Dg, 0, w, lane);
     dma_rows<TA::RE, C>(t + TA::DD, dDg + vb * ES, DV * ES, C, dDg, 0, w, lane);
     dma_rows<TA::RE, C>(t + TA::V, Vg + vb * ES, (size_t)H * DV * ES, len, Dg + vb * ES, DV * ES, w, lane);
@@ -489,7 +519,6 @@ __global__ __launch_bounds__(INTRA_THREADS) void k_bwd_intra(Params p) {
     dma_rows<RBC, C>(sm.Mm, Mg, RBC, C, Mg, 0, w, lane);
   }
   const int ti = tid & (C - 1);
-  const size_t gtc = arow + (size_t)min(ti, len - 1) * H;   // rows past the chunk re-read its last row
   float gb, gbeta, glam;
   TileRegs<E, C, DK, IT> rKf, rQf;
   // vector-memory operations a loading wave has issued after tile vt's, at
@@ -514,9 +543,9 @@ __global__ __launch_bounds__(INTRA_THREADS) void k_bwd_intra(Params p) {
     block_sync_lds();                 // tile vt visible; tile vt-1's buffer is free
     if (vt == 0) {
       asm volatile("" ::: "memory");
-      gb = p.wb[gi * C + ti];
-      gbeta = p.beta[gtc];
-      glam = p.lam[gtc];
+      gb = p.wb[gi * 3 * C + ti];
+      gbeta = p.wb[gi * 3 * C + C + ti];
+      glam = p.wb[gi * 3 * C + 2 * C + ti];
       rKf.load_clamped((const E*)p.k + arow * DK, (size_t)H * DK, len, tid);
       rQf.load_clamped((const E*)p.q + arow * DK, (size_t)H * DK, len, tid);
       asm volatile("" ::: "memory");
@@ -531,8 +560,8 @@ __global__ __launch_bounds__(INTRA_THREADS) void k_bwd_intra(Params p) {
 #pragma unroll
       for (int i = 0; i < HK; ++i) {
         const int kb = kb0 + i;
-        const FR bS = tile_frag<E, TA::RE>(t + TA::S, kb * 16, ks * KS, lane);
-        const FR bdS = tile_frag<E, TA::RE>(t + TA::DS, kb * 16, ks * KS, lane);
+        const FR bS = tile_tr_frag<E, TA::RK>(t + TA::S, ks * KS, kb * 16, lane);
+        const FR bdS = tile_tr_frag<E, TA::RK>(t + TA::DS, ks * KS, kb * 16, lane);
         aQ[i] = Mma<E>::mma(aO, bS, aQ[i]);
         aW[i] = Mma<E>::mma(adD, bS, aW[i]);
         aK[i] = Mma<E>::mma(aD, bdS, aK[i]);
@@ -553,17 +582,16 @@ __global__ __launch_bounds__(INTRA_THREADS) void k_bwd_intra(Params p) {
       }
     }
   }
-  // the two row-block-0 waves together read all of S^T and dS'^T once
+  // the two row-block-0 waves together read all of S and dS' once
   if (rb == 0) {
     sdot = wave_sum(sdot);
     if (lane == 0) sm.sdot[ch] = sdot;
   }
   if (tid < C) {
-    const bool ok = tid < len;
     sm.b[tid] = gb;
     sm.g[tid] = __expf(gb);
-    sm.beta[tid] = ok ? gbeta : 0.f;
-    sm.lam[tid] = ok ? glam : 0.f;
+    sm.beta[tid] = gbeta;   // zero past the chunk in the gate block
+    sm.lam[tid] = glam;
   }
 
   // ---------------- phase B1: G = X K^T, QK = Q K^T, dT2 = dW (g X)^T

@@ -472,6 +472,71 @@ __device__ inline f4 tr_col4(const float* base, int ld, int i0, int j0, int lane
   return r;
 }
 
+// ----------------------------------------------------------------- 16-wide k steps
+// Products with a C x C operand that was itself produced by an MFMA use the
+// 16-wide k step (v_mfma_f32_16x16x16_bf16, or four 16x16x4 fp32 steps), in
+// which lane l supplies the four k values 4 (l >> 4) .. +3 of its row or
+// column l & 15.  That is exactly how an MFMA result holds a 16 x 16 block
+// (rows 4 (l >> 4) + j, column l & 15), so a result block Z can serve as the
+// B operand (k = row of Z) or as the A operand of Z^T without leaving the
+// registers.  Q4<E>::t holds one lane's four values.
+template <typename E> struct Q4;
+template <> struct Q4<__bf16> {
+  typedef bf4 t;
+  __device__ static inline t from(f4 x) {
+    t r;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) r[j] = (__bf16)x[j];
+    return r;
+  }
+  __device__ static inline f4 mma(t a, t b, f4 c) {
+    typedef short s4 __attribute__((ext_vector_type(4)));
+    return __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(__builtin_bit_cast(s4, a), __builtin_bit_cast(s4, b), c, 0,
+                                                      0, 0);
+  }
+};
+template <> struct Q4<float> {
+  typedef f4 t;
+  __device__ static inline t from(f4 x) { return x; }
+  // four k-steps of 4; in step j lane group l >> 4 supplies k = 4 (l >> 4) + j
+  __device__ static inline f4 mma(t a, t b, f4 c) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) c = __builtin_amdgcn_mfma_f32_16x16x4f32(a[j], b[j], c, 0, 0, 0);
+    return c;
+  }
+};
+// Four k values (rows k0 + 4 (l >> 4) .. +3) of column j0 + (l & 15) of a
+// row-major LDS matrix (element (k, j) at base + k * ld + j): one transpose
+// read for 16-bit elements.
+template <typename E>
+__device__ inline typename Q4<E>::t tr_q4(const E* base, int ld, int k0, int j0, int lane);
+template <>
+__device__ inline bf4 tr_q4<__bf16>(const __bf16* base, int ld, int k0, int j0, int lane) {
+  typedef __attribute__((address_space(3))) bf4* lp;
+  const int L = lane & 15;
+  const __bf16* a = base + (size_t)(k0 + 4 * (lane >> 4) + (L >> 2)) * ld + j0 + 4 * (L & 3);
+  return __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lp)(uintptr_t)(uint32_t)(uintptr_t)a);
+}
+template <>
+__device__ inline f4 tr_q4<float>(const float* base, int ld, int k0, int j0, int lane) {
+  const float* a = base + (size_t)(k0 + 4 * (lane >> 4)) * ld + j0 + (lane & 15);
+  return f4{a[0], a[(size_t)ld], a[(size_t)2 * ld], a[(size_t)3 * ld]};
+}
+// Same from a swizzled direct-load tile with rows of RB bytes.
+template <typename E, int RB>
+__device__ inline typename Q4<E>::t tile_tr_q4(const char* t, int k0, int j0, int lane) {
+  if constexpr (sizeof(E) == 2) {
+    typedef __attribute__((address_space(3))) bf4* lp;
+    const int L = lane & 15;
+    const char* a = t + tile_off<RB>(k0 + 4 * (lane >> 4) + (L >> 2), 2 * (j0 + 4 * (L & 3)));
+    return __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lp)(uintptr_t)(uint32_t)(uintptr_t)a);
+  } else {
+    const int r = k0 + 4 * (lane >> 4), cb = 4 * (j0 + (lane & 15));
+    return f4{*(const float*)(t + tile_off<RB>(r, cb)), *(const float*)(t + tile_off<RB>(r + 1, cb)),
+              *(const float*)(t + tile_off<RB>(r + 2, cb)), *(const float*)(t + tile_off<RB>(r + 3, cb))};
+  }
+}
+
 // Same from an fp32 tile, converted to E; the fp32 values are returned in v.
 template <typename E>
 __device__ inline typename Mma<E>::frag tile_frag_f32(const char* t, int row0, int k0, int lane,
@@ -520,15 +585,15 @@ struct Params {
   // forward outputs
   void* o;
   float* Sfin;
-  void* saved;           // saved context: entry states S^T [slot][H][Dk][Dv] (dtype)
+  void* saved;           // saved context: entry states S [slot][H][Dv][Dk] (dtype)
   void* savedD;          // saved context: D [slot][H][C][Dv] (dtype)
   // chunk factors from the preparation, per slot and head (in the saved
   // context when one is kept, else in the workspace)
-  float* wb;             // [slot][H][C] chunk-local prefix sums of log alpha
-  void* wU;              // [slot][H] C x Dv, C-fragment tiled (workspace only)
-  void* wW;              // [slot][H][C][Dk]  W = T diag(g) X
-  void* wP;              // [slot][H][C][C]   P = Gam * M * Q K^T
-  void* wM;              // [slot][H][C][C]   M = (I + A)^{-1}, or nullptr when not kept
+  float* wb;             // [slot][H][3][C] gate block: chunk-local prefix sums b of
+                         // log alpha, beta, lambda (beta, lambda zero past the chunk)
+  void* wU;              // [slot][H] U^T (Dv x C), C-fragment tiled (workspace only)
+  void* wP;              // [slot][H][C][C]   P = Gam * M_causal * Q K^T
+  void* wM;              // [slot][H][C][C]   M = (I + A)^{-1}
   // backward
   const void* dO;
   const float* dSfin;
@@ -539,7 +604,7 @@ struct Params {
   float* dlam;
   float* dla;
   float* dS0;
-  void* w_dSo;           // [slot][H][Dk][Dv] gradient w.r.t. each chunk's exit state, transposed (dtype)
+  void* w_dSo;           // [slot][H][Dv][Dk] gradient w.r.t. each chunk's exit state (dtype)
   void* w_dDb;           // [slot][H][C][Dv] dD (dtype)
 };
 

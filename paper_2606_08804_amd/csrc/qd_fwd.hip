@@ -7,17 +7,19 @@
 //
 //   b_r = sum_{j<=r} log alpha_j,  g_r = exp(b_r),  Gam_ri = exp(b_r - b_i)
 //   X   = K + diag(lambda) Q
-//   A   = strictLower(diag(beta) (Gam * X K^T)),   T = (I + A)^{-1} diag(beta)
+//   A   = strictLower(diag(beta) (Gam * X K^T)),   M = (I + A)^{-1},  T = M diag(beta)
 //   U   = T V,   W = T diag(g) X
-//   D   = U - W S^T
-//   O   = diag(g) Q S^T + (Gam * M * Q K^T) D     (M includes the diagonal)
+//   D   = U - W S^T = U - M Y,   Y = diag(beta g) (K S^T + diag(lambda) Q S^T)
+//   O   = diag(g) Q S^T + (Gam * M_causal * Q K^T) D     (the mask includes the diagonal)
 //   S'  = g_C S + D^T diag(g_C / g) K
 //
 // k_prep   (persistent over chunk-head units, fully parallel): b, the Gram
-//          products, A, the UT solve, U and W; writes b, U, W, P and M.
+//          products, A, the UT solve; writes the gate block, M and U^T.
 // k_scan_fwd (one workgroup per sequence, head and Dv tile): the sequential
 //          pass over chunks; the state tile stays in MFMA accumulators in fp32;
-//          D, the chunk output and the state update are computed on chip.
+//          D, the chunk output and the state update are computed on chip from
+//          Q, K, M, U and the gates (W and the output operator are never
+//          formed in memory).
 #include "qd_common.h"
 #include "qd_launch.h"
 
@@ -28,24 +30,17 @@ namespace qd {
 template <typename E, int DK, int DV>
 struct alignas(16) PrepSmem {
   static constexpr int P = Pad<E>::v;
-  alignas(16) float b[C], g[C], gl[C], beta[C], lam[C];   // gl = g lambda
+  alignas(16) float b[C], beta[C], lam[C];
   union {
     struct {
       E K[C][DK + P];
       E Q[C][DK + P];
     } a;
-    E V[C][DV + P];           // after W, the last reader of K and Q
+    E V[C][DV + P];           // after the Gram products, the last readers of K and Q
   } u;
-  E Ws[C][DK + P];            // W staging for 16-byte stores
-  union {
-    float A[C][C + 4];        // strictly lower A, consumed by the solve
-    struct {
-      E Tg[C][C + P];         // T diag(g)
-      E Tgl[C][C + P];        // T diag(g lambda)
-    } t;                      // after the solve
-  } am;
+  float A[C][C + 4];          // strictly lower A, consumed by the solve
   alignas(16) float M[C][C + 4];
-  E Tm[C][C + P];             // P staging during the Gram products, then T
+  E Tm[C][C + P];             // P staging during the Gram products, then T = M diag(beta)
 };
 
 // Raw inputs of one (chunk, head) unit, staged in registers one unit ahead.
@@ -71,10 +66,10 @@ __device__ inline void store_tile(E* dst, const E* src, int ld, int tid) {
   }
 }
 
-// Writes b, U, W, P and, when p.wM is set, M = (I + A)^{-1} for every unit.
-// Persistent: each workgroup walks units blockIdx.x, +gridDim.x, ... and
-// prefetches the next unit's inputs into registers while computing the
-// current one.
+// Writes, for every unit, the gate block (b, beta, lambda), the intra-chunk
+// output operator P = Gam * M_causal * Q K^T, M = (I + A)^{-1} and U^T = (T V)^T.  Persistent: each workgroup walks units blockIdx.x,
+// +gridDim.x, ... and prefetches the next unit's inputs into registers while
+// computing the current one.
 template <typename E, int DK, int DV>
 __global__ __launch_bounds__(PREP_THREADS) void k_prep(Params p) {
   constexpr int NT = PREP_THREADS, NW = NT / 64;
@@ -120,18 +115,20 @@ __global__ __launch_bounds__(PREP_THREADS) void k_prep(Params p) {
     x.K.store(&sm.u.a.K[0][0], LK, tid);
     x.Q.store(&sm.u.a.Q[0][0], LK, tid);
     if (tid < C) {
-      const float b = wave_incl_scan(x.la, lane), g = __expf(b);
+      const float b = wave_incl_scan(x.la, lane);
       sm.b[tid] = b;
-      sm.g[tid] = g;
-      sm.gl[tid] = g * x.lam;
       sm.beta[tid] = x.beta;
       sm.lam[tid] = x.lam;
-      p.wb[gi * C + tid] = b;
+      // gate block: b, beta, lambda (zero past the chunk's end)
+      float* gblk = p.wb + gi * 3 * C;
+      gblk[tid] = b;
+      gblk[C + tid] = x.beta;
+      gblk[2 * C + tid] = x.lam;
     }
     block_sync_lds();
 
-    // Gram products K K^T and Q K^T, with X K^T = K K^T + diag(lambda) Q K^T;
-    // A (fp32) and P (staged in Tm)
+    // A = strictLower(diag(beta) Gam * X K^T), X K^T = K K^T + diag(lambda) Q K^T,
+    // and P (staged in Tm)
 #pragma unroll
     for (int tk = 0; tk < 16 / NW; ++tk) {
       const int t = w + tk * NW;
@@ -151,80 +148,50 @@ __global__ __launch_bounds__(PREP_THREADS) void k_prep(Params p) {
       for (int j = 0; j < 4; ++j) {
         const int r = m0 + frow(lane, j);
         const float gam = (r >= i) ? __expf(br[j] - bi) : 0.f;
-        sm.am.A[r][i] = (r > i) ? betr[j] * gam * (kk[j] + lr[j] * qk[j]) : 0.f;
+        sm.A[r][i] = (r > i) ? betr[j] * gam * (kk[j] + lr[j] * qk[j]) : 0.f;
         sm.Tm[r][i] = fromf<E>(gam * qk[j]);
       }
     }
     block_sync_lds();
-    // P out before the solve (whose barriers order the later T writes to Tm)
+    // V (K and Q are dead: the Gram products ended at the barrier above); P
+    // out before the solve, whose barriers order the later T writes to Tm
+    x.V.store(&sm.u.V[0][0], DV + P, tid);
     store_tile<E, C, NT>((E*)p.wP + gi * C * C, &sm.Tm[0][0], LC, tid);
 
-    // UT solve: M = (I + A)^{-1}, T = M diag(beta)
-    unit_lower_inverse<NT>(&sm.am.A[0][0], C + 4, &sm.M[0][0], C + 4, tid);
+    // UT solve: M = (I + A)^{-1} (its barriers also order the V stores)
+    unit_lower_inverse<NT>(&sm.A[0][0], C + 4, &sm.M[0][0], C + 4, tid);
     {
-      // T, T diag(g) and T diag(g lambda) into LDS (A is dead: the solve ends
-      // with a barrier) and M to global; a thread takes VEC consecutive
-      // columns of one row
+      // T = M diag(beta) into LDS and M to global; a thread takes VEC
+      // consecutive columns of one row
       constexpr int VEC = 16 / sizeof(E);
-      E* wM = (E*)p.wM;
+      E* wM = (E*)p.wM + gi * C * C;
       for (int idx = tid; idx < C * C / VEC; idx += NT) {
         const int r = idx / (C / VEC), i0 = (idx % (C / VEC)) * VEC;
         const bool upper = (i0 >> 4) > (r >> 4);   // strictly-upper block: zero
-        uint4 tr, tgr, tglr, mr;
+        uint4 tr, mr;
         E* te = (E*)&tr;
-        E* tge = (E*)&tgr;
-        E* tgle = (E*)&tglr;
         E* me = (E*)&mr;
-        float mv[VEC], bv[VEC], gv[VEC], glv[VEC];
+        float mv[VEC], bv[VEC];
 #pragma unroll
         for (int j = 0; j < VEC; j += 4) {
           *(f4*)&mv[j] = *(const f4*)&sm.M[r][i0 + j];
           *(f4*)&bv[j] = *(const f4*)&sm.beta[i0 + j];
-          *(f4*)&gv[j] = *(const f4*)&sm.g[i0 + j];
-          *(f4*)&glv[j] = *(const f4*)&sm.gl[i0 + j];
         }
 #pragma unroll
         for (int j = 0; j < VEC; ++j) {
           const float m = upper ? 0.f : mv[j];
-          const float tv = m * bv[j];
-          te[j] = fromf<E>(tv);
-          tge[j] = fromf<E>(tv * gv[j]);
-          tgle[j] = fromf<E>(tv * glv[j]);
+          te[j] = fromf<E>(m * bv[j]);
           me[j] = fromf<E>(m);
         }
         *(uint4*)&sm.Tm[r][i0] = tr;
-        *(uint4*)&sm.am.t.Tg[r][i0] = tgr;
-        *(uint4*)&sm.am.t.Tgl[r][i0] = tglr;
-        if (wM) *(uint4*)(wM + gi * C * C + r * C + i0) = mr;
+        *(uint4*)(wM + r * C + i0) = mr;
       }
     }
     block_sync_lds();
 
-    // W = T diag(g) X = T diag(g) K + T diag(g lambda) Q (B operands: transpose
-    // reads of K and Q), staged row-major for 16-byte stores
-#pragma unroll
-    for (int tk = 0; tk < (C / 16) * (DK / 16) / NW; ++tk) {
-      const int t = w + tk * NW;
-      const int m0 = (t / (DK / 16)) * 16, n0 = (t % (DK / 16)) * 16;
-      f4 wv = zero4();
-#pragma unroll
-      for (int ks = 0; ks < C / KS; ++ks) {
-        wv = Mma<E>::mma(Frag<E>::load(kmaj(&sm.am.t.Tg[0][0], LC), m0, ks * KS, lane),
-                         tr_frag<E>(&sm.u.a.K[0][0], LK, ks * KS, n0, lane), wv);
-        wv = Mma<E>::mma(Frag<E>::load(kmaj(&sm.am.t.Tgl[0][0], LC), m0, ks * KS, lane),
-                         tr_frag<E>(&sm.u.a.Q[0][0], LK, ks * KS, n0, lane), wv);
-      }
-#pragma unroll
-      for (int j = 0; j < 4; ++j) sm.Ws[m0 + frow(lane, j)][n0 + fcol(lane)] = fromf<E>(wv[j]);
-    }
-    block_sync_lds();
-    store_tile<E, DK, NT>((E*)p.wW + gi * C * DK, &sm.Ws[0][0], LK, tid);
-    // V (K and Q are dead: W, their last reader, ended at the barrier above)
-    x.V.store(&sm.u.V[0][0], DV + P, tid);
-    block_sync_lds();
-
-    // U = T V (the B operand is a transpose read of V), stored C-fragment
-    // tiled: tile (mt, nt) at ((mt*(DV/16)+nt)*64 + lane)*4
+    // U^T = V^T T^T (A operand: transpose reads of V), stored C-fragment
+    // tiled: the block of value rows 16 nt.. and chunk columns 16 mt.. at
+    // ((mt*(DV/16)+nt)*64 + lane)*4
     E* wU = (E*)p.wU + gi * C * DV;
 #pragma unroll
     for (int tk = 0; tk < (C / 16) * (DV / 16) / NW; ++tk) {
@@ -233,91 +200,93 @@ __global__ __launch_bounds__(PREP_THREADS) void k_prep(Params p) {
       f4 uu = zero4();
 #pragma unroll
       for (int ks = 0; ks < C / KS; ++ks)
-        uu = Mma<E>::mma(Frag<E>::load(kmaj(&sm.Tm[0][0], LC), m0, ks * KS, lane),
-                         tr_frag<E>(&sm.u.V[0][0], DV + P, ks * KS, n0, lane), uu);
+        uu = Mma<E>::mma(tr_frag<E>(&sm.u.V[0][0], DV + P, ks * KS, n0, lane),
+                         Frag<E>::load(kmaj(&sm.Tm[0][0], LC), m0, ks * KS, lane), uu);
       *(typename Quad<E>::raw*)(wU + ((size_t)t * 64 + lane) * 4) = Quad<E>::pack(uu);
     }
   }
 }
 
 // Forward-scan operands of one chunk, filled by direct global->LDS loads as
-// swizzled row-major tiles, in two sets by the phase that reads them:
-//   set A (D = U - W S^T):            W (C x Dk), this tile's U fragments (byte
-//                                     copy of the C-fragment-ordered layout), b;
-//   set B (output and state update):  Q, K (C x Dk), P (C x C), b.
-// Each set has its own ring of NBUF chunks and its own producer wave.
+// swizzled row-major tiles, in sets by the phases that read them:
+//   set A (phases 2-4): Q, K (C x Dk) and the gate block (b, beta, lambda);
+//   set B (phase 3):    M = (I + A)^{-1} (C x C) and this tile's U^T
+//                       fragments (byte copy of the C-fragment-ordered layout);
+//   P (phase 4):        the output operator Gam * M_causal * Q K^T (C x C).
+// Set A has a ring of NA chunks, set B and P one buffer each.  The four
+// producer waves split every tile's 1 KB instructions evenly; producers 0-2
+// also load one gate vector each.
 template <typename E, int DK, int BV>
 struct ScanFwdRing {
   static constexpr int RK = DK * (int)sizeof(E), RC = C * (int)sizeof(E);   // row bytes
   static constexpr int NB = BV / 16;
-  static constexpr int UM = NB * 64 * 4 * (int)sizeof(E);   // U bytes per 16-row block
-  static constexpr int AW = 0, AU = AW + C * RK, AB = AU + 4 * UM, ABYTES = AB + C * 4;
-  static constexpr int BQ = 0, BK = BQ + C * RK, BP = BK + C * RK, BB = BP + C * RC, BBYTES = BB + C * 4;
-  static constexpr int NBUF = sizeof(E) == 2 ? 2 : 1;      // fp32 tiles are twice as large
-  // direct loads per chunk of each of the two producers of a set (the 1 KB
-  // instructions of every tile split evenly; producer 1 also loads b)
-  static constexpr int IA = (AB - AW) / 1024, IB = (BB - BQ) / 1024;
-  static constexpr int LOADS_A0 = IA / 2, LOADS_A1 = IA / 2 + 1, LOADS_B0 = IB / 2, LOADS_B1 = IB / 2 + 1;
-  static_assert((C * RK / 1024) % 2 == 0 && (4 * UM / 1024) % 2 == 0 && (C * RC / 1024) % 2 == 0, "even split");
-  static_assert(NBUF == 1 || (LOADS_A1 <= 63 && LOADS_B1 <= 63), "outstanding-load counter range");
+  static constexpr int UM = NB * 64 * 4 * (int)sizeof(E);   // U bytes per 16-column block
+  static constexpr int AQ = 0, AK = AQ + C * RK, AG = AK + C * RK, ABYTES = AG + 3 * C * 4;
+  static constexpr int BM = 0, BU = BM + C * RC, BBYTES = BU + 4 * UM;
+  static constexpr int NA = sizeof(E) == 2 ? 3 : 2;         // fp32 tiles are twice as large
+  static constexpr int LQ = C * RK / 1024 / 4;              // loads per producer: Q
+  static constexpr int LK = C * RK / 1024 / 4;              // K (plus one gate vector for producers 0-2)
+  static constexpr int LB = (C * RC + 4 * UM) / 1024 / 4;   // M and U
+  static constexpr int LP = C * RC / 1024 / 4;              // P
+  static_assert((C * RK / 1024) % 4 == 0 && (C * RC / 1024) % 4 == 0 && UM % 1024 == 0, "even split");
+  static_assert(2 * LB + LQ + LP + LK + 1 <= 63, "outstanding-load counter range");
 };
 
 template <typename E, int DK, int BV>
 struct alignas(16) ScanFwdSmem {
   static constexpr int P = Pad<E>::v;
   typedef ScanFwdRing<E, DK, BV> R;
-  alignas(16) char ringA[R::NBUF][R::ABYTES];
-  alignas(16) char ringB[R::NBUF][R::BBYTES];
-  E Dt[BV][C + P];    // D^T
-  E Dkt[BV][C + P];   // (diag(g_C / g) D)^T
-  union {
-    struct {
-      E S[BV][DK + P];        // state tile (MFMA operand copy)
-      E Sf[DK][BV + P];       // entry-state tile staging for the saved context ([k][v])
-    } s;
-    E O[C][BV + P];           // output tile staging (after the state copies are dead)
-  } u;
+  alignas(16) char ringA[R::NA][R::ABYTES];
+  alignas(16) char ringB[R::BBYTES];
+  alignas(16) char Pt[C * R::RC];
+  E S[BV][DK + P];    // state tile (row v, column k): MFMA operand and saved-state source
+  E Y[C][BV + P];     // Y = diag(beta g) X S^T (row r, column v)
+  E D[C][BV + P];     // D = U - M Y
+  E Dk[C][BV + P];    // diag(g_C / g) D
+  E O[C][BV + P];     // output tile staging
 };
 
 // One workgroup per (sequence, head, Dv tile of BV = 32 value rows): four
-// compute waves and four producer waves (two per operand set; one wave alone
-// issues direct loads at only about 12 bytes per clock).  Compute wave w owns rows 16w.. of
-// the chunk's D and O tiles and key rows 16 KPW w.. of the state tile S^T
-// (Dk x BV), which lives in fp32 MFMA accumulators across the whole sequence.
+// compute waves and four producer waves (one wave alone issues direct loads
+// at only about 12 bytes per clock).  The state tile S^T (Dk x BV) lives in
+// fp32 MFMA accumulators across the whole sequence; compute wave w owns its
+// key rows 16 KPW w.. and the chunk rows 16w.. of every C-row operand.
 //
-// Per chunk the compute waves pass four barriers: B1 (start), B2 (S staged),
-// B3 (D staged), B4 (outputs staged).  Producers 0-1 stream set A, 2-3 set
-// B; each issues a chunk's loads while the compute waves work on phases
-// that no longer read the buffer being refilled, so that issuing (which
-// stalls the issuing wave while the memory pipeline is busy) overlaps compute
-// instead of delaying a barrier:
-//   set A of chunk c+2 is issued after B3 of chunk c (its last reader, phase
-//   2, is over) and waited for before B2 of chunk c+2;
-//   set B of chunk c+1 is issued in two parts between B1, B2 and B3 of chunk
-//   c (its buffer was released at B4 of chunk c-1) and waited for before B3
-//   of chunk c+1.
-// The producers issue no other memory operations, so their outstanding-load
-// counts are exact.  With one buffer per set (fp32) the refills follow the
-// last reader's barrier.  When p.o is null only the states are produced.
+// The chunk step never forms W = T diag(g) X (nor P): with T = M diag(beta),
+//   W S^T = M Y,  Y = diag(beta g) (K S^T + diag(lambda) Q S^T),
+// and Q S^T also serves the output, so a chunk reads Q, K, P, M, U and the
+// gates only.  Per chunk the compute waves pass three barriers:
+//   B_a  S staged, set A visible    phase 2: saved S; S K^T, S Q^T (as their
+//                                   transposes); Y;
+//   B_b  Y staged, set B visible    phase 3: output of the previous chunk;
+//                                   D = U - M Y;
+//   B_c  D staged, P visible        phase 4: saved D; O = diag(g) Q S^T + P D
+//                                   (as O^T = g (S Q^T)^T + D^T P^T); state
+//                                   update S^T <- g_C S^T + K^T Dk; S staged.
+// Producers: Q of chunk c+NA-1 and P of chunk c in phase 2, K and gates of
+// chunk c+NA-1 in phase 3, set B of chunk c+1 in phase 4; they wait for set B
+// of chunk c in phase 2, for P in phase 3 and for set A of chunk c+1 in
+// phase 4.  They issue no other memory operations, so their outstanding-load
+// counts are exact.  When p.o is null only the states are produced.
 template <typename E, int DK, int DV, int BV>
 __global__ __launch_bounds__(NTHREADS + 256) void k_scan_fwd(Params p) {
   constexpr int P = Pad<E>::v;
-  constexpr int LK = DK + P, LC = C + P;
+  constexpr int LK = DK + P, LV = BV + P;
   constexpr int NVT = DV / BV;
   constexpr int NB = BV / 16;                 // 16-column blocks per tile
   constexpr int KS = Mma<E>::KS;
+  constexpr int NKS = DK / KS;
   static_assert(DK / 16 == 2 * NWAVES || DK / 16 == NWAVES, "key blocks per wave");
   constexpr int KPW = DK / 16 / NWAVES;       // key row blocks of S^T per wave (1 or 2)
+  constexpr size_t ES = sizeof(E);
   typedef typename Quad<E>::raw QR;
   typedef typename Mma<E>::frag FR;
   typedef ScanFwdRing<E, DK, BV> R;
-  constexpr bool DB = R::NBUF == 2;
+  constexpr int NA = R::NA;
   __shared__ ScanFwdSmem<E, DK, BV> sm;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int prod = w - NWAVES;                // 0-3 for the producer waves, negative otherwise
   const bool producer = prod >= 0;
-  const bool prodA = prod == 0 || prod == 1, prodB = prod >= 2;
-  const int wp = prod & 1;                    // producer index within its set
   int unit, vt;
   if (!xcd_unit_tile(blockIdx.x, p.N * p.H, NVT, unit, vt)) return;
   const int H = p.H, n = unit / H, h = unit % H, v0 = vt * BV;
@@ -327,49 +296,51 @@ __global__ __launch_bounds__(NTHREADS + 256) void k_scan_fwd(Params p) {
   const int nch = max(0, min((e - s + C - 1) / C, p.n_slots - base));
   const bool with_o = p.o != nullptr;
 
-  auto chunk_ptrs = [&](int c, size_t& gi, const char*& Wg, int& len, size_t& arow) {
+  auto chunk_at = [&](int c, size_t& gi, size_t& arow, int& len) {
     const int t0 = s + c * C;
     len = min(C, e - t0);
     gi = (size_t)(base + c) * H + h;
     arow = (size_t)t0 * H + h;
-    Wg = (const char*)((const E*)p.wW + gi * C * DK);
   };
-  // producers 0-1: their share of set A of chunk c into buffer buf
-  auto issueA = [&](int c, int buf) {
+  // producers: Q of chunk c (rows past the chunk re-read its last row: they
+  // only meet zero gates)
+  auto issueQ = [&](int c) {
     size_t gi, arow;
-    const char* Wg;
     int len;
-    chunk_ptrs(c, gi, Wg, len, arow);
-    char* r = sm.ringA[buf];
-    dma_rows<R::RK, C, 2, true>(r + R::AW, Wg, R::RK, C, Wg, 0, wp, lane);
-#pragma unroll
-    for (int mt = 0; mt < 4; ++mt)
-      if ((mt & 1) == wp)
-        dma_block_asm<R::UM>(r + R::AU + mt * R::UM,
-                             (const char*)((const E*)p.wU + gi * C * DV + (size_t)(mt * (DV / 16) + vt * NB) * 256),
-                             lane);
-    if (wp == 1) dma4_asm(p.wb + gi * C + lane, r + R::AB);
+    chunk_at(c, gi, arow, len);
+    const char* Qg = (const char*)((const E*)p.q + arow * DK);
+    dma_rows<R::RK, C, 4, true>(sm.ringA[c % NA] + R::AQ, Qg, (size_t)H * R::RK, len,
+                                Qg + (size_t)(len - 1) * H * R::RK, 0, prod, lane);
   };
-  // producers 2-3: their share of part `part` (0: Q, P; 1: K, b; 2: both)
-  // of set B of chunk c into buffer buf; rows of Q and K past the chunk come
-  // from W, whose rows there are zero
-  auto issueB = [&](int c, int buf, int part) {
+  // producers: K and the gate block of chunk c
+  auto issueK = [&](int c) {
     size_t gi, arow;
-    const char* Wg;
     int len;
-    chunk_ptrs(c, gi, Wg, len, arow);
-    char* r = sm.ringB[buf];
-    if (part != 1) {
-      const char* Qg = (const char*)((const E*)p.q + arow * DK);
-      const char* Pg = (const char*)((const E*)p.wP + gi * C * C);
-      dma_rows<R::RK, C, 2, true>(r + R::BQ, Qg, (size_t)H * R::RK, len, Wg, R::RK, wp, lane);
-      dma_rows<R::RC, C, 2, true>(r + R::BP, Pg, R::RC, C, Pg, 0, wp, lane);
-    }
-    if (part != 0) {
-      const char* Kg = (const char*)((const E*)p.k + arow * DK);
-      dma_rows<R::RK, C, 2, true>(r + R::BK, Kg, (size_t)H * R::RK, len, Wg, R::RK, wp, lane);
-      if (wp == 1) dma4_asm(p.wb + gi * C + lane, r + R::BB);
-    }
+    chunk_at(c, gi, arow, len);
+    char* r = sm.ringA[c % NA];
+    const char* Kg = (const char*)((const E*)p.k + arow * DK);
+    dma_rows<R::RK, C, 4, true>(r + R::AK, Kg, (size_t)H * R::RK, len, Kg + (size_t)(len - 1) * H * R::RK, 0,
+                                prod, lane);
+    if (prod < 3) dma4_asm(p.wb + gi * 3 * C + prod * C + lane, r + R::AG + prod * C * 4);
+  };
+  // producers: P of chunk c
+  auto issueP = [&](int c) {
+    size_t gi, arow;
+    int len;
+    chunk_at(c, gi, arow, len);
+    const char* Pg = (const char*)((const E*)p.wP + gi * C * C);
+    dma_rows<R::RC, C, 4, true>(sm.Pt, Pg, R::RC, C, Pg, 0, prod, lane);
+  };
+  // producers: M and this tile's U^T fragments of chunk c
+  auto issueB = [&](int c) {
+    size_t gi, arow;
+    int len;
+    chunk_at(c, gi, arow, len);
+    const char* Mg = (const char*)((const E*)p.wM + gi * C * C);
+    dma_rows<R::RC, C, 4, true>(sm.ringB + R::BM, Mg, R::RC, C, Mg, 0, prod, lane);
+    dma_block_asm<R::UM>(sm.ringB + R::BU + prod * R::UM,
+                         (const char*)((const E*)p.wU + gi * C * DV + (size_t)(prod * (DV / 16) + vt * NB) * 256),
+                         lane);
   };
 
   // state: acc[i][nb] = S^T rows 16*(KPW*w+i).., columns 16*nb.. of this tile
@@ -384,174 +355,208 @@ __global__ __launch_bounds__(NTHREADS + 256) void k_scan_fwd(Params p) {
                                       frow(lane, 0))
                        : zero4();
     }
+  // S (row v, column k) into LDS for the next chunk
+  auto stage_S = [&]() {
+#pragma unroll
+    for (int i = 0; i < KPW; ++i)
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb)
+        *(QR*)&sm.S[nb * 16 + fcol(lane)][(KPW * w + i) * 16 + frow(lane, 0)] = Quad<E>::pack(acc[i][nb]);
+  };
+  // output rows of chunk c from the staging tile
+  auto store_O = [&](int c) {
+    constexpr int VEC = 16 / sizeof(E), PR = BV / VEC;
+    const int t0 = s + c * C, len = min(C, e - t0);
+    E* obase = (E*)p.o + ((size_t)t0 * H + h) * DV + v0;
+    for (int idx = tid; idx < C * PR; idx += NTHREADS) {
+      const int r = idx / PR, cc = (idx % PR) * VEC;
+      if (r < len) *(uint4*)(obase + (size_t)r * H * DV + cc) = *(const uint4*)&sm.O[r][cc];
+    }
+  };
 
   if (nch > 0) {
-    if (prodA) {
-      issueA(0, 0);
-      if (DB && nch > 1) issueA(1, 1);
-    } else if (prodB) {
-      issueB(0, 0, 2);
+    if (producer) {
+      for (int c = 0; c < NA - 1 && c < nch; ++c) {
+        issueQ(c);
+        issueK(c);
+      }
+      issueB(0);
+      wait_vm<0>();
+    } else {
+      stage_S();
     }
   }
   for (int c = 0; c < nch; ++c) {
-    const int t0 = s + c * C, len = min(C, e - t0);
     const size_t gi = (size_t)(base + c) * H + h;
-    const int buf = DB ? (c & 1) : 0;
-    const char* ra = sm.ringA[buf];
-    const char* rb = sm.ringB[buf];
-    FR sf[NB][DK / KS];                    // S fragments (B operand of D and O)
-    block_sync_lds();                      // B1: chunk c-1 done
-    // ---- phase 1: stage S (compute); producer 1 issues the first part of set B of chunk c+1
-    if (!producer) {
-#pragma unroll
-      for (int i = 0; i < KPW; ++i)
-#pragma unroll
-        for (int nb = 0; nb < NB; ++nb) {
-          const int kt = KPW * w + i;
-          *(QR*)&sm.u.s.S[nb * 16 + fcol(lane)][kt * 16 + frow(lane, 0)] = Quad<E>::pack(acc[i][nb]);
-          if (p.saved) {
-#pragma unroll
-            for (int j = 0; j < 4; ++j)
-              sm.u.s.Sf[kt * 16 + frow(lane, j)][nb * 16 + fcol(lane)] = fromf<E>(acc[i][nb][j]);
-          }
-        }
-    } else if (prodB) {
-      if (DB && c + 1 < nch) issueB(c + 1, (c + 1) & 1, 0);
-    } else {
-      // set A of chunk c must have landed (set A of chunk c+1 may be in flight)
-      if (DB && c + 1 < nch) {
-        if (wp == 0) wait_vm<DB ? R::LOADS_A0 : 0>();
-        else wait_vm<DB ? R::LOADS_A1 : 0>();
-      } else {
-        wait_vm<0>();
-      }
-    }
-    block_sync_lds();                      // B2: S staged; set A of chunk c visible
-    // ---- phase 2: saved S, D = U - W S^T (compute); producer 1 finishes set B
+    const char* ra = sm.ringA[c % NA];
+    const float* gb = (const float*)(ra + R::AG);   // b, then beta, then lambda
+    const int rr = 16 * w + fcol(lane);             // chunk row of this lane's result columns
+    f4 sq[NB];                                      // (S Q^T) block (v-block nb, r-block w), scaled by g_r
+    block_sync_lds();                      // B_a: S staged; set A of chunk c visible
+    // ---- phase 2
     if (!producer) {
       if (p.saved) {
-        // saved entry state, transposed (element (k, v) at [k][v]), 16-byte stores
-        constexpr int VEC = 16 / sizeof(E), PR = BV / VEC;
-        E* dst = (E*)p.saved + gi * DK * DV + v0;
-        for (int idx = tid; idx < DK * PR; idx += NTHREADS) {
+        // saved entry state S (row v, column k) of this tile, 16-byte stores
+        constexpr int VEC = 16 / sizeof(E), PR = DK / VEC;
+        E* dst = (E*)p.saved + gi * DV * DK + (size_t)v0 * DK;
+        for (int idx = tid; idx < BV * PR; idx += NTHREADS) {
           const int r = idx / PR, cc = (idx % PR) * VEC;
-          *(uint4*)(dst + (size_t)r * DV + cc) = *(const uint4*)&sm.u.s.Sf[r][cc];
+          *(uint4*)(dst + (size_t)r * DK + cc) = *(const uint4*)&sm.S[r][cc];
         }
       }
-      const float* bch = (const float*)(ra + R::AB);
-      const float bl = bch[C - 1];
+      FR sa[NB][NKS];
 #pragma unroll
       for (int nb = 0; nb < NB; ++nb)
 #pragma unroll
-        for (int ks = 0; ks < DK / KS; ++ks)
-          sf[nb][ks] = Frag<E>::load(kmaj(&sm.u.s.S[0][0], LK), nb * 16, ks * KS, lane);
-      // D = U - W S^T (rows 16w..), to LDS as D^T and (diag(g_C/g) D)^T
+        for (int ks = 0; ks < NKS; ++ks) sa[nb][ks] = Frag<E>::load(kmaj(&sm.S[0][0], LK), nb * 16, ks * KS, lane);
+      // (S K^T), (S Q^T): value rows, chunk columns 16w..
+      f4 sk[NB];
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb) sk[nb] = sq[nb] = zero4();
+#pragma unroll
+      for (int ks = 0; ks < NKS; ++ks) {
+        const FR kB = tile_frag<E, R::RK>(ra + R::AK, 16 * w, ks * KS, lane);
+        const FR qB = tile_frag<E, R::RK>(ra + R::AQ, 16 * w, ks * KS, lane);
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb) {
+          sk[nb] = Mma<E>::mma(sa[nb][ks], kB, sk[nb]);
+          sq[nb] = Mma<E>::mma(sa[nb][ks], qB, sq[nb]);
+        }
+      }
+      const float br = gb[rr], gr = __expf(br), bgr = gb[C + rr] * gr, lr = gb[2 * C + rr];
+      // Y (row r, column v) = beta_r g_r ((S K^T) + lambda_r (S Q^T))^T
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb) {
+        f4 y;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          y[j] = bgr * (sk[nb][j] + lr * sq[nb][j]);
+          sq[nb][j] *= gr;
+        }
+        *(QR*)&sm.Y[rr][nb * 16 + frow(lane, 0)] = Quad<E>::pack(y);
+      }
+    } else {
+      // Q of chunk c+NA-1 (its ring slot was freed at B_a) and P of chunk c
+      // (its buffer was freed at B_a); then set B of chunk c must have landed
+      if (c + NA - 1 < nch) {
+        issueQ(c + NA - 1);
+        issueP(c);
+        wait_vm<R::LQ + R::LP>();
+      } else {
+        issueP(c);
+        wait_vm<R::LP>();
+      }
+    }
+    block_sync_lds();                      // B_b: Y staged; set B of chunk c visible
+    // ---- phase 3
+    if (!producer) {
+      if (with_o && c > 0) store_O(c - 1);
+      // D^T (value rows, chunk columns 16w..) = U^T - Y^T M^T; M is lower
+      // triangular, so k blocks past this wave's rows are skipped
+      const float kbr = __expf(gb[C - 1] - gb[rr]);
 #pragma unroll
       for (int nb = 0; nb < NB; ++nb) {
         f4 d = zero4();
 #pragma unroll
-        for (int ks = 0; ks < DK / KS; ++ks)
-          d = Mma<E>::mma(tile_frag<E, R::RK>(ra + R::AW, 16 * w, ks * KS, lane), sf[nb][ks], d);
-        const QR uq = *(const QR*)(ra + R::AU + ((w * NB + nb) * 64 + lane) * 4 * sizeof(E));
+        for (int ks = 0; ks < C / KS; ++ks)
+          if (ks * KS <= 16 * w + 15)
+            d = Mma<E>::mma(tr_frag<E>(&sm.Y[0][0], LV, ks * KS, nb * 16, lane),
+                            tile_frag<E, R::RC>(sm.ringB + R::BM, 16 * w, ks * KS, lane), d);
+        const QR uq = *(const QR*)(sm.ringB + R::BU + ((w * NB + nb) * 64 + lane) * 4 * ES);
         f4 dk;
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
           d[j] = Quad<E>::get(uq, j) - d[j];
-          dk[j] = __expf(bl - bch[16 * w + frow(lane, j)]) * d[j];
+          dk[j] = kbr * d[j];
         }
-        *(QR*)&sm.Dt[nb * 16 + fcol(lane)][16 * w + frow(lane, 0)] = Quad<E>::pack(d);
-        *(QR*)&sm.Dkt[nb * 16 + fcol(lane)][16 * w + frow(lane, 0)] = Quad<E>::pack(dk);
+        *(QR*)&sm.D[rr][nb * 16 + frow(lane, 0)] = Quad<E>::pack(d);
+        *(QR*)&sm.Dk[rr][nb * 16 + frow(lane, 0)] = Quad<E>::pack(dk);
       }
-    } else if (prodB) {
-      if (DB && c + 1 < nch) {
-        issueB(c + 1, (c + 1) & 1, 1);
-        // set B of chunk c landed; chunk c+1's in flight
-        if (wp == 0) wait_vm<DB ? R::LOADS_B0 : 0>();
-        else wait_vm<DB ? R::LOADS_B1 : 0>();
+    } else {
+      // K and gates of chunk c+NA-1; then P of chunk c must have landed
+      if (c + NA - 1 < nch) {
+        issueK(c + NA - 1);
+        if (prod < 3) wait_vm<R::LK + 1>();
+        else wait_vm<R::LK>();
       } else {
         wait_vm<0>();
       }
     }
-    block_sync_lds();                      // B3: D staged; set B of chunk c visible; set A of chunk c free
-    // ---- phase 3: saved D, O, state update (compute); producer 0 refills set A
+    block_sync_lds();                      // B_c: D staged; P visible; set B of chunk c free
+    // ---- phase 4
     if (!producer) {
       if (p.saved) {
-        // D rows of this tile into the saved context (rows past the chunk are zero),
-        // read back from D^T; one thread per (row, 8-column group)
+        // D rows of this tile into the saved context (rows past the chunk are zero)
         constexpr int VEC = 16 / sizeof(E), PR = BV / VEC;
         E* dbase = (E*)p.savedD + gi * C * DV + v0;
         for (int idx = tid; idx < C * PR; idx += NTHREADS) {
-          const int r = idx % C, cc = (idx / C) * VEC;
-          uint4 o;
-          E* oe = (E*)&o;
-#pragma unroll
-          for (int j = 0; j < VEC; ++j) oe[j] = sm.Dt[cc + j][r];
-          *(uint4*)(dbase + (size_t)r * DV + cc) = o;
+          const int r = idx / PR, cc = (idx % PR) * VEC;
+          *(uint4*)(dbase + (size_t)r * DV + cc) = *(const uint4*)&sm.D[r][cc];
         }
       }
-      const float* bch = (const float*)(rb + R::BB);
-      const float gC = __expf(bch[C - 1]);
       if (with_o) {
-        // O = diag(g) Q S^T + P D   (rows 16w..)
-        f4 oo[NB];
+        // O^T (value rows, chunk columns 16w..) = g_r (S Q^T) + D^T P^T; P is
+        // causal, so k blocks past this wave's rows are skipped
 #pragma unroll
         for (int nb = 0; nb < NB; ++nb) {
-          f4 o1 = zero4(), o2 = zero4();
-#pragma unroll
-          for (int ks = 0; ks < DK / KS; ++ks)
-            o1 = Mma<E>::mma(tile_frag<E, R::RK>(rb + R::BQ, 16 * w, ks * KS, lane), sf[nb][ks], o1);
+          f4 o = sq[nb];
 #pragma unroll
           for (int ks = 0; ks < C / KS; ++ks)
-            o2 = Mma<E>::mma(tile_frag<E, R::RC>(rb + R::BP, 16 * w, ks * KS, lane),
-                             Frag<E>::load(kmaj(&sm.Dt[0][0], LC), nb * 16, ks * KS, lane), o2);
-#pragma unroll
-          for (int j = 0; j < 4; ++j) oo[nb][j] = __expf(bch[16 * w + frow(lane, j)]) * o1[j] + o2[j];
+            if (ks * KS <= 16 * w + 15)
+              o = Mma<E>::mma(tr_frag<E>(&sm.D[0][0], LV, ks * KS, nb * 16, lane),
+                              tile_frag<E, R::RC>(sm.Pt, 16 * w, ks * KS, lane), o);
+          *(QR*)&sm.O[rr][nb * 16 + frow(lane, 0)] = Quad<E>::pack(o);
         }
-        // the state copies aliased by O were last read before B3
-#pragma unroll
-        for (int nb = 0; nb < NB; ++nb)
-#pragma unroll
-          for (int j = 0; j < 4; ++j) sm.u.O[16 * w + frow(lane, j)][nb * 16 + fcol(lane)] = fromf<E>(oo[nb][j]);
       }
       // S^T <- g_C S^T + K^T diag(g_C/g) D  (K^T fragments are transpose reads of the K tile)
+      const float gC = __expf(gb[C - 1]);
 #pragma unroll
       for (int nb = 0; nb < NB; ++nb) {
 #pragma unroll
         for (int i = 0; i < KPW; ++i) acc[i][nb] = gC * acc[i][nb];
 #pragma unroll
         for (int ks = 0; ks < C / KS; ++ks) {
-          const FR bf = Frag<E>::load(kmaj(&sm.Dkt[0][0], LC), nb * 16, ks * KS, lane);
+          const FR bf = tr_frag<E>(&sm.Dk[0][0], LV, ks * KS, nb * 16, lane);
 #pragma unroll
           for (int i = 0; i < KPW; ++i)
-            acc[i][nb] = Mma<E>::mma(tile_tr_frag<E, R::RK>(rb + R::BK, ks * KS, 16 * (KPW * w + i), lane), bf,
+            acc[i][nb] = Mma<E>::mma(tile_tr_frag<E, R::RK>(ra + R::AK, ks * KS, 16 * (KPW * w + i), lane), bf,
                                      acc[i][nb]);
         }
       }
-    } else if (prodA) {
-      if (DB && c + 2 < nch) issueA(c + 2, c & 1);
-      if (!DB && c + 1 < nch) issueA(c + 1, 0);
-    }
-    block_sync_lds();                      // B4: O staged; set B of chunk c free
-    if (prodB) {
-      if (!DB && c + 1 < nch) issueB(c + 1, 0, 2);
-    } else if (!producer && with_o) {
-      constexpr int VEC = 16 / sizeof(E), PR = BV / VEC;
-      E* obase = (E*)p.o + ((size_t)t0 * H + h) * DV + v0;
-      for (int idx = tid; idx < C * PR; idx += NTHREADS) {
-        const int r = idx / PR, cc = (idx % PR) * VEC;
-        if (r < len) *(uint4*)(obase + (size_t)r * H * DV + cc) = *(const uint4*)&sm.u.O[r][cc];
+      stage_S();
+    } else if (c + 1 < nch) {
+      issueB(c + 1);
+      // set A of chunk c+1 complete: what was issued after its last part may
+      // still be in flight
+      if constexpr (NA == 2) {
+        wait_vm<R::LB>();
+      } else {
+        if (c == 0) {
+          // set A of chunk 1 came with the prologue, which waited for it
+        } else if (c + 2 < nch) {
+          if (prod < 3) wait_vm<2 * R::LB + R::LQ + R::LP + R::LK + 1>();
+          else wait_vm<2 * R::LB + R::LQ + R::LP + R::LK>();
+        } else {
+          wait_vm<2 * R::LB + R::LP>();
+        }
       }
     }
   }
-  if (p.Sfin && !producer) {
+  block_sync_lds();                        // output of the last chunk staged
+  if (producer) {
+    wait_vm<0>();
+  } else {
+    if (with_o && nch > 0) store_O(nch - 1);
+    if (p.Sfin) {
 #pragma unroll
-    for (int i = 0; i < KPW; ++i)
+      for (int i = 0; i < KPW; ++i)
 #pragma unroll
-      for (int nb = 0; nb < NB; ++nb) {
-        const int kt = KPW * w + i;
-        *(f4*)(p.Sfin + ((size_t)unit * DV + v0 + nb * 16 + fcol(lane)) * DK + kt * 16 + frow(lane, 0)) =
-            acc[i][nb];
-      }
+        for (int nb = 0; nb < NB; ++nb) {
+          const int kt = KPW * w + i;
+          *(f4*)(p.Sfin + ((size_t)unit * DV + v0 + nb * 16 + fcol(lane)) * DK + kt * 16 + frow(lane, 0)) =
+              acc[i][nb];
+        }
+    }
   }
 }
 

@@ -45,10 +45,10 @@ def test_saved_state_slots():
 
 
 def test_saved_context_bytes():
-    # per (slot, head): Dk x Dv state, C x Dv new values D, fp32 b (C), W (C x Dk),
-    # P and M (C x C), all but b in the activation dtype
+    # per (slot, head): Dv x Dk state, C x Dv new values D, fp32 gate block
+    # (b, beta, lambda: 3 x C), P and M (C x C), all but the gates in the activation dtype
     def per_unit(Dk, Dv, e):
-        return Dk * Dv * e + 64 * Dv * e + 64 * 4 + 64 * Dk * e + 2 * 64 * 64 * e
+        return Dk * Dv * e + 64 * Dv * e + 3 * 64 * 4 + 2 * 64 * 64 * e
     assert qdelta.saved_bytes(4, 4096, 16, 128, 128, 1) == 256 * 16 * per_unit(128, 128, 2)
     assert qdelta.saved_bytes(1, 100, 2, 64, 64, 0) == 2 * 2 * per_unit(64, 64, 4)
     assert qdelta.saved_bytes(4, 4096, 16, 96, 128, 1) == 0
