@@ -42,7 +42,7 @@ namespace qd {
 //   P (phase 2):        the output operator Gam * M_causal * Q K^T (C x C);
 //   M (phase 3):        (I + A)^{-1} (C x C).
 // The transposed operands (P, M^T, Q^T, K^T, dO^T) are LDS transpose reads
-// of these tiles.  Set X has a ring of NA chunks, P two buffers and M one.
+// of these tiles.  Set X has a ring of NA chunks, P of NP and M one buffer.
 // The four producer waves split every tile's 1 KB instructions evenly;
 // producers 0-2 also load one gate vector each.
 template <typename E, int DK, int BV>
@@ -51,6 +51,7 @@ struct ScanBwdRing {
   static constexpr int XQ = 0, XK = XQ + C * RK, XO = XK + C * RK, XG = XO + C * RO, XBYTES = XG + 3 * C * 4;
   static constexpr int MBYTES = C * RC;
   static constexpr int NA = sizeof(E) == 2 ? 3 : 2;
+  static constexpr int NP = sizeof(E) == 2 ? 2 : 1;         // P buffers
   static constexpr int LQ = C * RK / 1024 / 4;              // loads per producer: Q
   static constexpr int LK = (C * RK + C * RO) / 1024 / 4;   // K and dO (plus one gate vector for producers 0-2)
   static constexpr int LM = C * RC / 1024 / 4;              // M, and P
@@ -64,10 +65,11 @@ struct alignas(16) ScanBwdSmem {
   typedef ScanBwdRing<E, DK, BV> R;
   alignas(16) char ringX[R::NA][R::XBYTES];
   alignas(16) char ringM[R::MBYTES];
-  alignas(16) char ringP[2][R::MBYTES];
+  alignas(16) char ringP[R::NP][R::MBYTES];
   E dS[BV][DK + P];   // dS' tile (row v, column k): MFMA operand and output source
   E dD[C][BV + P];    // dD (row i, column v)
-  E dV[C][BV + P];    // dV (row r, column v)
+  E z1[C][BV + P];    // diag(g) (dO - diag(lambda) dV)  (row r, column v)
+  E z2[C][BV + P];    // -diag(g) dV
 };
 
 // One workgroup per (sequence, head, Dv tile of BV = 32): four compute waves
@@ -84,13 +86,15 @@ struct alignas(16) ScanBwdSmem {
 //   B_a  dS' staged, set X, P       phase 2: dS' output; dD = P^T dO +
 //        visible                    Kbar dS'^T (as its transpose); dD staged;
 //   B_b  dD staged, set M visible   phase 3: dD output; dV = diag(beta) M^T dD
-//                                   (as its transpose); dV staged;
-//   B_c  dV staged                  phase 4: dV output; entry-state gradient;
-//                                   dS' of the next chunk staged.
-// Producers: Q of the chunk NA-1 steps ahead and P of the next chunk in phase
-// 2, K, dO and gates of the chunk NA-1 steps ahead in phase 3, M of the next
-// chunk in phase 4; they wait for M in phase 2 and for set X and P of the
-// next chunk in phase 4.
+//                                   (as its transpose), stored; the gated
+//                                   operands z1, z2 of the state gradient
+//                                   formed elementwise from dV and dO;
+//   B_c  z1, z2 staged              phase 4: entry-state gradient
+//                                   Q^T z1 + K^T z2; dS' of the next chunk staged.
+// Producers: Q of the chunk NA-1 steps ahead in phase 2, K, dO and gates of
+// that chunk in phase 3, P of the next chunk in phase 2 (two buffers) or 3
+// (one), M of the next chunk in phase 4; they wait for M in phase 2 and for
+// set X and P of the next chunk in phase 4.
 template <typename E, int DK, int DV, int BV>
 __global__ __launch_bounds__(NTHREADS + 256) void k_scan_bwd(Params p) {
   constexpr int P = Pad<E>::v;
@@ -154,7 +158,7 @@ __global__ __launch_bounds__(NTHREADS + 256) void k_scan_bwd(Params p) {
     int len;
     chunk_at(nch - 1 - it, gi, arow, len);
     const char* Pg = (const char*)((const E*)p.wP + gi * C * C);
-    dma_rows<R::RC, C, 4, true>(sm.ringP[it & 1], Pg, R::RC, C, Pg, 0, prod, lane);
+    dma_rows<R::RC, C, 4, true>(sm.ringP[it % R::NP], Pg, R::RC, C, Pg, 0, prod, lane);
   };
   auto issueM = [&](int it) {
     size_t gi, arow;
@@ -235,7 +239,7 @@ __global__ __launch_bounds__(NTHREADS + 256) void k_scan_bwd(Params p) {
 #pragma unroll
       for (int ks = 0; ks < C / KS; ++ks)
         if (ks * KS + KS > 16 * w) {
-          const FR pB = tile_tr_frag<E, R::RC>(sm.ringP[it & 1], ks * KS, 16 * w, lane);
+          const FR pB = tile_tr_frag<E, R::RC>(sm.ringP[it % R::NP], ks * KS, 16 * w, lane);
 #pragma unroll
           for (int nb = 0; nb < NB; ++nb)
             dt[nb] = Mma<E>::mma(tile_tr_frag<E, R::RO>(rx + R::XO, ks * KS, nb * 16, lane), pB, dt[nb]);
@@ -245,19 +249,16 @@ __global__ __launch_bounds__(NTHREADS + 256) void k_scan_bwd(Params p) {
 #pragma unroll
       for (int nb = 0; nb < NB; ++nb) *(QR*)&sm.dD[rr][nb * 16 + frow(lane, 0)] = Quad<E>::pack(keep * dt[nb]);
     } else {
-      // Q of the chunk NA-1 steps ahead (its ring slot was freed at B_a) and P
-      // of the next chunk (its buffer was last read in the previous phase 2);
-      // then M of this chunk must have landed
-      if (it + NA - 1 < nch) {
-        issueQ(it + NA - 1);
-        issueP(it + 1);
-        wait_vm<R::LQ + R::LM>();
-      } else if (it + 1 < nch) {
-        issueP(it + 1);
-        wait_vm<R::LM>();
-      } else {
-        wait_vm<0>();
-      }
+      // Q of the chunk NA-1 steps ahead (its ring slot was freed at B_a) and,
+      // with two P buffers, P of the next chunk (its buffer was last read in
+      // the previous phase 2); then M of this chunk must have landed
+      const bool q_next = it + NA - 1 < nch, p_next = R::NP == 2 && it + 1 < nch;
+      if (q_next) issueQ(it + NA - 1);
+      if (p_next) issueP(it + 1);
+      if (q_next && p_next) wait_vm<R::LQ + R::LM>();
+      else if (q_next) wait_vm<R::LQ>();
+      else if (p_next) wait_vm<R::LM>();
+      else wait_vm<0>();
     }
     block_sync_lds();                      // B_b: dD staged; M of this chunk visible
     // ---- phase 3
@@ -272,8 +273,12 @@ __global__ __launch_bounds__(NTHREADS + 256) void k_scan_bwd(Params p) {
         }
       }
       // dV^T (value rows, chunk columns 16w..) = beta_r (dD^T M); M is lower
-      // triangular, so k blocks before this wave's rows are skipped
-      const float betar = gb[C + rr];
+      // triangular, so k blocks before this wave's rows are skipped.  Each
+      // lane holds four consecutive values of row rr: dV goes out directly,
+      // and z1 = g_r (dO - lambda_r dV), z2 = -g_r dV are formed here, where
+      // the wave's own rows cover the tile once.
+      const float betar = gb[C + rr], gr = __expf(gb[rr]), lr = gb[2 * C + rr];
+      E* vrow = (E*)p.dv + ((size_t)(t0 + rr) * H + h) * DV + v0;
 #pragma unroll
       for (int nb = 0; nb < NB; ++nb) {
         f4 dv = zero4();
@@ -282,26 +287,27 @@ __global__ __launch_bounds__(NTHREADS + 256) void k_scan_bwd(Params p) {
           if (ks * KS + KS > 16 * w)
             dv = Mma<E>::mma(tr_frag<E>(&sm.dD[0][0], LV, ks * KS, nb * 16, lane),
                              tile_tr_frag<E, R::RC>(sm.ringM, ks * KS, 16 * w, lane), dv);
+        const int v = nb * 16 + frow(lane, 0);
+        const QR doq = *(const QR*)(rx + R::XO + tile_off<R::RO>(rr, v * (int)sizeof(E)));
+        f4 a, b;
 #pragma unroll
-        for (int j = 0; j < 4; ++j) dv[j] *= betar;
-        *(QR*)&sm.dV[rr][nb * 16 + frow(lane, 0)] = Quad<E>::pack(dv);
+        for (int j = 0; j < 4; ++j) {
+          dv[j] *= betar;
+          a[j] = gr * (Quad<E>::get(doq, j) - lr * dv[j]);
+          b[j] = -gr * dv[j];
+        }
+        if (rr < len) *(QR*)(vrow + v) = Quad<E>::pack(dv);
+        *(QR*)&sm.z1[rr][v] = Quad<E>::pack(a);
+        *(QR*)&sm.z2[rr][v] = Quad<E>::pack(b);
       }
     } else {
       if (it + NA - 1 < nch) issueK(it + NA - 1);
+      if (R::NP == 1 && it + 1 < nch) issueP(it + 1);   // its buffer was last read in phase 2
     }
-    block_sync_lds();                      // B_c: dV staged; M of this chunk free
+    block_sync_lds();                      // B_c: z1, z2 staged; M of this chunk free
     // ---- phase 4
     if (!producer) {
-      {
-        constexpr int VEC = 16 / sizeof(E), PR = BV / VEC;
-        E* vdst = (E*)p.dv + ((size_t)t0 * H + h) * DV + v0;
-        for (int idx = tid; idx < C * PR; idx += NTHREADS) {
-          const int r = idx / PR, cc = (idx % PR) * VEC;
-          if (r < len) *(uint4*)(vdst + (size_t)r * H * DV + cc) = *(const uint4*)&sm.dV[r][cc];
-        }
-      }
-      // dS_entry^T = g_C dS'^T + Q^T diag(g) (dO - diag(lambda) dV) - K^T diag(g) dV;
-      // the gates scale the B fragments along the contracted token index
+      // dS_entry^T = g_C dS'^T + Q^T z1 + K^T z2
       const float gC = __expf(gb[C - 1]);
 #pragma unroll
       for (int i = 0; i < KPW; ++i)
@@ -309,34 +315,20 @@ __global__ __launch_bounds__(NTHREADS + 256) void k_scan_bwd(Params p) {
         for (int nb = 0; nb < NB; ++nb) acc[i][nb] = gC * acc[i][nb];
 #pragma unroll
       for (int ks = 0; ks < C / KS; ++ks) {
-        float gk[KPL], lk[KPL];
+        FR qa[KPW], ka[KPW];
 #pragma unroll
-        for (int e2 = 0; e2 < KPL; ++e2) {
-          const int r = ks * KS + (lane >> 4) * KPL + e2;
-          gk[e2] = __expf(gb[r]);
-          lk[e2] = gb[2 * C + r];
+        for (int i = 0; i < KPW; ++i) {
+          qa[i] = tile_tr_frag<E, R::RK>(rx + R::XQ, ks * KS, 16 * (KPW * w + i), lane);
+          ka[i] = tile_tr_frag<E, R::RK>(rx + R::XK, ks * KS, 16 * (KPW * w + i), lane);
         }
 #pragma unroll
         for (int nb = 0; nb < NB; ++nb) {
-          const FR fo = tile_tr_frag<E, R::RO>(rx + R::XO, ks * KS, nb * 16, lane);
-          const FR fv = tr_frag<E>(&sm.dV[0][0], LV, ks * KS, nb * 16, lane);
-          FR z1, z2;
-          const E* oe = (const E*)&fo;
-          const E* ve = (const E*)&fv;
-          E* z1e = (E*)&z1;
-          E* z2e = (E*)&z2;
-#pragma unroll
-          for (int e2 = 0; e2 < KPL; ++e2) {
-            const float dvv = tof(ve[e2]);
-            z1e[e2] = fromf<E>(gk[e2] * (tof(oe[e2]) - lk[e2] * dvv));
-            z2e[e2] = fromf<E>(-gk[e2] * dvv);
-          }
+          const FR z1 = tr_frag<E>(&sm.z1[0][0], LV, ks * KS, nb * 16, lane);
+          const FR z2 = tr_frag<E>(&sm.z2[0][0], LV, ks * KS, nb * 16, lane);
 #pragma unroll
           for (int i = 0; i < KPW; ++i) {
-            acc[i][nb] = Mma<E>::mma(tile_tr_frag<E, R::RK>(rx + R::XQ, ks * KS, 16 * (KPW * w + i), lane), z1,
-                                     acc[i][nb]);
-            acc[i][nb] = Mma<E>::mma(tile_tr_frag<E, R::RK>(rx + R::XK, ks * KS, 16 * (KPW * w + i), lane), z2,
-                                     acc[i][nb]);
+            acc[i][nb] = Mma<E>::mma(qa[i], z1, acc[i][nb]);
+            acc[i][nb] = Mma<E>::mma(ka[i], z2, acc[i][nb]);
           }
         }
       }
@@ -346,7 +338,7 @@ __global__ __launch_bounds__(NTHREADS + 256) void k_scan_bwd(Params p) {
       // set X and P of the next chunk complete: what was issued after the
       // later of their last parts may still be in flight
       if constexpr (NA == 2) {
-        wait_vm<R::LM>();                  // P, then K: only M follows
+        wait_vm<R::LM>();                  // K and P were issued last before M
       } else {
         if (it + 2 < nch) {                // P issued after K of the next chunk: K ahead and M follow
           if (prod < 3) wait_vm<R::LK + 1 + R::LM>();

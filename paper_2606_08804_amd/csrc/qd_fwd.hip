@@ -213,7 +213,7 @@ __global__ __launch_bounds__(PREP_THREADS) void k_prep(Params p) {
 //   set B (phase 3):    M = (I + A)^{-1} (C x C) and this tile's U^T
 //                       fragments (byte copy of the C-fragment-ordered layout);
 //   P (phase 4):        the output operator Gam * M_causal * Q K^T (C x C).
-// Set A has a ring of NA chunks, set B and P one buffer each.  The four
+// Set A has a ring of NA chunks, P of NP, set B one buffer.  The four
 // producer waves split every tile's 1 KB instructions evenly; producers 0-2
 // also load one gate vector each.
 template <typename E, int DK, int BV>
@@ -224,12 +224,13 @@ struct ScanFwdRing {
   static constexpr int AQ = 0, AK = AQ + C * RK, AG = AK + C * RK, ABYTES = AG + 3 * C * 4;
   static constexpr int BM = 0, BU = BM + C * RC, BBYTES = BU + 4 * UM;
   static constexpr int NA = sizeof(E) == 2 ? 3 : 2;         // fp32 tiles are twice as large
+  static constexpr int NP = sizeof(E) == 2 ? 2 : 1;         // P buffers
   static constexpr int LQ = C * RK / 1024 / 4;              // loads per producer: Q
   static constexpr int LK = C * RK / 1024 / 4;              // K (plus one gate vector for producers 0-2)
   static constexpr int LB = (C * RC + 4 * UM) / 1024 / 4;   // M and U
   static constexpr int LP = C * RC / 1024 / 4;              // P
   static_assert((C * RK / 1024) % 4 == 0 && (C * RC / 1024) % 4 == 0 && UM % 1024 == 0, "even split");
-  static_assert(2 * LB + LQ + LP + LK + 1 <= 63, "outstanding-load counter range");
+  static_assert(2 * LB + LQ + LP + 2 * (LK + 1) <= 63, "outstanding-load counter range");
 };
 
 template <typename E, int DK, int BV>
@@ -238,7 +239,7 @@ struct alignas(16) ScanFwdSmem {
   typedef ScanFwdRing<E, DK, BV> R;
   alignas(16) char ringA[R::NA][R::ABYTES];
   alignas(16) char ringB[R::BBYTES];
-  alignas(16) char Pt[C * R::RC];
+  alignas(16) char Pt[R::NP][C * R::RC];
   E S[BV][DK + P];    // state tile (row v, column k): MFMA operand and saved-state source
   E Y[C][BV + P];     // Y = diag(beta g) X S^T (row r, column v)
   E D[C][BV + P];     // D = U - M Y
@@ -263,10 +264,10 @@ struct alignas(16) ScanFwdSmem {
 //   B_c  D staged, P visible        phase 4: saved D; O = diag(g) Q S^T + P D
 //                                   (as O^T = g (S Q^T)^T + D^T P^T); state
 //                                   update S^T <- g_C S^T + K^T Dk; S staged.
-// Producers: Q of chunk c+NA-1 and P of chunk c in phase 2, K and gates of
-// chunk c+NA-1 in phase 3, set B of chunk c+1 in phase 4; they wait for set B
-// of chunk c in phase 2, for P in phase 3 and for set A of chunk c+1 in
-// phase 4.  They issue no other memory operations, so their outstanding-load
+// Producers: Q of chunk c+NA-1 and P of chunk c+NP-1 in phase 2, K and gates
+// of chunk c+NA-1 in phase 3, set B of chunk c+1 in phase 4; they wait for
+// set B of chunk c in phase 2, for P of chunk c in phase 3 and for set A of
+// chunk c+1 in phase 4.  They issue no other memory operations, so their outstanding-load
 // counts are exact.  When p.o is null only the states are produced.
 template <typename E, int DK, int DV, int BV>
 __global__ __launch_bounds__(NTHREADS + 256) void k_scan_fwd(Params p) {
@@ -329,7 +330,7 @@ __global__ __launch_bounds__(NTHREADS + 256) void k_scan_fwd(Params p) {
     int len;
     chunk_at(c, gi, arow, len);
     const char* Pg = (const char*)((const E*)p.wP + gi * C * C);
-    dma_rows<R::RC, C, 4, true>(sm.Pt, Pg, R::RC, C, Pg, 0, prod, lane);
+    dma_rows<R::RC, C, 4, true>(sm.Pt[c % R::NP], Pg, R::RC, C, Pg, 0, prod, lane);
   };
   // producers: M and this tile's U^T fragments of chunk c
   auto issueB = [&](int c) {
@@ -380,6 +381,7 @@ __global__ __launch_bounds__(NTHREADS + 256) void k_scan_fwd(Params p) {
         issueQ(c);
         issueK(c);
       }
+      if (R::NP == 2) issueP(0);
       issueB(0);
       wait_vm<0>();
     } else {
@@ -436,16 +438,15 @@ __global__ __launch_bounds__(NTHREADS + 256) void k_scan_fwd(Params p) {
         *(QR*)&sm.Y[rr][nb * 16 + frow(lane, 0)] = Quad<E>::pack(y);
       }
     } else {
-      // Q of chunk c+NA-1 (its ring slot was freed at B_a) and P of chunk c
-      // (its buffer was freed at B_a); then set B of chunk c must have landed
-      if (c + NA - 1 < nch) {
-        issueQ(c + NA - 1);
-        issueP(c);
-        wait_vm<R::LQ + R::LP>();
-      } else {
-        issueP(c);
-        wait_vm<R::LP>();
-      }
+      // Q of chunk c+NA-1 (its ring slot was freed at B_a) and P of chunk
+      // c+NP-1 (its buffer was last read in the previous phase 4); then set B
+      // of chunk c must have landed
+      const bool q_next = c + NA - 1 < nch, p_next = c + R::NP - 1 < nch;
+      if (q_next) issueQ(c + NA - 1);
+      if (p_next) issueP(c + R::NP - 1);
+      if (q_next && p_next) wait_vm<R::LQ + R::LP>();
+      else if (p_next) wait_vm<R::LP>();
+      else wait_vm<0>();
     }
     block_sync_lds();                      // B_b: Y staged; set B of chunk c visible
     // ---- phase 3
@@ -474,12 +475,25 @@ __global__ __launch_bounds__(NTHREADS + 256) void k_scan_fwd(Params p) {
       }
     } else {
       // K and gates of chunk c+NA-1; then P of chunk c must have landed
-      if (c + NA - 1 < nch) {
-        issueK(c + NA - 1);
-        if (prod < 3) wait_vm<R::LK + 1>();
+      const bool k_next = c + NA - 1 < nch;
+      if (k_next) issueK(c + NA - 1);
+      if constexpr (R::NP == 1) {
+        // issued in this chunk's phase 2: only the K loads follow
+        if (!k_next) wait_vm<0>();
+        else if (prod < 3) wait_vm<R::LK + 1>();
         else wait_vm<R::LK>();
-      } else {
-        wait_vm<0>();
+      } else if (c > 0) {
+        // issued in the previous phase 2; followed by K of chunk c+1, set B
+        // of chunk c, Q of chunk c+2, P of chunk c+1 and K of chunk c+2
+        if (k_next) {
+          if (prod < 3) wait_vm<R::LB + R::LQ + R::LP + 2 * (R::LK + 1)>();
+          else wait_vm<R::LB + R::LQ + R::LP + 2 * R::LK>();
+        } else if (c + 1 < nch) {
+          if (prod < 3) wait_vm<R::LB + R::LP + R::LK + 1>();
+          else wait_vm<R::LB + R::LP + R::LK>();
+        } else {
+          wait_vm<R::LB>();
+        }
       }
     }
     block_sync_lds();                      // B_c: D staged; P visible; set B of chunk c free
@@ -504,23 +518,26 @@ __global__ __launch_bounds__(NTHREADS + 256) void k_scan_fwd(Params p) {
           for (int ks = 0; ks < C / KS; ++ks)
             if (ks * KS <= 16 * w + 15)
               o = Mma<E>::mma(tr_frag<E>(&sm.D[0][0], LV, ks * KS, nb * 16, lane),
-                              tile_frag<E, R::RC>(sm.Pt, 16 * w, ks * KS, lane), o);
+                              tile_frag<E, R::RC>(sm.Pt[c % R::NP], 16 * w, ks * KS, lane), o);
           *(QR*)&sm.O[rr][nb * 16 + frow(lane, 0)] = Quad<E>::pack(o);
         }
       }
       // S^T <- g_C S^T + K^T diag(g_C/g) D  (K^T fragments are transpose reads of the K tile)
       const float gC = __expf(gb[C - 1]);
 #pragma unroll
-      for (int nb = 0; nb < NB; ++nb) {
+      for (int i = 0; i < KPW; ++i)
 #pragma unroll
-        for (int i = 0; i < KPW; ++i) acc[i][nb] = gC * acc[i][nb];
+        for (int nb = 0; nb < NB; ++nb) acc[i][nb] = gC * acc[i][nb];
 #pragma unroll
-        for (int ks = 0; ks < C / KS; ++ks) {
+      for (int ks = 0; ks < C / KS; ++ks) {
+        FR ka[KPW];
+#pragma unroll
+        for (int i = 0; i < KPW; ++i) ka[i] = tile_tr_frag<E, R::RK>(ra + R::AK, ks * KS, 16 * (KPW * w + i), lane);
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb) {
           const FR bf = tr_frag<E>(&sm.Dk[0][0], LV, ks * KS, nb * 16, lane);
 #pragma unroll
-          for (int i = 0; i < KPW; ++i)
-            acc[i][nb] = Mma<E>::mma(tile_tr_frag<E, R::RK>(ra + R::AK, ks * KS, 16 * (KPW * w + i), lane), bf,
-                                     acc[i][nb]);
+          for (int i = 0; i < KPW; ++i) acc[i][nb] = Mma<E>::mma(ka[i], bf, acc[i][nb]);
         }
       }
       stage_S();
