@@ -395,7 +395,7 @@ struct alignas(16) BwdSmem {
   float b[C], g[C], kb[C], beta[C], lam[C], db[C], dbeta[C];
   float rsum[5][2][C];      // per-row partial sums of the two column halves:
                             // dbeta rows, decay rows (B2); decay, Kbar, dlambda rows (B3)
-  float sdot[2];
+  float sdot[8];            // per-wave parts of <dS', S>
   union {
     alignas(16) char tiles[TileA<E, DK>::NBUF][TileA<E, DK>::BYTES];   // phase A
     struct {
@@ -473,12 +473,11 @@ __global__ __launch_bounds__(INTRA_THREADS) void k_bwd_intra(Params p) {
 
   // ---------------- phase A: contractions over the value dimension
   typedef TileA<E, DK> TA;
-  f4 aQ[HK], aK[HK], aW[HK], aP[2], aT[2];
+  f4 aQ[HK], aK[HK], aW[HK], aP[2], aT[2], asd = zero4();
 #pragma unroll
   for (int i = 0; i < HK; ++i) aQ[i] = aK[i] = aW[i] = zero4();
 #pragma unroll
   for (int i = 0; i < 2; ++i) aP[i] = aT[i] = zero4();
-  float sdot = 0.f;
   constexpr size_t ES = sizeof(E);
   const char* Sg = (const char*)((const E*)p.saved + gi * DK * DV);
   const char* dSg = (const char*)((const E*)p.w_dSo + gi * DK * DV);
@@ -557,12 +556,6 @@ __global__ __launch_bounds__(INTRA_THREADS) void k_bwd_intra(Params p) {
         aQ[i] = Mma<E>::mma(aO, bS, aQ[i]);
         aW[i] = Mma<E>::mma(adD, bS, aW[i]);
         aK[i] = Mma<E>::mma(aD, bdS, aK[i]);
-        if (rb == 0) {
-          const E* se = (const E*)&bS;
-          const E* de = (const E*)&bdS;
-#pragma unroll
-          for (int e = 0; e < Mma<E>::KPL; ++e) sdot += tof(se[e]) * tof(de[e]);
-        }
       }
 #pragma unroll
       for (int i = 0; i < 2; ++i) {
@@ -573,11 +566,23 @@ __global__ __launch_bounds__(INTRA_THREADS) void k_bwd_intra(Params p) {
         aT[i] = Mma<E>::mma(adD, bV, aT[i]);
       }
     }
+    // <dS', S> = trace(S dS'^T): wave w adds the diagonal 16 x 16 block
+    // (w & 1) of this tile's S dS'^T over the key steps w >> 1, +4, ...
+#pragma unroll
+    for (int ks = 0; ks < DK / KS; ks += 4)
+      if (ks + (w >> 1) < DK / KS)
+        asd = Mma<E>::mma(tile_frag<E, TA::RK>(t + TA::S, 16 * (w & 1), (ks + (w >> 1)) * KS, lane),
+                          tile_frag<E, TA::RK>(t + TA::DS, 16 * (w & 1), (ks + (w >> 1)) * KS, lane), asd);
   }
-  // the two row-block-0 waves together read all of S and dS' once
-  if (rb == 0) {
+  {
+    // diagonal elements of the accumulated block: row 4 (l >> 4) + j == column l & 15
+    const int j = (lane & 15) - 4 * (lane >> 4);
+    float sdot = 0.f;
+#pragma unroll
+    for (int jj = 0; jj < 4; ++jj)
+      if (jj == j) sdot = asd[jj];
     sdot = wave_sum(sdot);
-    if (lane == 0) sm.sdot[ch] = sdot;
+    if (lane == 0) sm.sdot[w] = sdot;
   }
   if (tid < C) {
     sm.b[tid] = gb;
@@ -844,7 +849,12 @@ __global__ __launch_bounds__(INTRA_THREADS) void k_bwd_intra(Params p) {
 #pragma unroll
     for (int off = 32; off >= 1; off >>= 1) tot += __shfl_xor(tot, off, 64);
     float dbj = sm.db[j] + sm.rsum[2][0][j] + sm.rsum[2][1][j] - tk;
-    if (j == C - 1) dbj += tot + sm.g[C - 1] * (sm.sdot[0] + sm.sdot[1]);
+    if (j == C - 1) {
+      float sd = 0.f;
+#pragma unroll
+      for (int q = 0; q < 8; ++q) sd += sm.sdot[q];
+      dbj += tot + sm.g[C - 1] * sd;
+    }
     float x = __shfl(dbj, C - 1 - j, 64);
     x = wave_incl_scan(x, lane);
     const float suffix = __shfl(x, C - 1 - j, 64);
