@@ -51,16 +51,15 @@
  * Saved context (written by the forward, read by the backward)
  * --------------------------------------------------------------
  *  A caller-owned device buffer of qdelta_saved_bytes() bytes (16-byte
- *  aligned) with six regions, one after the other, each indexed by unit
+ *  aligned) with five regions, one after the other, each indexed by unit
  *  u = slot * H + h (U = n_slots * H units):
- *    states  dtype [U, Dk, Dv]: the transposed entry state S^T of the chunk
- *            (element (k, v) = S[v][k]), rounded to the activation dtype (the
- *            backward's products take it as an MFMA operand of that type);
+ *    states  dtype [U, Dv, Dk]: the entry state S of the chunk, rounded to
+ *            the activation dtype (the backward's products take it as an MFMA
+ *            operand of that type);
  *    D       dtype [U, C, Dv]: the chunk's "new values" D = U - W S^T
  *            (App. D, WY form), rows >= the chunk's length zero;
- *    b       float32 [U, C]: chunk-local prefix sums of log alpha;
- *    W       dtype [U, C, Dk]: W = T diag(g) X of the WY form, rows >= the
- *            chunk's length zero;
+ *    gates   float32 [U, 3, C]: chunk-local prefix sums b of log alpha, then
+ *            beta and lambda (zero past the chunk's length);
  *    P       dtype [U, C, C]: the intra-chunk output operator
  *            Gam * M * (Q K^T) (Sec. 3.3 chunkwise form);
  *    M       dtype [U, C, C]: (I + A)^{-1} of the UT transform (App. D.2),

@@ -16,7 +16,7 @@ using qd::C;
 constexpr int kVersion = 10000;  // 1.0.0
 
 struct Layout {
-  size_t wb = 0, wU = 0, wP = 0, wM = 0;   // forward: chunk factors when no saved context is kept
+  size_t wb = 0, wT = 0, wP = 0, wM = 0;   // forward: chunk factors (T always, the rest when no saved context is kept)
   size_t dSo = 0, dDb = 0, ctx = 0;        // backward: scan outputs, room to recompute the context
   size_t total = 0;
 };
@@ -46,7 +46,7 @@ Layout make_layout(size_t units, int Dk, int Dv, int esz, bool bwd) {
     off += (bytes + 255) & ~size_t(255);
     return at;
   };
-  L.wU = take(units * C * Dv * esz);
+  L.wT = take(units * C * C * esz);
   if (bwd) {
     L.dSo = take(units * (size_t)Dv * Dk * esz);
     L.dDb = take(units * C * Dv * esz);
@@ -154,7 +154,7 @@ int fwd_impl(bool varlen, int32_t B, int32_t T, int32_t N, const int32_t* cu, in
   p.o = has_tokens ? o : nullptr;
   p.Sfin = final_state;
   const size_t units = s.slots * (size_t)H;
-  p.wU = w + L.wU;
+  p.wT = w + L.wT;
   if (saved) {
     bind_ctx(p, static_cast<char*>(saved), units, Dk, Dv, esz);
   } else {
@@ -216,7 +216,7 @@ int bwd_impl(bool varlen, int32_t B, int32_t T, int32_t N, const int32_t* cu, in
   } else {
     // recompute the saved context (no outputs) into the workspace
     bind_ctx(p, w + L.ctx, units, Dk, Dv, esz);
-    p.wU = w + L.wU;
+    p.wT = w + L.wT;
     e = qd::launch_fwd(p, dtype, Dk, Dv, 1, 1, stream);
     if (e != hipSuccess) return QDELTA_EHIP;
   }

@@ -591,9 +591,9 @@ struct Params {
   // context when one is kept, else in the workspace)
   float* wb;             // [slot][H][3][C] gate block: chunk-local prefix sums b of
                          // log alpha, beta, lambda (beta, lambda zero past the chunk)
-  void* wU;              // [slot][H] U^T (Dv x C), C-fragment tiled (workspace only)
   void* wP;              // [slot][H][C][C]   P = Gam * M_causal * Q K^T
   void* wM;              // [slot][H][C][C]   M = (I + A)^{-1}
+  void* wT;              // [slot][H][C][C]   T = M diag(beta) (workspace only)
   // backward
   const void* dO;
   const float* dSfin;

@@ -27,29 +27,23 @@
 
 namespace qd {
 
-template <typename E, int DK, int DV>
+template <typename E, int DK>
 struct alignas(16) PrepSmem {
   static constexpr int P = Pad<E>::v;
   alignas(16) float b[C], beta[C], lam[C];
-  union {
-    struct {
-      E K[C][DK + P];
-      E Q[C][DK + P];
-    } a;
-    E V[C][DV + P];           // after the Gram products, the last readers of K and Q
-  } u;
+  E K[C][DK + P];
+  E Q[C][DK + P];
   float A[C][C + 4];          // strictly lower A, consumed by the solve
   alignas(16) float M[C][C + 4];
-  E Tm[C][C + P];             // P staging during the Gram products, then T = M diag(beta)
+  E Pm[C][C + P];             // P staging
 };
 
 // Raw inputs of one (chunk, head) unit, staged in registers one unit ahead.
 constexpr int PREP_THREADS = 512;   // 8 waves: two per SIMD hide each other's latency
 
-template <typename E, int DK, int DV>
+template <typename E, int DK>
 struct PrepPre {
   TileRegs<E, C, DK, PREP_THREADS> K, Q;
-  TileRegs<E, C, DV, PREP_THREADS> V;
   float la, beta, lam;
   int t0, len, g, h;
   bool valid;
@@ -67,7 +61,8 @@ __device__ inline void store_tile(E* dst, const E* src, int ld, int tid) {
 }
 
 // Writes, for every unit, the gate block (b, beta, lambda), the intra-chunk
-// output operator P = Gam * M_causal * Q K^T, M = (I + A)^{-1} and U^T = (T V)^T.  Persistent: each workgroup walks units blockIdx.x,
+// output operator P = Gam * M_causal * Q K^T, M = (I + A)^{-1} and
+// T = M diag(beta).  Persistent: each workgroup walks units blockIdx.x,
 // +gridDim.x, ... and prefetches the next unit's inputs into registers while
 // computing the current one.
 template <typename E, int DK, int DV>
@@ -75,9 +70,8 @@ __global__ __launch_bounds__(PREP_THREADS) void k_prep(Params p) {
   constexpr int NT = PREP_THREADS, NW = NT / 64;
   constexpr int P = Pad<E>::v;
   constexpr int LK = DK + P, LC = C + P;
-  constexpr int KS = Mma<E>::KS;
-  typedef PrepPre<E, DK, DV> Pre;
-  __shared__ PrepSmem<E, DK, DV> sm;
+  typedef PrepPre<E, DK> Pre;
+  __shared__ PrepSmem<E, DK> sm;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int H = p.H;
   const int total = p.n_slots * H;
@@ -93,7 +87,6 @@ __global__ __launch_bounds__(PREP_THREADS) void k_prep(Params p) {
     const size_t row = (size_t)x.t0 * H + x.h;
     x.K.load((const E*)p.k + row * DK, (size_t)H * DK, x.len, tid);
     x.Q.load((const E*)p.q + row * DK, (size_t)H * DK, x.len, tid);
-    x.V.load((const E*)p.v + row * DV, (size_t)H * DV, x.len, tid);
     if (tid < C) {
       const bool ok = tid < x.len;
       const size_t gt = row + (size_t)tid * H;
@@ -112,8 +105,8 @@ __global__ __launch_bounds__(PREP_THREADS) void k_prep(Params p) {
     const int h = x.h;
     const size_t gi = (size_t)x.g * H + h;
     block_sync_lds();                        // previous unit's LDS use is over
-    x.K.store(&sm.u.a.K[0][0], LK, tid);
-    x.Q.store(&sm.u.a.Q[0][0], LK, tid);
+    x.K.store(&sm.K[0][0], LK, tid);
+    x.Q.store(&sm.Q[0][0], LK, tid);
     if (tid < C) {
       const float b = wave_incl_scan(x.la, lane);
       sm.b[tid] = b;
@@ -128,7 +121,7 @@ __global__ __launch_bounds__(PREP_THREADS) void k_prep(Params p) {
     block_sync_lds();
 
     // A = strictLower(diag(beta) Gam * X K^T), X K^T = K K^T + diag(lambda) Q K^T,
-    // and P (staged in Tm)
+    // and P (staged in Pm)
 #pragma unroll
     for (int tk = 0; tk < 16 / NW; ++tk) {
       const int t = w + tk * NW;
@@ -142,35 +135,33 @@ __global__ __launch_bounds__(PREP_THREADS) void k_prep(Params p) {
         betr[j] = sm.beta[r];
         lr[j] = sm.lam[r];
       }
-      const f4 kk = mma_k<E, DK>(kmaj(&sm.u.a.K[0][0], LK), kmaj(&sm.u.a.K[0][0], LK), m0, n0, zero4(), lane);
-      const f4 qk = mma_k<E, DK>(kmaj(&sm.u.a.Q[0][0], LK), kmaj(&sm.u.a.K[0][0], LK), m0, n0, zero4(), lane);
+      const f4 kk = mma_k<E, DK>(kmaj(&sm.K[0][0], LK), kmaj(&sm.K[0][0], LK), m0, n0, zero4(), lane);
+      const f4 qk = mma_k<E, DK>(kmaj(&sm.Q[0][0], LK), kmaj(&sm.K[0][0], LK), m0, n0, zero4(), lane);
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
         const int r = m0 + frow(lane, j);
         const float gam = (r >= i) ? __expf(br[j] - bi) : 0.f;
         sm.A[r][i] = (r > i) ? betr[j] * gam * (kk[j] + lr[j] * qk[j]) : 0.f;
-        sm.Tm[r][i] = fromf<E>(gam * qk[j]);
+        sm.Pm[r][i] = fromf<E>(gam * qk[j]);
       }
     }
     block_sync_lds();
-    // V (K and Q are dead: the Gram products ended at the barrier above); P
-    // out before the solve, whose barriers order the later T writes to Tm
-    x.V.store(&sm.u.V[0][0], DV + P, tid);
-    store_tile<E, C, NT>((E*)p.wP + gi * C * C, &sm.Tm[0][0], LC, tid);
+    store_tile<E, C, NT>((E*)p.wP + gi * C * C, &sm.Pm[0][0], LC, tid);
 
-    // UT solve: M = (I + A)^{-1} (its barriers also order the V stores)
+    // UT solve: M = (I + A)^{-1}; M and T = M diag(beta) are stored with
+    // strictly-upper 16 x 16 blocks zero; a thread takes VEC consecutive
+    // columns of one row
     unit_lower_inverse<NT>(&sm.A[0][0], C + 4, &sm.M[0][0], C + 4, tid);
     {
-      // T = M diag(beta) into LDS and M to global; a thread takes VEC
-      // consecutive columns of one row
       constexpr int VEC = 16 / sizeof(E);
       E* wM = (E*)p.wM + gi * C * C;
+      E* wT = (E*)p.wT + gi * C * C;
       for (int idx = tid; idx < C * C / VEC; idx += NT) {
         const int r = idx / (C / VEC), i0 = (idx % (C / VEC)) * VEC;
-        const bool upper = (i0 >> 4) > (r >> 4);   // strictly-upper block: zero
-        uint4 tr, mr;
-        E* te = (E*)&tr;
+        const bool upper = (i0 >> 4) > (r >> 4);
+        uint4 mr, tr;
         E* me = (E*)&mr;
+        E* te = (E*)&tr;
         float mv[VEC], bv[VEC];
 #pragma unroll
         for (int j = 0; j < VEC; j += 4) {
@@ -180,29 +171,12 @@ __global__ __launch_bounds__(PREP_THREADS) void k_prep(Params p) {
 #pragma unroll
         for (int j = 0; j < VEC; ++j) {
           const float m = upper ? 0.f : mv[j];
-          te[j] = fromf<E>(m * bv[j]);
           me[j] = fromf<E>(m);
+          te[j] = fromf<E>(m * bv[j]);
         }
-        *(uint4*)&sm.Tm[r][i0] = tr;
         *(uint4*)(wM + r * C + i0) = mr;
+        *(uint4*)(wT + r * C + i0) = tr;
       }
-    }
-    block_sync_lds();
-
-    // U^T = V^T T^T (A operand: transpose reads of V), stored C-fragment
-    // tiled: the block of value rows 16 nt.. and chunk columns 16 mt.. at
-    // ((mt*(DV/16)+nt)*64 + lane)*4
-    E* wU = (E*)p.wU + gi * C * DV;
-#pragma unroll
-    for (int tk = 0; tk < (C / 16) * (DV / 16) / NW; ++tk) {
-      const int t = w + tk * NW;
-      const int m0 = (t / (DV / 16)) * 16, n0 = (t % (DV / 16)) * 16;
-      f4 uu = zero4();
-#pragma unroll
-      for (int ks = 0; ks < C / KS; ++ks)
-        uu = Mma<E>::mma(tr_frag<E>(&sm.u.V[0][0], DV + P, ks * KS, n0, lane),
-                         Frag<E>::load(kmaj(&sm.Tm[0][0], LC), m0, ks * KS, lane), uu);
-      *(typename Quad<E>::raw*)(wU + ((size_t)t * 64 + lane) * 4) = Quad<E>::pack(uu);
     }
   }
 }
@@ -210,26 +184,24 @@ __global__ __launch_bounds__(PREP_THREADS) void k_prep(Params p) {
 // Forward-scan operands of one chunk, filled by direct global->LDS loads as
 // swizzled row-major tiles, in sets by the phases that read them:
 //   set A (phases 2-4): Q, K (C x Dk) and the gate block (b, beta, lambda);
-//   set B (phase 3):    M = (I + A)^{-1} (C x C) and this tile's U^T
-//                       fragments (byte copy of the C-fragment-ordered layout);
+//   set B (phase 3):    T = (I + A)^{-1} diag(beta) (C x C) and this tile's
+//                       columns of V (C x BV);
 //   P (phase 4):        the output operator Gam * M_causal * Q K^T (C x C).
 // Set A has a ring of NA chunks, P of NP, set B one buffer.  The four
 // producer waves split every tile's 1 KB instructions evenly; producers 0-2
 // also load one gate vector each.
 template <typename E, int DK, int BV>
 struct ScanFwdRing {
-  static constexpr int RK = DK * (int)sizeof(E), RC = C * (int)sizeof(E);   // row bytes
-  static constexpr int NB = BV / 16;
-  static constexpr int UM = NB * 64 * 4 * (int)sizeof(E);   // U bytes per 16-column block
+  static constexpr int RK = DK * (int)sizeof(E), RC = C * (int)sizeof(E), RO = BV * (int)sizeof(E);   // row bytes
   static constexpr int AQ = 0, AK = AQ + C * RK, AG = AK + C * RK, ABYTES = AG + 3 * C * 4;
-  static constexpr int BM = 0, BU = BM + C * RC, BBYTES = BU + 4 * UM;
+  static constexpr int BT = 0, BV_ = BT + C * RC, BBYTES = BV_ + C * RO;
   static constexpr int NA = sizeof(E) == 2 ? 3 : 2;         // fp32 tiles are twice as large
   static constexpr int NP = sizeof(E) == 2 ? 2 : 1;         // P buffers
   static constexpr int LQ = C * RK / 1024 / 4;              // loads per producer: Q
   static constexpr int LK = C * RK / 1024 / 4;              // K (plus one gate vector for producers 0-2)
-  static constexpr int LB = (C * RC + 4 * UM) / 1024 / 4;   // M and U
+  static constexpr int LB = (C * RC + C * RO) / 1024 / 4;   // T and V
   static constexpr int LP = C * RC / 1024 / 4;              // P
-  static_assert((C * RK / 1024) % 4 == 0 && (C * RC / 1024) % 4 == 0 && UM % 1024 == 0, "even split");
+  static_assert((C * RK / 1024) % 4 == 0 && (C * RC / 1024) % 4 == 0 && (C * RO / 1024) % 4 == 0, "even split");
   static_assert(2 * LB + LQ + LP + 2 * (LK + 1) <= 63, "outstanding-load counter range");
 };
 
@@ -241,8 +213,8 @@ struct alignas(16) ScanFwdSmem {
   alignas(16) char ringB[R::BBYTES];
   alignas(16) char Pt[R::NP][C * R::RC];
   E S[BV][DK + P];    // state tile (row v, column k): MFMA operand and saved-state source
-  E Y[C][BV + P];     // Y = diag(beta g) X S^T (row r, column v)
-  E D[C][BV + P];     // D = U - M Y
+  E Y[C][BV + P];     // -diag(g) X S^T (row r, column v)
+  E D[C][BV + P];     // D = T V - T diag(g) X S^T
   E Dk[C][BV + P];    // diag(g_C / g) D
   E O[C][BV + P];     // output tile staging
 };
@@ -253,14 +225,14 @@ struct alignas(16) ScanFwdSmem {
 // fp32 MFMA accumulators across the whole sequence; compute wave w owns its
 // key rows 16 KPW w.. and the chunk rows 16w.. of every C-row operand.
 //
-// The chunk step never forms W = T diag(g) X (nor P): with T = M diag(beta),
-//   W S^T = M Y,  Y = diag(beta g) (K S^T + diag(lambda) Q S^T),
-// and Q S^T also serves the output, so a chunk reads Q, K, P, M, U and the
+// The chunk step never forms W = T diag(g) X nor U = T V:
+//   D = U - W S^T = T V + T Y,  Y = -diag(g) (K S^T + diag(lambda) Q S^T),
+// and Q S^T also serves the output, so a chunk reads Q, K, P, T, V and the
 // gates only.  Per chunk the compute waves pass three barriers:
 //   B_a  S staged, set A visible    phase 2: saved S; S K^T, S Q^T (as their
 //                                   transposes); Y;
 //   B_b  Y staged, set B visible    phase 3: output of the previous chunk;
-//                                   D = U - M Y;
+//                                   D = T V + T Y;
 //   B_c  D staged, P visible        phase 4: saved D; O = diag(g) Q S^T + P D
 //                                   (as O^T = g (S Q^T)^T + D^T P^T); state
 //                                   update S^T <- g_C S^T + K^T Dk; S staged.
@@ -332,16 +304,17 @@ __global__ __launch_bounds__(NTHREADS + 256) void k_scan_fwd(Params p) {
     const char* Pg = (const char*)((const E*)p.wP + gi * C * C);
     dma_rows<R::RC, C, 4, true>(sm.Pt[c % R::NP], Pg, R::RC, C, Pg, 0, prod, lane);
   };
-  // producers: M and this tile's U^T fragments of chunk c
+  // producers: T and this tile's columns of V of chunk c (rows of V past the
+  // chunk re-read its last row: they only meet zero columns of T)
   auto issueB = [&](int c) {
     size_t gi, arow;
     int len;
     chunk_at(c, gi, arow, len);
-    const char* Mg = (const char*)((const E*)p.wM + gi * C * C);
-    dma_rows<R::RC, C, 4, true>(sm.ringB + R::BM, Mg, R::RC, C, Mg, 0, prod, lane);
-    dma_block_asm<R::UM>(sm.ringB + R::BU + prod * R::UM,
-                         (const char*)((const E*)p.wU + gi * C * DV + (size_t)(prod * (DV / 16) + vt * NB) * 256),
-                         lane);
+    const char* Tg = (const char*)((const E*)p.wT + gi * C * C);
+    const char* Vg = (const char*)((const E*)p.v + arow * DV + v0);
+    dma_rows<R::RC, C, 4, true>(sm.ringB + R::BT, Tg, R::RC, C, Tg, 0, prod, lane);
+    dma_rows<R::RO, C, 4, true>(sm.ringB + R::BV_, Vg, (size_t)H * DV * ES, len, Vg + (size_t)(len - 1) * H * DV * ES, 0,
+                                prod, lane);
   };
 
   // state: acc[i][nb] = S^T rows 16*(KPW*w+i).., columns 16*nb.. of this tile
@@ -425,14 +398,14 @@ __global__ __launch_bounds__(NTHREADS + 256) void k_scan_fwd(Params p) {
           sq[nb] = Mma<E>::mma(sa[nb][ks], qB, sq[nb]);
         }
       }
-      const float br = gb[rr], gr = __expf(br), bgr = gb[C + rr] * gr, lr = gb[2 * C + rr];
-      // Y (row r, column v) = beta_r g_r ((S K^T) + lambda_r (S Q^T))^T
+      const float gr = __expf(gb[rr]), ngr = -gr, lr = gb[2 * C + rr];
+      // Y (row r, column v) = -g_r ((S K^T) + lambda_r (S Q^T))^T
 #pragma unroll
       for (int nb = 0; nb < NB; ++nb) {
         f4 y;
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
-          y[j] = bgr * (sk[nb][j] + lr * sq[nb][j]);
+          y[j] = ngr * (sk[nb][j] + lr * sq[nb][j]);
           sq[nb][j] *= gr;
         }
         *(QR*)&sm.Y[rr][nb * 16 + frow(lane, 0)] = Quad<E>::pack(y);
@@ -452,24 +425,22 @@ __global__ __launch_bounds__(NTHREADS + 256) void k_scan_fwd(Params p) {
     // ---- phase 3
     if (!producer) {
       if (with_o && c > 0) store_O(c - 1);
-      // D^T (value rows, chunk columns 16w..) = U^T - Y^T M^T; M is lower
-      // triangular, so k blocks past this wave's rows are skipped
+      // D^T (value rows, chunk columns 16w..) = (V + Y)^T T^T as two products;
+      // T is lower triangular, so k blocks past this wave's rows are skipped
       const float kbr = __expf(gb[C - 1] - gb[rr]);
 #pragma unroll
       for (int nb = 0; nb < NB; ++nb) {
         f4 d = zero4();
 #pragma unroll
         for (int ks = 0; ks < C / KS; ++ks)
-          if (ks * KS <= 16 * w + 15)
-            d = Mma<E>::mma(tr_frag<E>(&sm.Y[0][0], LV, ks * KS, nb * 16, lane),
-                            tile_frag<E, R::RC>(sm.ringB + R::BM, 16 * w, ks * KS, lane), d);
-        const QR uq = *(const QR*)(sm.ringB + R::BU + ((w * NB + nb) * 64 + lane) * 4 * ES);
+          if (ks * KS <= 16 * w + 15) {
+            const FR tB = tile_frag<E, R::RC>(sm.ringB + R::BT, 16 * w, ks * KS, lane);
+            d = Mma<E>::mma(tile_tr_frag<E, R::RO>(sm.ringB + R::BV_, ks * KS, nb * 16, lane), tB, d);
+            d = Mma<E>::mma(tr_frag<E>(&sm.Y[0][0], LV, ks * KS, nb * 16, lane), tB, d);
+          }
         f4 dk;
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          d[j] = Quad<E>::get(uq, j) - d[j];
-          dk[j] = kbr * d[j];
-        }
+        for (int j = 0; j < 4; ++j) dk[j] = kbr * d[j];
         *(QR*)&sm.D[rr][nb * 16 + frow(lane, 0)] = Quad<E>::pack(d);
         *(QR*)&sm.Dk[rr][nb * 16 + frow(lane, 0)] = Quad<E>::pack(dk);
       }

@@ -61,7 +61,9 @@ def test_workspace_sizes_monotone_and_zero_for_unsupported():
     assert 0 < a < b
     assert ws(4, 8192, 16, 128, 128, 1) > a
     assert ws(4, 4096, 32, 128, 128, 1) > a
-    assert ws(4, 4096, 16, 128, 256, 1) > a
+    # the forward's chunk factors are C x C per unit: independent of Dv
+    assert ws(4, 4096, 16, 128, 256, 1) == a
+    assert ws(4, 4096, 16, 128, 256, 1, is_bwd=True) > b
     assert ws(4, 4096, 16, 96, 128, 1) == 0      # Dk 96 unsupported
     assert ws(4, 4096, 16, 128, 128, 0) == 0     # fp32 needs Dk 64
     assert ws(1, 100, 2, 64, 64, 0) > 0
