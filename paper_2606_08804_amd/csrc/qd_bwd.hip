@@ -517,7 +517,7 @@ __global__ __launch_bounds__(INTRA_THREADS) void k_bwd_intra(Params p) {
   // tile vt is one of the first NB0
   constexpr int ML = C * RBC / 1024 / NWAVES;
   constexpr int KQN = 3 + 2 * TileRegs<E, C, DK, IT>::N;
-  static_assert((NB0 - 1) * TA::LOADS + ML <= 63 && TA::LOADS + ML + KQN <= 63, "outstanding-load counter range");
+  static_assert((NB0 - 1) * TA::LOADS + ML <= 63 && 2 * TA::LOADS + ML + KQN <= 63, "outstanding-load counter range");
   constexpr int UVT = NVT > 4 ? 1 : NVT;   // full unroll only for short tile loops
 #pragma unroll UVT
   for (int vt = 0; vt < NVT; ++vt) {
@@ -526,6 +526,7 @@ __global__ __launch_bounds__(INTRA_THREADS) void k_bwd_intra(Params p) {
     const int extra = vt < NB0 ? ML + (vt >= 1 ? KQN : 0) : 0;
     const int pending = after * TA::LOADS + extra;
     if (vt == 0) wait_vm<(NB0 - 1) * TA::LOADS + ML>();
+    else if (pending >= 2 * TA::LOADS + ML + KQN) wait_vm<2 * TA::LOADS + ML + KQN>();
     else if (pending >= TA::LOADS + ML + KQN) wait_vm<TA::LOADS + ML + KQN>();
     else if (pending >= ML + KQN) wait_vm<ML + KQN>();
     else if (pending >= 2 * TA::LOADS) wait_vm<2 * TA::LOADS>();
