@@ -54,9 +54,9 @@ def stage_bytes_per_unit(stage, Dk, Dv, e):
     gates = C * 4
     state = Dv * Dk * 4
     cc_e = C * C * e
-    if stage in ("prep_fwd", "prep_bwd"):   # q,k,v, 3 gates -> gate block, U, P, M
-        return 2 * act_qk + act_v + 3 * gates + 3 * gates + act_v + 2 * cc_e
-    if stage == "scan_fwd":      # gate block, q, k, P, M, U -> o, state (dtype), D
+    if stage in ("prep_fwd", "prep_bwd"):   # q, k, 3 gates -> gate block, P, M, T
+        return 2 * act_qk + 3 * gates + 3 * gates + 3 * cc_e
+    if stage == "scan_fwd":      # gate block, q, k, P, T, v -> o, state (dtype), D
         return 3 * gates + 2 * act_qk + 2 * cc_e + act_v + act_v + state * e // 4 + act_v
     if stage == "scan_bwd":      # gate block, P, M, k, q, dO -> dS' (dtype), dD, dv
         return 3 * gates + 2 * cc_e + 2 * act_qk + act_v + state * e // 4 + act_v + act_v
