@@ -364,20 +364,28 @@ __global__ __launch_bounds__(NTHREADS + 256) void k_scan_bwd(Params p) {
 }
 
 // ------------------------------------------------------------------ intra
-// Fused intra-chunk backward, one workgroup per (chunk, head) unit.
+// Fused intra-chunk backward, one four-wave workgroup per (chunk, head) unit.
+// Two workgroups share a CU (under 80 KB of LDS and 256 VGPRs each), so that
+// one streams its value-dimension tiles (bound by the CU's memory pipeline)
+// while the other computes (bound by VALU work).  Wave w owns chunk rows
+// 16w.. of every C-row operand.
 //
-// Phase A walks the value dimension in tiles of 32 columns, streamed into LDS
-// by direct global->LDS loads through a ring of three tiles (two in flight
-// while one is consumed), and accumulates, for rows 16w.. of wave w,
-//   aQ = dO S,  aK = D dS',  aW = dD S   (C x Dk)   and   aP = dO D^T, aT = dD V^T (C x C).
-// Phase B1 forms the Gram products G = X K^T, Q K^T and the second part of
-// dT; B2 back-propagates through the UT solve with the saved (I + A)^{-1} and
-// forms dG, dQK and the beta and decay terms in MFMA-layout registers; B3
-// produces dX, dq and dk.  The tail turns the decay terms into d log alpha.
+// Phase A walks the value dimension in tiles of 32 columns through a ring of
+// two LDS tiles and accumulates
+//   (dO S)^T, (D dS')^T, (dD S)^T   (Dk x 16 blocks: key rows, this wave's chunk columns)
+//   dO D^T, dD V^T                  (this wave's chunk rows x C)
+// and <dS', S> from diagonal blocks of S dS'^T.
+// Phase B1: K K^T, Q K^T, dW K^T, dW Q^T (dW = -dD S) and (T^T dW)^T;
+// B2: UT-solve backward with the saved M, dG, dQK, dQK + diag(lambda) dG, the
+// beta and decay terms; B3: dX, dq, dk as transposes, stored from registers.
+// The tail turns the decay terms into d log alpha.
+//
+// Wherever a result is needed in the other orientation the transposed
+// product is computed instead, so that a lane holds four consecutive values
+// of one row and writes them to LDS (or global memory) as one store.
 
 // Phase-A tile of 32 value columns: S, dS' (32 value rows of Dk), D, V, dO,
-// dD (C rows of 32), each in the swizzled direct-load layout; a ring of NBUF
-// tiles keeps two in flight.
+// dD (C rows of 32), each in the swizzled direct-load layout.
 template <typename E, int DK>
 struct TileA {
   static constexpr int BV = 32;
@@ -385,195 +393,150 @@ struct TileA {
   static constexpr int RK = DK * (int)sizeof(E);    // row bytes of the state tiles
   static constexpr int S = 0, DS = S + BV * RK, D = DS + BV * RK, V = D + C * RE, DO = V + C * RE,
                        DD = DO + C * RE, BYTES = DD + C * RE;
-  static constexpr int NBUF = sizeof(E) == 2 ? 3 : 2;   // fp32 tiles are twice as large
   static constexpr int LOADS = BYTES / 1024 / NWAVES;   // direct loads per wave and tile
 };
 
 template <typename E, int DK>
-struct alignas(16) BwdSmem {
-  static constexpr int P = Pad<E>::v;
-  float b[C], g[C], kb[C], beta[C], lam[C], db[C], dbeta[C];
-  float rsum[5][2][C];      // per-row partial sums of the two column halves:
-                            // dbeta rows, decay rows (B2); decay, Kbar, dlambda rows (B3)
-  float sdot[8];            // per-wave parts of <dS', S>
-  union {
-    alignas(16) char tiles[TileA<E, DK>::NBUF][TileA<E, DK>::BYTES];   // phase A
-    struct {
-      struct {
-        E K[C][DK + P];       // chunk keys (r, k)
-        E Q[C][DK + P];       // chunk queries (r, k)
-        E dW[C][DK + P];      // dW = -dD S (r, k)
-      } b1;                   // from phase B1 to the end of phase B3
-      union {
-        struct {
-          union {
-            struct {
-              E MT[C][C + P];     // M^T (i, r)
-              E dMt[C][C + P];    // (dT diag(beta))^T (i, r)
-            } m;
-            struct {
-              E dG[C][C + P];     // dG (r, i), after M^T and dMinv^T are dead
-              E dQK[C][C + P];    // dQK (r, i)
-              E dGl[C][C + P];    // dQK + diag(lambda) dG (r, i)
-            } g;
-          } v;
-          E Y[C][C + P];          // M^T dT diag(beta) (r, i)
-          float dbc[16][C];       // column partial sums of dT (.) M, per row block and lane group
-          float ecc[16][C];       // column partial sums of the decay-gradient terms
-        } b2;
-        struct {
-          E keep[3][C][C + P];    // dG, dQK, dQK + diag(lambda) dG (phase-B3 A operands)
-          E oq[C][DK + P];        // dq staging, over the dead Y and column sums
-          E ok[C][DK + P];        // dk staging
-        } b3;
-      } u;
-    } s;
-  } x;
-  // M = (I + A)^{-1} (r, i), direct-loaded at the start (swizzled rows of C
-  // elements, outside the phase-A ring)
-  alignas(16) char Mm[C * C * sizeof(E)];
+struct alignas(16) IntraSmem {
+  typedef TileA<E, DK> TA;
+  static constexpr int RK = DK * (int)sizeof(E), RC = C * (int)sizeof(E);
+  // phase-B placement inside the ring (swizzled tiles): K, Q in slot 0; dW,
+  // (dT diag(beta))^T and Y in slot 1; dG over dW, dQK after it (or after K
+  // and Q in slot 0), dQK + diag(lambda) dG over Y
+  static constexpr int OK = 0, OQ = C * RK, OW = TA::BYTES, ODT = OW + C * RK, OY = ODT + C * RC, OG = OW;
+  static constexpr int OQK = 2 * C * RC <= C * RK ? OW + C * RC : 2 * C * RK;
+  static_assert(OY + C * RC <= 2 * TA::BYTES, "slot 1 holds dW, (dT diag(beta))^T and Y");
+  static_assert(2 * C * RC <= C * RK || 2 * C * RK + C * RC <= TA::BYTES, "room for dQK");
+  alignas(16) char ring[2][TA::BYTES];
+  alignas(16) char Mm[C * RC];    // M = (I + A)^{-1} (r, i), swizzled rows
+  float b[C], g[C], beta[C], lam[C];
+  float rdbeta[C], rer[C], rdb[C], rtk[C], rdl[C];   // row parts (each row owned by one wave)
+  float colp[2][NWAVES][C];                          // column parts per wave: dT (.) M, decay terms
+  float sdot[NWAVES];
 };
 
-// Eight waves: wave w takes rows 16 rb.. (rb = w & 3) of every C-row operand
-// and one half (ch = w >> 2) of the Dk column blocks and of the C x C column
-// blocks; two waves share each SIMD and hide each other's latency.
-constexpr int INTRA_THREADS = 2 * NTHREADS;
+constexpr int INTRA_THREADS = NTHREADS;
 
 template <typename E, int DK, int DV>
-__global__ __launch_bounds__(INTRA_THREADS) void k_bwd_intra(Params p) {
-  constexpr int P = Pad<E>::v;
-  constexpr int BV = 32;
-  constexpr int LC = C + P;
+__global__ __launch_bounds__(INTRA_THREADS) __attribute__((amdgpu_waves_per_eu(2, 2))) void k_bwd_intra(Params p) {
   constexpr int KS = Mma<E>::KS;
   constexpr int NKB = DK / 16;        // 16-column blocks of Dk
-  constexpr int HK = NKB / 2;         // Dk blocks per column half
+  constexpr int NKK = DK / KS;        // k steps over Dk
+  constexpr int NKC = C / KS;         // k steps over the chunk
+  constexpr int BV = 32;
   constexpr int NVT = DV / BV;
-  constexpr int IT = INTRA_THREADS;
+  constexpr size_t ES = sizeof(E);
   typedef typename Mma<E>::frag FR;
   typedef typename Quad<E>::raw QR;
-  __shared__ BwdSmem<E, DK> sm;
+  typedef TileA<E, DK> TA;
+  typedef IntraSmem<E, DK> SM;
+  constexpr int RK = SM::RK, RC = SM::RC;
+  static_assert(NVT >= 2, "at least two value tiles");
+  __shared__ SM sm;
   if ((int)blockIdx.x < p.lead) {
-    // a leading workgroup holds its CU for about half a unit, so that half of
-    // the CUs run phase-shifted and their value-dimension loads overlap the
-    // other half's compute phases
+    // leading workgroups hold their slot for about half a unit, so that the
+    // workgroups run phase-shifted and the value-dimension loads of some
+    // overlap the compute phases of others
     const long long t0c = clock64();
     while (clock64() - t0c < p.lead_cycles) __builtin_amdgcn_s_sleep(32);
     return;
   }
   const int bid = (int)blockIdx.x - p.lead;
   const int g = bid % p.n_slots, h = bid / p.n_slots, tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-  const int rb = w & 3, ch = w >> 2;
-  const int kb0 = ch * HK, ib0 = 2 * ch;
   int n, t0, len;
   if (!locate(p, g, n, t0, len)) return;
   const int H = p.H;
   const size_t gi = (size_t)g * H + h;
   const size_t arow = (size_t)t0 * H + h;   // first activation row of the chunk
-
+  const int rr = 16 * w + fcol(lane);       // chunk row of this lane's transposed results
 
   // ---------------- phase A: contractions over the value dimension
-  typedef TileA<E, DK> TA;
-  f4 aQ[HK], aK[HK], aW[HK], aP[2], aT[2], asd = zero4();
+  f4 aQt[NKB], aKt[NKB], aWt[NKB], aP[4], aT[4], asd = zero4();
 #pragma unroll
-  for (int i = 0; i < HK; ++i) aQ[i] = aK[i] = aW[i] = zero4();
+  for (int i = 0; i < NKB; ++i) aQt[i] = aKt[i] = aWt[i] = zero4();
 #pragma unroll
-  for (int i = 0; i < 2; ++i) aP[i] = aT[i] = zero4();
-  constexpr size_t ES = sizeof(E);
+  for (int i = 0; i < 4; ++i) aP[i] = aT[i] = zero4();
   const char* Sg = (const char*)((const E*)p.saved + gi * DK * DV);
   const char* dSg = (const char*)((const E*)p.w_dSo + gi * DK * DV);
   const char* Dg = (const char*)((const E*)p.savedD + gi * C * DV);
   const char* dDg = (const char*)((const E*)p.w_dDb + gi * C * DV);
   const char* dOg = (const char*)((const E*)p.dO + arow * DV);
   const char* Vg = (const char*)((const E*)p.v + arow * DV);
-  // direct loads are issued by waves 0-3 only; the others' waits are no-ops
-  const bool loader = w < NWAVES;
-  constexpr int RBC = C * (int)sizeof(E);
   // rows of V and dO past the chunk come from D, whose rows there are zero
   auto issue = [&](int vt) {
-    char* t = &sm.x.tiles[vt % TA::NBUF][0];
+    const int ln = lane;
+    char* t = sm.ring[vt & 1];
     const size_t vb = (size_t)vt * BV;
-    dma_rows<TA::RK, BV>(t + TA::S, Sg + vb * TA::RK, TA::RK, BV, Sg, 0, w, lane);
-    dma_rows<TA::RK, BV>(t + TA::DS, dSg + vb * TA::RK, TA::RK, BV, dSg, 0, w, lane);
-    dma_rows<TA::RE, C>(t + TA::D, Dg + vb * ES, DV * ES, C, Dg, 0, w, lane);
-    dma_rows<TA::RE, C>(t + TA::DD, dDg + vb * ES, DV * ES, C, dDg, 0, w, lane);
-    dma_rows<TA::RE, C>(t + TA::V, Vg + vb * ES, (size_t)H * DV * ES, len, Dg + vb * ES, DV * ES, w, lane);
-    dma_rows<TA::RE, C>(t + TA::DO, dOg + vb * ES, (size_t)H * DV * ES, len, Dg + vb * ES, DV * ES, w, lane);
+    dma_rows<RK, BV>(t + TA::S, Sg + vb * RK, RK, BV, Sg, 0, w, ln);
+    dma_rows<RK, BV>(t + TA::DS, dSg + vb * RK, RK, BV, dSg, 0, w, ln);
+    dma_rows<TA::RE, C>(t + TA::D, Dg + vb * ES, DV * ES, C, Dg, 0, w, ln);
+    dma_rows<TA::RE, C>(t + TA::DD, dDg + vb * ES, DV * ES, C, dDg, 0, w, ln);
+    dma_rows<TA::RE, C>(t + TA::V, Vg + vb * ES, (size_t)H * DV * ES, len, Dg + vb * ES, DV * ES, w, ln);
+    dma_rows<TA::RE, C>(t + TA::DO, dOg + vb * ES, (size_t)H * DV * ES, len, Dg + vb * ES, DV * ES, w, ln);
   };
-  // the first tiles and M = (I + A)^{-1} go out first; the gates and the
-  // chunk's K, Q rows (registers, needed from phase B on) follow once the
-  // first tile has landed, so that they do not compete with it
-  constexpr int NB0 = NVT < TA::NBUF ? NVT : TA::NBUF;
-  if (loader) {
-#pragma unroll
-    for (int vt = 0; vt < NB0; ++vt) issue(vt);
+  // first two tiles and M; then (after the first tile) the gates, and with
+  // the last tile the chunk's K and Q rows into the free slot 0 (for phase B;
+  // rows past the chunk re-read its last row and are zeroed afterwards)
+  issue(0);
+  issue(1);
+  {
     const char* Mg = (const char*)((const E*)p.wM + gi * C * C);
-    dma_rows<RBC, C>(sm.Mm, Mg, RBC, C, Mg, 0, w, lane);
+    dma_rows<RC, C>(sm.Mm, Mg, RC, C, Mg, 0, w, lane);
   }
-  const int ti = tid & (C - 1);
-  float gb, gbeta, glam;
-  TileRegs<E, C, DK, IT> rKf, rQf;
-  // vector-memory operations a loading wave has issued after tile vt's, at
-  // the wait for tile vt: later tiles, and M and the register loads when
-  // tile vt is one of the first NB0
-  constexpr int ML = C * RBC / 1024 / NWAVES;
-  constexpr int KQN = 3 + 2 * TileRegs<E, C, DK, IT>::N;
-  static_assert((NB0 - 1) * TA::LOADS + ML <= 63 && 2 * TA::LOADS + ML + KQN <= 63, "outstanding-load counter range");
-  constexpr int UVT = NVT > 4 ? 1 : NVT;   // full unroll only for short tile loops
-#pragma unroll UVT
+  constexpr int ML = C * RC / 1024 / NWAVES;
+  float gb = 0.f, gbeta = 0.f, glam = 0.f;
+  static_assert(NVT % 2 == 0, "the last tile uses slot 1");
+#pragma unroll 1
   for (int vt = 0; vt < NVT; ++vt) {
-    // tile vt is complete once at most `pending` later operations are outstanding
-    const int after = (vt == 0 ? NB0 : min(NVT, vt + TA::NBUF - 1)) - 1 - vt;
-    const int extra = vt < NB0 ? ML + (vt >= 1 ? KQN : 0) : 0;
-    const int pending = after * TA::LOADS + extra;
-    if (vt == 0) wait_vm<(NB0 - 1) * TA::LOADS + ML>();
-    else if (pending >= 2 * TA::LOADS + ML + KQN) wait_vm<2 * TA::LOADS + ML + KQN>();
-    else if (pending >= TA::LOADS + ML + KQN) wait_vm<TA::LOADS + ML + KQN>();
-    else if (pending >= ML + KQN) wait_vm<ML + KQN>();
-    else if (pending >= 2 * TA::LOADS) wait_vm<2 * TA::LOADS>();
-    else if (pending >= TA::LOADS) wait_vm<TA::LOADS>();
+    // later loads that may still be in flight when tile vt is complete
+    if (vt == 0) wait_vm<TA::LOADS + ML>();       // tile 1, M
+    else if (vt == 1) wait_vm<ML + 3>();          // M, gates
     else wait_vm<0>();
-    block_sync_lds();                 // tile vt visible; tile vt-1's buffer is free
+    block_sync_lds();                             // tile vt visible; tile vt-1's slot is free
     if (vt == 0) {
       asm volatile("" ::: "memory");
-      gb = p.wb[gi * 3 * C + ti];
-      gbeta = p.wb[gi * 3 * C + C + ti];
-      glam = p.wb[gi * 3 * C + 2 * C + ti];
-      rKf.load_clamped((const E*)p.k + arow * DK, (size_t)H * DK, len, tid);
-      rQf.load_clamped((const E*)p.q + arow * DK, (size_t)H * DK, len, tid);
+      const float* gblk = p.wb + gi * 3 * C;
+      gb = gblk[lane];
+      gbeta = gblk[C + lane];
+      glam = gblk[2 * C + lane];
       asm volatile("" ::: "memory");
     }
-    if (loader && vt >= 1 && vt + TA::NBUF - 1 < NVT) issue(vt + TA::NBUF - 1);
-    const char* t = &sm.x.tiles[vt % TA::NBUF][0];
+    if (vt >= 1 && vt + 1 < NVT) issue(vt + 1);
+    if (vt == NVT - 1) {
+      const char* Kg = (const char*)((const E*)p.k + arow * DK);
+      const char* Qg = (const char*)((const E*)p.q + arow * DK);
+      dma_rows<RK, C>(sm.ring[0] + SM::OK, Kg, (size_t)H * RK, len, Kg + (size_t)(len - 1) * H * RK, 0, w, lane);
+      dma_rows<RK, C>(sm.ring[0] + SM::OQ, Qg, (size_t)H * RK, len, Qg + (size_t)(len - 1) * H * RK, 0, w, lane);
+    }
+    const char* t = sm.ring[vt & 1];
+    int la = lane;                        // laundered: addresses formed per tile
+    asm volatile("" : "+v"(la));
 #pragma unroll
     for (int ks = 0; ks < BV / KS; ++ks) {
-      const FR aO = tile_frag<E, TA::RE>(t + TA::DO, 16 * rb, ks * KS, lane);
-      const FR adD = tile_frag<E, TA::RE>(t + TA::DD, 16 * rb, ks * KS, lane);
-      const FR aD = tile_frag<E, TA::RE>(t + TA::D, 16 * rb, ks * KS, lane);
+      const FR aO = tile_frag<E, TA::RE>(t + TA::DO, 16 * w, ks * KS, la);
+      const FR adD = tile_frag<E, TA::RE>(t + TA::DD, 16 * w, ks * KS, la);
+      const FR aD = tile_frag<E, TA::RE>(t + TA::D, 16 * w, ks * KS, la);
 #pragma unroll
-      for (int i = 0; i < HK; ++i) {
-        const int kb = kb0 + i;
-        const FR bS = tile_tr_frag<E, TA::RK>(t + TA::S, ks * KS, kb * 16, lane);
-        const FR bdS = tile_tr_frag<E, TA::RK>(t + TA::DS, ks * KS, kb * 16, lane);
-        aQ[i] = Mma<E>::mma(aO, bS, aQ[i]);
-        aW[i] = Mma<E>::mma(adD, bS, aW[i]);
-        aK[i] = Mma<E>::mma(aD, bdS, aK[i]);
+      for (int kb = 0; kb < NKB; ++kb) {
+        const FR bS = tile_tr_frag<E, RK>(t + TA::S, ks * KS, kb * 16, la);
+        const FR bdS = tile_tr_frag<E, RK>(t + TA::DS, ks * KS, kb * 16, la);
+        aQt[kb] = Mma<E>::mma(bS, aO, aQt[kb]);
+        aWt[kb] = Mma<E>::mma(bS, adD, aWt[kb]);
+        aKt[kb] = Mma<E>::mma(bdS, aD, aKt[kb]);
       }
 #pragma unroll
-      for (int i = 0; i < 2; ++i) {
-        const int ib = ib0 + i;
-        const FR bD = tile_frag<E, TA::RE>(t + TA::D, ib * 16, ks * KS, lane);
-        const FR bV = tile_frag<E, TA::RE>(t + TA::V, ib * 16, ks * KS, lane);
-        aP[i] = Mma<E>::mma(aO, bD, aP[i]);
-        aT[i] = Mma<E>::mma(adD, bV, aT[i]);
+      for (int cb = 0; cb < 4; ++cb) {
+        aP[cb] = Mma<E>::mma(aO, tile_frag<E, TA::RE>(t + TA::D, cb * 16, ks * KS, la), aP[cb]);
+        aT[cb] = Mma<E>::mma(adD, tile_frag<E, TA::RE>(t + TA::V, cb * 16, ks * KS, la), aT[cb]);
       }
     }
     // <dS', S> = trace(S dS'^T): wave w adds the diagonal 16 x 16 block
-    // (w & 1) of this tile's S dS'^T over the key steps w >> 1, +4, ...
+    // (w & 1) of this tile's S dS'^T over the key steps w >> 1, +2, ...
 #pragma unroll
-    for (int ks = 0; ks < DK / KS; ks += 4)
-      if (ks + (w >> 1) < DK / KS)
-        asd = Mma<E>::mma(tile_frag<E, TA::RK>(t + TA::S, 16 * (w & 1), (ks + (w >> 1)) * KS, lane),
-                          tile_frag<E, TA::RK>(t + TA::DS, 16 * (w & 1), (ks + (w >> 1)) * KS, lane), asd);
+    for (int ks = 0; ks < NKK; ks += 2)
+      if (ks + (w >> 1) < NKK)
+        asd = Mma<E>::mma(tile_frag<E, RK>(t + TA::S, 16 * (w & 1), (ks + (w >> 1)) * KS, la),
+                          tile_frag<E, RK>(t + TA::DS, 16 * (w & 1), (ks + (w >> 1)) * KS, la), asd);
   }
   {
     // diagonal elements of the accumulated block: row 4 (l >> 4) + j == column l & 15
@@ -585,284 +548,290 @@ __global__ __launch_bounds__(INTRA_THREADS) void k_bwd_intra(Params p) {
     sdot = wave_sum(sdot);
     if (lane == 0) sm.sdot[w] = sdot;
   }
-  if (tid < C) {
-    sm.b[tid] = gb;
-    sm.g[tid] = __expf(gb);
-    sm.beta[tid] = gbeta;   // zero past the chunk in the gate block
-    sm.lam[tid] = glam;
+  if (w == 0) {
+    sm.b[lane] = gb;
+    sm.g[lane] = __expf(gb);
+    sm.beta[lane] = gbeta;   // zero past the chunk in the gate block
+    sm.lam[lane] = glam;
   }
 
-  // ---------------- phase B1: G = X K^T, QK = Q K^T, dT2 = dW (g X)^T
-  constexpr int LKD = DK + P;
-  block_sync_lds();
-  rKf.store_rows(&sm.x.s.b1.K[0][0], LKD, len, tid);
-  rQf.store_rows(&sm.x.s.b1.Q[0][0], LKD, len, tid);
+  // ---------------- phase B1
+  // The lane index is laundered at each phase so that per-lane LDS addresses
+  // are formed where they are used rather than hoisted into long-lived
+  // registers (the compiler would spill them).
+  char* const ring = &sm.ring[0][0];
+  int lb = lane;
+  asm volatile("" : "+v"(lb));
+  wait_vm<0>();                            // K, Q landed
+  if (len < C) {
+    // rows of K and Q past the chunk are zero
+    constexpr int PR = RK / 16;
+    for (int idx = tid; idx < (C - len) * PR; idx += INTRA_THREADS) {
+      const int r = len + idx / PR, c = (idx % PR) * 16;
+      *(uint4*)(ring + SM::OK + tile_off<RK>(r, c)) = make_uint4(0, 0, 0, 0);
+      *(uint4*)(ring + SM::OQ + tile_off<RK>(r, c)) = make_uint4(0, 0, 0, 0);
+    }
+  }
+  block_sync_lds();                        // phase-A tiles consumed; gates, K, Q visible; slot 1 free
+  // dW = -dD S rows of this wave from (dD S)^T: four consecutive keys per lane
 #pragma unroll
-  for (int i = 0; i < HK; ++i)
-#pragma unroll
-    for (int j = 0; j < 4; ++j)
-      sm.x.s.b1.dW[16 * rb + frow(lane, j)][(kb0 + i) * 16 + fcol(lane)] = fromf<E>(-aW[i][j]);
-  if (tid < C) sm.kb[tid] = __expf(sm.b[C - 1] - sm.b[tid]);
+  for (int kb = 0; kb < NKB; ++kb)
+    *(QR*)(ring + SM::OW + tile_off<RK>(rr, (kb * 16 + frow(lb, 0)) * (int)ES)) = Quad<E>::pack(-aWt[kb]);
   block_sync_lds();
-  // G = X K^T = K K^T + diag(lambda) Q K^T and dT2 = dW (diag(g) X)^T =
-  // (dW K^T + dW Q^T diag(lambda)) diag(g): four products of the stored
-  // operands, the gates applied to the fp32 results
-  f4 aG[2], aQK[2], adT[2];
+  const int r0 = 16 * w + frow(lb, 0);
+  float lamr[4], betr[4], br4[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    lamr[j] = sm.lam[r0 + j];
+    betr[j] = sm.beta[r0 + j];
+    br4[j] = sm.b[r0 + j];
+  }
+  f4 aG[4], aQK[4], dT[4];
   {
-    f4 aKK[2], aDK[2], aDQ[2];
+    // dT = dD V^T + dW (diag(g) X)^T, the second part as
+    // (dW K^T + dW Q^T diag(lambda)) diag(g)
+    f4 aDK[4], aDQ[4];
 #pragma unroll
-    for (int i = 0; i < 2; ++i) aKK[i] = aQK[i] = aDK[i] = aDQ[i] = zero4();
+    for (int cb = 0; cb < 4; ++cb) aDK[cb] = aDQ[cb] = zero4();
 #pragma unroll
-    for (int ks = 0; ks < DK / KS; ++ks) {
-      const FR kA = Frag<E>::load(kmaj(&sm.x.s.b1.K[0][0], LKD), 16 * rb, ks * KS, lane);
-      const FR qA = Frag<E>::load(kmaj(&sm.x.s.b1.Q[0][0], LKD), 16 * rb, ks * KS, lane);
-      const FR dwA = Frag<E>::load(kmaj(&sm.x.s.b1.dW[0][0], LKD), 16 * rb, ks * KS, lane);
+    for (int ks = 0; ks < NKK; ++ks) {
+      const FR dwA = tile_frag<E, RK>(ring + SM::OW, 16 * w, ks * KS, lb);
 #pragma unroll
-      for (int i = 0; i < 2; ++i) {
-        const int ib = ib0 + i;
-        const FR kB = Frag<E>::load(kmaj(&sm.x.s.b1.K[0][0], LKD), ib * 16, ks * KS, lane);
-        const FR qB = Frag<E>::load(kmaj(&sm.x.s.b1.Q[0][0], LKD), ib * 16, ks * KS, lane);
-        aKK[i] = Mma<E>::mma(kA, kB, aKK[i]);
-        aQK[i] = Mma<E>::mma(qA, kB, aQK[i]);
-        aDK[i] = Mma<E>::mma(dwA, kB, aDK[i]);
-        aDQ[i] = Mma<E>::mma(dwA, qB, aDQ[i]);
+      for (int cb = 0; cb < 4; ++cb) {
+        aDK[cb] = Mma<E>::mma(dwA, tile_frag<E, RK>(ring + SM::OK, cb * 16, ks * KS, lb), aDK[cb]);
+        aDQ[cb] = Mma<E>::mma(dwA, tile_frag<E, RK>(ring + SM::OQ, cb * 16, ks * KS, lb), aDQ[cb]);
       }
     }
-    const int r0 = 16 * rb + frow(lane, 0);
 #pragma unroll
-    for (int i = 0; i < 2; ++i) {
-      const int c = (ib0 + i) * 16 + fcol(lane);
+    for (int cb = 0; cb < 4; ++cb) {
+      const int c = cb * 16 + fcol(lb);
       const float gc = sm.g[c], lc = sm.lam[c];
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        aG[i][j] = aKK[i][j] + sm.lam[r0 + j] * aQK[i][j];
-        adT[i][j] = gc * (aDK[i][j] + lc * aDQ[i][j]);
+      for (int j = 0; j < 4; ++j) dT[cb][j] = aT[cb][j] + gc * (aDK[cb][j] + lc * aDQ[cb][j]);
+    }
+  }
+  {
+    // G = X K^T = K K^T + diag(lambda) Q K^T (rows 16w.., all columns)
+    f4 aKK[4];
+#pragma unroll
+    for (int cb = 0; cb < 4; ++cb) aKK[cb] = aQK[cb] = zero4();
+#pragma unroll
+    for (int ks = 0; ks < NKK; ++ks) {
+      const FR kA = tile_frag<E, RK>(ring + SM::OK, 16 * w, ks * KS, lb);
+      const FR qA = tile_frag<E, RK>(ring + SM::OQ, 16 * w, ks * KS, lb);
+#pragma unroll
+      for (int cb = 0; cb < 4; ++cb) {
+        const FR kB = tile_frag<E, RK>(ring + SM::OK, cb * 16, ks * KS, lb);
+        aKK[cb] = Mma<E>::mma(kA, kB, aKK[cb]);
+        aQK[cb] = Mma<E>::mma(qA, kB, aQK[cb]);
       }
+    }
+#pragma unroll
+    for (int cb = 0; cb < 4; ++cb)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) aG[cb][j] = aKK[cb][j] + lamr[j] * aQK[cb][j];
+  }
+  // (T^T dW)^T = (diag(beta) M^T dW)^T: key rows, this wave's chunk columns;
+  // M is lower triangular, so k blocks before this wave's rows are skipped
+  f4 tdwt[NKB];
+  {
+    const float betc = sm.beta[rr];
+#pragma unroll
+    for (int kb = 0; kb < NKB; ++kb) {
+      f4 x = zero4();
+#pragma unroll
+      for (int ks = 0; ks < NKC; ++ks)
+        if (ks * KS + KS > 16 * w)
+          x = Mma<E>::mma(tile_tr_frag<E, RK>(ring + SM::OW, ks * KS, kb * 16, lb),
+                          tile_tr_frag<E, RC>(sm.Mm, ks * KS, 16 * w, lb), x);
+#pragma unroll
+      for (int j = 0; j < 4; ++j) tdwt[kb][j] = betc * x[j];
     }
   }
 
-  // ---------------- phase B2: UT-solve backward and the C x C gradient terms.
-  // Lane (w, lane) holds element (r, c) = (16 rb + frow(lane, j), 16 ib + fcol(lane))
-  // of every C x C accumulator, for the two column blocks ib of its half.
-  const int rw = 16 * rb + frow(lane, 0), cl = fcol(lane);
-  {
-    // dT = dD V^T + dW (g X)^T: column sums of dT (.) M feed dbeta; M^T and
-    // (dT diag(beta))^T become the operands of Y = M^T dT diag(beta)
+  // ---------------- phase B2: UT-solve backward and the C x C gradient terms
+  asm volatile("" : "+v"(lb));
+  // dT = dD V^T + dW (g X)^T; the column sums of dT (.) M feed dbeta;
+  // (dT diag(beta))^T is the operand of Y = M^T dT diag(beta)
 #pragma unroll
-    for (int i = 0; i < 2; ++i) {
-      const int c = (ib0 + i) * 16 + cl;
-      const float bc = sm.beta[c];
-      f4 mv, dm;
-      float cs = 0.f;
+  for (int cb = 0; cb < 4; ++cb) {
+    const int c = cb * 16 + fcol(lb);
+    const float bc = sm.beta[c];
+    f4 dm;
+    float cs = 0.f;
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const float m = tof(*(const E*)(sm.Mm + tile_off<RBC>(rw + j, c * (int)sizeof(E))));
-        const float dt = aT[i][j] + adT[i][j];
-        cs += dt * m;
-        mv[j] = m;
-        dm[j] = dt * bc;
-      }
-      *(QR*)&sm.x.s.u.b2.v.m.MT[c][rw] = Quad<E>::pack(mv);
-      *(QR*)&sm.x.s.u.b2.v.m.dMt[c][rw] = Quad<E>::pack(dm);
-      sm.x.s.u.b2.dbc[4 * rb + (lane >> 4)][c] = cs;
+    for (int j = 0; j < 4; ++j) {
+      cs += dT[cb][j] * tof(*(const E*)(sm.Mm + tile_off<RC>(r0 + j, c * (int)ES)));
+      dm[j] = dT[cb][j] * bc;
     }
+    *(QR*)(ring + SM::ODT + tile_off<RC>(c, r0 * (int)ES)) = Quad<E>::pack(dm);
+    cs += __shfl_xor(cs, 16, 64);
+    cs += __shfl_xor(cs, 32, 64);
+    if (lane < 16) sm.colp[0][w][c] = cs;
   }
-  block_sync_lds();
-  f4 adA[2];
+  block_sync_lds();                        // (dT diag(beta))^T complete; dW no longer read
+  f4 adA[4];
   {
-    // Y = M^T dMinv: rows 16 rb.., this half's column blocks
+    // Y^T = (dT diag(beta))^T M (chunk columns, this wave's rows), stored as Y rows
 #pragma unroll
-    for (int i = 0; i < 2; ++i) {
-      const int ib = ib0 + i;
-      const f4 y = mma_k<E, C>(kmaj(&sm.x.s.u.b2.v.m.MT[0][0], LC), kmaj(&sm.x.s.u.b2.v.m.dMt[0][0], LC), 16 * rb,
-                               ib * 16, zero4(), lane);
+    for (int cb = 0; cb < 4; ++cb) {
+      f4 y = zero4();
 #pragma unroll
-      for (int j = 0; j < 4; ++j) sm.x.s.u.b2.Y[rw + j][ib * 16 + cl] = fromf<E>(y[j]);
+      for (int ks = 0; ks < NKC; ++ks)
+        if (ks * KS + KS > 16 * w)
+          y = Mma<E>::mma(tile_frag<E, RC>(ring + SM::ODT, cb * 16, ks * KS, lb),
+                          tile_tr_frag<E, RC>(sm.Mm, ks * KS, 16 * w, lb), y);
+      *(QR*)(ring + SM::OY + tile_off<RC>(rr, (cb * 16 + frow(lb, 0)) * (int)ES)) = Quad<E>::pack(y);
     }
-    block_sync_lds();                  // Y complete; M^T and dMinv^T dead after this point
+    // dA = strictLower(-Y M^T) (this wave's rows; M lower triangular)
 #pragma unroll
-    for (int i = 0; i < 2; ++i) {           // dA = strictLower(-Y M^T)
-      adA[i] = zero4();
+    for (int cb = 0; cb < 4; ++cb) {
+      adA[cb] = zero4();
 #pragma unroll
-      for (int ks = 0; ks < C / KS; ++ks)
-        adA[i] = Mma<E>::mma(Frag<E>::load(kmaj(&sm.x.s.u.b2.Y[0][0], LC), 16 * rb, ks * KS, lane),
-                             tile_frag<E, RBC>(sm.Mm, (ib0 + i) * 16, ks * KS, lane), adA[i]);
+      for (int ks = 0; ks < NKC; ++ks)
+        if (ks * KS <= cb * 16 + 15)
+          adA[cb] = Mma<E>::mma(tile_frag<E, RC>(ring + SM::OY, 16 * w, ks * KS, lb),
+                                tile_frag<E, RC>(sm.Mm, cb * 16, ks * KS, lb), adA[cb]);
     }
   }
   {
     // dG = diag(beta) dA (.) Gamma, dQK = dP (.) Gamma (causal, inclusive),
-    // the decay-gradient terms t = (dG (.) G + dQK (.) QK) and the rows of
-    // dbeta from A = strictLower(diag(beta) Gamma (.) G)
-    float br[4], betar[4], lamr[4], dbr[4] = {0.f, 0.f, 0.f, 0.f}, er[4] = {0.f, 0.f, 0.f, 0.f};
+    // dQK + diag(lambda) dG (over Y: own rows), the decay-gradient terms
+    // t = dG (.) G + dQK (.) QK and the row parts of dbeta from
+    // A = strictLower(diag(beta) Gamma (.) G)
+    float dbr[4] = {0.f, 0.f, 0.f, 0.f}, er[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      br[j] = sm.b[rw + j];
-      betar[j] = sm.beta[rw + j];
-      lamr[j] = sm.lam[rw + j];
-    }
-#pragma unroll
-    for (int i = 0; i < 2; ++i) {
-      const int c = (ib0 + i) * 16 + cl;
+    for (int cb = 0; cb < 4; ++cb) {
+      const int c = cb * 16 + fcol(lb);
       const float bc = sm.b[c];
       float ec = 0.f;
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
-        const int r = rw + j;
-        const float gam = (r >= c) ? __expf(br[j] - bc) : 0.f;
-        const float dA = (r > c) ? -adA[i][j] : 0.f;
+        const int r = r0 + j;
+        const float gam = (r >= c) ? __expf(br4[j] - bc) : 0.f;
+        const float dA = (r > c) ? -adA[cb][j] : 0.f;
         const float dAg = dA * gam;
-        const float dg = dAg * betar[j];
-        const float dqk = aP[i][j] * gam;
-        const float t = dg * aG[i][j] + dqk * aQK[i][j];
-        dbr[j] += dAg * aG[i][j];
+        const float dg = dAg * betr[j];
+        const float dqk = aP[cb][j] * gam;
+        const float t = dg * aG[cb][j] + dqk * aQK[cb][j];
+        dbr[j] += dAg * aG[cb][j];
         er[j] += t;
         ec += t;
-        sm.x.s.u.b2.v.g.dG[r][c] = fromf<E>(dg);
-        sm.x.s.u.b2.v.g.dQK[r][c] = fromf<E>(dqk);
-        sm.x.s.u.b2.v.g.dGl[r][c] = fromf<E>(dqk + lamr[j] * dg);
+        *(E*)(ring + SM::OG + tile_off<RC>(r, c * (int)ES)) = fromf<E>(dg);
+        *(E*)(ring + SM::OQK + tile_off<RC>(r, c * (int)ES)) = fromf<E>(dqk);
+        *(E*)(ring + SM::OY + tile_off<RC>(r, c * (int)ES)) = fromf<E>(dqk + lamr[j] * dg);
       }
-      sm.x.s.u.b2.ecc[4 * rb + (lane >> 4)][c] = ec;
+      ec += __shfl_xor(ec, 16, 64);
+      ec += __shfl_xor(ec, 32, 64);
+      if (lane < 16) sm.colp[1][w][c] = ec;
     }
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       dbr[j] = sum16(dbr[j]);
       er[j] = sum16(er[j]);
     }
-    if (cl == 0) {
+    if (fcol(lb) == 0) {
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
-        sm.rsum[0][ch][rw + j] = dbr[j];
-        sm.rsum[1][ch][rw + j] = er[j];
+        sm.rdbeta[r0 + j] = dbr[j];
+        sm.rer[r0 + j] = er[j];
       }
     }
   }
-  block_sync_lds();
-  if (tid < C) {
-    // dbeta = row parts + colsum(dT (.) M); db = row parts - column parts of the decay terms
-    float cb = 0.f, ce = 0.f;
-#pragma unroll
-    for (int v = 0; v < 16; ++v) {
-      cb += sm.x.s.u.b2.dbc[v][tid];
-      ce += sm.x.s.u.b2.ecc[v][tid];
-    }
-    sm.dbeta[tid] = sm.rsum[0][0][tid] + sm.rsum[0][1][tid] + cb;
-    sm.db[tid] = sm.rsum[1][0][tid] + sm.rsum[1][1][tid] - ce;
-  }
-  block_sync_lds();                    // the b2 buffers are dead past here
+  block_sync_lds();                        // dG, dQK, dQK + diag(lambda) dG complete
 
-  // ---------------- phase B3: dX, dq, dk (rows 16 rb.., Dk blocks of this half)
-  // K^T, Q^T and dW^T fragments are transpose reads of the row-major K, Q, dW
-  // kept since phase B1; dG^T, (dQK + diag(lambda) dG)^T and M^T likewise
-  // (T^T dW = diag(beta) M^T dW; dQK^T Q + dG^T X = dG^T K + (dQK + diag(lambda) dG)^T Q)
+  asm volatile("" : "+v"(lb));
+  // ---------------- phase B3: dX, dq, dk as transposes (key rows, this
+  // wave's chunk columns); the K^T, Q^T operands are transpose reads of the
+  // row-major K, Q tiles
   {
-    constexpr int NTK = C / KS;
-    FR tA[NTK], gA[NTK], qkA[NTK], gltA[NTK], gtA[NTK];
-    const E* dGp = &sm.x.s.u.b2.v.g.dG[0][0];
-    const E* dQKp = &sm.x.s.u.b2.v.g.dQK[0][0];
-    const E* dGlp = &sm.x.s.u.b2.v.g.dGl[0][0];
+    FR gB[NKC], qkB[NKC], gtB[NKC], gltB[NKC];
 #pragma unroll
-    for (int ks = 0; ks < NTK; ++ks) {
-      tA[ks] = tile_tr_frag<E, RBC>(sm.Mm, ks * KS, 16 * rb, lane);
-      gA[ks] = Frag<E>::load(kmaj(dGp, LC), 16 * rb, ks * KS, lane);
-      qkA[ks] = Frag<E>::load(kmaj(dQKp, LC), 16 * rb, ks * KS, lane);
-      gltA[ks] = tr_frag<E>(dGlp, LC, ks * KS, 16 * rb, lane);
-      gtA[ks] = tr_frag<E>(dGp, LC, ks * KS, 16 * rb, lane);
+    for (int ks = 0; ks < NKC; ++ks) {
+      gB[ks] = tile_frag<E, RC>(ring + SM::OG, 16 * w, ks * KS, lb);       // dG rows, as (r, c)
+      qkB[ks] = tile_frag<E, RC>(ring + SM::OQK, 16 * w, ks * KS, lb);     // dQK rows
+      gtB[ks] = tile_tr_frag<E, RC>(ring + SM::OG, ks * KS, 16 * w, lb);   // dG columns, as (r, c) of dG^T
+      gltB[ks] = tile_tr_frag<E, RC>(ring + SM::OY, ks * KS, 16 * w, lb);  // (dQK + diag(lambda) dG) columns
     }
-    const int r0 = 16 * rb + frow(lane, 0);
-    float rdb[4] = {0.f, 0.f, 0.f, 0.f}, rtk[4] = {0.f, 0.f, 0.f, 0.f}, rdl[4] = {0.f, 0.f, 0.f, 0.f};
-    float gr4[4], lr4[4], kbr4[4], br4[4];
+    const float gr = sm.g[rr], lr = sm.lam[rr], kbr = __expf(sm.b[C - 1] - sm.b[rr]);
+    float s1 = 0.f, s2 = 0.f, s3 = 0.f;
+    E* dqo = (E*)p.dq + (arow + (size_t)rr * H) * DK;
+    E* dko = (E*)p.dk + (arow + (size_t)rr * H) * DK;
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      gr4[j] = sm.g[r0 + j];
-      lr4[j] = sm.lam[r0 + j];
-      kbr4[j] = sm.kb[r0 + j];
-      br4[j] = sm.beta[r0 + j];
-    }
-    const E* Kp = &sm.x.s.b1.K[0][0];
-    const E* Qp = &sm.x.s.b1.Q[0][0];
-    const E* dWp = &sm.x.s.b1.dW[0][0];
+    for (int kb = 0; kb < NKB; ++kb) {
+      f4 dxp = zero4(), dqp = zero4(), dkp = zero4();
 #pragma unroll
-    for (int i = 0; i < HK; ++i) {
-      const int kb = kb0 + i;
-      f4 dgx = zero4(), dxp = zero4(), dqp = zero4(), dkp = zero4();
-#pragma unroll
-      for (int ks = 0; ks < NTK; ++ks) {
-        const FR ktB = tr_frag<E>(Kp, LKD, ks * KS, kb * 16, lane);
-        const FR qtB = tr_frag<E>(Qp, LKD, ks * KS, kb * 16, lane);
-        const FR dwB = tr_frag<E>(dWp, LKD, ks * KS, kb * 16, lane);
-        dgx = Mma<E>::mma(tA[ks], dwB, dgx);      // M^T dW
-        dxp = Mma<E>::mma(gA[ks], ktB, dxp);      // dG K
-        dqp = Mma<E>::mma(qkA[ks], ktB, dqp);     // dQK K
-        dkp = Mma<E>::mma(gtA[ks], ktB, dkp);     // dG^T K
-        dkp = Mma<E>::mma(gltA[ks], qtB, dkp);    // (dQK + diag(lambda) dG)^T Q
+      for (int ks = 0; ks < NKC; ++ks) {
+        const FR kT = tile_tr_frag<E, RK>(ring + SM::OK, ks * KS, kb * 16, lb);
+        const FR qT = tile_tr_frag<E, RK>(ring + SM::OQ, ks * KS, kb * 16, lb);
+        dxp = Mma<E>::mma(kT, gB[ks], dxp);        // (dG K)^T
+        dqp = Mma<E>::mma(kT, qkB[ks], dqp);       // (dQK K)^T
+        dkp = Mma<E>::mma(kT, gtB[ks], dkp);       // (dG^T K)^T
+        dkp = Mma<E>::mma(qT, gltB[ks], dkp);      // ((dQK + diag(lambda) dG)^T Q)^T
       }
-      const int kc = kb * 16 + fcol(lane);
-      const f4 kv = tr_col4(Kp, LKD, r0, kb * 16, lane);
-      const f4 qv = tr_col4(Qp, LKD, r0, kb * 16, lane);
+      const int kc = kb * 16 + frow(lb, 0);
+      const QR kq = *(const QR*)(ring + SM::OK + tile_off<RK>(rr, kc * (int)ES));
+      const QR qq = *(const QR*)(ring + SM::OQ + tile_off<RK>(rr, kc * (int)ES));
+      f4 oq, ok;
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
-        const int r = r0 + j;
-        const float Kv = kv[j], Qv = qv[j];
-        const float gr = gr4[j], lr = lr4[j], kbr = kbr4[j];
-        const float X = Kv + lr * Qv, tdw = br4[j] * dgx[j];   // (T^T dW)_r
-        rdb[j] += gr * (X * tdw + Qv * aQ[i][j]);
-        rtk[j] += kbr * Kv * aK[i][j];
+        const float Kv = Quad<E>::get(kq, j), Qv = Quad<E>::get(qq, j);
+        const float X = Kv + lr * Qv, tdw = tdwt[kb][j], aq = aQt[kb][j], ak = aKt[kb][j];
+        s1 += X * tdw + Qv * aq;
+        s2 += Kv * ak;
         const float dX = gr * tdw + dxp[j];
-        rdl[j] += Qv * dX;
-        sm.x.s.u.b3.oq[r][kc] = fromf<E>(gr * aQ[i][j] + dqp[j] + lr * dX);
-        sm.x.s.u.b3.ok[r][kc] = fromf<E>(kbr * aK[i][j] + dkp[j] + dX);
+        s3 += Qv * dX;
+        oq[j] = gr * aq + dqp[j] + lr * dX;
+        ok[j] = kbr * ak + dkp[j] + dX;
+      }
+      if (rr < len) {
+        *(QR*)(dqo + kc) = Quad<E>::pack(oq);
+        *(QR*)(dko + kc) = Quad<E>::pack(ok);
       }
     }
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      rdb[j] = sum16(rdb[j]);
-      rtk[j] = sum16(rtk[j]);
-      rdl[j] = sum16(rdl[j]);
-    }
-    if (fcol(lane) == 0) {
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        sm.rsum[2][ch][r0 + j] = rdb[j];
-        sm.rsum[3][ch][r0 + j] = rtk[j];
-        sm.rsum[4][ch][r0 + j] = rdl[j];
-      }
+    s1 += __shfl_xor(s1, 16, 64);
+    s1 += __shfl_xor(s1, 32, 64);
+    s2 += __shfl_xor(s2, 16, 64);
+    s2 += __shfl_xor(s2, 32, 64);
+    s3 += __shfl_xor(s3, 16, 64);
+    s3 += __shfl_xor(s3, 32, 64);
+    if (lane < 16) {
+      sm.rdb[rr] = gr * s1;
+      sm.rtk[rr] = kbr * s2;
+      sm.rdl[rr] = s3;
     }
   }
   block_sync_lds();
-  {
-    constexpr int VEC = 16 / sizeof(E), PR = DK / VEC;
-    E* dqo = (E*)p.dq + arow * DK;
-    E* dko = (E*)p.dk + arow * DK;
-    for (int idx = tid; idx < C * PR; idx += IT) {
-      const int r = idx / PR, cc = (idx % PR) * VEC;
-      if (r < len) {
-        *(uint4*)(dqo + (size_t)r * H * DK + cc) = *(const uint4*)&sm.x.s.u.b3.oq[r][cc];
-        *(uint4*)(dko + (size_t)r * H * DK + cc) = *(const uint4*)&sm.x.s.u.b3.ok[r][cc];
-      }
+  if (w == 0) {
+    // dbeta = row parts + column sums of dT (.) M; db = decay row parts -
+    // column parts + the B3 terms; Kbar terms: db_r -= t_r,
+    // db_{C-1} += sum_r t_r + g_C <dS', S>; then dlog alpha_j = sum_{r >= j} db_r
+    // (chunk-local reverse cumulative sum)
+    const int j = lane;
+    float cb_ = 0.f, ce = 0.f;
+#pragma unroll
+    for (int q = 0; q < NWAVES; ++q) {
+      cb_ += sm.colp[0][q][j];
+      ce += sm.colp[1][q][j];
     }
-  }
-  if (tid < C) {
-    // Kbar terms: db_r -= t_r, db_{C-1} += sum_r t_r + g_C <dS', S>;
-    // then dlog alpha_j = sum_{r >= j} db_r (chunk-local reverse cumulative sum)
-    const int j = tid;
-    const float tk = sm.rsum[3][0][j] + sm.rsum[3][1][j];
+    const float tk = sm.rtk[j];
     float tot = tk;
 #pragma unroll
     for (int off = 32; off >= 1; off >>= 1) tot += __shfl_xor(tot, off, 64);
-    float dbj = sm.db[j] + sm.rsum[2][0][j] + sm.rsum[2][1][j] - tk;
+    float dbj = sm.rer[j] - ce + sm.rdb[j] - tk;
     if (j == C - 1) {
       float sd = 0.f;
 #pragma unroll
-      for (int q = 0; q < 8; ++q) sd += sm.sdot[q];
+      for (int q = 0; q < NWAVES; ++q) sd += sm.sdot[q];
       dbj += tot + sm.g[C - 1] * sd;
     }
     float x = __shfl(dbj, C - 1 - j, 64);
-    x = wave_incl_scan(x, lane);
+    x = wave_incl_scan(x, lb);
     const float suffix = __shfl(x, C - 1 - j, 64);
     if (j < len) {
       const size_t gt = arow + (size_t)j * H;
-      p.dbeta[gt] = sm.dbeta[j];
-      p.dlam[gt] = sm.rsum[4][0][j] + sm.rsum[4][1][j];
+      p.dbeta[gt] = sm.rdbeta[j] + cb_;
+      p.dlam[gt] = sm.rdl[j];
       if (p.dla) p.dla[gt] = suffix;
     }
   }
@@ -885,8 +854,8 @@ static hipError_t launch_bwd_t(const Params& p, hipStream_t st) {
     // HBM idle half the time.  Half of the CUs start about half a unit later.
     Params q = p;
     const int total = p.n_slots * p.H, cus = device_cu_count();
-    q.lead = total >= 4 * cus ? cus / 2 : 0;
-    q.lead_cycles = 15000;
+    q.lead = total >= 8 * cus ? cus : 0;    // two workgroups per CU: half of the slots
+    q.lead_cycles = 20000;
     prof_mark(ST_INTRA, 0, st);
     hipLaunchKernelGGL((k_bwd_intra<E, DK, DV>), dim3(total + q.lead), dim3(INTRA_THREADS), 0, st, q);
     prof_mark(ST_INTRA, 1, st);
