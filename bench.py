@@ -1,17 +1,26 @@
-"""Benchmark: chunkwise Q-Delta forward + backward on one MI355X.
+"""Benchmark: chunkwise Q-Delta on one MI355X.
 
-A step is one pass of the whole hot path over one synthetic batch of the
-training-step layer shape (B=4, T=4096, H=16, d_k=d_v=128, chunk 64, bf16
-activations, fp32 gates and states): the chunk forward (writing the per-chunk
-states) followed by the chunk backward.  Inputs are resident in HBM before the
-timed region.  Prints one JSON line.
+The default workload (``--workload train``) is the training-step layer shape
+(B=4, T=4096, H=16, d_k=d_v=128, chunk 64, bf16 activations, fp32 gates and
+states).  A step is the chunk forward (writing the per-chunk saved context)
+followed by the chunk backward.  Inputs are resident in HBM before the timed
+region.  Prints one JSON line.
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--gate G2] [--no-cpu]
+                    [--workload train|fwd|long|decode|varlen|tiny]
+
+The other workloads are the layer's other shapes: ``fwd`` (forward only,
+B=8 T=2048 H=8 d=128), ``long`` (forward only, B=1 T=65536 H=16 d=128),
+``decode`` (1024 successive single-token steps of 64 sequences, H=16 d=128;
+a step of the benchmark is all 1024 of them), ``varlen`` (packed 32768 tokens,
+lognormal lengths, H=32 d_k=128 d_v=256, forward + backward) and ``tiny``
+(fp32 forward, B=1 T=256 H=2 d=64).
 
 `roofline` describes the kernel with the largest share of the step time; its
 duration is measured live with HIP events recorded around each of its
-launches on the launch stream.  `cpu_baseline` times the fp64 CPU oracle on a
-bounded sample of the same workload on this host's cores.
+launches on the launch stream.  `kernels` gives the same figures for every
+kernel of the step.  `cpu_baseline` times the fp64 CPU oracle on a bounded
+sample of the same workload on this host's cores.
 """
 import argparse
 import hashlib
@@ -30,8 +39,9 @@ from paper_2606_08804_amd import qdelta, synth  # noqa: E402
 
 HBM_PEAK = 8.0e12          # B/s, MI355X HBM3E
 MFMA_BF16_PEAK = 2.5e15    # flop/s, dense bf16 MFMA
-METRIC = "Q-Delta chunk fwd+bwd tokens/s (T=4096,H=16,d=128,bf16); % MFMA peak"
+MFMA_F32_PEAK = 157.3e12   # flop/s, dense fp32 MFMA
 C = 64
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_train_bf16_B4_T4096_H16_d128.json")
 
 
 def fwd_flops_per_token_head(Dk, Dv):
@@ -45,25 +55,43 @@ def bwd_flops_per_token_head(Dk, Dv):
     return 2.5 * fwd_flops_per_token_head(Dk, Dv)
 
 
-def stage_bytes_per_unit(stage, Dk, Dv, e):
+def stage_bytes_per_unit(stage, Dk, Dv, e, saved=True):
     """Bytes one (chunk, head) unit of a kernel stage must move: every tensor
     it consumes or produces, counted once (activations e bytes, gates and
-    states 4 bytes, workspace hand-offs in their stored precision)."""
+    states 4 bytes, workspace hand-offs in their stored precision).  `saved`
+    says whether the forward keeps the context for a backward."""
     act_qk = C * Dk * e
     act_v = C * Dv * e
     gates = C * 4
     state = Dv * Dk * 4
     cc_e = C * C * e
-    if stage in ("prep_fwd", "prep_bwd"):   # q, k, 3 gates -> gate block, P, M, T
-        return 2 * act_qk + 3 * gates + 3 * gates + 3 * cc_e
-    if stage == "scan_fwd":      # gate block, q, k, P, T, v -> o, state (dtype), D
-        return 3 * gates + 2 * act_qk + 2 * cc_e + act_v + act_v + state * e // 4 + act_v
+    if stage in ("prep_fwd", "prep_bwd"):
+        # q, k, 3 gates -> gate block, P, T (and M when the context is kept)
+        return 2 * act_qk + 3 * gates + 3 * gates + (3 if saved else 2) * cc_e
+    if stage == "scan_fwd":
+        # gate block, q, k, P, T, v -> o (and the entry state in the
+        # activation dtype and D when the context is kept)
+        b = 3 * gates + 2 * act_qk + 2 * cc_e + act_v + act_v
+        return b + (state * e // 4 + act_v if saved else 0)
     if stage == "scan_bwd":      # gate block, P, M, k, q, dO -> dS' (dtype), dD, dv
         return 3 * gates + 2 * cc_e + 2 * act_qk + act_v + state * e // 4 + act_v + act_v
     if stage == "intra":         # gate block, S, dS' (dtype), D, dD, dO, v, q, k, M
         #                          -> dq, dk, dbeta, dlam, dlog_alpha
         return 3 * gates + 2 * state * e // 4 + 4 * act_v + 2 * act_qk + cc_e + 2 * act_qk + 3 * gates
     raise KeyError(stage)
+
+
+def stage_bytes_per_seq(stage, Dk, Dv, has_s0):
+    """Per (sequence, head) bytes a stage moves once: the fp32 initial state
+    read (when there is one) and the final state written by the forward scan;
+    the initial-state gradient written by the backward scan (the benchmark
+    passes no final-state gradient)."""
+    st = Dv * Dk * 4
+    if stage == "scan_fwd":
+        return (2 if has_s0 else 1) * st
+    if stage == "scan_bwd":
+        return st
+    return 0
 
 
 def source_digest():
@@ -80,9 +108,8 @@ def source_digest():
 def stored_traffic(stage):
     """HBM bytes per launch from the committed rocprofv3 counter summary, or
     None when there is none or the kernels changed since it was taken."""
-    path = os.path.join(ROOT, "profiles", "traffic_train_bf16_B4_T4096_H16_d128.json")
     try:
-        with open(path) as f:
+        with open(TRAFFIC_FILE) as f:
             t = json.load(f)
     except (OSError, ValueError):
         return None
@@ -92,36 +119,214 @@ def stored_traffic(stage):
     return None if s is None else s.get("hbm_bytes_per_launch")
 
 
-def cpu_baseline(d, units_sample, min_seconds=10.0):
-    """Time the fp64 oracle (forward + backward) on a sample of the workload's
-    (sequence, head) units, over the full sequence length."""
+def cpu_baseline(d, heads, with_bwd, tokens_per_unit_run, min_seconds=10.0):
+    """Time the fp64 oracle (forward, plus the BPTT backward when `with_bwd`)
+    on the (sequence, head) units of `heads` over the full sequences, repeated
+    until about `min_seconds` have been timed; scaled to tokens/s of the
+    whole workload (every (sequence, head) unit costs the same per token)."""
     from oracle import build as obuild
     from oracle import recurrent
     obuild.build(force=False)
-    B, T, H = d["q"].shape[:3]
-    heads = list(range(min(H, max(1, units_sample // B))))
+    H = d["q"].shape[2]
     f = synth.to_f64
     sl = lambda x: None if x is None else x[:, :, heads].contiguous()
-    q, k, v = f(sl(d["q"])), f(sl(d["k"])), f(sl(d["v"]))
-    beta, lam, la = f(sl(d["beta"])), f(sl(d["lam"])), f(sl(d["log_alpha"]))
+    pk = (lambda x: x) if d["cu_seqlens"] is None else (lambda x: None if x is None else x[0])
+    q, k, v = pk(f(sl(d["q"]))), pk(f(sl(d["k"]))), pk(f(sl(d["v"])))
+    beta, lam, la = pk(f(sl(d["beta"]))), pk(f(sl(d["lam"]))), pk(f(sl(d["log_alpha"])))
     S0 = None if d["initial_state"] is None else f(d["initial_state"][:, heads].contiguous())
-    dO = f(sl(d["d_o"]))
+    dO = pk(f(sl(d["d_o"]))) if with_bwd else None
+    cu = None if d["cu_seqlens"] is None else d["cu_seqlens"].numpy()
     threads = recurrent.default_threads()
-    # repeat the sample until about 10 s of CPU work have been timed
     reps, t0 = 0, time.perf_counter()
     while True:
-        recurrent.fwd(q, k, v, beta, lam, la, S0, nthreads=threads)
-        recurrent.bwd(q, k, v, beta, lam, la, S0, d_o=dO, nthreads=threads)
+        recurrent.fwd(q, k, v, beta, lam, la, S0, cu_seqlens=cu, nthreads=threads)
+        if with_bwd:
+            recurrent.bwd(q, k, v, beta, lam, la, S0, d_o=dO, cu_seqlens=cu, nthreads=threads)
         reps += 1
         total = time.perf_counter() - t0
         if total >= min_seconds or reps >= 30:
             break
     dt = total / reps
-    units = B * len(heads)
-    tokens_per_s = (B * T) / (dt * (B * H) / units)
+    frac = len(heads) / H
+    tokens_per_s = tokens_per_unit_run / (dt / frac)
+    what = "forward + BPTT backward" if with_bwd else "forward"
     return {"value": tokens_per_s, "unit": "tokens/s", "cores": threads, "kind": "oracle",
-            "sample": f"fp64 recurrence forward + BPTT backward of {units} of {B * H} (sequence, head) "
-                      f"units over T={T}, {reps} passes in {total:.1f} s ({dt:.2f} s each), scaled to all units"}
+            "sample": f"fp64 recurrence {what} of {len(heads)} of {H} heads (all sequences, all tokens), "
+                      f"{reps} passes in {total:.1f} s ({dt:.2f} s each), scaled to all heads"}
+
+
+def chunk_units(d, H):
+    """(chunk, head) units the chunk kernels process."""
+    if d["cu_seqlens"] is None:
+        B, T = d["q"].shape[:2]
+        return B * ((T + C - 1) // C) * H
+    return sum((L + C - 1) // C for L in d["lengths"]) * H
+
+
+def kernel_rooflines(stages, d, Dk, Dv, e, saved):
+    """Per kernel: average launch duration (HIP events) and the HBM roofline
+    of its algorithmic bytes."""
+    H = d["q"].shape[2]
+    units = chunk_units(d, H)
+    nseq = (d["q"].shape[0] if d["cu_seqlens"] is None else len(d["lengths"])) * H
+    out = {}
+    for s, (tot_ms, launches) in stages.items():
+        if not launches:
+            continue
+        avg_s = tot_ms / launches / 1e3
+        b = stage_bytes_per_unit(s, Dk, Dv, e, saved) * units + stage_bytes_per_seq(s, Dk, Dv, d["initial_state"] is not None) * nseq
+        out[s] = {"avg_launch_us": avg_s * 1e6, "alg_bytes_per_launch": b,
+                  "achieved_GBps": b / avg_s / 1e9, "frac": b / avg_s / HBM_PEAK}
+    return out
+
+
+def roofline_of(kern, dom, traffic):
+    k = kern[dom]
+    return {"bound": "hbm", "kernel": dom, "achieved": k["achieved_GBps"], "peak": HBM_PEAK / 1e9,
+            "unit": "GB/s", "frac": k["frac"], "traffic": traffic,
+            "alg_bytes_per_launch": k["alg_bytes_per_launch"], "avg_launch_us": k["avg_launch_us"]}
+
+
+def timed(step, steps, warmup):
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    qdelta.profile_begin()
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    start.record()
+    for _ in range(steps):
+        step()
+    end.record()
+    torch.cuda.synchronize()
+    stages = qdelta.profile_end()
+    return start.elapsed_time(end) / steps, stages
+
+
+def run_chunk(args, wid, with_bwd):
+    """Chunk forward (+ backward) workloads."""
+    w = synth.WORKLOADS[wid]
+    d = synth.make_workload(wid, args.gate)
+    dev = {k: (v.cuda() if isinstance(v, torch.Tensor) else v) for k, v in d.items()}
+    B, T, H, Dk, Dv = d["q"].shape[0], d["q"].shape[1], w.H, w.Dk, w.Dv
+    cu = dev["cu_seqlens"]
+    n_seqs = 0 if cu is None else len(d["lengths"])
+    dt = qdelta.QDELTA_BF16 if w.dtype == "bf16" else qdelta.QDELTA_F32
+    e = 2 if w.dtype == "bf16" else 4
+    wsf = torch.empty(max(1, qdelta.workspace_bytes(B, T, H, Dk, Dv, dt, n_seqs, False)), dtype=torch.uint8,
+                      device="cuda")
+    wsb = torch.empty(max(1, qdelta.workspace_bytes(B, T, H, Dk, Dv, dt, n_seqs, True)), dtype=torch.uint8,
+                      device="cuda")
+    args_in = (dev["q"], dev["k"], dev["v"], dev["beta"], dev["lam"], dev["log_alpha"], dev["initial_state"])
+
+    if with_bwd:
+        def step():
+            o, Sf, saved = qdelta.chunk_fwd(*args_in, cu_seqlens=cu, save_states=True, workspace=wsf)
+            qdelta.chunk_bwd(*args_in, saved, dev["d_o"], cu_seqlens=cu, workspace=wsb)
+    else:
+        def step():
+            qdelta.chunk_fwd(*args_in, cu_seqlens=cu, save_states=False, workspace=wsf)
+
+    ms, stages = timed(step, args.steps, args.warmup)
+    tokens = B * T
+    value = tokens / (ms / 1e3)
+    kern = kernel_rooflines(stages, d, Dk, Dv, e, with_bwd)
+    dom = max(kern, key=lambda s: kern[s]["avg_launch_us"])
+    traffic = stored_traffic(dom) if wid == 3 else None
+    fl = fwd_flops_per_token_head(Dk, Dv) + (bwd_flops_per_token_head(Dk, Dv) if with_bwd else 0)
+    peak = MFMA_BF16_PEAK if w.dtype == "bf16" else MFMA_F32_PEAK
+    what = "fwd+bwd" if with_bwd else "fwd"
+    shape = (f"T={T},H={H},d={Dk},bf16" if wid == 3 else
+             f"{w.name.split(' ', 1)[1]}")
+    metric = ("Q-Delta chunk fwd+bwd tokens/s (T=4096,H=16,d=128,bf16); % MFMA peak" if wid == 3 else
+              f"Q-Delta chunk {what} tokens/s ({shape})")
+    cfg = {"workload": w.name, "B": B, "T": T, "H": H, "Dk": Dk, "Dv": Dv, "chunk": C,
+           "gate_mode": args.gate, "parallelism": "single GPU"}
+    if n_seqs:
+        cfg["n_seqs"] = n_seqs
+    out = {
+        "metric": metric, "value": value, "unit": "tokens/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": ms, "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": w.dtype, "data": "synthetic", "config": cfg,
+        "mfma_frac_step": tokens * H * fl / (ms / 1e3) / peak,
+        "kernel_avg_us": {s: round(k["avg_launch_us"], 2) for s, k in kern.items()},
+        "kernels": kern,
+        "roofline": roofline_of(kern, dom, traffic),
+    }
+    if not args.no_cpu:
+        nh = H if wid in (1, 4) else max(1, min(H, args.cpu_units // max(1, B if n_seqs == 0 else 1)))
+        if wid == 5:
+            nh = 2
+        heads = list(range(nh))
+        out["cpu_baseline"] = cpu_baseline(d, heads, with_bwd, tokens)
+    return out
+
+
+def run_decode(args):
+    """1024 successive single-token updates of 64 sequences (H=16, d=128)."""
+    wl = synth.WORKLOADS[4]
+    N, steps_dec = wl.extra["decode_N"], wl.extra["decode_steps"]
+    H, D = wl.H, wl.Dk
+    d = synth.make_decode(N, H, D, steps_dec, gate_mode=args.gate)
+    q, k, v = d["q"].cuda(), d["k"].cuda(), d["v"].cuda()
+    beta, lam = d["beta"].cuda(), d["lam"].cuda()
+    la = d["log_alpha"].cuda() if d["log_alpha"] is not None else None
+    S0 = d["initial_state"].cuda()
+    S = S0.clone()
+    outs = torch.empty((steps_dec, N, H, D), dtype=torch.bfloat16, device="cuda")
+
+    def step():
+        S.copy_(S0)
+        for s in range(steps_dec):
+            qdelta.recurrent_step(q[s], k[s], v[s], beta[s], lam[s], None if la is None else la[s], S,
+                                  out=outs[s])
+
+    ms, stages = timed(step, args.steps, args.warmup)
+    tokens = N * steps_dec
+    tot_ms, launches = stages["step"]
+    avg_s = tot_ms / launches / 1e3
+    b = N * H * (2 * D * D * 4 + 4 * D * 2 + 3 * 4)
+    kern = {"step": {"avg_launch_us": avg_s * 1e6, "alg_bytes_per_launch": b,
+                     "achieved_GBps": b / avg_s / 1e9, "frac": b / avg_s / HBM_PEAK}}
+    out = {
+        "metric": "Q-Delta recurrent decode tokens/s (64 seqs x 1024 steps, H=16, d=128, bf16)",
+        "value": tokens / (ms / 1e3), "unit": "tokens/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": ms, "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": "decode 64 seqs x 1024 steps H16 d128", "N": N, "H": H, "Dk": D, "Dv": D,
+                   "decode_steps": steps_dec, "gate_mode": args.gate, "parallelism": "single GPU",
+                   "note": "a benchmark step is all 1024 decode steps (one launch each) plus one state reset copy"},
+        "us_per_decode_step": ms * 1e3 / steps_dec,
+        "kernel_avg_us": {"step": round(avg_s * 1e6, 2)},
+        "kernels": kern,
+        "roofline": roofline_of(kern, "step", None),
+    }
+    if not args.no_cpu:
+        from oracle import build as obuild
+        from oracle import recurrent
+        obuild.build(force=False)
+        f = synth.to_f64
+        nseq = 16
+        ref = {key: f(d[key][:, :nseq].transpose(0, 1).contiguous()) for key in ("q", "k", "v", "beta", "lam")}
+        lar = None if d["log_alpha"] is None else f(d["log_alpha"][:, :nseq].transpose(0, 1).contiguous())
+        S0r = f(d["initial_state"][:nseq])
+        threads = recurrent.default_threads()
+        reps, t0 = 0, time.perf_counter()
+        while True:
+            recurrent.fwd(ref["q"], ref["k"], ref["v"], ref["beta"], ref["lam"], lar, S0r, nthreads=threads)
+            reps += 1
+            total = time.perf_counter() - t0
+            if total >= 10.0 or reps >= 30:
+                break
+        dt = total / reps
+        out["cpu_baseline"] = {
+            "value": nseq * steps_dec / dt, "unit": "tokens/s", "cores": threads, "kind": "oracle",
+            "sample": f"fp64 recurrence over the same 1024 tokens for {nseq} of {N} sequences (all {H} heads), "
+                      f"{reps} passes in {total:.1f} s ({dt:.2f} s each)"}
+    return out
+
+
+WORKLOAD_IDS = {"train": 3, "fwd": 2, "long": 4, "varlen": 5, "tiny": 1}
 
 
 def main():
@@ -130,6 +335,7 @@ def main():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--gate", default="G2", choices=["G1", "G2", "G3"])
+    ap.add_argument("--workload", default="train", choices=["train", "fwd", "long", "decode", "varlen", "tiny"])
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--cpu-units", type=int, default=64)
     ap.add_argument("--calib-copy", type=int, default=0, metavar="MIB",
@@ -144,60 +350,11 @@ def main():
         print("no GPU visible", file=sys.stderr)
         sys.exit(1)
 
-    w = synth.WORKLOADS[3]
-    d = synth.make_workload(3, args.gate)
-    dev = {k: (v.cuda() if isinstance(v, torch.Tensor) else v) for k, v in d.items()}
-    B, T, H, Dk, Dv = w.B, w.T, w.H, w.Dk, w.Dv
-    dt = qdelta.QDELTA_BF16
-    wsf = torch.empty(qdelta.workspace_bytes(B, T, H, Dk, Dv, dt, 0, False), dtype=torch.uint8, device="cuda")
-    wsb = torch.empty(qdelta.workspace_bytes(B, T, H, Dk, Dv, dt, 0, True), dtype=torch.uint8, device="cuda")
-    args_in = (dev["q"], dev["k"], dev["v"], dev["beta"], dev["lam"], dev["log_alpha"], dev["initial_state"])
-
-    def step():
-        o, Sf, saved = qdelta.chunk_fwd(*args_in, save_states=True, workspace=wsf)
-        g = qdelta.chunk_bwd(*args_in, saved, dev["d_o"], workspace=wsb)
-        return o, g
-
-    for _ in range(args.warmup):
-        step()
-    torch.cuda.synchronize()
-    qdelta.profile_begin()
-    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    start.record()
-    for _ in range(args.steps):
-        step()
-    end.record()
-    torch.cuda.synchronize()
-    stages = qdelta.profile_end()
-    ms = start.elapsed_time(end) / args.steps
-    tokens = B * T
-    value = tokens / (ms / 1e3)
-
-    # dominant kernel and its roofline
-    dom = max(stages, key=lambda s: stages[s][0])
-    tot_ms, launches = stages[dom]
-    avg_s = tot_ms / launches / 1e3
-    units = qdelta.saved_state_slots(B, T) * H
-    alg_bytes = stage_bytes_per_unit(dom, Dk, Dv, 2) * units
-    achieved = alg_bytes / avg_s / 1e9
-    traffic = stored_traffic(dom)
-    roof = {"bound": "hbm", "kernel": dom, "achieved": achieved, "peak": HBM_PEAK / 1e9, "unit": "GB/s",
-            "frac": achieved / (HBM_PEAK / 1e9), "traffic": traffic,
-            "alg_bytes_per_launch": alg_bytes, "avg_launch_us": avg_s * 1e6}
-    step_flops = tokens * H * (fwd_flops_per_token_head(Dk, Dv) + bwd_flops_per_token_head(Dk, Dv))
-    breakdown = {s: round(v[0] / max(1, v[1]) * 1e3, 2) for s, v in stages.items() if v[1]}
-
-    out = {
-        "metric": METRIC, "value": value, "unit": "tokens/s", "n_gpus": 1, "steps": args.steps,
-        "warmup": args.warmup, "ms_per_step": ms, "higher_is_better": True, "scaling": "weak",
-        "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
-        "config": {"workload": w.name, "B": B, "T": T, "H": H, "Dk": Dk, "Dv": Dv, "chunk": C,
-                   "gate_mode": args.gate, "parallelism": "single GPU"},
-        "mfma_frac_step": step_flops / (ms / 1e3) / MFMA_BF16_PEAK,
-        "kernel_avg_us": breakdown,
-        "roofline": roof,
-    }
+    if args.workload == "decode":
+        out = run_decode(args)
+    else:
+        wid = WORKLOAD_IDS[args.workload]
+        out = run_chunk(args, wid, synth.WORKLOADS[wid].bwd)
     if args.calib_copy > 0:
         src = torch.ones(args.calib_copy << 20, dtype=torch.uint8, device="cuda")
         dst = torch.empty_like(src)
@@ -205,8 +362,6 @@ def main():
             dst.copy_(src)
         torch.cuda.synchronize()
         out["calib_copy_bytes"] = args.calib_copy << 20
-    if not args.no_cpu:
-        out["cpu_baseline"] = cpu_baseline(d, args.cpu_units)
     print(json.dumps(out), flush=True)
 
 

@@ -16,7 +16,7 @@ using qd::C;
 constexpr int kVersion = 10000;  // 1.0.0
 
 struct Layout {
-  size_t wb = 0, wT = 0, wP = 0, wM = 0;   // forward: chunk factors (T always, the rest when no saved context is kept)
+  size_t wb = 0, wT = 0, wP = 0;   // forward: chunk factors (T always, gates and P when no saved context is kept)
   size_t dSo = 0, dDb = 0, ctx = 0;        // backward: scan outputs, room to recompute the context
   size_t total = 0;
 };
@@ -54,7 +54,6 @@ Layout make_layout(size_t units, int Dk, int Dv, int esz, bool bwd) {
   } else {
     L.wb = take(units * 3 * C * 4);
     L.wP = take(units * C * C * esz);
-    L.wM = take(units * C * C * esz);
   }
   L.total = off;
   return L;
@@ -160,7 +159,7 @@ int fwd_impl(bool varlen, int32_t B, int32_t T, int32_t N, const int32_t* cu, in
   } else {
     p.wb = reinterpret_cast<float*>(w + L.wb);
     p.wP = w + L.wP;
-    p.wM = w + L.wM;
+    p.wM = nullptr;    // M feeds only the backward
   }
   hipError_t e = qd::launch_fwd(p, dtype, Dk, Dv, 0, 1, stream);
   return e == hipSuccess ? QDELTA_OK : QDELTA_EHIP;

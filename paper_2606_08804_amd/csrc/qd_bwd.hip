@@ -50,8 +50,11 @@ struct ScanBwdRing {
   static constexpr int RK = DK * (int)sizeof(E), RC = C * (int)sizeof(E), RO = BV * (int)sizeof(E);
   static constexpr int XQ = 0, XK = XQ + C * RK, XO = XK + C * RK, XG = XO + C * RO, XBYTES = XG + 3 * C * 4;
   static constexpr int MBYTES = C * RC;
-  static constexpr int NA = sizeof(E) == 2 ? 3 : 2;
-  static constexpr int NP = sizeof(E) == 2 ? 2 : 1;         // P buffers
+  // ring depths: fp32 tiles and 64-column value tiles leave room for two
+  // chunks of set X and one P buffer
+  static constexpr bool DEEP = sizeof(E) == 2 && BV == 32;
+  static constexpr int NA = DEEP ? 3 : 2;
+  static constexpr int NP = DEEP ? 2 : 1;                   // P buffers
   static constexpr int LQ = C * RK / 1024 / 4;              // loads per producer: Q
   static constexpr int LK = (C * RK + C * RO) / 1024 / 4;   // K and dO (plus one gate vector for producers 0-2)
   static constexpr int LM = C * RC / 1024 / 4;              // M, and P
@@ -840,12 +843,19 @@ __global__ __launch_bounds__(INTRA_THREADS) __attribute__((amdgpu_waves_per_eu(2
 // ------------------------------------------------------------------ launchers
 template <typename E, int DK, int DV>
 static hipError_t launch_bwd_t(const Params& p, hipStream_t st) {
-  constexpr int SBV = 32;   // value columns per backward-scan workgroup
   const int units = p.N * p.H;
-  const int nb = ((units + 7) / 8) * 8 * (DV / SBV);
+  const int bv = scan_bv<E, DV>(units);
+  const int nb = ((units + 7) / 8) * 8 * (DV / bv);
   if (nb > 0) {
     prof_mark(ST_SCAN_BWD, 0, st);
-    hipLaunchKernelGGL((k_scan_bwd<E, DK, DV, SBV>), dim3(nb), dim3(NTHREADS + 256), 0, st, p);
+    if constexpr (scan_bv_max<E, DV>() == 64) {
+      if (bv == 64)
+        hipLaunchKernelGGL((k_scan_bwd<E, DK, DV, 64>), dim3(nb), dim3(NTHREADS + 256), 0, st, p);
+      else
+        hipLaunchKernelGGL((k_scan_bwd<E, DK, DV, 32>), dim3(nb), dim3(NTHREADS + 256), 0, st, p);
+    } else {
+      hipLaunchKernelGGL((k_scan_bwd<E, DK, DV, 32>), dim3(nb), dim3(NTHREADS + 256), 0, st, p);
+    }
     prof_mark(ST_SCAN_BWD, 1, st);
   }
   if (p.n_slots > 0) {

@@ -769,6 +769,20 @@ __device__ inline float wave_incl_scan(float x, int lane) {
   return x;
 }
 
+// Value rows per scan workgroup.  Every value tile of a (sequence, head)
+// re-reads the chunk operands shared by all its tiles (Q, K, T, P, gates), so
+// wider tiles move fewer bytes per unit of work; 64-row tiles (bf16 only, for
+// LDS room) are used once they still give every CU at least two workgroups.
+template <typename E, int DV>
+constexpr int scan_bv_max() {
+  return (sizeof(E) == 2 && DV >= 64) ? 64 : 32;
+}
+template <typename E, int DV>
+inline int scan_bv(int units) {
+  if (scan_bv_max<E, DV>() == 64 && (long long)units * (DV / 64) >= 2LL * device_cu_count()) return 64;
+  return 32;
+}
+
 // XCD-aware mapping of a flat block id onto (unit, tile) pairs so that all
 // tiles of one unit are dispatched to the same XCD (blocks are handed to the
 // 8 XCDs round-robin).  Returns false for padding blocks.

@@ -61,8 +61,8 @@ __device__ inline void store_tile(E* dst, const E* src, int ld, int tid) {
 }
 
 // Writes, for every unit, the gate block (b, beta, lambda), the intra-chunk
-// output operator P = Gam * M_causal * Q K^T, M = (I + A)^{-1} and
-// T = M diag(beta).  Persistent: each workgroup walks units blockIdx.x,
+// output operator P = Gam * M_causal * Q K^T, M = (I + A)^{-1} (when p.wM is
+// set) and T = M diag(beta).  Persistent: each workgroup walks units blockIdx.x,
 // +gridDim.x, ... and prefetches the next unit's inputs into registers while
 // computing the current one.
 template <typename E, int DK, int DV>
@@ -148,13 +148,15 @@ __global__ __launch_bounds__(PREP_THREADS) void k_prep(Params p) {
     block_sync_lds();
     store_tile<E, C, NT>((E*)p.wP + gi * C * C, &sm.Pm[0][0], LC, tid);
 
-    // UT solve: M = (I + A)^{-1}; M and T = M diag(beta) are stored with
+    // UT solve: M = (I + A)^{-1}; M (only the backward reads it, so only
+    // when the context is kept) and T = M diag(beta) are stored with
     // strictly-upper 16 x 16 blocks zero; a thread takes VEC consecutive
     // columns of one row
     unit_lower_inverse<NT>(&sm.A[0][0], C + 4, &sm.M[0][0], C + 4, tid);
     {
+      const bool keep_m = p.wM != nullptr;
       constexpr int VEC = 16 / sizeof(E);
-      E* wM = (E*)p.wM + gi * C * C;
+      E* wM = keep_m ? (E*)p.wM + gi * C * C : nullptr;
       E* wT = (E*)p.wT + gi * C * C;
       for (int idx = tid; idx < C * C / VEC; idx += NT) {
         const int r = idx / (C / VEC), i0 = (idx % (C / VEC)) * VEC;
@@ -174,7 +176,7 @@ __global__ __launch_bounds__(PREP_THREADS) void k_prep(Params p) {
           me[j] = fromf<E>(m);
           te[j] = fromf<E>(m * bv[j]);
         }
-        *(uint4*)(wM + r * C + i0) = mr;
+        if (keep_m) *(uint4*)(wM + r * C + i0) = mr;
         *(uint4*)(wT + r * C + i0) = tr;
       }
     }
@@ -195,8 +197,11 @@ struct ScanFwdRing {
   static constexpr int RK = DK * (int)sizeof(E), RC = C * (int)sizeof(E), RO = BV * (int)sizeof(E);   // row bytes
   static constexpr int AQ = 0, AK = AQ + C * RK, AG = AK + C * RK, ABYTES = AG + 3 * C * 4;
   static constexpr int BT = 0, BV_ = BT + C * RC, BBYTES = BV_ + C * RO;
-  static constexpr int NA = sizeof(E) == 2 ? 3 : 2;         // fp32 tiles are twice as large
-  static constexpr int NP = sizeof(E) == 2 ? 2 : 1;         // P buffers
+  // ring depths: fp32 tiles and 64-column value tiles leave room for two
+  // chunks of set A and one P buffer
+  static constexpr bool DEEP = sizeof(E) == 2 && BV == 32;
+  static constexpr int NA = DEEP ? 3 : 2;
+  static constexpr int NP = DEEP ? 2 : 1;                   // P buffers
   static constexpr int LQ = C * RK / 1024 / 4;              // loads per producer: Q
   static constexpr int LK = C * RK / 1024 / 4;              // K (plus one gate vector for producers 0-2)
   static constexpr int LB = (C * RC + C * RO) / 1024 / 4;   // T and V
@@ -379,12 +384,8 @@ __global__ __launch_bounds__(NTHREADS + 256) void k_scan_fwd(Params p) {
           *(uint4*)(dst + (size_t)r * DK + cc) = *(const uint4*)&sm.S[r][cc];
         }
       }
-      FR sa[NB][NKS];
-#pragma unroll
-      for (int nb = 0; nb < NB; ++nb)
-#pragma unroll
-        for (int ks = 0; ks < NKS; ++ks) sa[nb][ks] = Frag<E>::load(kmaj(&sm.S[0][0], LK), nb * 16, ks * KS, lane);
-      // (S K^T), (S Q^T): value rows, chunk columns 16w..
+      // (S K^T), (S Q^T): value rows, chunk columns 16w..; the S fragments
+      // of one k step at a time are live
       f4 sk[NB];
 #pragma unroll
       for (int nb = 0; nb < NB; ++nb) sk[nb] = sq[nb] = zero4();
@@ -394,8 +395,9 @@ __global__ __launch_bounds__(NTHREADS + 256) void k_scan_fwd(Params p) {
         const FR qB = tile_frag<E, R::RK>(ra + R::AQ, 16 * w, ks * KS, lane);
 #pragma unroll
         for (int nb = 0; nb < NB; ++nb) {
-          sk[nb] = Mma<E>::mma(sa[nb][ks], kB, sk[nb]);
-          sq[nb] = Mma<E>::mma(sa[nb][ks], qB, sq[nb]);
+          const FR sa = Frag<E>::load(kmaj(&sm.S[0][0], LK), nb * 16, ks * KS, lane);
+          sk[nb] = Mma<E>::mma(sa, kB, sk[nb]);
+          sq[nb] = Mma<E>::mma(sa, qB, sq[nb]);
         }
       }
       const float gr = __expf(gb[rr]), ngr = -gr, lr = gb[2 * C + rr];
@@ -551,10 +553,12 @@ __global__ __launch_bounds__(NTHREADS + 256) void k_scan_fwd(Params p) {
 // ------------------------------------------------------------------ launchers
 template <typename E, int DK, int DV>
 static hipError_t launch_fwd_t(const Params& p, int in_bwd, int with_scan, hipStream_t st) {
-  constexpr int BV = 32;   // value columns per forward-scan workgroup
   if (p.n_slots > 0) {
     const int units = p.n_slots * p.H;
-    dim3 gp(min(units, device_cu_count()));
+    // two persistent workgroups per CU where each takes at most half the
+    // LDS, so that one's UT solve overlaps the other's loads
+    constexpr int per_cu = sizeof(PrepSmem<E, DK>) <= 80 * 1024 ? 2 : 1;
+    dim3 gp(min(units, per_cu * device_cu_count()));
     const int stage = in_bwd ? ST_PREP_BWD : ST_PREP_FWD;
     prof_mark(stage, 0, st);
     hipLaunchKernelGGL((k_prep<E, DK, DV>), gp, dim3(PREP_THREADS), 0, st, p);
@@ -562,10 +566,18 @@ static hipError_t launch_fwd_t(const Params& p, int in_bwd, int with_scan, hipSt
   }
   if (with_scan) {
     const int units = p.N * p.H;
-    const int nb = ((units + 7) / 8) * 8 * (DV / BV);
+    const int bv = scan_bv<E, DV>(units);
+    const int nb = ((units + 7) / 8) * 8 * (DV / bv);
     if (nb > 0) {
       prof_mark(ST_SCAN_FWD, 0, st);
-      hipLaunchKernelGGL((k_scan_fwd<E, DK, DV, BV>), dim3(nb), dim3(NTHREADS + 256), 0, st, p);
+      if constexpr (scan_bv_max<E, DV>() == 64) {
+        if (bv == 64)
+          hipLaunchKernelGGL((k_scan_fwd<E, DK, DV, 64>), dim3(nb), dim3(NTHREADS + 256), 0, st, p);
+        else
+          hipLaunchKernelGGL((k_scan_fwd<E, DK, DV, 32>), dim3(nb), dim3(NTHREADS + 256), 0, st, p);
+      } else {
+        hipLaunchKernelGGL((k_scan_fwd<E, DK, DV, 32>), dim3(nb), dim3(NTHREADS + 256), 0, st, p);
+      }
       prof_mark(ST_SCAN_FWD, 1, st);
     }
   }

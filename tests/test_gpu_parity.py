@@ -60,6 +60,17 @@ def test_fwd_empty_sequence_passes_state_through():
     assert torch.equal(Sf.cpu(), d["initial_state"])
 
 
+@pytest.mark.parametrize("Dk,Dv,B,H,T", [(128, 256, 4, 32, 130), (128, 128, 8, 32, 100), (64, 64, 16, 32, 70)])
+def test_wide_value_tiles(Dk, Dv, B, H, T):
+    """Enough (sequence, head) units that the scans take 64-row value tiles
+    (units x Dv/64 >= 2 x 256 CUs), forward and backward, ragged last chunk."""
+    d = synth.make(B, T, H, Dk, Dv, "bf16", "G3", seed=110 + Dv, s0=True, with_do=True)
+    o, Sf, saved = gpu_fwd(d, save_states=True)
+    _check(fwd_errors(d, o, Sf), TOL["bf16"], f"fwd wide tiles Dk={Dk} Dv={Dv}")
+    g = gpu_bwd(d, saved)
+    _check(bwd_errors(d, g), TOL["bf16"], f"bwd wide tiles Dk={Dk} Dv={Dv}")
+
+
 @pytest.mark.parametrize("gate", GATES)
 @pytest.mark.parametrize("Dv", [64, 128])
 def test_bwd_fp32(gate, Dv):
