@@ -115,7 +115,7 @@ __global__ __launch_bounds__(NTHREADS + 256) void k_scan_bwd(Params p) {
   // fp32 operands take 4-deep k-steps; their long k loops are only partly unrolled
   constexpr int UKD = NKS > 4 ? 4 : NKS;
   __shared__ ScanBwdSmem<E, DK, BV> sm;
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63, w = wave_id(tid);
   const int prod = w - NWAVES;               // 0-3 for the producer waves, negative otherwise
   const bool producer = prod >= 0;
   int unit, vt;
@@ -445,7 +445,7 @@ __global__ __launch_bounds__(INTRA_THREADS) __attribute__((amdgpu_waves_per_eu(2
     return;
   }
   const int bid = (int)blockIdx.x - p.lead;
-  const int g = bid % p.n_slots, h = bid / p.n_slots, tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int g = bid % p.n_slots, h = bid / p.n_slots, tid = threadIdx.x, lane = tid & 63, w = wave_id(tid);
   int n, t0, len;
   if (!locate(p, g, n, t0, len)) return;
   const int H = p.H;

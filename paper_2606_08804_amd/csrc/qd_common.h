@@ -20,6 +20,10 @@ constexpr int NTHREADS = 256;  // 4 wave64s per workgroup
 constexpr int NWAVES = NTHREADS / 64;
 
 typedef float f4 __attribute__((ext_vector_type(4)));
+
+// Wave index within the workgroup, in a scalar register: branches on it are
+// uniform, so they compile to scalar branches instead of exec-mask regions.
+__device__ inline int wave_id(int tid) { return __builtin_amdgcn_readfirstlane(tid >> 6); }
 typedef __bf16 bf8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf4 __attribute__((ext_vector_type(4)));
 
@@ -171,13 +175,10 @@ template <> struct Quad<__bf16> {
     const __bf16* e = (const __bf16*)&r;
     return (float)e[j];
   }
-  __device__ static inline raw pack(f4 x) {
-    raw r;
-    __bf16* e = (__bf16*)&r;
-#pragma unroll
-    for (int j = 0; j < 4; ++j) e[j] = (__bf16)x[j];
-    return r;
-  }
+  // one vector conversion, so that each pair of values takes a single
+  // two-source v_cvt_pk_bf16_f32 (element-wise conversions are rejoined with
+  // shifts and ors)
+  __device__ static inline raw pack(f4 x) { return __builtin_bit_cast(raw, __builtin_convertvector(x, bf4)); }
 };
 template <> struct Quad<float> {
   typedef uint4 raw;
@@ -406,10 +407,24 @@ __device__ inline void dma_block_asm(char* dst, const char* src, int lane) {
 // MFMA fragment (A or B operand; both map lane l to row l & 15 and to the
 // KPL consecutive k from (l >> 4) * KPL) read from a swizzled LDS tile of
 // element type E.
+//
+// 16-bit fragments start at a row that is a multiple of 16, so the swizzle of
+// each lane's row depends on the lane alone, and at a k offset that is a
+// multiple of 32 elements (whole groups of four 16-byte chunks), which enters
+// the chunk index as an XOR: the address is row0 RB + (frag_x(l) ^ 2 k0), one
+// lane constant per row size, and the rest folds into the instruction offset.
+template <int RB>
+__device__ inline int frag_x(int lane) {
+  return (lane & 15) * RB + (((lane >> 4) ^ tile_swz<RB>(lane & 15)) << 4);
+}
 template <typename E, int RB>
 __device__ inline typename Mma<E>::frag tile_frag(const char* t, int row0, int k0, int lane) {
-  const int row = row0 + (lane & 15), k = k0 + (lane >> 4) * Mma<E>::KPL;
-  return *(const typename Mma<E>::frag*)(t + tile_off<RB>(row, k * (int)sizeof(E)));
+  if constexpr (sizeof(E) == 2) {
+    return *(const typename Mma<E>::frag*)(t + row0 * RB + (frag_x<RB>(lane) ^ (2 * k0)));
+  } else {
+    const int row = row0 + (lane & 15), k = k0 + (lane >> 4) * Mma<E>::KPL;
+    return *(const typename Mma<E>::frag*)(t + tile_off<RB>(row, k * (int)sizeof(E)));
+  }
 }
 // Fragment of the TRANSPOSE of a swizzled LDS tile (rows of RB bytes): for
 // lane l the values at tile rows k0 + (l >> 4) * KPL + e, e < KPL, and column
@@ -417,15 +432,24 @@ __device__ inline typename Mma<E>::frag tile_frag(const char* t, int row0, int k
 // the tile column.  16-bit tiles use the LDS transpose read (see tr_frag
 // below): each 8-byte piece lies inside one 16-byte chunk, so the swizzle
 // applies per piece.
+//
+// With k0 a multiple of 16 and j0 a multiple of 16, the two 8-byte pieces of
+// lane l sit at k0 RB + (tr_y(l, 0) ^ 2 j0) and k0 RB + (tr_y(l, 4) ^ 2 j0)
+// (same reasoning as frag_x: the row swizzle depends on the lane alone and
+// the column offset is an XOR of whole chunk pairs).
+template <int RB>
+__device__ inline int tr_y(int lane, int dr) {
+  const int L = lane & 15, r = (lane >> 4) * 8 + (L >> 2) + dr;
+  return r * RB + ((((L & 3) >> 1) ^ tile_swz<RB>(r & 15)) << 4) + 8 * (L & 1);
+}
 template <typename E, int RB>
 __device__ inline typename Mma<E>::frag tile_tr_frag(const char* t, int k0, int j0, int lane) {
   if constexpr (sizeof(E) == 2) {
     typedef __bf16 v4b __attribute__((ext_vector_type(4)));
     typedef __attribute__((address_space(3))) v4b* lp;
-    const int L = lane & 15, i0 = k0 + (lane >> 4) * 8 + (L >> 2), jb = 2 * (j0 + 4 * (L & 3));
-    const v4b lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lp)(uintptr_t)(uint32_t)(uintptr_t)(t + tile_off<RB>(i0, jb)));
-    const v4b hi =
-        __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lp)(uintptr_t)(uint32_t)(uintptr_t)(t + tile_off<RB>(i0 + 4, jb)));
+    const char* b = t + k0 * RB;
+    const v4b lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lp)(uintptr_t)(uint32_t)(uintptr_t)(b + (tr_y<RB>(lane, 0) ^ (2 * j0))));
+    const v4b hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lp)(uintptr_t)(uint32_t)(uintptr_t)(b + (tr_y<RB>(lane, 4) ^ (2 * j0))));
     return __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
   } else {
     return *(const float*)(t + tile_off<RB>(k0 + (lane >> 4), 4 * (j0 + (lane & 15))));
@@ -691,7 +715,7 @@ __device__ inline float sum16(float x) {
 template <int NT>
 __device__ inline void unit_lower_inverse(float* sA, int lda, float* sM, int ldm, int tid) {
   static_assert(NT == 512, "eight waves");
-  const int lane = tid & 63, w = tid >> 6;
+  const int lane = tid & 63, w = wave_id(tid);
   auto blkA = [&](int i, int j) { return sA + (size_t)(16 * i) * lda + 16 * j; };
   auto blkM = [&](int i, int j) { return sM + (size_t)(16 * i) * ldm + 16 * j; };
   auto put = [&](float* dst, int ld, f4 v, float sc) {

@@ -72,7 +72,7 @@ __global__ __launch_bounds__(PREP_THREADS) void k_prep(Params p) {
   constexpr int LK = DK + P, LC = C + P;
   typedef PrepPre<E, DK> Pre;
   __shared__ PrepSmem<E, DK> sm;
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63, w = wave_id(tid);
   const int H = p.H;
   const int total = p.n_slots * H;
 
@@ -262,7 +262,7 @@ __global__ __launch_bounds__(NTHREADS + 256) void k_scan_fwd(Params p) {
   typedef ScanFwdRing<E, DK, BV> R;
   constexpr int NA = R::NA;
   __shared__ ScanFwdSmem<E, DK, BV> sm;
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63, w = wave_id(tid);
   const int prod = w - NWAVES;                // 0-3 for the producer waves, negative otherwise
   const bool producer = prod >= 0;
   int unit, vt;
