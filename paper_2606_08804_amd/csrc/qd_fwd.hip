@@ -555,10 +555,9 @@ template <typename E, int DK, int DV>
 static hipError_t launch_fwd_t(const Params& p, int in_bwd, int with_scan, hipStream_t st) {
   if (p.n_slots > 0) {
     const int units = p.n_slots * p.H;
-    // two persistent workgroups per CU where each takes at most half the
-    // LDS, so that one's UT solve overlaps the other's loads
-    constexpr int per_cu = sizeof(PrepSmem<E, DK>) <= 80 * 1024 ? 2 : 1;
-    dim3 gp(min(units, per_cu * device_cu_count()));
+    // one persistent workgroup per CU (a second one per CU measured no
+    // faster: each ran at half speed)
+    dim3 gp(min(units, device_cu_count()));
     const int stage = in_bwd ? ST_PREP_BWD : ST_PREP_FWD;
     prof_mark(stage, 0, st);
     hipLaunchKernelGGL((k_prep<E, DK, DV>), gp, dim3(PREP_THREADS), 0, st, p);
