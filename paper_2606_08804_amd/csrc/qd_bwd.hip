@@ -241,7 +241,7 @@ __global__ __launch_bounds__(NTHREADS + 256) void k_scan_bwd(Params p) {
       // + dO^T P (P causal: k blocks before this wave's key rows are skipped)
 #pragma unroll
       for (int ks = 0; ks < C / KS; ++ks)
-        if (ks * KS + KS > 16 * w) {
+        if (keep_kblock<E>(ks * KS + KS > 16 * w)) {
           const FR pB = tile_tr_frag<E, R::RC>(sm.ringP[it % R::NP], ks * KS, 16 * w, lane);
 #pragma unroll
           for (int nb = 0; nb < NB; ++nb)
@@ -287,7 +287,7 @@ __global__ __launch_bounds__(NTHREADS + 256) void k_scan_bwd(Params p) {
         f4 dv = zero4();
 #pragma unroll
         for (int ks = 0; ks < C / KS; ++ks)
-          if (ks * KS + KS > 16 * w)
+          if (keep_kblock<E>(ks * KS + KS > 16 * w))
             dv = Mma<E>::mma(tr_frag<E>(&sm.dD[0][0], LV, ks * KS, nb * 16, lane),
                              tile_tr_frag<E, R::RC>(sm.ringM, ks * KS, 16 * w, lane), dv);
         const int v = nb * 16 + frow(lane, 0);
@@ -644,7 +644,7 @@ __global__ __launch_bounds__(INTRA_THREADS) __attribute__((amdgpu_waves_per_eu(2
       f4 x = zero4();
 #pragma unroll
       for (int ks = 0; ks < NKC; ++ks)
-        if (ks * KS + KS > 16 * w)
+        if (keep_kblock<E>(ks * KS + KS > 16 * w))
           x = Mma<E>::mma(tile_tr_frag<E, RK>(ring + SM::OW, ks * KS, kb * 16, lb),
                           tile_tr_frag<E, RC>(sm.Mm, ks * KS, 16 * w, lb), x);
 #pragma unroll
@@ -681,7 +681,7 @@ __global__ __launch_bounds__(INTRA_THREADS) __attribute__((amdgpu_waves_per_eu(2
       f4 y = zero4();
 #pragma unroll
       for (int ks = 0; ks < NKC; ++ks)
-        if (ks * KS + KS > 16 * w)
+        if (keep_kblock<E>(ks * KS + KS > 16 * w))
           y = Mma<E>::mma(tile_frag<E, RC>(ring + SM::ODT, cb * 16, ks * KS, lb),
                           tile_tr_frag<E, RC>(sm.Mm, ks * KS, 16 * w, lb), y);
       *(QR*)(ring + SM::OY + tile_off<RC>(rr, (cb * 16 + frow(lb, 0)) * (int)ES)) = Quad<E>::pack(y);
@@ -692,7 +692,7 @@ __global__ __launch_bounds__(INTRA_THREADS) __attribute__((amdgpu_waves_per_eu(2
       adA[cb] = zero4();
 #pragma unroll
       for (int ks = 0; ks < NKC; ++ks)
-        if (ks * KS <= cb * 16 + 15)
+        if (keep_kblock<E>(ks * KS <= cb * 16 + 15))
           adA[cb] = Mma<E>::mma(tile_frag<E, RC>(ring + SM::OY, 16 * w, ks * KS, lb),
                                 tile_frag<E, RC>(sm.Mm, cb * 16, ks * KS, lb), adA[cb]);
     }

@@ -21,6 +21,14 @@ constexpr int NWAVES = NTHREADS / 64;
 
 typedef float f4 __attribute__((ext_vector_type(4)));
 
+// Lower-triangular chunk operands (T, M, P) are stored with exact zeros above
+// the 16 x 16 block diagonal, so products with them may skip those k blocks
+// or not: the fp32 forms (16 k steps per chunk) skip them; the bf16 forms
+// (two k steps) run every block, which keeps the waves' work equal and each
+// phase one basic block whose LDS reads can all be issued ahead of the MFMAs.
+template <typename E>
+__device__ constexpr bool keep_kblock(bool needed) { return sizeof(E) == 2 || needed; }
+
 // Wave index within the workgroup, in a scalar register: branches on it are
 // uniform, so they compile to scalar branches instead of exec-mask regions.
 __device__ inline int wave_id(int tid) { return __builtin_amdgcn_readfirstlane(tid >> 6); }
@@ -715,7 +723,7 @@ __device__ inline float sum16(float x) {
 template <int NT>
 __device__ inline void unit_lower_inverse(float* sA, int lda, float* sM, int ldm, int tid) {
   static_assert(NT == 512, "eight waves");
-  const int lane = tid & 63, w = wave_id(tid);
+  const int lane = tid & 63, w = tid >> 6;   // vector wave index (measured faster in the preparation kernel)
   auto blkA = [&](int i, int j) { return sA + (size_t)(16 * i) * lda + 16 * j; };
   auto blkM = [&](int i, int j) { return sM + (size_t)(16 * i) * ldm + 16 * j; };
   auto put = [&](float* dst, int ld, f4 v, float sc) {

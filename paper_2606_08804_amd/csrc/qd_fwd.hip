@@ -72,7 +72,7 @@ __global__ __launch_bounds__(PREP_THREADS) void k_prep(Params p) {
   constexpr int LK = DK + P, LC = C + P;
   typedef PrepPre<E, DK> Pre;
   __shared__ PrepSmem<E, DK> sm;
-  const int tid = threadIdx.x, lane = tid & 63, w = wave_id(tid);
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;   // vector wave index: measured faster here than the scalar one
   const int H = p.H;
   const int total = p.n_slots * H;
 
@@ -435,7 +435,7 @@ __global__ __launch_bounds__(NTHREADS + 256) void k_scan_fwd(Params p) {
         f4 d = zero4();
 #pragma unroll
         for (int ks = 0; ks < C / KS; ++ks)
-          if (ks * KS <= 16 * w + 15) {
+          if (keep_kblock<E>(ks * KS <= 16 * w + 15)) {
             const FR tB = tile_frag<E, R::RC>(sm.ringB + R::BT, 16 * w, ks * KS, lane);
             d = Mma<E>::mma(tile_tr_frag<E, R::RO>(sm.ringB + R::BV_, ks * KS, nb * 16, lane), tB, d);
             d = Mma<E>::mma(tr_frag<E>(&sm.Y[0][0], LV, ks * KS, nb * 16, lane), tB, d);
@@ -489,7 +489,7 @@ __global__ __launch_bounds__(NTHREADS + 256) void k_scan_fwd(Params p) {
           f4 o = sq[nb];
 #pragma unroll
           for (int ks = 0; ks < C / KS; ++ks)
-            if (ks * KS <= 16 * w + 15)
+            if (keep_kblock<E>(ks * KS <= 16 * w + 15))
               o = Mma<E>::mma(tr_frag<E>(&sm.D[0][0], LV, ks * KS, nb * 16, lane),
                               tile_frag<E, R::RC>(sm.Pt[c % R::NP], 16 * w, ks * KS, lane), o);
           *(QR*)&sm.O[rr][nb * 16 + frow(lane, 0)] = Quad<E>::pack(o);
