@@ -224,11 +224,16 @@ struct alignas(16) ScanFwdSmem {
   E O[C][BV + P];     // output tile staging
 };
 
-// One workgroup per (sequence, head, Dv tile of BV = 32 value rows): four
-// compute waves and four producer waves (one wave alone issues direct loads
-// at only about 12 bytes per clock).  The state tile S^T (Dk x BV) lives in
-// fp32 MFMA accumulators across the whole sequence; compute wave w owns its
-// key rows 16 KPW w.. and the chunk rows 16w.. of every C-row operand.
+// One workgroup per (sequence, head, Dv tile of BV value rows): NCW compute
+// waves and four producer waves (one wave alone issues direct loads at only
+// about 12 bytes per clock).  bf16 runs eight compute waves, two per SIMD:
+// a single wave reads LDS at only about 26 bytes per clock (16 with transpose
+// reads), so a chunk's fragment reads take half as long on each of twice as
+// many waves.  The state tile S^T (Dk x BV) lives in fp32 MFMA accumulators
+// across the whole sequence, split over the compute waves by key blocks (and
+// value blocks when there are more waves than key blocks); compute wave w
+// owns chunk rows 16 (w & 3).. of every C-row result and a range of its
+// value blocks.
 //
 // The chunk step never forms W = T diag(g) X nor U = T V:
 //   D = U - W S^T = T V + T Y,  Y = -diag(g) (K S^T + diag(lambda) Q S^T),
@@ -246,16 +251,24 @@ struct alignas(16) ScanFwdSmem {
 // set B of chunk c in phase 2, for P of chunk c in phase 3 and for set A of
 // chunk c+1 in phase 4.  They issue no other memory operations, so their outstanding-load
 // counts are exact.  When p.o is null only the states are produced.
-template <typename E, int DK, int DV, int BV>
-__global__ __launch_bounds__(NTHREADS + 256) void k_scan_fwd(Params p) {
+template <typename E, int DK, int DV, int BV, int NCW>
+__global__ __launch_bounds__(NCW * 64 + 256) void k_scan_fwd(Params p) {
   constexpr int P = Pad<E>::v;
   constexpr int LK = DK + P, LV = BV + P;
   constexpr int NVT = DV / BV;
   constexpr int NB = BV / 16;                 // 16-column blocks per tile
   constexpr int KS = Mma<E>::KS;
   constexpr int NKS = DK / KS;
-  static_assert(DK / 16 == 2 * NWAVES || DK / 16 == NWAVES, "key blocks per wave");
-  constexpr int KPW = DK / 16 / NWAVES;       // key row blocks of S^T per wave (1 or 2)
+  constexpr int NCT = NCW * 64;               // compute threads
+  // compute wave w: chunk rows 16 cb.. (cb = w & 3) of the C-row results,
+  // NBW value blocks from nb0 = (w >> 2) NBW; state tile S^T: KPW key
+  // blocks from kb0 and NBS value blocks from ns0
+  constexpr int NBW = NB / (NCW / 4);
+  constexpr int KB = DK / 16;
+  constexpr int KPW = KB >= NCW ? KB / NCW : 1;
+  constexpr int SG = KB >= NCW ? 1 : NCW / KB;   // waves that share a key block
+  constexpr int NBS = NB / SG;
+  static_assert(NCW % 4 == 0 && NBW >= 1 && NBS >= 1 && KPW * (NCW / SG) == KB, "wave mapping");
   constexpr size_t ES = sizeof(E);
   typedef typename Quad<E>::raw QR;
   typedef typename Mma<E>::frag FR;
@@ -263,8 +276,10 @@ __global__ __launch_bounds__(NTHREADS + 256) void k_scan_fwd(Params p) {
   constexpr int NA = R::NA;
   __shared__ ScanFwdSmem<E, DK, BV> sm;
   const int tid = threadIdx.x, lane = tid & 63, w = wave_id(tid);
-  const int prod = w - NWAVES;                // 0-3 for the producer waves, negative otherwise
+  const int prod = w - NCW;                   // 0-3 for the producer waves, negative otherwise
   const bool producer = prod >= 0;
+  const int cb = w & 3, nb0 = (w >> 2) * NBW;
+  const int kb0 = (w % (NCW / SG)) * KPW, ns0 = (w / (NCW / SG)) * NBS;
   int unit, vt;
   if (!xcd_unit_tile(blockIdx.x, p.N * p.H, NVT, unit, vt)) return;
   const int H = p.H, n = unit / H, h = unit % H, v0 = vt * BV;
@@ -322,32 +337,32 @@ __global__ __launch_bounds__(NTHREADS + 256) void k_scan_fwd(Params p) {
                                 prod, lane);
   };
 
-  // state: acc[i][nb] = S^T rows 16*(KPW*w+i).., columns 16*nb.. of this tile
-  f4 acc[KPW][NB];
+  // state: acc[i][j] = S^T rows 16 (kb0 + i).., columns 16 (ns0 + j).. of this tile
+  f4 acc[KPW][NBS];
 #pragma unroll
   for (int i = 0; i < KPW; ++i)
 #pragma unroll
-    for (int nb = 0; nb < NB; ++nb) {
-      const int kt = KPW * w + i;
-      acc[i][nb] = (p.S0 && !producer)
-                       ? *(const f4*)(p.S0 + ((size_t)unit * DV + v0 + nb * 16 + fcol(lane)) * DK + kt * 16 +
-                                      frow(lane, 0))
-                       : zero4();
+    for (int j = 0; j < NBS; ++j) {
+      const int kt = kb0 + i, nb = ns0 + j;
+      acc[i][j] = (p.S0 && !producer)
+                      ? *(const f4*)(p.S0 + ((size_t)unit * DV + v0 + nb * 16 + fcol(lane)) * DK + kt * 16 +
+                                     frow(lane, 0))
+                      : zero4();
     }
   // S (row v, column k) into LDS for the next chunk
   auto stage_S = [&]() {
 #pragma unroll
     for (int i = 0; i < KPW; ++i)
 #pragma unroll
-      for (int nb = 0; nb < NB; ++nb)
-        *(QR*)&sm.S[nb * 16 + fcol(lane)][(KPW * w + i) * 16 + frow(lane, 0)] = Quad<E>::pack(acc[i][nb]);
+      for (int j = 0; j < NBS; ++j)
+        *(QR*)&sm.S[(ns0 + j) * 16 + fcol(lane)][(kb0 + i) * 16 + frow(lane, 0)] = Quad<E>::pack(acc[i][j]);
   };
   // output rows of chunk c from the staging tile
   auto store_O = [&](int c) {
     constexpr int VEC = 16 / sizeof(E), PR = BV / VEC;
     const int t0 = s + c * C, len = min(C, e - t0);
     E* obase = (E*)p.o + ((size_t)t0 * H + h) * DV + v0;
-    for (int idx = tid; idx < C * PR; idx += NTHREADS) {
+    for (int idx = tid; idx < C * PR; idx += NCT) {
       const int r = idx / PR, cc = (idx % PR) * VEC;
       if (r < len) *(uint4*)(obase + (size_t)r * H * DV + cc) = *(const uint4*)&sm.O[r][cc];
     }
@@ -370,8 +385,8 @@ __global__ __launch_bounds__(NTHREADS + 256) void k_scan_fwd(Params p) {
     const size_t gi = (size_t)(base + c) * H + h;
     const char* ra = sm.ringA[c % NA];
     const float* gb = (const float*)(ra + R::AG);   // b, then beta, then lambda
-    const int rr = 16 * w + fcol(lane);             // chunk row of this lane's result columns
-    f4 sq[NB];                                      // (S Q^T) block (v-block nb, r-block w), scaled by g_r
+    const int rr = 16 * cb + fcol(lane);            // chunk row of this lane's result columns
+    f4 sq[NBW];                                     // (S Q^T) blocks (v-block nb0 + j, r-block cb), scaled by g_r
     block_sync_lds();                      // B_a: S staged; set A of chunk c visible
     // ---- phase 2
     if (!producer) {
@@ -379,38 +394,38 @@ __global__ __launch_bounds__(NTHREADS + 256) void k_scan_fwd(Params p) {
         // saved entry state S (row v, column k) of this tile, 16-byte stores
         constexpr int VEC = 16 / sizeof(E), PR = DK / VEC;
         E* dst = (E*)p.saved + gi * DV * DK + (size_t)v0 * DK;
-        for (int idx = tid; idx < BV * PR; idx += NTHREADS) {
+        for (int idx = tid; idx < BV * PR; idx += NCT) {
           const int r = idx / PR, cc = (idx % PR) * VEC;
           *(uint4*)(dst + (size_t)r * DK + cc) = *(const uint4*)&sm.S[r][cc];
         }
       }
       // (S K^T), (S Q^T): value rows, chunk columns 16w..; the S fragments
       // of one k step at a time are live
-      f4 sk[NB];
+      f4 sk[NBW];
 #pragma unroll
-      for (int nb = 0; nb < NB; ++nb) sk[nb] = sq[nb] = zero4();
+      for (int j = 0; j < NBW; ++j) sk[j] = sq[j] = zero4();
 #pragma unroll
       for (int ks = 0; ks < NKS; ++ks) {
-        const FR kB = tile_frag<E, R::RK>(ra + R::AK, 16 * w, ks * KS, lane);
-        const FR qB = tile_frag<E, R::RK>(ra + R::AQ, 16 * w, ks * KS, lane);
+        const FR kB = tile_frag<E, R::RK>(ra + R::AK, 16 * cb, ks * KS, lane);
+        const FR qB = tile_frag<E, R::RK>(ra + R::AQ, 16 * cb, ks * KS, lane);
 #pragma unroll
-        for (int nb = 0; nb < NB; ++nb) {
-          const FR sa = Frag<E>::load(kmaj(&sm.S[0][0], LK), nb * 16, ks * KS, lane);
-          sk[nb] = Mma<E>::mma(sa, kB, sk[nb]);
-          sq[nb] = Mma<E>::mma(sa, qB, sq[nb]);
+        for (int j = 0; j < NBW; ++j) {
+          const FR sa = Frag<E>::load(kmaj(&sm.S[0][0], LK), (nb0 + j) * 16, ks * KS, lane);
+          sk[j] = Mma<E>::mma(sa, kB, sk[j]);
+          sq[j] = Mma<E>::mma(sa, qB, sq[j]);
         }
       }
       const float gr = __expf(gb[rr]), ngr = -gr, lr = gb[2 * C + rr];
       // Y (row r, column v) = -g_r ((S K^T) + lambda_r (S Q^T))^T
 #pragma unroll
-      for (int nb = 0; nb < NB; ++nb) {
+      for (int jn = 0; jn < NBW; ++jn) {
         f4 y;
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
-          y[j] = ngr * (sk[nb][j] + lr * sq[nb][j]);
-          sq[nb][j] *= gr;
+          y[j] = ngr * (sk[jn][j] + lr * sq[jn][j]);
+          sq[jn][j] *= gr;
         }
-        *(QR*)&sm.Y[rr][nb * 16 + frow(lane, 0)] = Quad<E>::pack(y);
+        *(QR*)&sm.Y[rr][(nb0 + jn) * 16 + frow(lane, 0)] = Quad<E>::pack(y);
       }
     } else {
       // Q of chunk c+NA-1 (its ring slot was freed at B_a) and P of chunk
@@ -427,16 +442,17 @@ __global__ __launch_bounds__(NTHREADS + 256) void k_scan_fwd(Params p) {
     // ---- phase 3
     if (!producer) {
       if (with_o && c > 0) store_O(c - 1);
-      // D^T (value rows, chunk columns 16w..) = (V + Y)^T T^T as two products;
-      // T is lower triangular, so k blocks past this wave's rows are skipped
+      // D^T (value rows, chunk columns 16 cb..) = (V + Y)^T T^T as two
+      // products; T is lower triangular (k blocks past this wave's rows are zero)
       const float kbr = __expf(gb[C - 1] - gb[rr]);
 #pragma unroll
-      for (int nb = 0; nb < NB; ++nb) {
+      for (int jn = 0; jn < NBW; ++jn) {
+        const int nb = nb0 + jn;
         f4 d = zero4();
 #pragma unroll
         for (int ks = 0; ks < C / KS; ++ks)
-          if (keep_kblock<E>(ks * KS <= 16 * w + 15)) {
-            const FR tB = tile_frag<E, R::RC>(sm.ringB + R::BT, 16 * w, ks * KS, lane);
+          if (keep_kblock<E>(ks * KS <= 16 * cb + 15)) {
+            const FR tB = tile_frag<E, R::RC>(sm.ringB + R::BT, 16 * cb, ks * KS, lane);
             d = Mma<E>::mma(tile_tr_frag<E, R::RO>(sm.ringB + R::BV_, ks * KS, nb * 16, lane), tB, d);
             d = Mma<E>::mma(tr_frag<E>(&sm.Y[0][0], LV, ks * KS, nb * 16, lane), tB, d);
           }
@@ -476,22 +492,23 @@ __global__ __launch_bounds__(NTHREADS + 256) void k_scan_fwd(Params p) {
         // D rows of this tile into the saved context (rows past the chunk are zero)
         constexpr int VEC = 16 / sizeof(E), PR = BV / VEC;
         E* dbase = (E*)p.savedD + gi * C * DV + v0;
-        for (int idx = tid; idx < C * PR; idx += NTHREADS) {
+        for (int idx = tid; idx < C * PR; idx += NCT) {
           const int r = idx / PR, cc = (idx % PR) * VEC;
           *(uint4*)(dbase + (size_t)r * DV + cc) = *(const uint4*)&sm.D[r][cc];
         }
       }
       if (with_o) {
-        // O^T (value rows, chunk columns 16w..) = g_r (S Q^T) + D^T P^T; P is
-        // causal, so k blocks past this wave's rows are skipped
+        // O^T (value rows, chunk columns 16 cb..) = g_r (S Q^T) + D^T P^T; P
+        // is causal (k blocks past this wave's rows are zero)
 #pragma unroll
-        for (int nb = 0; nb < NB; ++nb) {
-          f4 o = sq[nb];
+        for (int jn = 0; jn < NBW; ++jn) {
+          const int nb = nb0 + jn;
+          f4 o = sq[jn];
 #pragma unroll
           for (int ks = 0; ks < C / KS; ++ks)
-            if (keep_kblock<E>(ks * KS <= 16 * w + 15))
+            if (keep_kblock<E>(ks * KS <= 16 * cb + 15))
               o = Mma<E>::mma(tr_frag<E>(&sm.D[0][0], LV, ks * KS, nb * 16, lane),
-                              tile_frag<E, R::RC>(sm.Pt[c % R::NP], 16 * w, ks * KS, lane), o);
+                              tile_frag<E, R::RC>(sm.Pt[c % R::NP], 16 * cb, ks * KS, lane), o);
           *(QR*)&sm.O[rr][nb * 16 + frow(lane, 0)] = Quad<E>::pack(o);
         }
       }
@@ -500,17 +517,17 @@ __global__ __launch_bounds__(NTHREADS + 256) void k_scan_fwd(Params p) {
 #pragma unroll
       for (int i = 0; i < KPW; ++i)
 #pragma unroll
-        for (int nb = 0; nb < NB; ++nb) acc[i][nb] = gC * acc[i][nb];
+        for (int j = 0; j < NBS; ++j) acc[i][j] = gC * acc[i][j];
 #pragma unroll
       for (int ks = 0; ks < C / KS; ++ks) {
         FR ka[KPW];
 #pragma unroll
-        for (int i = 0; i < KPW; ++i) ka[i] = tile_tr_frag<E, R::RK>(ra + R::AK, ks * KS, 16 * (KPW * w + i), lane);
+        for (int i = 0; i < KPW; ++i) ka[i] = tile_tr_frag<E, R::RK>(ra + R::AK, ks * KS, 16 * (kb0 + i), lane);
 #pragma unroll
-        for (int nb = 0; nb < NB; ++nb) {
-          const FR bf = tr_frag<E>(&sm.Dk[0][0], LV, ks * KS, nb * 16, lane);
+        for (int j = 0; j < NBS; ++j) {
+          const FR bf = tr_frag<E>(&sm.Dk[0][0], LV, ks * KS, (ns0 + j) * 16, lane);
 #pragma unroll
-          for (int i = 0; i < KPW; ++i) acc[i][nb] = Mma<E>::mma(ka[i], bf, acc[i][nb]);
+          for (int i = 0; i < KPW; ++i) acc[i][j] = Mma<E>::mma(ka[i], bf, acc[i][j]);
         }
       }
       stage_S();
@@ -541,10 +558,10 @@ __global__ __launch_bounds__(NTHREADS + 256) void k_scan_fwd(Params p) {
 #pragma unroll
       for (int i = 0; i < KPW; ++i)
 #pragma unroll
-        for (int nb = 0; nb < NB; ++nb) {
-          const int kt = KPW * w + i;
+        for (int j = 0; j < NBS; ++j) {
+          const int kt = kb0 + i, nb = ns0 + j;
           *(f4*)(p.Sfin + ((size_t)unit * DV + v0 + nb * 16 + fcol(lane)) * DK + kt * 16 + frow(lane, 0)) =
-              acc[i][nb];
+              acc[i][j];
         }
     }
   }
@@ -569,13 +586,16 @@ static hipError_t launch_fwd_t(const Params& p, int in_bwd, int with_scan, hipSt
     const int nb = ((units + 7) / 8) * 8 * (DV / bv);
     if (nb > 0) {
       prof_mark(ST_SCAN_FWD, 0, st);
+      // bf16: eight compute waves (two per SIMD, each with half of the LDS
+      // reads of a chunk); fp32: four
+      constexpr int NCW = sizeof(E) == 2 ? 8 : 4;
       if constexpr (scan_bv_max<E, DV>() == 64) {
         if (bv == 64)
-          hipLaunchKernelGGL((k_scan_fwd<E, DK, DV, 64>), dim3(nb), dim3(NTHREADS + 256), 0, st, p);
+          hipLaunchKernelGGL((k_scan_fwd<E, DK, DV, 64, NCW>), dim3(nb), dim3(NCW * 64 + 256), 0, st, p);
         else
-          hipLaunchKernelGGL((k_scan_fwd<E, DK, DV, 32>), dim3(nb), dim3(NTHREADS + 256), 0, st, p);
+          hipLaunchKernelGGL((k_scan_fwd<E, DK, DV, 32, NCW>), dim3(nb), dim3(NCW * 64 + 256), 0, st, p);
       } else {
-        hipLaunchKernelGGL((k_scan_fwd<E, DK, DV, 32>), dim3(nb), dim3(NTHREADS + 256), 0, st, p);
+        hipLaunchKernelGGL((k_scan_fwd<E, DK, DV, 32, NCW>), dim3(nb), dim3(NCW * 64 + 256), 0, st, p);
       }
       prof_mark(ST_SCAN_FWD, 1, st);
     }
