@@ -75,11 +75,13 @@ struct alignas(16) ScanBwdSmem {
   E z2[C][BV + P];    // -diag(g) dV
 };
 
-// One workgroup per (sequence, head, Dv tile of BV = 32): four compute waves
-// and four producer waves; reverse pass over the chunks.  The exit-state
-// gradient tile dS'^T (Dk x BV) lives in fp32 MFMA accumulators; compute wave
-// w owns its key rows 16 KPW w.. and the chunk rows 16w.. of every C-row
-// operand.
+// One workgroup per (sequence, head, Dv tile of BV value rows): NCW compute
+// waves (eight for bf16, two per SIMD, as in the forward scan) and four
+// producer waves; reverse pass over the chunks.  The exit-state gradient tile
+// dS'^T (Dk x BV) lives in fp32 MFMA accumulators, split over the compute
+// waves by key blocks (and value blocks when there are more waves than key
+// blocks); compute wave w owns chunk rows 16 (w & 3).. of every C-row result
+// and a range of its value blocks.
 //
 // W is not read: with W^T = X^T diag(g) diag(beta) M^T the entry-state
 // gradient is
@@ -98,16 +100,21 @@ struct alignas(16) ScanBwdSmem {
 // that chunk in phase 3, P of the next chunk in phase 2 (two buffers) or 3
 // (one), M of the next chunk in phase 4; they wait for M in phase 2 and for
 // set X and P of the next chunk in phase 4.
-template <typename E, int DK, int DV, int BV>
-__global__ __launch_bounds__(NTHREADS + 256) void k_scan_bwd(Params p) {
+template <typename E, int DK, int DV, int BV, int NCW>
+__global__ __launch_bounds__(NCW * 64 + 256) void k_scan_bwd(Params p) {
   constexpr int P = Pad<E>::v;
   constexpr int LK = DK + P, LV = BV + P;
   constexpr int NVT = DV / BV;
   constexpr int NB = BV / 16;
   constexpr int KS = Mma<E>::KS, KPL = Mma<E>::KPL;
   constexpr int NKS = DK / KS;
-  constexpr int KPW = DK / 16 / NWAVES;
-  static_assert(KPW >= 1 && KPW * 16 * NWAVES == DK, "key blocks per wave");
+  constexpr int NCT = NCW * 64;               // compute threads
+  constexpr int NBW = NB / (NCW / 4);         // value blocks per wave in phases 2-3
+  constexpr int KB = DK / 16;
+  constexpr int KPW = KB >= NCW ? KB / NCW : 1;   // key blocks of dS'^T per wave
+  constexpr int SG = KB >= NCW ? 1 : NCW / KB;    // waves that share a key block
+  constexpr int NBS = NB / SG;                    // value blocks of dS'^T per wave
+  static_assert(NCW % 4 == 0 && NBW >= 1 && NBS >= 1 && KPW * (NCW / SG) == KB, "wave mapping");
   typedef typename Quad<E>::raw QR;
   typedef typename Mma<E>::frag FR;
   typedef ScanBwdRing<E, DK, BV> R;
@@ -116,8 +123,10 @@ __global__ __launch_bounds__(NTHREADS + 256) void k_scan_bwd(Params p) {
   constexpr int UKD = NKS > 4 ? 4 : NKS;
   __shared__ ScanBwdSmem<E, DK, BV> sm;
   const int tid = threadIdx.x, lane = tid & 63, w = wave_id(tid);
-  const int prod = w - NWAVES;               // 0-3 for the producer waves, negative otherwise
+  const int prod = w - NCW;                  // 0-3 for the producer waves, negative otherwise
   const bool producer = prod >= 0;
+  const int cb = w & 3, nb0 = (w >> 2) * NBW;
+  const int kb0 = (w % (NCW / SG)) * KPW, ns0 = (w / (NCW / SG)) * NBS;
   int unit, vt;
   if (!xcd_unit_tile(blockIdx.x, p.N * p.H, NVT, unit, vt)) return;
   const int H = p.H, n = unit / H, h = unit % H, v0 = vt * BV;
@@ -171,23 +180,23 @@ __global__ __launch_bounds__(NTHREADS + 256) void k_scan_bwd(Params p) {
     dma_rows<R::RC, C, 4, true>(sm.ringM, Mg, R::RC, C, Mg, 0, prod, lane);
   };
 
-  f4 acc[KPW][NB];
+  f4 acc[KPW][NBS];
 #pragma unroll
   for (int i = 0; i < KPW; ++i)
 #pragma unroll
-    for (int nb = 0; nb < NB; ++nb) {
-      const int kt = KPW * w + i;
-      acc[i][nb] = (p.dSfin && !producer)
-                       ? *(const f4*)(p.dSfin + ((size_t)unit * DV + v0 + nb * 16 + fcol(lane)) * DK + kt * 16 +
-                                      frow(lane, 0))
-                       : zero4();
+    for (int j = 0; j < NBS; ++j) {
+      const int kt = kb0 + i, nb = ns0 + j;
+      acc[i][j] = (p.dSfin && !producer)
+                      ? *(const f4*)(p.dSfin + ((size_t)unit * DV + v0 + nb * 16 + fcol(lane)) * DK + kt * 16 +
+                                     frow(lane, 0))
+                      : zero4();
     }
   auto stage_dS = [&]() {
 #pragma unroll
     for (int i = 0; i < KPW; ++i)
 #pragma unroll
-      for (int nb = 0; nb < NB; ++nb)
-        *(QR*)&sm.dS[nb * 16 + fcol(lane)][(KPW * w + i) * 16 + frow(lane, 0)] = Quad<E>::pack(acc[i][nb]);
+      for (int j = 0; j < NBS; ++j)
+        *(QR*)&sm.dS[(ns0 + j) * 16 + fcol(lane)][(kb0 + i) * 16 + frow(lane, 0)] = Quad<E>::pack(acc[i][j]);
   };
 
   if (nch > 0) {
@@ -209,7 +218,7 @@ __global__ __launch_bounds__(NTHREADS + 256) void k_scan_bwd(Params p) {
     const int t0 = s + c * C, len = min(C, e - t0);
     const char* rx = sm.ringX[it % NA];
     const float* gb = (const float*)(rx + R::XG);   // b, then beta, then lambda
-    const int rr = 16 * w + fcol(lane);             // chunk row of this lane's result columns
+    const int rr = 16 * cb + fcol(lane);            // chunk row of this lane's result columns
     block_sync_lds();                      // B_a: dS' staged; set X of this chunk visible
     // ---- phase 2
     if (!producer) {
@@ -217,40 +226,41 @@ __global__ __launch_bounds__(NTHREADS + 256) void k_scan_bwd(Params p) {
         // dS' of this chunk for the intra-chunk kernel (row v, column k), 16-byte stores
         constexpr int VEC = 16 / sizeof(E), PR = DK / VEC;
         E* dst = (E*)p.w_dSo + gi * DV * DK + (size_t)v0 * DK;
-        for (int idx = tid; idx < BV * PR; idx += NTHREADS) {
+        for (int idx = tid; idx < BV * PR; idx += NCT) {
           const int r = idx / PR, cc = (idx % PR) * VEC;
           *(uint4*)(dst + (size_t)r * DK + cc) = *(const uint4*)&sm.dS[r][cc];
         }
       }
-      // dD^T (value rows, key columns 16w..) = dS' Kbar^T + dO^T P
+      // dD^T (value rows, chunk columns 16 cb..) = dS' Kbar^T + dO^T P
       const float bi = gb[rr], kbi = __expf(gb[C - 1] - bi);
-      f4 dt[NB];
+      f4 dt[NBW];
 #pragma unroll
-      for (int nb = 0; nb < NB; ++nb) dt[nb] = zero4();
+      for (int j = 0; j < NBW; ++j) dt[j] = zero4();
 #pragma unroll UKD
       for (int ks = 0; ks < NKS; ++ks) {
-        const FR kB = tile_frag<E, R::RK>(rx + R::XK, 16 * w, ks * KS, lane);
+        const FR kB = tile_frag<E, R::RK>(rx + R::XK, 16 * cb, ks * KS, lane);
 #pragma unroll
-        for (int nb = 0; nb < NB; ++nb)
-          dt[nb] = Mma<E>::mma(Frag<E>::load(kmaj(&sm.dS[0][0], LK), nb * 16, ks * KS, lane), kB, dt[nb]);
+        for (int j = 0; j < NBW; ++j)
+          dt[j] = Mma<E>::mma(Frag<E>::load(kmaj(&sm.dS[0][0], LK), (nb0 + j) * 16, ks * KS, lane), kB, dt[j]);
       }
 #pragma unroll
-      for (int nb = 0; nb < NB; ++nb)
+      for (int j = 0; j < NBW; ++j)
 #pragma unroll
-        for (int j = 0; j < 4; ++j) dt[nb][j] *= kbi;
-      // + dO^T P (P causal: k blocks before this wave's key rows are skipped)
+        for (int jj = 0; jj < 4; ++jj) dt[j][jj] *= kbi;
+      // + dO^T P (P causal: k blocks before this wave's chunk rows are zero)
 #pragma unroll
       for (int ks = 0; ks < C / KS; ++ks)
-        if (keep_kblock<E>(ks * KS + KS > 16 * w)) {
-          const FR pB = tile_tr_frag<E, R::RC>(sm.ringP[it % R::NP], ks * KS, 16 * w, lane);
+        if (keep_kblock<E>(ks * KS + KS > 16 * cb)) {
+          const FR pB = tile_tr_frag<E, R::RC>(sm.ringP[it % R::NP], ks * KS, 16 * cb, lane);
 #pragma unroll
-          for (int nb = 0; nb < NB; ++nb)
-            dt[nb] = Mma<E>::mma(tile_tr_frag<E, R::RO>(rx + R::XO, ks * KS, nb * 16, lane), pB, dt[nb]);
+          for (int j = 0; j < NBW; ++j)
+            dt[j] = Mma<E>::mma(tile_tr_frag<E, R::RO>(rx + R::XO, ks * KS, (nb0 + j) * 16, lane), pB, dt[j]);
         }
       // key rows past the chunk carry no gradient
       const float keep = rr < len ? 1.f : 0.f;
 #pragma unroll
-      for (int nb = 0; nb < NB; ++nb) *(QR*)&sm.dD[rr][nb * 16 + frow(lane, 0)] = Quad<E>::pack(keep * dt[nb]);
+      for (int j = 0; j < NBW; ++j)
+        *(QR*)&sm.dD[rr][(nb0 + j) * 16 + frow(lane, 0)] = Quad<E>::pack(keep * dt[j]);
     } else {
       // Q of the chunk NA-1 steps ahead (its ring slot was freed at B_a) and,
       // with two P buffers, P of the next chunk (its buffer was last read in
@@ -270,26 +280,27 @@ __global__ __launch_bounds__(NTHREADS + 256) void k_scan_bwd(Params p) {
         // dD rows for the intra-chunk kernel
         constexpr int VEC = 16 / sizeof(E), PR = BV / VEC;
         E* ddst = (E*)p.w_dDb + gi * C * DV + v0;
-        for (int idx = tid; idx < C * PR; idx += NTHREADS) {
+        for (int idx = tid; idx < C * PR; idx += NCT) {
           const int r = idx / PR, cc = (idx % PR) * VEC;
           *(uint4*)(ddst + (size_t)r * DV + cc) = *(const uint4*)&sm.dD[r][cc];
         }
       }
-      // dV^T (value rows, chunk columns 16w..) = beta_r (dD^T M); M is lower
-      // triangular, so k blocks before this wave's rows are skipped.  Each
+      // dV^T (value rows, chunk columns 16 cb..) = beta_r (dD^T M); M is lower
+      // triangular (k blocks before this wave's rows are zero).  Each
       // lane holds four consecutive values of row rr: dV goes out directly,
       // and z1 = g_r (dO - lambda_r dV), z2 = -g_r dV are formed here, where
       // the wave's own rows cover the tile once.
       const float betar = gb[C + rr], gr = __expf(gb[rr]), lr = gb[2 * C + rr];
       E* vrow = (E*)p.dv + ((size_t)(t0 + rr) * H + h) * DV + v0;
 #pragma unroll
-      for (int nb = 0; nb < NB; ++nb) {
+      for (int jn = 0; jn < NBW; ++jn) {
+        const int nb = nb0 + jn;
         f4 dv = zero4();
 #pragma unroll
         for (int ks = 0; ks < C / KS; ++ks)
-          if (keep_kblock<E>(ks * KS + KS > 16 * w))
+          if (keep_kblock<E>(ks * KS + KS > 16 * cb))
             dv = Mma<E>::mma(tr_frag<E>(&sm.dD[0][0], LV, ks * KS, nb * 16, lane),
-                             tile_tr_frag<E, R::RC>(sm.ringM, ks * KS, 16 * w, lane), dv);
+                             tile_tr_frag<E, R::RC>(sm.ringM, ks * KS, 16 * cb, lane), dv);
         const int v = nb * 16 + frow(lane, 0);
         const QR doq = *(const QR*)(rx + R::XO + tile_off<R::RO>(rr, v * (int)sizeof(E)));
         f4 a, b;
@@ -315,23 +326,23 @@ __global__ __launch_bounds__(NTHREADS + 256) void k_scan_bwd(Params p) {
 #pragma unroll
       for (int i = 0; i < KPW; ++i)
 #pragma unroll
-        for (int nb = 0; nb < NB; ++nb) acc[i][nb] = gC * acc[i][nb];
+        for (int j = 0; j < NBS; ++j) acc[i][j] = gC * acc[i][j];
 #pragma unroll
       for (int ks = 0; ks < C / KS; ++ks) {
         FR qa[KPW], ka[KPW];
 #pragma unroll
         for (int i = 0; i < KPW; ++i) {
-          qa[i] = tile_tr_frag<E, R::RK>(rx + R::XQ, ks * KS, 16 * (KPW * w + i), lane);
-          ka[i] = tile_tr_frag<E, R::RK>(rx + R::XK, ks * KS, 16 * (KPW * w + i), lane);
+          qa[i] = tile_tr_frag<E, R::RK>(rx + R::XQ, ks * KS, 16 * (kb0 + i), lane);
+          ka[i] = tile_tr_frag<E, R::RK>(rx + R::XK, ks * KS, 16 * (kb0 + i), lane);
         }
 #pragma unroll
-        for (int nb = 0; nb < NB; ++nb) {
-          const FR z1 = tr_frag<E>(&sm.z1[0][0], LV, ks * KS, nb * 16, lane);
-          const FR z2 = tr_frag<E>(&sm.z2[0][0], LV, ks * KS, nb * 16, lane);
+        for (int j = 0; j < NBS; ++j) {
+          const FR z1 = tr_frag<E>(&sm.z1[0][0], LV, ks * KS, (ns0 + j) * 16, lane);
+          const FR z2 = tr_frag<E>(&sm.z2[0][0], LV, ks * KS, (ns0 + j) * 16, lane);
 #pragma unroll
           for (int i = 0; i < KPW; ++i) {
-            acc[i][nb] = Mma<E>::mma(qa[i], z1, acc[i][nb]);
-            acc[i][nb] = Mma<E>::mma(ka[i], z2, acc[i][nb]);
+            acc[i][j] = Mma<E>::mma(qa[i], z1, acc[i][j]);
+            acc[i][j] = Mma<E>::mma(ka[i], z2, acc[i][j]);
           }
         }
       }
@@ -358,10 +369,10 @@ __global__ __launch_bounds__(NTHREADS + 256) void k_scan_bwd(Params p) {
 #pragma unroll
     for (int i = 0; i < KPW; ++i)
 #pragma unroll
-      for (int nb = 0; nb < NB; ++nb) {
-        const int kt = KPW * w + i;
+      for (int j = 0; j < NBS; ++j) {
+        const int kt = kb0 + i, nb = ns0 + j;
         *(f4*)(p.dS0 + ((size_t)unit * DV + v0 + nb * 16 + fcol(lane)) * DK + kt * 16 + frow(lane, 0)) =
-            acc[i][nb];
+            acc[i][j];
       }
   }
 }
@@ -848,13 +859,14 @@ static hipError_t launch_bwd_t(const Params& p, hipStream_t st) {
   const int nb = ((units + 7) / 8) * 8 * (DV / bv);
   if (nb > 0) {
     prof_mark(ST_SCAN_BWD, 0, st);
+    constexpr int NCW = sizeof(E) == 2 ? 8 : 4;   // compute waves: two per SIMD for bf16
     if constexpr (scan_bv_max<E, DV>() == 64) {
       if (bv == 64)
-        hipLaunchKernelGGL((k_scan_bwd<E, DK, DV, 64>), dim3(nb), dim3(NTHREADS + 256), 0, st, p);
+        hipLaunchKernelGGL((k_scan_bwd<E, DK, DV, 64, NCW>), dim3(nb), dim3(NCW * 64 + 256), 0, st, p);
       else
-        hipLaunchKernelGGL((k_scan_bwd<E, DK, DV, 32>), dim3(nb), dim3(NTHREADS + 256), 0, st, p);
+        hipLaunchKernelGGL((k_scan_bwd<E, DK, DV, 32, NCW>), dim3(nb), dim3(NCW * 64 + 256), 0, st, p);
     } else {
-      hipLaunchKernelGGL((k_scan_bwd<E, DK, DV, 32>), dim3(nb), dim3(NTHREADS + 256), 0, st, p);
+      hipLaunchKernelGGL((k_scan_bwd<E, DK, DV, 32, NCW>), dim3(nb), dim3(NCW * 64 + 256), 0, st, p);
     }
     prof_mark(ST_SCAN_BWD, 1, st);
   }

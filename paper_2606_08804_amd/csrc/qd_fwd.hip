@@ -390,15 +390,6 @@ __global__ __launch_bounds__(NCW * 64 + 256) void k_scan_fwd(Params p) {
     block_sync_lds();                      // B_a: S staged; set A of chunk c visible
     // ---- phase 2
     if (!producer) {
-      if (p.saved) {
-        // saved entry state S (row v, column k) of this tile, 16-byte stores
-        constexpr int VEC = 16 / sizeof(E), PR = DK / VEC;
-        E* dst = (E*)p.saved + gi * DV * DK + (size_t)v0 * DK;
-        for (int idx = tid; idx < BV * PR; idx += NCT) {
-          const int r = idx / PR, cc = (idx % PR) * VEC;
-          *(uint4*)(dst + (size_t)r * DK + cc) = *(const uint4*)&sm.S[r][cc];
-        }
-      }
       // (S K^T), (S Q^T): value rows, chunk columns 16w..; the S fragments
       // of one k step at a time are live
       f4 sk[NBW];
@@ -427,6 +418,18 @@ __global__ __launch_bounds__(NCW * 64 + 256) void k_scan_fwd(Params p) {
         }
         *(QR*)&sm.Y[rr][(nb0 + jn) * 16 + frow(lane, 0)] = Quad<E>::pack(y);
       }
+      // Global stores go out at the end of a phase: at its start they would
+      // queue behind the producers' direct loads for that phase and stall
+      // the compute wave.
+      if (p.saved) {
+        // saved entry state S (row v, column k) of this tile, 16-byte stores
+        constexpr int VEC = 16 / sizeof(E), PR = DK / VEC;
+        E* dst = (E*)p.saved + gi * DV * DK + (size_t)v0 * DK;
+        for (int idx = tid; idx < BV * PR; idx += NCT) {
+          const int r = idx / PR, cc = (idx % PR) * VEC;
+          *(uint4*)(dst + (size_t)r * DK + cc) = *(const uint4*)&sm.S[r][cc];
+        }
+      }
     } else {
       // Q of chunk c+NA-1 (its ring slot was freed at B_a) and P of chunk
       // c+NP-1 (its buffer was last read in the previous phase 4); then set B
@@ -441,7 +444,6 @@ __global__ __launch_bounds__(NCW * 64 + 256) void k_scan_fwd(Params p) {
     block_sync_lds();                      // B_b: Y staged; set B of chunk c visible
     // ---- phase 3
     if (!producer) {
-      if (with_o && c > 0) store_O(c - 1);
       // D^T (value rows, chunk columns 16 cb..) = (V + Y)^T T^T as two
       // products; T is lower triangular (k blocks past this wave's rows are zero)
       const float kbr = __expf(gb[C - 1] - gb[rr]);
@@ -462,6 +464,7 @@ __global__ __launch_bounds__(NCW * 64 + 256) void k_scan_fwd(Params p) {
         *(QR*)&sm.D[rr][nb * 16 + frow(lane, 0)] = Quad<E>::pack(d);
         *(QR*)&sm.Dk[rr][nb * 16 + frow(lane, 0)] = Quad<E>::pack(dk);
       }
+      if (with_o && c > 0) store_O(c - 1);
     } else {
       // K and gates of chunk c+NA-1; then P of chunk c must have landed
       const bool k_next = c + NA - 1 < nch;
@@ -488,15 +491,6 @@ __global__ __launch_bounds__(NCW * 64 + 256) void k_scan_fwd(Params p) {
     block_sync_lds();                      // B_c: D staged; P visible; set B of chunk c free
     // ---- phase 4
     if (!producer) {
-      if (p.saved) {
-        // D rows of this tile into the saved context (rows past the chunk are zero)
-        constexpr int VEC = 16 / sizeof(E), PR = BV / VEC;
-        E* dbase = (E*)p.savedD + gi * C * DV + v0;
-        for (int idx = tid; idx < C * PR; idx += NCT) {
-          const int r = idx / PR, cc = (idx % PR) * VEC;
-          *(uint4*)(dbase + (size_t)r * DV + cc) = *(const uint4*)&sm.D[r][cc];
-        }
-      }
       if (with_o) {
         // O^T (value rows, chunk columns 16 cb..) = g_r (S Q^T) + D^T P^T; P
         // is causal (k blocks past this wave's rows are zero)
@@ -531,6 +525,15 @@ __global__ __launch_bounds__(NCW * 64 + 256) void k_scan_fwd(Params p) {
         }
       }
       stage_S();
+      if (p.saved) {
+        // D rows of this tile into the saved context (rows past the chunk are zero)
+        constexpr int VEC = 16 / sizeof(E), PR = BV / VEC;
+        E* dbase = (E*)p.savedD + gi * C * DV + v0;
+        for (int idx = tid; idx < C * PR; idx += NCT) {
+          const int r = idx / PR, cc = (idx % PR) * VEC;
+          *(uint4*)(dbase + (size_t)r * DV + cc) = *(const uint4*)&sm.D[r][cc];
+        }
+      }
     } else if (c + 1 < nch) {
       issueB(c + 1);
       // set A of chunk c+1 complete: what was issued after its last part may
