@@ -253,7 +253,10 @@ void qd::prof_mark(int stage, int after, hipStream_t st) {
   if (!after) {
     if (i == (int)P.start[stage].size()) {
       hipEvent_t a = nullptr, b = nullptr;
-      if (hipEventCreate(&a) != hipSuccess || hipEventCreate(&b) != hipSuccess) {
+      // no system-scope fence: the events only time kernels on this device,
+      // and the fence made each record cost microseconds between launches
+      if (hipEventCreateWithFlags(&a, hipEventDisableSystemFence) != hipSuccess ||
+          hipEventCreateWithFlags(&b, hipEventDisableSystemFence) != hipSuccess) {
         P.failed = true;
         return;
       }
