@@ -90,6 +90,39 @@ def test_bwd_bf16(gate, Dk, Dv):
     _check(bwd_errors(d, g), TOL["bf16"], f"bwd bf16 {gate} Dk={Dk} Dv={Dv}")
 
 
+@pytest.mark.parametrize("gate", ["G1", "G3"])
+def test_bwd_matches_finite_differences_of_gpu_forward(gate):
+    """End-to-end gradient check that does not go through the oracle: the
+    directional derivative of L = <dO, o> + <dS_T, S_T>, computed by central
+    differences of the GPU forward (fp32), equals <grad, u> from the GPU
+    backward for a random direction u in each input."""
+    d = synth.make(1, 70, 1, 64, 64, "f32", gate, seed=121, s0=True, with_do=True)
+    dSf = torch.from_numpy(np.random.default_rng(11).standard_normal((1, 1, 64, 64)).astype(np.float32))
+    _, _, saved = gpu_fwd(d, save_states=True)
+    g = gpu_bwd(d, saved, d_final_state=dSf)
+    dO64, dSf64 = f64(d["d_o"]), f64(dSf)
+
+    def loss(dd):
+        o, Sf, _ = gpu_fwd(dd)
+        return float((f64(o.cpu()) * dO64).sum() + (f64(Sf.cpu()) * dSf64).sum())
+
+    rng = np.random.default_rng(12)
+    names = {"q": "dq", "k": "dk", "v": "dv", "beta": "dbeta", "lam": "dlam", "initial_state": "d_initial_state"}
+    if d["log_alpha"] is not None:
+        names["log_alpha"] = "dlog_alpha"
+    h = 1e-2
+    for key, gkey in names.items():
+        # a perturbation of about 1% of the input's own scale
+        scale = float(d[key].pow(2).mean().sqrt()) + 1e-3
+        u = torch.from_numpy((scale * rng.standard_normal(tuple(d[key].shape))).astype(np.float32))
+        plus, minus = dict(d), dict(d)
+        plus[key] = d[key] + h * u
+        minus[key] = d[key] - h * u
+        fd = (loss(plus) - loss(minus)) / (2 * h)
+        an = float((f64(g[gkey].cpu()) * f64(u)).sum())
+        assert abs(fd - an) <= 1e-2 * max(abs(an), 1e-3), (key, fd, an)
+
+
 def test_bwd_without_saved_states_matches_with():
     d = synth.make(1, 190, 2, 128, 128, "bf16", "G2", seed=107, s0=True, with_do=True)
     _, _, saved = gpu_fwd(d, save_states=True)
