@@ -12,12 +12,10 @@
 
 namespace qd {
 
-template <int LPR>
-__device__ inline float group_sum(float x) {
-#pragma unroll
-  for (int off = LPR / 2; off >= 1; off >>= 1) x += __shfl_xor(x, off, 64);
-  return x;
-}
+// Each lane group owns RPT state rows RPB apart (RPB = rows per workgroup
+// pass), so a wave has RPT independent 16-byte loads in flight instead of
+// one; the per-row dot products are reduced side by side.
+constexpr int STEP_RPT = 4;
 
 template <typename E, int DK>
 __global__ __launch_bounds__(NTHREADS) void k_step(int DV, int nrb, const E* __restrict__ q,
@@ -27,13 +25,13 @@ __global__ __launch_bounds__(NTHREADS) void k_step(int DV, int nrb, const E* __r
                                                   const float* __restrict__ la, float* __restrict__ S,
                                                   E* __restrict__ o) {
   constexpr int LPR = DK / 4;            // lanes per state row
-  constexpr int RPB = NTHREADS / LPR;    // rows per workgroup
+  constexpr int RPB = NTHREADS / LPR;    // rows per workgroup pass
+  constexpr int RPT = STEP_RPT;          // passes (rows per lane group)
   const size_t u = blockIdx.x / nrb;     // (sequence, head) unit
-  const int rb = blockIdx.x % nrb;       // block of RPB state rows
+  const int rb = blockIdx.x % nrb;       // block of RPB * RPT state rows
   const int tid = threadIdx.x;
-  const int row = rb * RPB + tid / LPR;
+  const int row0 = rb * RPB * RPT + tid / LPR;
   const int c0 = (tid % LPR) * 4;
-  if (row >= DV) return;                 // whole lane group leaves together
   float qv[4], kv[4];
 #pragma unroll
   for (int j = 0; j < 4; ++j) {
@@ -42,29 +40,59 @@ __global__ __launch_bounds__(NTHREADS) void k_step(int DV, int nrb, const E* __r
   }
   const float lm = lam[u], bt = beta[u];
   const float al = la ? __expf(la[u]) : 1.f;
-  float* Sr = S + (u * DV + row) * DK + c0;
-  f4 s = *(const f4*)Sr;
-  float px = 0.f;
+  float xv[4];
 #pragma unroll
-  for (int j = 0; j < 4; ++j) px += s[j] * (kv[j] + lm * qv[j]);
-  px = group_sum<LPR>(px);
-  const float e = bt * (tof(v[u * DV + row]) - al * px);
-  float oq = 0.f;
+  for (int j = 0; j < 4; ++j) xv[j] = kv[j] + lm * qv[j];
+  f4 s[RPT];
+  float vr[RPT];
 #pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    s[j] = al * s[j] + e * kv[j];
-    oq += s[j] * qv[j];
+  for (int i = 0; i < RPT; ++i) {        // rows past DV: the whole lane group skips them
+    const int row = row0 + i * RPB;
+    s[i] = row < DV ? *(const f4*)(S + (u * DV + row) * DK + c0) : zero4();
+    vr[i] = row < DV ? tof(v[u * DV + row]) : 0.f;
   }
-  *(f4*)Sr = s;
-  oq = group_sum<LPR>(oq);
-  if ((tid % LPR) == 0) o[u * DV + row] = fromf<E>(oq);
+  float px[RPT];
+#pragma unroll
+  for (int i = 0; i < RPT; ++i) {
+    px[i] = 0.f;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) px[i] += s[i][j] * xv[j];
+  }
+#pragma unroll
+  for (int off = LPR / 2; off >= 1; off >>= 1)
+#pragma unroll
+    for (int i = 0; i < RPT; ++i) px[i] += __shfl_xor(px[i], off, 64);
+  float oq[RPT];
+#pragma unroll
+  for (int i = 0; i < RPT; ++i) {
+    const float e = bt * (vr[i] - al * px[i]);
+    oq[i] = 0.f;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      s[i][j] = al * s[i][j] + e * kv[j];
+      oq[i] += s[i][j] * qv[j];
+    }
+    const int row = row0 + i * RPB;
+    if (row < DV) *(f4*)(S + (u * DV + row) * DK + c0) = s[i];
+  }
+#pragma unroll
+  for (int off = LPR / 2; off >= 1; off >>= 1)
+#pragma unroll
+    for (int i = 0; i < RPT; ++i) oq[i] += __shfl_xor(oq[i], off, 64);
+  if ((tid % LPR) == 0) {
+#pragma unroll
+    for (int i = 0; i < RPT; ++i) {
+      const int row = row0 + i * RPB;
+      if (row < DV) o[u * DV + row] = fromf<E>(oq[i]);
+    }
+  }
 }
 
 hipError_t launch_step(int N, int H, int Dk, int Dv, int dtype, const void* q, const void* k,
                        const void* v, const float* beta, const float* lam, const float* la,
                        float* state, void* o, hipStream_t st) {
   if (N == 0) return hipSuccess;
-  const int RPB = NTHREADS / (Dk / 4);
+  const int RPB = NTHREADS / (Dk / 4) * STEP_RPT;   // state rows per workgroup
   const int nrb = (Dv + RPB - 1) / RPB;
   dim3 grid((unsigned)((size_t)N * H * nrb));
 #define QD_STEP(ET, DKV)                                                                        \
