@@ -38,6 +38,7 @@ sys.path.insert(0, ROOT)
 from paper_2606_08804_amd import qdelta, synth  # noqa: E402
 
 HBM_PEAK = 8.0e12          # B/s, MI355X HBM3E
+VALU_F32_PEAK = 157.3e12   # flop/s, MI355X fp32 vector (256 CUs x 2.4 GHz)
 MFMA_BF16_PEAK = 2.5e15    # flop/s, dense bf16 MFMA
 MFMA_F32_PEAK = 157.3e12   # flop/s, dense fp32 MFMA
 C = 64
@@ -94,11 +95,16 @@ def stage_bytes_per_seq(stage, Dk, Dv, has_s0):
     return 0
 
 
+# Sources that build the chunk kernels the stored counters were taken on (the
+# decode kernel's own file is left out: it does not run in the training step).
+CHUNK_SOURCES = ("qd_api.hip", "qd_bwd.hip", "qd_common.h", "qd_fwd.hip", "qd_launch.h")
+
+
 def source_digest():
-    """Digest of the kernel sources, to tell whether stored counters still apply."""
+    """Digest of the chunk-kernel sources, to tell whether stored counters still apply."""
     h = hashlib.sha256()
     csrc = os.path.join(ROOT, "paper_2606_08804_amd", "csrc")
-    for f in sorted(os.listdir(csrc)):
+    for f in CHUNK_SOURCES:
         with open(os.path.join(csrc, f), "rb") as fh:
             h.update(f.encode())
             h.update(fh.read())
@@ -262,6 +268,92 @@ def run_chunk(args, wid, with_bwd):
     return out
 
 
+def run_layer(args):
+    """The autograd layer (gate and q/k/v/output projections + the chunk
+    kernels) forward and backward at the training shape: B=4, T=4096,
+    d_model = H*d = 2048, H=16, d=128, bf16 parameters and activations."""
+    from paper_2606_08804_amd import layer
+    B, T, H, d = 4, 4096, 16, 128
+    torch.manual_seed(0)
+    m = layer.QDeltaLayer(d_model=H * d, n_heads=H, head_dk=d, head_dv=d).to(torch.bfloat16).cuda()
+    g = torch.Generator(device="cuda").manual_seed(1)
+    h = torch.randn(B, T, H * d, device="cuda", generator=g).to(torch.bfloat16).requires_grad_()
+    dy = torch.randn(B, T, H * d, device="cuda", generator=g).to(torch.bfloat16)
+
+    def step():
+        m.zero_grad(set_to_none=True)
+        h.grad = None
+        m(h).backward(dy)
+
+    ms, stages = timed(step, args.steps, args.warmup)
+    tokens = B * T
+    dd = {"q": torch.empty(B, T, H, 0), "cu_seqlens": None, "initial_state": None}
+    kern = kernel_rooflines(stages, dd, d, d, 2, True)
+    dom = max(kern, key=lambda s: kern[s]["avg_launch_us"])
+    core_ms = sum(k["avg_launch_us"] * stages[s][1] for s, k in kern.items()) / 1e3 / args.steps
+    D = H * d
+    gemm_flops = 3 * 2 * tokens * D * (H * (3 * d) + 3 * H + H * d)   # fwd + two bwd products
+    return {
+        "metric": f"Q-Delta layer fwd+bwd tokens/s (B={B},T={T},d_model={D},H={H},d={d},bf16)",
+        "value": tokens / (ms / 1e3), "unit": "tokens/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": ms, "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": f"layer bf16 B={B} T={T} d_model={D} H={H} d={d} (decay on)",
+                   "parallelism": "single GPU"},
+        "qdelta_kernels_ms_per_step": core_ms,
+        "other_ms_per_step": ms - core_ms,
+        "projection_gemm_tflops_per_step": gemm_flops / 1e12,
+        "kernel_avg_us": {s: round(k["avg_launch_us"], 2) for s, k in kern.items()},
+        "kernels": kern,
+        # counters were taken on the chunk-kernel benchmark, not on this workload
+        "roofline": roofline_of(kern, dom, None),
+    }
+
+
+def run_recurrent(args):
+    """Fully recurrent forward on short continuing sequences (64 sequences
+    from a carried state, H=16, d=128, bf16) at T = 16 tokens, with the
+    chunkwise forward on the same input timed beside it, and both at T = 4
+    and T = 64 to show where the two forms cross over."""
+    B, H, d, T_main = 64, 16, 128, 16
+    by_T = {}
+    out_main = None
+    for T in (4, 16, 64):
+        dd = synth.make(B, T, H, d, d, "bf16", args.gate, seed=20260007, s0=True)
+        g = {k: (v.cuda() if isinstance(v, torch.Tensor) else v) for k, v in dd.items()}
+        ins = (g["q"], g["k"], g["v"], g["beta"], g["lam"], g["log_alpha"], g["initial_state"])
+        wsf = torch.empty(max(1, qdelta.workspace_bytes(B, T, H, d, d, qdelta.QDELTA_BF16, 0, False)),
+                          dtype=torch.uint8, device="cuda")
+        ms, stages = timed(lambda: qdelta.recurrent_fwd(*ins), args.steps, args.warmup)
+        ms_chunk, _ = timed(lambda: qdelta.chunk_fwd(*ins, save_states=False, workspace=wsf),
+                            args.steps, args.warmup)
+        by_T[T] = {"recurrent_ms": ms, "chunk_ms": ms_chunk}
+        if T == T_main:
+            tot, launches = stages["rec_fwd"]
+            out_main = (ms, tot / launches / 1e3, ms_chunk)
+    ms, avg_s, ms_chunk = out_main
+    T = T_main
+    # ALU roofline: 6 Dk Dv flops per token-head (S x and S q dot products, rank-1 update)
+    flops = B * T * H * 6 * d * d
+    kern = {"rec_fwd": {"avg_launch_us": avg_s * 1e6, "alg_flops_per_launch": flops,
+                        "achieved_TFLOPs": flops / avg_s / 1e12, "frac": flops / avg_s / VALU_F32_PEAK}}
+    return {
+        "metric": f"Q-Delta recurrent fwd tokens/s (B={B},T={T},H={H},d={d},bf16, carried state)",
+        "value": B * T / (ms / 1e3), "unit": "tokens/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": ms, "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": f"recurrent fwd bf16 B={B} T={T} H={H} d={d} with initial state",
+                   "gate_mode": args.gate, "parallelism": "single GPU"},
+        "chunk_fwd_ms_same_input": ms_chunk,
+        "by_T": by_T,
+        "kernel_avg_us": {"rec_fwd": round(avg_s * 1e6, 2)},
+        "kernels": kern,
+        "roofline": {"bound": "alu", "kernel": "rec_fwd", "achieved": flops / avg_s / 1e12,
+                     "peak": VALU_F32_PEAK / 1e12, "unit": "TFLOP/s", "frac": flops / avg_s / VALU_F32_PEAK,
+                     "traffic": None, "avg_launch_us": avg_s * 1e6},
+    }
+
+
 def run_decode(args):
     """1024 successive single-token updates of 64 sequences (H=16, d=128)."""
     wl = synth.WORKLOADS[4]
@@ -338,7 +430,7 @@ def main():
     ap.add_argument("--steps", type=int, default=100)
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--gate", default="G2", choices=["G1", "G2", "G3"])
-    ap.add_argument("--workload", default="train", choices=["train", "fwd", "long", "decode", "varlen", "tiny"])
+    ap.add_argument("--workload", default="train", choices=["train", "fwd", "long", "decode", "varlen", "tiny", "layer", "recurrent"])
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--cpu-units", type=int, default=64)
     ap.add_argument("--calib-copy", type=int, default=0, metavar="MIB",
@@ -355,6 +447,10 @@ def main():
 
     if args.workload == "decode":
         out = run_decode(args)
+    elif args.workload == "layer":
+        out = run_layer(args)
+    elif args.workload == "recurrent":
+        out = run_recurrent(args)
     else:
         wid = WORKLOAD_IDS[args.workload]
         out = run_chunk(args, wid, synth.WORKLOADS[wid].bwd)

@@ -115,7 +115,9 @@ size_t qdelta_chunk_workspace_bytes(int32_t B, int32_t T, int32_t H, int32_t Dk,
 
 /* Chunkwise forward (Sec. 3.3 chunkwise form; App. D).
  *   q, k [B,T,H,Dk], v [B,T,H,Dv]           activations (dtype)
- *   beta, lam [B,T,H]                        write strength and query-feedback gate (fp32)
+ *   beta [B,T,H]                             write strength (fp32)
+ *   lam [B,T,H] or NULL                      query-feedback gate (fp32); NULL means lambda == 0,
+ *                                            the gated delta rule of Sec. 2 (x_t = k_t)
  *   log_alpha [B,T,H] or NULL                log of the forget gate (fp32)
  *   initial_state [B,H,Dv,Dk] or NULL        entry state (NULL = zero)
  *   o [B,T,H,Dv]                             output o_t = S_t q_t (dtype)
@@ -144,7 +146,8 @@ int qdelta_chunk_fwd_varlen(int32_t T, int32_t N, const int32_t* cu_seqlens, int
  *   saved           the saved context from qdelta_chunk_fwd on the same inputs,
  *                   or NULL to recompute the state scan inside this call
  *   d_o [B,T,H,Dv]  (dtype);  d_final_state [B,H,Dv,Dk] or NULL (= zero)
- *   dq, dk [B,T,H,Dk], dv [B,T,H,Dv] (dtype); dbeta, dlam [B,T,H] (fp32)
+ *   dq, dk [B,T,H,Dk], dv [B,T,H,Dv] (dtype); dbeta [B,T,H] (fp32)
+ *   dlam [B,T,H] fp32: required iff lam != NULL, else must be NULL
  *   dlog_alpha [B,T,H] fp32: required iff log_alpha != NULL, else must be NULL
  *   d_initial_state [B,H,Dv,Dk] or NULL */
 int qdelta_chunk_bwd(int32_t B, int32_t T, int32_t H, int32_t Dk, int32_t Dv, int32_t chunk,
@@ -169,7 +172,7 @@ int qdelta_chunk_bwd_varlen(int32_t T, int32_t N, const int32_t* cu_seqlens, int
 /* One token of the recurrence for N sequences (decode), Sec. 3.3
  * Eq. (qdelta_decay) applied once:
  *   q, k [N,H,Dk], v [N,H,Dv] (dtype); beta, lam, log_alpha [N,H] (fp32,
- *   log_alpha may be NULL);  state [N,H,Dv,Dk] fp32, updated in place;
+ *   lam (NULL: lambda == 0) and log_alpha (NULL: alpha == 1) may be NULL);  state [N,H,Dv,Dk] fp32, updated in place;
  *   o [N,H,Dv] (dtype) = updated state times q.
  * Supported: Dk in {64, 128}, Dv a positive multiple of 8 up to 256, any dtype. */
 int qdelta_recurrent_step(int32_t N, int32_t H, int32_t Dk, int32_t Dv, int32_t dtype,
@@ -177,17 +180,42 @@ int qdelta_recurrent_step(int32_t N, int32_t H, int32_t Dk, int32_t Dv, int32_t 
                           const float* lam, const float* log_alpha, float* state, void* o,
                           hipStream_t stream);
 
+/* Fully recurrent forward over whole sequences: Sec. 3.3 Eq. (qdelta_decay)
+ * applied token by token (the paper provides this form beside the chunkwise
+ * one).  Same results as qdelta_chunk_fwd up to rounding, one launch, no
+ * workspace and no saved context (inference and short sequences).
+ *   q, k [B,T,H,Dk], v [B,T,H,Dv] (dtype); beta [B,T,H] fp32;
+ *   lam [B,T,H] or NULL (lambda == 0); log_alpha [B,T,H] or NULL (alpha == 1);
+ *   initial_state [B,H,Dv,Dk] fp32 or NULL (zero);
+ *   o [B,T,H,Dv] (dtype); final_state [B,H,Dv,Dk] fp32 or NULL.
+ * Supported: Dk in {64, 128}, Dv a positive multiple of 8 up to 256, any dtype. */
+int qdelta_recurrent_fwd(int32_t B, int32_t T, int32_t H, int32_t Dk, int32_t Dv, int32_t dtype,
+                         const void* q, const void* k, const void* v, const float* beta,
+                         const float* lam, const float* log_alpha, const float* initial_state,
+                         void* o, float* final_state, hipStream_t stream);
+
+/* Varlen recurrent forward: B == 1, T total tokens, N sequences delimited by
+ * the device array cu_seqlens[N+1] (entries are clamped to [0, T]); states
+ * are [N,H,Dv,Dk]. */
+int qdelta_recurrent_fwd_varlen(int32_t T, int32_t N, const int32_t* cu_seqlens, int32_t H,
+                                int32_t Dk, int32_t Dv, int32_t dtype, const void* q,
+                                const void* k, const void* v, const float* beta,
+                                const float* lam, const float* log_alpha,
+                                const float* initial_state, void* o, float* final_state,
+                                hipStream_t stream);
+
 /* Measurement facility (benchmarks and profiling only; not thread-safe).
  * qdelta_profile_begin() starts recording a pair of HIP events around every
  * kernel launch of the library, on the launch stream, tagged by stage:
  *   0 chunk preparation (forward)       1 forward state scan + chunk output
  *   2 chunk preparation (backward)      3 backward state scan (+ dv)
  *   4 intra-chunk backward              5 recurrent step
+ *   6 recurrent forward
  * qdelta_profile_end() waits for the recorded events, writes the summed kernel
  * time (milliseconds) and the number of launches of each stage into the
  * caller's arrays of QDELTA_N_STAGES entries (either may be NULL) and stops
  * recording.  Returns QDELTA_EHIP if an event call failed. */
-#define QDELTA_N_STAGES 6
+#define QDELTA_N_STAGES 7
 int qdelta_profile_begin(void);
 int qdelta_profile_end(float* ms, int32_t* launches);
 

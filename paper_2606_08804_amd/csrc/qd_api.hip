@@ -130,9 +130,10 @@ int fwd_impl(bool varlen, int32_t B, int32_t T, int32_t N, const int32_t* cu, in
   rc = check_dims(s.tokens, H, Dk, Dv, chunk, dtype);
   if (rc) return rc;
   const bool has_tokens = s.tokens > 0;
-  if (has_tokens && !(ok_ptr(q) && ok_ptr(k) && ok_ptr(v) && ok_ptr(beta) && ok_ptr(lam) && ok_ptr(o)))
+  if (has_tokens && !(ok_ptr(q) && ok_ptr(k) && ok_ptr(v) && ok_ptr(beta) && ok_ptr(o)))
     return QDELTA_EINVAL;
-  if (!ok_opt(log_alpha) || !ok_opt(initial_state) || !ok_opt(final_state) || !ok_opt(saved))
+  if (!ok_opt(lam) || !ok_opt(log_alpha) || !ok_opt(initial_state) || !ok_opt(final_state) ||
+      !ok_opt(saved))
     return QDELTA_EINVAL;
   const int esz = dtype == QDELTA_BF16 ? 2 : 4;
   const Layout L = make_layout(s.slots * (size_t)H, Dk, Dv, esz, false);
@@ -179,11 +180,13 @@ int bwd_impl(bool varlen, int32_t B, int32_t T, int32_t N, const int32_t* cu, in
   if (rc) return rc;
   const bool has_tokens = s.tokens > 0;
   if (has_tokens &&
-      !(ok_ptr(q) && ok_ptr(k) && ok_ptr(v) && ok_ptr(beta) && ok_ptr(lam) && ok_ptr(d_o) &&
-        ok_ptr(dq) && ok_ptr(dk) && ok_ptr(dv) && ok_ptr(dbeta) && ok_ptr(dlam)))
+      !(ok_ptr(q) && ok_ptr(k) && ok_ptr(v) && ok_ptr(beta) && ok_ptr(d_o) &&
+        ok_ptr(dq) && ok_ptr(dk) && ok_ptr(dv) && ok_ptr(dbeta)))
     return QDELTA_EINVAL;
   if ((log_alpha == nullptr) != (dlog_alpha == nullptr) && has_tokens) return QDELTA_EINVAL;
-  if (!ok_opt(log_alpha) || !ok_opt(dlog_alpha) || !ok_opt(initial_state) ||
+  if ((lam == nullptr) != (dlam == nullptr) && has_tokens) return QDELTA_EINVAL;
+  if (!ok_opt(lam) || !ok_opt(dlam) || !ok_opt(log_alpha) || !ok_opt(dlog_alpha) ||
+      !ok_opt(initial_state) ||
       !ok_opt(saved) || !ok_opt(d_final_state) || !ok_opt(d_initial_state))
     return QDELTA_EINVAL;
   const int esz = dtype == QDELTA_BF16 ? 2 : 4;
@@ -382,6 +385,48 @@ int qdelta_chunk_bwd_varlen(int32_t T, int32_t N, const int32_t* cu_seqlens, int
                   dlam, dlog_alpha, d_initial_state, ws, ws_bytes, stream);
 }
 
+static int rec_fwd_impl(bool varlen, int32_t B, int32_t T, int32_t N, const int32_t* cu, int32_t H,
+                 int32_t Dk, int32_t Dv, int32_t dtype, const void* q, const void* k,
+                 const void* v, const float* beta, const float* lam, const float* log_alpha,
+                 const float* initial_state, void* o, float* final_state, hipStream_t stream) {
+  if (T < 0 || H <= 0) return QDELTA_EINVAL;
+  if (varlen ? (N < 0 || cu == nullptr) : B < 0) return QDELTA_EINVAL;
+  if (dtype != QDELTA_F32 && dtype != QDELTA_BF16) return QDELTA_EINVAL;
+  if ((Dk != 64 && Dk != 128) || Dv <= 0 || Dv > 256 || (Dv % 8) != 0) return QDELTA_EUNSUPPORTED;
+  const int64_t tokens = varlen ? T : (int64_t)B * T;
+  const int32_t n_seqs = varlen ? N : B;
+  // token offsets (t * H + h) and unit indices stay below 2^31
+  if (tokens * H >= (int64_t(1) << 31) || (int64_t)n_seqs * H >= (int64_t(1) << 31))
+    return QDELTA_EUNSUPPORTED;
+  if (tokens > 0 && !(ok_ptr(q) && ok_ptr(k) && ok_ptr(v) && ok_ptr(beta) && ok_ptr(o)))
+    return QDELTA_EINVAL;
+  if (!ok_opt(lam) || !ok_opt(log_alpha) || !ok_opt(initial_state) || !ok_opt(final_state))
+    return QDELTA_EINVAL;
+  if (n_seqs == 0) return QDELTA_OK;
+  hipError_t e = qd::launch_rec_fwd(n_seqs, varlen ? 0 : T, varlen ? cu : nullptr, (int)tokens, H,
+                                    Dk, Dv, dtype, q, k, v, beta, lam, log_alpha, initial_state,
+                                    final_state, o, stream);
+  return e == hipSuccess ? QDELTA_OK : QDELTA_EHIP;
+}
+
+int qdelta_recurrent_fwd(int32_t B, int32_t T, int32_t H, int32_t Dk, int32_t Dv, int32_t dtype,
+                         const void* q, const void* k, const void* v, const float* beta,
+                         const float* lam, const float* log_alpha, const float* initial_state,
+                         void* o, float* final_state, hipStream_t stream) {
+  return rec_fwd_impl(false, B, T, B, nullptr, H, Dk, Dv, dtype, q, k, v, beta, lam, log_alpha,
+                      initial_state, o, final_state, stream);
+}
+
+int qdelta_recurrent_fwd_varlen(int32_t T, int32_t N, const int32_t* cu_seqlens, int32_t H,
+                                int32_t Dk, int32_t Dv, int32_t dtype, const void* q,
+                                const void* k, const void* v, const float* beta,
+                                const float* lam, const float* log_alpha,
+                                const float* initial_state, void* o, float* final_state,
+                                hipStream_t stream) {
+  return rec_fwd_impl(true, 1, T, N, cu_seqlens, H, Dk, Dv, dtype, q, k, v, beta, lam,
+                      log_alpha, initial_state, o, final_state, stream);
+}
+
 int qdelta_recurrent_step(int32_t N, int32_t H, int32_t Dk, int32_t Dv, int32_t dtype,
                           const void* q, const void* k, const void* v, const float* beta,
                           const float* lam, const float* log_alpha, float* state, void* o,
@@ -391,8 +436,8 @@ int qdelta_recurrent_step(int32_t N, int32_t H, int32_t Dk, int32_t Dv, int32_t 
   if ((Dk != 64 && Dk != 128) || Dv <= 0 || Dv > 256 || (Dv % 8) != 0) return QDELTA_EUNSUPPORTED;
   if ((int64_t)N * H * 32 >= (int64_t(1) << 31)) return QDELTA_EUNSUPPORTED;
   if (N == 0) return QDELTA_OK;
-  if (!(ok_ptr(q) && ok_ptr(k) && ok_ptr(v) && ok_ptr(beta) && ok_ptr(lam) && ok_ptr(state) &&
-        ok_ptr(o) && ok_opt(log_alpha)))
+  if (!(ok_ptr(q) && ok_ptr(k) && ok_ptr(v) && ok_ptr(beta) && ok_ptr(state) && ok_ptr(o) &&
+        ok_opt(lam) && ok_opt(log_alpha)))
     return QDELTA_EINVAL;
   hipError_t e = qd::launch_step(N, H, Dk, Dv, dtype, q, k, v, beta, lam, log_alpha, state, o, stream);
   return e == hipSuccess ? QDELTA_OK : QDELTA_EHIP;

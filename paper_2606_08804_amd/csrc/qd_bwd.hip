@@ -845,7 +845,7 @@ __global__ __launch_bounds__(INTRA_THREADS) __attribute__((amdgpu_waves_per_eu(2
     if (j < len) {
       const size_t gt = arow + (size_t)j * H;
       p.dbeta[gt] = sm.rdbeta[j] + cb_;
-      p.dlam[gt] = sm.rdl[j];
+      if (p.dlam) p.dlam[gt] = sm.rdl[j];
       if (p.dla) p.dla[gt] = suffix;
     }
   }

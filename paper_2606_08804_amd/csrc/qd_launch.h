@@ -14,7 +14,8 @@ enum Stage {
   ST_SCAN_BWD = 3,
   ST_INTRA = 4,
   ST_STEP = 5,
-  ST_COUNT = 6
+  ST_REC_FWD = 6,
+  ST_COUNT = 7
 };
 
 // Records a HIP event on `st` before (after == 0) or after (after == 1) a
@@ -36,5 +37,12 @@ hipError_t launch_bwd(const Params& p, int dtype, int Dk, int Dv, hipStream_t st
 hipError_t launch_step(int N, int H, int Dk, int Dv, int dtype, const void* q, const void* k,
                        const void* v, const float* beta, const float* lam, const float* la,
                        float* state, void* o, hipStream_t st);
+
+// Fully recurrent forward over whole sequences: dense (cu == nullptr, N
+// sequences of T tokens) or packed (cu[N+1] on the device, T_total tokens).
+hipError_t launch_rec_fwd(int N, int T, const int* cu, int T_total, int H, int Dk, int Dv,
+                          int dtype, const void* q, const void* k, const void* v,
+                          const float* beta, const float* lam, const float* la, const float* S0,
+                          float* Sfin, void* o, hipStream_t st);
 
 }  // namespace qd

@@ -12,6 +12,10 @@ chunk_fwd(q, k, v, beta, lam, log_alpha=None, initial_state=None, cu_seqlens=Non
 chunk_bwd(q, k, v, beta, lam, log_alpha, initial_state, saved_states, d_o,
           d_final_state=None, cu_seqlens=None) -> dict of gradients
 recurrent_step(q, k, v, beta, lam, log_alpha, state) -> o        (state updated in place)
+recurrent_fwd(q, k, v, beta, lam=None, log_alpha=None, initial_state=None, cu_seqlens=None)
+          -> (o, final_state)                                  (token by token, one launch)
+
+lam=None means lambda == 0 (the gated delta rule); log_alpha=None means alpha == 1.
 """
 import ctypes
 import os
@@ -29,10 +33,11 @@ EXPORTS = (
     "qdelta_status_string", "qdelta_version", "qdelta_saved_state_slots", "qdelta_saved_bytes",
     "qdelta_chunk_workspace_bytes", "qdelta_chunk_fwd", "qdelta_chunk_fwd_varlen",
     "qdelta_chunk_bwd", "qdelta_chunk_bwd_varlen", "qdelta_recurrent_step",
+    "qdelta_recurrent_fwd", "qdelta_recurrent_fwd_varlen",
     "qdelta_profile_begin", "qdelta_profile_end",
 )
 
-STAGES = ("prep_fwd", "scan_fwd", "prep_bwd", "scan_bwd", "intra", "step")
+STAGES = ("prep_fwd", "scan_fwd", "prep_bwd", "scan_bwd", "intra", "step", "rec_fwd")
 
 _lib = None
 
@@ -72,6 +77,10 @@ def lib():
         L.qdelta_chunk_bwd_varlen.restype = ctypes.c_int
         L.qdelta_recurrent_step.argtypes = [i32] * 5 + [P] * 8 + [P]
         L.qdelta_recurrent_step.restype = ctypes.c_int
+        L.qdelta_recurrent_fwd.argtypes = [i32] * 6 + [P] * 9 + [P]
+        L.qdelta_recurrent_fwd.restype = ctypes.c_int
+        L.qdelta_recurrent_fwd_varlen.argtypes = [i32, i32, P] + [i32] * 4 + [P] * 9 + [P]
+        L.qdelta_recurrent_fwd_varlen.restype = ctypes.c_int
         L.qdelta_profile_begin.argtypes = []
         L.qdelta_profile_begin.restype = ctypes.c_int
         L.qdelta_profile_end.argtypes = [P, P]
@@ -169,7 +178,7 @@ def chunk_fwd(q, k, v, beta, lam, log_alpha=None, initial_state=None, cu_seqlens
     _need(k, "k", q.dtype, q.shape)
     _need(v, "v", q.dtype, tuple(act) + (Dv,))
     _need(beta, "beta", torch.float32, act)
-    _need(lam, "lam", torch.float32, act)
+    _opt(lam, "lam", torch.float32, act)
     _opt(log_alpha, "log_alpha", torch.float32, act)
     _opt(initial_state, "initial_state", torch.float32, (N, H, Dv, Dk))
     if cu_seqlens is not None:
@@ -194,8 +203,9 @@ def chunk_fwd(q, k, v, beta, lam, log_alpha=None, initial_state=None, cu_seqlens
 
 def chunk_bwd(q, k, v, beta, lam, log_alpha, initial_state, saved_states, d_o,
               d_final_state=None, cu_seqlens=None, need_d_initial_state=True, workspace=None):
-    """Chunkwise Q-Delta backward.  Returns a dict: dq, dk, dv, dbeta, dlam,
-    dlog_alpha (None without decay), d_initial_state (None if not requested)."""
+    """Chunkwise Q-Delta backward.  Returns a dict: dq, dk, dv, dbeta, dlam
+    (None when lam is None), dlog_alpha (None without decay), d_initial_state
+    (None if not requested)."""
     L = lib()
     dt = _dt(q)
     B, T, H, Dk, Dv, N = _dims(q, v, cu_seqlens)
@@ -204,7 +214,7 @@ def chunk_bwd(q, k, v, beta, lam, log_alpha, initial_state, saved_states, d_o,
     _need(k, "k", q.dtype, q.shape)
     _need(v, "v", q.dtype, tuple(act) + (Dv,))
     _need(beta, "beta", torch.float32, act)
-    _need(lam, "lam", torch.float32, act)
+    _opt(lam, "lam", torch.float32, act)
     _opt(log_alpha, "log_alpha", torch.float32, act)
     _opt(initial_state, "initial_state", torch.float32, (N, H, Dv, Dk))
     _opt(saved_states, "saved_states")
@@ -222,7 +232,7 @@ def chunk_bwd(q, k, v, beta, lam, log_alpha, initial_state, saved_states, d_o,
     dk = torch.empty_like(k)
     dv = torch.empty_like(v)
     dbeta = torch.empty_like(beta)
-    dlam = torch.empty_like(lam)
+    dlam = torch.empty_like(lam) if lam is not None else None
     dla = torch.empty_like(log_alpha) if log_alpha is not None else None
     dS0 = torch.empty((N, H, Dv, Dk), dtype=torch.float32, device=dev) if need_d_initial_state else None
     nbytes = workspace_bytes(B, T, H, Dk, Dv, dt, n_seqs, True)
@@ -248,7 +258,7 @@ def recurrent_step(q, k, v, beta, lam, log_alpha, state, out=None):
     _need(k, "k", q.dtype, q.shape)
     _need(v, "v", q.dtype, (N, H, Dv))
     _need(beta, "beta", torch.float32, (N, H))
-    _need(lam, "lam", torch.float32, (N, H))
+    _opt(lam, "lam", torch.float32, (N, H))
     _opt(log_alpha, "log_alpha", torch.float32, (N, H))
     _need(state, "state", torch.float32, (N, H, Dv, Dk))
     o = out if out is not None else torch.empty((N, H, Dv), dtype=q.dtype, device=q.device)
@@ -257,6 +267,35 @@ def recurrent_step(q, k, v, beta, lam, log_alpha, state, out=None):
            L.qdelta_recurrent_step(N, H, Dk, Dv, dt, _p(q), _p(k), _p(v), _p(beta), _p(lam),
                                    _p(log_alpha), _p(state), _p(o), _stream()))
     return o
+
+
+def recurrent_fwd(q, k, v, beta, lam=None, log_alpha=None, initial_state=None, cu_seqlens=None,
+                  output_final_state=True):
+    """Fully recurrent forward (token by token, one launch).  Same layouts as
+    chunk_fwd.  Returns (o, final_state or None)."""
+    L = lib()
+    dt = _dt(q)
+    B, T, H, Dk, Dv, N = _dims(q, v, cu_seqlens)
+    act = q.shape[:-1]
+    _need(q, "q", q.dtype)
+    _need(k, "k", q.dtype, q.shape)
+    _need(v, "v", q.dtype, tuple(act) + (Dv,))
+    _need(beta, "beta", torch.float32, act)
+    _opt(lam, "lam", torch.float32, act)
+    _opt(log_alpha, "log_alpha", torch.float32, act)
+    _opt(initial_state, "initial_state", torch.float32, (N, H, Dv, Dk))
+    if cu_seqlens is not None:
+        _need(cu_seqlens, "cu_seqlens", torch.int32)
+    o = torch.empty(tuple(act) + (Dv,), dtype=q.dtype, device=q.device)
+    Sf = torch.empty((N, H, Dv, Dk), dtype=torch.float32, device=q.device) if output_final_state else None
+    common = (H, Dk, Dv, dt, _p(q), _p(k), _p(v), _p(beta), _p(lam), _p(log_alpha),
+              _p(initial_state), _p(o), _p(Sf), _stream())
+    if cu_seqlens is None:
+        _check("qdelta_recurrent_fwd", L.qdelta_recurrent_fwd(B, T, *common))
+    else:
+        _check("qdelta_recurrent_fwd_varlen",
+               L.qdelta_recurrent_fwd_varlen(T, N, _p(cu_seqlens), *common))
+    return o, Sf
 
 
 def profile_begin():

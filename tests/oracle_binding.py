@@ -1,0 +1,57 @@
+"""A stand-in for the library binding's chunk_fwd / chunk_bwd, computed by the
+fp64 oracle on the CPU, for tests of the autograd layer: its gradient wiring
+on the CPU, and the reference that the GPU layer is compared with.
+
+Same call signatures as ``paper_2606_08804_amd.qdelta``; results come back as
+CPU tensors in the inputs' dtype.  ``saved`` is a token that carries nothing:
+the oracle's backward recomputes the recurrence."""
+import numpy as np
+import torch
+
+from oracle import recurrent
+
+
+def _np(t):
+    return None if t is None else t.detach().cpu().double().numpy()
+
+
+def _packed(t, cu):
+    a = _np(t)
+    return None if a is None else (a[0] if cu is not None else a)
+
+
+def _zeros_like_gate(beta):
+    return np.zeros(beta.shape)
+
+
+def chunk_fwd(q, k, v, beta, lam, log_alpha=None, initial_state=None, cu_seqlens=None,
+              output_final_state=True, save_states=False, workspace=None):
+    cu = None if cu_seqlens is None else cu_seqlens.cpu().numpy()
+    lam_ = _packed(lam, cu) if lam is not None else _zeros_like_gate(_packed(beta, cu))
+    o, Sf = recurrent.fwd(_packed(q, cu), _packed(k, cu), _packed(v, cu), _packed(beta, cu), lam_,
+                          _packed(log_alpha, cu), _np(initial_state), cu_seqlens=cu)
+    if cu is not None:
+        o = o[None]
+    o = torch.from_numpy(o).to(q.dtype)
+    Sf = torch.from_numpy(Sf).to(torch.float32 if q.dtype != torch.float64 else q.dtype)
+    saved = torch.zeros(1, dtype=torch.uint8) if save_states else None
+    return o, (Sf if output_final_state else None), saved
+
+
+def chunk_bwd(q, k, v, beta, lam, log_alpha, initial_state, saved_states, d_o,
+              d_final_state=None, cu_seqlens=None, need_d_initial_state=True, workspace=None):
+    cu = None if cu_seqlens is None else cu_seqlens.cpu().numpy()
+    lam_ = _packed(lam, cu) if lam is not None else _zeros_like_gate(_packed(beta, cu))
+    g = recurrent.bwd(_packed(q, cu), _packed(k, cu), _packed(v, cu), _packed(beta, cu), lam_,
+                      _packed(log_alpha, cu), _np(initial_state), d_o=_packed(d_o, cu),
+                      d_final_state=_np(d_final_state), cu_seqlens=cu)
+    out = {}
+    like = dict(dq=q, dk=k, dv=v, dbeta=beta, dlam=lam, dlog_alpha=log_alpha,
+                d_initial_state=initial_state)
+    for key, ref in like.items():
+        if ref is None or g[key] is None or (key == "d_initial_state" and not need_d_initial_state):
+            out[key] = None
+            continue
+        a = g[key][None] if (cu is not None and key != "d_initial_state") else g[key]
+        out[key] = torch.from_numpy(np.ascontiguousarray(a)).to(ref.dtype)
+    return out

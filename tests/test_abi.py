@@ -22,7 +22,7 @@ def header_functions():
 def test_library_exports_every_declared_symbol():
     L = qdelta.lib()
     names = header_functions()
-    assert len(names) == 12
+    assert len(names) == 14
     for n in names:
         assert hasattr(L, n), n
     assert sorted(names) == sorted(qdelta.EXPORTS)
@@ -131,6 +131,29 @@ def test_recurrent_step_rejects_bad_arguments():
     assert L.qdelta_recurrent_step(1, 0, 64, 64, 1, f, f, f, f, f, None, f, f, None) == E.QDELTA_EINVAL
     assert L.qdelta_recurrent_step(0, 1, 64, 64, 1, None, None, None, None, None, None, None, None,
                                    None) == E.QDELTA_OK
+
+
+def test_recurrent_fwd_rejects_bad_arguments():
+    """Validation of the recurrent forward happens before any launch; calls
+    with nothing to do return OK without touching the device."""
+    L = qdelta.lib()
+    E = qdelta
+    f = FAKE
+    args = (f, f, f, f, None, None, None, f, None, None)
+    assert L.qdelta_recurrent_fwd(1, 8, 1, 96, 64, 1, *args) == E.QDELTA_EUNSUPPORTED
+    assert L.qdelta_recurrent_fwd(1, 8, 1, 64, 300, 1, *args) == E.QDELTA_EUNSUPPORTED
+    assert L.qdelta_recurrent_fwd(1, 8, 1, 64, 64, 7, *args) == E.QDELTA_EINVAL
+    assert L.qdelta_recurrent_fwd(1, -1, 1, 64, 64, 1, *args) == E.QDELTA_EINVAL
+    assert L.qdelta_recurrent_fwd(1, 8, 1, 64, 64, 1, f + 4, f, f, f, None, None, None, f, None,
+                                  None) == E.QDELTA_EINVAL
+    assert L.qdelta_recurrent_fwd(1, 8, 1, 64, 64, 1, None, f, f, f, None, None, None, f, None,
+                                  None) == E.QDELTA_EINVAL
+    assert L.qdelta_recurrent_fwd(1, 8, 1, 64, 64, 1, f, f, f, f, f + 8, None, None, f, None,
+                                  None) == E.QDELTA_EINVAL
+    # no sequences: nothing to do
+    assert L.qdelta_recurrent_fwd(0, 8, 1, 64, 64, 1, *([None] * 10)) == E.QDELTA_OK
+    assert L.qdelta_recurrent_fwd_varlen(0, 0, f, 1, 64, 64, 1, *([None] * 10)) == E.QDELTA_OK
+    assert L.qdelta_recurrent_fwd_varlen(8, 1, None, 1, 64, 64, 1, *args) == E.QDELTA_EINVAL
 
 
 def test_binding_validates_before_calling_library():

@@ -1,0 +1,57 @@
+"""The autograd layer on the GPU (bf16 parameters and activations, HIP
+recurrence) against the same layer in fp64 on the CPU with the recurrence
+computed by the oracle: output and the gradients of the input and of every
+parameter, normwise (max|got-ref|/max|ref|) within the bf16 tolerance; the
+scalar gate-bias gradient, a sum over every (token, head), relative to the
+sum of its summands' magnitudes."""
+import copy
+
+import pytest
+import torch
+
+from paper_2606_08804_amd import layer
+from tests import oracle_binding
+from tests.gpu_helpers import TOL, normwise
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.mark.parametrize("use_decay,varlen", [(True, False), (False, True)])
+def test_layer_matches_oracle_layer(monkeypatch, use_decay, varlen):
+    torch.manual_seed(41)
+    m = layer.QDeltaLayer(d_model=256, n_heads=2, head_dk=128, head_dv=128, use_decay=use_decay)
+    m = m.to(torch.bfloat16)
+    ref = copy.deepcopy(m).double()
+    g = torch.Generator().manual_seed(42)
+    B, T = (1, 270) if varlen else (2, 150)
+    h = torch.randn(B, T, 256, generator=g).to(torch.bfloat16)
+    dy = torch.randn(B, T, 256, generator=g).to(torch.bfloat16)
+    cu = torch.tensor([0, 70, 71, 270], dtype=torch.int32) if varlen else None
+
+    mg = m.cuda()
+    hg = h.cuda().requires_grad_()
+    y = mg(hg, cu_seqlens=None if cu is None else cu.cuda())
+    y.backward(dy.cuda())
+    torch.cuda.synchronize()
+
+    monkeypatch.setattr(layer, "_binding", oracle_binding)
+    # the reference's lambda bias, broadcast to one copy per (token, head), so
+    # that its gradient holds the summands of the scalar bias gradient
+    H = ref.H
+    ref.lambda_bias = torch.nn.Parameter(ref.lambda_bias.detach().expand(B, T, H).clone())
+    hr = h.double().requires_grad_()
+    yr = ref(hr, cu_seqlens=cu)
+    yr.backward(dy.double())
+
+    tol = TOL["bf16"]
+    assert normwise(y.detach().cpu().double().numpy(), yr.detach().numpy()) <= tol
+    assert normwise(hg.grad.cpu().double().numpy(), hr.grad.numpy()) <= tol
+    for (name, p), (_, pr) in zip(mg.named_parameters(), ref.named_parameters()):
+        if name == "lambda_bias":
+            # a sum over every (token, head) with cancellation: its error is
+            # measured against the sum of the summands' magnitudes
+            terms = pr.grad
+            err = abs(float(p.grad) - float(terms.sum())) / float(terms.abs().sum())
+        else:
+            err = normwise(p.grad.cpu().double().numpy(), pr.grad.numpy())
+        assert err <= tol, (name, err)

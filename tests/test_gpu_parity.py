@@ -200,6 +200,49 @@ def test_determinism():
             assert torch.equal(g1[key], g2[key]), key
 
 
+@pytest.mark.parametrize("dt", ["f32", "bf16"])
+@pytest.mark.parametrize("varlen", [False, True])
+def test_lambda_none_is_gated_delta_rule(dt, varlen):
+    """lam = NULL means lambda == 0: x_t = k_t, the gated delta rule.  The
+    result equals the oracle run with lambda = 0 and, bit for bit, the GPU
+    path run with an explicit all-zero lambda; no dlam is written."""
+    D = 128 if dt == "bf16" else 64
+    if varlen:
+        d = synth.make(1, 0, 2, D, D, dt, "G3", seed=131, s0=True, with_do=True,
+                       lengths=[70, 1, 130, 64])
+    else:
+        d = synth.make(2, 150, 2, D, D, dt, "G3", seed=131, s0=True, with_do=True)
+    d0 = dict(d, lam=torch.zeros_like(d["lam"]))
+    dn = dict(d, lam=None)
+    o, Sf, saved = gpu_fwd(dn, save_states=True)
+    _check(fwd_errors(d0, o, Sf), TOL[dt], f"fwd lam=None {dt}")
+    g = gpu_bwd(dn, saved)
+    assert g["dlam"] is None
+    _check(bwd_errors(d0, g, skip=("dlam",)), TOL[dt], f"bwd lam=None {dt}")
+    o0, Sf0, saved0 = gpu_fwd(d0, save_states=True)
+    g0 = gpu_bwd(d0, saved0)
+    assert torch.equal(o, o0) and torch.equal(Sf, Sf0)
+    for key in ("dq", "dk", "dv", "dbeta", "dlog_alpha", "d_initial_state"):
+        assert torch.equal(g[key], g0[key]), key
+
+
+def test_recurrent_step_lambda_none():
+    N, H, D = 8, 4, 128
+    d = synth.make(1, N, H, D, D, "bf16", "G2", seed=132)
+    S = torch.from_numpy(np.random.default_rng(6).normal(0, 0.02, (N, H, D, D)).astype(np.float32))
+    Sa, Sb = S.cuda(), S.cuda()
+    args = [d[key][0].cuda() for key in ("q", "k", "v", "beta")]
+    oa = qdelta.recurrent_step(*args, None, d["log_alpha"][0].cuda(), Sa)
+    ob = qdelta.recurrent_step(*args, torch.zeros(N, H, device="cuda"), d["log_alpha"][0].cuda(), Sb)
+    torch.cuda.synchronize()
+    assert torch.equal(oa, ob) and torch.equal(Sa, Sb)
+    ref_in = {key: d[key].transpose(0, 1).contiguous() for key in ("q", "k", "v", "beta", "log_alpha")}
+    ref_in.update(lam=torch.zeros(N, 1, H), initial_state=S, cu_seqlens=None)
+    o_ref, S_ref = oracle_fwd(ref_in)
+    assert normwise(f64(oa.cpu()[:, None]), o_ref) <= TOL["bf16"]
+    assert normwise(f64(Sa.cpu()), S_ref) <= TOL["bf16"]
+
+
 @pytest.mark.parametrize("dt,D", [("bf16", 128), ("f32", 64), ("bf16", 64)])
 def test_recurrent_step_parity(dt, D):
     N, H, steps = 8, 4, 5
