@@ -69,14 +69,21 @@ class QDeltaLayer(torch.nn.Module):
     (or wider)."""
 
     def __init__(self, d_model, n_heads, head_dk=128, head_dv=128, use_decay=True, qk_norm=True,
-                 lambda_bias=-0.8):
+                 lambda_bias=-0.8, fixed_lambda=None):
+        """fixed_lambda: None for the learned gate lambda_t = sigmoid(W h + b);
+        a number for a constant lambda (the paper's ablations: scalar 0.2, 0.5,
+        0.8, and 1.0 for "no gating"); 0 gives the gated delta rule (lambda is
+        passed as NULL).  use_decay=False gives alpha == 1 ("no state decay")."""
         super().__init__()
         self.d_model, self.H, self.dk, self.dv = d_model, n_heads, head_dk, head_dv
         self.use_decay, self.qk_norm = use_decay, qk_norm
+        self.fixed_lambda = None if fixed_lambda is None else float(fixed_lambda)
         self.w_qkv = torch.nn.Linear(d_model, n_heads * (2 * head_dk + head_dv), bias=False)
-        n_gates = 3 if use_decay else 2            # beta, lambda (, alpha)
+        # beta (, lambda) (, alpha)
+        n_gates = 1 + (self.fixed_lambda is None) + bool(use_decay)
         self.w_gates = torch.nn.Linear(d_model, n_gates * n_heads, bias=False)
-        self.lambda_bias = torch.nn.Parameter(torch.tensor(float(lambda_bias)))
+        if self.fixed_lambda is None:
+            self.lambda_bias = torch.nn.Parameter(torch.tensor(float(lambda_bias)))
         self.w_out = torch.nn.Linear(n_heads * head_dv, d_model, bias=False)
         self.reset_parameters()
 
@@ -85,13 +92,21 @@ class QDeltaLayer(torch.nn.Module):
             torch.nn.init.normal_(lin.weight, std=1.0 / math.sqrt(lin.in_features))
 
     def gates(self, h):
-        """beta, lambda, log alpha ([..., H] fp32 each; log alpha None without decay)."""
+        """beta, lambda, log alpha ([..., H] fp32 or wider; lambda None when
+        fixed at 0, log alpha None without decay)."""
         acc = torch.promote_types(h.dtype, torch.float32)
         g = self.w_gates(h).to(acc)
         H = self.H
         beta = torch.sigmoid(g[..., :H])
-        lam = torch.sigmoid(g[..., H:2 * H] + self.lambda_bias.to(acc))
-        log_alpha = F.logsigmoid(g[..., 2 * H:]) if self.use_decay else None
+        nxt = H
+        if self.fixed_lambda is None:
+            lam = torch.sigmoid(g[..., H:2 * H] + self.lambda_bias.to(acc))
+            nxt = 2 * H
+        elif self.fixed_lambda == 0.0:
+            lam = None
+        else:
+            lam = torch.full_like(beta, self.fixed_lambda)
+        log_alpha = F.logsigmoid(g[..., nxt:]) if self.use_decay else None
         return beta, lam, log_alpha
 
     def forward(self, h, initial_state=None, cu_seqlens=None, output_final_state=False):
@@ -105,7 +120,7 @@ class QDeltaLayer(torch.nn.Module):
             k = F.normalize(k.to(acc), dim=-1).to(h.dtype)
         beta, lam, log_alpha = self.gates(h)
         o, final_state = qdelta_chunk(q.contiguous(), k.contiguous(), v.contiguous(),
-                                      beta.contiguous(), lam.contiguous(),
+                                      beta.contiguous(), None if lam is None else lam.contiguous(),
                                       None if log_alpha is None else log_alpha.contiguous(),
                                       initial_state, cu_seqlens)
         y = self.w_out(o.reshape(B, T, H * dv))

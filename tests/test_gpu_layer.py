@@ -16,10 +16,12 @@ from tests.gpu_helpers import TOL, normwise
 pytestmark = pytest.mark.gpu
 
 
-@pytest.mark.parametrize("use_decay,varlen", [(True, False), (False, True)])
-def test_layer_matches_oracle_layer(monkeypatch, use_decay, varlen):
+@pytest.mark.parametrize("use_decay,varlen,fixed_lambda", [(True, False, None), (False, True, None),
+                                                          (True, False, 0.0)])
+def test_layer_matches_oracle_layer(monkeypatch, use_decay, varlen, fixed_lambda):
     torch.manual_seed(41)
-    m = layer.QDeltaLayer(d_model=256, n_heads=2, head_dk=128, head_dv=128, use_decay=use_decay)
+    m = layer.QDeltaLayer(d_model=256, n_heads=2, head_dk=128, head_dv=128, use_decay=use_decay,
+                          fixed_lambda=fixed_lambda)
     m = m.to(torch.bfloat16)
     ref = copy.deepcopy(m).double()
     g = torch.Generator().manual_seed(42)
@@ -37,8 +39,8 @@ def test_layer_matches_oracle_layer(monkeypatch, use_decay, varlen):
     monkeypatch.setattr(layer, "_binding", oracle_binding)
     # the reference's lambda bias, broadcast to one copy per (token, head), so
     # that its gradient holds the summands of the scalar bias gradient
-    H = ref.H
-    ref.lambda_bias = torch.nn.Parameter(ref.lambda_bias.detach().expand(B, T, H).clone())
+    if fixed_lambda is None:
+        ref.lambda_bias = torch.nn.Parameter(ref.lambda_bias.detach().expand(B, T, ref.H).clone())
     hr = h.double().requires_grad_()
     yr = ref(hr, cu_seqlens=cu)
     yr.backward(dy.double())

@@ -59,10 +59,11 @@ def test_function_gradcheck_varlen(oracle_core):
     assert torch.autograd.gradcheck(f, xs, eps=1e-6, atol=1e-7, rtol=1e-6)
 
 
-@pytest.mark.parametrize("use_decay", [True, False])
-def test_layer_gradcheck(oracle_core, use_decay):
+@pytest.mark.parametrize("use_decay,fixed_lambda", [(True, None), (False, None), (True, 0.5), (True, 0.0)])
+def test_layer_gradcheck(oracle_core, use_decay, fixed_lambda):
     torch.manual_seed(3)
-    m = layer.QDeltaLayer(d_model=6, n_heads=2, head_dk=3, head_dv=4, use_decay=use_decay).double()
+    m = layer.QDeltaLayer(d_model=6, n_heads=2, head_dk=3, head_dv=4, use_decay=use_decay,
+                          fixed_lambda=fixed_lambda).double()
     h = torch.randn(2, 5, 6, dtype=torch.float64, requires_grad=True)
     params = list(m.parameters())
 
@@ -90,3 +91,17 @@ def test_layer_has_no_cpu_path():
     m = layer.QDeltaLayer(d_model=8, n_heads=2, head_dk=64, head_dv=64)
     with pytest.raises((ValueError, OSError, RuntimeError)):
         m(torch.randn(1, 4, 8))
+
+
+def test_fixed_lambda_variants():
+    """The paper's ablations as layer settings: a constant lambda is passed as
+    a filled tensor, lambda = 0 as NULL (the gated delta rule), and no decay
+    as a NULL log alpha; the gate projection has one block per learned gate."""
+    h = torch.randn(1, 3, 8)
+    m = layer.QDeltaLayer(d_model=8, n_heads=2, head_dk=4, head_dv=4, fixed_lambda=0.8)
+    beta, lam, la = m.gates(h)
+    assert torch.equal(lam, torch.full_like(beta, 0.8)) and la is not None
+    assert m.w_gates.out_features == 4 and not hasattr(m, "lambda_bias")
+    m0 = layer.QDeltaLayer(d_model=8, n_heads=2, head_dk=4, head_dv=4, fixed_lambda=0, use_decay=False)
+    beta, lam, la = m0.gates(h)
+    assert lam is None and la is None and m0.w_gates.out_features == 2
