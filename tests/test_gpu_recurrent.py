@@ -62,3 +62,19 @@ def test_recurrent_fwd_empty_sequences_pass_state_through():
     o, Sf = rec_fwd(d)
     assert o.shape == (2, 0, 2, 64)
     assert torch.equal(Sf.cpu(), d["initial_state"])
+
+
+def test_recurrent_fwd_at_training_shape():
+    """B=4, T=4096, H=16, d=128, bf16, decay on, carried state: the
+    recurrent forward equals the oracle on sampled heads and the chunk
+    forward on every output."""
+    from tests.gpu_helpers import select_heads
+    d = synth.make(4, 4096, 16, 128, 128, "bf16", "G2", seed=145, s0=True)
+    o_r, S_r = rec_fwd(d)
+    o_c, S_c, _ = gpu_fwd(d)
+    assert normwise(f64(o_r.cpu()), f64(o_c.cpu())) <= TOL["bf16"]
+    assert normwise(f64(S_r.cpu()), f64(S_c.cpu())) <= TOL["bf16"]
+    heads = [0, 11]
+    ds = select_heads(d, heads)
+    errs = fwd_errors(ds, o_r[:, :, heads].contiguous(), S_r[:, heads].contiguous())
+    _check(errs, TOL["bf16"], "recurrent fwd at training shape (heads 0, 11)")
