@@ -6,11 +6,22 @@
 // Each state row S[v, :] is independent, so a row is owned by a group of
 // Dk/4 lanes (one float4 each): the state is read once and written once with
 // fully coalesced 16-byte accesses, and the two row dot products are reduced
-// with cross-lane shuffles.  The kernel is bound by HBM (or MALL) bandwidth.
+// with DPP lane moves (one shuffle across rows of 16).  The kernel is bound by
+// HBM (or MALL) bandwidth.
 #include "qd_common.h"
 #include "qd_launch.h"
 
 namespace qd {
+
+// Sum over each aligned group of L = 16 or 32 lanes: DPP within rows of 16
+// lanes, then one cross-row exchange for 32.
+template <int L>
+__device__ inline float row_sum(float x) {
+  static_assert(L == 16 || L == 32, "lane group of 16 or 32");
+  x = sum16(x);
+  if (L == 32) x += __shfl_xor(x, 16, 64);
+  return x;
+}
 
 // Each lane group owns RPT state rows RPB apart (RPB = rows per workgroup
 // pass), so a wave has RPT independent 16-byte loads in flight instead of
@@ -59,9 +70,7 @@ __global__ __launch_bounds__(NTHREADS) void k_step(int DV, int nrb, const E* __r
     for (int j = 0; j < 4; ++j) px[i] += s[i][j] * xv[j];
   }
 #pragma unroll
-  for (int off = LPR / 2; off >= 1; off >>= 1)
-#pragma unroll
-    for (int i = 0; i < RPT; ++i) px[i] += __shfl_xor(px[i], off, 64);
+  for (int i = 0; i < RPT; ++i) px[i] = row_sum<LPR>(px[i]);
   float oq[RPT];
 #pragma unroll
   for (int i = 0; i < RPT; ++i) {
@@ -76,9 +85,7 @@ __global__ __launch_bounds__(NTHREADS) void k_step(int DV, int nrb, const E* __r
     if (row < DV) *(f4*)(S + (u * DV + row) * DK + c0) = s[i];
   }
 #pragma unroll
-  for (int off = LPR / 2; off >= 1; off >>= 1)
-#pragma unroll
-    for (int i = 0; i < RPT; ++i) oq[i] += __shfl_xor(oq[i], off, 64);
+  for (int i = 0; i < RPT; ++i) oq[i] = row_sum<LPR>(oq[i]);
   if ((tid % LPR) == 0) {
 #pragma unroll
     for (int i = 0; i < RPT; ++i) {
@@ -113,7 +120,7 @@ hipError_t launch_step(int N, int H, int Dk, int Dv, int dtype, const void* q, c
 // token by token; the paper offers this form beside the chunkwise one).
 //
 // A state row is owned by a group of LPR = 8 lanes, each holding Dk/8
-// columns, so both per-token row dot products reduce in three shuffle steps;
+// columns, so both per-token row dot products reduce in three DPP steps;
 // the NT/8 lane groups of a workgroup hold RPT rows each in registers for
 // the whole sequence: the state is read once (initial state or zero) and
 // written once (final state).  Both row dot products use the state before
