@@ -57,3 +57,20 @@ def test_layer_matches_oracle_layer(monkeypatch, use_decay, varlen, fixed_lambda
         else:
             err = normwise(p.grad.cpu().double().numpy(), pr.grad.numpy())
         assert err <= tol, (name, err)
+
+
+def test_layer_continuation_with_carried_state():
+    """Running a sequence in two calls, the second from the first's final
+    state, equals one call over the whole sequence (output and final state)."""
+    torch.manual_seed(43)
+    m = layer.QDeltaLayer(d_model=256, n_heads=2, head_dk=128, head_dv=128).to(torch.bfloat16).cuda()
+    g = torch.Generator().manual_seed(44)
+    h = torch.randn(2, 200, 256, generator=g).to(torch.bfloat16).cuda()
+    with torch.no_grad():
+        y, S = m(h, output_final_state=True)
+        y1, S1 = m(h[:, :77].contiguous(), output_final_state=True)
+        y2, S2 = m(h[:, 77:].contiguous(), initial_state=S1, output_final_state=True)
+    torch.cuda.synchronize()
+    tol = TOL["bf16"]
+    assert normwise(torch.cat([y1, y2], 1).float().cpu().numpy(), y.float().cpu().numpy()) <= tol
+    assert normwise(S2.cpu().numpy(), S.cpu().numpy()) <= tol

@@ -78,3 +78,13 @@ def test_recurrent_fwd_at_training_shape():
     ds = select_heads(d, heads)
     errs = fwd_errors(ds, o_r[:, :, heads].contiguous(), S_r[:, heads].contiguous())
     _check(errs, TOL["bf16"], "recurrent fwd at training shape (heads 0, 11)")
+
+
+def test_recurrent_fwd_at_varlen_workload_size():
+    """The packed workload (32768 tokens, lognormal lengths up to 8192, H=32,
+    dk=128, dv=256, bf16): token by token equals chunkwise on every output."""
+    d = synth.make(1, 0, 32, 128, 256, "bf16", "G2", seed=146, varlen_tokens=32768)
+    o_r, S_r = rec_fwd(d)
+    o_c, S_c, _ = gpu_fwd(d)
+    assert normwise(f64(o_r.cpu()), f64(o_c.cpu())) <= TOL["bf16"]
+    assert normwise(f64(S_r.cpu()), f64(S_c.cpu())) <= TOL["bf16"]
