@@ -204,6 +204,22 @@ int qdelta_recurrent_fwd_varlen(int32_t T, int32_t N, const int32_t* cu_seqlens,
                                 const float* initial_state, void* o, float* final_state,
                                 hipStream_t stream);
 
+/* Row L2 normalisation for the layer's q and k (unit-norm keys are the
+ * condition of Sec. 3.4 Lemma 1): y = x / max(|x|, 1e-12) per row of D.
+ *   x        rows of D elements (dtype), row r at x + r * ld_x (ld_x >= D,
+ *            ld_x * element size a multiple of 16 bytes): strided views allowed
+ *   y        [rows, D] (dtype), contiguous
+ *   rnorm    [rows] fp32: 1 / max(|x|, 1e-12), negated for rows whose norm was
+ *            clamped; pass it to the backward unchanged
+ * Supported: D in {64, 128}, any dtype. */
+int qdelta_l2norm_fwd(int64_t rows, int32_t D, int64_t ld_x, int32_t dtype, const void* x, void* y,
+                      float* rnorm, hipStream_t stream);
+
+/* Backward of qdelta_l2norm_fwd: dx = r (dy - y (y . dy)) per row, r = |rnorm|
+ * (dx = r dy for a clamped row).  y, dy, dx [rows, D] contiguous (dtype). */
+int qdelta_l2norm_bwd(int64_t rows, int32_t D, int32_t dtype, const void* y, const float* rnorm,
+                      const void* dy, void* dx, hipStream_t stream);
+
 /* Measurement facility (benchmarks and profiling only; not thread-safe).
  * qdelta_profile_begin() starts recording a pair of HIP events around every
  * kernel launch of the library, on the launch stream, tagged by stage:

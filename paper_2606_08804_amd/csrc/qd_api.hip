@@ -427,6 +427,33 @@ int qdelta_recurrent_fwd_varlen(int32_t T, int32_t N, const int32_t* cu_seqlens,
                       log_alpha, initial_state, o, final_state, stream);
 }
 
+int qdelta_l2norm_fwd(int64_t rows, int32_t D, int64_t ld_x, int32_t dtype, const void* x, void* y,
+                      float* rnorm, hipStream_t stream) {
+  if (rows < 0 || ld_x < D) return QDELTA_EINVAL;
+  if (dtype != QDELTA_F32 && dtype != QDELTA_BF16) return QDELTA_EINVAL;
+  if (D != 64 && D != 128) return QDELTA_EUNSUPPORTED;
+  const int esz = dtype == QDELTA_BF16 ? 2 : 4;
+  if ((ld_x * esz) % 16 != 0) return QDELTA_EINVAL;
+  if (rows >= (int64_t(1) << 31)) return QDELTA_EUNSUPPORTED;
+  if (rows == 0) return QDELTA_OK;
+  if (!(ok_ptr(x) && ok_ptr(y) && ok_ptr(rnorm))) return QDELTA_EINVAL;
+  hipError_t e = qd::launch_l2norm(0, rows, D, ld_x, dtype, x, nullptr, nullptr, rnorm, nullptr, y,
+                                   stream);
+  return e == hipSuccess ? QDELTA_OK : QDELTA_EHIP;
+}
+
+int qdelta_l2norm_bwd(int64_t rows, int32_t D, int32_t dtype, const void* y, const float* rnorm,
+                      const void* dy, void* dx, hipStream_t stream) {
+  if (rows < 0) return QDELTA_EINVAL;
+  if (dtype != QDELTA_F32 && dtype != QDELTA_BF16) return QDELTA_EINVAL;
+  if (D != 64 && D != 128) return QDELTA_EUNSUPPORTED;
+  if (rows >= (int64_t(1) << 31)) return QDELTA_EUNSUPPORTED;
+  if (rows == 0) return QDELTA_OK;
+  if (!(ok_ptr(y) && ok_ptr(rnorm) && ok_ptr(dy) && ok_ptr(dx))) return QDELTA_EINVAL;
+  hipError_t e = qd::launch_l2norm(1, rows, D, D, dtype, nullptr, y, rnorm, nullptr, dy, dx, stream);
+  return e == hipSuccess ? QDELTA_OK : QDELTA_EHIP;
+}
+
 int qdelta_recurrent_step(int32_t N, int32_t H, int32_t Dk, int32_t Dv, int32_t dtype,
                           const void* q, const void* k, const void* v, const float* beta,
                           const float* lam, const float* log_alpha, float* state, void* o,

@@ -45,4 +45,10 @@ hipError_t launch_rec_fwd(int N, int T, const int* cu, int T_total, int H, int D
                           const float* beta, const float* lam, const float* la, const float* S0,
                           float* Sfin, void* o, hipStream_t st);
 
+// Row L2 normalisation (bwd == 0: x -> out, rn_out) or its backward
+// (bwd == 1: y, rn_in, dy -> out).
+hipError_t launch_l2norm(int bwd, long rows, int D, long ldx, int dtype, const void* x,
+                         const void* y, const float* rn_in, float* rn_out, const void* dy, void* out,
+                         hipStream_t st);
+
 }  // namespace qd

@@ -17,8 +17,8 @@ chunk forward and backward, and a module with the gate projections.
     paper's block appear only in its architecture figure (Fig. 1b) and are not
     part of this layer.
 
-The projections are ordinary library GEMMs; the recurrence is the library's
-kernels.  There is no CPU path: without the built library every call raises.
+The projections are ordinary library GEMMs; the q/k normalisation and the
+recurrence are the library's kernels.  There is no CPU path: without the built library every call raises.
 """
 import math
 
@@ -55,6 +55,22 @@ class QDeltaFunction(torch.autograd.Function):
                 g["d_initial_state"], None)
 
 
+class L2NormFunction(torch.autograd.Function):
+    """Row L2 normalisation over the last dim in one HIP pass each way
+    (strided rows read in place)."""
+
+    @staticmethod
+    def forward(ctx, x):
+        y, rn = _binding.l2norm_fwd(x)
+        ctx.save_for_backward(y, rn)
+        return y
+
+    @staticmethod
+    def backward(ctx, dy):
+        y, rn = ctx.saved_tensors
+        return _binding.l2norm_bwd(y, rn, dy.contiguous())
+
+
 def qdelta_chunk(q, k, v, beta, lam=None, log_alpha=None, initial_state=None, cu_seqlens=None):
     """Differentiable chunkwise Q-Delta.  Layouts as the C ABI: q, k [B,T,H,Dk],
     v [B,T,H,Dv] (bf16 or fp32), gates [B,T,H] fp32, states [N,H,Dv,Dk] fp32."""
@@ -65,8 +81,8 @@ class QDeltaLayer(torch.nn.Module):
     """Token mixer of a Q-Delta block: projections, gates, recurrence, output.
 
     Parameters live in the module's dtype (``.to(torch.bfloat16)`` runs the
-    recurrence on bf16 activations); gates and L2 norms are formed in fp32
-    (or wider)."""
+    recurrence on bf16 activations); gates are formed in fp32 (or wider), the
+    q and k L2 norms by the library's row-normalisation kernels."""
 
     def __init__(self, d_model, n_heads, head_dk=128, head_dv=128, use_decay=True, qk_norm=True,
                  lambda_bias=-0.8, fixed_lambda=None):
@@ -115,9 +131,8 @@ class QDeltaLayer(torch.nn.Module):
         qkv = self.w_qkv(h).view(B, T, H, 2 * dk + dv)
         q, k, v = qkv.split([dk, dk, dv], dim=-1)
         if self.qk_norm:
-            acc = torch.promote_types(h.dtype, torch.float32)
-            q = F.normalize(q.to(acc), dim=-1).to(h.dtype)
-            k = F.normalize(k.to(acc), dim=-1).to(h.dtype)
+            q = L2NormFunction.apply(q)
+            k = L2NormFunction.apply(k)
         beta, lam, log_alpha = self.gates(h)
         o, final_state = qdelta_chunk(q.contiguous(), k.contiguous(), v.contiguous(),
                                       beta.contiguous(), None if lam is None else lam.contiguous(),

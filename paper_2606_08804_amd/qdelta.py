@@ -14,6 +14,7 @@ chunk_bwd(q, k, v, beta, lam, log_alpha, initial_state, saved_states, d_o,
 recurrent_step(q, k, v, beta, lam, log_alpha, state) -> o        (state updated in place)
 recurrent_fwd(q, k, v, beta, lam=None, log_alpha=None, initial_state=None, cu_seqlens=None)
           -> (o, final_state)                                  (token by token, one launch)
+l2norm_fwd(x) -> (y, rnorm);  l2norm_bwd(y, rnorm, dy) -> dx   (row L2 norm for the layer's q, k)
 
 lam=None means lambda == 0 (the gated delta rule); log_alpha=None means alpha == 1.
 """
@@ -33,7 +34,7 @@ EXPORTS = (
     "qdelta_status_string", "qdelta_version", "qdelta_saved_state_slots", "qdelta_saved_bytes",
     "qdelta_chunk_workspace_bytes", "qdelta_chunk_fwd", "qdelta_chunk_fwd_varlen",
     "qdelta_chunk_bwd", "qdelta_chunk_bwd_varlen", "qdelta_recurrent_step",
-    "qdelta_recurrent_fwd", "qdelta_recurrent_fwd_varlen",
+    "qdelta_recurrent_fwd", "qdelta_recurrent_fwd_varlen", "qdelta_l2norm_fwd", "qdelta_l2norm_bwd",
     "qdelta_profile_begin", "qdelta_profile_end",
 )
 
@@ -81,6 +82,11 @@ def lib():
         L.qdelta_recurrent_fwd.restype = ctypes.c_int
         L.qdelta_recurrent_fwd_varlen.argtypes = [i32, i32, P] + [i32] * 4 + [P] * 9 + [P]
         L.qdelta_recurrent_fwd_varlen.restype = ctypes.c_int
+        i64 = ctypes.c_int64
+        L.qdelta_l2norm_fwd.argtypes = [i64, i32, i64, i32, P, P, P, P]
+        L.qdelta_l2norm_fwd.restype = ctypes.c_int
+        L.qdelta_l2norm_bwd.argtypes = [i64, i32, i32, P, P, P, P, P]
+        L.qdelta_l2norm_bwd.restype = ctypes.c_int
         L.qdelta_profile_begin.argtypes = []
         L.qdelta_profile_begin.restype = ctypes.c_int
         L.qdelta_profile_end.argtypes = [P, P]
@@ -296,6 +302,38 @@ def recurrent_fwd(q, k, v, beta, lam=None, log_alpha=None, initial_state=None, c
         _check("qdelta_recurrent_fwd_varlen",
                L.qdelta_recurrent_fwd_varlen(T, N, _p(cu_seqlens), *common))
     return o, Sf
+
+
+def l2norm_fwd(x):
+    """Row L2 normalisation over the last dim of x (rows may be strided, as in a
+    slice of a fused projection).  Returns (y contiguous, rnorm [rows] fp32)."""
+    D = x.shape[-1]
+    if not x.is_cuda:
+        raise ValueError("x must be a device tensor")
+    ld = x.stride(-2) if x.dim() >= 2 else D
+    expected = ld
+    for i in range(x.dim() - 3, -1, -1):    # leading dims must collapse into one row index
+        expected *= x.shape[i + 1]
+        if x.shape[i] > 1 and x.stride(i) != expected:
+            raise ValueError("x must have evenly strided rows")
+    if x.stride(-1) != 1:
+        raise ValueError("x must have unit stride in its last dim")
+    y = torch.empty(x.shape, dtype=x.dtype, device=x.device)
+    rn = torch.empty(x.shape[:-1], dtype=torch.float32, device=x.device)
+    _check("qdelta_l2norm_fwd", lib().qdelta_l2norm_fwd(x.numel() // D, D, ld, _dt(x), _p(x), _p(y),
+                                                        _p(rn), _stream()))
+    return y, rn
+
+
+def l2norm_bwd(y, rn, dy):
+    """dx for l2norm_fwd (contiguous, shaped like y)."""
+    _need(y, "y", y.dtype)
+    _need(dy, "dy", y.dtype, tuple(y.shape))
+    _need(rn, "rnorm", torch.float32, tuple(y.shape[:-1]))
+    dx = torch.empty_like(y)
+    _check("qdelta_l2norm_bwd", lib().qdelta_l2norm_bwd(y.numel() // y.shape[-1], y.shape[-1], _dt(y),
+                                                        _p(y), _p(rn), _p(dy), _p(dx), _stream()))
+    return dx
 
 
 def profile_begin():

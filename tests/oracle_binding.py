@@ -1,5 +1,5 @@
 """A stand-in for the library binding's chunk_fwd / chunk_bwd, computed by the
-fp64 oracle on the CPU, for tests of the autograd layer: its gradient wiring
+fp64 oracle on the CPU (and its row normalisation, from its definition), for tests of the autograd layer: its gradient wiring
 on the CPU, and the reference that the GPU layer is compared with.
 
 Same call signatures as ``paper_2606_08804_amd.qdelta``; results come back as
@@ -55,3 +55,17 @@ def chunk_bwd(q, k, v, beta, lam, log_alpha, initial_state, saved_states, d_o,
         a = g[key][None] if (cu is not None and key != "d_initial_state") else g[key]
         out[key] = torch.from_numpy(np.ascontiguousarray(a)).to(ref.dtype)
     return out
+
+
+def l2norm_fwd(x):
+    """The row normalisation's definition (same clamp and rnorm convention)."""
+    n = x.norm(dim=-1)
+    clamped = ~(n > 1e-12)
+    r = 1.0 / torch.where(clamped, torch.full_like(n, 1e-12), n)
+    return x * r[..., None], torch.where(clamped, -r, r)
+
+
+def l2norm_bwd(y, rn, dy):
+    r = rn.abs()[..., None]
+    proj = torch.where(rn > 0, (y * dy).sum(-1), torch.zeros_like(rn))[..., None]
+    return r * (dy - y * proj)

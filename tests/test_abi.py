@@ -16,13 +16,13 @@ HEADER = os.path.join(ROOT, "include", "qdelta.h")
 def header_functions():
     text = open(HEADER).read()
     text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
-    return sorted(set(re.findall(r"\b(qdelta_[a-z_]+)\s*\(", text)))
+    return sorted(set(re.findall(r"\b(qdelta_[a-z0-9_]+)\s*\(", text)))
 
 
 def test_library_exports_every_declared_symbol():
     L = qdelta.lib()
     names = header_functions()
-    assert len(names) == 14
+    assert len(names) == 16
     for n in names:
         assert hasattr(L, n), n
     assert sorted(names) == sorted(qdelta.EXPORTS)
@@ -154,6 +154,20 @@ def test_recurrent_fwd_rejects_bad_arguments():
     assert L.qdelta_recurrent_fwd(0, 8, 1, 64, 64, 1, *([None] * 10)) == E.QDELTA_OK
     assert L.qdelta_recurrent_fwd_varlen(0, 0, f, 1, 64, 64, 1, *([None] * 10)) == E.QDELTA_OK
     assert L.qdelta_recurrent_fwd_varlen(8, 1, None, 1, 64, 64, 1, *args) == E.QDELTA_EINVAL
+
+
+def test_l2norm_rejects_bad_arguments():
+    L = qdelta.lib()
+    E = qdelta
+    f = FAKE
+    assert L.qdelta_l2norm_fwd(4, 96, 96, 1, f, f, f, None) == E.QDELTA_EUNSUPPORTED
+    assert L.qdelta_l2norm_fwd(4, 128, 100, 1, f, f, f, None) == E.QDELTA_EINVAL    # ld below D
+    assert L.qdelta_l2norm_fwd(4, 128, 132, 1, f, f, f, None) == E.QDELTA_EINVAL    # 264-byte rows
+    assert L.qdelta_l2norm_fwd(4, 128, 128, 1, f + 2, f, f, None) == E.QDELTA_EINVAL
+    assert L.qdelta_l2norm_fwd(-1, 128, 128, 1, f, f, f, None) == E.QDELTA_EINVAL
+    assert L.qdelta_l2norm_fwd(0, 128, 128, 1, None, None, None, None) == E.QDELTA_OK
+    assert L.qdelta_l2norm_bwd(4, 128, 1, f, f, None, f, None) == E.QDELTA_EINVAL
+    assert L.qdelta_l2norm_bwd(0, 128, 1, None, None, None, None, None) == E.QDELTA_OK
 
 
 def test_binding_validates_before_calling_library():

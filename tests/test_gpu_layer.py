@@ -74,3 +74,28 @@ def test_layer_continuation_with_carried_state():
     tol = TOL["bf16"]
     assert normwise(torch.cat([y1, y2], 1).float().cpu().numpy(), y.float().cpu().numpy()) <= tol
     assert normwise(S2.cpu().numpy(), S.cpu().numpy()) <= tol
+
+
+@pytest.mark.parametrize("dt,D", [(torch.bfloat16, 128), (torch.bfloat16, 64), (torch.float32, 128),
+                                  (torch.float32, 64)])
+def test_l2norm_kernels_match_normalize(dt, D):
+    """Row normalisation of a strided slice of a fused projection (1001 rows,
+    one of them zero, so clamped) against F.normalize and its gradient in fp64."""
+    from paper_2606_08804_amd import qdelta
+    g = torch.Generator().manual_seed(45)
+    fused = torch.randn(7, 11, 13, 2 * D + 64, generator=g)
+    fused[3, 4, 5] = 0.0
+    fused = fused.to(dt)
+    dy = torch.randn(7, 11, 13, D, generator=g).to(dt)
+    x_cpu = fused[..., D:2 * D]                         # the k slice: strided rows
+    xr = x_cpu.double().requires_grad_()
+    yr = torch.nn.functional.normalize(xr, dim=-1, eps=1e-12)
+    yr.backward(dy.double())
+    x = fused.cuda()[..., D:2 * D]
+    y, rn = qdelta.l2norm_fwd(x)
+    dx = qdelta.l2norm_bwd(y, rn, dy.cuda())
+    torch.cuda.synchronize()
+    tol = TOL["bf16"] if dt == torch.bfloat16 else TOL["f32"]
+    assert normwise(y.double().cpu().numpy(), yr.detach().numpy()) <= tol
+    assert normwise(dx.double().cpu().numpy(), xr.grad.numpy()) <= tol
+    assert float(rn[3, 4, 5]) < 0 and torch.all(y[3, 4, 5] == 0)
