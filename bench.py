@@ -16,11 +16,21 @@ a step of the benchmark is all 1024 of them), ``varlen`` (packed 32768 tokens,
 lognormal lengths, H=32 d_k=128 d_v=256, forward + backward) and ``tiny``
 (fp32 forward, B=1 T=256 H=2 d=64).
 
-`roofline` describes the kernel with the largest share of the step time; its
-duration is measured live with HIP events recorded around each of its
-launches on the launch stream.  `kernels` gives the same figures for every
-kernel of the step.  `cpu_baseline` times the fp64 CPU oracle on a bounded
-sample of the same workload on this host's cores.
+Timing: untimed steps for --settle-ms (GPU clock ramp-up), W warm-up steps,
+then exactly K steps between two synchronisations with nothing else
+recorded (`ms_per_step`, `value`); then K more steps with the library's HIP
+events around every kernel launch on the launch stream, which give each
+kernel's average launch duration.
+
+Bytes: `step_alg_bytes` and every `alg_bytes_per_launch` count only the
+mandated streams (inputs read once, outputs written once, per-chunk entry
+states priced as fp32 through HBM; hand-offs between kernels excluded): 4900 B
+per token-head for the training step at d = 128.  `roofline` is the kernel
+with the largest share of the step; `traffic` is its HBM bytes per launch from
+the committed FETCH_SIZE/WRITE_SIZE counter summary (null once the kernel
+sources changed since it was taken).  `cpu_baseline` times the fp64 CPU oracle
+on a bounded sample of the same workload on this host's cores; `parity`
+compares the GPU outputs of the last timed step with that oracle run.
 """
 import argparse
 import hashlib
@@ -56,11 +66,61 @@ def bwd_flops_per_token_head(Dk, Dv):
     return 2.5 * fwd_flops_per_token_head(Dk, Dv)
 
 
-def stage_bytes_per_unit(stage, Dk, Dv, e, saved=True):
-    """Bytes one (chunk, head) unit of a kernel stage must move: every tensor
-    it consumes or produces, counted once (activations e bytes, gates and
-    states 4 bytes, workspace hand-offs in their stored precision).  `saved`
-    says whether the forward keeps the context for a backward."""
+def alg_bytes_per_token_head(Dk, Dv, e, with_bwd, saved=True):
+    """Algorithmic HBM bytes per token-head of a whole step: only the mandated
+    streams, each counted once -- inputs read once, outputs written once, and
+    the per-chunk entry states priced as fp32 going through HBM (written by the
+    forward, read by the backward).  Hand-offs between kernels (the chunk
+    factors T, P, M, the new values D, the exit-state gradients) are not
+    algorithmic.  At Dk = Dv = 128 in bf16 this is 2060 B forward and
+    2840 B backward, 4900 B per token-head in all."""
+    qkv = (2 * Dk + Dv) * e
+    gates = 3 * 4
+    states = Dv * Dk * 4 / C
+    fwd = qkv + gates + Dv * e + (states if saved else 0)
+    if not with_bwd:
+        return fwd
+    bwd = qkv + Dv * e + gates + states + (2 * Dk + Dv) * e + gates
+    return fwd + bwd
+
+
+def kernel_alg_bytes_per_token_head(stage, Dk, Dv, e, saved=True):
+    """The algorithmic streams of the per-step count that one kernel reads or
+    writes itself (a stream that several kernels read counts for each of
+    them; the gate block the preparation writes stands for the gates).
+    Hand-offs are excluded as in alg_bytes_per_token_head."""
+    qk = 2 * Dk * e
+    v = Dv * e
+    gates = 3 * 4
+    states = Dv * Dk * 4 / C
+    if stage in ("prep_fwd", "prep_bwd"):   # q, k, gates
+        return qk + gates
+    if stage == "scan_fwd":                 # q, k, v, gates -> o, entry states
+        return qk + v + gates + v + (states if saved else 0)
+    if stage == "scan_bwd":                 # q, k, dO, gates -> dv
+        return qk + v + gates + v
+    if stage == "intra":                    # q, k, v, dO, gates, entry states -> dq, dk, dgates
+        return qk + 2 * v + gates + states + qk + gates
+    raise KeyError(stage)
+
+
+def kernel_state_io_bytes_per_seq(stage, Dk, Dv, has_s0):
+    """Per (sequence, head) fp32 states a kernel moves once: the forward scan
+    reads the initial state (when there is one) and writes the final state;
+    the backward scan writes the initial-state gradient (the benchmark
+    passes no final-state gradient)."""
+    st = Dv * Dk * 4
+    if stage == "scan_fwd":
+        return (2 if has_s0 else 1) * st
+    if stage == "scan_bwd":
+        return st
+    return 0
+
+
+def handoff_bytes_per_unit(stage, Dk, Dv, e, saved=True):
+    """Every byte a kernel moves per (chunk, head) unit, hand-offs included
+    (activations e bytes, gates and states 4 bytes, hand-offs in their stored
+    precision): the figure to compare with counter traffic."""
     act_qk = C * Dk * e
     act_v = C * Dv * e
     gates = C * 4
@@ -80,19 +140,6 @@ def stage_bytes_per_unit(stage, Dk, Dv, e, saved=True):
         #                          -> dq, dk, dbeta, dlam, dlog_alpha
         return 3 * gates + 2 * state * e // 4 + 4 * act_v + 2 * act_qk + cc_e + 2 * act_qk + 3 * gates
     raise KeyError(stage)
-
-
-def stage_bytes_per_seq(stage, Dk, Dv, has_s0):
-    """Per (sequence, head) bytes a stage moves once: the fp32 initial state
-    read (when there is one) and the final state written by the forward scan;
-    the initial-state gradient written by the backward scan (the benchmark
-    passes no final-state gradient)."""
-    st = Dv * Dk * 4
-    if stage == "scan_fwd":
-        return (2 if has_s0 else 1) * st
-    if stage == "scan_bwd":
-        return st
-    return 0
 
 
 # Sources that build the chunk kernels the stored counters were taken on (the
@@ -125,11 +172,31 @@ def stored_traffic(stage):
     return None if s is None else s.get("hbm_bytes_per_launch")
 
 
+def host_info():
+    """CPU count, the CPUs this process may run on, and the CPU model."""
+    try:
+        aff = len(os.sched_getaffinity(0))
+    except AttributeError:  # pragma: no cover
+        aff = os.cpu_count()
+    model = None
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    return {"nproc": os.cpu_count(), "affinity_cpus": aff, "cpu_model": model}
+
+
 def cpu_baseline(d, heads, with_bwd, tokens_per_unit_run, min_seconds=10.0):
     """Time the fp64 oracle (forward, plus the BPTT backward when `with_bwd`)
     on the (sequence, head) units of `heads` over the full sequences, repeated
     until about `min_seconds` have been timed; scaled to tokens/s of the
-    whole workload (every (sequence, head) unit costs the same per token)."""
+    whole workload (every (sequence, head) unit costs the same per token).
+    Also returns the oracle's outputs of the last pass, against which the
+    benchmark checks the GPU's timed result."""
     from oracle import build as obuild
     from oracle import recurrent
     obuild.build(force=False)
@@ -142,12 +209,15 @@ def cpu_baseline(d, heads, with_bwd, tokens_per_unit_run, min_seconds=10.0):
     S0 = None if d["initial_state"] is None else f(d["initial_state"][:, heads].contiguous())
     dO = pk(f(sl(d["d_o"]))) if with_bwd else None
     cu = None if d["cu_seqlens"] is None else d["cu_seqlens"].numpy()
+    # the oracle's own thread count: one per CPU of this process, at most 16
+    # (the host share of one GPU on the measurement machines)
     threads = recurrent.default_threads()
     reps, t0 = 0, time.perf_counter()
     while True:
-        recurrent.fwd(q, k, v, beta, lam, la, S0, cu_seqlens=cu, nthreads=threads)
+        o_ref, S_ref = recurrent.fwd(q, k, v, beta, lam, la, S0, cu_seqlens=cu, nthreads=threads)
+        g_ref = None
         if with_bwd:
-            recurrent.bwd(q, k, v, beta, lam, la, S0, d_o=dO, cu_seqlens=cu, nthreads=threads)
+            g_ref = recurrent.bwd(q, k, v, beta, lam, la, S0, d_o=dO, cu_seqlens=cu, nthreads=threads)
         reps += 1
         total = time.perf_counter() - t0
         if total >= min_seconds or reps >= 30:
@@ -156,9 +226,47 @@ def cpu_baseline(d, heads, with_bwd, tokens_per_unit_run, min_seconds=10.0):
     frac = len(heads) / H
     tokens_per_s = tokens_per_unit_run / (dt / frac)
     what = "forward + BPTT backward" if with_bwd else "forward"
-    return {"value": tokens_per_s, "unit": "tokens/s", "cores": threads, "kind": "oracle",
-            "sample": f"fp64 recurrence {what} of {len(heads)} of {H} heads (all sequences, all tokens), "
-                      f"{reps} passes in {total:.1f} s ({dt:.2f} s each), scaled to all heads"}
+    out = {"value": tokens_per_s, "unit": "tokens/s", "cores": threads, "kind": "oracle",
+           "sample": f"fp64 recurrence {what} of {len(heads)} of {H} heads (all sequences, all tokens), "
+                     f"{reps} passes in {total:.1f} s ({dt:.2f} s each), scaled to all heads",
+           "threads_note": "one oracle thread per CPU available to this process, capped at 16 "
+                           "(the host CPU share of one GPU)"}
+    out.update(host_info())
+    return out, {"o": o_ref, "final_state": S_ref, "grads": g_ref}
+
+
+def normwise(got, ref):
+    """max|got - ref| / max|ref| (absolute when the reference is all zero)."""
+    got = np.asarray(got, dtype=np.float64)
+    ref = np.asarray(ref, dtype=np.float64)
+    scale = np.abs(ref).max() if ref.size else 0.0
+    err = np.abs(got - ref).max() if ref.size else 0.0
+    return float(err / scale if scale > 0 else err)
+
+
+def same_run_parity(d, heads, ref, got, dtype):
+    """Compares the GPU outputs of the last timed step, restricted to `heads`,
+    with the oracle outputs of the CPU baseline's last pass (normwise max
+    error per tensor, the tolerance of the activation dtype)."""
+    f = synth.to_f64
+    packed = d["cu_seqlens"] is not None
+    tol = 2e-2 if dtype == "bf16" else 1e-4
+
+    def act(x):       # [B, T, H, ...] device tensor -> sampled heads as fp64
+        x = x[:, :, heads].cpu()
+        return f(x[0] if packed else x)
+
+    errs = {"o": normwise(act(got["o"]), ref["o"]),
+            "final_state": normwise(f(got["final_state"][:, heads].cpu()), ref["final_state"])}
+    if ref["grads"] is not None:
+        g = got["grads"]
+        for key in ("dq", "dk", "dv", "dbeta", "dlam", "dlog_alpha"):
+            if g.get(key) is not None:
+                errs[key] = normwise(act(g[key]), ref["grads"][key])
+        errs["d_initial_state"] = normwise(f(g["d_initial_state"][:, heads].cpu()),
+                                           ref["grads"]["d_initial_state"])
+    return {"heads": list(heads), "tolerance": tol, "max_err": max(errs.values()),
+            "ok": all(v <= tol for v in errs.values()), "errors": errs}
 
 
 def chunk_units(d, H):
@@ -169,20 +277,32 @@ def chunk_units(d, H):
     return sum((L + C - 1) // C for L in d["lengths"]) * H
 
 
+def token_heads(d):
+    return d["q"].shape[0] * d["q"].shape[1] * d["q"].shape[2]
+
+
 def kernel_rooflines(stages, d, Dk, Dv, e, saved):
-    """Per kernel: average launch duration (HIP events) and the HBM roofline
-    of its algorithmic bytes."""
+    """Per kernel: average launch duration (HIP events on the launch stream)
+    and the HBM roofline of its algorithmic bytes (the mandated streams it
+    touches, states priced as fp32); the hand-off-inclusive byte count is
+    given beside it."""
     H = d["q"].shape[2]
     units = chunk_units(d, H)
+    th = token_heads(d)
     nseq = (d["q"].shape[0] if d["cu_seqlens"] is None else len(d["lengths"])) * H
+    has_s0 = d["initial_state"] is not None
     out = {}
     for s, (tot_ms, launches) in stages.items():
         if not launches:
             continue
         avg_s = tot_ms / launches / 1e3
-        b = stage_bytes_per_unit(s, Dk, Dv, e, saved) * units + stage_bytes_per_seq(s, Dk, Dv, d["initial_state"] is not None) * nseq
-        out[s] = {"avg_launch_us": avg_s * 1e6, "alg_bytes_per_launch": b,
-                  "achieved_GBps": b / avg_s / 1e9, "frac": b / avg_s / HBM_PEAK}
+        b = (kernel_alg_bytes_per_token_head(s, Dk, Dv, e, saved) * th
+             + kernel_state_io_bytes_per_seq(s, Dk, Dv, has_s0) * nseq)
+        bh = handoff_bytes_per_unit(s, Dk, Dv, e, saved) * units + kernel_state_io_bytes_per_seq(s, Dk, Dv, has_s0) * nseq
+        out[s] = {"avg_launch_us": avg_s * 1e6, "alg_bytes_per_launch": int(b),
+                  "achieved_GBps": b / avg_s / 1e9, "frac": b / avg_s / HBM_PEAK,
+                  "bytes_incl_handoffs_per_launch": int(bh),
+                  "GBps_incl_handoffs": bh / avg_s / 1e9}
     return out
 
 
@@ -193,20 +313,43 @@ def roofline_of(kern, dom, traffic):
             "alg_bytes_per_launch": k["alg_bytes_per_launch"], "avg_launch_us": k["avg_launch_us"]}
 
 
-def timed(step, steps, warmup):
+def settle(step, min_ms):
+    """Untimed steps until `min_ms` of wall time have passed: the GPU's clocks
+    ramp up over the first milliseconds of sustained work."""
+    if min_ms <= 0:
+        return 0
+    n, t0 = 0, time.perf_counter()
+    while True:
+        step()
+        n += 1
+        if n % 4 == 0:
+            torch.cuda.synchronize()
+            if (time.perf_counter() - t0) * 1e3 >= min_ms:
+                return n
+
+
+def timed(step, steps, warmup, settle_ms):
+    """Headline timing: W warm-up steps, then exactly K steps between two
+    synchronisations, timed with events on the launch stream and no other
+    instrumentation.  Then K more steps with the library's HIP events around
+    every kernel launch, for the per-kernel durations."""
+    n_settle = settle(step, settle_ms)
     for _ in range(warmup):
         step()
     torch.cuda.synchronize()
-    qdelta.profile_begin()
     start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
     start.record()
     for _ in range(steps):
         step()
     end.record()
     torch.cuda.synchronize()
+    ms = start.elapsed_time(end) / steps
+    qdelta.profile_begin()
+    for _ in range(steps):
+        step()
+    torch.cuda.synchronize()
     stages = qdelta.profile_end()
-    return start.elapsed_time(end) / steps, stages
+    return ms, stages, n_settle
 
 
 def run_chunk(args, wid, with_bwd):
@@ -224,23 +367,33 @@ def run_chunk(args, wid, with_bwd):
     wsb = torch.empty(max(1, qdelta.workspace_bytes(B, T, H, Dk, Dv, dt, n_seqs, True)), dtype=torch.uint8,
                       device="cuda")
     args_in = (dev["q"], dev["k"], dev["v"], dev["beta"], dev["lam"], dev["log_alpha"], dev["initial_state"])
+    last = {}
 
     if with_bwd:
         def step():
             o, Sf, saved = qdelta.chunk_fwd(*args_in, cu_seqlens=cu, save_states=True, workspace=wsf)
-            qdelta.chunk_bwd(*args_in, saved, dev["d_o"], cu_seqlens=cu, workspace=wsb)
+            g = qdelta.chunk_bwd(*args_in, saved, dev["d_o"], cu_seqlens=cu, workspace=wsb)
+            last.update(o=o, final_state=Sf, grads=g)
     else:
         def step():
-            qdelta.chunk_fwd(*args_in, cu_seqlens=cu, save_states=False, workspace=wsf)
+            o, Sf, _ = qdelta.chunk_fwd(*args_in, cu_seqlens=cu, save_states=False, workspace=wsf)
+            last.update(o=o, final_state=Sf)
 
-    ms, stages = timed(step, args.steps, args.warmup)
+    ms, stages, n_settle = timed(step, args.steps, args.warmup, args.settle_ms)
     tokens = B * T
+    th = tokens * H
     value = tokens / (ms / 1e3)
     kern = kernel_rooflines(stages, d, Dk, Dv, e, with_bwd)
     dom = max(kern, key=lambda s: kern[s]["avg_launch_us"])
     traffic = stored_traffic(dom) if wid == 3 else None
     fl = fwd_flops_per_token_head(Dk, Dv) + (bwd_flops_per_token_head(Dk, Dv) if with_bwd else 0)
     peak = MFMA_BF16_PEAK if w.dtype == "bf16" else MFMA_F32_PEAK
+    nseq = (B if n_seqs == 0 else n_seqs) * H
+    has_s0 = d["initial_state"] is not None
+    state_io = sum(kernel_state_io_bytes_per_seq(s, Dk, Dv, has_s0) for s in ("scan_fwd", "scan_bwd")
+                   if with_bwd or s == "scan_fwd") * nseq
+    bpth = alg_bytes_per_token_head(Dk, Dv, e, with_bwd, saved=with_bwd)
+    step_bytes = bpth * th + state_io
     what = "fwd+bwd" if with_bwd else "fwd"
     shape = (f"T={T},H={H},d={Dk},bf16" if wid == 3 else
              f"{w.name.split(' ', 1)[1]}")
@@ -250,11 +403,22 @@ def run_chunk(args, wid, with_bwd):
            "gate_mode": args.gate, "parallelism": "single GPU"}
     if n_seqs:
         cfg["n_seqs"] = n_seqs
+    step_traffic = None
+    if wid == 3:
+        per = [stored_traffic(s) for s in kern]
+        if all(x is not None for x in per):
+            step_traffic = int(sum(x * stages[s][1] / args.steps for x, s in zip(per, kern)))
     out = {
         "metric": metric, "value": value, "unit": "tokens/s", "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": ms, "higher_is_better": True, "scaling": "weak",
         "vs_baseline": None, "dtype": w.dtype, "data": "synthetic", "config": cfg,
-        "mfma_frac_step": tokens * H * fl / (ms / 1e3) / peak,
+        "clock_settle_steps": n_settle,
+        "mfma_frac_step": th * fl / (ms / 1e3) / peak,
+        "step_alg_bytes": {"per_token_head": bpth, "state_io": state_io, "total": int(step_bytes),
+                           "GBps": step_bytes / (ms / 1e3) / 1e9,
+                           "hbm_frac": step_bytes / (ms / 1e3) / HBM_PEAK,
+                           "counter_traffic": step_traffic,
+                           "traffic_over_alg": None if step_traffic is None else step_traffic / step_bytes},
         "kernel_avg_us": {s: round(k["avg_launch_us"], 2) for s, k in kern.items()},
         "kernels": kern,
         "roofline": roofline_of(kern, dom, traffic),
@@ -264,7 +428,9 @@ def run_chunk(args, wid, with_bwd):
         if wid == 5:
             nh = 2
         heads = list(range(nh))
-        out["cpu_baseline"] = cpu_baseline(d, heads, with_bwd, tokens)
+        cb, ref = cpu_baseline(d, heads, with_bwd, tokens)
+        out["cpu_baseline"] = cb
+        out["parity"] = same_run_parity(d, heads, ref, last, w.dtype)
     return out
 
 
@@ -285,7 +451,7 @@ def run_layer(args):
         h.grad = None
         m(h).backward(dy)
 
-    ms, stages = timed(step, args.steps, args.warmup)
+    ms, stages, n_settle = timed(step, args.steps, args.warmup, args.settle_ms)
     tokens = B * T
     dd = {"q": torch.empty(B, T, H, 0), "cu_seqlens": None, "initial_state": None}
     kern = kernel_rooflines(stages, dd, d, d, 2, True)
@@ -300,6 +466,7 @@ def run_layer(args):
         "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
         "config": {"workload": f"layer bf16 B={B} T={T} d_model={D} H={H} d={d} (decay on)",
                    "parallelism": "single GPU"},
+        "clock_settle_steps": n_settle,
         "qdelta_kernels_ms_per_step": core_ms,
         "other_ms_per_step": ms - core_ms,
         "projection_gemm_tflops_per_step": gemm_flops / 1e12,
@@ -324,9 +491,9 @@ def run_recurrent(args):
         ins = (g["q"], g["k"], g["v"], g["beta"], g["lam"], g["log_alpha"], g["initial_state"])
         wsf = torch.empty(max(1, qdelta.workspace_bytes(B, T, H, d, d, qdelta.QDELTA_BF16, 0, False)),
                           dtype=torch.uint8, device="cuda")
-        ms, stages = timed(lambda: qdelta.recurrent_fwd(*ins), args.steps, args.warmup)
-        ms_chunk, _ = timed(lambda: qdelta.chunk_fwd(*ins, save_states=False, workspace=wsf),
-                            args.steps, args.warmup)
+        ms, stages, _ = timed(lambda: qdelta.recurrent_fwd(*ins), args.steps, args.warmup, args.settle_ms)
+        ms_chunk, _, _ = timed(lambda: qdelta.chunk_fwd(*ins, save_states=False, workspace=wsf),
+                               args.steps, args.warmup, 0)
         by_T[T] = {"recurrent_ms": ms, "chunk_ms": ms_chunk}
         if T == T_main:
             tot, launches = stages["rec_fwd"]
@@ -374,7 +541,7 @@ def run_decode(args):
                                   out=outs[s])
 
     # a benchmark step here is 1024 launches (tens of milliseconds)
-    ms, stages = timed(step, min(args.steps, 10), min(args.warmup, 3))
+    ms, stages, n_settle = timed(step, min(args.steps, 10), min(args.warmup, 3), args.settle_ms)
     tokens = N * steps_dec
     tot_ms, launches = stages["step"]
     avg_s = tot_ms / launches / 1e3
@@ -389,6 +556,7 @@ def run_decode(args):
         "config": {"workload": "decode 64 seqs x 1024 steps H16 d128", "N": N, "H": H, "Dk": D, "Dv": D,
                    "decode_steps": steps_dec, "gate_mode": args.gate, "parallelism": "single GPU",
                    "note": "a benchmark step is all 1024 decode steps (one launch each) plus one state reset copy"},
+        "clock_settle_steps": n_settle,
         "us_per_decode_step": ms * 1e3 / steps_dec,
         "kernel_avg_us": {"step": round(avg_s * 1e6, 2)},
         "kernels": kern,
@@ -406,7 +574,8 @@ def run_decode(args):
         threads = recurrent.default_threads()
         reps, t0 = 0, time.perf_counter()
         while True:
-            recurrent.fwd(ref["q"], ref["k"], ref["v"], ref["beta"], ref["lam"], lar, S0r, nthreads=threads)
+            o_ref, S_ref = recurrent.fwd(ref["q"], ref["k"], ref["v"], ref["beta"], ref["lam"], lar, S0r,
+                                         nthreads=threads)
             reps += 1
             total = time.perf_counter() - t0
             if total >= 10.0 or reps >= 30:
@@ -415,7 +584,15 @@ def run_decode(args):
         out["cpu_baseline"] = {
             "value": nseq * steps_dec / dt, "unit": "tokens/s", "cores": threads, "kind": "oracle",
             "sample": f"fp64 recurrence over the same 1024 tokens for {nseq} of {N} sequences (all {H} heads), "
-                      f"{reps} passes in {total:.1f} s ({dt:.2f} s each)"}
+                      f"{reps} passes in {total:.1f} s ({dt:.2f} s each)",
+            "threads_note": "one oracle thread per CPU available to this process, capped at 16 "
+                            "(the host CPU share of one GPU)"}
+        out["cpu_baseline"].update(host_info())
+        # the timed steps' outputs (every step recomputes the same 1024 tokens from S0)
+        errs = {"o": normwise(f(outs[:, :nseq].transpose(0, 1).cpu()), o_ref),
+                "final_state": normwise(f(S[:nseq].cpu()), S_ref)}
+        out["parity"] = {"sequences": list(range(nseq)), "tolerance": 2e-2, "max_err": max(errs.values()),
+                         "ok": all(x <= 2e-2 for x in errs.values()), "errors": errs}
     return out
 
 
@@ -431,7 +608,10 @@ def main():
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--gate", default="G2", choices=["G1", "G2", "G3"])
     ap.add_argument("--workload", default="train", choices=["train", "fwd", "long", "decode", "varlen", "tiny", "layer", "recurrent"])
-    ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
+    ap.add_argument("--no-cpu", action="store_true",
+                    help="skip the CPU oracle baseline (and with it the same-run parity check)")
+    ap.add_argument("--settle-ms", type=float, default=200.0,
+                    help="untimed steps for this long before the warm-up steps (GPU clock ramp-up)")
     ap.add_argument("--cpu-units", type=int, default=64)
     ap.add_argument("--calib-copy", type=int, default=0, metavar="MIB",
                     help="after the run, copy a MIB-MiB device buffer three times (outside the timed "

@@ -14,12 +14,14 @@
 //   S'  = g_C S + D^T diag(g_C / g) K
 //
 // k_prep   (persistent over chunk-head units, fully parallel): b, the Gram
-//          products, A, the UT solve; writes the gate block, M and U^T.
+//          products, A, the UT solve; writes the gate block (b, beta,
+//          lambda), the output operator P = Gam * M_causal * Q K^T,
+//          T = M diag(beta) and, when a saved context is kept, M.
 // k_scan_fwd (one workgroup per sequence, head and Dv tile): the sequential
 //          pass over chunks; the state tile stays in MFMA accumulators in fp32;
-//          D, the chunk output and the state update are computed on chip from
-//          Q, K, M, U and the gates (W and the output operator are never
-//          formed in memory).
+//          D = T V + T Y, the chunk output and the state update are computed
+//          on chip from Q, K, V, T, P and the gates (U and W are never formed
+//          in memory).
 #include "qd_common.h"
 #include "qd_launch.h"
 

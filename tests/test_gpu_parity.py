@@ -30,7 +30,7 @@ def test_fwd_fp32(gate, Dv):
 
 
 @pytest.mark.parametrize("gate", GATES)
-@pytest.mark.parametrize("Dk,Dv", [(128, 128), (128, 256), (64, 64), (128, 64), (64, 256)])
+@pytest.mark.parametrize("Dk,Dv", [(128, 128), (128, 256), (64, 64), (128, 64), (64, 256), (64, 128)])
 def test_fwd_bf16(gate, Dk, Dv):
     d = synth.make(2, 300, 2, Dk, Dv, "bf16", gate, seed=102, s0=True)
     o, Sf, _ = gpu_fwd(d)
@@ -72,7 +72,7 @@ def test_wide_value_tiles(Dk, Dv, B, H, T):
 
 
 @pytest.mark.parametrize("gate", GATES)
-@pytest.mark.parametrize("Dv", [64, 128])
+@pytest.mark.parametrize("Dv", [64, 128, 256])
 def test_bwd_fp32(gate, Dv):
     d = synth.make(2, 150, 2, 64, Dv, "f32", gate, seed=105, s0=True, with_do=True)
     _, _, saved = gpu_fwd(d, save_states=True)
@@ -81,13 +81,56 @@ def test_bwd_fp32(gate, Dv):
     _check(bwd_errors(d, g, dSf), TOL["f32"], f"bwd fp32 {gate} Dv={Dv}")
 
 
+# every (Dk, Dv) instantiation of the bf16 kernels
+BF16_DIMS = [(128, 128), (128, 256), (64, 64), (128, 64), (64, 256), (64, 128)]
+
+
 @pytest.mark.parametrize("gate", GATES)
-@pytest.mark.parametrize("Dk,Dv", [(128, 128), (128, 256), (64, 64)])
+@pytest.mark.parametrize("Dk,Dv", BF16_DIMS)
 def test_bwd_bf16(gate, Dk, Dv):
     d = synth.make(2, 200, 2, Dk, Dv, "bf16", gate, seed=106, s0=True, with_do=True)
     _, _, saved = gpu_fwd(d, save_states=True)
     g = gpu_bwd(d, saved)
     _check(bwd_errors(d, g), TOL["bf16"], f"bwd bf16 {gate} Dk={Dk} Dv={Dv}")
+
+
+@pytest.mark.parametrize("gate", ["G1", "G3"])
+@pytest.mark.parametrize("Dk,Dv", [(128, 128), (64, 256)])
+def test_bwd_bf16_final_state_gradient(gate, Dk, Dv):
+    """A non-zero gradient of the final state enters the backward scan's
+    accumulator at the last chunk (bf16 activations, fp32 state gradient)."""
+    d = synth.make(2, 170, 2, Dk, Dv, "bf16", gate, seed=122, s0=True, with_do=True)
+    _, _, saved = gpu_fwd(d, save_states=True)
+    dSf = torch.from_numpy(np.random.default_rng(13).standard_normal((2, 2, Dv, Dk)).astype(np.float32))
+    g = gpu_bwd(d, saved, d_final_state=dSf)
+    _check(bwd_errors(d, g, dSf), TOL["bf16"], f"bwd bf16 dS_final {gate} Dk={Dk} Dv={Dv}")
+
+
+@pytest.mark.parametrize("dt", ["f32", "bf16"])
+@pytest.mark.parametrize("gate", ["G1", "G2", "G3"])
+def test_beta_zero_closed_form(dt, gate):
+    """beta = 0 writes nothing: the state only decays, S_t = (prod_{j<=t} alpha_j) S_0
+    (S_t = S_0 without decay) and o_t = S_t q_t.  Checked against that closed
+    form (fp64, independent of the oracle) and the oracle, forward and backward."""
+    D = 64 if dt == "f32" else 128
+    # with G2's decay (mean log alpha -0.81) the state leaves the fp32 range
+    # after about 100 tokens, so that mode runs a shorter sequence
+    T = 40 if gate == "G2" else 150
+    d = synth.make(2, T, 2, D, D, dt, gate, seed=123, s0=True, with_do=True)
+    d = dict(d, beta=torch.zeros_like(d["beta"]))
+    o, Sf, saved = gpu_fwd(d, save_states=True)
+    S0 = f64(d["initial_state"])                                   # [N, H, Dv, Dk]
+    cum = (np.zeros(d["beta"].shape) if d["log_alpha"] is None
+           else np.cumsum(f64(d["log_alpha"]), axis=1))            # [B, T, H]
+    decay = np.exp(cum)
+    S_T = decay[:, -1, :, None, None] * S0
+    o_ref = decay[..., None] * np.einsum("nhvk,nthk->nthv", S0, f64(d["q"]))
+    tol = TOL[dt]
+    assert normwise(f64(Sf.cpu()), S_T) <= tol
+    assert normwise(f64(o.cpu()), o_ref) <= tol
+    _check(fwd_errors(d, o, Sf), tol, f"beta=0 fwd {dt} {gate}")
+    g = gpu_bwd(d, saved)
+    _check(bwd_errors(d, g), tol, f"beta=0 bwd {dt} {gate}")
 
 
 @pytest.mark.parametrize("gate", ["G1", "G3"])

@@ -36,8 +36,9 @@ def test_training_step_full(gate):
     assert all(v <= TOL["bf16"] for v in e.values()), e
 
 
-def test_long_context_forward_sampled_heads():
-    d = synth.make_workload(4, "G1")
+@pytest.mark.parametrize("gate", ["G1", "G2"])
+def test_long_context_forward_sampled_heads(gate):
+    d = synth.make_workload(4, gate)
     o, Sf, _ = gpu_fwd(d)
     heads = [0, 7, 15]
     ds = select_heads(d, heads)
