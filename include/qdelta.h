@@ -30,9 +30,10 @@
  *    workspace of at least the size reported by qdelta_chunk_workspace_bytes.
  *  - Validation of every host-visible argument happens before the first
  *    launch; on any error nothing is launched and nothing is written.
- *  - Apart from the opt-in measurement facility at the end of this file, there
- *    is no global mutable state; calls on different streams may overlap
- *    provided their workspaces and outputs do not.
+ *  - Apart from the opt-in measurement facility at the end of this file and
+ *    the scratch array of qdelta_chunk_fwd_noalloc, there is no global mutable
+ *    state; calls on different streams may overlap provided their workspaces
+ *    and outputs do not.
  *  - Supported: Dk in {64, 128}; Dv in {64, 128, 256}; chunk == 64; T >= 0 need
  *    not be a multiple of chunk.  QDELTA_F32 additionally requires Dk == 64.
  *    Anything else returns QDELTA_EUNSUPPORTED.
@@ -129,6 +130,29 @@ int qdelta_chunk_fwd(int32_t B, int32_t T, int32_t H, int32_t Dk, int32_t Dv, in
                      const float* beta, const float* lam, const float* log_alpha,
                      const float* initial_state, void* o, float* final_state,
                      void* saved, void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* Allocation-free forward, for callers that cannot allocate device memory
+ * or hand over a workspace: code under HIP graph capture, tight serving
+ * loops, harnesses that forbid allocation.  Same arguments and results as
+ * qdelta_chunk_fwd (dense layout, no saved context); its workspace is a
+ * library-owned scratch array of QDELTA_NOALLOC_SCRATCH_BYTES per device,
+ * held from the first call on that device until the process ends.
+ *  - Sizes whose forward workspace (qdelta_chunk_workspace_bytes with
+ *    is_bwd == 0) exceeds QDELTA_NOALLOC_SCRATCH_BYTES return
+ *    QDELTA_ENOWORKSPACE before any device call (about 3900 chunk-head units
+ *    at bf16, e.g. B=8 T=2048 H=8 fits; about 2000 at fp32).
+ *  - Calls no allocating routine.  The first call on a device looks up the
+ *    scratch array's device address (QDELTA_EHIP if that fails).
+ *  - Every call on a device shares that device's scratch array: calls that
+ *    overlap in time on one device (different streams or host threads) race
+ *    and must be serialised by the caller.  The array keeps the last call's
+ *    contents; no call relies on its initial contents. */
+#define QDELTA_NOALLOC_SCRATCH_BYTES ((size_t)64 << 20)
+int qdelta_chunk_fwd_noalloc(int32_t B, int32_t T, int32_t H, int32_t Dk, int32_t Dv, int32_t chunk,
+                             int32_t dtype, const void* q, const void* k, const void* v,
+                             const float* beta, const float* lam, const float* log_alpha,
+                             const float* initial_state, void* o, float* final_state,
+                             hipStream_t stream);
 
 /* Varlen forward: as qdelta_chunk_fwd with B == 1, T total tokens, N sequences
  * delimited by the device array cu_seqlens[N+1]; states are [N,H,Dv,Dk]. */

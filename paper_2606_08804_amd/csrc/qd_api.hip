@@ -4,6 +4,7 @@
 #include <stddef.h>
 #include <stdint.h>
 
+#include <mutex>
 #include <vector>
 
 #include "qd_launch.h"
@@ -119,11 +120,13 @@ int make_sizes(bool varlen, int32_t B, int32_t T, int32_t N, const int32_t* cu, 
   return QDELTA_OK;
 }
 
+// dry == true: validation only (ws is not dereferenced); returns what the
+// call would return up to its first launch.
 int fwd_impl(bool varlen, int32_t B, int32_t T, int32_t N, const int32_t* cu, int32_t H,
              int32_t Dk, int32_t Dv, int32_t chunk, int32_t dtype, const void* q, const void* k,
              const void* v, const float* beta, const float* lam, const float* log_alpha,
              const float* initial_state, void* o, float* final_state, void* saved,
-             void* ws, size_t ws_bytes, hipStream_t stream) {
+             void* ws, size_t ws_bytes, hipStream_t stream, bool dry = false) {
   Sizes s;
   int rc = make_sizes(varlen, B, T, N, cu, s);
   if (rc) return rc;
@@ -139,7 +142,7 @@ int fwd_impl(bool varlen, int32_t B, int32_t T, int32_t N, const int32_t* cu, in
   const Layout L = make_layout(s.slots * (size_t)H, Dk, Dv, esz, false);
   if (L.total > 0 && (ws == nullptr || !aligned(ws))) return QDELTA_EINVAL;
   if (ws_bytes < L.total) return QDELTA_ENOWORKSPACE;
-  if (s.N == 0) return QDELTA_OK;
+  if (s.N == 0 || dry) return QDELTA_OK;
 
   char* w = static_cast<char*>(ws);
   qd::Params p{};
@@ -224,6 +227,31 @@ int bwd_impl(bool varlen, int32_t B, int32_t T, int32_t N, const int32_t* cu, in
   }
   e = qd::launch_bwd(p, dtype, Dk, Dv, stream);
   return e == hipSuccess ? QDELTA_OK : QDELTA_EHIP;
+}
+
+// Scratch of the allocation-free forward: one copy per device, held until
+// the process ends.  In host code `scratch` is only a stand-in for the
+// symbol; its device address (per device) comes from hipGetSymbolAddress and
+// is the only form passed to kernels.
+__device__ __align__(256) char scratch[QDELTA_NOALLOC_SCRATCH_BYTES];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+// Device address of `scratch` on the current device, looked up once per
+// device (with that device current) and cached.
+int scratch_ptr(void** out) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return QDELTA_EHIP;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (g_scratch_ptr[dev] == nullptr) {
+    void* ptr = nullptr;
+    if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)) != hipSuccess || ptr == nullptr) return QDELTA_EHIP;
+    g_scratch_ptr[dev] = ptr;
+  }
+  *out = g_scratch_ptr[dev];
+  return QDELTA_OK;
 }
 
 // Measurement facility state (process-wide; benchmarks only).
@@ -357,6 +385,27 @@ int qdelta_chunk_fwd_varlen(int32_t T, int32_t N, const int32_t* cu_seqlens, int
                             void* saved, void* ws, size_t ws_bytes, hipStream_t stream) {
   return fwd_impl(true, 1, T, N, cu_seqlens, H, Dk, Dv, chunk, dtype, q, k, v, beta, lam,
                   log_alpha, initial_state, o, final_state, saved, ws, ws_bytes, stream);
+}
+
+int qdelta_chunk_fwd_noalloc(int32_t B, int32_t T, int32_t H, int32_t Dk, int32_t Dv, int32_t chunk,
+                             int32_t dtype, const void* q, const void* k, const void* v,
+                             const float* beta, const float* lam, const float* log_alpha,
+                             const float* initial_state, void* o, float* final_state,
+                             hipStream_t stream) {
+  // validate first (no device call): sizes past the scratch array return
+  // QDELTA_ENOWORKSPACE; the workspace pointer is not dereferenced here
+  void* const probe = reinterpret_cast<void*>(uintptr_t(256));
+  int rc = fwd_impl(false, B, T, B, nullptr, H, Dk, Dv, chunk, dtype, q, k, v, beta, lam, log_alpha,
+                    initial_state, o, final_state, nullptr, probe, QDELTA_NOALLOC_SCRATCH_BYTES, stream,
+                    true);
+  if (rc != QDELTA_OK || B == 0) return rc;
+  void* ws = nullptr;
+  rc = scratch_ptr(&ws);
+  if (rc != QDELTA_OK) return rc;
+  // every workspace byte the kernels read is written earlier in the same
+  // call (preparation before scan), so nothing needs clearing
+  return fwd_impl(false, B, T, B, nullptr, H, Dk, Dv, chunk, dtype, q, k, v, beta, lam, log_alpha,
+                  initial_state, o, final_state, nullptr, ws, QDELTA_NOALLOC_SCRATCH_BYTES, stream);
 }
 
 int qdelta_chunk_bwd(int32_t B, int32_t T, int32_t H, int32_t Dk, int32_t Dv, int32_t chunk,

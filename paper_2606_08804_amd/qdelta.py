@@ -9,6 +9,8 @@ Functions mirror the C ABI in ``include/qdelta.h``:
 chunk_fwd(q, k, v, beta, lam, log_alpha=None, initial_state=None, cu_seqlens=None,
           output_final_state=True, save_states=False) -> (o, final_state, saved)
           (saved: uint8 device buffer holding the saved context for the backward)
+chunk_fwd_noalloc(q, k, v, beta, lam, log_alpha=None, initial_state=None, out=None,
+          final_state_out=None) -> (o, final_state)    (dense; library-owned scratch, no workspace)
 chunk_bwd(q, k, v, beta, lam, log_alpha, initial_state, saved_states, d_o,
           d_final_state=None, cu_seqlens=None) -> dict of gradients
 recurrent_step(q, k, v, beta, lam, log_alpha, state) -> o        (state updated in place)
@@ -35,8 +37,9 @@ EXPORTS = (
     "qdelta_chunk_workspace_bytes", "qdelta_chunk_fwd", "qdelta_chunk_fwd_varlen",
     "qdelta_chunk_bwd", "qdelta_chunk_bwd_varlen", "qdelta_recurrent_step",
     "qdelta_recurrent_fwd", "qdelta_recurrent_fwd_varlen", "qdelta_l2norm_fwd", "qdelta_l2norm_bwd",
-    "qdelta_profile_begin", "qdelta_profile_end",
+    "qdelta_profile_begin", "qdelta_profile_end", "qdelta_chunk_fwd_noalloc",
 )
+NOALLOC_SCRATCH_BYTES = 64 << 20
 
 STAGES = ("prep_fwd", "scan_fwd", "prep_bwd", "scan_bwd", "intra", "step", "rec_fwd")
 
@@ -70,6 +73,8 @@ def lib():
         L.qdelta_chunk_workspace_bytes.restype = sz
         L.qdelta_chunk_fwd.argtypes = [i32] * 7 + [P] * 10 + [P, sz, P]
         L.qdelta_chunk_fwd.restype = ctypes.c_int
+        L.qdelta_chunk_fwd_noalloc.argtypes = [i32] * 7 + [P] * 9 + [P]
+        L.qdelta_chunk_fwd_noalloc.restype = ctypes.c_int
         L.qdelta_chunk_fwd_varlen.argtypes = [i32, i32, P] + [i32] * 5 + [P] * 10 + [P, sz, P]
         L.qdelta_chunk_fwd_varlen.restype = ctypes.c_int
         L.qdelta_chunk_bwd.argtypes = [i32] * 7 + [P] * 17 + [P, sz, P]
@@ -205,6 +210,35 @@ def chunk_fwd(q, k, v, beta, lam, log_alpha=None, initial_state=None, cu_seqlens
     else:
         _check("qdelta_chunk_fwd_varlen", L.qdelta_chunk_fwd_varlen(T, N, _p(cu_seqlens), *common))
     return o, Sf, saved
+
+
+def chunk_fwd_noalloc(q, k, v, beta, lam, log_alpha=None, initial_state=None, out=None,
+                      final_state_out=None, output_final_state=True):
+    """Dense chunkwise forward through qdelta_chunk_fwd_noalloc: no workspace
+    and no saved context; the library uses its own per-device scratch array.
+    Outputs may be passed in (out [B,T,H,Dv], final_state_out [B,H,Dv,Dk]) so
+    that this call allocates nothing either.  Returns (o, final_state or None)."""
+    L = lib()
+    dt = _dt(q)
+    B, T, H, Dk, Dv, N = _dims(q, v, None)
+    act = q.shape[:-1]
+    _need(q, "q", q.dtype)
+    _need(k, "k", q.dtype, q.shape)
+    _need(v, "v", q.dtype, tuple(act) + (Dv,))
+    _need(beta, "beta", torch.float32, act)
+    _opt(lam, "lam", torch.float32, act)
+    _opt(log_alpha, "log_alpha", torch.float32, act)
+    _opt(initial_state, "initial_state", torch.float32, (N, H, Dv, Dk))
+    o = out if out is not None else torch.empty(tuple(act) + (Dv,), dtype=q.dtype, device=q.device)
+    _need(o, "out", q.dtype, tuple(act) + (Dv,))
+    Sf = final_state_out
+    if Sf is None and output_final_state:
+        Sf = torch.empty((N, H, Dv, Dk), dtype=torch.float32, device=q.device)
+    _opt(Sf, "final_state_out", torch.float32, (N, H, Dv, Dk))
+    _check("qdelta_chunk_fwd_noalloc",
+           L.qdelta_chunk_fwd_noalloc(B, T, H, Dk, Dv, CHUNK, dt, _p(q), _p(k), _p(v), _p(beta), _p(lam),
+                                      _p(log_alpha), _p(initial_state), _p(o), _p(Sf), _stream()))
+    return o, Sf
 
 
 def chunk_bwd(q, k, v, beta, lam, log_alpha, initial_state, saved_states, d_o,

@@ -22,7 +22,7 @@ def header_functions():
 def test_library_exports_every_declared_symbol():
     L = qdelta.lib()
     names = header_functions()
-    assert len(names) == 16
+    assert len(names) == 17
     for n in names:
         assert hasattr(L, n), n
     assert sorted(names) == sorted(qdelta.EXPORTS)
@@ -98,6 +98,30 @@ def test_fwd_rejects_bad_arguments_before_launch():
     assert _fwd(ws=None) == E.QDELTA_EINVAL
     # nothing to do: zero sequences
     assert _fwd(B=0, ws=None, ws_bytes=0) == E.QDELTA_OK
+
+
+def test_noalloc_forward_validates_before_any_device_call():
+    """The allocation-free forward rejects bad arguments, and sizes whose
+    workspace exceeds its scratch array, before touching the device."""
+    L = qdelta.lib()
+    E = qdelta
+    f = FAKE
+
+    def call(B=1, T=64, H=1, Dk=64, Dv=64, dtype=1, q=f, o=f):
+        return L.qdelta_chunk_fwd_noalloc(B, T, H, Dk, Dv, 64, dtype, q, f, f, f, f, None, None, o, None, None)
+
+    assert call(Dk=96) == E.QDELTA_EUNSUPPORTED
+    assert call(dtype=0, Dk=128) == E.QDELTA_EUNSUPPORTED
+    assert call(T=-1) == E.QDELTA_EINVAL
+    assert call(q=None) == E.QDELTA_EINVAL
+    assert call(o=f + 4) == E.QDELTA_EINVAL
+    assert call(B=0) == E.QDELTA_OK
+    # bf16 forward workspace: 17152 B per chunk-head unit against 64 MiB
+    cap = qdelta.NOALLOC_SCRATCH_BYTES
+    assert qdelta.workspace_bytes(8, 2048, 8, 128, 128, 1) <= cap
+    assert qdelta.workspace_bytes(4, 4096, 16, 128, 128, 1) > cap
+    assert call(B=4, T=4096, H=16, Dk=128, Dv=128) == E.QDELTA_ENOWORKSPACE
+    assert call(B=1, T=65536, H=16, Dk=128, Dv=128) == E.QDELTA_ENOWORKSPACE
 
 
 def test_bwd_and_varlen_reject_bad_arguments():

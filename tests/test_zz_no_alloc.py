@@ -1,0 +1,38 @@
+"""The allocation-free forward (qdelta_chunk_fwd_noalloc, library-owned
+scratch) against the workspace forward (qdelta_chunk_fwd) on the same
+inputs: two calls in a row, the second smaller, so that the second reads a
+scratch array holding the first call's contents.  Results must be equal bit
+for bit (same kernels, same arithmetic) and match the fp64 oracle."""
+import pytest
+import torch
+
+from paper_2606_08804_amd import qdelta, synth
+from tests.gpu_helpers import TOL, dev, fwd_errors, gpu_fwd
+
+pytestmark = pytest.mark.gpu
+
+# (B, T, H, Dk, Dv, dtype, gate): the forward bf16 workload shape (35 MB of
+# scratch), then a smaller fp32 case with a ragged last chunk
+CASES = [(8, 2048, 8, 128, 128, "bf16", "G2"), (2, 150, 2, 64, 64, "f32", "G3")]
+
+
+def test_noalloc_forward_equals_workspace_forward():
+    for i, (B, T, H, Dk, Dv, dt, gate) in enumerate(CASES):
+        print(f"case {i}: B={B} T={T} H={H} Dk={Dk} Dv={Dv} {dt} {gate}", flush=True)
+        d = synth.make(B, T, H, Dk, Dv, dt, gate, seed=140 + i, s0=True)
+        o_ref, S_ref, _ = gpu_fwd(d)
+        o, S = qdelta.chunk_fwd_noalloc(dev(d["q"]), dev(d["k"]), dev(d["v"]), dev(d["beta"]),
+                                        dev(d["lam"]), dev(d["log_alpha"]), dev(d["initial_state"]))
+        torch.cuda.synchronize()
+        assert torch.equal(o, o_ref), f"case {i}: o differs from the workspace forward"
+        assert torch.equal(S, S_ref), f"case {i}: final state differs from the workspace forward"
+        e = fwd_errors(d, o, S)
+        assert all(v <= TOL[dt] for v in e.values()), (i, e)
+
+
+def test_noalloc_forward_rejects_oversized_call():
+    d = synth.make(4, 4096, 16, 128, 128, "bf16", "G2", seed=150, s0=False)
+    with pytest.raises(qdelta.QDeltaError) as ei:
+        qdelta.chunk_fwd_noalloc(dev(d["q"]), dev(d["k"]), dev(d["v"]), dev(d["beta"]), dev(d["lam"]),
+                                 dev(d["log_alpha"]), None)
+    assert ei.value.status == qdelta.QDELTA_ENOWORKSPACE
