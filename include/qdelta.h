@@ -25,6 +25,13 @@
  *    QDELTA_F32.  Gates, states and gate gradients are always float32.
  *  - Decay is passed as log(alpha) (float32, <= 0 expected); log_alpha == NULL
  *    means alpha == 1 everywhere.  Gate values are not clamped.
+ *  - The query-feedback gate lambda is either per token and head (`lam`, a
+ *    [.., H] float32 tensor) or one constant for every token and head
+ *    (`lam` == NULL, value `lam_scalar`): the paper's ablations fix it to a
+ *    scalar (Sec. 4.2, table "Ablation on the query-feedback coefficient
+ *    lambda": 0.2, 0.5, 0.8, and 1 for no gating), and lam_scalar == 0 is the
+ *    gated delta rule of Sec. 2 (x_t = k_t).  The constant form reads no
+ *    lambda stream.
  *  - Calls are asynchronous on `stream` (0 = the null stream): no host
  *    synchronisation and no device allocation.  Scratch memory is a caller
  *    workspace of at least the size reported by qdelta_chunk_workspace_bytes.
@@ -117,8 +124,9 @@ size_t qdelta_chunk_workspace_bytes(int32_t B, int32_t T, int32_t H, int32_t Dk,
 /* Chunkwise forward (Sec. 3.3 chunkwise form; App. D).
  *   q, k [B,T,H,Dk], v [B,T,H,Dv]           activations (dtype)
  *   beta [B,T,H]                             write strength (fp32)
- *   lam [B,T,H] or NULL                      query-feedback gate (fp32); NULL means lambda == 0,
- *                                            the gated delta rule of Sec. 2 (x_t = k_t)
+ *   lam [B,T,H] or NULL                      query-feedback gate (fp32); NULL: lambda == lam_scalar
+ *   lam_scalar                               the constant lambda when lam is NULL (0: the gated
+ *                                            delta rule of Sec. 2, x_t = k_t)
  *   log_alpha [B,T,H] or NULL                log of the forget gate (fp32)
  *   initial_state [B,H,Dv,Dk] or NULL        entry state (NULL = zero)
  *   o [B,T,H,Dv]                             output o_t = S_t q_t (dtype)
@@ -127,7 +135,7 @@ size_t qdelta_chunk_workspace_bytes(int32_t B, int32_t T, int32_t H, int32_t Dk,
  *   ws, ws_bytes                             device workspace */
 int qdelta_chunk_fwd(int32_t B, int32_t T, int32_t H, int32_t Dk, int32_t Dv, int32_t chunk,
                      int32_t dtype, const void* q, const void* k, const void* v,
-                     const float* beta, const float* lam, const float* log_alpha,
+                     const float* beta, const float* lam, float lam_scalar, const float* log_alpha,
                      const float* initial_state, void* o, float* final_state,
                      void* saved, void* ws, size_t ws_bytes, hipStream_t stream);
 
@@ -150,16 +158,16 @@ int qdelta_chunk_fwd(int32_t B, int32_t T, int32_t H, int32_t Dk, int32_t Dv, in
 #define QDELTA_NOALLOC_SCRATCH_BYTES ((size_t)64 << 20)
 int qdelta_chunk_fwd_noalloc(int32_t B, int32_t T, int32_t H, int32_t Dk, int32_t Dv, int32_t chunk,
                              int32_t dtype, const void* q, const void* k, const void* v,
-                             const float* beta, const float* lam, const float* log_alpha,
-                             const float* initial_state, void* o, float* final_state,
-                             hipStream_t stream);
+                             const float* beta, const float* lam, float lam_scalar,
+                             const float* log_alpha, const float* initial_state, void* o,
+                             float* final_state, hipStream_t stream);
 
 /* Varlen forward: as qdelta_chunk_fwd with B == 1, T total tokens, N sequences
  * delimited by the device array cu_seqlens[N+1]; states are [N,H,Dv,Dk]. */
 int qdelta_chunk_fwd_varlen(int32_t T, int32_t N, const int32_t* cu_seqlens, int32_t H,
                             int32_t Dk, int32_t Dv, int32_t chunk, int32_t dtype,
                             const void* q, const void* k, const void* v, const float* beta,
-                            const float* lam, const float* log_alpha,
+                            const float* lam, float lam_scalar, const float* log_alpha,
                             const float* initial_state, void* o, float* final_state,
                             void* saved, void* ws, size_t ws_bytes, hipStream_t stream);
 
@@ -171,12 +179,15 @@ int qdelta_chunk_fwd_varlen(int32_t T, int32_t N, const int32_t* cu_seqlens, int
  *                   or NULL to recompute the state scan inside this call
  *   d_o [B,T,H,Dv]  (dtype);  d_final_state [B,H,Dv,Dk] or NULL (= zero)
  *   dq, dk [B,T,H,Dk], dv [B,T,H,Dv] (dtype); dbeta [B,T,H] (fp32)
- *   dlam [B,T,H] fp32: required iff lam != NULL, else must be NULL
+ *   dlam: lam != NULL: [B,T,H] fp32, required;
+ *         lam == NULL: NULL (no lambda gradient) or ONE fp32 that receives the
+ *         gradient with respect to the constant lambda (summed over every token
+ *         and head, in a fixed order: the same value on every run)
  *   dlog_alpha [B,T,H] fp32: required iff log_alpha != NULL, else must be NULL
  *   d_initial_state [B,H,Dv,Dk] or NULL */
 int qdelta_chunk_bwd(int32_t B, int32_t T, int32_t H, int32_t Dk, int32_t Dv, int32_t chunk,
                      int32_t dtype, const void* q, const void* k, const void* v,
-                     const float* beta, const float* lam, const float* log_alpha,
+                     const float* beta, const float* lam, float lam_scalar, const float* log_alpha,
                      const float* initial_state, const void* saved, const void* d_o,
                      const float* d_final_state, void* dq, void* dk, void* dv, float* dbeta,
                      float* dlam, float* dlog_alpha, float* d_initial_state, void* ws,
@@ -186,7 +197,7 @@ int qdelta_chunk_bwd(int32_t B, int32_t T, int32_t H, int32_t Dk, int32_t Dv, in
 int qdelta_chunk_bwd_varlen(int32_t T, int32_t N, const int32_t* cu_seqlens, int32_t H,
                             int32_t Dk, int32_t Dv, int32_t chunk, int32_t dtype,
                             const void* q, const void* k, const void* v, const float* beta,
-                            const float* lam, const float* log_alpha,
+                            const float* lam, float lam_scalar, const float* log_alpha,
                             const float* initial_state, const void* saved,
                             const void* d_o, const float* d_final_state, void* dq, void* dk,
                             void* dv, float* dbeta, float* dlam, float* dlog_alpha,
@@ -196,27 +207,28 @@ int qdelta_chunk_bwd_varlen(int32_t T, int32_t N, const int32_t* cu_seqlens, int
 /* One token of the recurrence for N sequences (decode), Sec. 3.3
  * Eq. (qdelta_decay) applied once:
  *   q, k [N,H,Dk], v [N,H,Dv] (dtype); beta, lam, log_alpha [N,H] (fp32,
- *   lam (NULL: lambda == 0) and log_alpha (NULL: alpha == 1) may be NULL);  state [N,H,Dv,Dk] fp32, updated in place;
+ *   lam (NULL: lambda == lam_scalar) and log_alpha (NULL: alpha == 1) may be
+ *   NULL);  state [N,H,Dv,Dk] fp32, updated in place;
  *   o [N,H,Dv] (dtype) = updated state times q.
  * Supported: Dk in {64, 128}, Dv a positive multiple of 8 up to 256, any dtype. */
 int qdelta_recurrent_step(int32_t N, int32_t H, int32_t Dk, int32_t Dv, int32_t dtype,
                           const void* q, const void* k, const void* v, const float* beta,
-                          const float* lam, const float* log_alpha, float* state, void* o,
-                          hipStream_t stream);
+                          const float* lam, float lam_scalar, const float* log_alpha, float* state,
+                          void* o, hipStream_t stream);
 
 /* Fully recurrent forward over whole sequences: Sec. 3.3 Eq. (qdelta_decay)
  * applied token by token (the paper provides this form beside the chunkwise
  * one).  Same results as qdelta_chunk_fwd up to rounding, one launch, no
  * workspace and no saved context (inference and short sequences).
  *   q, k [B,T,H,Dk], v [B,T,H,Dv] (dtype); beta [B,T,H] fp32;
- *   lam [B,T,H] or NULL (lambda == 0); log_alpha [B,T,H] or NULL (alpha == 1);
+ *   lam [B,T,H] or NULL (lambda == lam_scalar); log_alpha [B,T,H] or NULL (alpha == 1);
  *   initial_state [B,H,Dv,Dk] fp32 or NULL (zero);
  *   o [B,T,H,Dv] (dtype); final_state [B,H,Dv,Dk] fp32 or NULL.
  * Supported: Dk in {64, 128}, Dv a positive multiple of 8 up to 256, any dtype. */
 int qdelta_recurrent_fwd(int32_t B, int32_t T, int32_t H, int32_t Dk, int32_t Dv, int32_t dtype,
                          const void* q, const void* k, const void* v, const float* beta,
-                         const float* lam, const float* log_alpha, const float* initial_state,
-                         void* o, float* final_state, hipStream_t stream);
+                         const float* lam, float lam_scalar, const float* log_alpha,
+                         const float* initial_state, void* o, float* final_state, hipStream_t stream);
 
 /* Varlen recurrent forward: B == 1, T total tokens, N sequences delimited by
  * the device array cu_seqlens[N+1] (entries are clamped to [0, T]); states
@@ -224,7 +236,7 @@ int qdelta_recurrent_fwd(int32_t B, int32_t T, int32_t H, int32_t Dk, int32_t Dv
 int qdelta_recurrent_fwd_varlen(int32_t T, int32_t N, const int32_t* cu_seqlens, int32_t H,
                                 int32_t Dk, int32_t Dv, int32_t dtype, const void* q,
                                 const void* k, const void* v, const float* beta,
-                                const float* lam, const float* log_alpha,
+                                const float* lam, float lam_scalar, const float* log_alpha,
                                 const float* initial_state, void* o, float* final_state,
                                 hipStream_t stream);
 

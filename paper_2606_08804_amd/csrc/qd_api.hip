@@ -19,6 +19,7 @@ constexpr int kVersion = 10000;  // 1.0.0
 struct Layout {
   size_t wb = 0, wT = 0, wP = 0;   // forward: chunk factors (T always, gates and P when no saved context is kept)
   size_t dSo = 0, dDb = 0, ctx = 0;        // backward: scan outputs, room to recompute the context
+  size_t dlam = 0;                         // backward: per-unit partials of a constant lambda's gradient
   size_t total = 0;
 };
 
@@ -52,6 +53,7 @@ Layout make_layout(size_t units, int Dk, int Dv, int esz, bool bwd) {
     L.dSo = take(units * (size_t)Dv * Dk * esz);
     L.dDb = take(units * C * Dv * esz);
     L.ctx = take(ctx_layout(units, Dk, Dv, esz).total);
+    L.dlam = take(units * sizeof(float));
   } else {
     L.wb = take(units * 3 * C * 4);
     L.wP = take(units * C * C * esz);
@@ -124,7 +126,7 @@ int make_sizes(bool varlen, int32_t B, int32_t T, int32_t N, const int32_t* cu, 
 // call would return up to its first launch.
 int fwd_impl(bool varlen, int32_t B, int32_t T, int32_t N, const int32_t* cu, int32_t H,
              int32_t Dk, int32_t Dv, int32_t chunk, int32_t dtype, const void* q, const void* k,
-             const void* v, const float* beta, const float* lam, const float* log_alpha,
+             const void* v, const float* beta, const float* lam, float lam_c, const float* log_alpha,
              const float* initial_state, void* o, float* final_state, void* saved,
              void* ws, size_t ws_bytes, hipStream_t stream, bool dry = false) {
   Sizes s;
@@ -153,7 +155,7 @@ int fwd_impl(bool varlen, int32_t B, int32_t T, int32_t N, const int32_t* cu, in
   p.n_slots = (int)s.slots;
   p.cu = s.cu;
   p.q = q; p.k = k; p.v = v;
-  p.beta = beta; p.lam = lam; p.la = log_alpha; p.S0 = initial_state;
+  p.beta = beta; p.lam = lam; p.lam_c = lam_c; p.la = log_alpha; p.S0 = initial_state;
   p.o = has_tokens ? o : nullptr;
   p.Sfin = final_state;
   const size_t units = s.slots * (size_t)H;
@@ -171,7 +173,7 @@ int fwd_impl(bool varlen, int32_t B, int32_t T, int32_t N, const int32_t* cu, in
 
 int bwd_impl(bool varlen, int32_t B, int32_t T, int32_t N, const int32_t* cu, int32_t H,
              int32_t Dk, int32_t Dv, int32_t chunk, int32_t dtype, const void* q, const void* k,
-             const void* v, const float* beta, const float* lam, const float* log_alpha,
+             const void* v, const float* beta, const float* lam, float lam_c, const float* log_alpha,
              const float* initial_state, const void* saved, const void* d_o,
              const float* d_final_state, void* dq, void* dk, void* dv, float* dbeta, float* dlam,
              float* dlog_alpha, float* d_initial_state, void* ws, size_t ws_bytes,
@@ -187,8 +189,11 @@ int bwd_impl(bool varlen, int32_t B, int32_t T, int32_t N, const int32_t* cu, in
         ok_ptr(dq) && ok_ptr(dk) && ok_ptr(dv) && ok_ptr(dbeta)))
     return QDELTA_EINVAL;
   if ((log_alpha == nullptr) != (dlog_alpha == nullptr) && has_tokens) return QDELTA_EINVAL;
-  if ((lam == nullptr) != (dlam == nullptr) && has_tokens) return QDELTA_EINVAL;
-  if (!ok_opt(lam) || !ok_opt(dlam) || !ok_opt(log_alpha) || !ok_opt(dlog_alpha) ||
+  // per-token lambda: its gradient is required; constant lambda: dlam is
+  // optional and then receives one float
+  if (lam != nullptr && dlam == nullptr && has_tokens) return QDELTA_EINVAL;
+  if (lam == nullptr && dlam != nullptr && (reinterpret_cast<uintptr_t>(dlam) & 3u)) return QDELTA_EINVAL;
+  if (!ok_opt(lam) || (lam != nullptr && !ok_opt(dlam)) || !ok_opt(log_alpha) || !ok_opt(dlog_alpha) ||
       !ok_opt(initial_state) ||
       !ok_opt(saved) || !ok_opt(d_final_state) || !ok_opt(d_initial_state))
     return QDELTA_EINVAL;
@@ -196,7 +201,12 @@ int bwd_impl(bool varlen, int32_t B, int32_t T, int32_t N, const int32_t* cu, in
   const Layout L = make_layout(s.slots * (size_t)H, Dk, Dv, esz, true);
   if (L.total > 0 && (ws == nullptr || !aligned(ws))) return QDELTA_EINVAL;
   if (ws_bytes < L.total) return QDELTA_ENOWORKSPACE;
-  if (s.N == 0) return QDELTA_OK;
+  const bool dlam_const = lam == nullptr && dlam != nullptr;
+  if (s.N == 0) {
+    // nothing to differentiate: a requested constant-lambda gradient is zero
+    if (dlam_const) return qd::launch_zero(dlam, stream) == hipSuccess ? QDELTA_OK : QDELTA_EHIP;
+    return QDELTA_OK;
+  }
 
   char* w = static_cast<char*>(ws);
   qd::Params p{};
@@ -207,11 +217,14 @@ int bwd_impl(bool varlen, int32_t B, int32_t T, int32_t N, const int32_t* cu, in
   p.n_slots = (int)s.slots;
   p.cu = s.cu;
   p.q = q; p.k = k; p.v = v;
-  p.beta = beta; p.lam = lam; p.la = log_alpha; p.S0 = initial_state;
+  p.beta = beta; p.lam = lam; p.lam_c = lam_c; p.la = log_alpha; p.S0 = initial_state;
   p.dO = d_o;
   p.dSfin = d_final_state;
   p.dq = dq; p.dk = dk; p.dv = dv;
-  p.dbeta = dbeta; p.dlam = dlam; p.dla = dlog_alpha; p.dS0 = d_initial_state;
+  p.dbeta = dbeta; p.dla = dlog_alpha; p.dS0 = d_initial_state;
+  p.dlam = dlam_const ? nullptr : dlam;
+  p.dlam_sum = dlam_const ? dlam : nullptr;
+  p.w_dlam = dlam_const ? reinterpret_cast<float*>(w + L.dlam) : nullptr;
   p.w_dSo = w + L.dSo;
   p.w_dDb = w + L.dDb;
   const size_t units = s.slots * (size_t)H;
@@ -370,52 +383,52 @@ size_t qdelta_chunk_workspace_bytes(int32_t B, int32_t T, int32_t H, int32_t Dk,
 
 int qdelta_chunk_fwd(int32_t B, int32_t T, int32_t H, int32_t Dk, int32_t Dv, int32_t chunk,
                      int32_t dtype, const void* q, const void* k, const void* v,
-                     const float* beta, const float* lam, const float* log_alpha,
+                     const float* beta, const float* lam, float lam_scalar, const float* log_alpha,
                      const float* initial_state, void* o, float* final_state,
                      void* saved, void* ws, size_t ws_bytes, hipStream_t stream) {
-  return fwd_impl(false, B, T, B, nullptr, H, Dk, Dv, chunk, dtype, q, k, v, beta, lam,
+  return fwd_impl(false, B, T, B, nullptr, H, Dk, Dv, chunk, dtype, q, k, v, beta, lam, lam_scalar,
                   log_alpha, initial_state, o, final_state, saved, ws, ws_bytes, stream);
 }
 
 int qdelta_chunk_fwd_varlen(int32_t T, int32_t N, const int32_t* cu_seqlens, int32_t H,
                             int32_t Dk, int32_t Dv, int32_t chunk, int32_t dtype,
                             const void* q, const void* k, const void* v, const float* beta,
-                            const float* lam, const float* log_alpha,
+                            const float* lam, float lam_scalar, const float* log_alpha,
                             const float* initial_state, void* o, float* final_state,
                             void* saved, void* ws, size_t ws_bytes, hipStream_t stream) {
-  return fwd_impl(true, 1, T, N, cu_seqlens, H, Dk, Dv, chunk, dtype, q, k, v, beta, lam,
+  return fwd_impl(true, 1, T, N, cu_seqlens, H, Dk, Dv, chunk, dtype, q, k, v, beta, lam, lam_scalar,
                   log_alpha, initial_state, o, final_state, saved, ws, ws_bytes, stream);
 }
 
 int qdelta_chunk_fwd_noalloc(int32_t B, int32_t T, int32_t H, int32_t Dk, int32_t Dv, int32_t chunk,
                              int32_t dtype, const void* q, const void* k, const void* v,
-                             const float* beta, const float* lam, const float* log_alpha,
-                             const float* initial_state, void* o, float* final_state,
-                             hipStream_t stream) {
+                             const float* beta, const float* lam, float lam_scalar,
+                             const float* log_alpha, const float* initial_state, void* o,
+                             float* final_state, hipStream_t stream) {
   // validate first (no device call): sizes past the scratch array return
   // QDELTA_ENOWORKSPACE; the workspace pointer is not dereferenced here
   void* const probe = reinterpret_cast<void*>(uintptr_t(256));
-  int rc = fwd_impl(false, B, T, B, nullptr, H, Dk, Dv, chunk, dtype, q, k, v, beta, lam, log_alpha,
-                    initial_state, o, final_state, nullptr, probe, QDELTA_NOALLOC_SCRATCH_BYTES, stream,
-                    true);
+  int rc = fwd_impl(false, B, T, B, nullptr, H, Dk, Dv, chunk, dtype, q, k, v, beta, lam, lam_scalar,
+                    log_alpha, initial_state, o, final_state, nullptr, probe, QDELTA_NOALLOC_SCRATCH_BYTES,
+                    stream, true);
   if (rc != QDELTA_OK || B == 0) return rc;
   void* ws = nullptr;
   rc = scratch_ptr(&ws);
   if (rc != QDELTA_OK) return rc;
   // every workspace byte the kernels read is written earlier in the same
   // call (preparation before scan), so nothing needs clearing
-  return fwd_impl(false, B, T, B, nullptr, H, Dk, Dv, chunk, dtype, q, k, v, beta, lam, log_alpha,
-                  initial_state, o, final_state, nullptr, ws, QDELTA_NOALLOC_SCRATCH_BYTES, stream);
+  return fwd_impl(false, B, T, B, nullptr, H, Dk, Dv, chunk, dtype, q, k, v, beta, lam, lam_scalar,
+                  log_alpha, initial_state, o, final_state, nullptr, ws, QDELTA_NOALLOC_SCRATCH_BYTES, stream);
 }
 
 int qdelta_chunk_bwd(int32_t B, int32_t T, int32_t H, int32_t Dk, int32_t Dv, int32_t chunk,
                      int32_t dtype, const void* q, const void* k, const void* v,
-                     const float* beta, const float* lam, const float* log_alpha,
+                     const float* beta, const float* lam, float lam_scalar, const float* log_alpha,
                      const float* initial_state, const void* saved, const void* d_o,
                      const float* d_final_state, void* dq, void* dk, void* dv, float* dbeta,
                      float* dlam, float* dlog_alpha, float* d_initial_state, void* ws,
                      size_t ws_bytes, hipStream_t stream) {
-  return bwd_impl(false, B, T, B, nullptr, H, Dk, Dv, chunk, dtype, q, k, v, beta, lam,
+  return bwd_impl(false, B, T, B, nullptr, H, Dk, Dv, chunk, dtype, q, k, v, beta, lam, lam_scalar,
                   log_alpha, initial_state, saved, d_o, d_final_state, dq, dk, dv, dbeta,
                   dlam, dlog_alpha, d_initial_state, ws, ws_bytes, stream);
 }
@@ -423,20 +436,20 @@ int qdelta_chunk_bwd(int32_t B, int32_t T, int32_t H, int32_t Dk, int32_t Dv, in
 int qdelta_chunk_bwd_varlen(int32_t T, int32_t N, const int32_t* cu_seqlens, int32_t H,
                             int32_t Dk, int32_t Dv, int32_t chunk, int32_t dtype,
                             const void* q, const void* k, const void* v, const float* beta,
-                            const float* lam, const float* log_alpha,
+                            const float* lam, float lam_scalar, const float* log_alpha,
                             const float* initial_state, const void* saved,
                             const void* d_o, const float* d_final_state, void* dq, void* dk,
                             void* dv, float* dbeta, float* dlam, float* dlog_alpha,
                             float* d_initial_state, void* ws, size_t ws_bytes,
                             hipStream_t stream) {
-  return bwd_impl(true, 1, T, N, cu_seqlens, H, Dk, Dv, chunk, dtype, q, k, v, beta, lam,
+  return bwd_impl(true, 1, T, N, cu_seqlens, H, Dk, Dv, chunk, dtype, q, k, v, beta, lam, lam_scalar,
                   log_alpha, initial_state, saved, d_o, d_final_state, dq, dk, dv, dbeta,
                   dlam, dlog_alpha, d_initial_state, ws, ws_bytes, stream);
 }
 
 static int rec_fwd_impl(bool varlen, int32_t B, int32_t T, int32_t N, const int32_t* cu, int32_t H,
                  int32_t Dk, int32_t Dv, int32_t dtype, const void* q, const void* k,
-                 const void* v, const float* beta, const float* lam, const float* log_alpha,
+                 const void* v, const float* beta, const float* lam, float lam_c, const float* log_alpha,
                  const float* initial_state, void* o, float* final_state, hipStream_t stream) {
   if (T < 0 || H <= 0) return QDELTA_EINVAL;
   if (varlen ? (N < 0 || cu == nullptr) : B < 0) return QDELTA_EINVAL;
@@ -453,26 +466,26 @@ static int rec_fwd_impl(bool varlen, int32_t B, int32_t T, int32_t N, const int3
     return QDELTA_EINVAL;
   if (n_seqs == 0) return QDELTA_OK;
   hipError_t e = qd::launch_rec_fwd(n_seqs, varlen ? 0 : T, varlen ? cu : nullptr, (int)tokens, H,
-                                    Dk, Dv, dtype, q, k, v, beta, lam, log_alpha, initial_state,
+                                    Dk, Dv, dtype, q, k, v, beta, lam, lam_c, log_alpha, initial_state,
                                     final_state, o, stream);
   return e == hipSuccess ? QDELTA_OK : QDELTA_EHIP;
 }
 
 int qdelta_recurrent_fwd(int32_t B, int32_t T, int32_t H, int32_t Dk, int32_t Dv, int32_t dtype,
                          const void* q, const void* k, const void* v, const float* beta,
-                         const float* lam, const float* log_alpha, const float* initial_state,
-                         void* o, float* final_state, hipStream_t stream) {
-  return rec_fwd_impl(false, B, T, B, nullptr, H, Dk, Dv, dtype, q, k, v, beta, lam, log_alpha,
+                         const float* lam, float lam_scalar, const float* log_alpha,
+                         const float* initial_state, void* o, float* final_state, hipStream_t stream) {
+  return rec_fwd_impl(false, B, T, B, nullptr, H, Dk, Dv, dtype, q, k, v, beta, lam, lam_scalar, log_alpha,
                       initial_state, o, final_state, stream);
 }
 
 int qdelta_recurrent_fwd_varlen(int32_t T, int32_t N, const int32_t* cu_seqlens, int32_t H,
                                 int32_t Dk, int32_t Dv, int32_t dtype, const void* q,
                                 const void* k, const void* v, const float* beta,
-                                const float* lam, const float* log_alpha,
+                                const float* lam, float lam_scalar, const float* log_alpha,
                                 const float* initial_state, void* o, float* final_state,
                                 hipStream_t stream) {
-  return rec_fwd_impl(true, 1, T, N, cu_seqlens, H, Dk, Dv, dtype, q, k, v, beta, lam,
+  return rec_fwd_impl(true, 1, T, N, cu_seqlens, H, Dk, Dv, dtype, q, k, v, beta, lam, lam_scalar,
                       log_alpha, initial_state, o, final_state, stream);
 }
 
@@ -505,8 +518,8 @@ int qdelta_l2norm_bwd(int64_t rows, int32_t D, int32_t dtype, const void* y, con
 
 int qdelta_recurrent_step(int32_t N, int32_t H, int32_t Dk, int32_t Dv, int32_t dtype,
                           const void* q, const void* k, const void* v, const float* beta,
-                          const float* lam, const float* log_alpha, float* state, void* o,
-                          hipStream_t stream) {
+                          const float* lam, float lam_scalar, const float* log_alpha, float* state,
+                          void* o, hipStream_t stream) {
   if (N < 0 || H <= 0) return QDELTA_EINVAL;
   if (dtype != QDELTA_F32 && dtype != QDELTA_BF16) return QDELTA_EINVAL;
   if ((Dk != 64 && Dk != 128) || Dv <= 0 || Dv > 256 || (Dv % 8) != 0) return QDELTA_EUNSUPPORTED;
@@ -515,7 +528,8 @@ int qdelta_recurrent_step(int32_t N, int32_t H, int32_t Dk, int32_t Dv, int32_t 
   if (!(ok_ptr(q) && ok_ptr(k) && ok_ptr(v) && ok_ptr(beta) && ok_ptr(state) && ok_ptr(o) &&
         ok_opt(lam) && ok_opt(log_alpha)))
     return QDELTA_EINVAL;
-  hipError_t e = qd::launch_step(N, H, Dk, Dv, dtype, q, k, v, beta, lam, log_alpha, state, o, stream);
+  hipError_t e = qd::launch_step(N, H, Dk, Dv, dtype, q, k, v, beta, lam, lam_scalar, log_alpha, state, o,
+                                 stream);
   return e == hipSuccess ? QDELTA_OK : QDELTA_EHIP;
 }
 

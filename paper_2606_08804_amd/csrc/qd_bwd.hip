@@ -848,7 +848,38 @@ __global__ __launch_bounds__(INTRA_THREADS) __attribute__((amdgpu_waves_per_eu(2
       if (p.dlam) p.dlam[gt] = sm.rdl[j];
       if (p.dla) p.dla[gt] = suffix;
     }
+    if (p.w_dlam) {
+      // constant lambda: this unit's share of its gradient
+      const float part = wave_sum(j < len ? sm.rdl[j] : 0.f);
+      if (j == 0) p.w_dlam[gi] = part;
+    }
   }
+}
+
+// Gradient of a constant lambda: the sum of the per-unit partials of every
+// unit a chunk maps to, in a fixed order (one workgroup: strided per-thread
+// sums, then a tree), so the result is the same on every run.
+__global__ __launch_bounds__(NTHREADS) void k_sum_units(Params p) {
+  __shared__ float part[NTHREADS];
+  const int tid = threadIdx.x;
+  const int total = p.n_slots * p.H;
+  float acc = 0.f;
+  for (int u = tid; u < total; u += NTHREADS) {
+    int n, t0, len;
+    if (locate(p, u / p.H, n, t0, len)) acc += p.w_dlam[u];
+  }
+  part[tid] = acc;
+  __syncthreads();
+#pragma unroll
+  for (int off = NTHREADS / 2; off >= 1; off >>= 1) {
+    if (tid < off) part[tid] += part[tid + off];
+    __syncthreads();
+  }
+  if (tid == 0) *p.dlam_sum = part[0];
+}
+
+__global__ void k_zero1(float* x) {
+  if (threadIdx.x == 0) *x = 0.f;
 }
 
 // ------------------------------------------------------------------ launchers
@@ -882,6 +913,15 @@ static hipError_t launch_bwd_t(const Params& p, hipStream_t st) {
     hipLaunchKernelGGL((k_bwd_intra<E, DK, DV>), dim3(total + q.lead), dim3(INTRA_THREADS), 0, st, q);
     prof_mark(ST_INTRA, 1, st);
   }
+  if (p.dlam_sum) {
+    if (p.n_slots > 0) hipLaunchKernelGGL(k_sum_units, dim3(1), dim3(NTHREADS), 0, st, p);
+    else hipLaunchKernelGGL(k_zero1, dim3(1), dim3(64), 0, st, p.dlam_sum);
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_zero(float* x, hipStream_t st) {
+  hipLaunchKernelGGL(k_zero1, dim3(1), dim3(64), 0, st, x);
   return hipGetLastError();
 }
 

@@ -611,7 +611,8 @@ struct Params {
   const void* k;
   const void* v;
   const float* beta;
-  const float* lam;
+  const float* lam;      // per token and head, or nullptr: lambda == lam_c everywhere
+  float lam_c;
   const float* la;       // log alpha or nullptr
   const float* S0;       // initial state or nullptr
   // forward outputs
@@ -633,7 +634,9 @@ struct Params {
   void* dk;
   void* dv;
   float* dbeta;
-  float* dlam;
+  float* dlam;           // per token and head (lam given), else nullptr
+  float* dlam_sum;       // one float: gradient of the constant lambda (lam == nullptr), or nullptr
+  float* w_dlam;         // [slot][H] per-unit partial sums of the constant-lambda gradient
   float* dla;
   float* dS0;
   void* w_dSo;           // [slot][H][Dv][Dk] gradient w.r.t. each chunk's exit state (dtype)

@@ -94,7 +94,7 @@ __global__ __launch_bounds__(PREP_THREADS) void k_prep(Params p) {
       const size_t gt = row + (size_t)tid * H;
       x.la = (ok && p.la) ? p.la[gt] : 0.f;
       x.beta = ok ? p.beta[gt] : 0.f;
-      x.lam = (ok && p.lam) ? p.lam[gt] : 0.f;   // NULL: lambda == 0
+      x.lam = ok ? (p.lam ? p.lam[gt] : p.lam_c) : 0.f;   // NULL: the constant lambda
     }
   };
 

@@ -33,17 +33,20 @@ hipError_t launch_fwd(const Params& p, int dtype, int Dk, int Dv, int in_bwd, in
 // reverse state scan, then the intra-chunk gradient kernel.
 hipError_t launch_bwd(const Params& p, int dtype, int Dk, int Dv, hipStream_t st);
 
+// Writes 0 to one device float (a gradient with nothing to sum).
+hipError_t launch_zero(float* x, hipStream_t st);
+
 // One token of the recurrence for N sequences.
 hipError_t launch_step(int N, int H, int Dk, int Dv, int dtype, const void* q, const void* k,
-                       const void* v, const float* beta, const float* lam, const float* la,
+                       const void* v, const float* beta, const float* lam, float lam_c, const float* la,
                        float* state, void* o, hipStream_t st);
 
 // Fully recurrent forward over whole sequences: dense (cu == nullptr, N
 // sequences of T tokens) or packed (cu[N+1] on the device, T_total tokens).
 hipError_t launch_rec_fwd(int N, int T, const int* cu, int T_total, int H, int Dk, int Dv,
                           int dtype, const void* q, const void* k, const void* v,
-                          const float* beta, const float* lam, const float* la, const float* S0,
-                          float* Sfin, void* o, hipStream_t st);
+                          const float* beta, const float* lam, float lam_c, const float* la,
+                          const float* S0, float* Sfin, void* o, hipStream_t st);
 
 // Row L2 normalisation (bwd == 0: x -> out, rn_out) or its backward
 // (bwd == 1: y, rn_in, dy -> out).

@@ -32,7 +32,7 @@ template <typename E, int DK>
 __global__ __launch_bounds__(NTHREADS) void k_step(int DV, int nrb, const E* __restrict__ q,
                                                   const E* __restrict__ k, const E* __restrict__ v,
                                                   const float* __restrict__ beta,
-                                                  const float* __restrict__ lam,
+                                                  const float* __restrict__ lam, float lam_c,
                                                   const float* __restrict__ la, float* __restrict__ S,
                                                   E* __restrict__ o) {
   constexpr int LPR = DK / 4;            // lanes per state row
@@ -49,7 +49,7 @@ __global__ __launch_bounds__(NTHREADS) void k_step(int DV, int nrb, const E* __r
     qv[j] = tof(q[u * DK + c0 + j]);
     kv[j] = tof(k[u * DK + c0 + j]);
   }
-  const float lm = lam ? lam[u] : 0.f, bt = beta[u];
+  const float lm = lam ? lam[u] : lam_c, bt = beta[u];
   const float al = la ? __expf(la[u]) : 1.f;
   float xv[4];
 #pragma unroll
@@ -96,7 +96,7 @@ __global__ __launch_bounds__(NTHREADS) void k_step(int DV, int nrb, const E* __r
 }
 
 hipError_t launch_step(int N, int H, int Dk, int Dv, int dtype, const void* q, const void* k,
-                       const void* v, const float* beta, const float* lam, const float* la,
+                       const void* v, const float* beta, const float* lam, float lam_c, const float* la,
                        float* state, void* o, hipStream_t st) {
   if (N == 0) return hipSuccess;
   const int RPB = NTHREADS / (Dk / 4) * STEP_RPT;   // state rows per workgroup
@@ -104,7 +104,7 @@ hipError_t launch_step(int N, int H, int Dk, int Dv, int dtype, const void* q, c
   dim3 grid((unsigned)((size_t)N * H * nrb));
 #define QD_STEP(ET, DKV)                                                                        \
   hipLaunchKernelGGL((k_step<ET, DKV>), grid, dim3(NTHREADS), 0, st, Dv, nrb, (const ET*)q,     \
-                     (const ET*)k, (const ET*)v, beta, lam, la, state, (ET*)o)
+                     (const ET*)k, (const ET*)v, beta, lam, lam_c, la, state, (ET*)o)
   if (!((dtype == 1 || dtype == 0) && (Dk == 128 || Dk == 64))) return hipErrorInvalidValue;
   prof_mark(ST_STEP, 0, st);
   if (dtype == 1 && Dk == 128) QD_STEP(__bf16, 128);
@@ -151,7 +151,7 @@ template <typename E, int DK, int RPT, int NT>
 __global__ __launch_bounds__(NT) void k_rec_fwd(
     int T, int H, int DV, int nrb, const int* __restrict__ cu, int T_total, const E* __restrict__ q,
     const E* __restrict__ k, const E* __restrict__ v, const float* __restrict__ beta,
-    const float* __restrict__ lam, const float* __restrict__ la, const float* __restrict__ S0,
+    const float* __restrict__ lam, float lam_c, const float* __restrict__ la, const float* __restrict__ S0,
     float* __restrict__ Sfin, E* __restrict__ o) {
   constexpr int LPR = 8;                       // lanes per state row (group8_sum)
   constexpr int CPL = DK / LPR;                // columns per lane
@@ -224,6 +224,7 @@ __global__ __launch_bounds__(NT) void k_rec_fwd(
       const int which = tid / TB, t = tb + tid % TB;
       const float* src = which == 0 ? beta : which == 1 ? lam : la;
       if (src && t < t1) rg = src[(size_t)t * H + h];
+      else if (which == 1 && t < t1) rg = lam_c;           // constant lambda
     }
   };
   auto store_block = [&](int buf) {
@@ -351,8 +352,8 @@ __global__ __launch_bounds__(NT) void k_rec_fwd(
 
 hipError_t launch_rec_fwd(int N, int T, const int* cu, int T_total, int H, int Dk, int Dv,
                           int dtype, const void* q, const void* k, const void* v,
-                          const float* beta, const float* lam, const float* la, const float* S0,
-                          float* Sfin, void* o, hipStream_t st) {
+                          const float* beta, const float* lam, float lam_c, const float* la,
+                          const float* S0, float* Sfin, void* o, hipStream_t st) {
   if (N == 0) return hipSuccess;
   if (!((dtype == 1 || dtype == 0) && (Dk == 128 || Dk == 64))) return hipErrorInvalidValue;
   // 128 threads = 16 lane groups; up to eight rows per group, so one
@@ -364,8 +365,8 @@ hipError_t launch_rec_fwd(int N, int T, const int* cu, int T_total, int H, int D
   dim3 grid((unsigned)((size_t)N * H * nrb));
 #define QD_REC(ET, DKV, RPTV)                                                                   \
   hipLaunchKernelGGL((k_rec_fwd<ET, DKV, RPTV, NT>), grid, dim3(NT), 0, st, T, H, Dv, nrb, cu, \
-                     T_total, (const ET*)q, (const ET*)k, (const ET*)v, beta, lam, la, S0,     \
-                     Sfin, (ET*)o)
+                     T_total, (const ET*)q, (const ET*)k, (const ET*)v, beta, lam, lam_c, la,  \
+                     S0, Sfin, (ET*)o)
 #define QD_REC_R(ET, DKV)                                                    \
   if (rpt == 8) QD_REC(ET, DKV, 8); else if (rpt == 4) QD_REC(ET, DKV, 4);   \
   else if (rpt == 2) QD_REC(ET, DKV, 2); else QD_REC(ET, DKV, 1)

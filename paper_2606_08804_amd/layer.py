@@ -30,7 +30,8 @@ from . import qdelta as _binding
 
 class QDeltaFunction(torch.autograd.Function):
     """Autograd wrapper of the chunkwise forward (Sec. 3.3) and its exact
-    backward.  ``None`` for lam or log_alpha selects lambda == 0 or alpha == 1."""
+    backward.  lam is a per-token tensor, a number (one constant lambda, no
+    gradient taken) or None (lambda == 0); log_alpha None means alpha == 1."""
 
     @staticmethod
     def forward(ctx, q, k, v, beta, lam, log_alpha, initial_state, cu_seqlens):
@@ -38,12 +39,17 @@ class QDeltaFunction(torch.autograd.Function):
         o, final_state, saved = _binding.chunk_fwd(
             q, k, v, beta, lam, log_alpha, initial_state, cu_seqlens=cu_seqlens,
             output_final_state=True, save_states=need)
-        ctx.save_for_backward(q, k, v, beta, lam, log_alpha, initial_state, cu_seqlens, saved)
+        ctx.lam_const = None if isinstance(lam, torch.Tensor) else lam
+        lam_t = lam if isinstance(lam, torch.Tensor) else None
+        ctx.save_for_backward(q, k, v, beta, lam_t, log_alpha, initial_state, cu_seqlens, saved)
         return o, final_state
 
     @staticmethod
     def backward(ctx, d_o, d_final_state):
-        q, k, v, beta, lam, log_alpha, initial_state, cu_seqlens, saved = ctx.saved_tensors
+        q, k, v, beta, lam_t, log_alpha, initial_state, cu_seqlens, saved = ctx.saved_tensors
+        # a constant lambda is not differentiated here: passing it as None
+        # would mean lambda == 0, so hand the number over and drop its gradient
+        lam = lam_t if lam_t is not None else ctx.lam_const
         if d_o is None:
             d_o = torch.zeros(v.shape, dtype=v.dtype, device=v.device)
         dSf = None if d_final_state is None else d_final_state.contiguous()
@@ -51,7 +57,8 @@ class QDeltaFunction(torch.autograd.Function):
         g = _binding.chunk_bwd(q, k, v, beta, lam, log_alpha, initial_state, saved,
                                d_o.contiguous(), d_final_state=dSf, cu_seqlens=cu_seqlens,
                                need_d_initial_state=need_dS0)
-        return (g["dq"], g["dk"], g["dv"], g["dbeta"], g["dlam"], g["dlog_alpha"],
+        dlam = g["dlam"] if lam_t is not None else None
+        return (g["dq"], g["dk"], g["dv"], g["dbeta"], dlam, g["dlog_alpha"],
                 g["d_initial_state"], None)
 
 
@@ -88,8 +95,9 @@ class QDeltaLayer(torch.nn.Module):
                  lambda_bias=-0.8, fixed_lambda=None):
         """fixed_lambda: None for the learned gate lambda_t = sigmoid(W h + b);
         a number for a constant lambda (the paper's ablations: scalar 0.2, 0.5,
-        0.8, and 1.0 for "no gating"); 0 gives the gated delta rule (lambda is
-        passed as NULL).  use_decay=False gives alpha == 1 ("no state decay")."""
+        0.8, and 1.0 for "no gating"), handed to the kernels as a scalar, so no
+        lambda tensor is formed or read; 0 gives the gated delta rule.
+        use_decay=False gives alpha == 1 ("no state decay")."""
         super().__init__()
         self.d_model, self.H, self.dk, self.dv = d_model, n_heads, head_dk, head_dv
         self.use_decay, self.qk_norm = use_decay, qk_norm
@@ -108,8 +116,8 @@ class QDeltaLayer(torch.nn.Module):
             torch.nn.init.normal_(lin.weight, std=1.0 / math.sqrt(lin.in_features))
 
     def gates(self, h):
-        """beta, lambda, log alpha ([..., H] fp32 or wider; lambda None when
-        fixed at 0, log alpha None without decay)."""
+        """beta, lambda, log alpha ([..., H] fp32 or wider; lambda a number
+        when fixed, log alpha None without decay)."""
         acc = torch.promote_types(h.dtype, torch.float32)
         g = self.w_gates(h).to(acc)
         H = self.H
@@ -118,10 +126,8 @@ class QDeltaLayer(torch.nn.Module):
         if self.fixed_lambda is None:
             lam = torch.sigmoid(g[..., H:2 * H] + self.lambda_bias.to(acc))
             nxt = 2 * H
-        elif self.fixed_lambda == 0.0:
-            lam = None
         else:
-            lam = torch.full_like(beta, self.fixed_lambda)
+            lam = self.fixed_lambda
         log_alpha = F.logsigmoid(g[..., nxt:]) if self.use_decay else None
         return beta, lam, log_alpha
 
@@ -135,7 +141,7 @@ class QDeltaLayer(torch.nn.Module):
             k = L2NormFunction.apply(k)
         beta, lam, log_alpha = self.gates(h)
         o, final_state = qdelta_chunk(q.contiguous(), k.contiguous(), v.contiguous(),
-                                      beta.contiguous(), None if lam is None else lam.contiguous(),
+                                      beta.contiguous(), lam.contiguous() if isinstance(lam, torch.Tensor) else lam,
                                       None if log_alpha is None else log_alpha.contiguous(),
                                       initial_state, cu_seqlens)
         y = self.w_out(o.reshape(B, T, H * dv))

@@ -18,7 +18,9 @@ recurrent_fwd(q, k, v, beta, lam=None, log_alpha=None, initial_state=None, cu_se
           -> (o, final_state)                                  (token by token, one launch)
 l2norm_fwd(x) -> (y, rnorm);  l2norm_bwd(y, rnorm, dy) -> dx   (row L2 norm for the layer's q, k)
 
-lam=None means lambda == 0 (the gated delta rule); log_alpha=None means alpha == 1.
+lam: a [.., H] fp32 tensor (per token and head), a number (one constant for every
+token and head: the paper's fixed-lambda ablations), or None (lambda == 0, the gated
+delta rule); log_alpha=None means alpha == 1.
 """
 import ctypes
 import os
@@ -71,21 +73,23 @@ def lib():
         L.qdelta_saved_bytes.restype = sz
         L.qdelta_chunk_workspace_bytes.argtypes = [i32] * 9
         L.qdelta_chunk_workspace_bytes.restype = sz
-        L.qdelta_chunk_fwd.argtypes = [i32] * 7 + [P] * 10 + [P, sz, P]
+        f32 = ctypes.c_float
+        # gate arguments: beta, lam, lam_scalar, log_alpha
+        L.qdelta_chunk_fwd.argtypes = [i32] * 7 + [P] * 5 + [f32] + [P] * 5 + [P, sz, P]
         L.qdelta_chunk_fwd.restype = ctypes.c_int
-        L.qdelta_chunk_fwd_noalloc.argtypes = [i32] * 7 + [P] * 9 + [P]
+        L.qdelta_chunk_fwd_noalloc.argtypes = [i32] * 7 + [P] * 5 + [f32] + [P] * 4 + [P]
         L.qdelta_chunk_fwd_noalloc.restype = ctypes.c_int
-        L.qdelta_chunk_fwd_varlen.argtypes = [i32, i32, P] + [i32] * 5 + [P] * 10 + [P, sz, P]
+        L.qdelta_chunk_fwd_varlen.argtypes = [i32, i32, P] + [i32] * 5 + [P] * 5 + [f32] + [P] * 5 + [P, sz, P]
         L.qdelta_chunk_fwd_varlen.restype = ctypes.c_int
-        L.qdelta_chunk_bwd.argtypes = [i32] * 7 + [P] * 17 + [P, sz, P]
+        L.qdelta_chunk_bwd.argtypes = [i32] * 7 + [P] * 5 + [f32] + [P] * 12 + [P, sz, P]
         L.qdelta_chunk_bwd.restype = ctypes.c_int
-        L.qdelta_chunk_bwd_varlen.argtypes = [i32, i32, P] + [i32] * 5 + [P] * 17 + [P, sz, P]
+        L.qdelta_chunk_bwd_varlen.argtypes = [i32, i32, P] + [i32] * 5 + [P] * 5 + [f32] + [P] * 12 + [P, sz, P]
         L.qdelta_chunk_bwd_varlen.restype = ctypes.c_int
-        L.qdelta_recurrent_step.argtypes = [i32] * 5 + [P] * 8 + [P]
+        L.qdelta_recurrent_step.argtypes = [i32] * 5 + [P] * 5 + [f32] + [P] * 3 + [P]
         L.qdelta_recurrent_step.restype = ctypes.c_int
-        L.qdelta_recurrent_fwd.argtypes = [i32] * 6 + [P] * 9 + [P]
+        L.qdelta_recurrent_fwd.argtypes = [i32] * 6 + [P] * 5 + [f32] + [P] * 4 + [P]
         L.qdelta_recurrent_fwd.restype = ctypes.c_int
-        L.qdelta_recurrent_fwd_varlen.argtypes = [i32, i32, P] + [i32] * 4 + [P] * 9 + [P]
+        L.qdelta_recurrent_fwd_varlen.argtypes = [i32, i32, P] + [i32] * 4 + [P] * 5 + [f32] + [P] * 4 + [P]
         L.qdelta_recurrent_fwd_varlen.restype = ctypes.c_int
         i64 = ctypes.c_int64
         L.qdelta_l2norm_fwd.argtypes = [i64, i32, i64, i32, P, P, P, P]
@@ -132,6 +136,17 @@ def _need(t, name, dtype=None, shape=None):
 
 def _opt(t, name, dtype=None, shape=None):
     return None if t is None else _need(t, name, dtype, shape)
+
+
+def _lam(lam, shape):
+    """lambda as (tensor or None, constant): a tensor is per token and head;
+    None or a number is one constant for every token and head (None = 0,
+    the gated delta rule)."""
+    if lam is None:
+        return None, 0.0
+    if isinstance(lam, (int, float)):
+        return None, float(lam)
+    return _need(lam, "lam", torch.float32, shape), 0.0
 
 
 def _check(fn, status):
@@ -189,7 +204,7 @@ def chunk_fwd(q, k, v, beta, lam, log_alpha=None, initial_state=None, cu_seqlens
     _need(k, "k", q.dtype, q.shape)
     _need(v, "v", q.dtype, tuple(act) + (Dv,))
     _need(beta, "beta", torch.float32, act)
-    _opt(lam, "lam", torch.float32, act)
+    lam_t, lam_c = _lam(lam, act)
     _opt(log_alpha, "log_alpha", torch.float32, act)
     _opt(initial_state, "initial_state", torch.float32, (N, H, Dv, Dk))
     if cu_seqlens is not None:
@@ -203,7 +218,7 @@ def chunk_fwd(q, k, v, beta, lam, log_alpha=None, initial_state=None, cu_seqlens
         saved = torch.empty(saved_bytes(B, T, H, Dk, Dv, dt, n_seqs), dtype=torch.uint8, device=dev)
     nbytes = workspace_bytes(B, T, H, Dk, Dv, dt, n_seqs, False)
     ws = _workspace(nbytes, dev, workspace)
-    common = (H, Dk, Dv, CHUNK, dt, _p(q), _p(k), _p(v), _p(beta), _p(lam), _p(log_alpha),
+    common = (H, Dk, Dv, CHUNK, dt, _p(q), _p(k), _p(v), _p(beta), _p(lam_t), lam_c, _p(log_alpha),
               _p(initial_state), _p(o), _p(Sf), _p(saved), _p(ws), nbytes, _stream())
     if cu_seqlens is None:
         _check("qdelta_chunk_fwd", L.qdelta_chunk_fwd(B, T, *common))
@@ -226,7 +241,7 @@ def chunk_fwd_noalloc(q, k, v, beta, lam, log_alpha=None, initial_state=None, ou
     _need(k, "k", q.dtype, q.shape)
     _need(v, "v", q.dtype, tuple(act) + (Dv,))
     _need(beta, "beta", torch.float32, act)
-    _opt(lam, "lam", torch.float32, act)
+    lam_t, lam_c = _lam(lam, act)
     _opt(log_alpha, "log_alpha", torch.float32, act)
     _opt(initial_state, "initial_state", torch.float32, (N, H, Dv, Dk))
     o = out if out is not None else torch.empty(tuple(act) + (Dv,), dtype=q.dtype, device=q.device)
@@ -236,16 +251,17 @@ def chunk_fwd_noalloc(q, k, v, beta, lam, log_alpha=None, initial_state=None, ou
         Sf = torch.empty((N, H, Dv, Dk), dtype=torch.float32, device=q.device)
     _opt(Sf, "final_state_out", torch.float32, (N, H, Dv, Dk))
     _check("qdelta_chunk_fwd_noalloc",
-           L.qdelta_chunk_fwd_noalloc(B, T, H, Dk, Dv, CHUNK, dt, _p(q), _p(k), _p(v), _p(beta), _p(lam),
-                                      _p(log_alpha), _p(initial_state), _p(o), _p(Sf), _stream()))
+           L.qdelta_chunk_fwd_noalloc(B, T, H, Dk, Dv, CHUNK, dt, _p(q), _p(k), _p(v), _p(beta), _p(lam_t),
+                                      lam_c, _p(log_alpha), _p(initial_state), _p(o), _p(Sf), _stream()))
     return o, Sf
 
 
 def chunk_bwd(q, k, v, beta, lam, log_alpha, initial_state, saved_states, d_o,
               d_final_state=None, cu_seqlens=None, need_d_initial_state=True, workspace=None):
     """Chunkwise Q-Delta backward.  Returns a dict: dq, dk, dv, dbeta, dlam
-    (None when lam is None), dlog_alpha (None without decay), d_initial_state
-    (None if not requested)."""
+    (per token for a lam tensor; a 0-dim tensor, the gradient of the
+    constant, when lam is a number; None when lam is None), dlog_alpha (None
+    without decay), d_initial_state (None if not requested)."""
     L = lib()
     dt = _dt(q)
     B, T, H, Dk, Dv, N = _dims(q, v, cu_seqlens)
@@ -254,7 +270,7 @@ def chunk_bwd(q, k, v, beta, lam, log_alpha, initial_state, saved_states, d_o,
     _need(k, "k", q.dtype, q.shape)
     _need(v, "v", q.dtype, tuple(act) + (Dv,))
     _need(beta, "beta", torch.float32, act)
-    _opt(lam, "lam", torch.float32, act)
+    lam_t, lam_c = _lam(lam, act)
     _opt(log_alpha, "log_alpha", torch.float32, act)
     _opt(initial_state, "initial_state", torch.float32, (N, H, Dv, Dk))
     _opt(saved_states, "saved_states")
@@ -272,12 +288,17 @@ def chunk_bwd(q, k, v, beta, lam, log_alpha, initial_state, saved_states, d_o,
     dk = torch.empty_like(k)
     dv = torch.empty_like(v)
     dbeta = torch.empty_like(beta)
-    dlam = torch.empty_like(lam) if lam is not None else None
+    if lam_t is not None:
+        dlam = torch.empty_like(lam_t)
+    elif lam is not None:
+        dlam = torch.empty((), dtype=torch.float32, device=dev)
+    else:
+        dlam = None
     dla = torch.empty_like(log_alpha) if log_alpha is not None else None
     dS0 = torch.empty((N, H, Dv, Dk), dtype=torch.float32, device=dev) if need_d_initial_state else None
     nbytes = workspace_bytes(B, T, H, Dk, Dv, dt, n_seqs, True)
     ws = _workspace(nbytes, dev, workspace)
-    common = (H, Dk, Dv, CHUNK, dt, _p(q), _p(k), _p(v), _p(beta), _p(lam), _p(log_alpha),
+    common = (H, Dk, Dv, CHUNK, dt, _p(q), _p(k), _p(v), _p(beta), _p(lam_t), lam_c, _p(log_alpha),
               _p(initial_state), _p(saved_states), _p(d_o), _p(d_final_state), _p(dq), _p(dk),
               _p(dv), _p(dbeta), _p(dlam), _p(dla), _p(dS0), _p(ws), nbytes, _stream())
     if cu_seqlens is None:
@@ -298,13 +319,13 @@ def recurrent_step(q, k, v, beta, lam, log_alpha, state, out=None):
     _need(k, "k", q.dtype, q.shape)
     _need(v, "v", q.dtype, (N, H, Dv))
     _need(beta, "beta", torch.float32, (N, H))
-    _opt(lam, "lam", torch.float32, (N, H))
+    lam_t, lam_c = _lam(lam, (N, H))
     _opt(log_alpha, "log_alpha", torch.float32, (N, H))
     _need(state, "state", torch.float32, (N, H, Dv, Dk))
     o = out if out is not None else torch.empty((N, H, Dv), dtype=q.dtype, device=q.device)
     _need(o, "out", q.dtype, (N, H, Dv))
     _check("qdelta_recurrent_step",
-           L.qdelta_recurrent_step(N, H, Dk, Dv, dt, _p(q), _p(k), _p(v), _p(beta), _p(lam),
+           L.qdelta_recurrent_step(N, H, Dk, Dv, dt, _p(q), _p(k), _p(v), _p(beta), _p(lam_t), lam_c,
                                    _p(log_alpha), _p(state), _p(o), _stream()))
     return o
 
@@ -321,14 +342,14 @@ def recurrent_fwd(q, k, v, beta, lam=None, log_alpha=None, initial_state=None, c
     _need(k, "k", q.dtype, q.shape)
     _need(v, "v", q.dtype, tuple(act) + (Dv,))
     _need(beta, "beta", torch.float32, act)
-    _opt(lam, "lam", torch.float32, act)
+    lam_t, lam_c = _lam(lam, act)
     _opt(log_alpha, "log_alpha", torch.float32, act)
     _opt(initial_state, "initial_state", torch.float32, (N, H, Dv, Dk))
     if cu_seqlens is not None:
         _need(cu_seqlens, "cu_seqlens", torch.int32)
     o = torch.empty(tuple(act) + (Dv,), dtype=q.dtype, device=q.device)
     Sf = torch.empty((N, H, Dv, Dk), dtype=torch.float32, device=q.device) if output_final_state else None
-    common = (H, Dk, Dv, dt, _p(q), _p(k), _p(v), _p(beta), _p(lam), _p(log_alpha),
+    common = (H, Dk, Dv, dt, _p(q), _p(k), _p(v), _p(beta), _p(lam_t), lam_c, _p(log_alpha),
               _p(initial_state), _p(o), _p(Sf), _stream())
     if cu_seqlens is None:
         _check("qdelta_recurrent_fwd", L.qdelta_recurrent_fwd(B, T, *common))

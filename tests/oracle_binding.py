@@ -24,10 +24,20 @@ def _zeros_like_gate(beta):
     return np.zeros(beta.shape)
 
 
+def _lam(lam, beta, cu):
+    """Per-token lambda as an fp64 array: a tensor as is, a number broadcast
+    to every token and head, None as zero."""
+    if lam is None:
+        return _zeros_like_gate(_packed(beta, cu))
+    if isinstance(lam, (int, float)):
+        return np.full(_packed(beta, cu).shape, float(lam))
+    return _packed(lam, cu)
+
+
 def chunk_fwd(q, k, v, beta, lam, log_alpha=None, initial_state=None, cu_seqlens=None,
               output_final_state=True, save_states=False, workspace=None):
     cu = None if cu_seqlens is None else cu_seqlens.cpu().numpy()
-    lam_ = _packed(lam, cu) if lam is not None else _zeros_like_gate(_packed(beta, cu))
+    lam_ = _lam(lam, beta, cu)
     o, Sf = recurrent.fwd(_packed(q, cu), _packed(k, cu), _packed(v, cu), _packed(beta, cu), lam_,
                           _packed(log_alpha, cu), _np(initial_state), cu_seqlens=cu)
     if cu is not None:
@@ -41,18 +51,23 @@ def chunk_fwd(q, k, v, beta, lam, log_alpha=None, initial_state=None, cu_seqlens
 def chunk_bwd(q, k, v, beta, lam, log_alpha, initial_state, saved_states, d_o,
               d_final_state=None, cu_seqlens=None, need_d_initial_state=True, workspace=None):
     cu = None if cu_seqlens is None else cu_seqlens.cpu().numpy()
-    lam_ = _packed(lam, cu) if lam is not None else _zeros_like_gate(_packed(beta, cu))
+    lam_ = _lam(lam, beta, cu)
     g = recurrent.bwd(_packed(q, cu), _packed(k, cu), _packed(v, cu), _packed(beta, cu), lam_,
                       _packed(log_alpha, cu), _np(initial_state), d_o=_packed(d_o, cu),
                       d_final_state=_np(d_final_state), cu_seqlens=cu)
     out = {}
+    if isinstance(lam, (int, float)):
+        # a constant lambda: one gradient, the sum over every token and head
+        g = dict(g, dlam=np.asarray(g["dlam"].sum()))
+        lam = torch.zeros((), dtype=beta.dtype)
     like = dict(dq=q, dk=k, dv=v, dbeta=beta, dlam=lam, dlog_alpha=log_alpha,
                 d_initial_state=initial_state)
     for key, ref in like.items():
         if ref is None or g[key] is None or (key == "d_initial_state" and not need_d_initial_state):
             out[key] = None
             continue
-        a = g[key][None] if (cu is not None and key != "d_initial_state") else g[key]
+        packed_rows = cu is not None and key != "d_initial_state" and np.ndim(g[key]) > 0
+        a = g[key][None] if packed_rows else g[key]
         out[key] = torch.from_numpy(np.ascontiguousarray(a)).to(ref.dtype)
     return out
 

@@ -78,7 +78,7 @@ def _fwd(B=1, T=64, H=1, Dk=64, Dv=64, chunk=64, dtype=1, ptrs=None, ws=FAKE, ws
     if ptrs:
         p.update(ptrs)
     return qdelta.lib().qdelta_chunk_fwd(B, T, H, Dk, Dv, chunk, dtype, p["q"], p["k"], p["v"],
-                                         p["beta"], p["lam"], p["la"], p["s0"], p["o"], p["sf"],
+                                         p["beta"], p["lam"], 0.0, p["la"], p["s0"], p["o"], p["sf"],
                                          p["sv"], ws, ws_bytes, None)
 
 
@@ -108,7 +108,8 @@ def test_noalloc_forward_validates_before_any_device_call():
     f = FAKE
 
     def call(B=1, T=64, H=1, Dk=64, Dv=64, dtype=1, q=f, o=f):
-        return L.qdelta_chunk_fwd_noalloc(B, T, H, Dk, Dv, 64, dtype, q, f, f, f, f, None, None, o, None, None)
+        return L.qdelta_chunk_fwd_noalloc(B, T, H, Dk, Dv, 64, dtype, q, f, f, f, f, 0.0, None, None, o, None,
+                                          None)
 
     assert call(Dk=96) == E.QDELTA_EUNSUPPORTED
     assert call(dtype=0, Dk=128) == E.QDELTA_EUNSUPPORTED
@@ -129,31 +130,52 @@ def test_bwd_and_varlen_reject_bad_arguments():
     E = qdelta
     f = FAKE
     # log_alpha given but dlog_alpha missing
-    rc = L.qdelta_chunk_bwd(1, 64, 1, 64, 64, 64, 1, f, f, f, f, f, f, None, None, f, None, f, f, f, f,
+    rc = L.qdelta_chunk_bwd(1, 64, 1, 64, 64, 64, 1, f, f, f, f, f, 0.0, f, None, None, f, None, f, f, f, f,
                             f, None, None, f, 1 << 40, None)
     assert rc == E.QDELTA_EINVAL
     # too small workspace
-    rc = L.qdelta_chunk_bwd(1, 64, 1, 64, 64, 64, 1, f, f, f, f, f, None, None, None, f, None, f, f, f, f,
+    rc = L.qdelta_chunk_bwd(1, 64, 1, 64, 64, 64, 1, f, f, f, f, f, 0.0, None, None, None, f, None, f, f, f, f,
                             f, None, None, f, 1024, None)
     assert rc == E.QDELTA_ENOWORKSPACE
     # varlen needs cu_seqlens
-    rc = L.qdelta_chunk_fwd_varlen(64, 1, None, 1, 64, 64, 64, 1, f, f, f, f, f, None, None, f, None,
+    rc = L.qdelta_chunk_fwd_varlen(64, 1, None, 1, 64, 64, 64, 1, f, f, f, f, f, 0.0, None, None, f, None,
                                    None, f, 1 << 40, None)
     assert rc == E.QDELTA_EINVAL
-    rc = L.qdelta_chunk_bwd_varlen(64, -1, f, 1, 64, 64, 64, 1, f, f, f, f, f, None, None, None, f, None,
+    rc = L.qdelta_chunk_bwd_varlen(64, -1, f, 1, 64, 64, 64, 1, f, f, f, f, f, 0.0, None, None, None, f, None,
                                    f, f, f, f, f, None, None, f, 1 << 40, None)
     assert rc == E.QDELTA_EINVAL
+
+
+def test_bwd_lambda_gradient_rules():
+    """A per-token lambda needs its per-token gradient; a constant lambda
+    (lam NULL) takes either no gradient or one float (4-byte aligned)."""
+    L = qdelta.lib()
+    E = qdelta
+    f = FAKE
+
+    def bwd(lam, dlam, ws_bytes=1):
+        # the workspace check comes after the argument checks: 1 byte means
+        # "arguments valid" shows as QDELTA_ENOWORKSPACE, with no launch
+        return L.qdelta_chunk_bwd(1, 64, 1, 64, 64, 64, 1, f, f, f, f, lam, 0.5, None, None, None, f, None,
+                                  f, f, f, f, dlam, None, None, f, ws_bytes, None)
+
+    assert bwd(f, None) == E.QDELTA_EINVAL            # per-token lambda without its gradient
+    assert bwd(f, f + 4) == E.QDELTA_EINVAL           # misaligned per-token gradient
+    assert bwd(None, f + 4) == E.QDELTA_ENOWORKSPACE  # one float: 4-byte alignment suffices
+    assert bwd(None, f + 2) == E.QDELTA_EINVAL
+    assert bwd(None, None) == E.QDELTA_ENOWORKSPACE
+    assert bwd(f, f) == E.QDELTA_ENOWORKSPACE
 
 
 def test_recurrent_step_rejects_bad_arguments():
     L = qdelta.lib()
     E = qdelta
     f = FAKE
-    assert L.qdelta_recurrent_step(1, 1, 96, 64, 1, f, f, f, f, f, None, f, f, None) == E.QDELTA_EUNSUPPORTED
-    assert L.qdelta_recurrent_step(1, 1, 64, 12, 1, f, f, f, f, f, None, f, f, None) == E.QDELTA_EUNSUPPORTED
-    assert L.qdelta_recurrent_step(1, 1, 64, 64, 1, f, f, f, f, f, None, f + 4, f, None) == E.QDELTA_EINVAL
-    assert L.qdelta_recurrent_step(1, 0, 64, 64, 1, f, f, f, f, f, None, f, f, None) == E.QDELTA_EINVAL
-    assert L.qdelta_recurrent_step(0, 1, 64, 64, 1, None, None, None, None, None, None, None, None,
+    assert L.qdelta_recurrent_step(1, 1, 96, 64, 1, f, f, f, f, f, 0.0, None, f, f, None) == E.QDELTA_EUNSUPPORTED
+    assert L.qdelta_recurrent_step(1, 1, 64, 12, 1, f, f, f, f, f, 0.0, None, f, f, None) == E.QDELTA_EUNSUPPORTED
+    assert L.qdelta_recurrent_step(1, 1, 64, 64, 1, f, f, f, f, f, 0.0, None, f + 4, f, None) == E.QDELTA_EINVAL
+    assert L.qdelta_recurrent_step(1, 0, 64, 64, 1, f, f, f, f, f, 0.0, None, f, f, None) == E.QDELTA_EINVAL
+    assert L.qdelta_recurrent_step(0, 1, 64, 64, 1, None, None, None, None, None, 0.0, None, None, None,
                                    None) == E.QDELTA_OK
 
 
@@ -163,20 +185,21 @@ def test_recurrent_fwd_rejects_bad_arguments():
     L = qdelta.lib()
     E = qdelta
     f = FAKE
-    args = (f, f, f, f, None, None, None, f, None, None)
+    args = (f, f, f, f, None, 0.0, None, None, f, None, None)
     assert L.qdelta_recurrent_fwd(1, 8, 1, 96, 64, 1, *args) == E.QDELTA_EUNSUPPORTED
     assert L.qdelta_recurrent_fwd(1, 8, 1, 64, 300, 1, *args) == E.QDELTA_EUNSUPPORTED
     assert L.qdelta_recurrent_fwd(1, 8, 1, 64, 64, 7, *args) == E.QDELTA_EINVAL
     assert L.qdelta_recurrent_fwd(1, -1, 1, 64, 64, 1, *args) == E.QDELTA_EINVAL
-    assert L.qdelta_recurrent_fwd(1, 8, 1, 64, 64, 1, f + 4, f, f, f, None, None, None, f, None,
+    assert L.qdelta_recurrent_fwd(1, 8, 1, 64, 64, 1, f + 4, f, f, f, None, 0.0, None, None, f, None,
                                   None) == E.QDELTA_EINVAL
-    assert L.qdelta_recurrent_fwd(1, 8, 1, 64, 64, 1, None, f, f, f, None, None, None, f, None,
+    assert L.qdelta_recurrent_fwd(1, 8, 1, 64, 64, 1, None, f, f, f, None, 0.0, None, None, f, None,
                                   None) == E.QDELTA_EINVAL
-    assert L.qdelta_recurrent_fwd(1, 8, 1, 64, 64, 1, f, f, f, f, f + 8, None, None, f, None,
+    assert L.qdelta_recurrent_fwd(1, 8, 1, 64, 64, 1, f, f, f, f, f + 8, 0.0, None, None, f, None,
                                   None) == E.QDELTA_EINVAL
     # no sequences: nothing to do
-    assert L.qdelta_recurrent_fwd(0, 8, 1, 64, 64, 1, *([None] * 10)) == E.QDELTA_OK
-    assert L.qdelta_recurrent_fwd_varlen(0, 0, f, 1, 64, 64, 1, *([None] * 10)) == E.QDELTA_OK
+    none10 = [None] * 5 + [0.0] + [None] * 5
+    assert L.qdelta_recurrent_fwd(0, 8, 1, 64, 64, 1, *none10) == E.QDELTA_OK
+    assert L.qdelta_recurrent_fwd_varlen(0, 0, f, 1, 64, 64, 1, *none10) == E.QDELTA_OK
     assert L.qdelta_recurrent_fwd_varlen(8, 1, None, 1, 64, 64, 1, *args) == E.QDELTA_EINVAL
 
 

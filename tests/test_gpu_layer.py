@@ -17,7 +17,7 @@ pytestmark = pytest.mark.gpu
 
 
 @pytest.mark.parametrize("use_decay,varlen,fixed_lambda", [(True, False, None), (False, True, None),
-                                                          (True, False, 0.0)])
+                                                          (True, False, 0.0), (True, True, 0.5)])
 def test_layer_matches_oracle_layer(monkeypatch, use_decay, varlen, fixed_lambda):
     torch.manual_seed(41)
     m = layer.QDeltaLayer(d_model=256, n_heads=2, head_dk=128, head_dv=128, use_decay=use_decay,

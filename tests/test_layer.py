@@ -94,14 +94,32 @@ def test_layer_has_no_cpu_path():
 
 
 def test_fixed_lambda_variants():
-    """The paper's ablations as layer settings: a constant lambda is passed as
-    a filled tensor, lambda = 0 as NULL (the gated delta rule), and no decay
-    as a NULL log alpha; the gate projection has one block per learned gate."""
+    """The paper's ablations as layer settings: a constant lambda is handed
+    to the kernels as a number (no lambda tensor; 0 is the gated delta rule),
+    and no decay as a NULL log alpha; the gate projection has one block per
+    learned gate."""
     h = torch.randn(1, 3, 8)
     m = layer.QDeltaLayer(d_model=8, n_heads=2, head_dk=4, head_dv=4, fixed_lambda=0.8)
     beta, lam, la = m.gates(h)
-    assert torch.equal(lam, torch.full_like(beta, 0.8)) and la is not None
+    assert lam == 0.8 and isinstance(lam, float) and la is not None
     assert m.w_gates.out_features == 4 and not hasattr(m, "lambda_bias")
     m0 = layer.QDeltaLayer(d_model=8, n_heads=2, head_dk=4, head_dv=4, fixed_lambda=0, use_decay=False)
     beta, lam, la = m0.gates(h)
-    assert lam is None and la is None and m0.w_gates.out_features == 2
+    assert lam == 0.0 and la is None and m0.w_gates.out_features == 2
+
+
+def test_function_constant_lambda_gradcheck(oracle_core):
+    """A constant lambda given as a number: gradients of every tensor input
+    through the autograd function, and equal outputs to the same constant
+    given as a filled tensor."""
+    xs = _inputs(1, 6, 2, 3, 4, seed=5)
+    lam_c = 0.5
+    o_t, S_t = layer.qdelta_chunk(*xs[:4], torch.full_like(xs[3], lam_c), *xs[5:])
+    o_c, S_c = layer.qdelta_chunk(*xs[:4], lam_c, *xs[5:])
+    assert torch.equal(o_t, o_c) and torch.equal(S_t, S_c)
+    ts = [x.requires_grad_() for i, x in enumerate(xs) if i != 4]
+
+    def f(q, k, v, beta, la, S0):
+        return layer.qdelta_chunk(q, k, v, beta, lam_c, la, S0)
+
+    assert torch.autograd.gradcheck(f, ts, eps=1e-6, atol=1e-7, rtol=1e-6)
