@@ -101,6 +101,12 @@ def kernel_alg_bytes_per_token_head(stage, Dk, Dv, e, saved=True):
         return qk + v + gates + v
     if stage == "intra":                    # q, k, v, dO, gates, entry states -> dq, dk, dgates
         return qk + 2 * v + gates + states + qk + gates
+    if stage == "seg_maps":                 # q, k, v, gates (segment maps: hand-offs)
+        return qk + v + gates
+    if stage == "seg_out":                  # q, k, v, gates -> o
+        return qk + v + gates + v
+    if stage == "seg_compose":              # hand-offs only
+        return 0
     raise KeyError(stage)
 
 
@@ -113,6 +119,10 @@ def kernel_state_io_bytes_per_seq(stage, Dk, Dv, has_s0):
     if stage == "scan_fwd":
         return (2 if has_s0 else 1) * st
     if stage == "scan_bwd":
+        return st
+    if stage == "seg_compose":              # reads the initial state
+        return st if has_s0 else 0
+    if stage == "seg_out":                  # writes the final state
         return st
     return 0
 
@@ -139,6 +149,8 @@ def handoff_bytes_per_unit(stage, Dk, Dv, e, saved=True):
     if stage == "intra":         # gate block, S, dS' (dtype), D, dD, dO, v, q, k, M
         #                          -> dq, dk, dbeta, dlam, dlog_alpha
         return 3 * gates + 2 * state * e // 4 + 4 * act_v + 2 * act_qk + cc_e + 2 * act_qk + 3 * gates
+    if stage in ("seg_maps", "seg_out", "seg_compose"):
+        return 0                 # per-segment figures, not per unit
     raise KeyError(stage)
 
 
@@ -369,11 +381,25 @@ def run_chunk(args, wid, with_bwd):
     args_in = (dev["q"], dev["k"], dev["v"], dev["beta"], dev["lam"], dev["log_alpha"], dev["initial_state"])
     last = {}
 
+    # forward-only dense batches run the segment-parallel form when the
+    # library suggests more than one segment (long sequences, few heads)
+    n_seg = 1 if (with_bwd or cu is not None) else qdelta.suggest_segments(B, T, H, Dk, Dv)
+    single_ms = None
     if with_bwd:
         def step():
             o, Sf, saved = qdelta.chunk_fwd(*args_in, cu_seqlens=cu, save_states=True, workspace=wsf)
             g = qdelta.chunk_bwd(*args_in, saved, dev["d_o"], cu_seqlens=cu, workspace=wsb)
             last.update(o=o, final_state=Sf, grads=g)
+    elif n_seg > 1:
+        wss = torch.empty(qdelta.segmented_workspace_bytes(B, T, H, Dk, Dv, dt, n_seg), dtype=torch.uint8,
+                          device="cuda")
+
+        def step():
+            o, Sf, _ = qdelta.chunk_fwd_segmented(*args_in, n_segments=n_seg, workspace=wss)
+            last.update(o=o, final_state=Sf)
+
+        single_ms, _, _ = timed(lambda: qdelta.chunk_fwd(*args_in, save_states=False, workspace=wsf),
+                                args.steps, args.warmup, args.settle_ms)
     else:
         def step():
             o, Sf, _ = qdelta.chunk_fwd(*args_in, cu_seqlens=cu, save_states=False, workspace=wsf)
@@ -403,6 +429,8 @@ def run_chunk(args, wid, with_bwd):
            "gate_mode": args.gate, "parallelism": "single GPU"}
     if n_seqs:
         cfg["n_seqs"] = n_seqs
+    if n_seg > 1:
+        cfg["segments"] = n_seg
     step_traffic = None
     if wid == 3:
         per = [stored_traffic(s) for s in kern]
@@ -413,6 +441,7 @@ def run_chunk(args, wid, with_bwd):
         "warmup": args.warmup, "ms_per_step": ms, "higher_is_better": True, "scaling": "weak",
         "vs_baseline": None, "dtype": w.dtype, "data": "synthetic", "config": cfg,
         "clock_settle_steps": n_settle,
+        "single_pass_ms_per_step": single_ms,
         "mfma_frac_step": th * fl / (ms / 1e3) / peak,
         "step_alg_bytes": {"per_token_head": bpth, "state_io": state_io, "total": int(step_bytes),
                            "GBps": step_bytes / (ms / 1e3) / 1e9,
@@ -596,6 +625,42 @@ def run_decode(args):
     return out
 
 
+def run_segments(args):
+    """The segment-parallel forward against the single pass on long
+    sequences: B=1, T=65536, d=128, bf16, at H = 16 (the long-context
+    workload), 4 and 2, for 1 (the single pass), 2, 4, 8 and 16 segments;
+    `value` is the long-context workload with the library's suggested
+    segment count."""
+    T, d = 65536, 128
+    out_by_H = {}
+    main = None
+    for H in (16, 4, 2):
+        dd = synth.make(1, T, H, d, d, "bf16", args.gate, seed=20260004, s0=True)
+        g = {k: (v.cuda() if isinstance(v, torch.Tensor) else v) for k, v in dd.items()}
+        ins = (g["q"], g["k"], g["v"], g["beta"], g["lam"], g["log_alpha"], g["initial_state"])
+        sugg = qdelta.suggest_segments(1, T, H, d, d)
+        res = {}
+        for G in (1, 2, 4, 8, 16):
+            ws = torch.empty(qdelta.segmented_workspace_bytes(1, T, H, d, d, qdelta.QDELTA_BF16, G),
+                             dtype=torch.uint8, device="cuda")
+            ms, _, _ = timed(lambda: qdelta.chunk_fwd_segmented(*ins, n_segments=G, workspace=ws),
+                             args.steps, args.warmup, args.settle_ms if G == 1 else 0)
+            res[G] = ms
+        out_by_H[H] = {"ms_by_segments": res, "suggested": sugg, "best": min(res, key=res.get)}
+        if H == 16:
+            main = (res[sugg], sugg)
+    ms, sugg = main
+    return {
+        "metric": "Q-Delta chunk fwd tokens/s (B=1,T=65536,H=16,d=128,bf16), suggested segments",
+        "value": T / (ms / 1e3), "unit": "tokens/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": ms, "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": "long-context forward B1 T65536 d128, H 16 / 4 / 2, segment sweep",
+                   "gate_mode": args.gate, "parallelism": "single GPU", "segments_used": sugg},
+        "by_heads": out_by_H,
+    }
+
+
 WORKLOAD_IDS = {"train": 3, "fwd": 2, "long": 4, "varlen": 5, "tiny": 1}
 
 
@@ -607,7 +672,8 @@ def main():
     ap.add_argument("--steps", type=int, default=100)
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--gate", default="G2", choices=["G1", "G2", "G3"])
-    ap.add_argument("--workload", default="train", choices=["train", "fwd", "long", "decode", "varlen", "tiny", "layer", "recurrent"])
+    ap.add_argument("--workload", default="train",
+                    choices=["train", "fwd", "long", "decode", "varlen", "tiny", "layer", "recurrent", "segments"])
     ap.add_argument("--no-cpu", action="store_true",
                     help="skip the CPU oracle baseline (and with it the same-run parity check)")
     ap.add_argument("--settle-ms", type=float, default=200.0,
@@ -631,6 +697,8 @@ def main():
         out = run_layer(args)
     elif args.workload == "recurrent":
         out = run_recurrent(args)
+    elif args.workload == "segments":
+        out = run_segments(args)
     else:
         wid = WORKLOAD_IDS[args.workload]
         out = run_chunk(args, wid, synth.WORKLOADS[wid].bwd)

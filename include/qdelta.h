@@ -139,6 +139,37 @@ int qdelta_chunk_fwd(int32_t B, int32_t T, int32_t H, int32_t Dk, int32_t Dv, in
                      const float* initial_state, void* o, float* final_state,
                      void* saved, void* ws, size_t ws_bytes, hipStream_t stream);
 
+/* Segment-parallel forward (dense batch) for long sequences over few
+ * (sequence, head) pairs, where the single pass's one workgroup per
+ * (sequence, head, value tile) would leave most compute units idle.  Each
+ * chunk acts on the state as an affine map S -> S A_c + B_c (Sec. 3.3, the
+ * compact chunk update S' = S (g_C I - W^T Kbar) + U^T Kbar), so a run of
+ * chunks is one too.  Each sequence is cut into segments of
+ * ceil(ceil(T/chunk) / n_segments) chunks; every segment's map (A: Dk x Dk,
+ * B: Dv x Dk) is formed in parallel from a zero state, the segments' entry
+ * states follow in order (S_{g+1} = S_g A_g + B_g, fp32), and every segment
+ * is then run again from its entry state, writing its outputs.  About three
+ * times the scan work of the single pass (A has Dk rows) for up to
+ * n_segments times its parallelism.
+ *   Arguments as qdelta_chunk_fwd, plus n_segments >= 1 (1: the single
+ *   pass); ws_bytes >= qdelta_segmented_workspace_bytes(..., n_segments).
+ *   Results equal qdelta_chunk_fwd's up to rounding (not bit for bit: the
+ *   entry states come from composed maps). */
+int qdelta_chunk_fwd_segmented(int32_t B, int32_t T, int32_t H, int32_t Dk, int32_t Dv, int32_t chunk,
+                               int32_t dtype, const void* q, const void* k, const void* v,
+                               const float* beta, const float* lam, float lam_scalar,
+                               const float* log_alpha, const float* initial_state, void* o,
+                               float* final_state, void* saved, int32_t n_segments, void* ws,
+                               size_t ws_bytes, hipStream_t stream);
+
+/* Workspace bytes of qdelta_chunk_fwd_segmented (0 for invalid sizes). */
+size_t qdelta_segmented_workspace_bytes(int32_t B, int32_t T, int32_t H, int32_t Dk, int32_t Dv,
+                                        int32_t chunk, int32_t dtype, int32_t n_segments);
+
+/* Segment count that qdelta_chunk_fwd_segmented is expected to run fastest
+ * with on the current device (1: use the single pass).  Host-side only. */
+int32_t qdelta_suggest_segments(int32_t B, int32_t T, int32_t H, int32_t Dk, int32_t Dv);
+
 /* Allocation-free forward, for callers that cannot allocate device memory
  * or hand over a workspace: code under HIP graph capture, tight serving
  * loops, harnesses that forbid allocation.  Same arguments and results as
@@ -262,12 +293,13 @@ int qdelta_l2norm_bwd(int64_t rows, int32_t D, int32_t dtype, const void* y, con
  *   0 chunk preparation (forward)       1 forward state scan + chunk output
  *   2 chunk preparation (backward)      3 backward state scan (+ dv)
  *   4 intra-chunk backward              5 recurrent step
- *   6 recurrent forward
+ *   6 recurrent forward                 7 segment maps (segmented forward)
+ *   8 segment entry states              9 segment outputs
  * qdelta_profile_end() waits for the recorded events, writes the summed kernel
  * time (milliseconds) and the number of launches of each stage into the
  * caller's arrays of QDELTA_N_STAGES entries (either may be NULL) and stops
  * recording.  Returns QDELTA_EHIP if an event call failed. */
-#define QDELTA_N_STAGES 7
+#define QDELTA_N_STAGES 10
 int qdelta_profile_begin(void);
 int qdelta_profile_end(float* ms, int32_t* launches);
 

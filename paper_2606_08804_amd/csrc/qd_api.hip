@@ -62,6 +62,31 @@ Layout make_layout(size_t units, int Dk, int Dv, int esz, bool bwd) {
   return L;
 }
 
+// Segment-parallel forward: the forward layout, then each segment's map
+// (B and A rows, fp32) and each segment's entry state (fp32).
+struct SegLayout {
+  Layout fwd;
+  size_t out = 0, in = 0, total = 0;
+};
+SegLayout make_seg_layout(size_t units, size_t seq_heads, int G, int Dk, int Dv, int esz) {
+  SegLayout S;
+  S.fwd = make_layout(units, Dk, Dv, esz, false);
+  size_t off = S.fwd.total;
+  S.out = off;
+  off += (seq_heads * G * (size_t)(Dv + Dk) * Dk * 4 + 255) & ~size_t(255);
+  S.in = off;
+  off += (seq_heads * G * (size_t)Dv * Dk * 4 + 255) & ~size_t(255);
+  S.total = off;
+  return S;
+}
+
+// Chunks per segment and the number of non-empty segments for n_segments
+// requested over NT chunks.
+void seg_split(int NT, int n_segments, int& L, int& G) {
+  L = NT > 0 ? (NT + n_segments - 1) / n_segments : 1;
+  G = NT > 0 ? (NT + L - 1) / L : 1;
+}
+
 // Points the context fields of p (states, D, gates, P, M) into a context buffer.
 void bind_ctx(qd::Params& p, char* base, size_t units, int Dk, int Dv, int esz) {
   const Ctx c = ctx_layout(units, Dk, Dv, esz);
@@ -398,6 +423,87 @@ int qdelta_chunk_fwd_varlen(int32_t T, int32_t N, const int32_t* cu_seqlens, int
                             void* saved, void* ws, size_t ws_bytes, hipStream_t stream) {
   return fwd_impl(true, 1, T, N, cu_seqlens, H, Dk, Dv, chunk, dtype, q, k, v, beta, lam, lam_scalar,
                   log_alpha, initial_state, o, final_state, saved, ws, ws_bytes, stream);
+}
+
+size_t qdelta_segmented_workspace_bytes(int32_t B, int32_t T, int32_t H, int32_t Dk, int32_t Dv,
+                                        int32_t chunk, int32_t dtype, int32_t n_segments) {
+  if (B < 0 || T < 0 || n_segments < 1) return 0;
+  if (check_dims((int64_t)B * T, H, Dk, Dv, chunk, dtype) != QDELTA_OK) return 0;
+  int L, G;
+  seg_split((T + C - 1) / C, n_segments, L, G);
+  return make_seg_layout(slots_for(B, T, 0) * (size_t)H, (size_t)B * H, G, Dk, Dv,
+                         dtype == QDELTA_BF16 ? 2 : 4).total;
+}
+
+int32_t qdelta_suggest_segments(int32_t B, int32_t T, int32_t H, int32_t Dk, int32_t Dv) {
+  if (B <= 0 || T <= 0 || H <= 0 || Dk <= 0 || Dv <= 0) return 1;
+  const long long cus = qd::device_cu_count();
+  const long long seq_heads = (long long)B * H;
+  const int NT = (T + C - 1) / C;
+  // the single pass runs one workgroup per (sequence, head, 32 value rows);
+  // with half as many of them as CUs or more it is the faster form
+  // (measured at B1 T65536 d128: 16 heads, 64 workgroups, take 1.64 ms in
+  // one pass and 1.30 ms in four segments)
+  if (seq_heads * (Dv / 32) * 2 >= cus) return 1;
+  // the maps pass runs (Dv + Dk) / 32 workgroups per segment: up to two per
+  // CU, with segments of at least 16 chunks
+  int G = 1;
+  while (G < 16 && seq_heads * (2 * G) * ((Dv + Dk) / 32) <= 2 * cus && NT / (2 * G) >= 16) G *= 2;
+  return G;
+}
+
+int qdelta_chunk_fwd_segmented(int32_t B, int32_t T, int32_t H, int32_t Dk, int32_t Dv, int32_t chunk,
+                               int32_t dtype, const void* q, const void* k, const void* v,
+                               const float* beta, const float* lam, float lam_scalar,
+                               const float* log_alpha, const float* initial_state, void* o,
+                               float* final_state, void* saved, int32_t n_segments, void* ws,
+                               size_t ws_bytes, hipStream_t stream) {
+  if (n_segments < 1) return QDELTA_EINVAL;
+  if (n_segments == 1)
+    return fwd_impl(false, B, T, B, nullptr, H, Dk, Dv, chunk, dtype, q, k, v, beta, lam, lam_scalar,
+                    log_alpha, initial_state, o, final_state, saved, ws, ws_bytes, stream);
+  const size_t need = qdelta_segmented_workspace_bytes(B, T, H, Dk, Dv, chunk, dtype, n_segments);
+  // validation of everything else (no device call), with the forward's own workspace
+  int rc = fwd_impl(false, B, T, B, nullptr, H, Dk, Dv, chunk, dtype, q, k, v, beta, lam, lam_scalar,
+                    log_alpha, initial_state, o, final_state, saved, ws, ws_bytes, stream, true);
+  if (rc != QDELTA_OK) return rc;
+  if (ws_bytes < need) return QDELTA_ENOWORKSPACE;
+  if (B == 0) return QDELTA_OK;
+  const int esz = dtype == QDELTA_BF16 ? 2 : 4;
+  const int NT = (T + C - 1) / C;
+  int L, G;
+  seg_split(NT, n_segments, L, G);
+  if (G == 1)    // one segment is the single pass
+    return fwd_impl(false, B, T, B, nullptr, H, Dk, Dv, chunk, dtype, q, k, v, beta, lam, lam_scalar,
+                    log_alpha, initial_state, o, final_state, saved, ws, ws_bytes, stream);
+  const size_t slots = slots_for(B, T, 0), units = slots * (size_t)H;
+  const SegLayout S = make_seg_layout(units, (size_t)B * H, G, Dk, Dv, esz);
+  char* w = static_cast<char*>(ws);
+  qd::Params p{};
+  p.T = T;
+  p.N = B;
+  p.H = H;
+  p.NT = NT;
+  p.n_slots = (int)slots;
+  p.cu = nullptr;
+  p.q = q; p.k = k; p.v = v;
+  p.beta = beta; p.lam = lam; p.lam_c = lam_scalar; p.la = log_alpha; p.S0 = initial_state;
+  p.o = T > 0 ? o : nullptr;
+  p.Sfin = final_state;
+  p.wT = w + S.fwd.wT;
+  if (saved) {
+    bind_ctx(p, static_cast<char*>(saved), units, Dk, Dv, esz);
+  } else {
+    p.wb = reinterpret_cast<float*>(w + S.fwd.wb);
+    p.wP = w + S.fwd.wP;
+    p.wM = nullptr;
+  }
+  p.n_seg = G;
+  p.seg_chunks = L;
+  p.wSegOut = reinterpret_cast<float*>(w + S.out);
+  p.wSegIn = reinterpret_cast<float*>(w + S.in);
+  hipError_t e = qd::launch_fwd_seg(p, dtype, Dk, Dv, stream);
+  return e == hipSuccess ? QDELTA_OK : QDELTA_EHIP;
 }
 
 int qdelta_chunk_fwd_noalloc(int32_t B, int32_t T, int32_t H, int32_t Dk, int32_t Dv, int32_t chunk,

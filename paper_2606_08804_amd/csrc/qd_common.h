@@ -641,6 +641,12 @@ struct Params {
   float* dS0;
   void* w_dSo;           // [slot][H][Dv][Dk] gradient w.r.t. each chunk's exit state (dtype)
   void* w_dDb;           // [slot][H][C][Dv] dD (dtype)
+  // segment-parallel forward (dense batches): each sequence in n_seg
+  // segments of seg_chunks chunks
+  int n_seg;
+  int seg_chunks;
+  float* wSegOut;        // [N*H][n_seg][Dv + Dk][Dk] fp32: each segment's B (value rows) and A (map rows)
+  float* wSegIn;         // [N*H][n_seg][Dv][Dk] fp32: each segment's entry state
 };
 
 // Token range of sequence n; false when cu_seqlens is malformed for n.

@@ -253,7 +253,21 @@ struct alignas(16) ScanFwdSmem {
 // set B of chunk c in phase 2, for P of chunk c in phase 3 and for set A of
 // chunk c+1 in phase 4.  They issue no other memory operations, so their outstanding-load
 // counts are exact.  When p.o is null only the states are produced.
-template <typename E, int DK, int DV, int BV, int NCW>
+//
+// SEG selects the segment-parallel passes over long sequences (each
+// sequence split into p.n_seg segments of p.seg_chunks chunks; a chunk is an
+// affine map S -> S A + B of the state, Sec. 3.3 compact chunk update, and so
+// is a segment):
+//   SEG_NONE  one workgroup walks the whole sequence (the single pass);
+//   SEG_MAPS  per segment from a zero state, no outputs: the value tiles end
+//             at the segment's B, and DK / BV extra tiles whose rows start as
+//             rows of the identity and see no values (their V product is
+//             skipped) end at the rows of its A; both go to p.wSegOut;
+//   SEG_OUT   per segment from its entry state in p.wSegIn, with every
+//             output; the last segment writes the final state.
+enum { SEG_NONE = 0, SEG_MAPS = 1, SEG_OUT = 2 };
+
+template <typename E, int DK, int DV, int BV, int NCW, int SEG>
 __global__ __launch_bounds__(NCW * 64 + 256) void k_scan_fwd(Params p) {
   constexpr int P = Pad<E>::v;
   constexpr int LK = DK + P, LV = BV + P;
@@ -282,14 +296,24 @@ __global__ __launch_bounds__(NCW * 64 + 256) void k_scan_fwd(Params p) {
   const bool producer = prod >= 0;
   const int cb = w & 3, nb0 = (w >> 2) * NBW;
   const int kb0 = (w % (NCW / SG)) * KPW, ns0 = (w / (NCW / SG)) * NBS;
-  int unit, vt;
-  if (!xcd_unit_tile(blockIdx.x, p.N * p.H, NVT, unit, vt)) return;
-  const int H = p.H, n = unit / H, h = unit % H, v0 = vt * BV;
+  constexpr int G = SEG == SEG_NONE ? 1 : 0;          // 0: the run-time segment count
+  const int nseg = G ? G : p.n_seg;
+  constexpr int NTILE = NVT + (SEG == SEG_MAPS ? DK / BV : 0);
+  int su, vt;
+  if (!xcd_unit_tile(blockIdx.x, p.N * p.H * nseg, NTILE, su, vt)) return;
+  const int unit = G ? su : su / nseg, g = G ? 0 : su % nseg;
+  const bool map_tile = SEG == SEG_MAPS && vt >= NVT;  // rows of the segment's A (no values)
+  const int H = p.H, n = unit / H, h = unit % H;
+  const int v0 = map_tile ? 0 : vt * BV;               // V columns read (a map tile's are ignored)
+  const int r0 = vt * BV;                              // first state row (map rows follow the value rows)
   int s, e;
   if (!seq_range(p, n, s, e)) return;
   const int base = slot_base(p, n, s);
-  const int nch = max(0, min((e - s + C - 1) / C, p.n_slots - base));
-  const bool with_o = p.o != nullptr;
+  const int nch_all = max(0, min((e - s + C - 1) / C, p.n_slots - base));
+  const int cbeg = G ? 0 : min(g * p.seg_chunks, nch_all);
+  const int nch = G ? nch_all : min(cbeg + p.seg_chunks, nch_all);   // end of this workgroup's chunks
+  const bool with_o = SEG != SEG_MAPS && p.o != nullptr;
+  void* const saved = SEG == SEG_MAPS ? nullptr : p.saved;
 
   auto chunk_at = [&](int c, size_t& gi, size_t& arow, int& len) {
     const int t0 = s + c * C;
@@ -346,10 +370,21 @@ __global__ __launch_bounds__(NCW * 64 + 256) void k_scan_fwd(Params p) {
 #pragma unroll
     for (int j = 0; j < NBS; ++j) {
       const int kt = kb0 + i, nb = ns0 + j;
-      acc[i][j] = (p.S0 && !producer)
-                      ? *(const f4*)(p.S0 + ((size_t)unit * DV + v0 + nb * 16 + fcol(lane)) * DK + kt * 16 +
-                                     frow(lane, 0))
-                      : zero4();
+      if constexpr (SEG == SEG_NONE) {
+        acc[i][j] = (p.S0 && !producer)
+                        ? *(const f4*)(p.S0 + ((size_t)unit * DV + v0 + nb * 16 + fcol(lane)) * DK + kt * 16 +
+                                       frow(lane, 0))
+                        : zero4();
+      } else if constexpr (SEG == SEG_OUT) {
+        acc[i][j] = producer ? zero4()
+                             : *(const f4*)(p.wSegIn + ((size_t)su * DV + v0 + nb * 16 + fcol(lane)) * DK +
+                                            kt * 16 + frow(lane, 0));
+      } else {
+        // zero for the value rows; map row r starts as row r of the identity
+        const int r = r0 - DV + nb * 16 + fcol(lane);
+#pragma unroll
+        for (int jj = 0; jj < 4; ++jj) acc[i][j][jj] = (map_tile && r == kt * 16 + frow(lane, jj)) ? 1.f : 0.f;
+      }
     }
   // S (row v, column k) into LDS for the next chunk
   auto stage_S = [&]() {
@@ -370,20 +405,20 @@ __global__ __launch_bounds__(NCW * 64 + 256) void k_scan_fwd(Params p) {
     }
   };
 
-  if (nch > 0) {
+  if (nch > cbeg) {
     if (producer) {
-      for (int c = 0; c < NA - 1 && c < nch; ++c) {
+      for (int c = cbeg; c < cbeg + NA - 1 && c < nch; ++c) {
         issueQ(c);
         issueK(c);
       }
-      if (R::NP == 2) issueP(0);
-      issueB(0);
+      if (R::NP == 2) issueP(cbeg);
+      issueB(cbeg);
       wait_vm<0>();
     } else {
       stage_S();
     }
   }
-  for (int c = 0; c < nch; ++c) {
+  for (int c = cbeg; c < nch; ++c) {
     const size_t gi = (size_t)(base + c) * H + h;
     const char* ra = sm.ringA[c % NA];
     const float* gb = (const float*)(ra + R::AG);   // b, then beta, then lambda
@@ -423,10 +458,10 @@ __global__ __launch_bounds__(NCW * 64 + 256) void k_scan_fwd(Params p) {
       // Global stores go out at the end of a phase: at its start they would
       // queue behind the producers' direct loads for that phase and stall
       // the compute wave.
-      if (p.saved) {
+      if (saved) {
         // saved entry state S (row v, column k) of this tile, 16-byte stores
         constexpr int VEC = 16 / sizeof(E), PR = DK / VEC;
-        E* dst = (E*)p.saved + gi * DV * DK + (size_t)v0 * DK;
+        E* dst = (E*)saved + gi * DV * DK + (size_t)v0 * DK;
         for (int idx = tid; idx < BV * PR; idx += NCT) {
           const int r = idx / PR, cc = (idx % PR) * VEC;
           *(uint4*)(dst + (size_t)r * DK + cc) = *(const uint4*)&sm.S[r][cc];
@@ -457,7 +492,8 @@ __global__ __launch_bounds__(NCW * 64 + 256) void k_scan_fwd(Params p) {
         for (int ks = 0; ks < C / KS; ++ks)
           if (keep_kblock<E>(ks * KS <= 16 * cb + 15)) {
             const FR tB = tile_frag<E, R::RC>(sm.ringB + R::BT, 16 * cb, ks * KS, lane);
-            d = Mma<E>::mma(tile_tr_frag<E, R::RO>(sm.ringB + R::BV_, ks * KS, nb * 16, lane), tB, d);
+            if (!map_tile)   // the map rows see no values
+              d = Mma<E>::mma(tile_tr_frag<E, R::RO>(sm.ringB + R::BV_, ks * KS, nb * 16, lane), tB, d);
             d = Mma<E>::mma(tr_frag<E>(&sm.Y[0][0], LV, ks * KS, nb * 16, lane), tB, d);
           }
         f4 dk;
@@ -466,7 +502,7 @@ __global__ __launch_bounds__(NCW * 64 + 256) void k_scan_fwd(Params p) {
         *(QR*)&sm.D[rr][nb * 16 + frow(lane, 0)] = Quad<E>::pack(d);
         *(QR*)&sm.Dk[rr][nb * 16 + frow(lane, 0)] = Quad<E>::pack(dk);
       }
-      if (with_o && c > 0) store_O(c - 1);
+      if (with_o && c > cbeg) store_O(c - 1);
     } else {
       // K and gates of chunk c+NA-1; then P of chunk c must have landed
       const bool k_next = c + NA - 1 < nch;
@@ -476,7 +512,7 @@ __global__ __launch_bounds__(NCW * 64 + 256) void k_scan_fwd(Params p) {
         if (!k_next) wait_vm<0>();
         else if (prod < 3) wait_vm<R::LK + 1>();
         else wait_vm<R::LK>();
-      } else if (c > 0) {
+      } else if (c > cbeg) {
         // issued in the previous phase 2; followed by K of chunk c+1, set B
         // of chunk c, Q of chunk c+2, P of chunk c+1 and K of chunk c+2
         if (k_next) {
@@ -527,7 +563,7 @@ __global__ __launch_bounds__(NCW * 64 + 256) void k_scan_fwd(Params p) {
         }
       }
       stage_S();
-      if (p.saved) {
+      if (saved) {
         // D rows of this tile into the saved context (rows past the chunk are zero)
         constexpr int VEC = 16 / sizeof(E), PR = BV / VEC;
         E* dbase = (E*)p.savedD + gi * C * DV + v0;
@@ -543,7 +579,7 @@ __global__ __launch_bounds__(NCW * 64 + 256) void k_scan_fwd(Params p) {
       if constexpr (NA == 2) {
         wait_vm<R::LB>();
       } else {
-        if (c == 0) {
+        if (c == cbeg) {
           // set A of chunk 1 came with the prologue, which waited for it
         } else if (c + 2 < nch) {
           if (prod < 3) wait_vm<2 * R::LB + R::LQ + R::LP + R::LK + 1>();
@@ -558,8 +594,18 @@ __global__ __launch_bounds__(NCW * 64 + 256) void k_scan_fwd(Params p) {
   if (producer) {
     wait_vm<0>();
   } else {
-    if (with_o && nch > 0) store_O(nch - 1);
-    if (p.Sfin) {
+    if (with_o && nch > cbeg) store_O(nch - 1);
+    if (SEG == SEG_MAPS) {
+      // the segment's B (value rows) and A (map rows): [su][DV + DK][DK]
+#pragma unroll
+      for (int i = 0; i < KPW; ++i)
+#pragma unroll
+        for (int j = 0; j < NBS; ++j) {
+          const int kt = kb0 + i, nb = ns0 + j;
+          *(f4*)(p.wSegOut + ((size_t)su * (DV + DK) + r0 + nb * 16 + fcol(lane)) * DK + kt * 16 +
+                 frow(lane, 0)) = acc[i][j];
+        }
+    } else if (p.Sfin && (SEG == SEG_NONE || g == nseg - 1)) {
 #pragma unroll
       for (int i = 0; i < KPW; ++i)
 #pragma unroll
@@ -596,16 +642,100 @@ static hipError_t launch_fwd_t(const Params& p, int in_bwd, int with_scan, hipSt
       constexpr int NCW = sizeof(E) == 2 ? 8 : 4;
       if constexpr (scan_bv_max<E, DV>() == 64) {
         if (bv == 64)
-          hipLaunchKernelGGL((k_scan_fwd<E, DK, DV, 64, NCW>), dim3(nb), dim3(NCW * 64 + 256), 0, st, p);
+          hipLaunchKernelGGL((k_scan_fwd<E, DK, DV, 64, NCW, SEG_NONE>), dim3(nb), dim3(NCW * 64 + 256), 0, st, p);
         else
-          hipLaunchKernelGGL((k_scan_fwd<E, DK, DV, 32, NCW>), dim3(nb), dim3(NCW * 64 + 256), 0, st, p);
+          hipLaunchKernelGGL((k_scan_fwd<E, DK, DV, 32, NCW, SEG_NONE>), dim3(nb), dim3(NCW * 64 + 256), 0, st, p);
       } else {
-        hipLaunchKernelGGL((k_scan_fwd<E, DK, DV, 32, NCW>), dim3(nb), dim3(NCW * 64 + 256), 0, st, p);
+        hipLaunchKernelGGL((k_scan_fwd<E, DK, DV, 32, NCW, SEG_NONE>), dim3(nb), dim3(NCW * 64 + 256), 0, st, p);
       }
       prof_mark(ST_SCAN_FWD, 1, st);
     }
   }
   return hipGetLastError();
+}
+
+// Entry states of the segments of every (sequence, head): S_0 = the initial
+// state (or zero), S_{g+1} = S_g A_g + B_g with segment g's map from the
+// SEG_MAPS pass, in fp32.  One workgroup per (sequence, head, 16 value rows)
+// walks the segments in order; the rows live in LDS between steps.
+template <int DK, int DV>
+__global__ __launch_bounds__(NTHREADS) void k_seg_compose(Params p) {
+  constexpr int RB = 16;                       // value rows per workgroup
+  constexpr int RPT = RB * DK / NTHREADS;      // rows per thread (one column each)
+  constexpr int TPR = NTHREADS / DK;           // threads per column
+  static_assert(RB * DK % NTHREADS == 0 && NTHREADS % DK == 0, "thread mapping");
+  __shared__ float Srow[RB][DK];
+  const int nrb = DV / RB;
+  const int unit = blockIdx.x / nrb, rb = blockIdx.x % nrb, tid = threadIdx.x;
+  const int G = p.n_seg;
+  const int k = tid % DK, rsub = tid / DK;     // column k; rows rsub, rsub + TPR, ...
+  float cur[RPT];
+#pragma unroll
+  for (int m = 0; m < RPT; ++m) {
+    const int v = rb * RB + rsub + m * TPR;
+    cur[m] = p.S0 ? p.S0[((size_t)unit * DV + v) * DK + k] : 0.f;
+  }
+  for (int g = 0; g < G; ++g) {
+    const size_t su = (size_t)unit * G + g;
+#pragma unroll
+    for (int m = 0; m < RPT; ++m) {
+      const int v = rb * RB + rsub + m * TPR;
+      p.wSegIn[(su * DV + v) * DK + k] = cur[m];
+      Srow[rsub + m * TPR][k] = cur[m];
+    }
+    if (g + 1 == G) break;
+    __syncthreads();
+    // next entry: rows of S_g A_g + B_g
+    const float* Bm = p.wSegOut + su * (DV + DK) * DK;
+    const float* Am = Bm + (size_t)DV * DK;
+#pragma unroll
+    for (int m = 0; m < RPT; ++m) cur[m] = Bm[(size_t)(rb * RB + rsub + m * TPR) * DK + k];
+    for (int r = 0; r < DK; ++r) {
+      const float a = Am[(size_t)r * DK + k];
+#pragma unroll
+      for (int m = 0; m < RPT; ++m) cur[m] += Srow[rsub + m * TPR][r] * a;
+    }
+    __syncthreads();                           // Srow is rewritten in the next step
+  }
+}
+
+// Segment-parallel forward (dense batch): preparation, the maps of every
+// segment (from zero), their composition into segment entry states, and the
+// outputs pass of every segment from its entry state.
+template <typename E, int DK, int DV>
+static hipError_t launch_fwd_seg_t(const Params& p, hipStream_t st) {
+  hipError_t e = launch_fwd_t<E, DK, DV>(p, 0, 0, st);    // preparation only
+  if (e != hipSuccess) return e;
+  const int units = p.N * p.H;
+  if (units == 0) return hipSuccess;
+  constexpr int NCW = sizeof(E) == 2 ? 8 : 4;
+  constexpr int BV = 32;                       // the segment grid fills the CUs with narrow tiles
+  const int su8 = ((units * p.n_seg + 7) / 8) * 8;
+  prof_mark(ST_SEG_MAPS, 0, st);
+  hipLaunchKernelGGL((k_scan_fwd<E, DK, DV, BV, NCW, SEG_MAPS>), dim3(su8 * (DV + DK) / BV),
+                     dim3(NCW * 64 + 256), 0, st, p);
+  prof_mark(ST_SEG_MAPS, 1, st);
+  prof_mark(ST_SEG_COMPOSE, 0, st);
+  hipLaunchKernelGGL((k_seg_compose<DK, DV>), dim3(units * (DV / 16)), dim3(NTHREADS), 0, st, p);
+  prof_mark(ST_SEG_COMPOSE, 1, st);
+  prof_mark(ST_SEG_OUT, 0, st);
+  hipLaunchKernelGGL((k_scan_fwd<E, DK, DV, BV, NCW, SEG_OUT>), dim3(su8 * DV / BV), dim3(NCW * 64 + 256), 0,
+                     st, p);
+  prof_mark(ST_SEG_OUT, 1, st);
+  return hipGetLastError();
+}
+
+hipError_t launch_fwd_seg(const Params& p, int dtype, int Dk, int Dv, hipStream_t st) {
+#define QD_CASE(ET, DKV, DVV) \
+  if (Dk == DKV && Dv == DVV) return launch_fwd_seg_t<ET, DKV, DVV>(p, st);
+  if (dtype == 1) {
+    QD_CASE(__bf16, 64, 64) QD_CASE(__bf16, 64, 128) QD_CASE(__bf16, 64, 256)
+    QD_CASE(__bf16, 128, 64) QD_CASE(__bf16, 128, 128) QD_CASE(__bf16, 128, 256)
+  } else {
+    QD_CASE(float, 64, 64) QD_CASE(float, 64, 128) QD_CASE(float, 64, 256)
+  }
+#undef QD_CASE
+  return hipErrorInvalidValue;
 }
 
 hipError_t launch_fwd(const Params& p, int dtype, int Dk, int Dv, int in_bwd, int with_scan,

@@ -15,7 +15,10 @@ enum Stage {
   ST_INTRA = 4,
   ST_STEP = 5,
   ST_REC_FWD = 6,
-  ST_COUNT = 7
+  ST_SEG_MAPS = 7,
+  ST_SEG_COMPOSE = 8,
+  ST_SEG_OUT = 9,
+  ST_COUNT = 10
 };
 
 // Records a HIP event on `st` before (after == 0) or after (after == 1) a
@@ -28,6 +31,11 @@ void prof_mark(int stage, int after, hipStream_t st);
 // backward that recomputes the saved context).
 hipError_t launch_fwd(const Params& p, int dtype, int Dk, int Dv, int in_bwd, int with_scan,
                       hipStream_t st);
+
+// Segment-parallel forward of a dense batch (p.n_seg segments of
+// p.seg_chunks chunks per sequence; p.wSegOut, p.wSegIn set): preparation,
+// segment maps, composition, outputs.
+hipError_t launch_fwd_seg(const Params& p, int dtype, int Dk, int Dv, hipStream_t st);
 
 // Backward once the saved context (states, D, b, W, P, M) is in place:
 // reverse state scan, then the intra-chunk gradient kernel.

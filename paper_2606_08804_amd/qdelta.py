@@ -11,6 +11,8 @@ chunk_fwd(q, k, v, beta, lam, log_alpha=None, initial_state=None, cu_seqlens=Non
           (saved: uint8 device buffer holding the saved context for the backward)
 chunk_fwd_noalloc(q, k, v, beta, lam, log_alpha=None, initial_state=None, out=None,
           final_state_out=None) -> (o, final_state)    (dense; library-owned scratch, no workspace)
+chunk_fwd_segmented(q, k, v, beta, lam, log_alpha=None, initial_state=None, n_segments=None,
+          save_states=False) -> (o, final_state, saved)   (dense; long sequences, few heads)
 chunk_bwd(q, k, v, beta, lam, log_alpha, initial_state, saved_states, d_o,
           d_final_state=None, cu_seqlens=None) -> dict of gradients
 recurrent_step(q, k, v, beta, lam, log_alpha, state) -> o        (state updated in place)
@@ -40,10 +42,12 @@ EXPORTS = (
     "qdelta_chunk_bwd", "qdelta_chunk_bwd_varlen", "qdelta_recurrent_step",
     "qdelta_recurrent_fwd", "qdelta_recurrent_fwd_varlen", "qdelta_l2norm_fwd", "qdelta_l2norm_bwd",
     "qdelta_profile_begin", "qdelta_profile_end", "qdelta_chunk_fwd_noalloc",
+    "qdelta_chunk_fwd_segmented", "qdelta_segmented_workspace_bytes", "qdelta_suggest_segments",
 )
 NOALLOC_SCRATCH_BYTES = 64 << 20
 
-STAGES = ("prep_fwd", "scan_fwd", "prep_bwd", "scan_bwd", "intra", "step", "rec_fwd")
+STAGES = ("prep_fwd", "scan_fwd", "prep_bwd", "scan_bwd", "intra", "step", "rec_fwd", "seg_maps",
+          "seg_compose", "seg_out")
 
 _lib = None
 
@@ -79,6 +83,12 @@ def lib():
         L.qdelta_chunk_fwd.restype = ctypes.c_int
         L.qdelta_chunk_fwd_noalloc.argtypes = [i32] * 7 + [P] * 5 + [f32] + [P] * 4 + [P]
         L.qdelta_chunk_fwd_noalloc.restype = ctypes.c_int
+        L.qdelta_chunk_fwd_segmented.argtypes = [i32] * 7 + [P] * 5 + [f32] + [P] * 5 + [i32, P, sz, P]
+        L.qdelta_chunk_fwd_segmented.restype = ctypes.c_int
+        L.qdelta_segmented_workspace_bytes.argtypes = [i32] * 8
+        L.qdelta_segmented_workspace_bytes.restype = sz
+        L.qdelta_suggest_segments.argtypes = [i32] * 5
+        L.qdelta_suggest_segments.restype = i32
         L.qdelta_chunk_fwd_varlen.argtypes = [i32, i32, P] + [i32] * 5 + [P] * 5 + [f32] + [P] * 5 + [P, sz, P]
         L.qdelta_chunk_fwd_varlen.restype = ctypes.c_int
         L.qdelta_chunk_bwd.argtypes = [i32] * 7 + [P] * 5 + [f32] + [P] * 12 + [P, sz, P]
@@ -224,6 +234,49 @@ def chunk_fwd(q, k, v, beta, lam, log_alpha=None, initial_state=None, cu_seqlens
         _check("qdelta_chunk_fwd", L.qdelta_chunk_fwd(B, T, *common))
     else:
         _check("qdelta_chunk_fwd_varlen", L.qdelta_chunk_fwd_varlen(T, N, _p(cu_seqlens), *common))
+    return o, Sf, saved
+
+
+def suggest_segments(B, T, H, Dk, Dv):
+    """Segment count the segment-parallel forward is expected to run fastest
+    with on the current device (1: the single pass)."""
+    return int(lib().qdelta_suggest_segments(B, T, H, Dk, Dv))
+
+
+def segmented_workspace_bytes(B, T, H, Dk, Dv, dtype, n_segments):
+    return int(lib().qdelta_segmented_workspace_bytes(B, T, H, Dk, Dv, CHUNK, dtype, n_segments))
+
+
+def chunk_fwd_segmented(q, k, v, beta, lam, log_alpha=None, initial_state=None, n_segments=None,
+                        output_final_state=True, save_states=False, workspace=None):
+    """Segment-parallel chunkwise forward of a dense batch (long sequences,
+    few (sequence, head) pairs).  n_segments None: the library's suggestion
+    for this device.  Returns (o, final_state or None, saved or None), as
+    chunk_fwd."""
+    L = lib()
+    dt = _dt(q)
+    B, T, H, Dk, Dv, N = _dims(q, v, None)
+    act = q.shape[:-1]
+    _need(q, "q", q.dtype)
+    _need(k, "k", q.dtype, q.shape)
+    _need(v, "v", q.dtype, tuple(act) + (Dv,))
+    _need(beta, "beta", torch.float32, act)
+    lam_t, lam_c = _lam(lam, act)
+    _opt(log_alpha, "log_alpha", torch.float32, act)
+    _opt(initial_state, "initial_state", torch.float32, (N, H, Dv, Dk))
+    G = suggest_segments(B, T, H, Dk, Dv) if n_segments is None else int(n_segments)
+    dev = q.device
+    o = torch.empty(tuple(act) + (Dv,), dtype=q.dtype, device=dev)
+    Sf = torch.empty((N, H, Dv, Dk), dtype=torch.float32, device=dev) if output_final_state else None
+    saved = None
+    if save_states:
+        saved = torch.empty(saved_bytes(B, T, H, Dk, Dv, dt, 0), dtype=torch.uint8, device=dev)
+    nbytes = segmented_workspace_bytes(B, T, H, Dk, Dv, dt, max(G, 1))
+    ws = _workspace(nbytes, dev, workspace)
+    _check("qdelta_chunk_fwd_segmented",
+           L.qdelta_chunk_fwd_segmented(B, T, H, Dk, Dv, CHUNK, dt, _p(q), _p(k), _p(v), _p(beta), _p(lam_t),
+                                        lam_c, _p(log_alpha), _p(initial_state), _p(o), _p(Sf), _p(saved), G,
+                                        _p(ws), nbytes, _stream()))
     return o, Sf, saved
 
 

@@ -22,7 +22,7 @@ def header_functions():
 def test_library_exports_every_declared_symbol():
     L = qdelta.lib()
     names = header_functions()
-    assert len(names) == 17
+    assert len(names) == 20
     for n in names:
         assert hasattr(L, n), n
     assert sorted(names) == sorted(qdelta.EXPORTS)
@@ -123,6 +123,35 @@ def test_noalloc_forward_validates_before_any_device_call():
     assert qdelta.workspace_bytes(4, 4096, 16, 128, 128, 1) > cap
     assert call(B=4, T=4096, H=16, Dk=128, Dv=128) == E.QDELTA_ENOWORKSPACE
     assert call(B=1, T=65536, H=16, Dk=128, Dv=128) == E.QDELTA_ENOWORKSPACE
+
+
+def test_segmented_forward_sizes_and_validation():
+    """Workspace of the segment-parallel forward: the forward's own plus each
+    segment's map (Dv + Dk rows of Dk, fp32) and entry state (Dv x Dk fp32);
+    bad arguments are rejected before any launch; the suggested segment
+    count is 1 where the single pass fills the chip."""
+    L = qdelta.lib()
+    E = qdelta
+    f = FAKE
+    base = qdelta.workspace_bytes(1, 65536, 16, 128, 128, 1)
+    # 1024 chunks in 4 segments of 256
+    extra = 16 * 4 * (256 * 128 * 4 + 128 * 128 * 4)
+    assert qdelta.segmented_workspace_bytes(1, 65536, 16, 128, 128, 1, 4) == base + extra
+    # 10 chunks asked for 4 segments: 3 chunks each, so 4 non-empty segments
+    b10 = qdelta.workspace_bytes(2, 640, 2, 64, 64, 0)
+    assert qdelta.segmented_workspace_bytes(2, 640, 2, 64, 64, 0, 4) == b10 + 4 * 4 * (128 * 64 * 4 + 64 * 64 * 4)
+    assert qdelta.segmented_workspace_bytes(1, 640, 2, 64, 64, 0, 0) == 0
+
+    def call(n_segments=4, ws_bytes=1 << 40, Dk=64, q=f):
+        return L.qdelta_chunk_fwd_segmented(1, 640, 2, Dk, 64, 64, 1, q, f, f, f, f, 0.0, None, None, f, None,
+                                            None, n_segments, f, ws_bytes, None)
+
+    assert call(n_segments=0) == E.QDELTA_EINVAL
+    assert call(Dk=96) == E.QDELTA_EUNSUPPORTED
+    assert call(q=None) == E.QDELTA_EINVAL
+    assert call(ws_bytes=qdelta.workspace_bytes(1, 640, 2, 64, 64, 1)) == E.QDELTA_ENOWORKSPACE
+    assert qdelta.suggest_segments(4, 4096, 16, 128, 128) == 1
+    assert qdelta.suggest_segments(1, 65536, 2, 128, 128) > 1
 
 
 def test_bwd_and_varlen_reject_bad_arguments():
