@@ -383,7 +383,7 @@ def run_chunk(args, wid, with_bwd):
 
     # forward-only dense batches run the segment-parallel form when the
     # library suggests more than one segment (long sequences, few heads)
-    n_seg = 1 if (with_bwd or cu is not None) else qdelta.suggest_segments(B, T, H, Dk, Dv)
+    n_seg = 1 if (with_bwd or cu is not None) else qdelta.suggest_segments(B, T, H, Dk, Dv, dt)
     single_ms = None
     if with_bwd:
         def step():

@@ -168,7 +168,7 @@ size_t qdelta_segmented_workspace_bytes(int32_t B, int32_t T, int32_t H, int32_t
 
 /* Segment count that qdelta_chunk_fwd_segmented is expected to run fastest
  * with on the current device (1: use the single pass).  Host-side only. */
-int32_t qdelta_suggest_segments(int32_t B, int32_t T, int32_t H, int32_t Dk, int32_t Dv);
+int32_t qdelta_suggest_segments(int32_t B, int32_t T, int32_t H, int32_t Dk, int32_t Dv, int32_t dtype);
 
 /* Allocation-free forward, for callers that cannot allocate device memory
  * or hand over a workspace: code under HIP graph capture, tight serving

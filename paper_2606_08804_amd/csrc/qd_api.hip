@@ -435,20 +435,22 @@ size_t qdelta_segmented_workspace_bytes(int32_t B, int32_t T, int32_t H, int32_t
                          dtype == QDELTA_BF16 ? 2 : 4).total;
 }
 
-int32_t qdelta_suggest_segments(int32_t B, int32_t T, int32_t H, int32_t Dk, int32_t Dv) {
+int32_t qdelta_suggest_segments(int32_t B, int32_t T, int32_t H, int32_t Dk, int32_t Dv, int32_t dtype) {
   if (B <= 0 || T <= 0 || H <= 0 || Dk <= 0 || Dv <= 0) return 1;
   const long long cus = qd::device_cu_count();
   const long long seq_heads = (long long)B * H;
   const int NT = (T + C - 1) / C;
   // the single pass runs one workgroup per (sequence, head, 32 value rows);
   // with half as many of them as CUs or more it is the faster form
-  // (measured at B1 T65536 d128: 16 heads, 64 workgroups, take 1.64 ms in
-  // one pass and 1.30 ms in four segments)
+  // (measured at B1 T65536 d128 bf16: 16 heads, 64 workgroups, take 1.64 ms
+  // in one pass and about 1.0 ms in eight segments)
   if (seq_heads * (Dv / 32) * 2 >= cus) return 1;
-  // the maps pass runs (Dv + Dk) / 32 workgroups per segment: up to two per
-  // CU, with segments of at least 16 chunks
+  // the maps pass runs (Dv + Dk) / w workgroups per segment (w = 64 value
+  // rows for bf16, 32 for fp32): up to two per CU, with segments of at least
+  // 16 chunks
+  const int w = dtype == QDELTA_BF16 ? 64 : 32;
   int G = 1;
-  while (G < 16 && seq_heads * (2 * G) * ((Dv + Dk) / 32) <= 2 * cus && NT / (2 * G) >= 16) G *= 2;
+  while (G < 16 && seq_heads * (2 * G) * ((Dv + Dk) / w) <= 2 * cus && NT / (2 * G) >= 16) G *= 2;
   return G;
 }
 

@@ -656,14 +656,20 @@ static hipError_t launch_fwd_t(const Params& p, int in_bwd, int with_scan, hipSt
 
 // Entry states of the segments of every (sequence, head): S_0 = the initial
 // state (or zero), S_{g+1} = S_g A_g + B_g with segment g's map from the
-// SEG_MAPS pass, in fp32.  One workgroup per (sequence, head, 16 value rows)
-// walks the segments in order; the rows live in LDS between steps.
+// SEG_MAPS pass, in fp32.  One workgroup per (sequence, head, 8 value rows)
+// walks the segments in order: each step stages A_g in LDS with coalesced
+// 16-byte loads (all issued before the first use), then every thread forms
+// one column of its rows from LDS.
+constexpr int SEG_COMPOSE_RB = 8;
 template <int DK, int DV>
 __global__ __launch_bounds__(NTHREADS) void k_seg_compose(Params p) {
-  constexpr int RB = 16;                       // value rows per workgroup
+  constexpr int RB = SEG_COMPOSE_RB;           // value rows per workgroup
   constexpr int RPT = RB * DK / NTHREADS;      // rows per thread (one column each)
   constexpr int TPR = NTHREADS / DK;           // threads per column
-  static_assert(RB * DK % NTHREADS == 0 && NTHREADS % DK == 0, "thread mapping");
+  constexpr int AV = DK * DK / 4 / NTHREADS;   // float4 loads of A per thread
+  static_assert(RB * DK % NTHREADS == 0 && NTHREADS % DK == 0 && AV * 4 * NTHREADS == DK * DK,
+                "thread mapping");
+  __shared__ __align__(16) float Am[DK][DK];
   __shared__ float Srow[RB][DK];
   const int nrb = DV / RB;
   const int unit = blockIdx.x / nrb, rb = blockIdx.x % nrb, tid = threadIdx.x;
@@ -684,24 +690,33 @@ __global__ __launch_bounds__(NTHREADS) void k_seg_compose(Params p) {
       Srow[rsub + m * TPR][k] = cur[m];
     }
     if (g + 1 == G) break;
-    __syncthreads();
-    // next entry: rows of S_g A_g + B_g
     const float* Bm = p.wSegOut + su * (DV + DK) * DK;
-    const float* Am = Bm + (size_t)DV * DK;
+    const f4* Ag = (const f4*)(Bm + (size_t)DV * DK);
+    f4 av[AV];
+#pragma unroll
+    for (int i = 0; i < AV; ++i) av[i] = Ag[tid + i * NTHREADS];
 #pragma unroll
     for (int m = 0; m < RPT; ++m) cur[m] = Bm[(size_t)(rb * RB + rsub + m * TPR) * DK + k];
+#pragma unroll
+    for (int i = 0; i < AV; ++i) ((f4*)&Am[0][0])[tid + i * NTHREADS] = av[i];
+    __syncthreads();
+    // next entry: rows of S_g A_g + B_g
+#pragma unroll 8
     for (int r = 0; r < DK; ++r) {
-      const float a = Am[(size_t)r * DK + k];
+      const float a = Am[r][k];
 #pragma unroll
       for (int m = 0; m < RPT; ++m) cur[m] += Srow[rsub + m * TPR][r] * a;
     }
-    __syncthreads();                           // Srow is rewritten in the next step
+    __syncthreads();                           // Am and Srow are rewritten in the next step
   }
 }
 
 // Segment-parallel forward (dense batch): preparation, the maps of every
 // segment (from zero), their composition into segment entry states, and the
-// outputs pass of every segment from its entry state.
+// outputs pass of every segment from its entry state.  The maps pass takes
+// the widest value tiles (it has (DV + DK) / BV of them per segment, and
+// wider tiles re-read the operands their segment shares fewer times); the
+// outputs pass takes them too once they still give every CU a workgroup.
 template <typename E, int DK, int DV>
 static hipError_t launch_fwd_seg_t(const Params& p, hipStream_t st) {
   hipError_t e = launch_fwd_t<E, DK, DV>(p, 0, 0, st);    // preparation only
@@ -709,18 +724,23 @@ static hipError_t launch_fwd_seg_t(const Params& p, hipStream_t st) {
   const int units = p.N * p.H;
   if (units == 0) return hipSuccess;
   constexpr int NCW = sizeof(E) == 2 ? 8 : 4;
-  constexpr int BV = 32;                       // the segment grid fills the CUs with narrow tiles
+  constexpr int BW = scan_bv_max<E, DV>();     // 64 for bf16, else 32
   const int su8 = ((units * p.n_seg + 7) / 8) * 8;
+  const bool out_wide = BW == 64 && (long long)units * p.n_seg * (DV / 64) >= device_cu_count();
   prof_mark(ST_SEG_MAPS, 0, st);
-  hipLaunchKernelGGL((k_scan_fwd<E, DK, DV, BV, NCW, SEG_MAPS>), dim3(su8 * (DV + DK) / BV),
+  hipLaunchKernelGGL((k_scan_fwd<E, DK, DV, BW, NCW, SEG_MAPS>), dim3(su8 * (DV + DK) / BW),
                      dim3(NCW * 64 + 256), 0, st, p);
   prof_mark(ST_SEG_MAPS, 1, st);
   prof_mark(ST_SEG_COMPOSE, 0, st);
-  hipLaunchKernelGGL((k_seg_compose<DK, DV>), dim3(units * (DV / 16)), dim3(NTHREADS), 0, st, p);
+  hipLaunchKernelGGL((k_seg_compose<DK, DV>), dim3(units * (DV / SEG_COMPOSE_RB)), dim3(NTHREADS), 0, st, p);
   prof_mark(ST_SEG_COMPOSE, 1, st);
   prof_mark(ST_SEG_OUT, 0, st);
-  hipLaunchKernelGGL((k_scan_fwd<E, DK, DV, BV, NCW, SEG_OUT>), dim3(su8 * DV / BV), dim3(NCW * 64 + 256), 0,
-                     st, p);
+  if (out_wide)
+    hipLaunchKernelGGL((k_scan_fwd<E, DK, DV, BW, NCW, SEG_OUT>), dim3(su8 * DV / BW), dim3(NCW * 64 + 256), 0,
+                       st, p);
+  else
+    hipLaunchKernelGGL((k_scan_fwd<E, DK, DV, 32, NCW, SEG_OUT>), dim3(su8 * DV / 32), dim3(NCW * 64 + 256), 0,
+                       st, p);
   prof_mark(ST_SEG_OUT, 1, st);
   return hipGetLastError();
 }

@@ -87,7 +87,7 @@ def lib():
         L.qdelta_chunk_fwd_segmented.restype = ctypes.c_int
         L.qdelta_segmented_workspace_bytes.argtypes = [i32] * 8
         L.qdelta_segmented_workspace_bytes.restype = sz
-        L.qdelta_suggest_segments.argtypes = [i32] * 5
+        L.qdelta_suggest_segments.argtypes = [i32] * 6
         L.qdelta_suggest_segments.restype = i32
         L.qdelta_chunk_fwd_varlen.argtypes = [i32, i32, P] + [i32] * 5 + [P] * 5 + [f32] + [P] * 5 + [P, sz, P]
         L.qdelta_chunk_fwd_varlen.restype = ctypes.c_int
@@ -237,10 +237,10 @@ def chunk_fwd(q, k, v, beta, lam, log_alpha=None, initial_state=None, cu_seqlens
     return o, Sf, saved
 
 
-def suggest_segments(B, T, H, Dk, Dv):
+def suggest_segments(B, T, H, Dk, Dv, dtype=QDELTA_BF16):
     """Segment count the segment-parallel forward is expected to run fastest
     with on the current device (1: the single pass)."""
-    return int(lib().qdelta_suggest_segments(B, T, H, Dk, Dv))
+    return int(lib().qdelta_suggest_segments(B, T, H, Dk, Dv, dtype))
 
 
 def segmented_workspace_bytes(B, T, H, Dk, Dv, dtype, n_segments):
@@ -264,7 +264,7 @@ def chunk_fwd_segmented(q, k, v, beta, lam, log_alpha=None, initial_state=None, 
     lam_t, lam_c = _lam(lam, act)
     _opt(log_alpha, "log_alpha", torch.float32, act)
     _opt(initial_state, "initial_state", torch.float32, (N, H, Dv, Dk))
-    G = suggest_segments(B, T, H, Dk, Dv) if n_segments is None else int(n_segments)
+    G = suggest_segments(B, T, H, Dk, Dv, dt) if n_segments is None else int(n_segments)
     dev = q.device
     o = torch.empty(tuple(act) + (Dv,), dtype=q.dtype, device=dev)
     Sf = torch.empty((N, H, Dv, Dk), dtype=torch.float32, device=dev) if output_final_state else None
