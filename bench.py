@@ -507,32 +507,54 @@ def run_layer(args):
 
 
 def run_recurrent(args):
-    """Fully recurrent forward on short continuing sequences (64 sequences
-    from a carried state, H=16, d=128, bf16) at T = 16 tokens, with the
-    chunkwise forward on the same input timed beside it, and both at T = 4
-    and T = 64 to show where the two forms cross over."""
+    """The fully recurrent form on short continuing sequences (64 sequences
+    from a carried state, H=16, d=128, bf16) at T = 16 tokens: forward, and
+    forward + backward as a training step, each with the chunkwise form on
+    the same input timed beside it; both again at T = 4 and T = 64 to show
+    where the two forms cross over."""
     B, H, d, T_main = 64, 16, 128, 16
     by_T = {}
-    out_main = None
+    main = None
     for T in (4, 16, 64):
-        dd = synth.make(B, T, H, d, d, "bf16", args.gate, seed=20260007, s0=True)
+        dd = synth.make(B, T, H, d, d, "bf16", args.gate, seed=20260007, s0=True, with_do=True)
         g = {k: (v.cuda() if isinstance(v, torch.Tensor) else v) for k, v in dd.items()}
         ins = (g["q"], g["k"], g["v"], g["beta"], g["lam"], g["log_alpha"], g["initial_state"])
         wsf = torch.empty(max(1, qdelta.workspace_bytes(B, T, H, d, d, qdelta.QDELTA_BF16, 0, False)),
                           dtype=torch.uint8, device="cuda")
+        wsb = torch.empty(max(1, qdelta.workspace_bytes(B, T, H, d, d, qdelta.QDELTA_BF16, 0, True)),
+                          dtype=torch.uint8, device="cuda")
+        wsr = torch.empty(qdelta.recurrent_workspace_bytes(B, T, H, d, d), dtype=torch.uint8, device="cuda")
+
+        def rec_train():
+            qdelta.recurrent_fwd(*ins)
+            qdelta.recurrent_bwd(*ins, g["d_o"], workspace=wsr)
+
+        def chunk_train():
+            _, _, saved = qdelta.chunk_fwd(*ins, save_states=True, workspace=wsf)
+            qdelta.chunk_bwd(*ins, saved, g["d_o"], workspace=wsb)
+
         ms, stages, _ = timed(lambda: qdelta.recurrent_fwd(*ins), args.steps, args.warmup, args.settle_ms)
         ms_chunk, _, _ = timed(lambda: qdelta.chunk_fwd(*ins, save_states=False, workspace=wsf),
                                args.steps, args.warmup, 0)
-        by_T[T] = {"recurrent_ms": ms, "chunk_ms": ms_chunk}
+        ms_tr, st_tr, _ = timed(rec_train, args.steps, args.warmup, 0)
+        ms_ctr, _, _ = timed(chunk_train, args.steps, args.warmup, 0)
+        by_T[T] = {"recurrent_fwd_ms": ms, "chunk_fwd_ms": ms_chunk,
+                   "recurrent_fwd_bwd_ms": ms_tr, "chunk_fwd_bwd_ms": ms_ctr,
+                   "recurrent_bwd_kernel_us": st_tr["rec_bwd"][0] / st_tr["rec_bwd"][1] * 1e3}
         if T == T_main:
             tot, launches = stages["rec_fwd"]
-            out_main = (ms, tot / launches / 1e3, ms_chunk)
-    ms, avg_s, ms_chunk = out_main
+            btot, blaunch = st_tr["rec_bwd"]
+            main = (ms, tot / launches / 1e3, ms_chunk, ms_tr, btot / blaunch / 1e3, ms_ctr)
+    ms, avg_s, ms_chunk, ms_tr, avg_b, ms_ctr = main
     T = T_main
-    # ALU roofline: 6 Dk Dv flops per token-head (S x and S q dot products, rank-1 update)
+    # ALU roofline: forward 6 Dk Dv flops per token-head (S x and S q dot
+    # products, rank-1 update); backward 22 Dk Dv (three sweeps: 6 + 8 + 8)
     flops = B * T * H * 6 * d * d
+    bflops = B * T * H * 22 * d * d
     kern = {"rec_fwd": {"avg_launch_us": avg_s * 1e6, "alg_flops_per_launch": flops,
-                        "achieved_TFLOPs": flops / avg_s / 1e12, "frac": flops / avg_s / VALU_F32_PEAK}}
+                        "achieved_TFLOPs": flops / avg_s / 1e12, "frac": flops / avg_s / VALU_F32_PEAK},
+            "rec_bwd": {"avg_launch_us": avg_b * 1e6, "alg_flops_per_launch": bflops,
+                        "achieved_TFLOPs": bflops / avg_b / 1e12, "frac": bflops / avg_b / VALU_F32_PEAK}}
     return {
         "metric": f"Q-Delta recurrent fwd tokens/s (B={B},T={T},H={H},d={d},bf16, carried state)",
         "value": B * T / (ms / 1e3), "unit": "tokens/s", "n_gpus": 1, "steps": args.steps,
@@ -541,8 +563,10 @@ def run_recurrent(args):
         "config": {"workload": f"recurrent fwd bf16 B={B} T={T} H={H} d={d} with initial state",
                    "gate_mode": args.gate, "parallelism": "single GPU"},
         "chunk_fwd_ms_same_input": ms_chunk,
+        "recurrent_fwd_bwd_tokens_per_s": B * T / (ms_tr / 1e3), "recurrent_fwd_bwd_ms": ms_tr,
+        "chunk_fwd_bwd_ms_same_input": ms_ctr,
         "by_T": by_T,
-        "kernel_avg_us": {"rec_fwd": round(avg_s * 1e6, 2)},
+        "kernel_avg_us": {k: round(v["avg_launch_us"], 2) for k, v in kern.items()},
         "kernels": kern,
         "roofline": {"bound": "alu", "kernel": "rec_fwd", "achieved": flops / avg_s / 1e12,
                      "peak": VALU_F32_PEAK / 1e12, "unit": "TFLOP/s", "frac": flops / avg_s / VALU_F32_PEAK,

@@ -271,6 +271,42 @@ int qdelta_recurrent_fwd_varlen(int32_t T, int32_t N, const int32_t* cu_seqlens,
                                 const float* initial_state, void* o, float* final_state,
                                 hipStream_t stream);
 
+/* Workspace bytes of qdelta_recurrent_bwd[_varlen] for these sizes
+ * (n_seqs == 0: dense B x T; n_seqs > 0: varlen, T total tokens): per
+ * token-head 3 Dv + Dk + 1 fp32, per (sequence, head) Dv fp32.  0 for
+ * unsupported sizes. */
+size_t qdelta_recurrent_workspace_bytes(int32_t B, int32_t T, int32_t H, int32_t Dk, int32_t Dv,
+                                        int32_t n_seqs);
+
+/* Backward of the fully recurrent form (the paper ships kernels for both the
+ * fully recurrent and the chunkwise form, Sec. 3.3): exact gradients (up to
+ * rounding) of L = <d_o, o> + <d_final_state, final_state> through
+ * Eq. (qdelta_decay) token by token, one launch, no saved context (the
+ * states are recomputed).  Arguments and gradient conventions as
+ * qdelta_chunk_bwd (dense layout; dlam per token for a lam tensor, one float
+ * or NULL for a constant lambda), plus a workspace of
+ * qdelta_recurrent_workspace_bytes.  Same results as qdelta_chunk_bwd up to
+ * rounding; meant for short sequences, where the chunk form's per-chunk
+ * work does not pay off.
+ * Supported: Dk in {64, 128}, Dv in {32, 64, 128, 256}, any dtype. */
+int qdelta_recurrent_bwd(int32_t B, int32_t T, int32_t H, int32_t Dk, int32_t Dv, int32_t dtype,
+                         const void* q, const void* k, const void* v, const float* beta,
+                         const float* lam, float lam_scalar, const float* log_alpha,
+                         const float* initial_state, const void* d_o, const float* d_final_state,
+                         void* dq, void* dk, void* dv, float* dbeta, float* dlam, float* dlog_alpha,
+                         float* d_initial_state, void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* Varlen recurrent backward: B == 1, T total tokens, N sequences delimited
+ * by the device array cu_seqlens[N+1] (entries clamped to [0, T]); states
+ * are [N,H,Dv,Dk]. */
+int qdelta_recurrent_bwd_varlen(int32_t T, int32_t N, const int32_t* cu_seqlens, int32_t H, int32_t Dk,
+                                int32_t Dv, int32_t dtype, const void* q, const void* k, const void* v,
+                                const float* beta, const float* lam, float lam_scalar,
+                                const float* log_alpha, const float* initial_state, const void* d_o,
+                                const float* d_final_state, void* dq, void* dk, void* dv, float* dbeta,
+                                float* dlam, float* dlog_alpha, float* d_initial_state, void* ws,
+                                size_t ws_bytes, hipStream_t stream);
+
 /* Row L2 normalisation for the layer's q and k (unit-norm keys are the
  * condition of Sec. 3.4 Lemma 1): y = x / max(|x|, 1e-12) per row of D.
  *   x        rows of D elements (dtype), row r at x + r * ld_x (ld_x >= D,
@@ -295,11 +331,12 @@ int qdelta_l2norm_bwd(int64_t rows, int32_t D, int32_t dtype, const void* y, con
  *   4 intra-chunk backward              5 recurrent step
  *   6 recurrent forward                 7 segment maps (segmented forward)
  *   8 segment entry states              9 segment outputs
+ *  10 recurrent backward
  * qdelta_profile_end() waits for the recorded events, writes the summed kernel
  * time (milliseconds) and the number of launches of each stage into the
  * caller's arrays of QDELTA_N_STAGES entries (either may be NULL) and stops
  * recording.  Returns QDELTA_EHIP if an event call failed. */
-#define QDELTA_N_STAGES 10
+#define QDELTA_N_STAGES 11
 int qdelta_profile_begin(void);
 int qdelta_profile_end(float* ms, int32_t* launches);
 

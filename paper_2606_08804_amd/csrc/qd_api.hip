@@ -597,6 +597,97 @@ int qdelta_recurrent_fwd_varlen(int32_t T, int32_t N, const int32_t* cu_seqlens,
                       log_alpha, initial_state, o, final_state, stream);
 }
 
+size_t qdelta_recurrent_workspace_bytes(int32_t B, int32_t T, int32_t H, int32_t Dk, int32_t Dv,
+                                        int32_t n_seqs) {
+  if (B < 0 || T < 0 || H <= 0 || n_seqs < 0) return 0;
+  if ((Dk != 64 && Dk != 128) || (Dv != 32 && Dv != 64 && Dv != 128 && Dv != 256)) return 0;
+  const size_t tok = n_seqs > 0 ? (size_t)T : (size_t)B * T;
+  const size_t units = (size_t)(n_seqs > 0 ? n_seqs : B) * H;
+  auto r = [](size_t b) { return (b + 255) & ~size_t(255); };
+  return 3 * r(tok * H * Dv * 4) + r(tok * H * Dk * 4) + r(units * Dv * 4) + r(tok * H * 4);
+}
+
+static int rec_bwd_impl(bool varlen, int32_t B, int32_t T, int32_t N, const int32_t* cu, int32_t H,
+                        int32_t Dk, int32_t Dv, int32_t dtype, const void* q, const void* k, const void* v,
+                        const float* beta, const float* lam, float lam_c, const float* log_alpha,
+                        const float* initial_state, const void* d_o, const float* d_final_state, void* dq,
+                        void* dk, void* dv, float* dbeta, float* dlam, float* dlog_alpha,
+                        float* d_initial_state, void* ws, size_t ws_bytes, hipStream_t stream) {
+  if (T < 0 || H <= 0) return QDELTA_EINVAL;
+  if (varlen ? (N < 0 || cu == nullptr) : B < 0) return QDELTA_EINVAL;
+  if (dtype != QDELTA_F32 && dtype != QDELTA_BF16) return QDELTA_EINVAL;
+  if ((Dk != 64 && Dk != 128) || (Dv != 32 && Dv != 64 && Dv != 128 && Dv != 256)) return QDELTA_EUNSUPPORTED;
+  const int64_t tokens = varlen ? T : (int64_t)B * T;
+  const int32_t n_seqs = varlen ? N : B;
+  if (tokens * H * (int64_t)(Dv > Dk ? Dv : Dk) >= (int64_t(1) << 31) || (int64_t)n_seqs * H >= (int64_t(1) << 31))
+    return QDELTA_EUNSUPPORTED;
+  const bool has_tokens = tokens > 0;
+  if (has_tokens && !(ok_ptr(q) && ok_ptr(k) && ok_ptr(v) && ok_ptr(beta) && ok_ptr(d_o) && ok_ptr(dq) &&
+                      ok_ptr(dk) && ok_ptr(dv) && ok_ptr(dbeta)))
+    return QDELTA_EINVAL;
+  if ((log_alpha == nullptr) != (dlog_alpha == nullptr) && has_tokens) return QDELTA_EINVAL;
+  if (lam != nullptr && dlam == nullptr && has_tokens) return QDELTA_EINVAL;
+  if (lam == nullptr && dlam != nullptr && (reinterpret_cast<uintptr_t>(dlam) & 3u)) return QDELTA_EINVAL;
+  if (!ok_opt(lam) || (lam != nullptr && !ok_opt(dlam)) || !ok_opt(log_alpha) || !ok_opt(dlog_alpha) ||
+      !ok_opt(initial_state) || !ok_opt(d_final_state) || !ok_opt(d_initial_state))
+    return QDELTA_EINVAL;
+  const size_t need = qdelta_recurrent_workspace_bytes(B, T, H, Dk, Dv, varlen ? (N > 0 ? N : 1) : 0);
+  if (need > 0 && (ws == nullptr || !aligned(ws))) return QDELTA_EINVAL;
+  if (ws_bytes < need) return QDELTA_ENOWORKSPACE;
+  const bool dlam_const = lam == nullptr && dlam != nullptr;
+  if (n_seqs == 0) {
+    if (dlam_const) return qd::launch_zero(dlam, stream) == hipSuccess ? QDELTA_OK : QDELTA_EHIP;
+    return QDELTA_OK;
+  }
+  const size_t tok = (size_t)tokens;
+  auto r = [](size_t b) { return (b + 255) & ~size_t(255); };
+  char* w = static_cast<char*>(ws);
+  qd::RecBwdArgs a{};
+  a.T = varlen ? 0 : T;
+  a.cu = varlen ? cu : nullptr;
+  a.T_total = (int)tokens;
+  a.H = H;
+  a.DV = Dv;
+  a.q = q; a.k = k; a.v = v; a.dO = d_o;
+  a.beta = beta; a.lam = lam; a.lam_c = lam_c; a.la = log_alpha; a.S0 = initial_state; a.dSfin = d_final_state;
+  a.dq = dq; a.dk = dk; a.dv = dv;
+  a.dbeta = dbeta; a.dla = dlog_alpha; a.dS0 = d_initial_state;
+  a.dlam = dlam_const ? nullptr : dlam;
+  size_t off = 0;
+  a.wP = reinterpret_cast<float*>(w + off); off += r(tok * H * Dv * 4);
+  a.wZ = reinterpret_cast<float*>(w + off); off += r(tok * H * Dv * 4);
+  a.wDP = reinterpret_cast<float*>(w + off); off += r(tok * H * Dv * 4);
+  a.wWK = reinterpret_cast<float*>(w + off); off += r(tok * H * Dk * 4);
+  a.wF = reinterpret_cast<float*>(w + off); off += r((size_t)n_seqs * H * Dv * 4);
+  a.wDL = dlam_const ? reinterpret_cast<float*>(w + off) : nullptr;
+  hipError_t e = qd::launch_rec_bwd(a, n_seqs * H, dtype, Dk, dlam_const ? dlam : nullptr, (long long)tok * H,
+                                    stream);
+  return e == hipSuccess ? QDELTA_OK : QDELTA_EHIP;
+}
+
+int qdelta_recurrent_bwd(int32_t B, int32_t T, int32_t H, int32_t Dk, int32_t Dv, int32_t dtype,
+                         const void* q, const void* k, const void* v, const float* beta,
+                         const float* lam, float lam_scalar, const float* log_alpha,
+                         const float* initial_state, const void* d_o, const float* d_final_state,
+                         void* dq, void* dk, void* dv, float* dbeta, float* dlam, float* dlog_alpha,
+                         float* d_initial_state, void* ws, size_t ws_bytes, hipStream_t stream) {
+  return rec_bwd_impl(false, B, T, B, nullptr, H, Dk, Dv, dtype, q, k, v, beta, lam, lam_scalar, log_alpha,
+                      initial_state, d_o, d_final_state, dq, dk, dv, dbeta, dlam, dlog_alpha, d_initial_state, ws,
+                      ws_bytes, stream);
+}
+
+int qdelta_recurrent_bwd_varlen(int32_t T, int32_t N, const int32_t* cu_seqlens, int32_t H, int32_t Dk,
+                                int32_t Dv, int32_t dtype, const void* q, const void* k, const void* v,
+                                const float* beta, const float* lam, float lam_scalar,
+                                const float* log_alpha, const float* initial_state, const void* d_o,
+                                const float* d_final_state, void* dq, void* dk, void* dv, float* dbeta,
+                                float* dlam, float* dlog_alpha, float* d_initial_state, void* ws,
+                                size_t ws_bytes, hipStream_t stream) {
+  return rec_bwd_impl(true, 1, T, N, cu_seqlens, H, Dk, Dv, dtype, q, k, v, beta, lam, lam_scalar, log_alpha,
+                      initial_state, d_o, d_final_state, dq, dk, dv, dbeta, dlam, dlog_alpha, d_initial_state, ws,
+                      ws_bytes, stream);
+}
+
 int qdelta_l2norm_fwd(int64_t rows, int32_t D, int64_t ld_x, int32_t dtype, const void* x, void* y,
                       float* rnorm, hipStream_t stream) {
   if (rows < 0 || ld_x < D) return QDELTA_EINVAL;

@@ -18,7 +18,8 @@ enum Stage {
   ST_SEG_MAPS = 7,
   ST_SEG_COMPOSE = 8,
   ST_SEG_OUT = 9,
-  ST_COUNT = 10
+  ST_REC_BWD = 10,
+  ST_COUNT = 11
 };
 
 // Records a HIP event on `st` before (after == 0) or after (after == 1) a
@@ -55,6 +56,28 @@ hipError_t launch_rec_fwd(int N, int T, const int* cu, int T_total, int H, int D
                           int dtype, const void* q, const void* k, const void* v,
                           const float* beta, const float* lam, float lam_c, const float* la,
                           const float* S0, float* Sfin, void* o, hipStream_t st);
+
+// Arguments of the fully recurrent backward (one workgroup per (sequence,
+// head) unit).
+struct RecBwdArgs {
+  int T;                    // dense: tokens per sequence
+  const int* cu;            // varlen: cu_seqlens[N+1] (device), clamped to [0, T_total]
+  int T_total;
+  int H, DV;
+  const void *q, *k, *v, *dO;
+  const float *beta, *lam, *la, *S0, *dSfin;
+  float lam_c;              // lambda when lam is nullptr
+  void *dq, *dk, *dv;
+  float *dbeta, *dlam, *dla, *dS0;
+  float* wDL;               // per token-head gradient of a constant lambda (else nullptr)
+  float *wP, *wZ, *wDP, *wWK, *wF;   // workspace: [tok][H][DV] x3 and [tok][H][DK] fp32, [unit][DV] fp32
+};
+
+// Fully recurrent backward over `units` (sequence, head) units; when
+// dlam_sum is set, the constant lambda's gradient (sum of a.wDL over
+// n_tok_heads entries) is written there.
+hipError_t launch_rec_bwd(const RecBwdArgs& a, int units, int dtype, int Dk, float* dlam_sum, long long n_tok_heads,
+                          hipStream_t st);
 
 // Row L2 normalisation (bwd == 0: x -> out, rn_out) or its backward
 // (bwd == 1: y, rn_in, dy -> out).

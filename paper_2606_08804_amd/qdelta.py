@@ -18,6 +18,8 @@ chunk_bwd(q, k, v, beta, lam, log_alpha, initial_state, saved_states, d_o,
 recurrent_step(q, k, v, beta, lam, log_alpha, state) -> o        (state updated in place)
 recurrent_fwd(q, k, v, beta, lam=None, log_alpha=None, initial_state=None, cu_seqlens=None)
           -> (o, final_state)                                  (token by token, one launch)
+recurrent_bwd(q, k, v, beta, lam, log_alpha, initial_state, d_o, d_final_state=None,
+          cu_seqlens=None) -> dict of gradients                (token by token, one launch)
 l2norm_fwd(x) -> (y, rnorm);  l2norm_bwd(y, rnorm, dy) -> dx   (row L2 norm for the layer's q, k)
 
 lam: a [.., H] fp32 tensor (per token and head), a number (one constant for every
@@ -43,11 +45,12 @@ EXPORTS = (
     "qdelta_recurrent_fwd", "qdelta_recurrent_fwd_varlen", "qdelta_l2norm_fwd", "qdelta_l2norm_bwd",
     "qdelta_profile_begin", "qdelta_profile_end", "qdelta_chunk_fwd_noalloc",
     "qdelta_chunk_fwd_segmented", "qdelta_segmented_workspace_bytes", "qdelta_suggest_segments",
+    "qdelta_recurrent_workspace_bytes", "qdelta_recurrent_bwd", "qdelta_recurrent_bwd_varlen",
 )
 NOALLOC_SCRATCH_BYTES = 64 << 20
 
 STAGES = ("prep_fwd", "scan_fwd", "prep_bwd", "scan_bwd", "intra", "step", "rec_fwd", "seg_maps",
-          "seg_compose", "seg_out")
+          "seg_compose", "seg_out", "rec_bwd")
 
 _lib = None
 
@@ -101,6 +104,13 @@ def lib():
         L.qdelta_recurrent_fwd.restype = ctypes.c_int
         L.qdelta_recurrent_fwd_varlen.argtypes = [i32, i32, P] + [i32] * 4 + [P] * 5 + [f32] + [P] * 4 + [P]
         L.qdelta_recurrent_fwd_varlen.restype = ctypes.c_int
+        L.qdelta_recurrent_workspace_bytes.argtypes = [i32] * 6
+        L.qdelta_recurrent_workspace_bytes.restype = sz
+        # q, k, v, beta, lam, lam_scalar, log_alpha, S0, dO, dSf, dq, dk, dv, dbeta, dlam, dla, dS0, ws, bytes, stream
+        L.qdelta_recurrent_bwd.argtypes = [i32] * 6 + [P] * 5 + [f32] + [P] * 11 + [P, sz, P]
+        L.qdelta_recurrent_bwd.restype = ctypes.c_int
+        L.qdelta_recurrent_bwd_varlen.argtypes = [i32, i32, P] + [i32] * 4 + [P] * 5 + [f32] + [P] * 11 + [P, sz, P]
+        L.qdelta_recurrent_bwd_varlen.restype = ctypes.c_int
         i64 = ctypes.c_int64
         L.qdelta_l2norm_fwd.argtypes = [i64, i32, i64, i32, P, P, P, P]
         L.qdelta_l2norm_fwd.restype = ctypes.c_int
@@ -410,6 +420,53 @@ def recurrent_fwd(q, k, v, beta, lam=None, log_alpha=None, initial_state=None, c
         _check("qdelta_recurrent_fwd_varlen",
                L.qdelta_recurrent_fwd_varlen(T, N, _p(cu_seqlens), *common))
     return o, Sf
+
+
+def recurrent_workspace_bytes(B, T, H, Dk, Dv, n_seqs=0):
+    return int(lib().qdelta_recurrent_workspace_bytes(B, T, H, Dk, Dv, n_seqs))
+
+
+def recurrent_bwd(q, k, v, beta, lam, log_alpha, initial_state, d_o, d_final_state=None, cu_seqlens=None,
+                  need_d_initial_state=True, workspace=None):
+    """Backward of the fully recurrent form (token by token, one launch, no
+    saved context).  Same layouts and returned gradients as chunk_bwd."""
+    L = lib()
+    dt = _dt(q)
+    B, T, H, Dk, Dv, N = _dims(q, v, cu_seqlens)
+    act = q.shape[:-1]
+    _need(q, "q", q.dtype)
+    _need(k, "k", q.dtype, q.shape)
+    _need(v, "v", q.dtype, tuple(act) + (Dv,))
+    _need(beta, "beta", torch.float32, act)
+    lam_t, lam_c = _lam(lam, act)
+    _opt(log_alpha, "log_alpha", torch.float32, act)
+    _opt(initial_state, "initial_state", torch.float32, (N, H, Dv, Dk))
+    _need(d_o, "d_o", q.dtype, tuple(act) + (Dv,))
+    _opt(d_final_state, "d_final_state", torch.float32, (N, H, Dv, Dk))
+    if cu_seqlens is not None:
+        _need(cu_seqlens, "cu_seqlens", torch.int32)
+    dev = q.device
+    dq, dk, dv = torch.empty_like(q), torch.empty_like(k), torch.empty_like(v)
+    dbeta = torch.empty_like(beta)
+    if lam_t is not None:
+        dlam = torch.empty_like(lam_t)
+    elif lam is not None:
+        dlam = torch.empty((), dtype=torch.float32, device=dev)
+    else:
+        dlam = None
+    dla = torch.empty_like(log_alpha) if log_alpha is not None else None
+    dS0 = torch.empty((N, H, Dv, Dk), dtype=torch.float32, device=dev) if need_d_initial_state else None
+    n_seqs = N if cu_seqlens is not None else 0
+    nbytes = recurrent_workspace_bytes(B, T, H, Dk, Dv, n_seqs)
+    ws = _workspace(nbytes, dev, workspace)
+    common = (H, Dk, Dv, dt, _p(q), _p(k), _p(v), _p(beta), _p(lam_t), lam_c, _p(log_alpha), _p(initial_state),
+              _p(d_o), _p(d_final_state), _p(dq), _p(dk), _p(dv), _p(dbeta), _p(dlam), _p(dla), _p(dS0),
+              _p(ws), nbytes, _stream())
+    if cu_seqlens is None:
+        _check("qdelta_recurrent_bwd", L.qdelta_recurrent_bwd(B, T, *common))
+    else:
+        _check("qdelta_recurrent_bwd_varlen", L.qdelta_recurrent_bwd_varlen(T, N, _p(cu_seqlens), *common))
+    return dict(dq=dq, dk=dk, dv=dv, dbeta=dbeta, dlam=dlam, dlog_alpha=dla, d_initial_state=dS0)
 
 
 def l2norm_fwd(x):

@@ -22,7 +22,7 @@ def header_functions():
 def test_library_exports_every_declared_symbol():
     L = qdelta.lib()
     names = header_functions()
-    assert len(names) == 20
+    assert len(names) == 23
     for n in names:
         assert hasattr(L, n), n
     assert sorted(names) == sorted(qdelta.EXPORTS)
@@ -152,6 +152,32 @@ def test_segmented_forward_sizes_and_validation():
     assert call(ws_bytes=qdelta.workspace_bytes(1, 640, 2, 64, 64, 1)) == E.QDELTA_ENOWORKSPACE
     assert qdelta.suggest_segments(4, 4096, 16, 128, 128) == 1
     assert qdelta.suggest_segments(1, 65536, 2, 128, 128) > 1
+
+
+def test_recurrent_bwd_sizes_and_validation():
+    L = qdelta.lib()
+    E = qdelta
+    f = FAKE
+    # per token-head 3 Dv + Dk + 1 fp32, per (sequence, head) Dv fp32 (each region 256-byte aligned)
+    r = lambda b: (b + 255) // 256 * 256
+    tok, H, Dk, Dv = 64 * 16, 16, 128, 128
+    assert qdelta.recurrent_workspace_bytes(64, 16, H, Dk, Dv) == \
+        3 * r(tok * H * Dv * 4) + r(tok * H * Dk * 4) + r(64 * H * Dv * 4) + r(tok * H * 4)
+    assert qdelta.recurrent_workspace_bytes(1, 8, 1, 64, 96) == 0
+
+    def call(Dk=64, Dv=64, dtype=1, lam=f, dlam=f, la=None, dla=None, ws_bytes=1 << 40, dq=f):
+        return L.qdelta_recurrent_bwd(1, 8, 1, Dk, Dv, dtype, f, f, f, f, lam, 0.5, la, None, f, None, dq, f, f, f,
+                                      dlam, dla, None, f, ws_bytes, None)
+
+    assert call(Dv=96) == E.QDELTA_EUNSUPPORTED
+    assert call(dtype=5) == E.QDELTA_EINVAL
+    assert call(dq=None) == E.QDELTA_EINVAL
+    assert call(la=f) == E.QDELTA_EINVAL                  # log alpha without its gradient
+    assert call(dlam=None) == E.QDELTA_EINVAL             # per-token lambda without its gradient
+    assert call(lam=None, dlam=f + 2) == E.QDELTA_EINVAL  # constant lambda's gradient: one aligned float
+    assert call(ws_bytes=16) == E.QDELTA_ENOWORKSPACE
+    assert L.qdelta_recurrent_bwd_varlen(8, 1, None, 1, 64, 64, 1, f, f, f, f, f, 0.0, None, None, f, None, f, f, f,
+                                         f, f, None, None, f, 1 << 40, None) == E.QDELTA_EINVAL
 
 
 def test_bwd_and_varlen_reject_bad_arguments():
