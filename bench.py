@@ -52,7 +52,9 @@ VALU_F32_PEAK = 157.3e12   # flop/s, MI355X fp32 vector (256 CUs x 2.4 GHz)
 MFMA_BF16_PEAK = 2.5e15    # flop/s, dense bf16 MFMA
 MFMA_F32_PEAK = 157.3e12   # flop/s, dense fp32 MFMA
 C = 64
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_train_bf16_B4_T4096_H16_d128.json")
+# committed FETCH_SIZE / WRITE_SIZE summaries, one per workload
+TRAFFIC_FILES = {w: os.path.join(ROOT, "profiles", f"traffic_{w}.json")
+                 for w in ("train", "fwd", "long", "decode", "varlen", "tiny", "recurrent")}
 
 
 def fwd_flops_per_token_head(Dk, Dv):
@@ -154,29 +156,31 @@ def handoff_bytes_per_unit(stage, Dk, Dv, e, saved=True):
     raise KeyError(stage)
 
 
-# Sources that build the chunk kernels the stored counters were taken on (the
-# decode kernel's own file is left out: it does not run in the training step).
-CHUNK_SOURCES = ("qd_api.hip", "qd_bwd.hip", "qd_common.h", "qd_fwd.hip", "qd_launch.h")
+# Sources of the kernels whose counters are stored: the kernel files and the
+# workspace layout.  A stored summary applies only while they hash to the
+# digest stored with it.
+KERNEL_SOURCES = ("qd_api.hip", "qd_bwd.hip", "qd_common.h", "qd_fwd.hip", "qd_rec_bwd.hip", "qd_step.hip")
 
 
 def source_digest():
-    """Digest of the chunk-kernel sources, to tell whether stored counters still apply."""
+    """Digest of the kernel sources, to tell whether stored counters still apply."""
     h = hashlib.sha256()
     csrc = os.path.join(ROOT, "paper_2606_08804_amd", "csrc")
-    for f in CHUNK_SOURCES:
+    for f in KERNEL_SOURCES:
         with open(os.path.join(csrc, f), "rb") as fh:
             h.update(f.encode())
             h.update(fh.read())
     return h.hexdigest()[:16]
 
 
-def stored_traffic(stage):
-    """HBM bytes per launch from the committed rocprofv3 counter summary, or
-    None when there is none or the kernels changed since it was taken."""
+def stored_traffic(workload, stage):
+    """HBM bytes per launch of a stage from the committed rocprofv3 counter
+    summary of a workload, or None when there is none or the kernels changed
+    since it was taken."""
     try:
-        with open(TRAFFIC_FILE) as f:
+        with open(TRAFFIC_FILES[workload]) as f:
             t = json.load(f)
-    except (OSError, ValueError):
+    except (KeyError, OSError, ValueError):
         return None
     if t.get("source_digest") != source_digest():
         return None
@@ -411,7 +415,8 @@ def run_chunk(args, wid, with_bwd):
     value = tokens / (ms / 1e3)
     kern = kernel_rooflines(stages, d, Dk, Dv, e, with_bwd)
     dom = max(kern, key=lambda s: kern[s]["avg_launch_us"])
-    traffic = stored_traffic(dom) if wid == 3 else None
+    wname = {v: k for k, v in WORKLOAD_IDS.items()}[wid]
+    traffic = stored_traffic(wname, dom)
     fl = fwd_flops_per_token_head(Dk, Dv) + (bwd_flops_per_token_head(Dk, Dv) if with_bwd else 0)
     peak = MFMA_BF16_PEAK if w.dtype == "bf16" else MFMA_F32_PEAK
     nseq = (B if n_seqs == 0 else n_seqs) * H
@@ -432,10 +437,9 @@ def run_chunk(args, wid, with_bwd):
     if n_seg > 1:
         cfg["segments"] = n_seg
     step_traffic = None
-    if wid == 3:
-        per = [stored_traffic(s) for s in kern]
-        if all(x is not None for x in per):
-            step_traffic = int(sum(x * stages[s][1] / args.steps for x, s in zip(per, kern)))
+    per = [stored_traffic(wname, s) for s in kern]
+    if all(x is not None for x in per):
+        step_traffic = int(sum(x * stages[s][1] / args.steps for x, s in zip(per, kern)))
     out = {
         "metric": metric, "value": value, "unit": "tokens/s", "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": ms, "higher_is_better": True, "scaling": "weak",
@@ -613,7 +617,7 @@ def run_decode(args):
         "us_per_decode_step": ms * 1e3 / steps_dec,
         "kernel_avg_us": {"step": round(avg_s * 1e6, 2)},
         "kernels": kern,
-        "roofline": roofline_of(kern, "step", None),
+        "roofline": roofline_of(kern, "step", stored_traffic("decode", "step")),
     }
     if not args.no_cpu:
         from oracle import build as obuild
