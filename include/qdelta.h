@@ -41,9 +41,11 @@
  *    the scratch array of qdelta_chunk_fwd_noalloc, there is no global mutable
  *    state; calls on different streams may overlap provided their workspaces
  *    and outputs do not.
- *  - Supported: Dk in {64, 128}; Dv in {64, 128, 256}; chunk == 64; T >= 0 need
- *    not be a multiple of chunk.  QDELTA_F32 additionally requires Dk == 64.
- *    Anything else returns QDELTA_EUNSUPPORTED.
+  *  - Supported: Dk in {64, 128}; Dv in {64, 128, 256}; chunk == 64; T >= 0 need
+ *    not be a multiple of chunk.  The chunk entry points additionally require
+ *    Dk == 64 for QDELTA_F32 (their fp32 operand tiles at Dk == 128 exceed the
+ *    160 KB of LDS of a compute unit).  Anything else returns
+ *    QDELTA_EUNSUPPORTED.
  *
  * Sequence layouts
  * ----------------
