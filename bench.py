@@ -591,14 +591,39 @@ def run_decode(args):
     S = S0.clone()
     outs = torch.empty((steps_dec, N, H, D), dtype=torch.bfloat16, device="cuda")
 
-    def step():
-        S.copy_(S0)
+    def decode_all():
         for s in range(steps_dec):
             qdelta.recurrent_step(q[s], k[s], v[s], beta[s], lam[s], None if la is None else la[s], S,
                                   out=outs[s])
 
-    # a benchmark step here is 1024 launches (tens of milliseconds)
-    ms, stages, n_settle = timed(step, min(args.steps, 10), min(args.warmup, 3), args.settle_ms)
+    def eager_step():
+        S.copy_(S0)
+        decode_all()
+
+    # the 1024 launches of a step captured once into a HIP graph (a serving
+    # loop's form: no host launch per token); the state reset stays outside
+    # the graph as ordinary stream work
+    torch.cuda.synchronize()
+    S.copy_(S0)
+    graph = torch.cuda.CUDAGraph()
+    cap = torch.cuda.Stream()
+    cap.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(cap):
+        decode_all()                      # one eager pass on the capture stream before capturing
+        torch.cuda.synchronize()
+        S.copy_(S0)
+        with torch.cuda.graph(graph, stream=cap):
+            decode_all()
+    torch.cuda.current_stream().wait_stream(cap)
+    torch.cuda.synchronize()
+
+    def graph_step():
+        S.copy_(S0)
+        graph.replay()
+
+    # a benchmark step here is 1024 decode steps (tens of milliseconds)
+    ms, stages, n_settle = timed(eager_step, min(args.steps, 10), min(args.warmup, 3), args.settle_ms)
+    ms_graph, _, _ = timed(graph_step, min(args.steps, 10), min(args.warmup, 3), 0)
     tokens = N * steps_dec
     tot_ms, launches = stages["step"]
     avg_s = tot_ms / launches / 1e3
@@ -612,9 +637,12 @@ def run_decode(args):
         "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
         "config": {"workload": "decode 64 seqs x 1024 steps H16 d128", "N": N, "H": H, "Dk": D, "Dv": D,
                    "decode_steps": steps_dec, "gate_mode": args.gate, "parallelism": "single GPU",
-                   "note": "a benchmark step is all 1024 decode steps (one launch each) plus one state reset copy"},
+                   "note": "a benchmark step is all 1024 decode steps (one launch each) plus one state reset "
+                           "copy; graph_* is the same step replayed from a captured HIP graph"},
         "clock_settle_steps": n_settle,
         "us_per_decode_step": ms * 1e3 / steps_dec,
+        "graph_ms_per_step": ms_graph,
+        "graph_us_per_decode_step": ms_graph * 1e3 / steps_dec,
         "kernel_avg_us": {"step": round(avg_s * 1e6, 2)},
         "kernels": kern,
         "roofline": roofline_of(kern, "step", stored_traffic("decode", "step")),
