@@ -290,6 +290,11 @@ __global__ __launch_bounds__(NCW * 64 + 256) void k_scan_fwd(Params p) {
   typedef typename Mma<E>::frag FR;
   typedef ScanFwdRing<E, DK, BV> R;
   constexpr int NA = R::NA;
+  // the maps pass produces no output: it loads no P, and its map tiles load
+  // no V (their V product is skipped), so their set B is T alone
+  constexpr bool MAPS = SEG == SEG_MAPS;
+  static_assert(!MAPS || (NA == 2 && R::NP == 1), "the maps pass runs the two-deep ring with one P buffer");
+  constexpr int LT = C * R::RC / 1024 / 4;    // loads per producer: T alone
   __shared__ ScanFwdSmem<E, DK, BV> sm;
   const int tid = threadIdx.x, lane = tid & 63, w = wave_id(tid);
   const int prod = w - NCW;                   // 0-3 for the producer waves, negative otherwise
@@ -344,6 +349,7 @@ __global__ __launch_bounds__(NCW * 64 + 256) void k_scan_fwd(Params p) {
   };
   // producers: P of chunk c
   auto issueP = [&](int c) {
+    if constexpr (MAPS) return;
     size_t gi, arow;
     int len;
     chunk_at(c, gi, arow, len);
@@ -359,8 +365,9 @@ __global__ __launch_bounds__(NCW * 64 + 256) void k_scan_fwd(Params p) {
     const char* Tg = (const char*)((const E*)p.wT + gi * C * C);
     const char* Vg = (const char*)((const E*)p.v + arow * DV + v0);
     dma_rows<R::RC, C, 4, true>(sm.ringB + R::BT, Tg, R::RC, C, Tg, 0, prod, lane);
-    dma_rows<R::RO, C, 4, true>(sm.ringB + R::BV_, Vg, (size_t)H * DV * ES, len, Vg + (size_t)(len - 1) * H * DV * ES, 0,
-                                prod, lane);
+    if (!map_tile)
+      dma_rows<R::RO, C, 4, true>(sm.ringB + R::BV_, Vg, (size_t)H * DV * ES, len,
+                                  Vg + (size_t)(len - 1) * H * DV * ES, 0, prod, lane);
   };
 
   // state: acc[i][j] = S^T rows 16 (kb0 + i).., columns 16 (ns0 + j).. of this tile
@@ -474,9 +481,15 @@ __global__ __launch_bounds__(NCW * 64 + 256) void k_scan_fwd(Params p) {
       const bool q_next = c + NA - 1 < nch, p_next = c + R::NP - 1 < nch;
       if (q_next) issueQ(c + NA - 1);
       if (p_next) issueP(c + R::NP - 1);
-      if (q_next && p_next) wait_vm<R::LQ + R::LP>();
-      else if (p_next) wait_vm<R::LP>();
-      else wait_vm<0>();
+      if constexpr (MAPS) {
+        // set B of chunk c was issued before Q of chunk c+1
+        if (q_next) wait_vm<R::LQ>();
+        else wait_vm<0>();
+      } else {
+        if (q_next && p_next) wait_vm<R::LQ + R::LP>();
+        else if (p_next) wait_vm<R::LP>();
+        else wait_vm<0>();
+      }
     }
     block_sync_lds();                      // B_b: Y staged; set B of chunk c visible
     // ---- phase 3
@@ -507,7 +520,9 @@ __global__ __launch_bounds__(NCW * 64 + 256) void k_scan_fwd(Params p) {
       // K and gates of chunk c+NA-1; then P of chunk c must have landed
       const bool k_next = c + NA - 1 < nch;
       if (k_next) issueK(c + NA - 1);
-      if constexpr (R::NP == 1) {
+      if constexpr (MAPS) {
+        // no P to wait for
+      } else if constexpr (R::NP == 1) {
         // issued in this chunk's phase 2: only the K loads follow
         if (!k_next) wait_vm<0>();
         else if (prod < 3) wait_vm<R::LK + 1>();
@@ -577,7 +592,8 @@ __global__ __launch_bounds__(NCW * 64 + 256) void k_scan_fwd(Params p) {
       // set A of chunk c+1 complete: what was issued after its last part may
       // still be in flight
       if constexpr (NA == 2) {
-        wait_vm<R::LB>();
+        if (MAPS && map_tile) wait_vm<LT>();
+        else wait_vm<R::LB>();
       } else {
         if (c == cbeg) {
           // set A of chunk 1 came with the prologue, which waited for it
