@@ -103,3 +103,13 @@ def test_recurrent_bwd_training_shape_sampled_heads():
     gs = {k: (None if v is None else (v[:, heads] if k == "d_initial_state" else v[:, :, heads]).contiguous())
           for k, v in g.items()}
     _check(bwd_errors(ds, gs), TOL["bf16"], "rec bwd B64 T16 H16")
+
+
+@pytest.mark.parametrize("dt,D,gate,T", [("f32", 64, "G3", 2048), ("f32", 64, "G1", 2048), ("bf16", 128, "G2", 4096)])
+def test_recurrent_bwd_long_sequences(dt, D, gate, T):
+    """The reverse sweep carries the per-row scalar <G_t, S_t> through every
+    token instead of the states: long sequences (slow decay, no decay) stay
+    within the tolerance, dlog alpha included."""
+    d = synth.make(1, T, 2, D, D, dt, gate, seed=190, s0=True, with_do=True)
+    g = rec_bwd(d)
+    _check(bwd_errors(d, g), TOL[dt], f"rec bwd {dt} {gate} T={T}")
