@@ -673,9 +673,9 @@ static hipError_t launch_fwd_t(const Params& p, int in_bwd, int with_scan, hipSt
 // Entry states of the segments of every (sequence, head): S_0 = the initial
 // state (or zero), S_{g+1} = S_g A_g + B_g with segment g's map from the
 // SEG_MAPS pass, in fp32.  One workgroup per (sequence, head, 8 value rows)
-// walks the segments in order: each step stages A_g in LDS with coalesced
-// 16-byte loads (all issued before the first use), then every thread forms
-// one column of its rows from LDS.
+// walks the segments in order: each step stages A_g in LDS (coalesced
+// 16-byte loads, issued one step ahead so that their latency overlaps the
+// previous step), then every thread forms one column of its rows from LDS.
 constexpr int SEG_COMPOSE_RB = 8;
 template <int DK, int DV>
 __global__ __launch_bounds__(NTHREADS) void k_seg_compose(Params p) {
@@ -686,17 +686,28 @@ __global__ __launch_bounds__(NTHREADS) void k_seg_compose(Params p) {
   static_assert(RB * DK % NTHREADS == 0 && NTHREADS % DK == 0 && AV * 4 * NTHREADS == DK * DK,
                 "thread mapping");
   __shared__ __align__(16) float Am[DK][DK];
-  __shared__ float Srow[RB][DK];
+  __shared__ __align__(16) float Srow[RB][DK];
   const int nrb = DV / RB;
   const int unit = blockIdx.x / nrb, rb = blockIdx.x % nrb, tid = threadIdx.x;
   const int G = p.n_seg;
   const int k = tid % DK, rsub = tid / DK;     // column k; rows rsub, rsub + TPR, ...
-  float cur[RPT];
+  float cur[RPT], bn[RPT];
+  f4 av[AV];
+  // map g's A (registers) and B rows of this thread, loaded one step ahead
+  auto fetch = [&](int g) {
+    const float* Bm = p.wSegOut + ((size_t)unit * G + g) * (DV + DK) * DK;
+    const f4* Ag = (const f4*)(Bm + (size_t)DV * DK);
+#pragma unroll
+    for (int i = 0; i < AV; ++i) av[i] = Ag[tid + i * NTHREADS];
+#pragma unroll
+    for (int m = 0; m < RPT; ++m) bn[m] = Bm[(size_t)(rb * RB + rsub + m * TPR) * DK + k];
+  };
 #pragma unroll
   for (int m = 0; m < RPT; ++m) {
     const int v = rb * RB + rsub + m * TPR;
     cur[m] = p.S0 ? p.S0[((size_t)unit * DV + v) * DK + k] : 0.f;
   }
+  if (G > 1) fetch(0);
   for (int g = 0; g < G; ++g) {
     const size_t su = (size_t)unit * G + g;
 #pragma unroll
@@ -706,22 +717,21 @@ __global__ __launch_bounds__(NTHREADS) void k_seg_compose(Params p) {
       Srow[rsub + m * TPR][k] = cur[m];
     }
     if (g + 1 == G) break;
-    const float* Bm = p.wSegOut + su * (DV + DK) * DK;
-    const f4* Ag = (const f4*)(Bm + (size_t)DV * DK);
-    f4 av[AV];
-#pragma unroll
-    for (int i = 0; i < AV; ++i) av[i] = Ag[tid + i * NTHREADS];
-#pragma unroll
-    for (int m = 0; m < RPT; ++m) cur[m] = Bm[(size_t)(rb * RB + rsub + m * TPR) * DK + k];
 #pragma unroll
     for (int i = 0; i < AV; ++i) ((f4*)&Am[0][0])[tid + i * NTHREADS] = av[i];
-    __syncthreads();
-    // next entry: rows of S_g A_g + B_g
-#pragma unroll 8
-    for (int r = 0; r < DK; ++r) {
-      const float a = Am[r][k];
 #pragma unroll
-      for (int m = 0; m < RPT; ++m) cur[m] += Srow[rsub + m * TPR][r] * a;
+    for (int m = 0; m < RPT; ++m) cur[m] = bn[m];
+    if (g + 2 < G) fetch(g + 1);                 // in flight during this step
+    __syncthreads();
+    // next entry: rows of S_g A_g + B_g (four state columns per LDS read)
+#pragma unroll 4
+    for (int r = 0; r < DK; r += 4) {
+      const float a0 = Am[r][k], a1 = Am[r + 1][k], a2 = Am[r + 2][k], a3 = Am[r + 3][k];
+#pragma unroll
+      for (int m = 0; m < RPT; ++m) {
+        const f4 sr = *(const f4*)&Srow[rsub + m * TPR][r];
+        cur[m] += sr[0] * a0 + sr[1] * a1 + sr[2] * a2 + sr[3] * a3;
+      }
     }
     __syncthreads();                           // Am and Srow are rewritten in the next step
   }
