@@ -113,3 +113,13 @@ def test_recurrent_bwd_long_sequences(dt, D, gate, T):
     d = synth.make(1, T, 2, D, D, dt, gate, seed=190, s0=True, with_do=True)
     g = rec_bwd(d)
     _check(bwd_errors(d, g), TOL[dt], f"rec bwd {dt} {gate} T={T}")
+
+
+def test_recurrent_bwd_empty_sequences():
+    """T = 0: no token gradients; the initial-state gradient is the
+    final-state gradient passed straight through."""
+    d = synth.make(2, 0, 2, 128, 128, "bf16", "G2", seed=191, s0=True, with_do=True)
+    dSf = _dsf(d, 192)
+    g = rec_bwd(d, dSf)
+    assert g["dq"].numel() == 0
+    assert torch.equal(g["d_initial_state"].cpu(), dSf)

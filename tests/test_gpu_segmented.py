@@ -74,3 +74,14 @@ def test_segmented_long_context_full(gate):
     o_ref, S_ref = oracle_fwd(ds)
     assert normwise(f64(o[:, :, heads].cpu()), o_ref) <= TOL["bf16"]
     assert normwise(f64(Sf[:, heads].cpu()), S_ref) <= TOL["bf16"]
+
+
+def test_segmented_empty_inputs():
+    """T = 0 passes the initial state through; B = 0 launches nothing."""
+    d = synth.make(2, 0, 2, 128, 128, "bf16", "G2", seed=175, s0=True)
+    o, Sf, _ = seg_fwd(d, 4)
+    assert o.shape == (2, 0, 2, 128)
+    assert torch.equal(Sf.cpu(), d["initial_state"])
+    d0 = synth.make(0, 128, 2, 128, 128, "bf16", "G2", seed=176, s0=False)
+    o0, Sf0, _ = seg_fwd(d0, 4)
+    assert o0.shape == (0, 128, 2, 128) and Sf0.shape == (0, 2, 128, 128)
