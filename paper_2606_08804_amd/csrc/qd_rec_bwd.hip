@@ -27,8 +27,8 @@
 // sweeps over its tokens:
 //   A (forward)  recompute the states; store p_t and z_t = dO_t * o_t per row, and F_T;
 //   B (reverse)  carry G; write dv, dbeta, dlog alpha, dp_t and sum_i e_i G[i,:];
-//   C (forward)  recompute the states; the column sums S^T dO, S^T dp and
-//                dO . e give dq, dk and dlambda.
+//   C (forward)  recompute the states (p_t read back from sweep A); the
+//                column sums S^T dO, S^T dp and dO . e give dq, dk and dlambda.
 // Every sweep has the layout of the recurrent forward: a state row is held
 // by a group of 8 lanes (Dk / 8 columns each), 32 groups hold Dv / 32 rows
 // each.  Row dot products reduce over the 8 lanes with DPP; sums over rows
@@ -135,7 +135,7 @@ struct alignas(16) RecBwdSmem {
   alignas(16) E v[2][RB_TB][DVP];
   alignas(16) E dO[2][RB_TB][DVP];
   alignas(16) float a[2][RB_TB][DVP];        // B: p_t;  C: dp_t
-  alignas(16) float b[2][RB_TB][DVP];        // B: z_{t-1}
+  alignas(16) float b[2][RB_TB][DVP];        // B: z_{t-1};  C: p_t
   alignas(16) float g[2][3][RB_TB];          // beta, lambda, log alpha
   float pv[RB_TB][4][2][DK];                 // per-wave column sums (B: e G; C: S^T dO, S^T dp)
   float ps[RB_TB][4][2];                     // per-wave row-scalar sums
@@ -173,7 +173,7 @@ __global__ __launch_bounds__(RB_NT) void k_rec_bwd(RecBwdArgs a) {
   Rows<DV * 4> ra, rb2;
   float rg = 0.f;
   // stages the block starting at token tb; `sweep` selects the per-row
-  // arrays (A: none; B: p_t and z_{t-1}; C: dp_t)
+  // arrays (A: none; B: p_t and z_{t-1}; C: dp_t and p_t)
   auto load = [&](int tb, int sweep) {
     rq.load(qb, rowK, tb, t0, t1, tid);
     rk.load(kb, rowK, tb, t0, t1, tid);
@@ -184,6 +184,7 @@ __global__ __launch_bounds__(RB_NT) void k_rec_bwd(RecBwdArgs a) {
       rb2.load((const char*)a.wZ + (size_t)h * DV * 4, rowF, tb - 1, t0, t1 - 1, tid);   // z_{t-1}
     } else if (sweep == 2) {
       ra.load((const char*)a.wDP + (size_t)h * DV * 4, rowF, tb, t0, t1, tid);
+      rb2.load((const char*)a.wP + (size_t)h * DV * 4, rowF, tb, t0, t1, tid);
     }
     rg = 0.f;
     if (tid < 3 * RB_TB) {
@@ -200,7 +201,7 @@ __global__ __launch_bounds__(RB_NT) void k_rec_bwd(RecBwdArgs a) {
     rv.store((char*)&sm.v[buf][0][0], tid);
     ro.store((char*)&sm.dO[buf][0][0], tid);
     if (sweep >= 1) ra.store((char*)&sm.a[buf][0][0], tid);
-    if (sweep == 1) rb2.store((char*)&sm.b[buf][0][0], tid);
+    if (sweep >= 1) rb2.store((char*)&sm.b[buf][0][0], tid);
     if (tid < 3 * RB_TB) sm.g[buf][tid / RB_TB][tid % RB_TB] = rg;
   };
   // per-token operands of this lane: q, k, x = k + lambda q, and the gates
@@ -403,15 +404,14 @@ __global__ __launch_bounds__(RB_NT) void k_rec_bwd(RecBwdArgs a) {
     if (bk + 1 < nblk) load(tb + RB_TB, 2);
     for (int tt = 0; tt < nt; ++tt) {
       token(buf, tt);
-      float w1[CPL], w2[CPL], cs = 0.f, pm[RPT];
+      float w1[CPL], w2[CPL], cs = 0.f;
 #pragma unroll
       for (int j = 0; j < CPL; ++j) w1[j] = w2[j] = 0.f;
 #pragma unroll
-      for (int m = 0; m < RPT; ++m) pm[m] = dot(st[m], xv);
-#pragma unroll
       for (int m = 0; m < RPT; ++m) {
+        // p_t = S_{t-1} x_t as sweep A computed it from the same states
         const float dOi = tof(sm.dO[buf][tt][row(m)]), dpi = sm.a[buf][tt][row(m)];
-        const float e = bt * (tof(sm.v[buf][tt][row(m)]) - al * pm[m]);
+        const float e = bt * (tof(sm.v[buf][tt][row(m)]) - al * sm.b[buf][tt][row(m)]);
         cs += dOi * e;
 #pragma unroll
         for (int j = 0; j < CPL; ++j) {
