@@ -146,11 +146,11 @@ def handoff_bytes_per_unit(stage, Dk, Dv, e, saved=True):
         # activation dtype and D when the context is kept)
         b = 3 * gates + 2 * act_qk + 2 * cc_e + act_v + act_v
         return b + (state * e // 4 + act_v if saved else 0)
-    if stage == "scan_bwd":      # gate block, P, M, k, q, dO -> dS' (dtype), dD, dv
-        return 3 * gates + 2 * cc_e + 2 * act_qk + act_v + state * e // 4 + act_v + act_v
-    if stage == "intra":         # gate block, S, dS' (dtype), D, dD, dO, v, q, k, M
+    if stage == "scan_bwd":      # gate block, P, M, k, q, dO -> dS' (dtype), dv
+        return 3 * gates + 2 * cc_e + 2 * act_qk + act_v + state * e // 4 + act_v
+    if stage == "intra":         # gate block, S, dS' (dtype), D, dO, v, q, k, P, M
         #                          -> dq, dk, dbeta, dlam, dlog_alpha
-        return 3 * gates + 2 * state * e // 4 + 4 * act_v + 2 * act_qk + cc_e + 2 * act_qk + 3 * gates
+        return 3 * gates + 2 * state * e // 4 + 3 * act_v + 2 * act_qk + 2 * cc_e + 2 * act_qk + 3 * gates
     if stage in ("seg_maps", "seg_out", "seg_compose"):
         return 0                 # per-segment figures, not per unit
     raise KeyError(stage)

@@ -18,7 +18,7 @@ constexpr int kVersion = 10000;  // 1.0.0
 
 struct Layout {
   size_t wb = 0, wT = 0, wP = 0;   // forward: chunk factors (T always, gates and P when no saved context is kept)
-  size_t dSo = 0, dDb = 0, ctx = 0;        // backward: scan outputs, room to recompute the context
+  size_t dSo = 0, ctx = 0;                 // backward: scan output dS', room to recompute the context
   size_t dlam = 0;                         // backward: per-unit partials of a constant lambda's gradient
   size_t total = 0;
 };
@@ -51,7 +51,6 @@ Layout make_layout(size_t units, int Dk, int Dv, int esz, bool bwd) {
   L.wT = take(units * C * C * esz);
   if (bwd) {
     L.dSo = take(units * (size_t)Dv * Dk * esz);
-    L.dDb = take(units * C * Dv * esz);
     L.ctx = take(ctx_layout(units, Dk, Dv, esz).total);
     L.dlam = take(units * sizeof(float));
   } else {
@@ -251,7 +250,6 @@ int bwd_impl(bool varlen, int32_t B, int32_t T, int32_t N, const int32_t* cu, in
   p.dlam_sum = dlam_const ? dlam : nullptr;
   p.w_dlam = dlam_const ? reinterpret_cast<float*>(w + L.dlam) : nullptr;
   p.w_dSo = w + L.dSo;
-  p.w_dDb = w + L.dDb;
   const size_t units = s.slots * (size_t)H;
   hipError_t e = hipSuccess;
   if (saved) {

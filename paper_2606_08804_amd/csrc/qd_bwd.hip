@@ -10,6 +10,7 @@
 //     dS   = g_C dS' + dO^T diag(g) Q - dD^T W    (gradient w.r.t. the entry state)
 //          = g_C dS' + (dO - diag(lambda) dV)^T diag(g) Q - dV^T diag(g) K
 //   intra-chunk (parallel over chunks):
+//     dD   (formed again from dS', dO and P, exactly as the scan formed it)
 //     D    = U - W S^T
 //     dQ   = diag(g) dO S + dQK K + diag(lambda) dX,      dQK = Gam * M * (dO D^T)
 //     dK   = diag(g_C/g) D dS' + dQK^T Q + dG^T X + dX
@@ -23,8 +24,8 @@
 //     every term through g, Gam, Kbar and g_C.
 //
 // k_scan_bwd  : one workgroup per (sequence, head, Dv tile); dS^T tile in fp32
-//               accumulators; per chunk writes dD and dS' and produces dV.
-// k_bwd_intra : per (chunk, head); the products that contract over Dv
+//               accumulators; per chunk writes dS' and produces dV.
+// k_bwd_intra : per (chunk, head); dD, then the products that contract over Dv
 //               (dO S, D dS', dD S, dO D^T, dD V^T), then the UT-solve backward
 //               and the products over Dk; final dq, dk, dbeta, dlambda, dlog alpha.
 #include "qd_common.h"
@@ -106,7 +107,7 @@ __global__ __launch_bounds__(NCW * 64 + 256) void k_scan_bwd(Params p) {
   constexpr int LK = DK + P, LV = BV + P;
   constexpr int NVT = DV / BV;
   constexpr int NB = BV / 16;
-  constexpr int KS = Mma<E>::KS, KPL = Mma<E>::KPL;
+  constexpr int KS = Mma<E>::KS;
   constexpr int NKS = DK / KS;
   constexpr int NCT = NCW * 64;               // compute threads
   constexpr int NBW = NB / (NCW / 4);         // value blocks per wave in phases 2-3
@@ -276,15 +277,6 @@ __global__ __launch_bounds__(NCW * 64 + 256) void k_scan_bwd(Params p) {
     block_sync_lds();                      // B_b: dD staged; M of this chunk visible
     // ---- phase 3
     if (!producer) {
-      {
-        // dD rows for the intra-chunk kernel
-        constexpr int VEC = 16 / sizeof(E), PR = BV / VEC;
-        E* ddst = (E*)p.w_dDb + gi * C * DV + v0;
-        for (int idx = tid; idx < C * PR; idx += NCT) {
-          const int r = idx / PR, cc = (idx % PR) * VEC;
-          *(uint4*)(ddst + (size_t)r * DV + cc) = *(const uint4*)&sm.dD[r][cc];
-        }
-      }
       // dV^T (value rows, chunk columns 16 cb..) = beta_r (dD^T M); M is lower
       // triangular (k blocks before this wave's rows are zero).  Each
       // lane holds four consecutive values of row rr: dV goes out directly,
@@ -385,7 +377,11 @@ __global__ __launch_bounds__(NCW * 64 + 256) void k_scan_bwd(Params p) {
 // 16w.. of every C-row operand.
 //
 // Phase A walks the value dimension in tiles of 32 columns through a ring of
-// two LDS tiles and accumulates
+// two LDS tiles.  The tile's dD rows are not read from memory: each wave
+// forms its own rows as the backward scan does (dD^T = dS' Kbar^T + dO^T P,
+// the same operands in the same order, so the values are the scan's own),
+// from its rows of K held in registers and P, which sits in the M buffer
+// until the last tile.  Then it accumulates
 //   (dO S)^T, (D dS')^T, (dD S)^T   (Dk x 16 blocks: key rows, this wave's chunk columns)
 //   dO D^T, dD V^T                  (this wave's chunk rows x C)
 // and <dS', S> from diagonal blocks of S dS'^T.
@@ -398,8 +394,9 @@ __global__ __launch_bounds__(NCW * 64 + 256) void k_scan_bwd(Params p) {
 // product is computed instead, so that a lane holds four consecutive values
 // of one row and writes them to LDS (or global memory) as one store.
 
-// Phase-A tile of 32 value columns: S, dS' (32 value rows of Dk), D, V, dO,
-// dD (C rows of 32), each in the swizzled direct-load layout.
+// Phase-A tile of 32 value columns: S, dS' (32 value rows of Dk), D, V, dO
+// (C rows of 32), each in the swizzled direct-load layout, and room for the
+// tile's dD (C rows of 32), which the kernel forms itself.
 template <typename E, int DK>
 struct TileA {
   static constexpr int BV = 32;
@@ -407,7 +404,7 @@ struct TileA {
   static constexpr int RK = DK * (int)sizeof(E);    // row bytes of the state tiles
   static constexpr int S = 0, DS = S + BV * RK, D = DS + BV * RK, V = D + C * RE, DO = V + C * RE,
                        DD = DO + C * RE, BYTES = DD + C * RE;
-  static constexpr int LOADS = BYTES / 1024 / NWAVES;   // direct loads per wave and tile
+  static constexpr int LOADS = (BYTES - C * RE) / 1024 / NWAVES;   // direct loads per wave and tile
 };
 
 template <typename E, int DK>
@@ -422,7 +419,7 @@ struct alignas(16) IntraSmem {
   static_assert(OY + C * RC <= 2 * TA::BYTES, "slot 1 holds dW, (dT diag(beta))^T and Y");
   static_assert(2 * C * RC <= C * RK || 2 * C * RK + C * RC <= TA::BYTES, "room for dQK");
   alignas(16) char ring[2][TA::BYTES];
-  alignas(16) char Mm[C * RC];    // M = (I + A)^{-1} (r, i), swizzled rows
+  alignas(16) char Mm[C * RC];    // P (phase A), then M = (I + A)^{-1} (r, i), swizzled rows
   float b[C], g[C], beta[C], lam[C];
   float rdbeta[C], rer[C], rdb[C], rtk[C], rdl[C];   // row parts (each row owned by one wave)
   float colp[2][NWAVES][C];                          // column parts per wave: dT (.) M, decay terms
@@ -473,58 +470,92 @@ __global__ __launch_bounds__(INTRA_THREADS) __attribute__((amdgpu_waves_per_eu(2
   const char* Sg = (const char*)((const E*)p.saved + gi * DK * DV);
   const char* dSg = (const char*)((const E*)p.w_dSo + gi * DK * DV);
   const char* Dg = (const char*)((const E*)p.savedD + gi * C * DV);
-  const char* dDg = (const char*)((const E*)p.w_dDb + gi * C * DV);
   const char* dOg = (const char*)((const E*)p.dO + arow * DV);
   const char* Vg = (const char*)((const E*)p.v + arow * DV);
+  // the gate block (b, beta, lambda; waves 0-2 one vector each, straight
+  // into LDS) and this wave's rows of K as B operands of Kbar dS'^T (k = key;
+  // rows past the chunk re-read its last row: their dD rows are zeroed),
+  // ahead of the tiles
+  if (w < 3) dma4_asm(p.wb + gi * 3 * C + w * C + lane, (char*)(w == 0 ? sm.b : w == 1 ? sm.beta : sm.lam));
+  FR kf[NKK];
+  {
+    const E* kr = (const E*)p.k + (arow + (size_t)min(rr, len - 1) * H) * DK + (lane >> 4) * Mma<E>::KPL;
+#pragma unroll
+    for (int ks = 0; ks < NKK; ++ks) {
+      if constexpr (sizeof(E) == 2) kf[ks] = __builtin_bit_cast(FR, gload16_asm(kr + ks * KS));
+      else kf[ks] = gload4_asm(kr + ks * KS);
+    }
+  }
   // rows of V and dO past the chunk come from D, whose rows there are zero
   auto issue = [&](int vt) {
     const int ln = lane;
     char* t = sm.ring[vt & 1];
     const size_t vb = (size_t)vt * BV;
-    dma_rows<RK, BV>(t + TA::S, Sg + vb * RK, RK, BV, Sg, 0, w, ln);
-    dma_rows<RK, BV>(t + TA::DS, dSg + vb * RK, RK, BV, dSg, 0, w, ln);
-    dma_rows<TA::RE, C>(t + TA::D, Dg + vb * ES, DV * ES, C, Dg, 0, w, ln);
-    dma_rows<TA::RE, C>(t + TA::DD, dDg + vb * ES, DV * ES, C, dDg, 0, w, ln);
-    dma_rows<TA::RE, C>(t + TA::V, Vg + vb * ES, (size_t)H * DV * ES, len, Dg + vb * ES, DV * ES, w, ln);
-    dma_rows<TA::RE, C>(t + TA::DO, dOg + vb * ES, (size_t)H * DV * ES, len, Dg + vb * ES, DV * ES, w, ln);
+    dma_rows<RK, BV, NWAVES, true>(t + TA::S, Sg + vb * RK, RK, BV, Sg, 0, w, ln);
+    dma_rows<RK, BV, NWAVES, true>(t + TA::DS, dSg + vb * RK, RK, BV, dSg, 0, w, ln);
+    dma_rows<TA::RE, C, NWAVES, true>(t + TA::D, Dg + vb * ES, DV * ES, C, Dg, 0, w, ln);
+    dma_rows<TA::RE, C, NWAVES, true>(t + TA::V, Vg + vb * ES, (size_t)H * DV * ES, len, Dg + vb * ES, DV * ES, w, ln);
+    dma_rows<TA::RE, C, NWAVES, true>(t + TA::DO, dOg + vb * ES, (size_t)H * DV * ES, len, Dg + vb * ES, DV * ES, w, ln);
   };
-  // first two tiles and M; then (after the first tile) the gates, and with
-  // the last tile the chunk's K and Q rows into the free slot 0 (for phase B;
-  // rows past the chunk re-read its last row and are zeroed afterwards)
-  issue(0);
-  issue(1);
-  {
-    const char* Mg = (const char*)((const E*)p.wM + gi * C * C);
-    dma_rows<RC, C>(sm.Mm, Mg, RC, C, Mg, 0, w, lane);
-  }
+  // first tile, P (into the M buffer), second tile; with the last tile the
+  // chunk's K and Q rows into the
+  // free slot 0 (for phase B; rows past the chunk re-read its last row and
+  // are zeroed afterwards), and once the last tile's dD is formed, M over P
   constexpr int ML = C * RC / 1024 / NWAVES;
-  float gb = 0.f, gbeta = 0.f, glam = 0.f;
+  issue(0);
+  {
+    const char* Pg = (const char*)((const E*)p.wP + gi * C * C);
+    dma_rows<RC, C, NWAVES, true>(sm.Mm, Pg, RC, C, Pg, 0, w, lane);
+  }
+  issue(1);
+  wait_vm<TA::LOADS>();                           // all but tile 1 landed
+#pragma unroll
+  for (int ks = 0; ks < NKK; ++ks) reg_ready(kf[ks]);
   static_assert(NVT % 2 == 0, "the last tile uses slot 1");
+  float kbi = 0.f;                                // g_C / g of this lane's row
 #pragma unroll 1
   for (int vt = 0; vt < NVT; ++vt) {
-    // later loads that may still be in flight when tile vt is complete
-    if (vt == 0) wait_vm<TA::LOADS + ML>();       // tile 1, M
-    else if (vt == 1) wait_vm<ML + 3>();          // M, gates
-    else wait_vm<0>();
+    if (vt > 0) wait_vm<0>();                     // tile vt (issued during tile vt-1)
     block_sync_lds();                             // tile vt visible; tile vt-1's slot is free
-    if (vt == 0) {
-      asm volatile("" ::: "memory");
-      const float* gblk = p.wb + gi * 3 * C;
-      gb = gblk[lane];
-      gbeta = gblk[C + lane];
-      glam = gblk[2 * C + lane];
-      asm volatile("" ::: "memory");
-    }
+    if (vt == 0) kbi = __expf(sm.b[C - 1] - sm.b[rr]);
     if (vt >= 1 && vt + 1 < NVT) issue(vt + 1);
     if (vt == NVT - 1) {
       const char* Kg = (const char*)((const E*)p.k + arow * DK);
       const char* Qg = (const char*)((const E*)p.q + arow * DK);
-      dma_rows<RK, C>(sm.ring[0] + SM::OK, Kg, (size_t)H * RK, len, Kg + (size_t)(len - 1) * H * RK, 0, w, lane);
-      dma_rows<RK, C>(sm.ring[0] + SM::OQ, Qg, (size_t)H * RK, len, Qg + (size_t)(len - 1) * H * RK, 0, w, lane);
+      dma_rows<RK, C, NWAVES, true>(sm.ring[0] + SM::OK, Kg, (size_t)H * RK, len, Kg + (size_t)(len - 1) * H * RK, 0, w, lane);
+      dma_rows<RK, C, NWAVES, true>(sm.ring[0] + SM::OQ, Qg, (size_t)H * RK, len, Qg + (size_t)(len - 1) * H * RK, 0, w, lane);
     }
-    const char* t = sm.ring[vt & 1];
+    char* t = sm.ring[vt & 1];
     int la = lane;                        // laundered: addresses formed per tile
     asm volatile("" : "+v"(la));
+    {
+      // this wave's rows of the tile's dD, as their transpose (value rows,
+      // chunk columns 16w..): dS' Kbar^T + dO^T P, P causal; rows past the
+      // chunk carry no gradient
+      const float keep = rr < len ? 1.f : 0.f;
+#pragma unroll
+      for (int nb = 0; nb < BV / 16; ++nb) {
+        f4 dt = zero4();
+#pragma unroll
+        for (int ks = 0; ks < NKK; ++ks) dt = Mma<E>::mma(tile_frag<E, RK>(t + TA::DS, nb * 16, ks * KS, la), kf[ks], dt);
+#pragma unroll
+        for (int jj = 0; jj < 4; ++jj) dt[jj] *= kbi;
+#pragma unroll
+        for (int ks = 0; ks < NKC; ++ks)
+          if (keep_kblock<E>(ks * KS + KS > 16 * w))
+            dt = Mma<E>::mma(tile_tr_frag<E, TA::RE>(t + TA::DO, ks * KS, nb * 16, la),
+                             tile_tr_frag<E, RC>(sm.Mm, ks * KS, 16 * w, la), dt);
+        *(QR*)(t + TA::DD + tile_off<TA::RE>(rr, (nb * 16 + frow(la, 0)) * (int)ES)) = Quad<E>::pack(keep * dt);
+      }
+      // the wave reads back only its own rows: its LDS accesses complete in order
+      asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+    }
+    if (vt == NVT - 1) {
+      // every wave is past its last read of P: M goes over it
+      block_sync_lds();
+      const char* Mg = (const char*)((const E*)p.wM + gi * C * C);
+      dma_rows<RC, C, NWAVES, true>(sm.Mm, Mg, RC, C, Mg, 0, w, lane);
+    }
 #pragma unroll
     for (int ks = 0; ks < BV / KS; ++ks) {
       const FR aO = tile_frag<E, TA::RE>(t + TA::DO, 16 * w, ks * KS, la);
@@ -559,15 +590,12 @@ __global__ __launch_bounds__(INTRA_THREADS) __attribute__((amdgpu_waves_per_eu(2
 #pragma unroll
     for (int jj = 0; jj < 4; ++jj)
       if (jj == j) sdot = asd[jj];
-    sdot = wave_sum(sdot);
+    int ls = lane;
+    asm volatile("" : "+v"(ls));
+    sdot = wave_sum_l(sdot, ls);
     if (lane == 0) sm.sdot[w] = sdot;
   }
-  if (w == 0) {
-    sm.b[lane] = gb;
-    sm.g[lane] = __expf(gb);
-    sm.beta[lane] = gbeta;   // zero past the chunk in the gate block
-    sm.lam[lane] = glam;
-  }
+  if (w == 0) sm.g[lane] = __expf(sm.b[lane]);   // (beta, lambda: zero past the chunk in the gate block)
 
   // ---------------- phase B1
   // The lane index is laundered at each phase so that per-lane LDS addresses
@@ -576,14 +604,17 @@ __global__ __launch_bounds__(INTRA_THREADS) __attribute__((amdgpu_waves_per_eu(2
   char* const ring = &sm.ring[0][0];
   int lb = lane;
   asm volatile("" : "+v"(lb));
-  wait_vm<0>();                            // K, Q landed
+  wait_vm<ML>();                           // this wave's K, Q rows landed (M may be in flight)
   if (len < C) {
-    // rows of K and Q past the chunk are zero
-    constexpr int PR = RK / 16;
-    for (int idx = tid; idx < (C - len) * PR; idx += INTRA_THREADS) {
+    // rows of K and Q past the chunk are zero; each wave clears the rows its
+    // own loads filled (rows of instruction i belong to wave i mod NWAVES)
+    constexpr int PR = RK / 16, RPI = 1024 / RK;
+    for (int idx = lane; idx < (C - len) * PR; idx += 64) {
       const int r = len + idx / PR, c = (idx % PR) * 16;
-      *(uint4*)(ring + SM::OK + tile_off<RK>(r, c)) = make_uint4(0, 0, 0, 0);
-      *(uint4*)(ring + SM::OQ + tile_off<RK>(r, c)) = make_uint4(0, 0, 0, 0);
+      if ((r / RPI) % NWAVES == w) {
+        *(uint4*)(ring + SM::OK + tile_off<RK>(r, c)) = make_uint4(0, 0, 0, 0);
+        *(uint4*)(ring + SM::OQ + tile_off<RK>(r, c)) = make_uint4(0, 0, 0, 0);
+      }
     }
   }
   block_sync_lds();                        // phase-A tiles consumed; gates, K, Q visible; slot 1 free
@@ -647,6 +678,8 @@ __global__ __launch_bounds__(INTRA_THREADS) __attribute__((amdgpu_waves_per_eu(2
   }
   // (T^T dW)^T = (diag(beta) M^T dW)^T: key rows, this wave's chunk columns;
   // M is lower triangular, so k blocks before this wave's rows are skipped
+  wait_vm<0>();
+  block_sync_lds();                        // M visible
   f4 tdwt[NKB];
   {
     const float betc = sm.beta[rr];
@@ -679,8 +712,8 @@ __global__ __launch_bounds__(INTRA_THREADS) __attribute__((amdgpu_waves_per_eu(2
       dm[j] = dT[cb][j] * bc;
     }
     *(QR*)(ring + SM::ODT + tile_off<RC>(c, r0 * (int)ES)) = Quad<E>::pack(dm);
-    cs += __shfl_xor(cs, 16, 64);
-    cs += __shfl_xor(cs, 32, 64);
+    cs += lane_xor(cs, 16, lb);
+    cs += lane_xor(cs, 32, lb);
     if (lane < 16) sm.colp[0][w][c] = cs;
   }
   block_sync_lds();                        // (dT diag(beta))^T complete; dW no longer read
@@ -735,8 +768,8 @@ __global__ __launch_bounds__(INTRA_THREADS) __attribute__((amdgpu_waves_per_eu(2
         *(E*)(ring + SM::OQK + tile_off<RC>(r, c * (int)ES)) = fromf<E>(dqk);
         *(E*)(ring + SM::OY + tile_off<RC>(r, c * (int)ES)) = fromf<E>(dqk + lamr[j] * dg);
       }
-      ec += __shfl_xor(ec, 16, 64);
-      ec += __shfl_xor(ec, 32, 64);
+      ec += lane_xor(ec, 16, lb);
+      ec += lane_xor(ec, 32, lb);
       if (lane < 16) sm.colp[1][w][c] = ec;
     }
 #pragma unroll
@@ -803,12 +836,12 @@ __global__ __launch_bounds__(INTRA_THREADS) __attribute__((amdgpu_waves_per_eu(2
         *(QR*)(dko + kc) = Quad<E>::pack(ok);
       }
     }
-    s1 += __shfl_xor(s1, 16, 64);
-    s1 += __shfl_xor(s1, 32, 64);
-    s2 += __shfl_xor(s2, 16, 64);
-    s2 += __shfl_xor(s2, 32, 64);
-    s3 += __shfl_xor(s3, 16, 64);
-    s3 += __shfl_xor(s3, 32, 64);
+    s1 += lane_xor(s1, 16, lb);
+    s1 += lane_xor(s1, 32, lb);
+    s2 += lane_xor(s2, 16, lb);
+    s2 += lane_xor(s2, 32, lb);
+    s3 += lane_xor(s3, 16, lb);
+    s3 += lane_xor(s3, 32, lb);
     if (lane < 16) {
       sm.rdb[rr] = gr * s1;
       sm.rtk[rr] = kbr * s2;
@@ -831,7 +864,7 @@ __global__ __launch_bounds__(INTRA_THREADS) __attribute__((amdgpu_waves_per_eu(2
     const float tk = sm.rtk[j];
     float tot = tk;
 #pragma unroll
-    for (int off = 32; off >= 1; off >>= 1) tot += __shfl_xor(tot, off, 64);
+    for (int off = 32; off >= 1; off >>= 1) tot += lane_xor(tot, off, lb);
     float dbj = sm.rer[j] - ce + sm.rdb[j] - tk;
     if (j == C - 1) {
       float sd = 0.f;
@@ -839,9 +872,9 @@ __global__ __launch_bounds__(INTRA_THREADS) __attribute__((amdgpu_waves_per_eu(2
       for (int q = 0; q < NWAVES; ++q) sd += sm.sdot[q];
       dbj += tot + sm.g[C - 1] * sd;
     }
-    float x = __shfl(dbj, C - 1 - j, 64);
-    x = wave_incl_scan(x, lb);
-    const float suffix = __shfl(x, C - 1 - j, 64);
+    float x = lane_from(dbj, C - 1 - j);
+    x = wave_incl_scan_l(x, lb);
+    const float suffix = lane_from(x, C - 1 - j);
     if (j < len) {
       const size_t gt = arow + (size_t)j * H;
       p.dbeta[gt] = sm.rdbeta[j] + cb_;
@@ -850,7 +883,7 @@ __global__ __launch_bounds__(INTRA_THREADS) __attribute__((amdgpu_waves_per_eu(2
     }
     if (p.w_dlam) {
       // constant lambda: this unit's share of its gradient
-      const float part = wave_sum(j < len ? sm.rdl[j] : 0.f);
+      const float part = wave_sum_l(j < len ? sm.rdl[j] : 0.f, lb);
       if (j == 0) p.w_dlam[gi] = part;
     }
   }

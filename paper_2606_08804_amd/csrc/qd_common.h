@@ -377,6 +377,27 @@ __device__ inline void dma4_asm(const void* g, char* lds) {
   const uint32_t base = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)lds);
   asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dword %1, off" ::"s"(base), "v"(g) : "memory", "m0");
 }
+
+// A global load into registers through inline assembly (16 or 4 bytes per
+// lane), for kernels whose direct loads are in assembly form: the compiler
+// does not count it either, so it adds no wait that would also cover the
+// later direct loads.  The caller waits for it with an explicit vmcnt count
+// in straight-line code and then passes the value through reg_ready(), the
+// first point at which the compiler may read the register.
+__device__ inline uint4 gload16_asm(const void* g) {
+  uint4 r;
+  asm volatile("global_load_dwordx4 %0, %1, off" : "=v"(r) : "v"(g) : "memory");
+  return r;
+}
+__device__ inline float gload4_asm(const void* g) {
+  float r;
+  asm volatile("global_load_dword %0, %1, off" : "=v"(r) : "v"(g) : "memory");
+  return r;
+}
+template <typename T>
+__device__ inline void reg_ready(T& x) {
+  asm volatile("" : "+v"(x));
+}
 #pragma clang diagnostic pop
 
 // Direct global->LDS copy of a ROWS x RB-byte block (row stride `stride`
@@ -640,7 +661,6 @@ struct Params {
   float* dla;
   float* dS0;
   void* w_dSo;           // [slot][H][Dv][Dk] gradient w.r.t. each chunk's exit state (dtype)
-  void* w_dDb;           // [slot][H][C][Dv] dD (dtype)
   // segment-parallel forward (dense batches): each sequence in n_seg
   // segments of seg_chunks chunks
   int n_seg;
@@ -701,7 +721,28 @@ __device__ inline float wave_sum(float x) {
   return x;
 }
 
-// Sum over the 16 lanes that share (lane >> 4).
+// Lane exchanges (ds_bpermute) addressed from a lane index the caller
+// supplies: a kernel near its register limit passes an index laundered per
+// phase, so that the exchange addresses of one phase are not kept alive
+// through the next.  Same values and order as the __shfl forms.
+__device__ inline float lane_from(float x, int src) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_ds_bpermute(src << 2, __builtin_bit_cast(int, x)));
+}
+__device__ inline float lane_xor(float x, int off, int lane) { return lane_from(x, lane ^ off); }
+__device__ inline float wave_sum_l(float x, int lane) {
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) x += lane_xor(x, off, lane);
+  return x;
+}
+__device__ inline float wave_incl_scan_l(float x, int lane) {
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) {
+    const float y = lane_from(x, (lane - off) & 63);
+    if (lane >= off) x += y;
+  }
+  return x;
+}
+
 // Sum over each row of 16 lanes with DPP lane moves (no LDS crossbar):
 // swaps within pairs and quads, then rotations by 4 and 8 within the row.
 template <int CTRL>
