@@ -475,16 +475,13 @@ __global__ __launch_bounds__(INTRA_THREADS) __attribute__((amdgpu_waves_per_eu(2
   // the gate block (b, beta, lambda; waves 0-2 one vector each, straight
   // into LDS) and this wave's rows of K as B operands of Kbar dS'^T (k = key;
   // rows past the chunk re-read its last row: their dD rows are zeroed),
-  // ahead of the tiles
+  // ahead of the first tile
   if (w < 3) dma4_asm(p.wb + gi * 3 * C + w * C + lane, (char*)(w == 0 ? sm.b : w == 1 ? sm.beta : sm.lam));
   FR kf[NKK];
   {
     const E* kr = (const E*)p.k + (arow + (size_t)min(rr, len - 1) * H) * DK + (lane >> 4) * Mma<E>::KPL;
 #pragma unroll
-    for (int ks = 0; ks < NKK; ++ks) {
-      if constexpr (sizeof(E) == 2) kf[ks] = __builtin_bit_cast(FR, gload16_asm(kr + ks * KS));
-      else kf[ks] = gload4_asm(kr + ks * KS);
-    }
+    for (int ks = 0; ks < NKK; ++ks) kf[ks] = *(const FR*)(kr + ks * KS);
   }
   // rows of V and dO past the chunk come from D, whose rows there are zero
   auto issue = [&](int vt) {
@@ -497,10 +494,71 @@ __global__ __launch_bounds__(INTRA_THREADS) __attribute__((amdgpu_waves_per_eu(2
     dma_rows<TA::RE, C, NWAVES, true>(t + TA::V, Vg + vb * ES, (size_t)H * DV * ES, len, Dg + vb * ES, DV * ES, w, ln);
     dma_rows<TA::RE, C, NWAVES, true>(t + TA::DO, dOg + vb * ES, (size_t)H * DV * ES, len, Dg + vb * ES, DV * ES, w, ln);
   };
-  // first tile, P (into the M buffer), second tile; with the last tile the
-  // chunk's K and Q rows into the
-  // free slot 0 (for phase B; rows past the chunk re-read its last row and
-  // are zeroed afterwards), and once the last tile's dD is formed, M over P
+  // this wave's rows of the tile's dD, as their transpose (value rows, chunk
+  // columns 16w..): dS' Kbar^T + dO^T P, P causal; rows past the chunk carry
+  // no gradient
+  float kbi = 0.f;                                // g_C / g of this lane's row
+  auto form_dD = [&](char* t, int la) {
+    const float keep = rr < len ? 1.f : 0.f;
+#pragma unroll
+    for (int nb = 0; nb < BV / 16; ++nb) {
+      f4 dt = zero4();
+#pragma unroll
+      for (int ks = 0; ks < NKK; ++ks) dt = Mma<E>::mma(tile_frag<E, RK>(t + TA::DS, nb * 16, ks * KS, la), kf[ks], dt);
+#pragma unroll
+      for (int jj = 0; jj < 4; ++jj) dt[jj] *= kbi;
+#pragma unroll
+      for (int ks = 0; ks < NKC; ++ks)
+        if (keep_kblock<E>(ks * KS + KS > 16 * w))
+          dt = Mma<E>::mma(tile_tr_frag<E, TA::RE>(t + TA::DO, ks * KS, nb * 16, la),
+                           tile_tr_frag<E, RC>(sm.Mm, ks * KS, 16 * w, la), dt);
+      *(QR*)(t + TA::DD + tile_off<TA::RE>(rr, (nb * 16 + frow(la, 0)) * (int)ES)) = Quad<E>::pack(keep * dt);
+    }
+    // the wave reads back only its own rows: its LDS accesses complete in order
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+  };
+  // the tile's products: WITH_DD selects those that take dD (dD S, dD V^T),
+  // WITHOUT_DD the others (dO S, D dS', dO D^T and <dS', S>)
+  enum { WITHOUT_DD = 1, WITH_DD = 2 };
+  auto products = [&](const char* t, int la, int which) {
+#pragma unroll
+    for (int ks = 0; ks < BV / KS; ++ks) {
+      const FR aO = tile_frag<E, TA::RE>(t + TA::DO, 16 * w, ks * KS, la);
+      const FR aD = tile_frag<E, TA::RE>(t + TA::D, 16 * w, ks * KS, la);
+      FR adD = aD;
+      if (which & WITH_DD) adD = tile_frag<E, TA::RE>(t + TA::DD, 16 * w, ks * KS, la);
+#pragma unroll
+      for (int kb = 0; kb < NKB; ++kb) {
+        const FR bS = tile_tr_frag<E, RK>(t + TA::S, ks * KS, kb * 16, la);
+        if (which & WITHOUT_DD) {
+          const FR bdS = tile_tr_frag<E, RK>(t + TA::DS, ks * KS, kb * 16, la);
+          aQt[kb] = Mma<E>::mma(bS, aO, aQt[kb]);
+          aKt[kb] = Mma<E>::mma(bdS, aD, aKt[kb]);
+        }
+        if (which & WITH_DD) aWt[kb] = Mma<E>::mma(bS, adD, aWt[kb]);
+      }
+#pragma unroll
+      for (int cb = 0; cb < 4; ++cb) {
+        if (which & WITHOUT_DD) aP[cb] = Mma<E>::mma(aO, tile_frag<E, TA::RE>(t + TA::D, cb * 16, ks * KS, la), aP[cb]);
+        if (which & WITH_DD) aT[cb] = Mma<E>::mma(adD, tile_frag<E, TA::RE>(t + TA::V, cb * 16, ks * KS, la), aT[cb]);
+      }
+    }
+    if (which & WITHOUT_DD) {
+      // <dS', S> = trace(S dS'^T): wave w adds the diagonal 16 x 16 block
+      // (w & 1) of this tile's S dS'^T over the key steps w >> 1, +2, ...
+#pragma unroll
+      for (int ks = 0; ks < NKK; ks += 2)
+        if (ks + (w >> 1) < NKK)
+          asd = Mma<E>::mma(tile_frag<E, RK>(t + TA::S, 16 * (w & 1), (ks + (w >> 1)) * KS, la),
+                            tile_frag<E, RK>(t + TA::DS, 16 * (w & 1), (ks + (w >> 1)) * KS, la), asd);
+    }
+  };
+
+  // First tile, P (into the M buffer) and the second tile; every later tile
+  // once the one before it has landed; with the last tile the chunk's K and Q
+  // rows into the free slot 0 (for phase B; rows past the chunk re-read its
+  // last row and are zeroed afterwards), and once the last tile's dD is
+  // formed, M over P.
   constexpr int ML = C * RC / 1024 / NWAVES;
   issue(0);
   {
@@ -508,17 +566,27 @@ __global__ __launch_bounds__(INTRA_THREADS) __attribute__((amdgpu_waves_per_eu(2
     dma_rows<RC, C, NWAVES, true>(sm.Mm, Pg, RC, C, Pg, 0, w, lane);
   }
   issue(1);
-  wait_vm<TA::LOADS>();                           // all but tile 1 landed
-#pragma unroll
-  for (int ks = 0; ks < NKK; ++ks) reg_ready(kf[ks]);
   static_assert(NVT % 2 == 0, "the last tile uses slot 1");
-  float kbi = 0.f;                                // g_C / g of this lane's row
+  wait_vm<TA::LOADS>();                           // all but tile 1 landed
+  block_sync_lds();
+  kbi = __expf(sm.b[C - 1] - sm.b[rr]);
+  {
+    // The first tile runs the products without dD first.  The K rows are the
+    // compiler's own loads, and at their first use (forming dD) it waits with
+    // a count of its own loads only, so for the second tile as well, which
+    // has had that time to land.
+    char* t = sm.ring[0];
+    int la = lane;
+    asm volatile("" : "+v"(la));
+    products(t, la, WITHOUT_DD);
+    form_dD(t, la);
+    products(t, la, WITH_DD);
+  }
 #pragma unroll 1
-  for (int vt = 0; vt < NVT; ++vt) {
-    if (vt > 0) wait_vm<0>();                     // tile vt (issued during tile vt-1)
+  for (int vt = 1; vt < NVT; ++vt) {
+    wait_vm<0>();                                 // tile vt (issued during tile vt-1)
     block_sync_lds();                             // tile vt visible; tile vt-1's slot is free
-    if (vt == 0) kbi = __expf(sm.b[C - 1] - sm.b[rr]);
-    if (vt >= 1 && vt + 1 < NVT) issue(vt + 1);
+    if (vt + 1 < NVT) issue(vt + 1);
     if (vt == NVT - 1) {
       const char* Kg = (const char*)((const E*)p.k + arow * DK);
       const char* Qg = (const char*)((const E*)p.q + arow * DK);
@@ -528,60 +596,14 @@ __global__ __launch_bounds__(INTRA_THREADS) __attribute__((amdgpu_waves_per_eu(2
     char* t = sm.ring[vt & 1];
     int la = lane;                        // laundered: addresses formed per tile
     asm volatile("" : "+v"(la));
-    {
-      // this wave's rows of the tile's dD, as their transpose (value rows,
-      // chunk columns 16w..): dS' Kbar^T + dO^T P, P causal; rows past the
-      // chunk carry no gradient
-      const float keep = rr < len ? 1.f : 0.f;
-#pragma unroll
-      for (int nb = 0; nb < BV / 16; ++nb) {
-        f4 dt = zero4();
-#pragma unroll
-        for (int ks = 0; ks < NKK; ++ks) dt = Mma<E>::mma(tile_frag<E, RK>(t + TA::DS, nb * 16, ks * KS, la), kf[ks], dt);
-#pragma unroll
-        for (int jj = 0; jj < 4; ++jj) dt[jj] *= kbi;
-#pragma unroll
-        for (int ks = 0; ks < NKC; ++ks)
-          if (keep_kblock<E>(ks * KS + KS > 16 * w))
-            dt = Mma<E>::mma(tile_tr_frag<E, TA::RE>(t + TA::DO, ks * KS, nb * 16, la),
-                             tile_tr_frag<E, RC>(sm.Mm, ks * KS, 16 * w, la), dt);
-        *(QR*)(t + TA::DD + tile_off<TA::RE>(rr, (nb * 16 + frow(la, 0)) * (int)ES)) = Quad<E>::pack(keep * dt);
-      }
-      // the wave reads back only its own rows: its LDS accesses complete in order
-      asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
-    }
+    form_dD(t, la);
     if (vt == NVT - 1) {
       // every wave is past its last read of P: M goes over it
       block_sync_lds();
       const char* Mg = (const char*)((const E*)p.wM + gi * C * C);
       dma_rows<RC, C, NWAVES, true>(sm.Mm, Mg, RC, C, Mg, 0, w, lane);
     }
-#pragma unroll
-    for (int ks = 0; ks < BV / KS; ++ks) {
-      const FR aO = tile_frag<E, TA::RE>(t + TA::DO, 16 * w, ks * KS, la);
-      const FR adD = tile_frag<E, TA::RE>(t + TA::DD, 16 * w, ks * KS, la);
-      const FR aD = tile_frag<E, TA::RE>(t + TA::D, 16 * w, ks * KS, la);
-#pragma unroll
-      for (int kb = 0; kb < NKB; ++kb) {
-        const FR bS = tile_tr_frag<E, RK>(t + TA::S, ks * KS, kb * 16, la);
-        const FR bdS = tile_tr_frag<E, RK>(t + TA::DS, ks * KS, kb * 16, la);
-        aQt[kb] = Mma<E>::mma(bS, aO, aQt[kb]);
-        aWt[kb] = Mma<E>::mma(bS, adD, aWt[kb]);
-        aKt[kb] = Mma<E>::mma(bdS, aD, aKt[kb]);
-      }
-#pragma unroll
-      for (int cb = 0; cb < 4; ++cb) {
-        aP[cb] = Mma<E>::mma(aO, tile_frag<E, TA::RE>(t + TA::D, cb * 16, ks * KS, la), aP[cb]);
-        aT[cb] = Mma<E>::mma(adD, tile_frag<E, TA::RE>(t + TA::V, cb * 16, ks * KS, la), aT[cb]);
-      }
-    }
-    // <dS', S> = trace(S dS'^T): wave w adds the diagonal 16 x 16 block
-    // (w & 1) of this tile's S dS'^T over the key steps w >> 1, +2, ...
-#pragma unroll
-    for (int ks = 0; ks < NKK; ks += 2)
-      if (ks + (w >> 1) < NKK)
-        asd = Mma<E>::mma(tile_frag<E, RK>(t + TA::S, 16 * (w & 1), (ks + (w >> 1)) * KS, la),
-                          tile_frag<E, RK>(t + TA::DS, 16 * (w & 1), (ks + (w >> 1)) * KS, la), asd);
+    products(t, la, WITHOUT_DD | WITH_DD);
   }
   {
     // diagonal elements of the accumulated block: row 4 (l >> 4) + j == column l & 15

@@ -377,28 +377,14 @@ __device__ inline void dma4_asm(const void* g, char* lds) {
   const uint32_t base = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)lds);
   asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dword %1, off" ::"s"(base), "v"(g) : "memory", "m0");
 }
+#pragma clang diagnostic pop
 
-// A global load into registers through inline assembly (16 or 4 bytes per
-// lane), for kernels whose direct loads are in assembly form: the compiler
-// does not count it either, so it adds no wait that would also cover the
-// later direct loads.  The caller waits for it with an explicit vmcnt count
-// in straight-line code and then passes the value through reg_ready(), the
-// first point at which the compiler may read the register.
-__device__ inline uint4 gload16_asm(const void* g) {
-  uint4 r;
-  asm volatile("global_load_dwordx4 %0, %1, off" : "=v"(r) : "v"(g) : "memory");
-  return r;
-}
-__device__ inline float gload4_asm(const void* g) {
-  float r;
-  asm volatile("global_load_dword %0, %1, off" : "=v"(r) : "v"(g) : "memory");
-  return r;
-}
+// Passes a register through an empty assembly statement: the compiler must
+// have the value at this point, so it waits here for its own load of it.
 template <typename T>
 __device__ inline void reg_ready(T& x) {
   asm volatile("" : "+v"(x));
 }
-#pragma clang diagnostic pop
 
 // Direct global->LDS copy of a ROWS x RB-byte block (row stride `stride`
 // bytes) into the swizzled layout at `dst`.  Each instruction moves 1 KB

@@ -32,30 +32,24 @@ namespace qd {
 template <typename E, int DK>
 struct alignas(16) PrepSmem {
   static constexpr int P = Pad<E>::v;
+  static constexpr int RK = DK * (int)sizeof(E);
+  alignas(16) char Kt[2][C * RK];   // K and Q of a unit (swizzled direct-load tiles),
+  alignas(16) char Qt[2][C * RK];   // the next unit's landing while this one is solved
   alignas(16) float b[C], beta[C], lam[C];
-  E K[C][DK + P];
-  E Q[C][DK + P];
+  alignas(16) float rla[C], rbeta[C], rlam[C];   // raw gate vectors of the unit in flight
   float A[C][C + 4];          // strictly lower A, consumed by the solve
   alignas(16) float M[C][C + 4];
   E Pm[C][C + P];             // P staging
 };
 
-// Raw inputs of one (chunk, head) unit, staged in registers one unit ahead.
 constexpr int PREP_THREADS = 512;   // 8 waves: two per SIMD hide each other's latency
-
-template <typename E, int DK>
-struct PrepPre {
-  TileRegs<E, C, DK, PREP_THREADS> K, Q;
-  float la, beta, lam;
-  int t0, len, g, h;
-  bool valid;
-};
 
 // Copies a C x D LDS tile (row stride ld elements) to a dense row-major
 // global block with 16-byte stores.
 template <typename E, int D, int NT>
 __device__ inline void store_tile(E* dst, const E* src, int ld, int tid) {
   constexpr int VEC = 16 / sizeof(E), PR = D / VEC;
+#pragma unroll
   for (int idx = tid; idx < C * PR; idx += NT) {
     const int r = idx / PR, c = (idx % PR) * VEC;
     *(uint4*)(dst + (size_t)r * D + c) = *(const uint4*)(src + (size_t)r * ld + c);
@@ -64,61 +58,90 @@ __device__ inline void store_tile(E* dst, const E* src, int ld, int tid) {
 
 // Writes, for every unit, the gate block (b, beta, lambda), the intra-chunk
 // output operator P = Gam * M_causal * Q K^T, M = (I + A)^{-1} (when p.wM is
-// set) and T = M diag(beta).  Persistent: each workgroup walks units blockIdx.x,
-// +gridDim.x, ... and prefetches the next unit's inputs into registers while
-// computing the current one.
+// set) and T = M diag(beta).  Persistent: each workgroup walks units
+// blockIdx.x, +gridDim.x, ...  The next unit's K, Q and raw gate vectors go
+// straight into LDS (direct loads in assembly form; K and Q into the other
+// buffer) once this unit's P is out, so they land during the UT solve; the
+// only memory operations issued after them are this unit's M and T stores,
+// which fixes the wait count at the top of the next unit (the compiler's
+// wait for register loads would also cover every store still in flight).
 template <typename E, int DK, int DV>
 __global__ __launch_bounds__(PREP_THREADS) void k_prep(Params p) {
   constexpr int NT = PREP_THREADS, NW = NT / 64;
   constexpr int P = Pad<E>::v;
-  constexpr int LK = DK + P, LC = C + P;
-  typedef PrepPre<E, DK> Pre;
+  constexpr int LC = C + P;
+  constexpr int RK = DK * (int)sizeof(E), KS = Mma<E>::KS;
+  constexpr int VEC = 16 / sizeof(E), MT_ITERS = C * C / VEC / NT;   // M/T store rounds per thread
+  static_assert(C == 64 && C * C / VEC % NT == 0, "wave 0 holds the gate vectors; M/T stores split evenly");
+  typedef typename Mma<E>::frag FR;
   __shared__ PrepSmem<E, DK> sm;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;   // vector wave index: measured faster here than the scalar one
   const int H = p.H;
   const int total = p.n_slots * H;
 
-  auto fetch = [&](int u, Pre& x) {
+  struct Unit {
+    int g, h, t0, len;
+    bool valid;
+  };
+  auto find = [&](int u, Unit& x) {
     x.valid = false;
     if (u >= total) return;
     x.g = u / H;
     x.h = u % H;
     int n;
-    if (!locate(p, x.g, n, x.t0, x.len)) return;
-    x.valid = true;
+    x.valid = locate(p, x.g, n, x.t0, x.len);
+  };
+  // K, Q rows past the chunk re-read its last row: they meet only zero
+  // gates, or masked entries of P; so do the raw gates, masked when read
+  auto issue = [&](const Unit& x, int buf) {
+    if (!x.valid) return;
     const size_t row = (size_t)x.t0 * H + x.h;
-    x.K.load((const E*)p.k + row * DK, (size_t)H * DK, x.len, tid);
-    x.Q.load((const E*)p.q + row * DK, (size_t)H * DK, x.len, tid);
-    if (tid < C) {
-      const bool ok = tid < x.len;
-      const size_t gt = row + (size_t)tid * H;
-      x.la = (ok && p.la) ? p.la[gt] : 0.f;
-      x.beta = ok ? p.beta[gt] : 0.f;
-      x.lam = ok ? (p.lam ? p.lam[gt] : p.lam_c) : 0.f;   // NULL: the constant lambda
+    const char* Kg = (const char*)((const E*)p.k + row * DK);
+    const char* Qg = (const char*)((const E*)p.q + row * DK);
+    dma_rows<RK, C, NW, true>(sm.Kt[buf], Kg, (size_t)H * RK, x.len, Kg + (size_t)(x.len - 1) * H * RK, 0, w, lane);
+    dma_rows<RK, C, NW, true>(sm.Qt[buf], Qg, (size_t)H * RK, x.len, Qg + (size_t)(x.len - 1) * H * RK, 0, w, lane);
+    if (w == 0) {
+      const size_t gt = row + (size_t)min(lane, x.len - 1) * H;
+      if (p.la) dma4_asm(p.la + gt, (char*)sm.rla);
+      dma4_asm(p.beta + gt, (char*)sm.rbeta);
+      if (p.lam) dma4_asm(p.lam + gt, (char*)sm.rlam);
     }
   };
 
-  Pre pre;
-  fetch(blockIdx.x, pre);
-  for (int u = blockIdx.x; u < total; u += gridDim.x) {
-    const Pre x = pre;
-    fetch(u + gridDim.x, pre);
-    if (!x.valid) continue;                 // uniform across the workgroup
+  Unit cur;
+  find(blockIdx.x, cur);
+  issue(cur, 0);
+  wait_vm<0>();
+  int buf = 0;
+  for (int u = blockIdx.x; u < total; u += gridDim.x, buf ^= 1) {
+    const Unit x = cur;
+    Unit nx;
+    find(u + gridDim.x, nx);
+    block_sync_lds();                        // x's K, Q landed in every wave; the previous unit's LDS use is over
+    if (!x.valid) {                          // uniform across the workgroup
+      issue(nx, buf ^ 1);
+      wait_vm<0>();
+      cur = nx;
+      continue;
+    }
     const int h = x.h;
     const size_t gi = (size_t)x.g * H + h;
-    block_sync_lds();                        // previous unit's LDS use is over
-    x.K.store(&sm.K[0][0], LK, tid);
-    x.Q.store(&sm.Q[0][0], LK, tid);
-    if (tid < C) {
-      const float b = wave_incl_scan(x.la, lane);
-      sm.b[tid] = b;
-      sm.beta[tid] = x.beta;
-      sm.lam[tid] = x.lam;
+    const char* Kt = sm.Kt[buf];
+    const char* Qt = sm.Qt[buf];
+    if (w == 0) {
+      // gates past the chunk's end are zero; NULL lambda: the constant
+      const bool ok = lane < x.len;
+      const float la = (ok && p.la) ? sm.rla[lane] : 0.f, be = ok ? sm.rbeta[lane] : 0.f;
+      const float lm = ok ? (p.lam ? sm.rlam[lane] : p.lam_c) : 0.f;
+      const float b = wave_incl_scan(la, lane);
+      sm.b[lane] = b;
+      sm.beta[lane] = be;
+      sm.lam[lane] = lm;
       // gate block: b, beta, lambda (zero past the chunk's end)
       float* gblk = p.wb + gi * 3 * C;
-      gblk[tid] = b;
-      gblk[C + tid] = x.beta;
-      gblk[2 * C + tid] = x.lam;
+      gblk[lane] = b;
+      gblk[C + lane] = be;
+      gblk[2 * C + lane] = lm;
     }
     block_sync_lds();
 
@@ -137,8 +160,13 @@ __global__ __launch_bounds__(PREP_THREADS) void k_prep(Params p) {
         betr[j] = sm.beta[r];
         lr[j] = sm.lam[r];
       }
-      const f4 kk = mma_k<E, DK>(kmaj(&sm.K[0][0], LK), kmaj(&sm.K[0][0], LK), m0, n0, zero4(), lane);
-      const f4 qk = mma_k<E, DK>(kmaj(&sm.Q[0][0], LK), kmaj(&sm.K[0][0], LK), m0, n0, zero4(), lane);
+      f4 kk = zero4(), qk = zero4();
+#pragma unroll
+      for (int ks = 0; ks < DK / KS; ++ks) {
+        const FR kB = tile_frag<E, RK>(Kt, n0, ks * KS, lane);
+        kk = Mma<E>::mma(tile_frag<E, RK>(Kt, m0, ks * KS, lane), kB, kk);
+        qk = Mma<E>::mma(tile_frag<E, RK>(Qt, m0, ks * KS, lane), kB, qk);
+      }
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
         const int r = m0 + frow(lane, j);
@@ -149,6 +177,7 @@ __global__ __launch_bounds__(PREP_THREADS) void k_prep(Params p) {
     }
     block_sync_lds();
     store_tile<E, C, NT>((E*)p.wP + gi * C * C, &sm.Pm[0][0], LC, tid);
+    issue(nx, buf ^ 1);
 
     // UT solve: M = (I + A)^{-1}; M (only the backward reads it, so only
     // when the context is kept) and T = M diag(beta) are stored with
@@ -157,7 +186,6 @@ __global__ __launch_bounds__(PREP_THREADS) void k_prep(Params p) {
     unit_lower_inverse<NT>(&sm.A[0][0], C + 4, &sm.M[0][0], C + 4, tid);
     {
       const bool keep_m = p.wM != nullptr;
-      constexpr int VEC = 16 / sizeof(E);
       E* wM = keep_m ? (E*)p.wM + gi * C * C : nullptr;
       E* wT = (E*)p.wT + gi * C * C;
       for (int idx = tid; idx < C * C / VEC; idx += NT) {
@@ -181,7 +209,11 @@ __global__ __launch_bounds__(PREP_THREADS) void k_prep(Params p) {
         if (keep_m) *(uint4*)(wM + r * C + i0) = mr;
         *(uint4*)(wT + r * C + i0) = tr;
       }
+      // the next unit's loads went out before these stores (in-order counter)
+      if (keep_m) wait_vm<2 * MT_ITERS>();
+      else wait_vm<MT_ITERS>();
     }
+    cur = nx;
   }
 }
 
