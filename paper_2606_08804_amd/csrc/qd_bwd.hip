@@ -588,10 +588,21 @@ __global__ __launch_bounds__(INTRA_THREADS) __attribute__((amdgpu_waves_per_eu(2
     block_sync_lds();                             // tile vt visible; tile vt-1's slot is free
     if (vt + 1 < NVT) issue(vt + 1);
     if (vt == NVT - 1) {
-      const char* Kg = (const char*)((const E*)p.k + arow * DK);
+      // phase B's K rows come from the waves' registers (rows past the
+      // chunk written as zero), its Q rows from memory
       const char* Qg = (const char*)((const E*)p.q + arow * DK);
-      dma_rows<RK, C, NWAVES, true>(sm.ring[0] + SM::OK, Kg, (size_t)H * RK, len, Kg + (size_t)(len - 1) * H * RK, 0, w, lane);
       dma_rows<RK, C, NWAVES, true>(sm.ring[0] + SM::OQ, Qg, (size_t)H * RK, len, Qg + (size_t)(len - 1) * H * RK, 0, w, lane);
+      const float kz = rr < len ? 1.f : 0.f;
+#pragma unroll
+      for (int ks = 0; ks < NKK; ++ks) {
+        const int kbyte = (ks * KS + (lane >> 4) * Mma<E>::KPL) * (int)ES;
+        if constexpr (sizeof(E) == 2) {
+          const uint4 z = make_uint4(0, 0, 0, 0);
+          *(uint4*)(sm.ring[0] + SM::OK + tile_off<RK>(rr, kbyte)) = kz != 0.f ? __builtin_bit_cast(uint4, kf[ks]) : z;
+        } else {
+          *(float*)(sm.ring[0] + SM::OK + tile_off<RK>(rr, kbyte)) = kz * kf[ks];
+        }
+      }
     }
     char* t = sm.ring[vt & 1];
     int la = lane;                        // laundered: addresses formed per tile
@@ -626,17 +637,14 @@ __global__ __launch_bounds__(INTRA_THREADS) __attribute__((amdgpu_waves_per_eu(2
   char* const ring = &sm.ring[0][0];
   int lb = lane;
   asm volatile("" : "+v"(lb));
-  wait_vm<ML>();                           // this wave's K, Q rows landed (M may be in flight)
+  wait_vm<ML>();                           // this wave's Q rows landed (M may be in flight)
   if (len < C) {
-    // rows of K and Q past the chunk are zero; each wave clears the rows its
-    // own loads filled (rows of instruction i belong to wave i mod NWAVES)
+    // rows of Q past the chunk are zero; each wave clears the rows its own
+    // loads filled (rows of instruction i belong to wave i mod NWAVES)
     constexpr int PR = RK / 16, RPI = 1024 / RK;
     for (int idx = lane; idx < (C - len) * PR; idx += 64) {
       const int r = len + idx / PR, c = (idx % PR) * 16;
-      if ((r / RPI) % NWAVES == w) {
-        *(uint4*)(ring + SM::OK + tile_off<RK>(r, c)) = make_uint4(0, 0, 0, 0);
-        *(uint4*)(ring + SM::OQ + tile_off<RK>(r, c)) = make_uint4(0, 0, 0, 0);
-      }
+      if ((r / RPI) % NWAVES == w) *(uint4*)(ring + SM::OQ + tile_off<RK>(r, c)) = make_uint4(0, 0, 0, 0);
     }
   }
   block_sync_lds();                        // phase-A tiles consumed; gates, K, Q visible; slot 1 free
