@@ -827,6 +827,25 @@ __device__ inline void unit_lower_inverse(float* sA, int lda, float* sM, int ldm
   block_sync_lds();
 }
 
+// Inclusive prefix sum over the 64 lanes of a wave with DPP lane moves (no
+// LDS crossbar): shifts by 1, 2, 4 and 8 within each row of 16 (lanes
+// shifted in from outside the row read 0), then row 0's total added to row 1
+// and row 2's to row 3 (row broadcast of lane 15), then rows 0-1's total to
+// rows 2-3 (row broadcast of lane 31).
+template <int CTRL, int ROWS, bool BOUND>
+__device__ inline float dpp_src(float x) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, x), CTRL, ROWS, 0xF, BOUND));
+}
+__device__ inline float wave_incl_scan_dpp(float x) {
+  x += dpp_src<0x111, 0xF, true>(x);    // row_shr:1
+  x += dpp_src<0x112, 0xF, true>(x);    // row_shr:2
+  x += dpp_src<0x114, 0xF, true>(x);    // row_shr:4
+  x += dpp_src<0x118, 0xF, true>(x);    // row_shr:8
+  x += dpp_src<0x142, 0xA, false>(x);   // row_bcast:15 into rows 1 and 3
+  x += dpp_src<0x143, 0xC, false>(x);   // row_bcast:31 into rows 2 and 3
+  return x;
+}
+
 // Inclusive prefix sum of 64 values held one per lane of wave 0 (lane < 64).
 __device__ inline float wave_incl_scan(float x, int lane) {
 #pragma unroll

@@ -133,7 +133,7 @@ __global__ __launch_bounds__(PREP_THREADS) void k_prep(Params p) {
       const bool ok = lane < x.len;
       const float la = (ok && p.la) ? sm.rla[lane] : 0.f, be = ok ? sm.rbeta[lane] : 0.f;
       const float lm = ok ? (p.lam ? sm.rlam[lane] : p.lam_c) : 0.f;
-      const float b = wave_incl_scan(la, lane);
+      const float b = wave_incl_scan_dpp(la);
       sm.b[lane] = b;
       sm.beta[lane] = be;
       sm.lam[lane] = lm;
