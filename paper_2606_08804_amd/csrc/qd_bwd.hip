@@ -903,7 +903,7 @@ __global__ __launch_bounds__(INTRA_THREADS) __attribute__((amdgpu_waves_per_eu(2
       dbj += tot + sm.g[C - 1] * sd;
     }
     float x = lane_from(dbj, C - 1 - j);
-    x = wave_incl_scan_l(x, lb);
+    x = wave_incl_scan_dpp(x);
     const float suffix = lane_from(x, C - 1 - j);
     if (j < len) {
       const size_t gt = arow + (size_t)j * H;

@@ -720,14 +720,6 @@ __device__ inline float wave_sum_l(float x, int lane) {
   for (int off = 32; off >= 1; off >>= 1) x += lane_xor(x, off, lane);
   return x;
 }
-__device__ inline float wave_incl_scan_l(float x, int lane) {
-#pragma unroll
-  for (int off = 1; off < 64; off <<= 1) {
-    const float y = lane_from(x, (lane - off) & 63);
-    if (lane >= off) x += y;
-  }
-  return x;
-}
 
 // Sum over each row of 16 lanes with DPP lane moves (no LDS crossbar):
 // swaps within pairs and quads, then rotations by 4 and 8 within the row.
@@ -846,15 +838,6 @@ __device__ inline float wave_incl_scan_dpp(float x) {
   return x;
 }
 
-// Inclusive prefix sum of 64 values held one per lane of wave 0 (lane < 64).
-__device__ inline float wave_incl_scan(float x, int lane) {
-#pragma unroll
-  for (int off = 1; off < 64; off <<= 1) {
-    const float y = __shfl_up(x, off, 64);
-    if (lane >= off) x += y;
-  }
-  return x;
-}
 
 // Value rows per scan workgroup.  Every value tile of a (sequence, head)
 // re-reads the chunk operands shared by all its tiles (Q, K, T, P, gates), so
