@@ -162,14 +162,41 @@ def handoff_bytes_per_unit(stage, Dk, Dv, e, saved=True):
 KERNEL_SOURCES = ("qd_api.hip", "qd_bwd.hip", "qd_common.h", "qd_fwd.hip", "qd_rec_bwd.hip", "qd_step.hip")
 
 
+def strip_comments(src):
+    """C++ source without its comments, trailing blanks and empty lines (string
+    and character literals kept whole), so that editing a comment does not
+    change the digest."""
+    out, i, n = [], 0, len(src)
+    while i < n:
+        c = src[i]
+        if c in "\"'":
+            j = i + 1
+            while j < n and src[j] != c:
+                j += 2 if src[j] == "\\" else 1
+            out.append(src[i:j + 1])
+            i = j + 1
+        elif src.startswith("//", i):
+            j = src.find("\n", i)
+            i = n if j < 0 else j
+        elif src.startswith("/*", i):
+            j = src.find("*/", i + 2)
+            i = n if j < 0 else j + 2
+        else:
+            out.append(c)
+            i += 1
+    lines = (l.rstrip() for l in "".join(out).split("\n"))
+    return "\n".join(l for l in lines if l)
+
+
 def source_digest():
-    """Digest of the kernel sources, to tell whether stored counters still apply."""
+    """Digest of the kernel sources' code (comments left out), to tell whether
+    stored counters still apply."""
     h = hashlib.sha256()
     csrc = os.path.join(ROOT, "paper_2606_08804_amd", "csrc")
     for f in KERNEL_SOURCES:
-        with open(os.path.join(csrc, f), "rb") as fh:
+        with open(os.path.join(csrc, f), encoding="utf-8") as fh:
             h.update(f.encode())
-            h.update(fh.read())
+            h.update(strip_comments(fh.read()).encode())
     return h.hexdigest()[:16]
 
 

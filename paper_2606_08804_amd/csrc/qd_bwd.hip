@@ -91,7 +91,7 @@ struct alignas(16) ScanBwdSmem {
 // waves pass three barriers:
 //   B_a  dS' staged, set X, P       phase 2: dS' output; dD = P^T dO +
 //        visible                    Kbar dS'^T (as its transpose); dD staged;
-//   B_b  dD staged, set M visible   phase 3: dD output; dV = diag(beta) M^T dD
+//   B_b  dD staged, set M visible   phase 3: dV = diag(beta) M^T dD
 //                                   (as its transpose), stored; the gated
 //                                   operands z1, z2 of the state gradient
 //                                   formed elementwise from dV and dO;
@@ -555,10 +555,10 @@ __global__ __launch_bounds__(INTRA_THREADS) __attribute__((amdgpu_waves_per_eu(2
   };
 
   // First tile, P (into the M buffer) and the second tile; every later tile
-  // once the one before it has landed; with the last tile the chunk's K and Q
-  // rows into the free slot 0 (for phase B; rows past the chunk re-read its
-  // last row and are zeroed afterwards), and once the last tile's dD is
-  // formed, M over P.
+  // once the one before it has landed; with the last tile the chunk's Q rows
+  // into the free slot 0 (for phase B; rows past the chunk re-read its last
+  // row and are zeroed afterwards) beside the K rows the waves write from
+  // their registers, and once the last tile's dD is formed, M over P.
   constexpr int ML = C * RC / 1024 / NWAVES;
   issue(0);
   {
