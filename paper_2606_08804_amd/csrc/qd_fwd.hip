@@ -33,19 +33,22 @@ template <typename E, int DK>
 struct alignas(16) PrepSmem {
   static constexpr int P = Pad<E>::v;
   static constexpr int RK = DK * (int)sizeof(E);
-  alignas(16) char Kt[2][C * RK];   // K and Q of a unit (swizzled direct-load tiles),
-  alignas(16) char Qt[2][C * RK];   // the next unit's landing while this one is solved
-  alignas(16) float b[C], beta[C], lam[C];
-  alignas(16) float rla[C], rbeta[C], rlam[C];   // raw gate vectors of the unit in flight
-  float A[C][C + 4];          // strictly lower A, consumed by the solve
+  alignas(16) char Kt[C * RK];      // K and Q of a unit (swizzled direct-load tiles); the
+  alignas(16) char Qt[C * RK];      // next unit's land here once the Gram products are done
+  alignas(16) float rla[C], rbeta[C], rlam[C];   // raw gate vectors of the next unit
+  alignas(16) float b[C], beta[C], lam[C];       // the gate block
+  float A[C][C + 4];          // strictly lower A, consumed (overwritten) by the solve
   alignas(16) float M[C][C + 4];
-  E Pm[C][C + P];             // P staging
+  E Pm[C][C + P];             // P staging; its blocks above the diagonal stay zero
 };
 
-constexpr int PREP_THREADS = 512;   // 8 waves: two per SIMD hide each other's latency
+// Four waves per workgroup and two workgroups per CU: each workgroup's
+// barriers pace only itself, so the latency chains of one (UT solve, Gram)
+// run beside the other's.
+constexpr int PREP_THREADS = 256;
 
 // Copies a C x D LDS tile (row stride ld elements) to a dense row-major
-// global block with 16-byte stores.
+// global block with 16-byte stores by NT threads.
 template <typename E, int D, int NT>
 __device__ inline void store_tile(E* dst, const E* src, int ld, int tid) {
   constexpr int VEC = 16 / sizeof(E), PR = D / VEC;
@@ -59,25 +62,31 @@ __device__ inline void store_tile(E* dst, const E* src, int ld, int tid) {
 // Writes, for every unit, the gate block (b, beta, lambda), the intra-chunk
 // output operator P = Gam * M_causal * Q K^T, M = (I + A)^{-1} (when p.wM is
 // set) and T = M diag(beta).  Persistent: each workgroup walks units
-// blockIdx.x, +gridDim.x, ...  The next unit's K, Q and raw gate vectors go
-// straight into LDS (direct loads in assembly form; K and Q into the other
-// buffer) once this unit's P is out, so they land during the UT solve; the
-// only memory operations issued after them are this unit's M and T stores,
-// which fixes the wait count at the top of the next unit (the compiler's
-// wait for register loads would also cover every store still in flight).
+// blockIdx.x, +gridDim.x, ...: the gate block (wave 0) and the Gram products
+// K K^T, Q K^T (wave w: its row of 16 x 16 blocks), A and P, P's store, the
+// UT solve (the blocked inverse below, the products of each level spread over
+// the four waves), M and T.  Once the Gram products are done the next unit's
+// K, Q and raw gates go straight into LDS (direct loads in assembly form) and
+// land during the solve; the only memory operations issued after them are
+// this unit's P, M and T stores, which fixes the wait count at the top of
+// the next unit (the compiler's wait for register loads would also cover
+// every store still in flight).
 template <typename E, int DK, int DV>
 __global__ __launch_bounds__(PREP_THREADS) void k_prep(Params p) {
   constexpr int NT = PREP_THREADS, NW = NT / 64;
   constexpr int P = Pad<E>::v;
-  constexpr int LC = C + P;
-  constexpr int RK = DK * (int)sizeof(E), KS = Mma<E>::KS;
-  constexpr int VEC = 16 / sizeof(E), MT_ITERS = C * C / VEC / NT;   // M/T store rounds per thread
-  static_assert(C == 64 && C * C / VEC % NT == 0, "wave 0 holds the gate vectors; M/T stores split evenly");
+  constexpr int LC = C + P, LA = C + 4;
+  constexpr int RK = DK * (int)sizeof(E), KS = Mma<E>::KS, NKK = DK / KS;
+  constexpr int VEC = 16 / sizeof(E);
+  constexpr int MT_ITERS = C * C / VEC / NT;   // M/T store rounds per thread
+  constexpr int PT_ITERS = C * C / VEC / NT;   // P store rounds per thread
+  static_assert(C == 64 && NW == 4 && (C * C / VEC) % NT == 0, "four waves, one row of blocks each");
   typedef typename Mma<E>::frag FR;
   __shared__ PrepSmem<E, DK> sm;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;   // vector wave index: measured faster here than the scalar one
   const int H = p.H;
   const int total = p.n_slots * H;
+  const bool keep_m = p.wM != nullptr;
 
   struct Unit {
     int g, h, t0, len;
@@ -93,13 +102,13 @@ __global__ __launch_bounds__(PREP_THREADS) void k_prep(Params p) {
   };
   // K, Q rows past the chunk re-read its last row: they meet only zero
   // gates, or masked entries of P; so do the raw gates, masked when read
-  auto issue = [&](const Unit& x, int buf) {
+  auto issue = [&](const Unit& x) {
     if (!x.valid) return;
     const size_t row = (size_t)x.t0 * H + x.h;
     const char* Kg = (const char*)((const E*)p.k + row * DK);
     const char* Qg = (const char*)((const E*)p.q + row * DK);
-    dma_rows<RK, C, NW, true>(sm.Kt[buf], Kg, (size_t)H * RK, x.len, Kg + (size_t)(x.len - 1) * H * RK, 0, w, lane);
-    dma_rows<RK, C, NW, true>(sm.Qt[buf], Qg, (size_t)H * RK, x.len, Qg + (size_t)(x.len - 1) * H * RK, 0, w, lane);
+    dma_rows<RK, C, NW, true>(sm.Kt, Kg, (size_t)H * RK, x.len, Kg + (size_t)(x.len - 1) * H * RK, 0, w, lane);
+    dma_rows<RK, C, NW, true>(sm.Qt, Qg, (size_t)H * RK, x.len, Qg + (size_t)(x.len - 1) * H * RK, 0, w, lane);
     if (w == 0) {
       const size_t gt = row + (size_t)min(lane, x.len - 1) * H;
       if (p.la) dma4_asm(p.la + gt, (char*)sm.rla);
@@ -108,26 +117,35 @@ __global__ __launch_bounds__(PREP_THREADS) void k_prep(Params p) {
     }
   };
 
+  // UT solve, M = (I + A)^{-1} blocked 16 x 16: A~_mj = A_mj M_jj,
+  // M_ij = -sum_{m=j+1..i} M_im A~_mj
+  auto blkA = [&](int i, int j) { return &sm.A[16 * i][16 * j]; };
+  auto blkM = [&](int i, int j) { return &sm.M[16 * i][16 * j]; };
+  auto put = [&](float* dst, f4 v, float sc) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) dst[frow(lane, j) * LA + fcol(lane)] = sc * v[j];
+  };
+  auto prod = [&](const float* a, const float* m, f4 acc) {
+    return mma_k<float, 16>(kmaj(a, LA), imaj(m, LA), 0, 0, acc, lane);
+  };
+
+  for (int idx = tid; idx < C * LC; idx += NT) (&sm.Pm[0][0])[idx] = fromf<E>(0.f);
   Unit cur;
   find(blockIdx.x, cur);
-  issue(cur, 0);
+  issue(cur);
   wait_vm<0>();
-  int buf = 0;
-  for (int u = blockIdx.x; u < total; u += gridDim.x, buf ^= 1) {
+  for (int u = blockIdx.x; u < total; u += gridDim.x) {
     const Unit x = cur;
     Unit nx;
     find(u + gridDim.x, nx);
-    block_sync_lds();                        // x's K, Q landed in every wave; the previous unit's LDS use is over
+    block_sync_lds();                        // x's inputs landed in every wave; the previous unit's LDS use is over
     if (!x.valid) {                          // uniform across the workgroup
-      issue(nx, buf ^ 1);
+      issue(nx);
       wait_vm<0>();
       cur = nx;
       continue;
     }
-    const int h = x.h;
-    const size_t gi = (size_t)x.g * H + h;
-    const char* Kt = sm.Kt[buf];
-    const char* Qt = sm.Qt[buf];
+    const size_t gi = (size_t)x.g * H + x.h;
     if (w == 0) {
       // gates past the chunk's end are zero; NULL lambda: the constant
       const bool ok = lane < x.len;
@@ -137,58 +155,128 @@ __global__ __launch_bounds__(PREP_THREADS) void k_prep(Params p) {
       sm.b[lane] = b;
       sm.beta[lane] = be;
       sm.lam[lane] = lm;
-      // gate block: b, beta, lambda (zero past the chunk's end)
       float* gblk = p.wb + gi * 3 * C;
       gblk[lane] = b;
       gblk[C + lane] = be;
       gblk[2 * C + lane] = lm;
     }
-    block_sync_lds();
-
-    // A = strictLower(diag(beta) Gam * X K^T), X K^T = K K^T + diag(lambda) Q K^T,
-    // and P (staged in Pm)
+    // K K^T and Q K^T: row block w, all four column blocks
+    f4 kk[4], qk[4];
 #pragma unroll
-    for (int tk = 0; tk < 16 / NW; ++tk) {
-      const int t = w + tk * NW;
-      const int m0 = (t >> 2) * 16, n0 = (t & 3) * 16, i = n0 + fcol(lane);
-      const float bi = sm.b[i];
+    for (int n = 0; n < 4; ++n) kk[n] = qk[n] = zero4();
+#pragma unroll
+    for (int ks = 0; ks < NKK; ++ks) {
+      const FR kA = tile_frag<E, RK>(sm.Kt, 16 * w, ks * KS, lane);
+      const FR qA = tile_frag<E, RK>(sm.Qt, 16 * w, ks * KS, lane);
+#pragma unroll
+      for (int n = 0; n < 4; ++n) {
+        const FR kB = tile_frag<E, RK>(sm.Kt, 16 * n, ks * KS, lane);
+        kk[n] = Mma<E>::mma(kA, kB, kk[n]);
+        qk[n] = Mma<E>::mma(qA, kB, qk[n]);
+      }
+    }
+    block_sync_lds();                        // gates visible; K and Q no longer read
+    issue(nx);                               // lands during the solve
+    {
+      // A = strictLower(diag(beta) Gam * X K^T), X K^T = K K^T + diag(lambda) Q K^T,
+      // and P (staged in Pm), blocks on and below the diagonal
       float br[4], betr[4], lr[4];
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
-        const int r = m0 + frow(lane, j);
+        const int r = 16 * w + frow(lane, j);
         br[j] = sm.b[r];
         betr[j] = sm.beta[r];
         lr[j] = sm.lam[r];
       }
-      f4 kk = zero4(), qk = zero4();
 #pragma unroll
-      for (int ks = 0; ks < DK / KS; ++ks) {
-        const FR kB = tile_frag<E, RK>(Kt, n0, ks * KS, lane);
-        kk = Mma<E>::mma(tile_frag<E, RK>(Kt, m0, ks * KS, lane), kB, kk);
-        qk = Mma<E>::mma(tile_frag<E, RK>(Qt, m0, ks * KS, lane), kB, qk);
-      }
+      for (int n = 0; n < 4; ++n) {
+        if (n > w) continue;                  // uniform: above the diagonal
+        const int i = 16 * n + fcol(lane);
+        const float bi = sm.b[i];
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const int r = m0 + frow(lane, j);
-        const float gam = (r >= i) ? __expf(br[j] - bi) : 0.f;
-        sm.A[r][i] = (r > i) ? betr[j] * gam * (kk[j] + lr[j] * qk[j]) : 0.f;
-        sm.Pm[r][i] = fromf<E>(gam * qk[j]);
+        for (int j = 0; j < 4; ++j) {
+          const int r = 16 * w + frow(lane, j);
+          const float gam = (r >= i) ? __expf(br[j] - bi) : 0.f;
+          sm.A[r][i] = (r > i) ? betr[j] * gam * (kk[n][j] + lr[j] * qk[n][j]) : 0.f;
+          sm.Pm[r][i] = fromf<E>(gam * qk[n][j]);
+        }
       }
     }
     block_sync_lds();
     store_tile<E, C, NT>((E*)p.wP + gi * C * C, &sm.Pm[0][0], LC, tid);
-    issue(nx, buf ^ 1);
-
-    // UT solve: M = (I + A)^{-1}; M (only the backward reads it, so only
-    // when the context is kept) and T = M diag(beta) are stored with
-    // strictly-upper 16 x 16 blocks zero; a thread takes VEC consecutive
-    // columns of one row
-    unit_lower_inverse<NT>(&sm.A[0][0], C + 4, &sm.M[0][0], C + 4, tid);
+    if (lane < 16) {
+      // column j of (I + A_ww)^{-1}; row r of the block is read as four
+      // broadcast 16-byte loads one row ahead of its use
+      const int j = lane;
+      const float* blk = blkA(w, w);
+      float m[16];
+      f4 cu[4], nxt[4];
+#pragma unroll
+      for (int qq = 0; qq < 4; ++qq) cu[qq] = *(const f4*)(blk + (size_t)1 * LA + 4 * qq);
+      m[0] = (j == 0) ? 1.f : 0.f;
+#pragma unroll
+      for (int r = 1; r < 16; ++r) {
+        if (r + 1 < 16) {
+#pragma unroll
+          for (int qq = 0; qq < 4; ++qq) nxt[qq] = *(const f4*)(blk + (size_t)(r + 1) * LA + 4 * qq);
+        }
+        float s4[4] = {(r == j) ? 1.f : 0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int i = 0; i < r; ++i) s4[i & 3] -= cu[i >> 2][i & 3] * m[i];
+        m[r] = (s4[0] + s4[1]) + (s4[2] + s4[3]);
+#pragma unroll
+        for (int qq = 0; qq < 4; ++qq) cu[qq] = nxt[qq];
+      }
+      float* out = blkM(w, w);
+#pragma unroll
+      for (int r = 0; r < 16; ++r) out[r * LA + j] = m[r];
+    }
+    block_sync_lds();
     {
-      const bool keep_m = p.wM != nullptr;
+      // A~ blocks: wave 0 (1,0) and (3,1), wave 1 (2,1) and (3,0), wave 2 (3,2), wave 3 (2,0)
+      auto tilde = [&](int bm, int bj) { put(blkA(bm, bj), prod(blkA(bm, bj), blkM(bj, bj), zero4()), 1.f); };
+      if (w == 0) { tilde(1, 0); tilde(3, 1); }
+      else if (w == 1) { tilde(2, 1); tilde(3, 0); }
+      else if (w == 2) tilde(3, 2);
+      else tilde(2, 0);
+    }
+    block_sync_lds();
+    // level 1: M_10, M_21, M_32 and the diagonal-block parts of M_20, M_31, M_30
+    f4 part = zero4();
+    if (w < 3) {
+      const int bb = w + 1;                  // M_b,b-1 = -M_bb A~_b,b-1
+      put(blkM(bb, bb - 1), prod(blkM(bb, bb), blkA(bb, bb - 1), zero4()), -1.f);
+      if (w == 0) part = prod(blkM(2, 2), blkA(2, 0), zero4());        // M_20
+      else if (w == 1) part = prod(blkM(3, 3), blkA(3, 1), zero4());   // M_31
+      else part = prod(blkM(3, 3), blkA(3, 0), zero4());               // M_30
+    }
+    block_sync_lds();
+    // level 2: M_20 += M_21 A~_10, M_31 += M_32 A~_21, M_30 += M_32 A~_20
+    if (w == 0) {
+      part = prod(blkM(2, 1), blkA(1, 0), part);
+      put(blkM(2, 0), part, -1.f);
+    } else if (w == 1) {
+      part = prod(blkM(3, 2), blkA(2, 1), part);
+      put(blkM(3, 1), part, -1.f);
+    } else if (w == 2) {
+      part = prod(blkM(3, 2), blkA(2, 0), part);
+    }
+    block_sync_lds();
+    // level 3: M_30 += M_31 A~_10
+    if (w == 2) {
+      part = prod(blkM(3, 1), blkA(1, 0), part);
+      put(blkM(3, 0), part, -1.f);
+    }
+    block_sync_lds();
+    {
+      // M (only the backward reads it, so only when the context is kept) and
+      // T = M diag(beta), strictly-upper 16 x 16 blocks zero; a thread takes
+      // VEC consecutive columns of one row
       E* wM = keep_m ? (E*)p.wM + gi * C * C : nullptr;
       E* wT = (E*)p.wT + gi * C * C;
-      for (int idx = tid; idx < C * C / VEC; idx += NT) {
+#pragma unroll
+      for (int it = 0; it < MT_ITERS; ++it) {
+        const int idx = tid + it * NT;
         const int r = idx / (C / VEC), i0 = (idx % (C / VEC)) * VEC;
         const bool upper = (i0 >> 4) > (r >> 4);
         uint4 mr, tr;
@@ -209,9 +297,10 @@ __global__ __launch_bounds__(PREP_THREADS) void k_prep(Params p) {
         if (keep_m) *(uint4*)(wM + r * C + i0) = mr;
         *(uint4*)(wT + r * C + i0) = tr;
       }
-      // the next unit's loads went out before these stores (in-order counter)
-      if (keep_m) wait_vm<2 * MT_ITERS>();
-      else wait_vm<MT_ITERS>();
+      // the next unit's loads went out before P's and these stores (in-order
+      // counter)
+      if (keep_m) wait_vm<PT_ITERS + 2 * MT_ITERS>();
+      else wait_vm<PT_ITERS + MT_ITERS>();
     }
     cur = nx;
   }
@@ -671,9 +760,8 @@ template <typename E, int DK, int DV>
 static hipError_t launch_fwd_t(const Params& p, int in_bwd, int with_scan, hipStream_t st) {
   if (p.n_slots > 0) {
     const int units = p.n_slots * p.H;
-    // one persistent workgroup per CU (a second one per CU measured no
-    // faster: each ran at half speed)
-    dim3 gp(min(units, device_cu_count()));
+    // two persistent four-wave workgroups per CU
+    dim3 gp(min(units, 2 * device_cu_count()));
     const int stage = in_bwd ? ST_PREP_BWD : ST_PREP_FWD;
     prof_mark(stage, 0, st);
     hipLaunchKernelGGL((k_prep<E, DK, DV>), gp, dim3(PREP_THREADS), 0, st, p);
