@@ -735,90 +735,6 @@ __device__ inline float sum16(float x) {
   return x;
 }
 
-// ----------------------------------------------------------------- UT solve
-// Inverse of the unit lower-triangular C x C matrix I + A (the UT transform
-// of the delta-rule chunk form), A strictly lower, fp32, at sA[r*lda + i].
-// Writes M = (I + A)^{-1} to sM[r*ldm + i] for the 16 x 16 blocks on and
-// below the diagonal; the strictly-upper blocks of sM are left untouched and
-// callers treat them as zero.  sA is overwritten.  Called by all threads of
-// an eight-wave workgroup.
-//  1. diagonal blocks M_jj = (I + A_jj)^{-1} by forward substitution (one
-//     lane per column, row sums split four ways to shorten the FMA chain);
-//  2. A~_mj = A_mj M_jj for the six blocks below the diagonal, in place;
-//  3. from M L = I: M_ij = -sum_{m=j+1..i} M_im A~_mj, by block distance
-//     i - j, one fp32 MFMA product per wave and level (products that need
-//     only the diagonal blocks start at the first level).
-template <int NT>
-__device__ inline void unit_lower_inverse(float* sA, int lda, float* sM, int ldm, int tid) {
-  static_assert(NT == 512, "eight waves");
-  const int lane = tid & 63, w = tid >> 6;   // vector wave index (measured faster in the preparation kernel)
-  auto blkA = [&](int i, int j) { return sA + (size_t)(16 * i) * lda + 16 * j; };
-  auto blkM = [&](int i, int j) { return sM + (size_t)(16 * i) * ldm + 16 * j; };
-  auto put = [&](float* dst, int ld, f4 v, float sc) {
-#pragma unroll
-    for (int j = 0; j < 4; ++j) dst[frow(lane, j) * ld + fcol(lane)] = sc * v[j];
-  };
-  if (w < 4 && lane < 16) {
-    // column j of (I + A_ww)^{-1}; row r of the block is read as four
-    // broadcast 16-byte loads one row ahead of its use
-    const int j = lane;
-    const float* blk = blkA(w, w);
-    float m[16];
-    f4 cur[4], nxt[4];
-#pragma unroll
-    for (int q = 0; q < 4; ++q) cur[q] = *(const f4*)(blk + (size_t)1 * lda + 4 * q);
-    m[0] = (j == 0) ? 1.f : 0.f;
-#pragma unroll
-    for (int r = 1; r < 16; ++r) {
-      if (r + 1 < 16) {
-#pragma unroll
-        for (int q = 0; q < 4; ++q) nxt[q] = *(const f4*)(blk + (size_t)(r + 1) * lda + 4 * q);
-      }
-      float s4[4] = {(r == j) ? 1.f : 0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-      for (int i = 0; i < r; ++i) s4[i & 3] -= cur[i >> 2][i & 3] * m[i];
-      m[r] = (s4[0] + s4[1]) + (s4[2] + s4[3]);
-#pragma unroll
-      for (int q = 0; q < 4; ++q) cur[q] = nxt[q];
-    }
-    float* out = blkM(w, w);
-#pragma unroll
-    for (int r = 0; r < 16; ++r) out[r * ldm + j] = m[r];
-  }
-  block_sync_lds();
-  // wave -> (m, j) of A~_mj: (1,0) (2,1) (3,2) (2,0) (3,1) (3,0)
-  const int bm = (w < 3) ? w + 1 : (w == 3 ? 2 : 3);
-  const int bj = (w < 3) ? w : (w == 4 ? 1 : 0);
-  if (w < 6) {
-    const f4 t = mma_k<float, 16>(kmaj(blkA(bm, bj), lda), imaj(blkM(bj, bj), ldm), 0, 0, zero4(), lane);
-    put(blkA(bm, bj), lda, t, 1.f);
-  }
-  block_sync_lds();
-  // level 1: M_10, M_21, M_32 (waves 0-2) and the partial sums of M_20, M_31,
-  // M_30 that use diagonal blocks only (waves 3-5)
-  f4 part = zero4();
-  if (w < 6) {
-    const int bi = (w < 3) ? w + 1 : (w == 3 ? 2 : 3);   // M_{bi,bi} A~_{bm,bj}
-    part = mma_k<float, 16>(kmaj(blkM(bi, bi), ldm), imaj(blkA(bm, bj), lda), 0, 0, part, lane);
-    if (w < 3) put(blkM(bm, bj), ldm, part, -1.f);
-  }
-  block_sync_lds();
-  // level 2: M_20 += M_21 A~_10, M_31 += M_32 A~_21, and M_30 += M_32 A~_20
-  if (w >= 3 && w < 6) {
-    const int li = (w == 3) ? 2 : 3, lm = (w == 3) ? 1 : 2;     // M_{li,lm}
-    const int ai = (w == 3) ? 1 : 2, aj = (w == 5) ? 0 : ai - 1; // A~_{lm,aj}
-    part = mma_k<float, 16>(kmaj(blkM(li, lm), ldm), imaj(blkA(ai, aj), lda), 0, 0, part, lane);
-    if (w < 5) put(blkM(li, aj), ldm, part, -1.f);
-  }
-  block_sync_lds();
-  // level 3: M_30 += M_31 A~_10
-  if (w == 5) {
-    part = mma_k<float, 16>(kmaj(blkM(3, 1), ldm), imaj(blkA(1, 0), lda), 0, 0, part, lane);
-    put(blkM(3, 0), ldm, part, -1.f);
-  }
-  block_sync_lds();
-}
-
 // Inclusive prefix sum over the 64 lanes of a wave with DPP lane moves (no
 // LDS crossbar): shifts by 1, 2, 4 and 8 within each row of 16 (lanes
 // shifted in from outside the row read 0), then row 0's total added to row 1
