@@ -120,60 +120,11 @@ __device__ inline f4 mma_k(AV a, BV b, int m0, int n0, f4 acc, int lane) {
   return acc;
 }
 
-// Same with a run-time contraction length (multiple of KS).
-template <typename E, typename AV, typename BV>
-__device__ inline f4 mma_kn(AV a, BV b, int m0, int n0, int K, f4 acc, int lane) {
-  for (int k0 = 0; k0 < K; k0 += Mma<E>::KS)
-    acc = Mma<E>::mma(Frag<E>::load(a, m0, k0, lane), Frag<E>::load(b, n0, k0, lane), acc);
-  return acc;
-}
-
 __device__ inline f4 zero4() { return f4{0.f, 0.f, 0.f, 0.f}; }
 
 // Row of C-fragment element j for this lane, relative to the tile origin.
 __device__ inline int frow(int lane, int j) { return ((lane >> 4) << 2) + j; }
 __device__ inline int fcol(int lane) { return lane & 15; }
-
-// ----------------------------------------------------------------- tile loads
-// Load rows [0, C) of a [*, ld_g] global matrix block (row stride `gs`
-// elements, D columns) into LDS dst[r*ld + c], zero-filling rows >= len.
-template <typename E, int D, int NT = NTHREADS>
-__device__ inline void load_rows(E* dst, int ld, const E* src, size_t gs, int len, int tid) {
-  constexpr int VEC = 16 / sizeof(E);
-  constexpr int PR = D / VEC;
-  for (int idx = tid; idx < C * PR; idx += NT) {
-    const int r = idx / PR, c = (idx % PR) * VEC;
-    uint4 val = make_uint4(0, 0, 0, 0);
-    if (r < len) val = *(const uint4*)(src + (size_t)r * gs + c);
-    *(uint4*)(dst + (size_t)r * ld + c) = val;
-  }
-}
-
-// Same, storing the transpose: dst[c*ld + r] = scale(r) * src[r][c].
-template <typename E, int D, typename Scale, int NT = NTHREADS>
-__device__ inline void load_rows_t(E* dst, int ld, const E* src, size_t gs, int len, int tid,
-                                   Scale scale) {
-  constexpr int VEC = 16 / sizeof(E);
-  constexpr int PR = D / VEC;
-  for (int idx = tid; idx < C * PR; idx += NT) {
-    const int r = idx % C, c = (idx / C) * VEC;   // consecutive threads -> consecutive rows
-    E vals[VEC];
-    if (r < len) {
-      uint4 raw = *(const uint4*)(src + (size_t)r * gs + c);
-      const E* pv = (const E*)&raw;
-      const float s = scale(r);
-#pragma unroll
-      for (int j = 0; j < VEC; ++j) vals[j] = fromf<E>(tof(pv[j]) * s);
-    } else {
-#pragma unroll
-      for (int j = 0; j < VEC; ++j) vals[j] = fromf<E>(0.f);
-    }
-#pragma unroll
-    for (int j = 0; j < VEC; ++j) dst[(size_t)(c + j) * ld + r] = vals[j];
-  }
-}
-
-struct One { __device__ float operator()(int) const { return 1.f; } };
 
 // Four consecutive activation-dtype values of one lane's C fragment.
 template <typename E> struct Quad;
@@ -200,127 +151,8 @@ template <> struct Quad<float> {
   }
 };
 
-// Register staging of an R x COLS tile (row stride `rs` elements in global,
-// rows >= valid read as zero) for software prefetch: load() issues the global
-// reads, store() writes the tile to LDS with 16-byte stores.
-template <typename E, int R, int COLS, int NT = NTHREADS>
-struct TileRegs {
-  static constexpr int VEC = 16 / sizeof(E);
-  static constexpr int PR = COLS / VEC;
-  static constexpr int TOTAL = R * PR;
-  static constexpr int N = (TOTAL + NT - 1) / NT;
-  static_assert(TOTAL % NT == 0 || TOTAL < NT, "tile must split evenly over the workgroup");
-  uint4 v[N];
-  __device__ static inline bool owns(int i, int tid) { return TOTAL >= NT || tid + i * NT < TOTAL; }
-  __device__ inline void load(const E* src, size_t rs, int valid, int tid) {
-#pragma unroll
-    for (int i = 0; i < N; ++i) {
-      const int idx = tid + i * NT, r = idx / PR, c = (idx % PR) * VEC;
-      v[i] = (owns(i, tid) && r < valid) ? *(const uint4*)(src + (size_t)r * rs + c) : make_uint4(0, 0, 0, 0);
-    }
-  }
-  __device__ inline void store(E* dst, int ld, int tid) const {
-#pragma unroll
-    for (int i = 0; i < N; ++i) {
-      const int idx = tid + i * NT, r = idx / PR, c = (idx % PR) * VEC;
-      if (owns(i, tid)) *(uint4*)(dst + (size_t)r * ld + c) = v[i];
-    }
-  }
-  // Branch-free variant for loads that must not wait on each other: rows at
-  // or past `valid` (>= 1) re-read row valid - 1, and store_rows() writes
-  // them as zero.
-  __device__ inline void load_clamped(const E* src, size_t rs, int valid, int tid) {
-#pragma unroll
-    for (int i = 0; i < N; ++i) {
-      const int idx = tid + i * NT, r = min(idx / PR, valid - 1), c = (idx % PR) * VEC;
-      if (owns(i, tid)) v[i] = *(const uint4*)(src + (size_t)r * rs + c);
-    }
-  }
-  __device__ inline void store_rows(E* dst, int ld, int valid, int tid) const {
-#pragma unroll
-    for (int i = 0; i < N; ++i) {
-      const int idx = tid + i * NT, r = idx / PR, c = (idx % PR) * VEC;
-      if (owns(i, tid)) *(uint4*)(dst + (size_t)r * ld + c) = r < valid ? v[i] : make_uint4(0, 0, 0, 0);
-    }
-  }
-};
-
-// As TileRegs, but consecutive threads take consecutive rows, so that the
-// transposed LDS store storeT() (dst[c*ld + r]) is free of bank conflicts.
-template <typename E, int R, int COLS, int NT = NTHREADS>
-struct TileRegsT {
-  static constexpr int VEC = 16 / sizeof(E);
-  static constexpr int PR = COLS / VEC;
-  static constexpr int N = R * PR / NT;
-  static_assert(N >= 1 && N * NT == R * PR && NT % R == 0, "tile split");
-  uint4 v[N];
-  __device__ inline void load(const E* src, size_t rs, int valid, int tid) {
-#pragma unroll
-    for (int i = 0; i < N; ++i) {
-      const int idx = tid + i * NT, r = idx % R, c = (idx / R) * VEC;
-      v[i] = r < valid ? *(const uint4*)(src + (size_t)r * rs + c) : make_uint4(0, 0, 0, 0);
-    }
-  }
-  __device__ inline void storeT(E* dst, int ld, int tid) const {
-#pragma unroll
-    for (int i = 0; i < N; ++i) {
-      const int idx = tid + i * NT, r = idx % R, c = (idx / R) * VEC;
-      const E* e = (const E*)&v[i];
-#pragma unroll
-      for (int j = 0; j < VEC; ++j) dst[(size_t)(c + j) * ld + r] = e[j];
-    }
-  }
-};
-
-// fp32 tile staged in registers and written to LDS converted to E.
-template <typename E, int R, int COLS, int NT = NTHREADS>
-struct TileRegsF {
-  static constexpr int PR = COLS / 4;
-  static constexpr int TOTAL = R * PR;
-  static constexpr int N = TOTAL / NT;
-  static_assert(N >= 1 && N * NT == TOTAL, "tile split");
-  f4 v[N];
-  __device__ inline void load(const float* src, size_t rs, int tid) {
-#pragma unroll
-    for (int i = 0; i < N; ++i) {
-      const int idx = tid + i * NT, r = idx / PR, c = (idx % PR) * 4;
-      v[i] = *(const f4*)(src + (size_t)r * rs + c);
-    }
-  }
-  __device__ inline void store(E* dst, int ld, int tid) const {
-#pragma unroll
-    for (int i = 0; i < N; ++i) {
-      const int idx = tid + i * NT, r = idx / PR, c = (idx % PR) * 4;
-      *(typename Quad<E>::raw*)(dst + (size_t)r * ld + c) = Quad<E>::pack(v[i]);
-    }
-  }
-};
-
-struct NoRegs {};
-
 // Number of compute units of the current device (host side, cached).
 int device_cu_count();
-
-template <typename F> __device__ inline F zero_frag();
-template <> __device__ inline bf8 zero_frag<bf8>() { return __builtin_bit_cast(bf8, make_uint4(0, 0, 0, 0)); }
-template <> __device__ inline float zero_frag<float>() { return 0.f; }
-
-// MFMA A-operand fragments of one 16-row block, loaded straight from global
-// memory into registers (row-major source, k contiguous, row stride `ld`).
-// Rows at or beyond `valid` (relative to the block's first row) read as zero.
-template <typename E, int K>
-struct AFrag {
-  typedef typename Mma<E>::frag frag;
-  static constexpr int NK = K / Mma<E>::KS;
-  frag f[NK];
-  __device__ inline void load(const E* row0, size_t ld, int valid, int lane) {
-    const int r = lane & 15;
-    const E* src = row0 + (size_t)r * ld + (lane >> 4) * Mma<E>::KPL;
-#pragma unroll
-    for (int ks = 0; ks < NK; ++ks)
-      f[ks] = r < valid ? *(const frag*)(src + ks * Mma<E>::KS) : zero_frag<frag>();
-  }
-};
 
 // Workgroup barrier that orders LDS traffic only: outstanding global loads
 // (software prefetch) stay in flight across it.
@@ -379,13 +211,6 @@ __device__ inline void dma4_asm(const void* g, char* lds) {
 }
 #pragma clang diagnostic pop
 
-// Passes a register through an empty assembly statement: the compiler must
-// have the value at this point, so it waits here for its own load of it.
-template <typename T>
-__device__ inline void reg_ready(T& x) {
-  asm volatile("" : "+v"(x));
-}
-
 // Direct global->LDS copy of a ROWS x RB-byte block (row stride `stride`
 // bytes) into the swizzled layout at `dst`.  Each instruction moves 1 KB
 // (lane i writes LDS bytes 16i..16i+15 of it); wave w of NW issues
@@ -408,15 +233,6 @@ __device__ inline void dma_rows(char* dst, const char* src, size_t stride, int v
       __builtin_amdgcn_global_load_lds((const void*)g, (__attribute__((address_space(3))) void*)(dst + i * 1024),
                                        16, 0, 0);
   }
-}
-
-// Direct global->LDS copy (assembly form) of NBYTES contiguous bytes, a
-// multiple of 1 KB, by one wave, byte for byte.
-template <int NBYTES>
-__device__ inline void dma_block_asm(char* dst, const char* src, int lane) {
-  static_assert(NBYTES % 1024 == 0, "whole instructions");
-#pragma unroll
-  for (int i = 0; i < NBYTES / 1024; ++i) dma16_asm(src + i * 1024 + lane * 16, dst + i * 1024);
 }
 
 // MFMA fragment (A or B operand; both map lane l to row l & 15 and to the
@@ -493,113 +309,6 @@ template <>
 __device__ inline float tr_frag<float>(const float* base, int ld, int k0, int j0, int lane) {
   return base[(size_t)(k0 + (lane >> 4)) * ld + j0 + (lane & 15)];
 }
-// Four consecutive rows i0 .. i0+3 of column j0 + (l & 15) of a row-major
-// 16-bit LDS matrix for lane l (one transpose read; lanes of a 16-lane group
-// share i0), returned as floats.
-__device__ inline f4 tr_col4(const __bf16* base, int ld, int i0, int j0, int lane) {
-  typedef __bf16 v4b __attribute__((ext_vector_type(4)));
-  typedef __attribute__((address_space(3))) v4b* lp;
-  const int L = lane & 15;
-  const __bf16* a = base + (size_t)(i0 + (L >> 2)) * ld + j0 + 4 * (L & 3);
-  const v4b v = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lp)(uintptr_t)(uint32_t)(uintptr_t)a);
-  return f4{(float)v[0], (float)v[1], (float)v[2], (float)v[3]};
-}
-__device__ inline f4 tr_col4(const float* base, int ld, int i0, int j0, int lane) {
-  f4 r;
-#pragma unroll
-  for (int e = 0; e < 4; ++e) r[e] = base[(size_t)(i0 + e) * ld + j0 + (lane & 15)];
-  return r;
-}
-
-// ----------------------------------------------------------------- 16-wide k steps
-// Products with a C x C operand that was itself produced by an MFMA use the
-// 16-wide k step (v_mfma_f32_16x16x16_bf16, or four 16x16x4 fp32 steps), in
-// which lane l supplies the four k values 4 (l >> 4) .. +3 of its row or
-// column l & 15.  That is exactly how an MFMA result holds a 16 x 16 block
-// (rows 4 (l >> 4) + j, column l & 15), so a result block Z can serve as the
-// B operand (k = row of Z) or as the A operand of Z^T without leaving the
-// registers.  Q4<E>::t holds one lane's four values.
-template <typename E> struct Q4;
-template <> struct Q4<__bf16> {
-  typedef bf4 t;
-  __device__ static inline t from(f4 x) {
-    t r;
-#pragma unroll
-    for (int j = 0; j < 4; ++j) r[j] = (__bf16)x[j];
-    return r;
-  }
-  __device__ static inline f4 mma(t a, t b, f4 c) {
-    typedef short s4 __attribute__((ext_vector_type(4)));
-    return __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(__builtin_bit_cast(s4, a), __builtin_bit_cast(s4, b), c, 0,
-                                                      0, 0);
-  }
-};
-template <> struct Q4<float> {
-  typedef f4 t;
-  __device__ static inline t from(f4 x) { return x; }
-  // four k-steps of 4; in step j lane group l >> 4 supplies k = 4 (l >> 4) + j
-  __device__ static inline f4 mma(t a, t b, f4 c) {
-#pragma unroll
-    for (int j = 0; j < 4; ++j) c = __builtin_amdgcn_mfma_f32_16x16x4f32(a[j], b[j], c, 0, 0, 0);
-    return c;
-  }
-};
-// Four k values (rows k0 + 4 (l >> 4) .. +3) of column j0 + (l & 15) of a
-// row-major LDS matrix (element (k, j) at base + k * ld + j): one transpose
-// read for 16-bit elements.
-template <typename E>
-__device__ inline typename Q4<E>::t tr_q4(const E* base, int ld, int k0, int j0, int lane);
-template <>
-__device__ inline bf4 tr_q4<__bf16>(const __bf16* base, int ld, int k0, int j0, int lane) {
-  typedef __attribute__((address_space(3))) bf4* lp;
-  const int L = lane & 15;
-  const __bf16* a = base + (size_t)(k0 + 4 * (lane >> 4) + (L >> 2)) * ld + j0 + 4 * (L & 3);
-  return __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lp)(uintptr_t)(uint32_t)(uintptr_t)a);
-}
-template <>
-__device__ inline f4 tr_q4<float>(const float* base, int ld, int k0, int j0, int lane) {
-  const float* a = base + (size_t)(k0 + 4 * (lane >> 4)) * ld + j0 + (lane & 15);
-  return f4{a[0], a[(size_t)ld], a[(size_t)2 * ld], a[(size_t)3 * ld]};
-}
-// Same from a swizzled direct-load tile with rows of RB bytes.
-template <typename E, int RB>
-__device__ inline typename Q4<E>::t tile_tr_q4(const char* t, int k0, int j0, int lane) {
-  if constexpr (sizeof(E) == 2) {
-    typedef __attribute__((address_space(3))) bf4* lp;
-    const int L = lane & 15;
-    const char* a = t + tile_off<RB>(k0 + 4 * (lane >> 4) + (L >> 2), 2 * (j0 + 4 * (L & 3)));
-    return __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lp)(uintptr_t)(uint32_t)(uintptr_t)a);
-  } else {
-    const int r = k0 + 4 * (lane >> 4), cb = 4 * (j0 + (lane & 15));
-    return f4{*(const float*)(t + tile_off<RB>(r, cb)), *(const float*)(t + tile_off<RB>(r + 1, cb)),
-              *(const float*)(t + tile_off<RB>(r + 2, cb)), *(const float*)(t + tile_off<RB>(r + 3, cb))};
-  }
-}
-
-// Same from an fp32 tile, converted to E; the fp32 values are returned in v.
-template <typename E>
-__device__ inline typename Mma<E>::frag tile_frag_f32(const char* t, int row0, int k0, int lane,
-                                                      float (&v)[Mma<E>::KPL]) {
-  constexpr int RB = 128;
-  const int row = row0 + (lane & 15), k = k0 + (lane >> 4) * Mma<E>::KPL;
-  if constexpr (Mma<E>::KPL == 8) {
-    const f4 a = *(const f4*)(t + tile_off<RB>(row, k * 4));
-    const f4 b = *(const f4*)(t + tile_off<RB>(row, k * 4 + 16));
-    typename Mma<E>::frag f;
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      v[e] = a[e];
-      v[4 + e] = b[e];
-      f[e] = (E)a[e];
-      f[4 + e] = (E)b[e];
-    }
-    return f;
-  } else {
-    v[0] = *(const float*)(t + tile_off<RB>(row, k * 4));
-    return v[0];
-  }
-}
-
 
 
 // ----------------------------------------------------------------- parameters
@@ -701,12 +410,6 @@ __device__ inline bool locate(const Params& p, int g, int& n, int& t0, int& len)
 }
 
 // ----------------------------------------------------------------- reductions
-__device__ inline float wave_sum(float x) {
-#pragma unroll
-  for (int off = 32; off >= 1; off >>= 1) x += __shfl_xor(x, off, 64);
-  return x;
-}
-
 // Lane exchanges (ds_bpermute) addressed from a lane index the caller
 // supplies: a kernel near its register limit passes an index laundered per
 // phase, so that the exchange addresses of one phase are not kept alive
