@@ -62,8 +62,8 @@ __device__ inline void store_tile(E* dst, const E* src, int ld, int tid) {
 // Writes, for every unit, the gate block (b, beta, lambda), the intra-chunk
 // output operator P = Gam * M_causal * Q K^T, M = (I + A)^{-1} (when p.wM is
 // set) and T = M diag(beta).  Persistent: each workgroup walks units
-// blockIdx.x, +gridDim.x, ...: the gate block (wave 0) and the Gram products
-// K K^T, Q K^T (wave w: its row of 16 x 16 blocks), A and P, P's store, the
+// blockIdx.x, +gridDim.x, ...: the gate block and the Gram products K K^T,
+// Q K^T of the 16 x 16 blocks on and below the diagonal, A and P, P's store, the
 // UT solve (the blocked inverse below, the products of each level spread over
 // the four waves), M and T.  Once the Gram products are done the next unit's
 // K, Q and raw gates go straight into LDS (direct loads in assembly form) and
@@ -146,7 +146,11 @@ __global__ __launch_bounds__(PREP_THREADS) void k_prep(Params p) {
       continue;
     }
     const size_t gi = (size_t)x.g * H + x.h;
-    if (w == 0) {
+    const int ws = wave_id(tid);             // scalar: the branches below are uniform
+    // the ten 16 x 16 blocks on and below the diagonal (the others are zero in
+    // A and P): wave 0 (0,0) (1,0) (1,1), wave 1 (2,0) (2,1) (2,2), wave 2
+    // (3,0) (3,1) and the gate block, wave 3 (3,2) (3,3)
+    if (ws == 2) {
       // gates past the chunk's end are zero; NULL lambda: the constant
       const bool ok = lane < x.len;
       const float la = (ok && p.la) ? sm.rla[lane] : 0.f, be = ok ? sm.rbeta[lane] : 0.f;
@@ -160,46 +164,74 @@ __global__ __launch_bounds__(PREP_THREADS) void k_prep(Params p) {
       gblk[C + lane] = be;
       gblk[2 * C + lane] = lm;
     }
-    // K K^T and Q K^T: row block w, all four column blocks
-    f4 kk[4], qk[4];
+    // K K^T and Q K^T of the wave's blocks (row, column); operand fragments
+    // shared within a wave are read once
+    f4 kk[3], qk[3];
 #pragma unroll
-    for (int n = 0; n < 4; ++n) kk[n] = qk[n] = zero4();
+    for (int n = 0; n < 3; ++n) kk[n] = qk[n] = zero4();
+    auto gram = [&](auto... blk) {
+      constexpr int NBK = sizeof...(blk);
+      constexpr int br[NBK] = {(decltype(blk)::value / 4)...}, bc[NBK] = {(decltype(blk)::value % 4)...};
 #pragma unroll
-    for (int ks = 0; ks < NKK; ++ks) {
-      const FR kA = tile_frag<E, RK>(sm.Kt, 16 * w, ks * KS, lane);
-      const FR qA = tile_frag<E, RK>(sm.Qt, 16 * w, ks * KS, lane);
+      for (int ks = 0; ks < NKK; ++ks) {
+        FR kf[4], qf[4];
 #pragma unroll
-      for (int n = 0; n < 4; ++n) {
-        const FR kB = tile_frag<E, RK>(sm.Kt, 16 * n, ks * KS, lane);
-        kk[n] = Mma<E>::mma(kA, kB, kk[n]);
-        qk[n] = Mma<E>::mma(qA, kB, qk[n]);
+        for (int b = 0; b < NBK; ++b) {
+          kf[br[b]] = tile_frag<E, RK>(sm.Kt, 16 * br[b], ks * KS, lane);
+          qf[br[b]] = tile_frag<E, RK>(sm.Qt, 16 * br[b], ks * KS, lane);
+          kf[bc[b]] = tile_frag<E, RK>(sm.Kt, 16 * bc[b], ks * KS, lane);
+        }
+#pragma unroll
+        for (int b = 0; b < NBK; ++b) {
+          kk[b] = Mma<E>::mma(kf[br[b]], kf[bc[b]], kk[b]);
+          qk[b] = Mma<E>::mma(qf[br[b]], kf[bc[b]], qk[b]);
+        }
       }
-    }
+    };
+    typedef std::integral_constant<int, 0> B00;
+    typedef std::integral_constant<int, 4> B10;
+    typedef std::integral_constant<int, 5> B11;
+    typedef std::integral_constant<int, 8> B20;
+    typedef std::integral_constant<int, 9> B21;
+    typedef std::integral_constant<int, 10> B22;
+    typedef std::integral_constant<int, 12> B30;
+    typedef std::integral_constant<int, 13> B31;
+    typedef std::integral_constant<int, 14> B32;
+    typedef std::integral_constant<int, 15> B33;
+    if (ws == 0) gram(B00(), B10(), B11());
+    else if (ws == 1) gram(B20(), B21(), B22());
+    else if (ws == 2) gram(B30(), B31());
+    else gram(B32(), B33());
     block_sync_lds();                        // gates visible; K and Q no longer read
     issue(nx);                               // lands during the solve
     {
       // A = strictLower(diag(beta) Gam * X K^T), X K^T = K K^T + diag(lambda) Q K^T,
-      // and P (staged in Pm), blocks on and below the diagonal
-      float br[4], betr[4], lr[4];
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const int r = 16 * w + frow(lane, j);
-        br[j] = sm.b[r];
-        betr[j] = sm.beta[r];
-        lr[j] = sm.lam[r];
-      }
-#pragma unroll
-      for (int n = 0; n < 4; ++n) {
-        if (n > w) continue;                  // uniform: above the diagonal
+      // and P (staged in Pm), the wave's blocks
+      auto epilogue = [&](int m, int n, const f4& kkb, const f4& qkb) {
         const int i = 16 * n + fcol(lane);
         const float bi = sm.b[i];
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
-          const int r = 16 * w + frow(lane, j);
-          const float gam = (r >= i) ? __expf(br[j] - bi) : 0.f;
-          sm.A[r][i] = (r > i) ? betr[j] * gam * (kk[n][j] + lr[j] * qk[n][j]) : 0.f;
-          sm.Pm[r][i] = fromf<E>(gam * qk[n][j]);
+          const int r = 16 * m + frow(lane, j);
+          const float gam = (r >= i) ? __expf(sm.b[r] - bi) : 0.f;
+          sm.A[r][i] = (r > i) ? sm.beta[r] * gam * (kkb[j] + sm.lam[r] * qkb[j]) : 0.f;
+          sm.Pm[r][i] = fromf<E>(gam * qkb[j]);
         }
+      };
+      if (ws == 0) {
+        epilogue(0, 0, kk[0], qk[0]);
+        epilogue(1, 0, kk[1], qk[1]);
+        epilogue(1, 1, kk[2], qk[2]);
+      } else if (ws == 1) {
+        epilogue(2, 0, kk[0], qk[0]);
+        epilogue(2, 1, kk[1], qk[1]);
+        epilogue(2, 2, kk[2], qk[2]);
+      } else if (ws == 2) {
+        epilogue(3, 0, kk[0], qk[0]);
+        epilogue(3, 1, kk[1], qk[1]);
+      } else {
+        epilogue(3, 2, kk[0], qk[0]);
+        epilogue(3, 3, kk[1], qk[1]);
       }
     }
     block_sync_lds();
