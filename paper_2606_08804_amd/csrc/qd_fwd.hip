@@ -29,58 +29,70 @@
 
 namespace qd {
 
+// 16 x 16 fp32 blocks of A and M in the preparation kernel: row stride 20
+// floats (16-byte rows for vector stores; the 16 rows of a fragment read fall
+// in distinct banks).  Twelve slots: 0-3 the diagonal blocks (A_ww, then
+// M_ww over it: only the inverse of that block reads A_ww); 4-9 the blocks
+// A_10, A_20, A_21, A_30, A_31, A_32 (then A~ in place); M_10 and M_21 in 10
+// and 11; M_32, M_31, M_20 and M_30 over A~_32, A~_31, A~_30 and A~_20, each
+// written once the solve has read that A~ block for the last time.
+constexpr int PREP_LB = 20;
+constexpr int PREP_SLOTS = 12;
+__device__ inline int prep_slot_a(int i, int j) {
+  if (i == j) return i;
+  return i == 1 ? 4 : i == 2 ? 5 + j : 7 + j;
+}
+__device__ inline int prep_slot_m(int i, int j) {
+  if (i == j) return i;
+  const int ij = 4 * i + j;
+  return ij == 4 ? 10 : ij == 9 ? 11 : ij == 14 ? 9 : ij == 13 ? 8 : ij == 8 ? 7 : 5;
+}
+
 template <typename E, int DK>
 struct alignas(16) PrepSmem {
-  static constexpr int P = Pad<E>::v;
   static constexpr int RK = DK * (int)sizeof(E);
   alignas(16) char Kt[C * RK];      // K and Q of a unit (swizzled direct-load tiles); the
   alignas(16) char Qt[C * RK];      // next unit's land here once the Gram products are done
   alignas(16) float rla[C], rbeta[C], rlam[C];   // raw gate vectors of the next unit
   alignas(16) float b[C], beta[C], lam[C];       // the gate block
-  float A[C][C + 4];          // strictly lower A, consumed (overwritten) by the solve
-  alignas(16) float M[C][C + 4];
-  E Pm[C][C + P];             // P staging; its blocks above the diagonal stay zero
+  alignas(16) float blk[PREP_SLOTS][16][PREP_LB];   // A and M blocks on and below the diagonal
 };
 
-// Four waves per workgroup and two workgroups per CU: each workgroup's
-// barriers pace only itself, so the latency chains of one (UT solve, Gram)
-// run beside the other's.
+// Four waves per workgroup; with bf16 inputs three workgroups share a CU
+// (under 54 KB of LDS and 168 registers each), so that the latency chains of
+// one (UT solve, Gram) run beside the others'.  fp32 operands take more
+// registers: at most two per CU (one when the LDS allows no more).
 constexpr int PREP_THREADS = 256;
-
-// Copies a C x D LDS tile (row stride ld elements) to a dense row-major
-// global block with 16-byte stores by NT threads.
-template <typename E, int D, int NT>
-__device__ inline void store_tile(E* dst, const E* src, int ld, int tid) {
-  constexpr int VEC = 16 / sizeof(E), PR = D / VEC;
-#pragma unroll
-  for (int idx = tid; idx < C * PR; idx += NT) {
-    const int r = idx / PR, c = (idx % PR) * VEC;
-    *(uint4*)(dst + (size_t)r * D + c) = *(const uint4*)(src + (size_t)r * ld + c);
-  }
+template <typename E, int DK>
+constexpr int prep_per_cu() {
+  constexpr int fit = sizeof(PrepSmem<E, DK>) * 3 <= 160 * 1024 ? 3 : sizeof(PrepSmem<E, DK>) * 2 <= 160 * 1024 ? 2 : 1;
+  return sizeof(E) == 2 ? fit : (fit < 2 ? fit : 2);
 }
 
 // Writes, for every unit, the gate block (b, beta, lambda), the intra-chunk
 // output operator P = Gam * M_causal * Q K^T, M = (I + A)^{-1} (when p.wM is
 // set) and T = M diag(beta).  Persistent: each workgroup walks units
 // blockIdx.x, +gridDim.x, ...: the gate block and the Gram products K K^T,
-// Q K^T of the 16 x 16 blocks on and below the diagonal, A and P, P's store, the
-// UT solve (the blocked inverse below, the products of each level spread over
-// the four waves), M and T.  Once the Gram products are done the next unit's
-// K, Q and raw gates go straight into LDS (direct loads in assembly form) and
-// land during the solve; the only memory operations issued after them are
-// this unit's P, M and T stores, which fixes the wait count at the top of
-// the next unit (the compiler's wait for register loads would also cover
-// every store still in flight).
+// Q K^T of the 16 x 16 blocks on and below the diagonal, A and P (P stored
+// straight from registers, its blocks above the diagonal as zeros), the UT
+// solve (the blocked inverse below, the products of each level spread over
+// the four waves), M and T.  The Gram blocks are formed as their transposes
+// (operands swapped), so that a lane holds four consecutive columns of one
+// row: one vector store into A and one into P.  Once the Gram products are
+// done the next unit's K, Q and raw gates go straight into LDS (direct loads
+// in assembly form) and land during the solve; the only memory operations
+// issued after them are this unit's P, M and T stores, which fixes the wait
+// count at the top of the next unit (the compiler's wait for register loads
+// would also cover every store still in flight).
 template <typename E, int DK, int DV>
-__global__ __launch_bounds__(PREP_THREADS) void k_prep(Params p) {
+__global__ __launch_bounds__(PREP_THREADS) __attribute__((amdgpu_waves_per_eu(prep_per_cu<E, DK>(), prep_per_cu<E, DK>()))) void k_prep(Params p) {
   constexpr int NT = PREP_THREADS, NW = NT / 64;
-  constexpr int P = Pad<E>::v;
-  constexpr int LC = C + P, LA = C + 4;
+  constexpr int LB = PREP_LB;
   constexpr int RK = DK * (int)sizeof(E), KS = Mma<E>::KS, NKK = DK / KS;
   constexpr int VEC = 16 / sizeof(E);
   constexpr int MT_ITERS = C * C / VEC / NT;   // M/T store rounds per thread
-  constexpr int PT_ITERS = C * C / VEC / NT;   // P store rounds per thread
-  static_assert(C == 64 && NW == 4 && (C * C / VEC) % NT == 0, "four waves, one row of blocks each");
+  constexpr int P_STORES = 4;                  // P stores per lane: computed blocks plus zero blocks
+  static_assert(C == 64 && NW == 4 && (C * C / VEC) % NT == 0, "four waves");
   typedef typename Mma<E>::frag FR;
   __shared__ PrepSmem<E, DK> sm;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;   // vector wave index: measured faster here than the scalar one
@@ -119,17 +131,16 @@ __global__ __launch_bounds__(PREP_THREADS) void k_prep(Params p) {
 
   // UT solve, M = (I + A)^{-1} blocked 16 x 16: A~_mj = A_mj M_jj,
   // M_ij = -sum_{m=j+1..i} M_im A~_mj
-  auto blkA = [&](int i, int j) { return &sm.A[16 * i][16 * j]; };
-  auto blkM = [&](int i, int j) { return &sm.M[16 * i][16 * j]; };
+  auto blkA = [&](int i, int j) { return &sm.blk[prep_slot_a(i, j)][0][0]; };
+  auto blkM = [&](int i, int j) { return &sm.blk[prep_slot_m(i, j)][0][0]; };
   auto put = [&](float* dst, f4 v, float sc) {
 #pragma unroll
-    for (int j = 0; j < 4; ++j) dst[frow(lane, j) * LA + fcol(lane)] = sc * v[j];
+    for (int j = 0; j < 4; ++j) dst[frow(lane, j) * LB + fcol(lane)] = sc * v[j];
   };
   auto prod = [&](const float* a, const float* m, f4 acc) {
-    return mma_k<float, 16>(kmaj(a, LA), imaj(m, LA), 0, 0, acc, lane);
+    return mma_k<float, 16>(kmaj(a, LB), imaj(m, LB), 0, 0, acc, lane);
   };
 
-  for (int idx = tid; idx < C * LC; idx += NT) (&sm.Pm[0][0])[idx] = fromf<E>(0.f);
   Unit cur;
   find(blockIdx.x, cur);
   issue(cur);
@@ -164,8 +175,9 @@ __global__ __launch_bounds__(PREP_THREADS) void k_prep(Params p) {
       gblk[C + lane] = be;
       gblk[2 * C + lane] = lm;
     }
-    // K K^T and Q K^T of the wave's blocks (row, column); operand fragments
-    // shared within a wave are read once
+    // K K^T and Q K^T of the wave's blocks (row, column), each as its
+    // transpose: K_c K_r^T and K_c Q_r^T; operand fragments shared within a
+    // wave are read once
     f4 kk[3], qk[3];
 #pragma unroll
     for (int n = 0; n < 3; ++n) kk[n] = qk[n] = zero4();
@@ -183,8 +195,8 @@ __global__ __launch_bounds__(PREP_THREADS) void k_prep(Params p) {
         }
 #pragma unroll
         for (int b = 0; b < NBK; ++b) {
-          kk[b] = Mma<E>::mma(kf[br[b]], kf[bc[b]], kk[b]);
-          qk[b] = Mma<E>::mma(qf[br[b]], kf[bc[b]], qk[b]);
+          kk[b] = Mma<E>::mma(kf[bc[b]], kf[br[b]], kk[b]);
+          qk[b] = Mma<E>::mma(kf[bc[b]], qf[br[b]], qk[b]);
         }
       }
     };
@@ -206,51 +218,64 @@ __global__ __launch_bounds__(PREP_THREADS) void k_prep(Params p) {
     issue(nx);                               // lands during the solve
     {
       // A = strictLower(diag(beta) Gam * X K^T), X K^T = K K^T + diag(lambda) Q K^T,
-      // and P (staged in Pm), the wave's blocks
+      // and P, the wave's blocks: lane row 16 m + (l & 15), columns 16 n + 4 (l >> 4)..
+      typedef typename Quad<E>::raw QR;
+      E* Pg = (E*)p.wP + gi * C * C;
+      const int rl = fcol(lane), c4 = frow(lane, 0);
       auto epilogue = [&](int m, int n, const f4& kkb, const f4& qkb) {
-        const int i = 16 * n + fcol(lane);
-        const float bi = sm.b[i];
+        const int r = 16 * m + rl, i0 = 16 * n + c4;
+        const float br = sm.b[r], ber = sm.beta[r], lmr = sm.lam[r];
+        const f4 bi = *(const f4*)&sm.b[i0];
+        f4 a, pv;
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
-          const int r = 16 * m + frow(lane, j);
-          const float gam = (r >= i) ? __expf(sm.b[r] - bi) : 0.f;
-          sm.A[r][i] = (r > i) ? sm.beta[r] * gam * (kkb[j] + sm.lam[r] * qkb[j]) : 0.f;
-          sm.Pm[r][i] = fromf<E>(gam * qkb[j]);
+          const int i = i0 + j;
+          const float gam = (r >= i) ? __expf(br - bi[j]) : 0.f;
+          a[j] = (r > i) ? ber * gam * (kkb[j] + lmr * qkb[j]) : 0.f;
+          pv[j] = gam * qkb[j];
         }
+        *(f4*)(blkA(m, n) + rl * LB + c4) = a;
+        *(QR*)(Pg + (size_t)r * C + i0) = Quad<E>::pack(pv);
       };
+      auto zero_p = [&](int m, int n) { *(QR*)(Pg + (size_t)(16 * m + rl) * C + 16 * n + c4) = Quad<E>::pack(zero4()); };
       if (ws == 0) {
         epilogue(0, 0, kk[0], qk[0]);
         epilogue(1, 0, kk[1], qk[1]);
         epilogue(1, 1, kk[2], qk[2]);
+        zero_p(0, 1);
       } else if (ws == 1) {
         epilogue(2, 0, kk[0], qk[0]);
         epilogue(2, 1, kk[1], qk[1]);
         epilogue(2, 2, kk[2], qk[2]);
+        zero_p(1, 2);
       } else if (ws == 2) {
         epilogue(3, 0, kk[0], qk[0]);
         epilogue(3, 1, kk[1], qk[1]);
+        zero_p(0, 2);
+        zero_p(0, 3);
       } else {
         epilogue(3, 2, kk[0], qk[0]);
         epilogue(3, 3, kk[1], qk[1]);
+        zero_p(1, 3);
+        zero_p(2, 3);
       }
     }
     block_sync_lds();
-    store_tile<E, C, NT>((E*)p.wP + gi * C * C, &sm.Pm[0][0], LC, tid);
     if (lane < 16) {
-      // column j of (I + A_ww)^{-1}; row r of the block is read as four
-      // broadcast 16-byte loads one row ahead of its use
+      // column j of (I + A_ww)^{-1}, written over A_ww; row r of the block is
+      // read as four broadcast 16-byte loads one row ahead of its use
       const int j = lane;
-      const float* blk = blkA(w, w);
+      float* blk = blkA(w, w);
       float m[16];
       f4 cu[4], nxt[4];
 #pragma unroll
-      for (int qq = 0; qq < 4; ++qq) cu[qq] = *(const f4*)(blk + (size_t)1 * LA + 4 * qq);
+      for (int qq = 0; qq < 4; ++qq) cu[qq] = *(const f4*)(blk + (size_t)1 * LB + 4 * qq);
       m[0] = (j == 0) ? 1.f : 0.f;
 #pragma unroll
       for (int r = 1; r < 16; ++r) {
         if (r + 1 < 16) {
 #pragma unroll
-          for (int qq = 0; qq < 4; ++qq) nxt[qq] = *(const f4*)(blk + (size_t)(r + 1) * LA + 4 * qq);
+          for (int qq = 0; qq < 4; ++qq) nxt[qq] = *(const f4*)(blk + (size_t)(r + 1) * LB + 4 * qq);
         }
         float s4[4] = {(r == j) ? 1.f : 0.f, 0.f, 0.f, 0.f};
 #pragma unroll
@@ -259,9 +284,8 @@ __global__ __launch_bounds__(PREP_THREADS) void k_prep(Params p) {
 #pragma unroll
         for (int qq = 0; qq < 4; ++qq) cu[qq] = nxt[qq];
       }
-      float* out = blkM(w, w);
 #pragma unroll
-      for (int r = 0; r < 16; ++r) out[r * LA + j] = m[r];
+      for (int r = 0; r < 16; ++r) blk[r * LB + j] = m[r];
     }
     block_sync_lds();
     {
@@ -274,6 +298,7 @@ __global__ __launch_bounds__(PREP_THREADS) void k_prep(Params p) {
     }
     block_sync_lds();
     // level 1: M_10, M_21, M_32 and the diagonal-block parts of M_20, M_31, M_30
+    // (M_32 goes over A~_32, which only this product reads)
     f4 part = zero4();
     if (w < 3) {
       const int bb = w + 1;                  // M_b,b-1 = -M_bb A~_b,b-1
@@ -284,6 +309,7 @@ __global__ __launch_bounds__(PREP_THREADS) void k_prep(Params p) {
     }
     block_sync_lds();
     // level 2: M_20 += M_21 A~_10, M_31 += M_32 A~_21, M_30 += M_32 A~_20
+    // (M_20 over A~_30, M_31 over A~_31: both last read in level 1)
     if (w == 0) {
       part = prod(blkM(2, 1), blkA(1, 0), part);
       put(blkM(2, 0), part, -1.f);
@@ -294,7 +320,7 @@ __global__ __launch_bounds__(PREP_THREADS) void k_prep(Params p) {
       part = prod(blkM(3, 2), blkA(2, 0), part);
     }
     block_sync_lds();
-    // level 3: M_30 += M_31 A~_10
+    // level 3: M_30 += M_31 A~_10 (over A~_20, last read in level 2)
     if (w == 2) {
       part = prod(blkM(3, 1), blkA(1, 0), part);
       put(blkM(3, 0), part, -1.f);
@@ -311,13 +337,14 @@ __global__ __launch_bounds__(PREP_THREADS) void k_prep(Params p) {
         const int idx = tid + it * NT;
         const int r = idx / (C / VEC), i0 = (idx % (C / VEC)) * VEC;
         const bool upper = (i0 >> 4) > (r >> 4);
+        const float* src = blkM(r >> 4, upper ? r >> 4 : i0 >> 4) + (r & 15) * LB + (i0 & 15);
         uint4 mr, tr;
         E* me = (E*)&mr;
         E* te = (E*)&tr;
         float mv[VEC], bv[VEC];
 #pragma unroll
         for (int j = 0; j < VEC; j += 4) {
-          *(f4*)&mv[j] = *(const f4*)&sm.M[r][i0 + j];
+          *(f4*)&mv[j] = *(const f4*)(src + j);
           *(f4*)&bv[j] = *(const f4*)&sm.beta[i0 + j];
         }
 #pragma unroll
@@ -331,8 +358,8 @@ __global__ __launch_bounds__(PREP_THREADS) void k_prep(Params p) {
       }
       // the next unit's loads went out before P's and these stores (in-order
       // counter)
-      if (keep_m) wait_vm<PT_ITERS + 2 * MT_ITERS>();
-      else wait_vm<PT_ITERS + MT_ITERS>();
+      if (keep_m) wait_vm<P_STORES + 2 * MT_ITERS>();
+      else wait_vm<P_STORES + MT_ITERS>();
     }
     cur = nx;
   }
@@ -792,8 +819,8 @@ template <typename E, int DK, int DV>
 static hipError_t launch_fwd_t(const Params& p, int in_bwd, int with_scan, hipStream_t st) {
   if (p.n_slots > 0) {
     const int units = p.n_slots * p.H;
-    // two persistent four-wave workgroups per CU
-    dim3 gp(min(units, 2 * device_cu_count()));
+    // persistent four-wave workgroups, as many per CU as fit
+    dim3 gp(min(units, prep_per_cu<E, DK>() * device_cu_count()));
     const int stage = in_bwd ? ST_PREP_BWD : ST_PREP_FWD;
     prof_mark(stage, 0, st);
     hipLaunchKernelGGL((k_prep<E, DK, DV>), gp, dim3(PREP_THREADS), 0, st, p);
