@@ -66,12 +66,15 @@
  *    states  dtype [U, Dv, Dk]: the entry state S of the chunk, rounded to
  *            the activation dtype (the backward's products take it as an MFMA
  *            operand of that type);
- *    D       dtype [U, C, Dv]: the chunk's "new values" D = U - W S^T
- *            (App. D, WY form), rows >= the chunk's length zero;
+ *    D       dtype [U, Dv/32, C, 32]: the chunk's "new values" D = U - W S^T
+ *            (App. D, WY form) in tiles of 32 value columns, each tile a
+ *            contiguous C x 32 row-major block; rows >= the chunk's length
+ *            zero;
  *    gates   float32 [U, 3, C]: chunk-local prefix sums b of log alpha, then
  *            beta and lambda (zero past the chunk's length);
  *    P       dtype [U, C, C]: the intra-chunk output operator
- *            Gam * M * (Q K^T) (Sec. 3.3 chunkwise form);
+ *            Gam * M * (Q K^T) (Sec. 3.3 chunkwise form), rows >= the
+ *            chunk's length zero;
  *    M       dtype [U, C, C]: (I + A)^{-1} of the UT transform (App. D.2),
  *            row-major, strictly-upper 16 x 16 blocks zero.
  *  The backward reads all of it and so needs no preparation pass of its own.

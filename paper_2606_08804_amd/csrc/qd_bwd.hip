@@ -152,7 +152,7 @@ __global__ __launch_bounds__(NCW * 64 + 256) void k_scan_bwd(Params p) {
     dma_rows<R::RK, C, 4, true>(sm.ringX[it % NA] + R::XQ, Qg, (size_t)H * R::RK, len,
                                 Qg + (size_t)(len - 1) * H * R::RK, 0, prod, lane);
   };
-  // producers: K, dO (rows past the chunk from D, zero there) and the gates
+  // producers: K, dO (rows past the chunk from P, zero there) and the gates
   auto issueK = [&](int it) {
     size_t gi, arow;
     int len;
@@ -160,10 +160,11 @@ __global__ __launch_bounds__(NCW * 64 + 256) void k_scan_bwd(Params p) {
     char* r = sm.ringX[it % NA];
     const char* Kg = (const char*)((const E*)p.k + arow * DK);
     const char* Og = (const char*)((const E*)p.dO + arow * DV + v0);
-    const char* Dg = (const char*)((const E*)p.savedD + gi * C * DV + v0);
+    const char* Pz = (const char*)((const E*)p.wP + gi * C * C);
+    static_assert(R::RO <= R::RC, "a zero row of P covers a row of dO");
     dma_rows<R::RK, C, 4, true>(r + R::XK, Kg, (size_t)H * R::RK, len, Kg + (size_t)(len - 1) * H * R::RK, 0,
                                 prod, lane);
-    dma_rows<R::RO, C, 4, true>(r + R::XO, Og, (size_t)H * DV * sizeof(E), len, Dg, DV * sizeof(E), prod, lane);
+    dma_rows<R::RO, C, 4, true>(r + R::XO, Og, (size_t)H * DV * sizeof(E), len, Pz, R::RC, prod, lane);
     if (prod < 3) dma4_asm(p.wb + gi * 3 * C + prod * C + lane, r + R::XG + prod * C * 4);
   };
   auto issueP = [&](int it) {
@@ -469,7 +470,7 @@ __global__ __launch_bounds__(INTRA_THREADS) __attribute__((amdgpu_waves_per_eu(2
   for (int i = 0; i < 4; ++i) aP[i] = aT[i] = zero4();
   const char* Sg = (const char*)((const E*)p.saved + gi * DK * DV);
   const char* dSg = (const char*)((const E*)p.w_dSo + gi * DK * DV);
-  const char* Dg = (const char*)((const E*)p.savedD + gi * C * DV);
+  const char* Dg = (const char*)((const E*)p.savedD + gi * C * DV);   // 32-column tiles, C x 32 each
   const char* dOg = (const char*)((const E*)p.dO + arow * DV);
   const char* Vg = (const char*)((const E*)p.v + arow * DV);
   // the gate block (b, beta, lambda; waves 0-2 one vector each, straight
@@ -484,15 +485,17 @@ __global__ __launch_bounds__(INTRA_THREADS) __attribute__((amdgpu_waves_per_eu(2
     for (int ks = 0; ks < NKK; ++ks) kf[ks] = *(const FR*)(kr + ks * KS);
   }
   // rows of V and dO past the chunk come from D, whose rows there are zero
+  static_assert(BV == 32, "one saved-D tile per value tile");
   auto issue = [&](int vt) {
     const int ln = lane;
     char* t = sm.ring[vt & 1];
     const size_t vb = (size_t)vt * BV;
+    const char* Dt = Dg + vb * C * ES;   // this value tile's C x 32 block of D
     dma_rows<RK, BV, NWAVES, true>(t + TA::S, Sg + vb * RK, RK, BV, Sg, 0, w, ln);
     dma_rows<RK, BV, NWAVES, true>(t + TA::DS, dSg + vb * RK, RK, BV, dSg, 0, w, ln);
-    dma_rows<TA::RE, C, NWAVES, true>(t + TA::D, Dg + vb * ES, DV * ES, C, Dg, 0, w, ln);
-    dma_rows<TA::RE, C, NWAVES, true>(t + TA::V, Vg + vb * ES, (size_t)H * DV * ES, len, Dg + vb * ES, DV * ES, w, ln);
-    dma_rows<TA::RE, C, NWAVES, true>(t + TA::DO, dOg + vb * ES, (size_t)H * DV * ES, len, Dg + vb * ES, DV * ES, w, ln);
+    dma_rows<TA::RE, C, NWAVES, true>(t + TA::D, Dt, TA::RE, C, Dt, 0, w, ln);
+    dma_rows<TA::RE, C, NWAVES, true>(t + TA::V, Vg + vb * ES, (size_t)H * DV * ES, len, Dt, TA::RE, w, ln);
+    dma_rows<TA::RE, C, NWAVES, true>(t + TA::DO, dOg + vb * ES, (size_t)H * DV * ES, len, Dt, TA::RE, w, ln);
   };
   // this wave's rows of the tile's dD, as their transpose (value rows, chunk
   // columns 16w..): dS' Kbar^T + dO^T P, P causal; rows past the chunk carry

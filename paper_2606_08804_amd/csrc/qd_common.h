@@ -335,7 +335,7 @@ struct Params {
   void* o;
   float* Sfin;
   void* saved;           // saved context: entry states S [slot][H][Dv][Dk] (dtype)
-  void* savedD;          // saved context: D [slot][H][C][Dv] (dtype)
+  void* savedD;          // saved context: D [slot][H][Dv/32][C][32] (dtype), 32-column tiles
   // chunk factors from the preparation, per slot and head (in the saved
   // context when one is kept, else in the workspace)
   float* wb;             // [slot][H][3][C] gate block: chunk-local prefix sums b of

@@ -219,6 +219,9 @@ __global__ __launch_bounds__(PREP_THREADS) __attribute__((amdgpu_waves_per_eu(pr
     {
       // A = strictLower(diag(beta) Gam * X K^T), X K^T = K K^T + diag(lambda) Q K^T,
       // and P, the wave's blocks: lane row 16 m + (l & 15), columns 16 n + 4 (l >> 4)..
+      // Rows past the chunk's end are zero in both (in A through beta): no
+      // output reads those rows of P, and the backward scan takes them as
+      // the zero rows of its output-gradient tiles.
       typedef typename Quad<E>::raw QR;
       E* Pg = (E*)p.wP + gi * C * C;
       const int rl = fcol(lane), c4 = frow(lane, 0);
@@ -230,7 +233,7 @@ __global__ __launch_bounds__(PREP_THREADS) __attribute__((amdgpu_waves_per_eu(pr
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
           const int i = i0 + j;
-          const float gam = (r >= i) ? __expf(br - bi[j]) : 0.f;
+          const float gam = (r >= i && r < x.len) ? __expf(br - bi[j]) : 0.f;
           a[j] = (r > i) ? ber * gam * (kkb[j] + lmr * qkb[j]) : 0.f;
           pv[j] = gam * qkb[j];
         }
@@ -759,12 +762,14 @@ __global__ __launch_bounds__(NCW * 64 + 256) void k_scan_fwd(Params p) {
       }
       stage_S();
       if (saved) {
-        // D rows of this tile into the saved context (rows past the chunk are zero)
-        constexpr int VEC = 16 / sizeof(E), PR = BV / VEC;
-        E* dbase = (E*)p.savedD + gi * C * DV + v0;
+        // D rows of this tile into the saved context (rows past the chunk are
+        // zero), whose 32-column tiles are contiguous C x 32 blocks: each
+        // workgroup writes whole blocks
+        constexpr int VEC = 16 / sizeof(E), PR = BV / VEC, PT = 32 / VEC;
+        E* dbase = (E*)p.savedD + gi * C * DV + (size_t)v0 * C;
         for (int idx = tid; idx < C * PR; idx += NCT) {
-          const int r = idx / PR, cc = (idx % PR) * VEC;
-          *(uint4*)(dbase + (size_t)r * DV + cc) = *(const uint4*)&sm.D[r][cc];
+          const int sub = idx / (C * PT), r = (idx / PT) % C, cc = (idx % PT) * VEC;
+          *(uint4*)(dbase + (size_t)sub * C * 32 + (size_t)r * 32 + cc) = *(const uint4*)&sm.D[r][sub * 32 + cc];
         }
       }
     } else if (c + 1 < nch) {
