@@ -137,7 +137,7 @@ def handoff_bytes_per_unit(stage, Dk, Dv, e, saved=True):
     act_v = C * Dv * e
     gates = C * 4
     state = Dv * Dk * 4
-    cc_e = C * C * e
+    cc_e = 10 * 256 * e          # C x C operators stored as their ten lower 16 x 16 blocks
     if stage in ("prep_fwd", "prep_bwd"):
         # q, k, 3 gates -> gate block, P, T (and M when the context is kept)
         return 2 * act_qk + 3 * gates + 3 * gates + (3 if saved else 2) * cc_e

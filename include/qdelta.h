@@ -61,8 +61,8 @@
  * Saved context (written by the forward, read by the backward)
  * --------------------------------------------------------------
  *  A caller-owned device buffer of qdelta_saved_bytes() bytes (16-byte
- *  aligned) with five regions, one after the other, each indexed by unit
- *  u = slot * H + h (U = n_slots * H units):
+ *  aligned) with six regions, one after the other, all but the fourth
+ *  indexed by unit u = slot * H + h (U = n_slots * H units):
  *    states  dtype [U, Dv, Dk]: the entry state S of the chunk, rounded to
  *            the activation dtype (the backward's products take it as an MFMA
  *            operand of that type);
@@ -72,11 +72,14 @@
  *            zero;
  *    gates   float32 [U, 3, C]: chunk-local prefix sums b of log alpha, then
  *            beta and lambda (zero past the chunk's length);
- *    P       dtype [U, C, C]: the intra-chunk output operator
- *            Gam * M * (Q K^T) (Sec. 3.3 chunkwise form), rows >= the
+ *    zero    1024 bytes of zeros (rows of zeros for the backward's loads);
+ *    P       dtype [U, 10, 16, 16]: the intra-chunk output operator
+ *            Gam * M * (Q K^T) (Sec. 3.3 chunkwise form), lower triangular
+ *            in 16 x 16 blocks and stored as those ten blocks: block (r, c),
+ *            c <= r, at index r (r + 1) / 2 + c, each row-major; rows >= the
  *            chunk's length zero;
- *    M       dtype [U, C, C]: (I + A)^{-1} of the UT transform (App. D.2),
- *            row-major, strictly-upper 16 x 16 blocks zero.
+ *    M       dtype [U, 10, 16, 16]: (I + A)^{-1} of the UT transform
+ *            (App. D.2), its ten blocks on and below the diagonal, as P.
  *  The backward reads all of it and so needs no preparation pass of its own.
  *  n_slots from qdelta_saved_state_slots.  Chunk c (0-based) of sequence n
  *  occupies slot  n*ceil(T/chunk) + c  (dense) or  floor(cu[n]/chunk) + n + c
@@ -183,8 +186,8 @@ int32_t qdelta_suggest_segments(int32_t B, int32_t T, int32_t H, int32_t Dk, int
  * held from the first call on that device until the process ends.
  *  - Sizes whose forward workspace (qdelta_chunk_workspace_bytes with
  *    is_bwd == 0) exceeds QDELTA_NOALLOC_SCRATCH_BYTES return
- *    QDELTA_ENOWORKSPACE before any device call (about 3900 chunk-head units
- *    at bf16, e.g. B=8 T=2048 H=8 fits; about 2000 at fp32).
+ *    QDELTA_ENOWORKSPACE before any device call (about 6100 chunk-head units
+ *    at bf16, e.g. B=4 T=4096 H=16 fits; about 3100 at fp32).
  *  - Calls no allocating routine.  The first call on a device looks up the
  *    scratch array's device address (QDELTA_EHIP if that fails).
  *  - Every call on a device shares that device's scratch array: calls that

@@ -17,26 +17,28 @@ using qd::C;
 constexpr int kVersion = 10000;  // 1.0.0
 
 struct Layout {
-  size_t wb = 0, wT = 0, wP = 0;   // forward: chunk factors (T always, gates and P when no saved context is kept)
+  size_t wb = 0, wT = 0, wP = 0, wZ = 0;   // forward: chunk factors (T always; gates, P and the zero block when no saved context is kept)
   size_t dSo = 0, ctx = 0;                 // backward: scan output dS', room to recompute the context
   size_t dlam = 0;                         // backward: per-unit partials of a constant lambda's gradient
   size_t total = 0;
 };
 
-// Saved context, per unit (slot, head), region after region: S [Dv][Dk],
-// D [C][Dv], gate block fp32 [3][C] (b, beta, lambda), P [C][C], M [C][C]
-// (all but the gates in the activation dtype).
+// Saved context, region after region: per unit (slot, head) S [Dv][Dk] and
+// D [Dv/32][C][32]; per unit the gate block fp32 [3][C] (b, beta, lambda);
+// one 1 KB zero block; per unit P and M, each as the ten 16 x 16 blocks on
+// and below the diagonal (all but the gates in the activation dtype).
 struct Ctx {
-  size_t states, D, b, P, M, total;
+  size_t states, D, b, Z, P, M, total;
 };
 Ctx ctx_layout(size_t units, int Dk, int Dv, int esz) {
   Ctx c;
   c.states = 0;
   c.D = c.states + units * (size_t)Dk * Dv * esz;
   c.b = c.D + units * (size_t)C * Dv * esz;
-  c.P = c.b + units * (size_t)3 * C * 4;
-  c.M = c.P + units * (size_t)C * C * esz;
-  c.total = c.M + units * (size_t)C * C * esz;
+  c.Z = c.b + units * (size_t)3 * C * 4;
+  c.P = c.Z + (units > 0 ? 1024 : 0);
+  c.M = c.P + units * (size_t)qd::LBT_ELEMS * esz;
+  c.total = c.M + units * (size_t)qd::LBT_ELEMS * esz;
   return c;
 }
 
@@ -48,14 +50,15 @@ Layout make_layout(size_t units, int Dk, int Dv, int esz, bool bwd) {
     off += (bytes + 255) & ~size_t(255);
     return at;
   };
-  L.wT = take(units * C * C * esz);
+  L.wT = take(units * qd::LBT_ELEMS * esz);
   if (bwd) {
     L.dSo = take(units * (size_t)Dv * Dk * esz);
     L.ctx = take(ctx_layout(units, Dk, Dv, esz).total);
     L.dlam = take(units * sizeof(float));
   } else {
     L.wb = take(units * 3 * C * 4);
-    L.wP = take(units * C * C * esz);
+    L.wZ = take(units > 0 ? 1024 : 0);
+    L.wP = take(units * qd::LBT_ELEMS * esz);
   }
   L.total = off;
   return L;
@@ -92,6 +95,7 @@ void bind_ctx(qd::Params& p, char* base, size_t units, int Dk, int Dv, int esz) 
   p.saved = base + c.states;
   p.savedD = base + c.D;
   p.wb = reinterpret_cast<float*>(base + c.b);
+  p.wZ = base + c.Z;
   p.wP = base + c.P;
   p.wM = base + c.M;
 }
@@ -188,6 +192,7 @@ int fwd_impl(bool varlen, int32_t B, int32_t T, int32_t N, const int32_t* cu, in
     bind_ctx(p, static_cast<char*>(saved), units, Dk, Dv, esz);
   } else {
     p.wb = reinterpret_cast<float*>(w + L.wb);
+    p.wZ = w + L.wZ;
     p.wP = w + L.wP;
     p.wM = nullptr;    // M feeds only the backward
   }
@@ -495,6 +500,7 @@ int qdelta_chunk_fwd_segmented(int32_t B, int32_t T, int32_t H, int32_t Dk, int3
     bind_ctx(p, static_cast<char*>(saved), units, Dk, Dv, esz);
   } else {
     p.wb = reinterpret_cast<float*>(w + S.fwd.wb);
+    p.wZ = w + S.fwd.wZ;
     p.wP = w + S.fwd.wP;
     p.wM = nullptr;
   }

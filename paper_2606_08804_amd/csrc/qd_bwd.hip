@@ -152,7 +152,8 @@ __global__ __launch_bounds__(NCW * 64 + 256) void k_scan_bwd(Params p) {
     dma_rows<R::RK, C, 4, true>(sm.ringX[it % NA] + R::XQ, Qg, (size_t)H * R::RK, len,
                                 Qg + (size_t)(len - 1) * H * R::RK, 0, prod, lane);
   };
-  // producers: K, dO (rows past the chunk from P, zero there) and the gates
+  // producers: K, dO (rows past the chunk from the preparation's zero block)
+  // and the gates
   auto issueK = [&](int it) {
     size_t gi, arow;
     int len;
@@ -160,26 +161,23 @@ __global__ __launch_bounds__(NCW * 64 + 256) void k_scan_bwd(Params p) {
     char* r = sm.ringX[it % NA];
     const char* Kg = (const char*)((const E*)p.k + arow * DK);
     const char* Og = (const char*)((const E*)p.dO + arow * DV + v0);
-    const char* Pz = (const char*)((const E*)p.wP + gi * C * C);
-    static_assert(R::RO <= R::RC, "a zero row of P covers a row of dO");
+    static_assert(R::RO <= 1024, "a row of dO within the zero block");
     dma_rows<R::RK, C, 4, true>(r + R::XK, Kg, (size_t)H * R::RK, len, Kg + (size_t)(len - 1) * H * R::RK, 0,
                                 prod, lane);
-    dma_rows<R::RO, C, 4, true>(r + R::XO, Og, (size_t)H * DV * sizeof(E), len, Pz, R::RC, prod, lane);
+    dma_rows<R::RO, C, 4, true>(r + R::XO, Og, (size_t)H * DV * sizeof(E), len, (const char*)p.wZ, 0, prod, lane);
     if (prod < 3) dma4_asm(p.wb + gi * 3 * C + prod * C + lane, r + R::XG + prod * C * 4);
   };
   auto issueP = [&](int it) {
     size_t gi, arow;
     int len;
     chunk_at(nch - 1 - it, gi, arow, len);
-    const char* Pg = (const char*)((const E*)p.wP + gi * C * C);
-    dma_rows<R::RC, C, 4, true>(sm.ringP[it % R::NP], Pg, R::RC, C, Pg, 0, prod, lane);
+    dma_lbt<E, 4>(sm.ringP[it % R::NP], (const char*)((const E*)p.wP + gi * LBT_ELEMS), prod, lane);
   };
   auto issueM = [&](int it) {
     size_t gi, arow;
     int len;
     chunk_at(nch - 1 - it, gi, arow, len);
-    const char* Mg = (const char*)((const E*)p.wM + gi * C * C);
-    dma_rows<R::RC, C, 4, true>(sm.ringM, Mg, R::RC, C, Mg, 0, prod, lane);
+    dma_lbt<E, 4>(sm.ringM, (const char*)((const E*)p.wM + gi * LBT_ELEMS), prod, lane);
   };
 
   f4 acc[KPW][NBS];
@@ -201,6 +199,12 @@ __global__ __launch_bounds__(NCW * 64 + 256) void k_scan_bwd(Params p) {
         *(QR*)&sm.dS[(ns0 + j) * 16 + fcol(lane)][(kb0 + i) * 16 + frow(lane, 0)] = Quad<E>::pack(acc[i][j]);
   };
 
+  // P and M arrive packed: the chunks above their diagonal blocks are zeroed
+  // once here and never loaded (the first barrier of the loop orders these
+  // stores before any read)
+  zero_upper_chunks<E>(sm.ringM, tid, NCT + 256);
+#pragma unroll
+  for (int i = 0; i < R::NP; ++i) zero_upper_chunks<E>(sm.ringP[i], tid, NCT + 256);
   if (nch > 0) {
     if (producer) {
       for (int it = 0; it < NA - 1 && it < nch; ++it) {
@@ -563,10 +567,13 @@ __global__ __launch_bounds__(INTRA_THREADS) __attribute__((amdgpu_waves_per_eu(2
   // row and are zeroed afterwards) beside the K rows the waves write from
   // their registers, and once the last tile's dD is formed, M over P.
   constexpr int ML = C * RC / 1024 / NWAVES;
+  // P and M arrive packed: the chunks above their diagonal blocks are zeroed
+  // once here and never loaded (ordered before any read by the barrier after
+  // the first tile)
+  zero_upper_chunks<E>(sm.Mm, tid, INTRA_THREADS);
   issue(0);
   {
-    const char* Pg = (const char*)((const E*)p.wP + gi * C * C);
-    dma_rows<RC, C, NWAVES, true>(sm.Mm, Pg, RC, C, Pg, 0, w, lane);
+    dma_lbt<E, NWAVES>(sm.Mm, (const char*)((const E*)p.wP + gi * LBT_ELEMS), w, lane);
   }
   issue(1);
   static_assert(NVT % 2 == 0, "the last tile uses slot 1");
@@ -614,8 +621,7 @@ __global__ __launch_bounds__(INTRA_THREADS) __attribute__((amdgpu_waves_per_eu(2
     if (vt == NVT - 1) {
       // every wave is past its last read of P: M goes over it
       block_sync_lds();
-      const char* Mg = (const char*)((const E*)p.wM + gi * C * C);
-      dma_rows<RC, C, NWAVES, true>(sm.Mm, Mg, RC, C, Mg, 0, w, lane);
+      dma_lbt<E, NWAVES>(sm.Mm, (const char*)((const E*)p.wM + gi * LBT_ELEMS), w, lane);
     }
     products(t, la, WITHOUT_DD | WITH_DD);
   }

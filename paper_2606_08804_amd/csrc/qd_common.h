@@ -168,6 +168,29 @@ __device__ inline void wait_vm() {
   asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
 }
 
+// wait_vm with a count known only at run time (uniform across the wave, 0-15).
+__device__ inline void wait_vm_n(int n) {
+  switch (n) {
+    case 0: wait_vm<0>(); break;
+    case 1: wait_vm<1>(); break;
+    case 2: wait_vm<2>(); break;
+    case 3: wait_vm<3>(); break;
+    case 4: wait_vm<4>(); break;
+    case 5: wait_vm<5>(); break;
+    case 6: wait_vm<6>(); break;
+    case 7: wait_vm<7>(); break;
+    case 8: wait_vm<8>(); break;
+    case 9: wait_vm<9>(); break;
+    case 10: wait_vm<10>(); break;
+    case 11: wait_vm<11>(); break;
+    case 12: wait_vm<12>(); break;
+    case 13: wait_vm<13>(); break;
+    case 14: wait_vm<14>(); break;
+    case 15: wait_vm<15>(); break;
+    default: wait_vm<0>(); break;
+  }
+}
+
 // LDS tiles written by direct loads are rows of RB bytes (64, 128 or 256) made of
 // 16-byte chunks; chunk c of row r sits at slot c ^ swz(r).  swz is a linear
 // (XOR) map of the low four row bits, chosen by measuring on gfx950 every such
@@ -232,6 +255,49 @@ __device__ inline void dma_rows(char* dst, const char* src, size_t stride, int v
     else
       __builtin_amdgcn_global_load_lds((const void*)g, (__attribute__((address_space(3))) void*)(dst + i * 1024),
                                        16, 0, 0);
+  }
+}
+
+// C x C operators whose 16 x 16 blocks above the diagonal are zero (P, M, T)
+// are stored packed: the ten blocks on and below the diagonal, block (r, c)
+// (c <= r) at index r (r + 1) / 2 + c, each row-major.  Stores then cover
+// whole blocks (whole cache lines) and 37.5% fewer bytes move.
+constexpr int LBT_ELEMS = 10 * 256;
+__device__ inline int lbt_block(int br, int bc) { return br * (br + 1) / 2 + bc; }
+
+// Direct load of a packed C x C operand into the swizzled row-major LDS tile
+// at `dst` (rows of C elements): the same instructions as a full tile, with
+// the lanes of chunks above the diagonal masked off, so those LDS bytes keep
+// what zero_upper_chunks wrote there once.  Every instruction covers whole
+// rows, whose first block is on or below the diagonal, so each has active
+// lanes and the outstanding-load count is that of a full tile.
+template <typename E, int NW>
+__device__ inline void dma_lbt(char* dst, const char* src, int w, int lane) {
+  constexpr int RB = C * (int)sizeof(E), NCH = RB / 16, RPI = 1024 / RB, NI = C / RPI;
+  constexpr int BCH = 16 * (int)sizeof(E) / 16;   // 16-byte chunks per block row
+  static_assert(NI % NW == 0, "instructions split evenly over the waves");
+#pragma unroll
+  for (int j = 0; j < NI / NW; ++j) {
+    int l = lane;                     // formed again per instruction: no address kept live across them
+    asm volatile("" : "+v"(l));
+    const int i = j * NW + w;
+    const int row = i * RPI + l / NCH;
+    const int c = (l % NCH) ^ tile_swz<RB>(row);
+    const int br = row >> 4, bc = c / BCH;
+    if (bc <= br)
+      dma16_asm(src + ((size_t)lbt_block(br, bc) * 256 + (row & 15) * 16) * sizeof(E) + (c % BCH) * 16,
+                dst + i * 1024);
+  }
+}
+
+// Zeroes the chunks above the diagonal blocks of a swizzled C x C LDS tile
+// (the ones dma_lbt never writes), nthreads threads from thread t.
+template <typename E>
+__device__ inline void zero_upper_chunks(char* dst, int t, int nthreads) {
+  constexpr int RB = C * (int)sizeof(E), NCH = RB / 16, BCH = 16 * (int)sizeof(E) / 16;
+  for (int idx = t; idx < C * NCH; idx += nthreads) {
+    const int row = idx / NCH, c = idx % NCH;
+    if (c / BCH > (row >> 4)) *(uint4*)(dst + row * RB + ((c ^ tile_swz<RB>(row)) << 4)) = make_uint4(0, 0, 0, 0);
   }
 }
 
@@ -340,9 +406,10 @@ struct Params {
   // context when one is kept, else in the workspace)
   float* wb;             // [slot][H][3][C] gate block: chunk-local prefix sums b of
                          // log alpha, beta, lambda (beta, lambda zero past the chunk)
-  void* wP;              // [slot][H][C][C]   P = Gam * M_causal * Q K^T
-  void* wM;              // [slot][H][C][C]   M = (I + A)^{-1}
-  void* wT;              // [slot][H][C][C]   T = M diag(beta) (workspace only)
+  void* wP;              // [slot][H][LBT_ELEMS] P = Gam * M_causal * Q K^T (packed lower blocks)
+  void* wM;              // [slot][H][LBT_ELEMS] M = (I + A)^{-1}           (packed lower blocks)
+  void* wT;              // [slot][H][LBT_ELEMS] T = M diag(beta) (workspace only; packed)
+  void* wZ;              // 1 KB of zeros, written by the preparation kernel: zero rows for direct loads
   // backward
   const void* dO;
   const float* dSfin;

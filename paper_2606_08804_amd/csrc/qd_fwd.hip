@@ -90,9 +90,10 @@ __global__ __launch_bounds__(PREP_THREADS) __attribute__((amdgpu_waves_per_eu(pr
   constexpr int LB = PREP_LB;
   constexpr int RK = DK * (int)sizeof(E), KS = Mma<E>::KS, NKK = DK / KS;
   constexpr int VEC = 16 / sizeof(E);
-  constexpr int MT_ITERS = C * C / VEC / NT;   // M/T store rounds per thread
-  constexpr int P_STORES = 4;                  // P stores per lane: computed blocks plus zero blocks
-  static_assert(C == 64 && NW == 4 && (C * C / VEC) % NT == 0, "four waves");
+  constexpr int BCH = 16 / VEC;                 // M/T stores per block row
+  constexpr int MT_STORES = 10 * 16 * BCH;      // M/T stores per matrix (packed)
+  constexpr int MT_ROUNDS = (MT_STORES + NT - 1) / NT;
+  static_assert(C == 64 && NW == 4 && MT_STORES % 64 == 0, "four waves; whole-wave store rounds");
   typedef typename Mma<E>::frag FR;
   __shared__ PrepSmem<E, DK> sm;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;   // vector wave index: measured faster here than the scalar one
@@ -141,6 +142,9 @@ __global__ __launch_bounds__(PREP_THREADS) __attribute__((amdgpu_waves_per_eu(pr
     return mma_k<float, 16>(kmaj(a, LB), imaj(m, LB), 0, 0, acc, lane);
   };
 
+  // the zero block that the kernels reading this launch's outputs take as
+  // zero rows (covered by the wait below)
+  if (blockIdx.x == 0 && w == 0) *(uint4*)((char*)p.wZ + lane * 16) = make_uint4(0, 0, 0, 0);
   Unit cur;
   find(blockIdx.x, cur);
   issue(cur);
@@ -219,11 +223,11 @@ __global__ __launch_bounds__(PREP_THREADS) __attribute__((amdgpu_waves_per_eu(pr
     {
       // A = strictLower(diag(beta) Gam * X K^T), X K^T = K K^T + diag(lambda) Q K^T,
       // and P, the wave's blocks: lane row 16 m + (l & 15), columns 16 n + 4 (l >> 4)..
-      // Rows past the chunk's end are zero in both (in A through beta): no
-      // output reads those rows of P, and the backward scan takes them as
-      // the zero rows of its output-gradient tiles.
+      // Rows past the chunk's end are zero in both (in A through beta; no
+      // output reads those rows of P).  P is stored packed, block (m, n) as
+      // one contiguous 16 x 16 block written by the wave's 64 lanes.
       typedef typename Quad<E>::raw QR;
-      E* Pg = (E*)p.wP + gi * C * C;
+      E* Pg = (E*)p.wP + gi * LBT_ELEMS;
       const int rl = fcol(lane), c4 = frow(lane, 0);
       auto epilogue = [&](int m, int n, const f4& kkb, const f4& qkb) {
         const int r = 16 * m + rl, i0 = 16 * n + c4;
@@ -238,29 +242,22 @@ __global__ __launch_bounds__(PREP_THREADS) __attribute__((amdgpu_waves_per_eu(pr
           pv[j] = gam * qkb[j];
         }
         *(f4*)(blkA(m, n) + rl * LB + c4) = a;
-        *(QR*)(Pg + (size_t)r * C + i0) = Quad<E>::pack(pv);
+        *(QR*)(Pg + (size_t)lbt_block(m, n) * 256 + rl * 16 + c4) = Quad<E>::pack(pv);
       };
-      auto zero_p = [&](int m, int n) { *(QR*)(Pg + (size_t)(16 * m + rl) * C + 16 * n + c4) = Quad<E>::pack(zero4()); };
       if (ws == 0) {
         epilogue(0, 0, kk[0], qk[0]);
         epilogue(1, 0, kk[1], qk[1]);
         epilogue(1, 1, kk[2], qk[2]);
-        zero_p(0, 1);
       } else if (ws == 1) {
         epilogue(2, 0, kk[0], qk[0]);
         epilogue(2, 1, kk[1], qk[1]);
         epilogue(2, 2, kk[2], qk[2]);
-        zero_p(1, 2);
       } else if (ws == 2) {
         epilogue(3, 0, kk[0], qk[0]);
         epilogue(3, 1, kk[1], qk[1]);
-        zero_p(0, 2);
-        zero_p(0, 3);
       } else {
         epilogue(3, 2, kk[0], qk[0]);
         epilogue(3, 3, kk[1], qk[1]);
-        zero_p(1, 3);
-        zero_p(2, 3);
       }
     }
     block_sync_lds();
@@ -331,16 +328,19 @@ __global__ __launch_bounds__(PREP_THREADS) __attribute__((amdgpu_waves_per_eu(pr
     block_sync_lds();
     {
       // M (only the backward reads it, so only when the context is kept) and
-      // T = M diag(beta), strictly-upper 16 x 16 blocks zero; a thread takes
-      // VEC consecutive columns of one row
-      E* wM = keep_m ? (E*)p.wM + gi * C * C : nullptr;
-      E* wT = (E*)p.wT + gi * C * C;
+      // T = M diag(beta), packed like P; a thread takes VEC consecutive
+      // columns of one block row.  The stores per matrix are a multiple of
+      // 64, so whole waves run a round or skip it.
+      E* wM = keep_m ? (E*)p.wM + gi * LBT_ELEMS : nullptr;
+      E* wT = (E*)p.wT + gi * LBT_ELEMS;
 #pragma unroll
-      for (int it = 0; it < MT_ITERS; ++it) {
+      for (int it = 0; it < MT_ROUNDS; ++it) {
+        if (it * NT + ws * 64 >= MT_STORES) break;
         const int idx = tid + it * NT;
-        const int r = idx / (C / VEC), i0 = (idx % (C / VEC)) * VEC;
-        const bool upper = (i0 >> 4) > (r >> 4);
-        const float* src = blkM(r >> 4, upper ? r >> 4 : i0 >> 4) + (r & 15) * LB + (i0 & 15);
+        const int k = idx / (16 * BCH), q = idx % (16 * BCH);
+        const int rr = q / BCH, cc = (q % BCH) * VEC;   // row and first column inside block k
+        const int br = k < 1 ? 0 : k < 3 ? 1 : k < 6 ? 2 : 3, bc = k - br * (br + 1) / 2;
+        const float* src = blkM(br, bc) + rr * LB + cc;
         uint4 mr, tr;
         E* me = (E*)&mr;
         E* te = (E*)&tr;
@@ -348,21 +348,21 @@ __global__ __launch_bounds__(PREP_THREADS) __attribute__((amdgpu_waves_per_eu(pr
 #pragma unroll
         for (int j = 0; j < VEC; j += 4) {
           *(f4*)&mv[j] = *(const f4*)(src + j);
-          *(f4*)&bv[j] = *(const f4*)&sm.beta[i0 + j];
+          *(f4*)&bv[j] = *(const f4*)&sm.beta[16 * bc + cc + j];
         }
 #pragma unroll
         for (int j = 0; j < VEC; ++j) {
-          const float m = upper ? 0.f : mv[j];
-          me[j] = fromf<E>(m);
-          te[j] = fromf<E>(m * bv[j]);
+          me[j] = fromf<E>(mv[j]);
+          te[j] = fromf<E>(mv[j] * bv[j]);
         }
-        if (keep_m) *(uint4*)(wM + r * C + i0) = mr;
-        *(uint4*)(wT + r * C + i0) = tr;
+        const int at = k * 256 + rr * 16 + cc;
+        if (keep_m) *(uint4*)(wM + at) = mr;
+        *(uint4*)(wT + at) = tr;
       }
       // the next unit's loads went out before P's and these stores (in-order
-      // counter)
-      if (keep_m) wait_vm<P_STORES + 2 * MT_ITERS>();
-      else wait_vm<P_STORES + MT_ITERS>();
+      // counter): three or two P blocks per wave, then its rounds of M and T
+      const int rounds = (MT_STORES - ws * 64 + NT - 1) / NT;
+      wait_vm_n((ws < 2 ? 3 : 2) + (keep_m ? 2 : 1) * rounds);
     }
     cur = nx;
   }
@@ -536,8 +536,7 @@ __global__ __launch_bounds__(NCW * 64 + 256) void k_scan_fwd(Params p) {
     size_t gi, arow;
     int len;
     chunk_at(c, gi, arow, len);
-    const char* Pg = (const char*)((const E*)p.wP + gi * C * C);
-    dma_rows<R::RC, C, 4, true>(sm.Pt[c % R::NP], Pg, R::RC, C, Pg, 0, prod, lane);
+    dma_lbt<E, 4>(sm.Pt[c % R::NP], (const char*)((const E*)p.wP + gi * LBT_ELEMS), prod, lane);
   };
   // producers: T and this tile's columns of V of chunk c (rows of V past the
   // chunk re-read its last row: they only meet zero columns of T)
@@ -545,9 +544,8 @@ __global__ __launch_bounds__(NCW * 64 + 256) void k_scan_fwd(Params p) {
     size_t gi, arow;
     int len;
     chunk_at(c, gi, arow, len);
-    const char* Tg = (const char*)((const E*)p.wT + gi * C * C);
     const char* Vg = (const char*)((const E*)p.v + arow * DV + v0);
-    dma_rows<R::RC, C, 4, true>(sm.ringB + R::BT, Tg, R::RC, C, Tg, 0, prod, lane);
+    dma_lbt<E, 4>(sm.ringB + R::BT, (const char*)((const E*)p.wT + gi * LBT_ELEMS), prod, lane);
     if (!map_tile)
       dma_rows<R::RO, C, 4, true>(sm.ringB + R::BV_, Vg, (size_t)H * DV * ES, len,
                                   Vg + (size_t)(len - 1) * H * DV * ES, 0, prod, lane);
@@ -595,6 +593,14 @@ __global__ __launch_bounds__(NCW * 64 + 256) void k_scan_fwd(Params p) {
     }
   };
 
+  // T and P arrive packed: the chunks above their diagonal blocks are zeroed
+  // once here and never loaded (the first barrier of the loop orders these
+  // stores before any read)
+  zero_upper_chunks<E>(sm.ringB + R::BT, tid, NCT + 256);
+  if constexpr (!MAPS) {
+#pragma unroll
+    for (int i = 0; i < R::NP; ++i) zero_upper_chunks<E>(sm.Pt[i], tid, NCT + 256);
+  }
   if (nch > cbeg) {
     if (producer) {
       for (int c = cbeg; c < cbeg + NA - 1 && c < nch; ++c) {

@@ -46,11 +46,13 @@ def test_saved_state_slots():
 
 def test_saved_context_bytes():
     # per (slot, head): Dv x Dk state, C x Dv new values D, fp32 gate block
-    # (b, beta, lambda: 3 x C), P and M (C x C), all but the gates in the activation dtype
+    # (b, beta, lambda: 3 x C), P and M (the ten 16 x 16 blocks on and below
+    # the diagonal of C x C), all but the gates in the activation dtype; plus
+    # one 1 KB zero block
     def per_unit(Dk, Dv, e):
-        return Dk * Dv * e + 64 * Dv * e + 3 * 64 * 4 + 2 * 64 * 64 * e
-    assert qdelta.saved_bytes(4, 4096, 16, 128, 128, 1) == 256 * 16 * per_unit(128, 128, 2)
-    assert qdelta.saved_bytes(1, 100, 2, 64, 64, 0) == 2 * 2 * per_unit(64, 64, 4)
+        return Dk * Dv * e + 64 * Dv * e + 3 * 64 * 4 + 2 * 10 * 256 * e
+    assert qdelta.saved_bytes(4, 4096, 16, 128, 128, 1) == 256 * 16 * per_unit(128, 128, 2) + 1024
+    assert qdelta.saved_bytes(1, 100, 2, 64, 64, 0) == 2 * 2 * per_unit(64, 64, 4) + 1024
     assert qdelta.saved_bytes(4, 4096, 16, 96, 128, 1) == 0
 
 
@@ -117,11 +119,12 @@ def test_noalloc_forward_validates_before_any_device_call():
     assert call(q=None) == E.QDELTA_EINVAL
     assert call(o=f + 4) == E.QDELTA_EINVAL
     assert call(B=0) == E.QDELTA_OK
-    # bf16 forward workspace: 17152 B per chunk-head unit against 64 MiB
+    # bf16 forward workspace: 11008 B per chunk-head unit (packed T and P, the
+    # gate block) and a 1 KB zero block, against 64 MiB
     cap = qdelta.NOALLOC_SCRATCH_BYTES
-    assert qdelta.workspace_bytes(8, 2048, 8, 128, 128, 1) <= cap
-    assert qdelta.workspace_bytes(4, 4096, 16, 128, 128, 1) > cap
-    assert call(B=4, T=4096, H=16, Dk=128, Dv=128) == E.QDELTA_ENOWORKSPACE
+    assert qdelta.workspace_bytes(4, 4096, 16, 128, 128, 1) <= cap
+    assert qdelta.workspace_bytes(8, 4096, 16, 128, 128, 1) > cap
+    assert call(B=8, T=4096, H=16, Dk=128, Dv=128) == E.QDELTA_ENOWORKSPACE
     assert call(B=1, T=65536, H=16, Dk=128, Dv=128) == E.QDELTA_ENOWORKSPACE
 
 

@@ -31,7 +31,7 @@ def test_noalloc_forward_equals_workspace_forward():
 
 
 def test_noalloc_forward_rejects_oversized_call():
-    d = synth.make(4, 4096, 16, 128, 128, "bf16", "G2", seed=150, s0=False)
+    d = synth.make(8, 4096, 16, 128, 128, "bf16", "G2", seed=150, s0=False)
     with pytest.raises(qdelta.QDeltaError) as ei:
         qdelta.chunk_fwd_noalloc(dev(d["q"]), dev(d["k"]), dev(d["v"]), dev(d["beta"]), dev(d["lam"]),
                                  dev(d["log_alpha"]), None)
