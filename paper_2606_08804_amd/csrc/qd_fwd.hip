@@ -105,11 +105,24 @@ __global__ __launch_bounds__(PREP_THREADS) __attribute__((amdgpu_waves_per_eu(pr
     int g, h, t0, len;
     bool valid;
   };
+  // Work item u -> (slot, head).  Workgroups sit on XCD blockIdx.x mod 8
+  // and step by a multiple of 8, so item u runs on XCD u mod 8; every head
+  // of a slot is given to the same XCD, because the raw gate vectors of the
+  // H heads of a token share cache lines (H x 4 bytes per token), which each
+  // XCD's L2 would otherwise fetch again.  Slots past the last multiple of 8
+  // keep the plain order.
+  const int total8 = (p.n_slots / 8) * 8 * H;
   auto find = [&](int u, Unit& x) {
     x.valid = false;
     if (u >= total) return;
-    x.g = u / H;
-    x.h = u % H;
+    if (u < total8) {
+      const int k = u >> 3;
+      x.g = 8 * (k / H) + (u & 7);
+      x.h = k % H;
+    } else {
+      x.g = u / H;
+      x.h = u % H;
+    }
     int n;
     x.valid = locate(p, x.g, n, x.t0, x.len);
   };
