@@ -457,8 +457,27 @@ __global__ __launch_bounds__(INTRA_THREADS) __attribute__((amdgpu_waves_per_eu(2
     while (clock64() - t0c < p.lead_cycles) __builtin_amdgcn_s_sleep(32);
     return;
   }
+  // Workgroup -> (slot, head), slot-grouped: the H heads of eight slots
+  // take H * 8 consecutive workgroups, slot g on XCD g mod 8 (workgroups go
+  // to XCD blockIdx.x mod 8, and the sleepers number a multiple of 8).  A
+  // token's gate gradients (dbeta, dlambda, dlog alpha: H x 4 bytes each)
+  // share cache lines across the heads, so the heads of a slot write them
+  // into one L2 at about the same time and the lines leave it whole; and
+  // the heads of one token read adjacent rows of q, k, v and dO.  Slots past
+  // the last multiple of 8 follow in plain order.
   const int bid = (int)blockIdx.x - p.lead;
-  const int g = bid % p.n_slots, h = bid / p.n_slots, tid = threadIdx.x, lane = tid & 63, w = wave_id(tid);
+  const int H8 = p.H * 8, ns8 = (p.n_slots / 8) * 8, tot8 = ns8 * p.H;
+  int g, h;
+  if (bid < tot8) {
+    const int r = bid % H8;
+    g = 8 * (bid / H8) + (r & 7);
+    h = r >> 3;
+  } else {
+    const int idx = bid - tot8, nt = p.n_slots - ns8;
+    g = ns8 + idx % nt;
+    h = idx / nt;
+  }
+  const int tid = threadIdx.x, lane = tid & 63, w = wave_id(tid);
   int n, t0, len;
   if (!locate(p, g, n, t0, len)) return;
   const int H = p.H;
@@ -979,7 +998,7 @@ static hipError_t launch_bwd_t(const Params& p, hipStream_t st) {
     // HBM idle half the time.  Half of the CUs start about half a unit later.
     Params q = p;
     const int total = p.n_slots * p.H, cus = device_cu_count();
-    q.lead = total >= 8 * cus ? cus : 0;    // two workgroups per CU: half of the slots
+    q.lead = total >= 8 * cus ? cus / 8 * 8 : 0;   // two workgroups per CU: half of the slots (a multiple of 8)
     q.lead_cycles = 20000;
     prof_mark(ST_INTRA, 0, st);
     hipLaunchKernelGGL((k_bwd_intra<E, DK, DV>), dim3(total + q.lead), dim3(INTRA_THREADS), 0, st, q);
