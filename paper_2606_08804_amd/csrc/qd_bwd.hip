@@ -433,8 +433,13 @@ struct alignas(16) IntraSmem {
 
 constexpr int INTRA_THREADS = NTHREADS;
 
+// Two workgroups per CU with bf16 operands; fp32 tiles take more than half
+// of the LDS, so one, with the whole register file.
+template <typename E>
+constexpr int intra_per_cu() { return sizeof(E) == 2 ? 2 : 1; }
+
 template <typename E, int DK, int DV>
-__global__ __launch_bounds__(INTRA_THREADS) __attribute__((amdgpu_waves_per_eu(2, 2))) void k_bwd_intra(Params p) {
+__global__ __launch_bounds__(INTRA_THREADS) __attribute__((amdgpu_waves_per_eu(intra_per_cu<E>(), intra_per_cu<E>()))) void k_bwd_intra(Params p) {
   constexpr int KS = Mma<E>::KS;
   constexpr int NKB = DK / 16;        // 16-column blocks of Dk
   constexpr int NKK = DK / KS;        // k steps over Dk
