@@ -71,6 +71,19 @@ def test_wide_value_tiles(Dk, Dv, B, H, T):
     _check(bwd_errors(d, g), TOL["bf16"], f"bwd wide tiles Dk={Dk} Dv={Dv}")
 
 
+@pytest.mark.parametrize("dt,B,H,T", [("bf16", 3, 5, 950), ("f32", 1, 3, 700), ("bf16", 1, 7, 64 * 8 * 3)])
+def test_odd_head_counts_and_slot_tails(dt, B, H, T):
+    """Head counts that are not powers of two and slot counts that are not
+    multiples of 8 (the preparation and intra kernels hand the heads of each
+    group of eight slots to one XCD and walk the remaining slots in plain
+    order; 24 slots with 7 heads leave no tail), forward and backward."""
+    d = synth.make(B, T, H, 64, 64, dt, "G2", seed=140 + H, s0=True, with_do=True)
+    o, Sf, saved = gpu_fwd(d, save_states=True)
+    _check(fwd_errors(d, o, Sf), TOL[dt], f"fwd {dt} H={H} T={T}")
+    g = gpu_bwd(d, saved)
+    _check(bwd_errors(d, g), TOL[dt], f"bwd {dt} H={H} T={T}")
+
+
 @pytest.mark.parametrize("gate", GATES)
 @pytest.mark.parametrize("Dv", [64, 128, 256])
 def test_bwd_fp32(gate, Dv):
